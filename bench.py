@@ -1,0 +1,379 @@
+"""Benchmark of the barrier-free collectives on one MI355X.
+
+Headline (one JSON line on stdout):
+  * p50 microseconds per AllReduce at 16 KiB per rank: 8 virtual ranks,
+    bfloat16, batch 1 x hidden 8192, normal(0,1) inputs, one-shot with
+    8-byte packets, `--steps` back-to-back calls with the epoch incremented
+    (a "step" is one such call).  Per-call latency is the interval between
+    consecutive calls' completion times, taken inside the kernels from the
+    100 MHz constant clock; it includes launch and dispatch, exactly as the
+    floor below does.
+  * the single-GPU floor measured the same way: back-to-back launches of a
+    kernel with the same grid whose only work is one dependent HBM round
+    trip (ratio = p50 / floor p50).
+  * HBM GB/s at 64 MiB per rank (8 ranks, binary32, two-shot with 128-byte
+    line packets): algorithmic bytes per call / average kernel time, the time
+    taken with HIP events on the stream the kernels run on.
+  * the CPU oracle timed on the host on a bounded sample of the 16 KiB
+    workload (cpu_baseline).
+
+Options: --gpus must be 1 (the virtual ranks share one GPU).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+TICK_US = 0.01  # 100 MHz constant clock
+
+
+def log(msg: str) -> None:
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2607_16100_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode())
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def pct(a, q):
+    return float(np.percentile(np.asarray(a, dtype=np.float64), q))
+
+
+# ----------------------------------------------------------------------------
+def stamped_loop(torch, ll, launch, steps: int, warmup: int, grid_hint: int):
+    """Run `launch(i)` warmup+steps times back to back; the timed calls write
+    per-workgroup start/end stamps.  Returns (intervals_us, spans_us, wall_s)."""
+    for i in range(warmup):
+        launch(i)
+    torch.cuda.synchronize()
+    grid, _ = ll.ll_last_grid()
+    grid = max(grid, grid_hint)
+    stamps = torch.zeros(steps * 2 * grid, dtype=torch.int64, device="cuda")
+    base = stamps.data_ptr()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        ll.ll_debug_stamp_next(base + i * 2 * grid * 8)
+        launch(warmup + i)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    s = stamps.view(steps, 2, grid).cpu().numpy().astype(np.int64)
+    g_used, _ = ll.ll_last_grid()
+    starts = s[:, 0, :g_used].min(axis=1)
+    ends = s[:, 1, :g_used].max(axis=1)
+    intervals = np.diff(ends) * TICK_US
+    spans = (ends - starts) * TICK_US
+    return intervals, spans, wall
+
+
+def bench_headline(torch, ll, steps, warmup):
+    from paper_2607_16100_amd import workloads as wl
+    from paper_2607_16100_amd.region import SymRegion
+
+    p, n = 8, 8192
+    x = wl.normal(p, n, "bf16", sigma=1.0, seed=0)
+    reg = SymRegion(p, n, "bf16")
+    reg.init()
+    reg.write_inputs(x)
+    s = reg.stream_handle()
+
+    def launch(i):
+        st = reg.allreduce(n, "oneshot")
+        if st != ll.LL_OK:
+            raise RuntimeError(ll.ll_strerror(st))
+
+    intervals, spans, wall = stamped_loop(torch, ll, launch, steps, warmup, 1)
+    ll.check(ll.ll_check(s), "headline")
+    grid, threads = ll.ll_last_grid()
+    # event-timed mean without stamps, same loop
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    for i in range(steps):
+        launch(i)
+    ev1.record()
+    torch.cuda.synchronize()
+    ev_mean_us = ev0.elapsed_time(ev1) * 1000.0 / steps
+    ll.check(ll.ll_check(s), "headline")
+    # parity of the last call
+    import oracle  # the benchmark's check: same oracle as the tests
+
+    got = reg.read_out(p * n, np.uint16).reshape(p, n)
+    exact = bool(np.array_equal(got, oracle.allreduce(x)))
+    return {
+        "p50_us": pct(intervals, 50), "p99_us": pct(intervals, 99), "mean_us": float(np.mean(intervals)),
+        "span_p50_us": pct(spans, 50), "event_mean_us": ev_mean_us, "wall_s": wall, "grid": grid,
+        "threads": threads, "bit_exact": exact, "epochs": reg.epoch,
+    }
+
+
+def bench_floor(torch, ll, steps, warmup, grid, threads):
+    """Back-to-back floor kernels (same grid), each loading a line nobody has
+    touched for a long time (a 1 GiB table > the 256 MiB last-level cache)."""
+    words = (1 << 30) // 8
+    chase = torch.zeros(words, dtype=torch.int64, device="cuda")
+    sink = torch.zeros(16, dtype=torch.int64, device="cuda")
+    s = torch.cuda.current_stream().cuda_stream
+    line_words = 16  # 128 bytes
+    stride_lines = 4099
+
+    def launch_floor(i):
+        start = ((i * stride_lines) % (words // line_words)) * line_words
+        st = ll.ll_probe_floor(chase.data_ptr(), words, start, sink.data_ptr(), grid, threads, 0, s)
+        if st != ll.LL_OK:
+            raise RuntimeError(ll.ll_strerror(st))
+
+    def launch_empty(i):
+        st = ll.ll_probe_empty(grid, threads, 0, s)
+        if st != ll.LL_OK:
+            raise RuntimeError(ll.ll_strerror(st))
+
+    out = {}
+    for name, fn, probe in (("floor", launch_floor, "floor"), ("empty", launch_empty, "empty")):
+        for i in range(warmup):
+            fn(i)
+        torch.cuda.synchronize()
+        stamps = torch.zeros(steps * 2 * grid, dtype=torch.int64, device="cuda")
+        base = stamps.data_ptr()
+        for i in range(steps):
+            if probe == "floor":
+                start = (((warmup + i) * stride_lines) % (words // line_words)) * line_words
+                st = ll.ll_probe_floor(chase.data_ptr(), words, start, sink.data_ptr(), grid, threads,
+                                       base + i * 2 * grid * 8, s)
+            else:
+                st = ll.ll_probe_empty(grid, threads, base + i * 2 * grid * 8, s)
+            if st != ll.LL_OK:
+                raise RuntimeError(ll.ll_strerror(st))
+        torch.cuda.synchronize()
+        arr = stamps.view(steps, 2, grid).cpu().numpy()
+        ends = arr[:, 1, :].max(axis=1)
+        starts = arr[:, 0, :].min(axis=1)
+        iv = np.diff(ends) * TICK_US
+        out[name] = {"p50_us": pct(iv, 50), "p99_us": pct(iv, 99), "span_p50_us": pct((ends - starts) * TICK_US, 50)}
+    # dependent-load latency of the same table (pointer chase of cold lines)
+    perm = np.random.default_rng(1).permutation(words // line_words // 64)[:4096] * 64 * line_words
+    nxt = np.roll(perm, -1)
+    idx = torch.from_numpy(perm.astype(np.int64)).cuda()
+    chase.index_copy_(0, idx, torch.from_numpy(nxt.astype(np.int64)).cuda())
+    res = torch.zeros(3, dtype=torch.int64, device="cuda")
+    ll.check(ll.ll_probe_chase(chase.data_ptr(), words, int(perm[0]), 2000, res.data_ptr(), s), "chase")
+    torch.cuda.synchronize()
+    r = res.cpu().numpy()
+    out["hbm_dependent_load_us"] = float(r[0]) * TICK_US / 2000
+    out["hbm_dependent_load_cycles"] = float(r[1]) / 2000
+    del chase
+    return out
+
+
+def bench_sol_pieces(torch, ll):
+    """The paper's speed-of-light pieces (Sec. VI) measured on one chip."""
+    s = torch.cuda.current_stream().cuda_stream
+    buf = torch.zeros(1024, dtype=torch.int32, device="cuda")
+    out = torch.zeros(7, dtype=torch.int64, device="cuda")
+    iters = 2000
+    ll.check(ll.ll_probe_fence_l2(buf.data_ptr(), iters, out.data_ptr(), s), "fence")
+    torch.cuda.synchronize()
+    o = out.cpu().numpy()
+    fence_us = o[0] * TICK_US / iters
+    sc1_us = o[2] * TICK_US / iters
+    flags = torch.zeros(2048, dtype=torch.int32, device="cuda")
+    pp = torch.zeros(3, dtype=torch.int64, device="cuda")
+    rounds = 2000
+    ll.check(ll.ll_probe_pingpong(flags.data_ptr(), rounds, 8, 1, 10_000_000, pp.data_ptr(), s), "pingpong")
+    torch.cuda.synchronize()
+    q = pp.cpu().numpy()
+    done = int(q[1])
+    ping_us = (q[0] * TICK_US / done) if done else float("nan")
+    remote = (ping_us - 2 * fence_us) / 2
+    ids = torch.zeros(64, dtype=torch.int32, device="cuda")
+    ll.check(ll.ll_probe_xcd(ids.data_ptr(), 64, 64, s), "xcd")
+    torch.cuda.synchronize()
+    xcd = ids.cpu().numpy().tolist()
+    return {
+        "fence_us": fence_us, "coherent_load_us": sc1_us, "pingpong_us": ping_us, "pingpong_rounds": done,
+        "remote_store_us": remote, "sol_us": 2 * fence_us + remote,
+        "xcd_of_workgroup_0_15": xcd[:16],
+    }
+
+
+def bench_bandwidth(torch, ll, count, algos, iters=20, warmup=3):
+    """Average kernel time (HIP events on the launch stream) and GB/s at `count`
+    binary32 elements per rank, 8 ranks."""
+    from paper_2607_16100_amd import bytemodel
+    from paper_2607_16100_amd import workloads as wl
+    from paper_2607_16100_amd.region import SymRegion
+
+    p = 8
+    reg = SymRegion(p, count, "f32", out_elems=p * count)
+    reg.init()
+    # inputs generated on the device from a seeded torch generator (the values
+    # do not affect timing; parity at this size is covered by the tests)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(0)
+    rows = (torch.rand((p, count), generator=g, device="cuda", dtype=torch.float32) * 2 - 1)
+    reg.write_inputs_device(rows.view(torch.uint8).view(p, count * 4))
+    del rows
+    stream = torch.cuda.current_stream()
+    res = {}
+    for algo in algos:
+        for _ in range(warmup):
+            ll.check(reg.allreduce(count, algo), algo)
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for _ in range(iters):
+            ll.check(reg.allreduce(count, algo), algo)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        ll.check(ll.ll_check(stream.cuda_stream), algo)
+        us = ev0.elapsed_time(ev1) * 1000.0 / iters
+        nbytes = bytemodel.allreduce_bytes(algo, p, count, 4)
+        useful = bytemodel.useful_bytes(p, count, 4)
+        grid, threads = ll.ll_last_grid()
+        res[algo] = {"kernel_us": us, "algorithmic_bytes": nbytes, "gbps": nbytes / us / 1e3,
+                     "useful_gbps": useful / us / 1e3, "grid": grid, "threads": threads}
+    del reg
+    return res
+
+
+def bench_cpu_baseline(seconds: float):
+    import oracle
+    from paper_2607_16100_amd import workloads as wl
+
+    x = wl.normal(8, 8192, "bf16", sigma=1.0, seed=0)
+    times = []
+    t_end = time.perf_counter() + seconds
+    while time.perf_counter() < t_end:
+        t0 = time.perf_counter()
+        oracle.allreduce(x)
+        times.append(time.perf_counter() - t0)
+    return {"value": float(np.median(times)) * 1e6, "unit": "us", "cores": 1, "kind": "oracle",
+            "sample": f"8 ranks x 8192 bf16 (the 16 KiB workload) reduced {len(times)} times in ~{seconds:.0f} s "
+                      f"by the single-threaded C oracle; median per call"}
+
+
+def traffic_from_profiles(kernel_hash: str):
+    """HBM bytes per launch from the committed counter summary, if it was taken
+    from the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", "twoshot_line_f32_64MiB_p8_counters.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        with open(path) as f:
+            d = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if d.get("kernel_source_hash") != kernel_hash:
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10000)
+    ap.add_argument("--warmup", type=int, default=200)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--bw-iters", type=int, default=20)
+    ap.add_argument("--only", default="", help="comma list of sections: headline,floor,sol,bw,cpu")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs its P virtual ranks on one GPU; --gpus {args.gpus} is not supported "
+              f"(the multi-GPU design is described but not built)", file=sys.stderr)
+        sys.exit(2)
+    only = set(x for x in args.only.split(",") if x)
+
+    def want(sec):
+        return not only or sec in only
+
+    import torch
+
+    from paper_2607_16100_amd import llcoll as ll
+
+    torch.cuda.set_device(0)
+    props = torch.cuda.get_device_properties(0)
+    log(f"device: {props.name} {getattr(props, 'gcnArchName', '')} CUs={props.multi_processor_count}")
+    ll.ll_set_poll_timeout(200_000_000)
+    result = {}
+    if want("headline"):
+        log("headline: 16 KiB bf16 one-shot, 8 ranks")
+        result["headline"] = bench_headline(torch, ll, args.steps, args.warmup)
+        log(json.dumps(result["headline"]))
+    grid = result.get("headline", {}).get("grid", 64)
+    threads = result.get("headline", {}).get("threads", 256)
+    if want("floor"):
+        log("floor")
+        result["floor"] = bench_floor(torch, ll, args.steps, args.warmup, grid, threads)
+        log(json.dumps(result["floor"]))
+    if want("sol"):
+        log("speed-of-light pieces")
+        result["sol"] = bench_sol_pieces(torch, ll)
+        log(json.dumps(result["sol"]))
+    if want("bw"):
+        log("bandwidth at 64 MiB per rank")
+        result["bw"] = bench_bandwidth(torch, ll, 16 << 20, ["twoshot_line", "twoshot", "oneshot_line", "oneshot"],
+                                       iters=args.bw_iters)
+        log(json.dumps(result["bw"]))
+    if want("cpu"):
+        log("cpu baseline")
+        result["cpu"] = bench_cpu_baseline(args.cpu_seconds)
+        log(json.dumps(result["cpu"]))
+
+    h = result.get("headline", {})
+    fl = result.get("floor", {}).get("floor", {})
+    bw = result.get("bw", {}).get("twoshot_line")
+    khash = kernel_source_hash()
+    roofline = None
+    if bw:
+        roofline = {"bound": "hbm", "achieved": round(bw["gbps"], 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": round(bw["gbps"] / PEAK_HBM_GBS, 4), "traffic": traffic_from_profiles(khash),
+                    "kernel": "k_twoshot<ProtoLine, f32, 8> (64 MiB per rank)",
+                    "kernel_us": round(bw["kernel_us"], 2), "algorithmic_bytes": bw["algorithmic_bytes"]}
+    line = {
+        "metric": "p50 µs per AllReduce at 16 KB (P=8, bf16) + HBM GB/s at 64 MB",
+        "value": round(h["p50_us"], 3) if h else None,
+        "unit": "µs",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(h["wall_s"] * 1000.0 / args.steps, 5) if h else None,
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "AllReduce sum, 8 virtual ranks on one GPU, bf16 batch 1 x hidden 8192 "
+                               "(16 KiB per rank), one-shot 8-byte packets, back-to-back calls",
+                   "ranks": 8, "elements_per_rank": 8192, "element_type": "bf16", "accumulate": "f32",
+                   "parallelism": "8 virtual ranks / 1 GPU"},
+        "p99_us": round(h["p99_us"], 3) if h else None,
+        "floor_p50_us": round(fl["p50_us"], 3) if fl else None,
+        "ratio_to_floor": round(h["p50_us"] / fl["p50_us"], 3) if (h and fl) else None,
+        "hbm_gbps_64MB": round(bw["gbps"], 1) if bw else None,
+        "roofline": roofline,
+        "cpu_baseline": result.get("cpu"),
+        "detail": result,
+        "kernel_source_hash": khash,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

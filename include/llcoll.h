@@ -1,0 +1,177 @@
+/*
+ * llcoll -- barrier-free low-latency collectives for one MI355X (gfx950).
+ *
+ * C ABI.  Every entry point takes plain pointers and sizes; device pointers
+ * are HIP device addresses, `stream` is a hipStream_t passed as void* (NULL =
+ * the null stream).  No call allocates, frees or synchronises, except
+ * ll_check (which synchronises the stream it is given).  Every call checks its
+ * arguments before it touches the HIP runtime, so argument errors are
+ * reported the same way with or without a GPU.
+ *
+ * The method (the paper's Secs. III-V): an AllReduce in which every rank
+ * pushes its data into peers' scratch ("push mode", Sec. III-A), and
+ * receivers detect arrival from a flag packed into the same store as the data
+ * (the LL protocol, Sec. IV), so no memory barrier is needed between ranks.
+ * One-shot: every rank sends its whole input to every peer and reduces all P
+ * contributions itself.  Two-shot: ReduceScatter (each rank reduces one
+ * chunk) followed by AllGather of the reduced chunks (Sec. III-A).
+ *
+ * Virtual ranks.  The P ranks live on one GPU: rank r owns the slice
+ * [sym_base + r*rank_stride, sym_base + (r+1)*rank_stride) of a single
+ * symmetric allocation, and is served by its own workgroups.  Rank r's data
+ * reaches another rank only through flagged packets written into that rank's
+ * slice; no rank reads another rank's input.
+ *
+ * Slice layout (a pure function of rank_stride and nranks, identical for
+ * every call on a region, so a byte's role never changes between calls):
+ *   [0, cap)                      input area: the rank's input, at offset 0
+ *   [cap, cap + A8)               8-byte packet area {payload u32, flag u32}
+ *   [cap + A8, cap + A8 + A128)   128-byte line area
+ * cap (the input capacity, a multiple of 256 bytes) is the largest input for
+ * which both packet areas fit every algorithm; ll_input_capacity reports it.
+ *
+ * Element types: binary32 and bfloat16.  The reduction is the sum of the P
+ * inputs in ascending rank order, accumulated in binary32, rounded once to the
+ * element type (round to nearest even).  Results are therefore identical on
+ * every rank and for every algorithm and launch shape.
+ *
+ * Epochs.  The flag carried by every packet is the caller's `epoch`, which
+ * must be >= 1 and must strictly increase over all calls on one region (any
+ * entry point); 0 marks zeroed scratch (ll_init).  After epoch 0xFFFFFFFF,
+ * call ll_init again and restart at 1.  (The paper's buffer object keeps this
+ * counter internally and advances it itself, Sec. V; here the caller owns it.)
+ *
+ * Outputs.  `out` is a separate device buffer (it must not overlap the
+ * symmetric region) holding the P per-rank outputs back to back:
+ *   AllReduce      rank r's result at out + r*count*esize
+ *   ReduceScatter  rank r's chunk  at out + r*recvcount*esize
+ *   AllGather      rank r's result at out + r*nranks*sendcount*esize
+ *
+ * Ownership.  The caller allocates and frees the symmetric region and `out`,
+ * and keeps them alive until the stream has run the call.  The library keeps
+ * no per-region state.  Two calls on one region must not run concurrently
+ * (use one stream per region).
+ *
+ * Failure.  Every wait on a flag is bounded (ll_set_poll_timeout).  A wait
+ * that expires records LL_ERR_TIMEOUT in a device status word and lets the
+ * kernel finish; ll_check reports it.  The outputs of such a call are
+ * undefined.
+ */
+#ifndef LLCOLL_H
+#define LLCOLL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { LL_F32 = 0, LL_BF16 = 1 } ll_dtype;
+typedef enum { LL_SUM = 0 } ll_op;
+
+/* AllReduce algorithm.  *_LINE variants carry 120 payload bytes per 128-byte
+ * line instead of 4 per 8-byte packet. */
+typedef enum {
+  LL_ALGO_AUTO = 0,          /* chosen by message size */
+  LL_ALGO_ONESHOT = 1,       /* one-shot, 8-byte packets (Sec. III-A, Sec. IV "LL") */
+  LL_ALGO_TWOSHOT = 2,       /* two-shot (ReduceScatter + AllGather), 8-byte packets */
+  LL_ALGO_TWOSHOT_LINE = 3,  /* two-shot, 128-byte line packets */
+  LL_ALGO_ONESHOT_LINE = 4   /* one-shot, 128-byte line packets */
+} ll_algo;
+
+/* Packet format for the stand-alone ReduceScatter / AllGather. */
+typedef enum { LL_PROTO_AUTO = 0, LL_PROTO_PACKET8 = 1, LL_PROTO_LINE128 = 2 } ll_proto;
+
+/* Status codes. */
+#define LL_OK 0
+#define LL_ERR_INVALID -1     /* null pointer, nranks outside [2,8], misaligned pointer or
+                                 stride, epoch 0, out overlapping the region, bad enum value */
+#define LL_ERR_UNSUPPORTED -2 /* dtype or op not supported */
+#define LL_ERR_SCRATCH -3     /* input larger than the region's input capacity */
+#define LL_ERR_HIP -4         /* the HIP runtime reported an error (see ll_strerror) */
+#define LL_ERR_TIMEOUT -5     /* a flag wait expired (reported by ll_check) */
+
+#define LL_MAX_RANKS 8
+#define LL_ALIGN 256
+
+/* Minimum rank_stride (bytes, multiple of 256) whose input capacity holds
+ * `count` elements of `dt` for nranks ranks.  `count` is the per-rank input
+ * length of the largest call the region will serve: count for AllReduce,
+ * nranks*recvcount for ReduceScatter, sendcount for AllGather.  This is the
+ * host-side sizing helper of Sec. V ("Host-side Functions"). */
+int ll_slice_bytes(size_t count, ll_dtype dt, int nranks, size_t *min_rank_stride);
+
+/* Input capacity in bytes of a region with this rank_stride and rank count. */
+int ll_input_capacity(size_t rank_stride, int nranks, size_t *capacity_bytes);
+
+/* Zero both packet areas of every slice (flag 0 = nothing received), on
+ * `stream`.  Call once after allocating a region, and again before reusing it
+ * after epoch 0xFFFFFFFF or after a timed-out call.  Sec. V: the LL reset
+ * value is zero. */
+int ll_init(void *sym_base, size_t rank_stride, int nranks, void *stream);
+
+/* AllReduce (sum) of `count` elements per rank, algorithm chosen by size.
+ * Input of rank r: sym_base + r*rank_stride, count elements.  One kernel
+ * launch on `stream`; returns after enqueueing. */
+int ll_allreduce(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt,
+                 ll_op op, int nranks, uint32_t epoch, void *stream);
+
+/* Same, with the algorithm named. */
+int ll_allreduce_algo(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt,
+                      ll_op op, int nranks, uint32_t epoch, void *stream, ll_algo algo);
+
+/* ReduceScatter (sum): rank r's input is nranks*recvcount elements; rank r
+ * receives elements [r*recvcount, (r+1)*recvcount) of the sum (Sec. III-A). */
+int ll_reduce_scatter(void *sym_base, size_t rank_stride, void *out, size_t recvcount,
+                      ll_dtype dt, ll_op op, int nranks, uint32_t epoch, void *stream);
+int ll_reduce_scatter_proto(void *sym_base, size_t rank_stride, void *out, size_t recvcount,
+                            ll_dtype dt, ll_op op, int nranks, uint32_t epoch, void *stream,
+                            ll_proto proto);
+
+/* AllGather: rank r's input is sendcount elements; every rank receives the
+ * concatenation of all inputs in rank order (Sec. III-A). */
+int ll_allgather(void *sym_base, size_t rank_stride, void *out, size_t sendcount, ll_dtype dt,
+                 int nranks, uint32_t epoch, void *stream);
+int ll_allgather_proto(void *sym_base, size_t rank_stride, void *out, size_t sendcount,
+                       ll_dtype dt, int nranks, uint32_t epoch, void *stream, ll_proto proto);
+
+/* Synchronise `stream`, then report and clear the device status word:
+ * LL_OK, LL_ERR_TIMEOUT, or LL_ERR_HIP. */
+int ll_check(void *stream);
+
+/* Details of the last timeout seen by ll_check: rank, the bit mask of peers
+ * not heard from, and the epoch waited for.  Any pointer may be NULL. */
+int ll_last_timeout(int *rank, uint32_t *missing_peers, uint32_t *epoch);
+
+/* Human-readable text for a status code. */
+const char *ll_strerror(int status);
+
+/* ---- tuning and test hooks (process-wide settings; not thread-safe) ---- */
+
+/* Workgroups per rank and threads per workgroup for the following calls;
+ * 0 = automatic.  threads must be a multiple of 64 in [64, 1024].  Results do
+ * not depend on these settings. */
+int ll_set_launch(int workgroups_per_rank, int threads);
+
+/* Flag-wait budget in ticks of the 100 MHz constant clock (default 2e8,
+ * i.e. 2 s).  Must be >= 1. */
+int ll_set_poll_timeout(uint64_t ticks);
+
+/* Test hook: rank `rank` publishes nothing (-1 = off), so its peers' waits
+ * expire; used to test timeout reporting. */
+int ll_debug_mute_rank(int rank);
+
+/* Benchmark hook: when `stamps` (device memory) is non-NULL, the next launch
+ * writes each workgroup's start and end time (100 MHz ticks) to
+ * stamps[b] and stamps[grid + b].  The pointer is used for one launch only. */
+int ll_debug_stamp_next(uint64_t *stamps);
+
+/* Grid (total workgroups) of the last launch. */
+int ll_last_grid(int *grid, int *threads);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LLCOLL_H */

@@ -1,0 +1,77 @@
+/*
+ * llcoll measurement probes -- C ABI (same library as llcoll.h).
+ *
+ * These kernels measure what the collectives are judged against:
+ *
+ *  - The single-GPU latency floor: an empty kernel and a "floor" kernel (one
+ *    dependent HBM round trip) launched with the collective's grid.  A small
+ *    AllReduce on one GPU cannot finish faster than launching a kernel and
+ *    waiting for one memory round trip.
+ *  - The pieces of the paper's speed-of-light model (Sec. VI): the latency of
+ *    a fence (the paper's L2 round-trip proxy), of a coherent load, and of a
+ *    ping-pong between two workgroups on different XCDs (the single-chip
+ *    stand-in for the GPU-to-GPU ping-pong), from which
+ *    L_remote_store = (L_ping_pong - 2 L_L2_RTT) / 2 and
+ *    L_SoL = 2 L_L2_RTT + L_remote_store.
+ *  - Chip facts the packet formats rely on: the workgroup-to-XCD map and a
+ *    litmus test for torn packets across XCDs.
+ *
+ * All pointers are device pointers; `stream` is a hipStream_t (NULL = null
+ * stream).  Every wait inside a probe is bounded.  Return codes are those of
+ * llcoll.h.  Times are in ticks of the 100 MHz constant clock ("ticks") or
+ * shader-clock cycles ("cycles").
+ */
+#ifndef LLPROBE_H
+#define LLPROBE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Empty kernel.  If stamps != NULL, workgroup b writes its start time to
+ * stamps[b] and its end time to stamps[grid + b]. */
+int ll_probe_empty(int grid, int threads, uint64_t *stamps, void *stream);
+
+/* Floor kernel: lane 0 of workgroup 0 loads chase[start] and stores it to
+ * sink[0]; every other workgroup exits at once.  stamps as above. */
+int ll_probe_floor(const uint64_t *chase, uint64_t chase_len, uint64_t start, uint64_t *sink, int grid,
+                   int threads, uint64_t *stamps, void *stream);
+
+/* One lane follows idx = chase[idx] `steps` times from `start`.
+ * out3 = {ticks, cycles, final idx}. */
+int ll_probe_chase(const uint64_t *chase, uint64_t chase_len, uint64_t start, int steps, uint64_t *out3,
+                   void *stream);
+
+/* One lane, `iters` times each: store + agent-scope fence; dependent coherent
+ * (sc1) load of one line; dependent sc0 load of one line.  buf4k: 4 KiB of
+ * device memory whose dword 16 is zero.  out7 = {fence ticks, fence cycles,
+ * sc1 ticks, sc1 cycles, sc0 ticks, sc0 cycles, sink}. */
+int ll_probe_fence_l2(uint32_t *buf4k, int iters, uint64_t *out7, void *stream);
+
+/* Ping-pong between workgroup 0 and workgroup `peer` of a `grid`-workgroup
+ * launch, `rounds` exchanges; each wait gives up after limit_ticks.
+ * flags8k: 8 KiB of zeroed device memory.  out3 = {ticks, exchanges
+ * completed, cycles}. */
+int ll_probe_pingpong(uint32_t *flags8k, int rounds, int grid, int peer, uint64_t limit_ticks, uint64_t *out3,
+                      void *stream);
+
+/* ids[b] = XCD index of workgroup b. */
+int ll_probe_xcd(uint32_t *ids, int grid, int threads, void *stream);
+
+/* Torn-packet litmus across XCDs.  grid/2 writer workgroups each rewrite
+ * `lines` 128-byte lines `iters` times; grid/2 reader workgroups read another
+ * writer's lines `reads` times.  layout 0 = 8-byte packets, 1 = 128-byte lines
+ * with a flag per 64-byte half.  buf: zeroed, >= grid/2 * lines * 128 bytes.
+ * counts4 (zeroed) = {units seen, torn units, 16-byte loads with two different
+ * flags, lines with two different half flags}. */
+int ll_probe_litmus(uint32_t *buf, size_t buf_bytes, int grid, int lines, int iters, int reads, int layout,
+                    unsigned long long *counts4, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LLPROBE_H */

@@ -1,0 +1,65 @@
+"""Algorithmic HBM bytes per call of each collective (the roofline numerator).
+
+Counted per call over all P ranks: every byte the method itself must read or
+write in HBM -- the inputs read, every packet written into a peer's slot and
+read back by its owner, and the outputs written.  Packets carry 4 payload
+bytes per 8 (8-byte packets) or 120 per 128 (128-byte lines).  Per rank this
+is the paper's per-GPU communication volume of Table I (one-shot LL
+2(N-1)M, two-shot LL 4(N-1)M/N) plus the local input reads and output
+writes; the 8-byte-packet expansion factor 2 is the "halves the effective
+payload bandwidth" of the LL protocol (Sec. IV).
+"""
+from __future__ import annotations
+
+import math
+
+EXPANSION = {"packet8": 2.0, "line128": 128.0 / 120.0}
+
+
+def comm_volume_per_rank(algo: str, p: int, m: float, proto: str) -> float:
+    """Bytes one rank sends to its peers (Table I, "Comm. Volume per GPU")."""
+    e = EXPANSION[proto]
+    if algo == "oneshot":
+        return e * (p - 1) * m
+    if algo == "twoshot":
+        return 2 * e * (p - 1) * m / p
+    raise ValueError(algo)
+
+
+def _proto(algo: str) -> tuple[str, str]:
+    base = {"oneshot": "oneshot", "oneshot_line": "oneshot", "twoshot": "twoshot", "twoshot_line": "twoshot"}[algo]
+    proto = "line128" if algo.endswith("_line") else "packet8"
+    return base, proto
+
+
+def allreduce_bytes(algo: str, p: int, count: int, esize: int) -> float:
+    """HBM bytes moved by one AllReduce call of `count` elements per rank."""
+    m = count * esize
+    base, proto = _proto(algo)
+    e = EXPANSION[proto]
+    if base == "oneshot":
+        # read input M; write (P-1) packet copies; read them back; write output M
+        per_rank = m + 2 * e * (p - 1) * m + m
+    else:
+        # RS: read input M, write and read (P-1) chunk packets; AG: write and
+        # read (P-1) reduced-chunk packets; write output M
+        c = math.ceil(count / p) * esize
+        per_rank = m + 4 * e * (p - 1) * c + m
+    return p * per_rank
+
+
+def reduce_scatter_bytes(proto: str, p: int, recvcount: int, esize: int) -> float:
+    c = recvcount * esize
+    e = EXPANSION[proto]
+    return p * (p * c + 2 * e * (p - 1) * c + c)
+
+
+def allgather_bytes(proto: str, p: int, sendcount: int, esize: int) -> float:
+    s = sendcount * esize
+    e = EXPANSION[proto]
+    return p * (s + 2 * e * (p - 1) * s + p * s)
+
+
+def useful_bytes(p: int, count: int, esize: int) -> float:
+    """Read every input once and write every output once."""
+    return 2.0 * p * count * esize

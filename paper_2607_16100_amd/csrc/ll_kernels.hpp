@@ -1,0 +1,383 @@
+// Collective kernels: one-shot and two-shot AllReduce, ReduceScatter and
+// AllGather over P virtual ranks on one GPU.
+//
+// Grid = P * W workgroups.  Workgroup b serves rank r = b % P as its part
+// w = b / P.  Workgroups are dispatched round-robin over the chip's XCDs, so
+// with P = 8 every rank lives on its own XCD and every rank-to-rank hop
+// crosses the fabric, the single-chip stand-in for a GPU-to-GPU link.
+//
+// Every rank moves its data to another rank only by storing flagged packets
+// into a slot of that rank's slice ("push mode", Sec. III-A); it never reads
+// another rank's input.  A slot (d <- s) is the region of rank d's slice that
+// receives rank s's packets; slot number of s in d's list is s - (s > d).
+//
+// Work division: the lanes of all W workgroups of a rank cover the packet
+// units of a stream in a grid-stride loop; lane g of part w handles the same
+// unit indices on every rank, so a waiting lane only ever waits for the lanes
+// of the same part on other ranks, which are resident (the host keeps the
+// grid within what the chip holds at once).  Every wait is bounded.
+#pragma once
+
+#include "ll_device.hpp"
+
+namespace llc {
+
+struct KArgs {
+  char *sym;          // symmetric region base
+  uint64_t stride;    // bytes per rank slice
+  char *out;          // dense per-rank outputs
+  int64_t n;          // AllReduce: count; ReduceScatter: recvcount; AllGather: sendcount
+  int64_t chunk;      // two-shot chunk length in elements
+  uint64_t area;      // offset of the packet area used by this call, in every slice
+  uint64_t slot;      // bytes per slot
+  uint64_t timeout;   // flag-wait budget, 100 MHz ticks
+  uint64_t *stamps;   // optional per-workgroup start/end times
+  uint32_t epoch;     // flag value of this call
+  int32_t mute;       // rank that publishes nothing (test hook), or -1
+  uint32_t al4;       // every element stream of this call starts 4-byte aligned
+  uint32_t pad_;
+};
+
+__device__ __forceinline__ int slot_of(int src, int dst) { return src - (src > dst ? 1 : 0); }
+
+struct Part {
+  int r, w, W;
+};
+
+template <int P>
+__device__ __forceinline__ Part part_of_block() {
+  Part p;
+  p.r = (int)(blockIdx.x % P);
+  p.w = (int)(blockIdx.x / P);
+  p.W = (int)(gridDim.x / P);
+  return p;
+}
+
+__device__ __forceinline__ void stamp_start(const KArgs &a) {
+  if (a.stamps != nullptr && threadIdx.x == 0) a.stamps[blockIdx.x] = now_ticks();
+}
+
+__device__ __forceinline__ void stamp_end(const KArgs &a) {
+  if (a.stamps != nullptr) {
+    __syncthreads();
+    if (threadIdx.x == 0) a.stamps[gridDim.x + blockIdx.x] = now_ticks();
+  }
+}
+
+// Poll the P-1 slots (r <- q) at byte offset `off` of every slot until every
+// flag equals the epoch.  All pending loads of an iteration are issued before
+// any is checked (parallel polling across ranks, Sec. VII Obs. 1); a lane
+// re-loads only the peers it has not yet heard from.
+template <class Pr, int P>
+__device__ __forceinline__ void poll_all(char *area_r, uint64_t slot, uint32_t off, int r, uint32_t epoch,
+                                         uint64_t deadline, u32x4 *got) {
+  // One resource covers the P-1 slots; the slot is selected by the scalar offset.
+  const rsrc_t rs = make_rsrc(area_r, (uint32_t)((uint64_t)(P - 1) * slot));
+  uint32_t pend = ((1u << P) - 1u) & ~(1u << r);
+#pragma unroll
+  for (int q = 0; q < P; ++q) got[q] = u32x4{0u, 0u, 0u, 0u};
+  int spins = 0;
+  while (true) {
+    compiler_fence();
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      if (q == r) continue;
+      if (pend & (1u << q)) got[q] = ld_pkt(rs, off, uniform_u32((uint32_t)((uint64_t)slot_of(q, r) * slot)));
+    }
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      if (q == r) continue;
+      const bool rdy = Pr::ready(got[q], epoch);
+      if ((pend & (1u << q)) && rdy) pend &= ~(1u << q);
+    }
+    if (pend == 0) break;
+    if ((++spins & 15) == 0 && now_ticks() > deadline) {
+      report_timeout(r, pend, epoch);
+      break;
+    }
+  }
+}
+
+// Store one packet to slot (q <- r) of every peer q, starting with r+1 so
+// that the ranks do not all write to the same peer at once.  Every address
+// is computed from wave-uniform values.
+template <int P>
+__device__ __forceinline__ void bcast(const KArgs &a, uint64_t area, int r, uint32_t off, u32x4 pk) {
+#pragma unroll
+  for (int k = 1; k < P; ++k) {
+    const int q = (r + k) % P;
+    char *dst = a.sym + (uint64_t)q * a.stride + area + (uint64_t)slot_of(r, q) * a.slot;
+    st_pkt(make_rsrc(dst, (uint32_t)a.slot), off, pk);
+  }
+}
+
+// Reduce one lane's words: x_0 + x_1 + ... + x_{P-1} in ascending rank order,
+// binary32 accumulation starting from x_0, own contribution at position r,
+// one rounding to the element type (Sec. IV error analysis; recvReduce,
+// Sec. V).  `got[q]` are unpacked payload words for q != r.
+template <class Pr, int DT, int P>
+__device__ __forceinline__ u32x4 reduce_ordered(const u32x4 *got, u32x4 own, int r) {
+  constexpr int K = Elem<DT>::kPerWord;
+  constexpr int NW = Pr::kMaxWords;
+  float acc[NW * K];
+#pragma unroll
+  for (int q = 0; q < P; ++q) {
+    const u32x4 x = (q == r) ? own : got[q];
+    const uint32_t wv[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+    for (int j = 0; j < NW; ++j) {
+      float f[K];
+      Elem<DT>::widen(wv[j], f);
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        if (q == 0) {
+          acc[j * K + k] = f[k];
+        } else {
+          acc[j * K + k] = acc[j * K + k] + f[k];
+        }
+      }
+    }
+  }
+  uint32_t res[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int j = 0; j < NW; ++j) res[j] = Elem<DT>::narrow(&acc[j * K]);
+  u32x4 v = {res[0], res[1], res[2], res[3]};
+  return v;
+}
+
+// ---------------------------------------------------------------------------
+// One-shot AllReduce (Sec. III-A; the per-thread load -> bcast -> recvReduce
+// -> store sequence of Sec. V).  Slot (d <- s) holds all of s's input.
+template <class Pr, int DT, int P>
+__global__ __launch_bounds__(1024) void k_oneshot(KArgs a) {
+  stamp_start(a);
+  const Part pt = part_of_block<P>();
+  const int r = pt.r;
+  constexpr int E = Elem<DT>::kBytes;
+  const uint64_t deadline = now_ticks() + a.timeout;
+  char *const slice_r = a.sym + (uint64_t)r * a.stride;
+  const int64_t n = a.n;
+  const int64_t units = Pr::units((n * E + 3) / 4);
+  char *const out_r = a.out + (uint64_t)r * (uint64_t)n * E;
+
+  char *const area_r = slice_r + a.area;
+  const bool publish = (r != a.mute);
+  const int64_t g = (int64_t)pt.w * blockDim.x + threadIdx.x;
+  const int sub = (int)(g % Pr::kLanes);
+  const int64_t ustep = (int64_t)pt.W * blockDim.x / Pr::kLanes;
+
+  for (int64_t u = g / Pr::kLanes; u < units; u += ustep) {
+    const int64_t w0 = Pr::word0(u, sub);
+    const int cnt = Pr::count(sub);
+    const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+    const u32x4 own = load_words<DT>(slice_r, w0, cnt, n, true);
+    if (publish) bcast<P>(a, a.area, r, off, Pr::pack(own, a.epoch, sub));
+    u32x4 got[P];
+    poll_all<Pr, P>(area_r, a.slot, off, r, a.epoch, deadline, got);
+#pragma unroll
+    for (int q = 0; q < P; ++q) got[q] = Pr::unpack(got[q], sub);
+    const u32x4 res = reduce_ordered<Pr, DT, P>(got, own, r);
+    store_words<DT>(out_r, w0, cnt, n, a.al4 != 0, res);
+  }
+  stamp_end(a);
+}
+
+// ---------------------------------------------------------------------------
+// Two-shot AllReduce (Sec. III-A): ReduceScatter then AllGather, fused in one
+// kernel.  The input is cut into P chunks of `chunk` elements (the last ones
+// may be short or empty); rank c owns chunk c.
+//   phase 1  send chunk c to slot (c <- r) of its owner, for every c != r
+//   phase 2  reduce own chunk r from the P-1 received copies and the own
+//            input, store it, and send the result to slot (q <- r) of every
+//            peer's AllGather area
+//   phase 3  receive every other reduced chunk and store it
+// RS slots occupy the first P-1 slots of the area, AG slots the next P-1.
+template <class Pr, int DT, int P>
+__global__ __launch_bounds__(1024) void k_twoshot(KArgs a) {
+  stamp_start(a);
+  const Part pt = part_of_block<P>();
+  const int r = pt.r;
+  constexpr int E = Elem<DT>::kBytes;
+  const uint64_t deadline = now_ticks() + a.timeout;
+  char *const slice_r = a.sym + (uint64_t)r * a.stride;
+  const int64_t n = a.n;
+  const int64_t C = a.chunk;
+  const int64_t units = Pr::units((C * E + 3) / 4);
+  char *const out_r = a.out + (uint64_t)r * (uint64_t)n * E;
+  const uint64_t ag_area = a.area + (uint64_t)(P - 1) * a.slot;
+  const bool publish = (r != a.mute);
+  const bool al4 = a.al4 != 0;
+
+  const int64_t g = (int64_t)pt.w * blockDim.x + threadIdx.x;
+  const int sub = (int)(g % Pr::kLanes);
+  const int64_t u0 = g / Pr::kLanes;
+  const int64_t ustep = (int64_t)pt.W * blockDim.x / Pr::kLanes;
+
+  // phase 1: scatter the other ranks' chunks to their owners
+  if (publish) {
+    for (int64_t u = u0; u < units; u += ustep) {
+      const int64_t w0 = Pr::word0(u, sub);
+      const int cnt = Pr::count(sub);
+      const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+      u32x4 v[P];
+#pragma unroll
+      for (int k = 1; k < P; ++k) {
+        const int c = (r + k) % P;
+        const int64_t nc = n - c * C < C ? (n - c * C > 0 ? n - c * C : 0) : C;
+        v[k] = load_words<DT>(slice_r + c * C * E, w0, cnt, nc, true);
+      }
+#pragma unroll
+      for (int k = 1; k < P; ++k) {
+        const int c = (r + k) % P;
+        char *dst = a.sym + (uint64_t)c * a.stride + a.area + (uint64_t)slot_of(r, c) * a.slot;
+        st_pkt(make_rsrc(dst, (uint32_t)a.slot), off, Pr::pack(v[k], a.epoch, sub));
+      }
+    }
+  }
+
+  // phase 2: reduce the own chunk and publish it to every peer
+  {
+    const int64_t nr = n - r * C < C ? (n - r * C > 0 ? n - r * C : 0) : C;
+    for (int64_t u = u0; u < units; u += ustep) {
+      const int64_t w0 = Pr::word0(u, sub);
+      const int cnt = Pr::count(sub);
+      const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+      const u32x4 own = load_words<DT>(slice_r + r * C * E, w0, cnt, nr, true);
+      u32x4 got[P];
+      poll_all<Pr, P>(slice_r + a.area, a.slot, off, r, a.epoch, deadline, got);
+#pragma unroll
+      for (int q = 0; q < P; ++q) got[q] = Pr::unpack(got[q], sub);
+      const u32x4 res = reduce_ordered<Pr, DT, P>(got, own, r);
+      store_words<DT>(out_r + r * C * E, w0, cnt, nr, al4, res);
+      if (publish) bcast<P>(a, ag_area, r, off, Pr::pack(res, a.epoch, sub));
+    }
+  }
+
+  // phase 3: gather every other reduced chunk
+  {
+    for (int64_t u = u0; u < units; u += ustep) {
+      const int64_t w0 = Pr::word0(u, sub);
+      const int cnt = Pr::count(sub);
+      const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+      u32x4 got[P];
+      poll_all<Pr, P>(slice_r + ag_area, a.slot, off, r, a.epoch, deadline, got);
+#pragma unroll
+      for (int q = 0; q < P; ++q) {
+        if (q == r) continue;
+        const int64_t nq = n - q * C < C ? (n - q * C > 0 ? n - q * C : 0) : C;
+        store_words<DT>(out_r + q * C * E, w0, cnt, nq, al4, Pr::unpack(got[q], sub));
+      }
+    }
+  }
+  stamp_end(a);
+}
+
+// ---------------------------------------------------------------------------
+// Stand-alone ReduceScatter: rank r's input is P chunks of m = a.n elements;
+// chunk c goes to slot (c <- r); rank r reduces chunk r.  Same two steps as
+// phases 1-2 of the two-shot kernel, with chunks of exactly m elements.
+template <class Pr, int DT, int P>
+__global__ __launch_bounds__(1024) void k_reduce_scatter(KArgs a) {
+  stamp_start(a);
+  const Part pt = part_of_block<P>();
+  const int r = pt.r;
+  constexpr int E = Elem<DT>::kBytes;
+  const uint64_t deadline = now_ticks() + a.timeout;
+  char *const slice_r = a.sym + (uint64_t)r * a.stride;
+  const int64_t m = a.n;
+  const int64_t units = Pr::units((m * E + 3) / 4);
+  const bool al4 = a.al4 != 0;
+  const bool publish = (r != a.mute);
+  const int64_t g = (int64_t)pt.w * blockDim.x + threadIdx.x;
+  const int sub = (int)(g % Pr::kLanes);
+  const int64_t u0 = g / Pr::kLanes;
+  const int64_t ustep = (int64_t)pt.W * blockDim.x / Pr::kLanes;
+
+  if (publish) {
+    for (int64_t u = u0; u < units; u += ustep) {
+      const int64_t w0 = Pr::word0(u, sub);
+      const int cnt = Pr::count(sub);
+      const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+      u32x4 v[P];
+#pragma unroll
+      for (int k = 1; k < P; ++k) {
+        const int c = (r + k) % P;
+        v[k] = load_words<DT>(slice_r + c * m * E, w0, cnt, m, al4);
+      }
+#pragma unroll
+      for (int k = 1; k < P; ++k) {
+        const int c = (r + k) % P;
+        char *dst = a.sym + (uint64_t)c * a.stride + a.area + (uint64_t)slot_of(r, c) * a.slot;
+        st_pkt(make_rsrc(dst, (uint32_t)a.slot), off, Pr::pack(v[k], a.epoch, sub));
+      }
+    }
+  }
+
+  char *const out_r = a.out + (uint64_t)r * (uint64_t)m * E;
+  for (int64_t u = u0; u < units; u += ustep) {
+    const int64_t w0 = Pr::word0(u, sub);
+    const int cnt = Pr::count(sub);
+    const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+    const u32x4 own = load_words<DT>(slice_r + r * m * E, w0, cnt, m, al4);
+    u32x4 got[P];
+    poll_all<Pr, P>(slice_r + a.area, a.slot, off, r, a.epoch, deadline, got);
+#pragma unroll
+    for (int q = 0; q < P; ++q) got[q] = Pr::unpack(got[q], sub);
+    const u32x4 res = reduce_ordered<Pr, DT, P>(got, own, r);
+    store_words<DT>(out_r, w0, cnt, m, al4, res);
+  }
+  stamp_end(a);
+}
+
+// ---------------------------------------------------------------------------
+// Stand-alone AllGather: rank r sends its s = a.n input elements to slot
+// (q <- r) of every peer, copies them to its own output, and stores what it
+// receives from peer q at block q of its output.
+template <class Pr, int DT, int P>
+__global__ __launch_bounds__(1024) void k_allgather(KArgs a) {
+  stamp_start(a);
+  const Part pt = part_of_block<P>();
+  const int r = pt.r;
+  constexpr int E = Elem<DT>::kBytes;
+  const uint64_t deadline = now_ticks() + a.timeout;
+  char *const slice_r = a.sym + (uint64_t)r * a.stride;
+  const int64_t s = a.n;
+  const int64_t units = Pr::units((s * E + 3) / 4);
+  const bool al4 = a.al4 != 0;
+  char *const out_r = a.out + (uint64_t)r * (uint64_t)P * s * E;
+  const bool publish = (r != a.mute);
+  const int64_t g = (int64_t)pt.w * blockDim.x + threadIdx.x;
+  const int sub = (int)(g % Pr::kLanes);
+  const int64_t ustep = (int64_t)pt.W * blockDim.x / Pr::kLanes;
+
+  for (int64_t u = g / Pr::kLanes; u < units; u += ustep) {
+    const int64_t w0 = Pr::word0(u, sub);
+    const int cnt = Pr::count(sub);
+    const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+    const u32x4 own = load_words<DT>(slice_r, w0, cnt, s, true);
+    if (publish) bcast<P>(a, a.area, r, off, Pr::pack(own, a.epoch, sub));
+    store_words<DT>(out_r + r * s * E, w0, cnt, s, al4, own);
+    u32x4 got[P];
+    poll_all<Pr, P>(slice_r + a.area, a.slot, off, r, a.epoch, deadline, got);
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      if (q == r) continue;
+      store_words<DT>(out_r + q * s * E, w0, cnt, s, al4, Pr::unpack(got[q], sub));
+    }
+  }
+  stamp_end(a);
+}
+
+// Zero the packet areas [lo, hi) of every slice.
+__global__ __launch_bounds__(256) void k_zero_areas(char *sym, uint64_t stride, int nranks, uint64_t lo, uint64_t hi) {
+  const uint64_t per = (hi - lo) / 16;
+  const uint64_t total = per * (uint64_t)nranks;
+  const u32x4 z = {0u, 0u, 0u, 0u};
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (uint64_t)gridDim.x * blockDim.x) {
+    const uint64_t rk = i / per;
+    const uint64_t k = i % per;
+    *(u32x4 *)(sym + rk * stride + lo + k * 16) = z;
+  }
+}
+
+}  // namespace llc

@@ -1,0 +1,77 @@
+// Slice layout arithmetic (host side).
+//
+// A region is P slices of `stride` bytes.  Each slice is
+//   [0, cap)                   input area (the rank's input at offset 0)
+//   [cap, cap + A8)            8-byte packet area
+//   [cap + A8, cap + A8 + A128) 128-byte line area
+// where cap is the largest multiple of 256 for which both areas, sized for
+// the most demanding algorithm at an input of cap bytes, fit in the slice.
+// The layout therefore depends only on (stride, P): a byte that holds input
+// in one call is never read as a flag in another, and the two packet formats
+// never share bytes, so a stale payload word can never pose as a flag.
+//
+// Within an area a call places its slots from the area's start:
+//   one-shot / AllGather   P-1 slots, each holding a full input
+//   ReduceScatter          P-1 slots, each holding one chunk
+//   two-shot               P-1 ReduceScatter slots, then P-1 AllGather slots,
+//                          each holding one chunk
+// In the 8-byte area every packet is 8-byte aligned, so flags always sit at
+// the odd dwords; in the line area every line is 128-byte aligned, so flags
+// always sit at dwords 15 and 31 of a line.
+#pragma once
+
+#include <stdint.h>
+
+#include <algorithm>
+
+namespace llc {
+namespace layout {
+
+constexpr uint64_t kAlign = 256;
+constexpr uint64_t kMaxInputBytes = 256ull << 20;  // keeps every call's P-1 slots within 4 GiB
+
+inline uint64_t roundup(uint64_t x, uint64_t m) { return (x + m - 1) / m * m; }
+inline uint64_t ceil_div(uint64_t x, uint64_t m) { return (x + m - 1) / m; }
+
+// Slot bytes for a payload of `bytes`.
+inline uint64_t slot8(uint64_t bytes) { return roundup(ceil_div(bytes, 4) * 8, kAlign); }
+inline uint64_t slot128(uint64_t bytes) { return roundup(ceil_div(ceil_div(bytes, 4), 30) * 128, kAlign); }
+
+// Two-shot chunk length in elements: ceil(n / P) rounded up to 16 bytes.
+inline uint64_t twoshot_chunk(uint64_t n, int P, int esize) {
+  const uint64_t g = 16 / (uint64_t)esize;
+  return roundup(ceil_div(n, (uint64_t)P), g);
+}
+
+// Upper bound of a two-shot chunk's bytes for an input of M bytes, for either
+// element size (ceil(n/P)*esize <= M/P + 4).
+inline uint64_t chunk_bound(uint64_t M, int P) { return roundup(ceil_div(M, (uint64_t)P) + 4, 16); }
+
+inline uint64_t area8(uint64_t M, int P) {
+  const uint64_t p1 = (uint64_t)(P - 1);
+  return std::max(p1 * slot8(M), 2 * p1 * slot8(chunk_bound(M, P)));
+}
+
+inline uint64_t area128(uint64_t M, int P) {
+  const uint64_t p1 = (uint64_t)(P - 1);
+  return std::max(p1 * slot128(M), 2 * p1 * slot128(chunk_bound(M, P)));
+}
+
+inline uint64_t slice_for(uint64_t cap, int P) { return cap + area8(cap, P) + area128(cap, P); }
+
+// Largest cap (multiple of 256, at most kMaxInputBytes) with slice_for(cap) <= stride.
+inline uint64_t capacity(uint64_t stride, int P) {
+  uint64_t lo = 0, hi = std::min(stride, kMaxInputBytes) / kAlign;
+  while (lo < hi) {
+    const uint64_t mid = (lo + hi + 1) / 2;
+    if (slice_for(mid * kAlign, P) <= stride) {
+      lo = mid;
+    } else {
+      hi = mid - 1;
+    }
+  }
+  return lo * kAlign;
+}
+
+}  // namespace layout
+}  // namespace llc

@@ -1,0 +1,565 @@
+// C-ABI entry points of the llcoll library (declared in include/llcoll.h and
+// include/llprobe.h): argument checking, slice layout, launch shape, kernel
+// dispatch.  Argument checking happens before any HIP call.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <atomic>
+#include <mutex>
+
+#include "../../include/llcoll.h"
+#include "../../include/llprobe.h"
+#include "ll_device.hpp"
+#include "ll_kernels.hpp"
+#include "ll_layout.hpp"
+#include "ll_probe.hpp"
+
+namespace llc {
+__device__ uint32_t g_ll_status[4];
+}
+
+using namespace llc;
+namespace L = llc::layout;
+
+namespace {
+
+// ---------------------------------------------------------------- settings
+std::atomic<int> g_wg_per_rank{0};
+std::atomic<int> g_threads{0};
+std::atomic<uint64_t> g_timeout{200000000ull};  // 2 s of the 100 MHz clock
+std::atomic<int> g_mute{-1};
+std::atomic<uint64_t *> g_stamps{nullptr};
+std::atomic<int> g_last_grid{0};
+std::atomic<int> g_last_threads{0};
+thread_local int t_last_hip = 0;
+thread_local char t_msg[256];
+struct TimeoutInfo {
+  int rank = -1;
+  uint32_t missing = 0, epoch = 0;
+};
+TimeoutInfo g_last_timeout;
+std::mutex g_mu;
+
+// ---------------------------------------------------------------- kernels
+enum Kind { K_ONESHOT = 0, K_TWOSHOT = 1, K_RS = 2, K_AG = 3, K_KINDS = 4 };
+enum Proto { PR_LL = 0, PR_LINE = 1, PR_COUNT = 2 };
+
+typedef void (*kernel_fn)(KArgs);
+
+template <class Pr, int DT, int P>
+void fill_row(kernel_fn *row) {
+  row[K_ONESHOT] = k_oneshot<Pr, DT, P>;
+  row[K_TWOSHOT] = k_twoshot<Pr, DT, P>;
+  row[K_RS] = k_reduce_scatter<Pr, DT, P>;
+  row[K_AG] = k_allgather<Pr, DT, P>;
+}
+
+// table[proto][dtype][P][kind]
+struct Table {
+  kernel_fn k[PR_COUNT][2][LL_MAX_RANKS + 1][K_KINDS];
+  Table() {
+    memset(k, 0, sizeof k);
+    fill<2>();
+    fill<3>();
+    fill<4>();
+    fill<5>();
+    fill<6>();
+    fill<7>();
+    fill<8>();
+  }
+  template <int P>
+  void fill() {
+    fill_row<ProtoLL, 0, P>(k[PR_LL][0][P]);
+    fill_row<ProtoLL, 1, P>(k[PR_LL][1][P]);
+    fill_row<ProtoLine, 0, P>(k[PR_LINE][0][P]);
+    fill_row<ProtoLine, 1, P>(k[PR_LINE][1][P]);
+  }
+};
+
+const Table &table() {
+  static const Table t;
+  return t;
+}
+
+// Per-device facts, queried on first use.
+struct DevInfo {
+  bool ok = false;
+  int cus = 0;
+};
+DevInfo g_dev[64];
+
+int device_info(DevInfo *out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    t_last_hip = (int)e;
+    return LL_ERR_HIP;
+  }
+  if (dev < 0 || dev >= 64) return LL_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (!g_dev[dev].ok) {
+    int cus = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) {
+      t_last_hip = (int)e;
+      return LL_ERR_HIP;
+    }
+    g_dev[dev].cus = cus;
+    g_dev[dev].ok = true;
+  }
+  *out = g_dev[dev];
+  return LL_OK;
+}
+
+// Largest grid of `fn` that is resident at once with `threads` per workgroup.
+int resident_grid(kernel_fn fn, int threads, int *grid_out) {
+  DevInfo d;
+  int st = device_info(&d);
+  if (st != LL_OK) return st;
+  int per_cu = 0;
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(fn), threads, 0);
+  if (e != hipSuccess) {
+    t_last_hip = (int)e;
+    return LL_ERR_HIP;
+  }
+  if (per_cu < 1) per_cu = 1;
+  *grid_out = per_cu * d.cus;
+  return LL_OK;
+}
+
+inline int esize_of(ll_dtype dt) { return dt == LL_BF16 ? 2 : 4; }
+
+int check_common(const void *sym_base, size_t rank_stride, const void *out, int nranks, uint32_t epoch) {
+  if (sym_base == nullptr || out == nullptr) return LL_ERR_INVALID;
+  if (nranks < 2 || nranks > LL_MAX_RANKS) return LL_ERR_INVALID;
+  if (((uintptr_t)sym_base % LL_ALIGN) != 0 || (rank_stride % LL_ALIGN) != 0 || rank_stride == 0) return LL_ERR_INVALID;
+  if (((uintptr_t)out % 16) != 0) return LL_ERR_INVALID;
+  if (epoch == 0) return LL_ERR_INVALID;
+  return LL_OK;
+}
+
+int check_dtype_op(int dt, int op) {
+  if (dt != LL_F32 && dt != LL_BF16) return LL_ERR_UNSUPPORTED;
+  if (op != LL_SUM) return LL_ERR_UNSUPPORTED;
+  return LL_OK;
+}
+
+bool overlaps(const void *a, uint64_t alen, const void *b, uint64_t blen) {
+  const uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+  return a0 < b0 + blen && b0 < a0 + alen;
+}
+
+struct Plan {
+  Kind kind;
+  Proto proto;
+  int dt, P;
+  KArgs a;
+  int64_t units;  // packet units per stream
+};
+
+int launch(const Plan &pl, void *stream) {
+  const kernel_fn fn = table().k[pl.proto][pl.dt][pl.P][pl.kind];
+  if (fn == nullptr) return LL_ERR_UNSUPPORTED;
+  int threads = g_threads.load();
+  if (threads == 0) threads = 256;
+  const int lanes_per_unit = pl.proto == PR_LINE ? ProtoLine::kLanes : ProtoLL::kLanes;
+  int cap_grid = 0;
+  int st = resident_grid(fn, threads, &cap_grid);
+  if (st != LL_OK) return st;
+  int wmax = cap_grid / pl.P;
+  if (wmax < 1) return LL_ERR_UNSUPPORTED;
+  int W = g_wg_per_rank.load();
+  if (W == 0) {
+    const int64_t lanes = pl.units * lanes_per_unit;
+    int64_t want = (lanes + threads - 1) / threads;
+    if (want < 1) want = 1;
+    W = (int)(want < wmax ? want : wmax);
+  } else if (W > wmax) {
+    W = wmax;  // never launch more than can be resident: waits depend on co-residency
+  }
+  const int grid = W * pl.P;
+  KArgs a = pl.a;
+  a.timeout = g_timeout.load();
+  a.mute = g_mute.load();
+  a.stamps = g_stamps.exchange(nullptr);
+  hipLaunchKernelGGL(fn, dim3(grid), dim3(threads), 0, (hipStream_t)stream, a);
+  hipError_t e = hipGetLastError();
+  g_last_grid.store(grid);
+  g_last_threads.store(threads);
+  if (e != hipSuccess) {
+    t_last_hip = (int)e;
+    return LL_ERR_HIP;
+  }
+  return LL_OK;
+}
+
+// Region geometry of one call; fails with LL_ERR_SCRATCH when the input does
+// not fit the region's input capacity.
+struct Region {
+  uint64_t cap, a8, a128;
+};
+
+int region_of(size_t rank_stride, int P, uint64_t in_bytes, Region *rg) {
+  const uint64_t cap = L::capacity(rank_stride, P);
+  if (L::slice_for(cap, P) > rank_stride) return LL_ERR_SCRATCH;
+  if (in_bytes > L::kMaxInputBytes) return LL_ERR_UNSUPPORTED;
+  if (in_bytes > cap) return LL_ERR_SCRATCH;
+  rg->cap = cap;
+  rg->a8 = L::area8(cap, P);
+  rg->a128 = L::area128(cap, P);
+  return LL_OK;
+}
+
+KArgs base_args(void *sym_base, size_t rank_stride, void *out, uint32_t epoch) {
+  KArgs a;
+  memset(&a, 0, sizeof a);
+  a.sym = (char *)sym_base;
+  a.stride = rank_stride;
+  a.out = (char *)out;
+  a.epoch = epoch;
+  a.mute = -1;
+  return a;
+}
+
+ll_algo auto_algo(uint64_t in_bytes, int P) {
+  (void)P;
+  if (in_bytes <= (256u << 10)) return LL_ALGO_ONESHOT;
+  return LL_ALGO_TWOSHOT_LINE;
+}
+
+ll_proto auto_proto(uint64_t in_bytes) { return in_bytes <= (64u << 10) ? LL_PROTO_PACKET8 : LL_PROTO_LINE128; }
+
+}  // namespace
+
+// =================================================================== C ABI
+extern "C" {
+
+int ll_slice_bytes(size_t count, ll_dtype dt, int nranks, size_t *min_rank_stride) {
+  if (min_rank_stride == nullptr) return LL_ERR_INVALID;
+  if (nranks < 2 || nranks > LL_MAX_RANKS) return LL_ERR_INVALID;
+  if (dt != LL_F32 && dt != LL_BF16) return LL_ERR_UNSUPPORTED;
+  const uint64_t es = (uint64_t)esize_of(dt);
+  if (count > L::kMaxInputBytes / es) return LL_ERR_UNSUPPORTED;
+  const uint64_t cap = L::roundup((uint64_t)count * es, L::kAlign);
+  *min_rank_stride = (size_t)L::slice_for(cap, nranks);
+  return LL_OK;
+}
+
+int ll_input_capacity(size_t rank_stride, int nranks, size_t *capacity_bytes) {
+  if (capacity_bytes == nullptr) return LL_ERR_INVALID;
+  if (nranks < 2 || nranks > LL_MAX_RANKS) return LL_ERR_INVALID;
+  if (rank_stride % LL_ALIGN != 0) return LL_ERR_INVALID;
+  const uint64_t cap = L::capacity(rank_stride, nranks);
+  if (L::slice_for(cap, nranks) > rank_stride) return LL_ERR_SCRATCH;
+  *capacity_bytes = (size_t)cap;
+  return LL_OK;
+}
+
+int ll_init(void *sym_base, size_t rank_stride, int nranks, void *stream) {
+  if (sym_base == nullptr) return LL_ERR_INVALID;
+  if (nranks < 2 || nranks > LL_MAX_RANKS) return LL_ERR_INVALID;
+  if (((uintptr_t)sym_base % LL_ALIGN) != 0 || rank_stride % LL_ALIGN != 0 || rank_stride == 0) return LL_ERR_INVALID;
+  Region rg;
+  int st = region_of(rank_stride, nranks, 0, &rg);
+  if (st != LL_OK) return st;
+  const uint64_t lo = rg.cap, hi = rg.cap + rg.a8 + rg.a128;
+  if (hi == lo) return LL_OK;
+  DevInfo d;
+  st = device_info(&d);
+  if (st != LL_OK) return st;
+  hipLaunchKernelGGL(k_zero_areas, dim3(d.cus * 4), dim3(256), 0, (hipStream_t)stream, (char *)sym_base,
+                     (uint64_t)rank_stride, nranks, lo, hi);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    t_last_hip = (int)e;
+    return LL_ERR_HIP;
+  }
+  return LL_OK;
+}
+
+int ll_allreduce_algo(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt, ll_op op,
+                      int nranks, uint32_t epoch, void *stream, ll_algo algo) {
+  int st = check_common(sym_base, rank_stride, out, nranks, epoch);
+  if (st != LL_OK) return st;
+  st = check_dtype_op((int)dt, (int)op);
+  if (st != LL_OK) return st;
+  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_ONESHOT_LINE) return LL_ERR_INVALID;
+  const int es = esize_of(dt);
+  const uint64_t in_bytes = (uint64_t)count * es;
+  if (count > L::kMaxInputBytes) return LL_ERR_UNSUPPORTED;
+  if (overlaps(out, in_bytes * nranks, sym_base, (uint64_t)rank_stride * nranks)) return LL_ERR_INVALID;
+  Region rg;
+  st = region_of(rank_stride, nranks, in_bytes, &rg);
+  if (st != LL_OK) return st;
+  if (count == 0) return LL_OK;
+  if (algo == LL_ALGO_AUTO) algo = auto_algo(in_bytes, nranks);
+
+  Plan pl;
+  pl.dt = (int)dt;
+  pl.P = nranks;
+  pl.a = base_args(sym_base, rank_stride, out, epoch);
+  pl.a.n = (int64_t)count;
+  pl.a.al4 = (in_bytes % 4 == 0) ? 1u : 0u;
+  const bool line = (algo == LL_ALGO_TWOSHOT_LINE || algo == LL_ALGO_ONESHOT_LINE);
+  pl.proto = line ? PR_LINE : PR_LL;
+  pl.a.area = line ? rg.cap + rg.a8 : rg.cap;
+  if (algo == LL_ALGO_ONESHOT || algo == LL_ALGO_ONESHOT_LINE) {
+    pl.kind = K_ONESHOT;
+    pl.a.slot = line ? L::slot128(in_bytes) : L::slot8(in_bytes);
+    const int64_t words = (int64_t)L::ceil_div(in_bytes, 4);
+    pl.units = line ? ProtoLine::units(words) : ProtoLL::units(words);
+  } else {
+    pl.kind = K_TWOSHOT;
+    const uint64_t C = L::twoshot_chunk(count, nranks, es);
+    pl.a.chunk = (int64_t)C;
+    pl.a.slot = line ? L::slot128(C * es) : L::slot8(C * es);
+    const int64_t words = (int64_t)L::ceil_div(C * es, 4);
+    pl.units = line ? ProtoLine::units(words) : ProtoLL::units(words);
+  }
+  return launch(pl, stream);
+}
+
+int ll_allreduce(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt, ll_op op, int nranks,
+                 uint32_t epoch, void *stream) {
+  return ll_allreduce_algo(sym_base, rank_stride, out, count, dt, op, nranks, epoch, stream, LL_ALGO_AUTO);
+}
+
+int ll_reduce_scatter_proto(void *sym_base, size_t rank_stride, void *out, size_t recvcount, ll_dtype dt,
+                            ll_op op, int nranks, uint32_t epoch, void *stream, ll_proto proto) {
+  int st = check_common(sym_base, rank_stride, out, nranks, epoch);
+  if (st != LL_OK) return st;
+  st = check_dtype_op((int)dt, (int)op);
+  if (st != LL_OK) return st;
+  if ((int)proto < LL_PROTO_AUTO || (int)proto > LL_PROTO_LINE128) return LL_ERR_INVALID;
+  const int es = esize_of(dt);
+  if (recvcount > L::kMaxInputBytes) return LL_ERR_UNSUPPORTED;
+  const uint64_t chunk_bytes = (uint64_t)recvcount * es;
+  const uint64_t in_bytes = chunk_bytes * nranks;
+  if (overlaps(out, chunk_bytes * nranks, sym_base, (uint64_t)rank_stride * nranks)) return LL_ERR_INVALID;
+  Region rg;
+  st = region_of(rank_stride, nranks, in_bytes, &rg);
+  if (st != LL_OK) return st;
+  if (recvcount == 0) return LL_OK;
+  if (proto == LL_PROTO_AUTO) proto = auto_proto(in_bytes);
+  Plan pl;
+  pl.kind = K_RS;
+  pl.dt = (int)dt;
+  pl.P = nranks;
+  pl.proto = proto == LL_PROTO_LINE128 ? PR_LINE : PR_LL;
+  pl.a = base_args(sym_base, rank_stride, out, epoch);
+  pl.a.n = (int64_t)recvcount;
+  pl.a.al4 = (chunk_bytes % 4 == 0) ? 1u : 0u;
+  pl.a.area = pl.proto == PR_LINE ? rg.cap + rg.a8 : rg.cap;
+  pl.a.slot = pl.proto == PR_LINE ? L::slot128(chunk_bytes) : L::slot8(chunk_bytes);
+  const int64_t words = (int64_t)L::ceil_div(chunk_bytes, 4);
+  pl.units = pl.proto == PR_LINE ? ProtoLine::units(words) : ProtoLL::units(words);
+  return launch(pl, stream);
+}
+
+int ll_reduce_scatter(void *sym_base, size_t rank_stride, void *out, size_t recvcount, ll_dtype dt, ll_op op,
+                      int nranks, uint32_t epoch, void *stream) {
+  return ll_reduce_scatter_proto(sym_base, rank_stride, out, recvcount, dt, op, nranks, epoch, stream,
+                                 LL_PROTO_AUTO);
+}
+
+int ll_allgather_proto(void *sym_base, size_t rank_stride, void *out, size_t sendcount, ll_dtype dt, int nranks,
+                       uint32_t epoch, void *stream, ll_proto proto) {
+  int st = check_common(sym_base, rank_stride, out, nranks, epoch);
+  if (st != LL_OK) return st;
+  st = check_dtype_op((int)dt, LL_SUM);
+  if (st != LL_OK) return st;
+  if ((int)proto < LL_PROTO_AUTO || (int)proto > LL_PROTO_LINE128) return LL_ERR_INVALID;
+  const int es = esize_of(dt);
+  if (sendcount > L::kMaxInputBytes) return LL_ERR_UNSUPPORTED;
+  const uint64_t in_bytes = (uint64_t)sendcount * es;
+  if (overlaps(out, in_bytes * nranks * nranks, sym_base, (uint64_t)rank_stride * nranks)) return LL_ERR_INVALID;
+  Region rg;
+  st = region_of(rank_stride, nranks, in_bytes, &rg);
+  if (st != LL_OK) return st;
+  if (sendcount == 0) return LL_OK;
+  if (proto == LL_PROTO_AUTO) proto = auto_proto(in_bytes * nranks);
+  Plan pl;
+  pl.kind = K_AG;
+  pl.dt = (int)dt;
+  pl.P = nranks;
+  pl.proto = proto == LL_PROTO_LINE128 ? PR_LINE : PR_LL;
+  pl.a = base_args(sym_base, rank_stride, out, epoch);
+  pl.a.n = (int64_t)sendcount;
+  pl.a.al4 = (in_bytes % 4 == 0) ? 1u : 0u;
+  pl.a.area = pl.proto == PR_LINE ? rg.cap + rg.a8 : rg.cap;
+  pl.a.slot = pl.proto == PR_LINE ? L::slot128(in_bytes) : L::slot8(in_bytes);
+  const int64_t words = (int64_t)L::ceil_div(in_bytes, 4);
+  pl.units = pl.proto == PR_LINE ? ProtoLine::units(words) : ProtoLL::units(words);
+  return launch(pl, stream);
+}
+
+int ll_allgather(void *sym_base, size_t rank_stride, void *out, size_t sendcount, ll_dtype dt, int nranks,
+                 uint32_t epoch, void *stream) {
+  return ll_allgather_proto(sym_base, rank_stride, out, sendcount, dt, nranks, epoch, stream, LL_PROTO_AUTO);
+}
+
+int ll_check(void *stream) {
+  hipError_t e = hipStreamSynchronize((hipStream_t)stream);
+  if (e != hipSuccess) {
+    t_last_hip = (int)e;
+    return LL_ERR_HIP;
+  }
+  uint32_t st[4] = {0, 0, 0, 0};
+  e = hipMemcpyFromSymbol(st, HIP_SYMBOL(llc::g_ll_status), sizeof st, 0, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) {
+    t_last_hip = (int)e;
+    return LL_ERR_HIP;
+  }
+  if (st[0] == 0) return LL_OK;
+  const uint32_t zero[4] = {0, 0, 0, 0};
+  e = hipMemcpyToSymbol(HIP_SYMBOL(llc::g_ll_status), zero, sizeof zero, 0, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    t_last_hip = (int)e;
+    return LL_ERR_HIP;
+  }
+  {
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_last_timeout.rank = (int)st[1];
+    g_last_timeout.missing = st[2];
+    g_last_timeout.epoch = st[3];
+  }
+  return st[0] == kStatusTimeout ? LL_ERR_TIMEOUT : LL_ERR_HIP;
+}
+
+int ll_last_timeout(int *rank, uint32_t *missing_peers, uint32_t *epoch) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  if (rank) *rank = g_last_timeout.rank;
+  if (missing_peers) *missing_peers = g_last_timeout.missing;
+  if (epoch) *epoch = g_last_timeout.epoch;
+  return LL_OK;
+}
+
+const char *ll_strerror(int status) {
+  switch (status) {
+    case LL_OK:
+      return "success";
+    case LL_ERR_INVALID:
+      return "invalid argument";
+    case LL_ERR_UNSUPPORTED:
+      return "unsupported data type, operation or size";
+    case LL_ERR_SCRATCH:
+      return "input larger than the region's input capacity (rank_stride too small)";
+    case LL_ERR_HIP:
+      snprintf(t_msg, sizeof t_msg, "HIP runtime error: %s", hipGetErrorString((hipError_t)t_last_hip));
+      return t_msg;
+    case LL_ERR_TIMEOUT:
+      return "a flag wait timed out (a peer never published, or the epoch was reused)";
+    default:
+      return "unknown status";
+  }
+}
+
+int ll_set_launch(int workgroups_per_rank, int threads) {
+  if (workgroups_per_rank < 0 || workgroups_per_rank > 4096) return LL_ERR_INVALID;
+  if (threads != 0 && (threads < 64 || threads > 1024 || threads % 64 != 0)) return LL_ERR_INVALID;
+  g_wg_per_rank.store(workgroups_per_rank);
+  g_threads.store(threads);
+  return LL_OK;
+}
+
+int ll_set_poll_timeout(uint64_t ticks) {
+  if (ticks == 0) return LL_ERR_INVALID;
+  g_timeout.store(ticks);
+  return LL_OK;
+}
+
+int ll_debug_mute_rank(int rank) {
+  if (rank < -1 || rank >= LL_MAX_RANKS) return LL_ERR_INVALID;
+  g_mute.store(rank);
+  return LL_OK;
+}
+
+int ll_debug_stamp_next(uint64_t *stamps) {
+  g_stamps.store(stamps);
+  return LL_OK;
+}
+
+int ll_last_grid(int *grid, int *threads) {
+  if (grid) *grid = g_last_grid.load();
+  if (threads) *threads = g_last_threads.load();
+  return LL_OK;
+}
+
+// ------------------------------------------------------------------ probes
+static int probe_launch_check(int grid, int threads) {
+  if (grid < 1 || grid > 65536) return LL_ERR_INVALID;
+  if (threads < 64 || threads > 1024 || threads % 64 != 0) return LL_ERR_INVALID;
+  return LL_OK;
+}
+
+static int hip_status() {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    t_last_hip = (int)e;
+    return LL_ERR_HIP;
+  }
+  return LL_OK;
+}
+
+int ll_probe_empty(int grid, int threads, uint64_t *stamps, void *stream) {
+  int st = probe_launch_check(grid, threads);
+  if (st != LL_OK) return st;
+  hipLaunchKernelGGL(k_probe_empty, dim3(grid), dim3(threads), 0, (hipStream_t)stream, stamps);
+  return hip_status();
+}
+
+int ll_probe_floor(const uint64_t *chase, uint64_t chase_len, uint64_t start, uint64_t *sink, int grid, int threads,
+                   uint64_t *stamps, void *stream) {
+  int st = probe_launch_check(grid, threads);
+  if (st != LL_OK) return st;
+  if (chase == nullptr || sink == nullptr || start >= chase_len) return LL_ERR_INVALID;
+  hipLaunchKernelGGL(k_probe_floor, dim3(grid), dim3(threads), 0, (hipStream_t)stream, chase, start, sink, stamps);
+  return hip_status();
+}
+
+int ll_probe_chase(const uint64_t *chase, uint64_t chase_len, uint64_t start, int steps, uint64_t *out3,
+                   void *stream) {
+  if (chase == nullptr || out3 == nullptr || start >= chase_len || steps < 1) return LL_ERR_INVALID;
+  hipLaunchKernelGGL(k_probe_chase, dim3(1), dim3(64), 0, (hipStream_t)stream, chase, chase_len, start, steps, out3);
+  return hip_status();
+}
+
+int ll_probe_fence_l2(uint32_t *buf4k, int iters, uint64_t *out7, void *stream) {
+  if (buf4k == nullptr || out7 == nullptr || iters < 1) return LL_ERR_INVALID;
+  hipLaunchKernelGGL(k_probe_fence_l2, dim3(1), dim3(64), 0, (hipStream_t)stream, buf4k, iters, out7);
+  return hip_status();
+}
+
+int ll_probe_pingpong(uint32_t *flags8k, int rounds, int grid, int peer, uint64_t limit_ticks, uint64_t *out3,
+                      void *stream) {
+  if (flags8k == nullptr || out3 == nullptr || rounds < 1 || grid < 2 || grid > 1024 || peer < 1 || peer >= grid ||
+      limit_ticks == 0)
+    return LL_ERR_INVALID;
+  hipLaunchKernelGGL(k_probe_pingpong, dim3(grid), dim3(64), 0, (hipStream_t)stream, flags8k, rounds, peer,
+                     limit_ticks, out3);
+  return hip_status();
+}
+
+int ll_probe_xcd(uint32_t *ids, int grid, int threads, void *stream) {
+  int st = probe_launch_check(grid, threads);
+  if (st != LL_OK) return st;
+  if (ids == nullptr) return LL_ERR_INVALID;
+  hipLaunchKernelGGL(k_probe_xcd, dim3(grid), dim3(threads), 0, (hipStream_t)stream, ids);
+  return hip_status();
+}
+
+int ll_probe_litmus(uint32_t *buf, size_t buf_bytes, int grid, int lines, int iters, int reads, int layout,
+                    unsigned long long *counts4, void *stream) {
+  if (buf == nullptr || counts4 == nullptr) return LL_ERR_INVALID;
+  if (grid < 2 || grid % 2 != 0 || grid > 512 || lines < 1 || iters < 1 || reads < 1) return LL_ERR_INVALID;
+  if (layout != 0 && layout != 1) return LL_ERR_INVALID;
+  if ((uint64_t)(grid / 2) * (uint64_t)lines * 128u > buf_bytes) return LL_ERR_INVALID;
+  if ((uint64_t)lines * 128u > 0xFFFFFFFFull) return LL_ERR_INVALID;
+  hipLaunchKernelGGL(k_probe_litmus, dim3(grid), dim3(256), 0, (hipStream_t)stream, buf, lines, iters, reads, layout,
+                     counts4);
+  return hip_status();
+}
+
+}  // extern "C"

@@ -1,0 +1,195 @@
+"""Python binding of the llcoll C ABI (``include/llcoll.h``, ``include/llprobe.h``).
+
+Argument marshalling only: every function has the C name, takes the same
+arguments (device pointers and streams as integers) and returns the C status
+code.  All computation happens in the HIP library; if the library has not
+been built this module fails to import -- there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libllcoll.so")
+
+LL_F32, LL_BF16 = 0, 1
+LL_SUM = 0
+LL_ALGO_AUTO, LL_ALGO_ONESHOT, LL_ALGO_TWOSHOT, LL_ALGO_TWOSHOT_LINE, LL_ALGO_ONESHOT_LINE = 0, 1, 2, 3, 4
+LL_PROTO_AUTO, LL_PROTO_PACKET8, LL_PROTO_LINE128 = 0, 1, 2
+
+LL_OK = 0
+LL_ERR_INVALID = -1
+LL_ERR_UNSUPPORTED = -2
+LL_ERR_SCRATCH = -3
+LL_ERR_HIP = -4
+LL_ERR_TIMEOUT = -5
+
+ALGOS = {
+    "auto": LL_ALGO_AUTO, "oneshot": LL_ALGO_ONESHOT, "twoshot": LL_ALGO_TWOSHOT,
+    "twoshot_line": LL_ALGO_TWOSHOT_LINE, "oneshot_line": LL_ALGO_ONESHOT_LINE,
+}
+PROTOS = {"auto": LL_PROTO_AUTO, "packet8": LL_PROTO_PACKET8, "line128": LL_PROTO_LINE128}
+DTYPES = {"f32": LL_F32, "bf16": LL_BF16}
+
+# name -> (restype, argtypes)
+_vp, _sz, _i, _u32, _u64 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_uint32, ctypes.c_uint64
+_SIGS = {
+    "ll_slice_bytes": (_i, [_sz, _i, _i, ctypes.POINTER(_sz)]),
+    "ll_input_capacity": (_i, [_sz, _i, ctypes.POINTER(_sz)]),
+    "ll_init": (_i, [_vp, _sz, _i, _vp]),
+    "ll_allreduce": (_i, [_vp, _sz, _vp, _sz, _i, _i, _i, _u32, _vp]),
+    "ll_allreduce_algo": (_i, [_vp, _sz, _vp, _sz, _i, _i, _i, _u32, _vp, _i]),
+    "ll_reduce_scatter": (_i, [_vp, _sz, _vp, _sz, _i, _i, _i, _u32, _vp]),
+    "ll_reduce_scatter_proto": (_i, [_vp, _sz, _vp, _sz, _i, _i, _i, _u32, _vp, _i]),
+    "ll_allgather": (_i, [_vp, _sz, _vp, _sz, _i, _i, _u32, _vp]),
+    "ll_allgather_proto": (_i, [_vp, _sz, _vp, _sz, _i, _i, _u32, _vp, _i]),
+    "ll_check": (_i, [_vp]),
+    "ll_last_timeout": (_i, [ctypes.POINTER(_i), ctypes.POINTER(_u32), ctypes.POINTER(_u32)]),
+    "ll_strerror": (ctypes.c_char_p, [_i]),
+    "ll_set_launch": (_i, [_i, _i]),
+    "ll_set_poll_timeout": (_i, [_u64]),
+    "ll_debug_mute_rank": (_i, [_i]),
+    "ll_debug_stamp_next": (_i, [_vp]),
+    "ll_last_grid": (_i, [ctypes.POINTER(_i), ctypes.POINTER(_i)]),
+    "ll_probe_empty": (_i, [_i, _i, _vp, _vp]),
+    "ll_probe_floor": (_i, [_vp, _u64, _u64, _vp, _i, _i, _vp, _vp]),
+    "ll_probe_chase": (_i, [_vp, _u64, _u64, _i, _vp, _vp]),
+    "ll_probe_fence_l2": (_i, [_vp, _i, _vp, _vp]),
+    "ll_probe_pingpong": (_i, [_vp, _i, _i, _i, _u64, _vp, _vp]),
+    "ll_probe_xcd": (_i, [_vp, _i, _i, _vp]),
+    "ll_probe_litmus": (_i, [_vp, _sz, _i, _i, _i, _i, _i, _vp, _vp]),
+}
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"llcoll HIP library not built ({LIB_PATH}); run __graft_entry__.build()")
+_lib = ctypes.CDLL(LIB_PATH)
+for _name, (_res, _args) in _SIGS.items():
+    _fn = getattr(_lib, _name)
+    _fn.restype = _res
+    _fn.argtypes = _args
+
+
+class LLError(RuntimeError):
+    def __init__(self, status: int, where: str = ""):
+        self.status = status
+        super().__init__(f"{where}: {ll_strerror(status)} ({status})" if where else f"{ll_strerror(status)} ({status})")
+
+
+def check(status: int, where: str = "") -> int:
+    if status != LL_OK:
+        raise LLError(status, where)
+    return status
+
+
+def exported_symbols():
+    return list(_SIGS)
+
+
+def library():
+    return _lib
+
+
+# ---------------------------------------------------------------- C entry points
+def ll_slice_bytes(count: int, dt: int, nranks: int):
+    out = ctypes.c_size_t(0)
+    st = _lib.ll_slice_bytes(count, dt, nranks, ctypes.byref(out))
+    return st, out.value
+
+
+def ll_input_capacity(rank_stride: int, nranks: int):
+    out = ctypes.c_size_t(0)
+    st = _lib.ll_input_capacity(rank_stride, nranks, ctypes.byref(out))
+    return st, out.value
+
+
+def ll_init(sym_base, rank_stride, nranks, stream):
+    return _lib.ll_init(sym_base, rank_stride, nranks, stream)
+
+
+def ll_allreduce(sym_base, rank_stride, out, count, dt, op, nranks, epoch, stream):
+    return _lib.ll_allreduce(sym_base, rank_stride, out, count, dt, op, nranks, epoch, stream)
+
+
+def ll_allreduce_algo(sym_base, rank_stride, out, count, dt, op, nranks, epoch, stream, algo):
+    return _lib.ll_allreduce_algo(sym_base, rank_stride, out, count, dt, op, nranks, epoch, stream, algo)
+
+
+def ll_reduce_scatter(sym_base, rank_stride, out, recvcount, dt, op, nranks, epoch, stream):
+    return _lib.ll_reduce_scatter(sym_base, rank_stride, out, recvcount, dt, op, nranks, epoch, stream)
+
+
+def ll_reduce_scatter_proto(sym_base, rank_stride, out, recvcount, dt, op, nranks, epoch, stream, proto):
+    return _lib.ll_reduce_scatter_proto(sym_base, rank_stride, out, recvcount, dt, op, nranks, epoch, stream, proto)
+
+
+def ll_allgather(sym_base, rank_stride, out, sendcount, dt, nranks, epoch, stream):
+    return _lib.ll_allgather(sym_base, rank_stride, out, sendcount, dt, nranks, epoch, stream)
+
+
+def ll_allgather_proto(sym_base, rank_stride, out, sendcount, dt, nranks, epoch, stream, proto):
+    return _lib.ll_allgather_proto(sym_base, rank_stride, out, sendcount, dt, nranks, epoch, stream, proto)
+
+
+def ll_check(stream):
+    return _lib.ll_check(stream)
+
+
+def ll_last_timeout():
+    r, m, e = ctypes.c_int(0), ctypes.c_uint32(0), ctypes.c_uint32(0)
+    _lib.ll_last_timeout(ctypes.byref(r), ctypes.byref(m), ctypes.byref(e))
+    return r.value, m.value, e.value
+
+
+def ll_strerror(status: int) -> str:
+    return _lib.ll_strerror(status).decode()
+
+
+def ll_set_launch(workgroups_per_rank: int, threads: int):
+    return _lib.ll_set_launch(workgroups_per_rank, threads)
+
+
+def ll_set_poll_timeout(ticks: int):
+    return _lib.ll_set_poll_timeout(ticks)
+
+
+def ll_debug_mute_rank(rank: int):
+    return _lib.ll_debug_mute_rank(rank)
+
+
+def ll_debug_stamp_next(stamps):
+    return _lib.ll_debug_stamp_next(stamps)
+
+
+def ll_last_grid():
+    g, t = ctypes.c_int(0), ctypes.c_int(0)
+    _lib.ll_last_grid(ctypes.byref(g), ctypes.byref(t))
+    return g.value, t.value
+
+
+def ll_probe_empty(grid, threads, stamps, stream):
+    return _lib.ll_probe_empty(grid, threads, stamps, stream)
+
+
+def ll_probe_floor(chase, chase_len, start, sink, grid, threads, stamps, stream):
+    return _lib.ll_probe_floor(chase, chase_len, start, sink, grid, threads, stamps, stream)
+
+
+def ll_probe_chase(chase, chase_len, start, steps, out3, stream):
+    return _lib.ll_probe_chase(chase, chase_len, start, steps, out3, stream)
+
+
+def ll_probe_fence_l2(buf4k, iters, out7, stream):
+    return _lib.ll_probe_fence_l2(buf4k, iters, out7, stream)
+
+
+def ll_probe_pingpong(flags8k, rounds, grid, peer, limit_ticks, out3, stream):
+    return _lib.ll_probe_pingpong(flags8k, rounds, grid, peer, limit_ticks, out3, stream)
+
+
+def ll_probe_xcd(ids, grid, threads, stream):
+    return _lib.ll_probe_xcd(ids, grid, threads, stream)
+
+
+def ll_probe_litmus(buf, buf_bytes, grid, lines, iters, reads, layout, counts4, stream):
+    return _lib.ll_probe_litmus(buf, buf_bytes, grid, lines, iters, reads, layout, counts4, stream)

@@ -1,0 +1,112 @@
+"""Device memory plumbing for the collectives (torch allocations only).
+
+``SymRegion`` holds one symmetric allocation of P rank slices plus an output
+buffer, keeps the caller-owned epoch counter, and calls the C ABI through
+``llcoll``.  torch provides memory, copies and the stream; no arithmetic of
+the collectives happens here.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import llcoll as ll
+
+_ALIGN = 256
+
+
+def _aligned(nbytes: int, device) -> tuple[torch.Tensor, int]:
+    """A uint8 tensor of at least nbytes whose returned address is 256-byte aligned."""
+    t = torch.empty(nbytes + _ALIGN, dtype=torch.uint8, device=device)
+    base = t.data_ptr()
+    pad = (-base) % _ALIGN
+    return t, pad
+
+
+def _np_to_u8(bits: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.uint8).reshape(-1))
+
+
+class SymRegion:
+    """P slices of ``rank_stride`` bytes in one allocation, plus ``out``.
+
+    ``max_count`` elements of ``dtype`` ("f32" / "bf16") is the largest
+    per-rank input the region must hold; ``out_elems`` sizes the output
+    buffer (defaults to what an AllGather of max_count needs).
+    """
+
+    def __init__(self, nranks: int, max_count: int, dtype: str, device="cuda:0", out_elems: int | None = None,
+                 rank_stride: int | None = None):
+        self.nranks = nranks
+        self.dtype = dtype
+        self.dt = ll.DTYPES[dtype]
+        self.esize = 4 if dtype == "f32" else 2
+        st, need = ll.ll_slice_bytes(max_count, self.dt, nranks)
+        ll.check(st, "ll_slice_bytes")
+        self.rank_stride = rank_stride if rank_stride is not None else need
+        self.device = torch.device(device)
+        self._sym, pad = _aligned(nranks * self.rank_stride, self.device)
+        self.sym = self._sym[pad:pad + nranks * self.rank_stride]
+        if out_elems is None:
+            out_elems = nranks * nranks * max(max_count, 1)
+        self._out, opad = _aligned(out_elems * self.esize, self.device)
+        self.out = self._out[opad:opad + out_elems * self.esize]
+        self.epoch = 0
+
+    # -- addresses
+    @property
+    def base(self) -> int:
+        return self.sym.data_ptr()
+
+    @property
+    def out_ptr(self) -> int:
+        return self.out.data_ptr()
+
+    @staticmethod
+    def stream_handle(stream=None) -> int:
+        s = stream if stream is not None else torch.cuda.current_stream()
+        return s.cuda_stream
+
+    # -- set-up
+    def init(self, stream=None) -> None:
+        ll.check(ll.ll_init(self.base, self.rank_stride, self.nranks, self.stream_handle(stream)), "ll_init")
+        self.epoch = 0
+
+    def next_epoch(self) -> int:
+        if self.epoch >= 0xFFFFFFFF:
+            raise RuntimeError("epoch space exhausted: call init() first")
+        self.epoch += 1
+        return self.epoch
+
+    def write_inputs(self, bits: np.ndarray) -> None:
+        """Copy rank r's raw element bits (row r of a [P, n] array) to offset 0 of slice r."""
+        assert bits.shape[0] == self.nranks
+        row_bytes = bits.shape[1] * bits.dtype.itemsize
+        host = _np_to_u8(bits).reshape(self.nranks, row_bytes)
+        view = self.sym.view(self.nranks, self.rank_stride)[:, :row_bytes]
+        view.copy_(host.to(self.device, non_blocking=False))
+
+    def write_inputs_device(self, rows: torch.Tensor) -> None:
+        """Same as write_inputs for a [P, n_bytes] uint8 tensor already on the device."""
+        view = self.sym.view(self.nranks, self.rank_stride)[:, :rows.shape[1]]
+        view.copy_(rows)
+
+    def read_out(self, nelems_total: int, np_dtype) -> np.ndarray:
+        nbytes = nelems_total * np.dtype(np_dtype).itemsize
+        return self.out[:nbytes].cpu().numpy().view(np_dtype).copy()
+
+    # -- collectives (one launch each, on the given stream)
+    def allreduce(self, count: int, algo: str = "auto", stream=None, epoch: int | None = None) -> int:
+        e = self.next_epoch() if epoch is None else epoch
+        return ll.ll_allreduce_algo(self.base, self.rank_stride, self.out_ptr, count, self.dt, ll.LL_SUM,
+                                    self.nranks, e, self.stream_handle(stream), ll.ALGOS[algo])
+
+    def reduce_scatter(self, recvcount: int, proto: str = "auto", stream=None, epoch: int | None = None) -> int:
+        e = self.next_epoch() if epoch is None else epoch
+        return ll.ll_reduce_scatter_proto(self.base, self.rank_stride, self.out_ptr, recvcount, self.dt, ll.LL_SUM,
+                                          self.nranks, e, self.stream_handle(stream), ll.PROTOS[proto])
+
+    def allgather(self, sendcount: int, proto: str = "auto", stream=None, epoch: int | None = None) -> int:
+        e = self.next_epoch() if epoch is None else epoch
+        return ll.ll_allgather_proto(self.base, self.rank_stride, self.out_ptr, sendcount, self.dt, self.nranks, e,
+                                     self.stream_handle(stream), ll.PROTOS[proto])

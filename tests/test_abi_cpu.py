@@ -1,0 +1,173 @@
+"""The C-ABI library on the CPU: it loads, exports what the headers declare, and
+rejects bad arguments before touching the HIP runtime (no GPU needed)."""
+from __future__ import annotations
+
+import os
+import re
+
+import pytest
+
+from paper_2607_16100_amd import llcoll as ll
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("llcoll.h", "llprobe.h")]
+
+F32, BF16 = ll.LL_F32, ll.LL_BF16
+GOOD_BASE = 1 << 40          # fake, 256-aligned device addresses: never dereferenced
+GOOD_OUT = 1 << 41
+
+
+def declared_functions():
+    names = []
+    for h in HEADERS:
+        text = open(h).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names += re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(ll_[a-z_0-9]+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+def test_headers_declare_the_boundary():
+    names = declared_functions()
+    for must in ("ll_slice_bytes", "ll_init", "ll_allreduce", "ll_allreduce_algo", "ll_reduce_scatter",
+                 "ll_allgather", "ll_check", "ll_strerror", "ll_probe_empty", "ll_probe_floor"):
+        assert must in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ll.library()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    assert set(declared_functions()) == set(ll.exported_symbols())
+
+
+def stride_for(count, dt, p):
+    st, s = ll.ll_slice_bytes(count, dt, p)
+    assert st == ll.LL_OK
+    return s
+
+
+def ar(count=1024, dt=F32, p=4, base=GOOD_BASE, stride=None, out=GOOD_OUT, epoch=1, op=ll.LL_SUM,
+       algo=ll.LL_ALGO_ONESHOT):
+    if stride is None:
+        stride = stride_for(max(count, 1), dt if dt in (F32, BF16) else F32, p if 2 <= p <= 8 else 2)
+    return ll.ll_allreduce_algo(base, stride, out, count, dt, op, p, epoch, 0, algo)
+
+
+@pytest.mark.parametrize("kwargs,want", [
+    (dict(base=0), ll.LL_ERR_INVALID),
+    (dict(out=0), ll.LL_ERR_INVALID),
+    (dict(p=1), ll.LL_ERR_INVALID),
+    (dict(p=9), ll.LL_ERR_INVALID),
+    (dict(base=GOOD_BASE + 128), ll.LL_ERR_INVALID),
+    (dict(out=GOOD_OUT + 8), ll.LL_ERR_INVALID),
+    (dict(stride=1000), ll.LL_ERR_INVALID),
+    (dict(epoch=0), ll.LL_ERR_INVALID),
+    (dict(dt=7), ll.LL_ERR_UNSUPPORTED),
+    (dict(op=1), ll.LL_ERR_UNSUPPORTED),
+    (dict(algo=9), ll.LL_ERR_INVALID),
+    (dict(stride=256), ll.LL_ERR_SCRATCH),
+    (dict(count=1 << 29, stride=1 << 20), ll.LL_ERR_UNSUPPORTED),
+    (dict(out=GOOD_BASE + 512), ll.LL_ERR_INVALID),   # out overlaps the region
+    (dict(count=0), ll.LL_OK),                        # nothing to do, no launch
+])
+def test_allreduce_argument_checks(kwargs, want):
+    assert ar(**kwargs) == want
+
+
+def test_scratch_error_when_input_exceeds_capacity():
+    stride = stride_for(1000, F32, 8)
+    cap = ll.ll_input_capacity(stride, 8)[1]
+    assert ar(count=cap // 4 + 1, p=8, stride=stride) == ll.LL_ERR_SCRATCH
+    assert ar(count=100000, p=8, stride=stride) == ll.LL_ERR_SCRATCH
+
+
+def test_rs_ag_argument_checks():
+    stride = stride_for(8 * 64, BF16, 8)
+    rs = ll.ll_reduce_scatter_proto
+    ag = ll.ll_allgather_proto
+    assert rs(GOOD_BASE, stride, GOOD_OUT, 64, BF16, ll.LL_SUM, 8, 0, 0, 0) == ll.LL_ERR_INVALID
+    assert rs(GOOD_BASE, stride, GOOD_OUT, 64, BF16, 3, 8, 1, 0, 0) == ll.LL_ERR_UNSUPPORTED
+    assert rs(GOOD_BASE, stride, GOOD_OUT, 64, BF16, ll.LL_SUM, 8, 1, 0, 5) == ll.LL_ERR_INVALID
+    assert rs(GOOD_BASE, stride, GOOD_OUT, 65, BF16, ll.LL_SUM, 8, 1, 0, 0) == ll.LL_ERR_SCRATCH
+    assert rs(GOOD_BASE, stride, GOOD_OUT, 0, BF16, ll.LL_SUM, 8, 1, 0, 0) == ll.LL_OK
+    assert ag(GOOD_BASE, stride, GOOD_OUT, 8 * 64 + 1, BF16, 8, 1, 0, 0) == ll.LL_ERR_SCRATCH
+    assert ag(GOOD_BASE, stride, 0, 64, BF16, 8, 1, 0, 0) == ll.LL_ERR_INVALID
+    assert ag(GOOD_BASE, stride, GOOD_OUT, 0, BF16, 8, 1, 0, 0) == ll.LL_OK
+
+
+def test_init_argument_checks():
+    assert ll.ll_init(0, 4096, 4, 0) == ll.LL_ERR_INVALID
+    assert ll.ll_init(GOOD_BASE, 4096, 1, 0) == ll.LL_ERR_INVALID
+    assert ll.ll_init(GOOD_BASE + 8, 4096, 4, 0) == ll.LL_ERR_INVALID
+    assert ll.ll_init(GOOD_BASE, 256, 8, 0) == ll.LL_ERR_SCRATCH  # packet areas do not fit
+
+
+@pytest.mark.parametrize("dt,es", [(F32, 4), (BF16, 2)])
+@pytest.mark.parametrize("p", [2, 3, 4, 8])
+def test_slice_bytes_gives_enough_capacity(dt, es, p):
+    prev = 0
+    for count in [1, 2, 3, 7, 64, 1000, 4096, 8192, 7168 * 16, 1 << 20, (64 << 20) // es]:
+        st, stride = ll.ll_slice_bytes(count, dt, p)
+        assert st == ll.LL_OK and stride % 256 == 0
+        assert stride >= prev  # monotone in the input size
+        prev = stride
+        st, cap = ll.ll_input_capacity(stride, p)
+        assert st == ll.LL_OK
+        assert cap >= count * es and cap % 256 == 0
+        # the region is not much larger than the input plus the slots it needs
+        assert stride <= 24 * max(cap, 256) + 4 * 1024 * p
+
+
+def test_slice_bytes_argument_checks():
+    assert ll.ll_slice_bytes(10, F32, 1)[0] == ll.LL_ERR_INVALID
+    assert ll.ll_slice_bytes(10, 5, 4)[0] == ll.LL_ERR_UNSUPPORTED
+    assert ll.ll_slice_bytes((256 << 20) // 4 + 1, F32, 4)[0] == ll.LL_ERR_UNSUPPORTED
+    assert ll.ll_input_capacity(1000, 4)[0] == ll.LL_ERR_INVALID
+
+
+def test_capacity_is_a_function_of_stride_and_ranks_only():
+    # the layout (and with it every flag position) depends on nothing else
+    for p in (2, 8):
+        s = ll.ll_slice_bytes(5000, F32, p)[1]
+        assert ll.ll_input_capacity(s, p) == ll.ll_input_capacity(s, p)
+        assert ll.ll_input_capacity(s + 256, p)[1] >= ll.ll_input_capacity(s, p)[1]
+
+
+def test_setters():
+    assert ll.ll_set_launch(0, 0) == ll.LL_OK
+    assert ll.ll_set_launch(1, 100) == ll.LL_ERR_INVALID
+    assert ll.ll_set_launch(-1, 64) == ll.LL_ERR_INVALID
+    assert ll.ll_set_poll_timeout(0) == ll.LL_ERR_INVALID
+    assert ll.ll_set_poll_timeout(200_000_000) == ll.LL_OK
+    assert ll.ll_debug_mute_rank(9) == ll.LL_ERR_INVALID
+    assert ll.ll_debug_mute_rank(-1) == ll.LL_OK
+
+
+def test_strerror_covers_every_code():
+    for code in (0, -1, -2, -3, -4, -5):
+        assert ll.ll_strerror(code) and ll.ll_strerror(code) != "unknown status"
+    assert ll.ll_strerror(42) == "unknown status"
+
+
+def test_probe_argument_checks():
+    assert ll.ll_probe_empty(0, 64, 0, 0) == ll.LL_ERR_INVALID
+    assert ll.ll_probe_empty(8, 100, 0, 0) == ll.LL_ERR_INVALID
+    assert ll.ll_probe_floor(0, 10, 0, GOOD_OUT, 8, 64, 0, 0) == ll.LL_ERR_INVALID
+    assert ll.ll_probe_floor(GOOD_BASE, 10, 10, GOOD_OUT, 8, 64, 0, 0) == ll.LL_ERR_INVALID
+    assert ll.ll_probe_litmus(GOOD_BASE, 1024, 16, 64, 1, 1, 0, GOOD_OUT, 0) == ll.LL_ERR_INVALID  # buffer too small
+    assert ll.ll_probe_pingpong(GOOD_BASE, 10, 8, 8, 100, GOOD_OUT, 0) == ll.LL_ERR_INVALID
+
+
+def test_product_fails_loudly_without_the_library(tmp_path, monkeypatch):
+    """No silent fallback: importing the binding with the library missing raises."""
+    import importlib.util
+    import shutil
+
+    src = os.path.join(ROOT, "paper_2607_16100_amd", "llcoll.py")
+    pkg = tmp_path / "fakepkg"
+    pkg.mkdir()
+    shutil.copy(src, pkg / "llcoll.py")
+    spec = importlib.util.spec_from_file_location("fakepkg.llcoll", pkg / "llcoll.py")
+    mod = importlib.util.module_from_spec(spec)
+    with pytest.raises(ImportError):
+        spec.loader.exec_module(mod)

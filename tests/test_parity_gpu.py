@@ -1,0 +1,321 @@
+"""GPU parity: the HIP collectives against the CPU oracle, bit for bit.
+
+Every test calls the library through its C ABI (``llcoll``) on cuda:0 and
+compares raw element bits with ``oracle`` (0 ulp for binary32 and bfloat16:
+binary32 accumulation in ascending rank order, one rounding).
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+import oracle  # noqa: E402
+from paper_2607_16100_amd import workloads as wl  # noqa: E402
+
+if torch.cuda.is_available():
+    from paper_2607_16100_amd import llcoll as ll  # noqa: E402
+    from paper_2607_16100_amd.region import SymRegion  # noqa: E402
+else:  # pragma: no cover
+    pytest.skip("no GPU", allow_module_level=True)
+
+AR_ALGOS = ["oneshot", "twoshot", "twoshot_line", "oneshot_line"]
+PROTOS = ["packet8", "line128"]
+NP = {"f32": np.uint32, "bf16": np.uint16}
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def check_ok(st, what):
+    assert st == ll.LL_OK, f"{what}: {ll.ll_strerror(st)}"
+    st2 = ll.ll_check(stream())
+    assert st2 == ll.LL_OK, f"{what}: ll_check says {ll.ll_strerror(st2)}"
+
+
+def run_allreduce(reg: SymRegion, x: np.ndarray, algo: str) -> np.ndarray:
+    p, n = x.shape
+    reg.write_inputs(x)
+    check_ok(reg.allreduce(n, algo), f"allreduce {algo} P={p} n={n}")
+    return reg.read_out(p * n, x.dtype).reshape(p, n)
+
+
+def assert_bits_equal(got, want, what):
+    if not np.array_equal(got, want):
+        bad = np.argwhere(got != want)
+        r, i = bad[0]
+        raise AssertionError(f"{what}: {len(bad)} elements differ; first at rank {r} index {i}: "
+                             f"got {int(got[r, i]):#x} want {int(want[r, i]):#x}")
+
+
+TEST_TIMEOUT_TICKS = 20_000_000  # 200 ms per flag wait: thousands of times a correct call's duration
+
+
+@pytest.fixture(autouse=True)
+def _reset_settings():
+    ll.ll_set_launch(0, 0)
+    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
+    ll.ll_debug_mute_rank(-1)
+    yield
+    ll.ll_set_launch(0, 0)
+    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
+    ll.ll_debug_mute_rank(-1)
+
+
+# ------------------------------------------------------------ configuration C1
+def test_c1_oneshot_p4_f32_1024():
+    """One-shot, 4 ranks, binary32, 1024 uniform(-1,1) elements per rank (seed r), epoch 1."""
+    x = wl.uniform(4, 1024, "f32", seed=0)
+    reg = SymRegion(4, 1024, "f32")
+    reg.init()
+    reg.write_inputs(x)
+    check_ok(reg.allreduce(1024, "oneshot", epoch=1), "C1")
+    got = reg.read_out(4 * 1024, np.uint32).reshape(4, 1024)
+    assert_bits_equal(got, oracle.allreduce(x), "C1")
+
+
+# ------------------------------------------------ every algorithm, ragged sizes
+SMALL_N = [1, 2, 3, 5, 17, 63, 64, 65, 129, 1000, 4099, 30 * 8 * 3 + 7]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("p", [2, 3, 4, 5, 8])
+def test_allreduce_all_algorithms_ragged(dtype, p):
+    """All four algorithms on one region, sizes across several units with ragged
+    tails, alternating calls (the slice layout keeps every flag position fixed)."""
+    reg = SymRegion(p, max(SMALL_N), dtype)
+    reg.init()
+    for n in SMALL_N:
+        x = wl.uniform(p, n, dtype, seed=100 + n)
+        want = oracle.allreduce(x)
+        for algo in AR_ALGOS:
+            say(f"allreduce {algo} P={p} {dtype} n={n}")
+            assert_bits_equal(run_allreduce(reg, x, algo), want, f"{algo} P={p} {dtype} n={n}")
+
+
+@pytest.mark.parametrize("algo", AR_ALGOS)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_allreduce_special_values(algo, dtype):
+    """Order pins, signed zeros and subnormals go through the kernels unchanged."""
+    p = 8
+    cols = [
+        [2.0 ** 24, 1.0, -(2.0 ** 24), 0, 0, 0, 0, 0],
+        [-(2.0 ** 24), 0, 2.0 ** 24, 1.0, 0, 0, 0, 0],
+        [256.0, 1.0, 1.0, 0, 0, 0, 0, 0],
+        [256.0, 1.0, 0, 0, 0, 0, 0, 0],
+        [-0.0] * 8,
+        [2.0 ** -130, 2.0 ** -130, 0, 0, 0, 0, 0, 0],
+    ]
+    vals = np.array(cols * 50, dtype=np.float32).T.copy()  # [8, 300]
+    bits = vals.view(np.uint32)
+    if dtype == "bf16":
+        bits = (bits >> 16).astype(np.uint16)
+    reg = SymRegion(p, bits.shape[1], dtype)
+    reg.init()
+    assert_bits_equal(run_allreduce(reg, bits, algo), oracle.allreduce(bits), f"special {algo} {dtype}")
+
+
+# ------------------------------------------------------------ configuration C2
+def test_c2_oneshot_bf16_16k_10k_calls():
+    """8 ranks, bfloat16, 8192 normal(0,1) elements per rank, one-shot with
+    8-byte packets, 10,000 back-to-back calls with the epoch incremented."""
+    p, n = 8, 8192
+    x = wl.normal(p, n, "bf16", sigma=1.0, seed=0)
+    want = oracle.allreduce(x)
+    reg = SymRegion(p, n, "bf16")
+    reg.init()
+    reg.write_inputs(x)
+    s = stream()
+    for i in range(10_000):
+        st = reg.allreduce(n, "oneshot")
+        assert st == ll.LL_OK
+        if i % 1000 == 999:
+            assert ll.ll_check(s) == ll.LL_OK, f"C2: status after call {i}"
+    assert ll.ll_check(s) == ll.LL_OK
+    got = reg.read_out(p * n, np.uint16).reshape(p, n)
+    assert_bits_equal(got, want, "C2 after 10k calls")
+    assert reg.epoch == 10_000
+
+
+@pytest.mark.parametrize("algo", AR_ALGOS)
+def test_changing_inputs_never_return_stale_packets(algo):
+    """New inputs every call (seed r + 1000 k): a packet left from an earlier
+    epoch would show up as a wrong value."""
+    p, n = 8, 8192
+    reg = SymRegion(p, n, "bf16")
+    reg.init()
+    for k in range(60):
+        x = wl.normal(p, n, "bf16", seed=1000 * k)
+        assert_bits_equal(run_allreduce(reg, x, algo), oracle.allreduce(x), f"{algo} change {k}")
+
+
+# ------------------------------------------------------------ configuration C3
+def test_c3_twoshot_bf16_1mib_vs_oneshot():
+    """8 ranks, bfloat16, 64 x 8192 normal(0, 0.5) per rank: two-shot (both
+    packet formats) equals the oracle and equals one-shot."""
+    p, n = 8, 64 * 8192
+    x = wl.normal(p, n, "bf16", sigma=0.5, seed=0)
+    want = oracle.allreduce(x)
+    reg = SymRegion(p, n, "bf16")
+    reg.init()
+    outs = {}
+    for algo in AR_ALGOS:
+        say(f"C3 {algo}")
+        outs[algo] = run_allreduce(reg, x, algo)
+        assert_bits_equal(outs[algo], want, f"C3 {algo}")
+    assert np.array_equal(outs["twoshot"], outs["oneshot"])
+
+
+# ------------------------------------------------------------ configuration C4
+C4_SIZES = [2 ** k for k in range(1, 27)]
+
+
+def test_c4_size_sweep_parity():
+    """8 ranks, binary32 uniform(-1,1): every power-of-two size from 2 to 2^26
+    elements per rank, one-shot and two-shot with both packet formats."""
+    p = 8
+    big = C4_SIZES[-1]
+    reg = SymRegion(p, big, "f32", out_elems=p * big)
+    reg.init()
+    for n in C4_SIZES:
+        x = wl.uniform(p, n, "f32", seed=0)
+        want = oracle.allreduce(x)
+        for algo in AR_ALGOS:
+            say(f"C4 {algo} n={n}")
+            assert_bits_equal(run_allreduce(reg, x, algo), want, f"C4 {algo} n={n}")
+
+
+# ------------------------------------------------------------ configuration C5
+@pytest.mark.parametrize("p", [8, 4])
+@pytest.mark.parametrize("b", [1, 16, 256])
+@pytest.mark.parametrize("kind", ["normal", "adversarial"])
+def test_c5_reduce_scatter_and_allgather(p, b, kind):
+    """hidden 7168 x batch b, bfloat16: ReduceScatter of b*7168 per rank and
+    AllGather of b*7168/P per rank, both packet formats; AG(RS(x)) == AR(x)."""
+    total = 7168 * b
+    m = total // p
+    x = wl.make(kind, p, total, "bf16", seed=0)
+    want_rs = oracle.reduce_scatter(x)
+    reg = SymRegion(p, total, "bf16", out_elems=p * total)
+    reg.init()
+    for proto in PROTOS:
+        say(f"C5 RS {kind} P={p} b={b} {proto}")
+        reg.write_inputs(x)
+        check_ok(reg.reduce_scatter(m, proto), "reduce_scatter")
+        got_rs = reg.read_out(p * m, np.uint16).reshape(p, m)
+        assert_bits_equal(got_rs, want_rs, f"RS {proto}")
+        say(f"C5 AG {kind} P={p} b={b} {proto}")
+        reg.write_inputs(got_rs)
+        check_ok(reg.allgather(m, proto), "allgather")
+        got_ag = reg.read_out(p * p * m, np.uint16).reshape(p, p * m)
+        assert_bits_equal(got_ag, oracle.allgather(got_rs), f"AG {proto}")
+        assert_bits_equal(got_ag, oracle.allreduce(x), f"AG(RS) == AR {proto}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("proto", PROTOS)
+@pytest.mark.parametrize("p,m", [(2, 1), (3, 7), (4, 33), (8, 5), (8, 61), (5, 250)])
+def test_rs_ag_ragged(dtype, proto, p, m):
+    """Chunks whose byte offsets are not 4-byte aligned (odd bfloat16 counts)."""
+    x = wl.uniform(p, p * m, dtype, seed=7)
+    reg = SymRegion(p, p * m, dtype, out_elems=p * p * m)
+    reg.init()
+    reg.write_inputs(x)
+    check_ok(reg.reduce_scatter(m, proto), "rs")
+    rs = reg.read_out(p * m, NP[dtype]).reshape(p, m)
+    assert_bits_equal(rs, oracle.reduce_scatter(x), f"RS ragged {proto}")
+    reg.write_inputs(x[:, :m].copy())
+    check_ok(reg.allgather(m, proto), "ag")
+    ag = reg.read_out(p * p * m, NP[dtype]).reshape(p, p * m)
+    assert_bits_equal(ag, oracle.allgather(x[:, :m].copy()), f"AG ragged {proto}")
+
+
+# ------------------------------------------------------------ invariants
+@pytest.mark.parametrize("algo", AR_ALGOS)
+def test_result_independent_of_launch_shape(algo):
+    p, n = 8, 50_000
+    x = wl.uniform(p, n, "bf16", seed=3)
+    want = oracle.allreduce(x)
+    reg = SymRegion(p, n, "bf16")
+    reg.init()
+    for wg, threads in [(1, 64), (1, 1024), (3, 256), (16, 128), (0, 0)]:
+        ll.ll_set_launch(wg, threads)
+        say(f"launch {algo} wg={wg} threads={threads}")
+        assert_bits_equal(run_allreduce(reg, x, algo), want, f"{algo} wg={wg} t={threads}")
+
+
+def test_large_epochs_and_reinit():
+    """Epochs near the top of the 32-bit range, one per call, then ll_init and a
+    restart at epoch 1."""
+    p, n = 4, 3000
+    x = wl.uniform(p, n, "f32", seed=9)
+    want = oracle.allreduce(x)
+    reg = SymRegion(p, n, "f32")
+    reg.init()
+    reg.write_inputs(x)
+    for algo, e in zip(AR_ALGOS, (0x7FFFFFFF, 0x80000000, 0xFFFFFFFE, 0xFFFFFFFF)):
+        check_ok(reg.allreduce(n, algo, epoch=e), f"epoch {e:#x}")
+        assert_bits_equal(reg.read_out(p * n, np.uint32).reshape(p, n), want, f"{algo} epoch {e:#x}")
+    reg.init()
+    check_ok(reg.allreduce(n, "twoshot", epoch=1), "after init")
+    assert_bits_equal(reg.read_out(p * n, np.uint32).reshape(p, n), want, "after re-init")
+
+
+def test_count_zero_is_a_no_op():
+    reg = SymRegion(4, 16, "f32")
+    reg.init()
+    assert reg.allreduce(0, "oneshot") == ll.LL_OK
+    assert reg.reduce_scatter(0, "packet8") == ll.LL_OK
+    assert reg.allgather(0, "line128") == ll.LL_OK
+    assert ll.ll_check(stream()) == ll.LL_OK
+
+
+# ------------------------------------------------------------ failure handling
+@pytest.mark.parametrize("algo", ["oneshot", "twoshot_line"])
+def test_missing_peer_times_out_and_is_reported(algo):
+    """Rank 3 publishes nothing; its peers' bounded waits expire (after 2 ms),
+    every kernel still finishes, and ll_check reports the timeout."""
+    p, n = 8, 4096
+    x = wl.uniform(p, n, "f32", seed=1)
+    reg = SymRegion(p, n, "f32")
+    reg.init()
+    reg.write_inputs(x)
+    ll.ll_set_poll_timeout(200_000)  # 2 ms
+    ll.ll_debug_mute_rank(3)
+    st = reg.allreduce(n, algo)
+    assert st == ll.LL_OK
+    assert ll.ll_check(stream()) == ll.LL_ERR_TIMEOUT
+    rank, missing, epoch = ll.ll_last_timeout()
+    assert rank != 3 and missing == (1 << 3) and epoch == reg.epoch
+    ll.ll_debug_mute_rank(-1)
+    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
+    reg.init()
+    check_ok(reg.allreduce(n, algo), "after timeout")
+    assert_bits_equal(reg.read_out(p * n, np.uint32).reshape(p, n), oracle.allreduce(x), "after timeout")
+
+
+def test_next_epoch_sees_new_inputs():
+    """Back-to-back calls with consecutive epochs and different inputs: each
+    call returns the sum of its own inputs."""
+    p, n = 4, 512
+    a = wl.uniform(p, n, "f32", seed=1)
+    b = wl.uniform(p, n, "f32", seed=2)
+    reg = SymRegion(p, n, "f32")
+    reg.init()
+    reg.write_inputs(a)
+    check_ok(reg.allreduce(n, "oneshot", epoch=5), "a")
+    assert_bits_equal(reg.read_out(p * n, np.uint32).reshape(p, n), oracle.allreduce(a), "epoch 5")
+    reg.write_inputs(b)
+    check_ok(reg.allreduce(n, "oneshot", epoch=6), "b")
+    assert_bits_equal(reg.read_out(p * n, np.uint32).reshape(p, n), oracle.allreduce(b), "epoch 6")

@@ -1,0 +1,72 @@
+"""GPU checks of the chip facts the packet formats rely on, and of the
+measurement probes (all bounded; nothing here can wait forever)."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():  # pragma: no cover
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2607_16100_amd import llcoll as ll  # noqa: E402
+
+
+def stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def test_workgroups_are_dealt_round_robin_over_xcds():
+    """Workgroup b runs on XCD b mod 8, so rank r = b mod P of an 8-rank launch
+    owns one XCD and every rank-to-rank packet crosses the fabric."""
+    grid = 256
+    ids = torch.full((grid,), 99, dtype=torch.int32, device="cuda")
+    assert ll.ll_probe_xcd(ids.data_ptr(), grid, 64, stream()) == ll.LL_OK
+    torch.cuda.synchronize()
+    x = ids.cpu().numpy()
+    nx = int(x.max()) + 1
+    print("XCDs seen:", nx, "first 16:", x[:16].tolist(), flush=True)
+    assert nx == 8
+    assert np.array_equal(x, np.arange(grid) % 8)
+
+
+@pytest.mark.parametrize("layout,name", [(0, "8-byte packets"), (1, "128-byte lines, flag per 64-byte half")])
+def test_no_torn_packets_across_xcds(layout, name):
+    """Writers on one XCD rewrite packets while readers on another XCD read
+    them: every unit whose flag is set must carry that round's payload."""
+    grid, lines, iters, reads = 16, 256, 3000, 3000
+    buf = torch.zeros(grid // 2 * lines * 32, dtype=torch.int32, device="cuda")
+    counts = torch.zeros(4, dtype=torch.int64, device="cuda")
+    st = ll.ll_probe_litmus(buf.data_ptr(), buf.numel() * 4, grid, lines, iters, reads, layout,
+                            counts.data_ptr(), stream())
+    assert st == ll.LL_OK
+    torch.cuda.synchronize()
+    seen, torn, split16, splitline = counts.cpu().numpy().tolist()
+    print(f"litmus {name}: seen={seen} torn={torn} split16={split16} splitline={splitline}", flush=True)
+    assert seen > 100_000
+    assert torn == 0
+
+
+def test_floor_and_empty_kernels_run():
+    words = 1 << 20
+    chase = torch.zeros(words, dtype=torch.int64, device="cuda")
+    sink = torch.zeros(4, dtype=torch.int64, device="cuda")
+    stamps = torch.zeros(2 * 64, dtype=torch.int64, device="cuda")
+    assert ll.ll_probe_empty(64, 256, stamps.data_ptr(), stream()) == ll.LL_OK
+    assert ll.ll_probe_floor(chase.data_ptr(), words, 4096, sink.data_ptr(), 64, 256, stamps.data_ptr(),
+                             stream()) == ll.LL_OK
+    torch.cuda.synchronize()
+    s = stamps.cpu().numpy()
+    assert np.all(s[64:] >= s[:64]) and np.all(s > 0)
+
+
+def test_pingpong_completes():
+    flags = torch.zeros(2048, dtype=torch.int32, device="cuda")
+    out = torch.zeros(3, dtype=torch.int64, device="cuda")
+    assert ll.ll_probe_pingpong(flags.data_ptr(), 500, 8, 1, 10_000_000, out.data_ptr(), stream()) == ll.LL_OK
+    torch.cuda.synchronize()
+    ticks, done, cycles = out.cpu().numpy().tolist()
+    print(f"pingpong: {done} rounds, {ticks * 10 / max(done, 1):.0f} ns per round", flush=True)
+    assert done == 500
