@@ -2,12 +2,15 @@
 
 Headline (one JSON line on stdout):
   * p50 microseconds per AllReduce at 16 KiB per rank: 8 virtual ranks,
-    bfloat16, batch 1 x hidden 8192, normal(0,1) inputs, one-shot with
-    8-byte packets, `--steps` back-to-back calls with the epoch incremented
-    (a "step" is one such call).  Per-call latency is the interval between
-    consecutive calls' completion times, taken inside the kernels from the
-    100 MHz constant clock; it includes launch and dispatch, exactly as the
-    floor below does.
+    bfloat16, batch 1 x hidden 8192, normal(0,1) inputs, the library's
+    default algorithm for that size (one-shot, 8-byte packets), `--steps`
+    back-to-back calls with the epoch incremented (a "step" is one such call).
+    Per-call latency is the interval between consecutive calls' completion
+    times, taken inside the kernels from the 100 MHz constant clock; it
+    includes launch and dispatch.  The launches are queued from C behind a
+    short spin kernel, so the GPU, not Python, sets the pace; the same is done
+    for the floor below.  (The mean with one Python launch per call is
+    reported too, as python_launched_mean_us.)
   * the single-GPU floor measured the same way: back-to-back launches of a
     kernel with the same grid whose only work is one dependent HBM round
     trip (ratio = p50 / floor p50).
@@ -57,30 +60,36 @@ def pct(a, q):
 
 
 # ----------------------------------------------------------------------------
-def stamped_loop(torch, ll, launch, steps: int, warmup: int, grid_hint: int):
-    """Run `launch(i)` warmup+steps times back to back; the timed calls write
-    per-workgroup start/end stamps.  Returns (intervals_us, spans_us, wall_s)."""
-    for i in range(warmup):
-        launch(i)
-    torch.cuda.synchronize()
-    grid, _ = ll.ll_last_grid()
-    grid = max(grid, grid_hint)
-    stamps = torch.zeros(steps * 2 * grid, dtype=torch.int64, device="cuda")
-    base = stamps.data_ptr()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(steps):
-        ll.ll_debug_stamp_next(base + i * 2 * grid * 8)
-        launch(warmup + i)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    s = stamps.view(steps, 2, grid).cpu().numpy().astype(np.int64)
-    g_used, _ = ll.ll_last_grid()
-    starts = s[:, 0, :g_used].min(axis=1)
-    ends = s[:, 1, :g_used].max(axis=1)
+HOLD_TICKS = 3_000_000  # 30 ms: long enough for the host to queue a batch of launches
+
+
+def stamp_stats(stamps, steps, grid):
+    a = stamps.view(steps, 2, grid).cpu().numpy().astype(np.int64)
+    starts = a[:, 0, :].min(axis=1)
+    ends = a[:, 1, :].max(axis=1)
     intervals = np.diff(ends) * TICK_US
     spans = (ends - starts) * TICK_US
-    return intervals, spans, wall
+    return intervals, spans
+
+
+def gpu_paced(torch, ll, launch_batch, steps, grid, batch=2000):
+    """Per-call completion intervals of `steps` back-to-back launches, queued
+    behind a short spin kernel so that the GPU, not the host, sets the pace.
+    `launch_batch(first, count, stamps_ptr, stride)` queues `count` launches."""
+    s = torch.cuda.current_stream().cuda_stream
+    iv_all, sp_all = [], []
+    done = 0
+    while done < steps:
+        cnt = min(batch, steps - done)
+        stamps = torch.zeros(cnt * 2 * grid, dtype=torch.int64, device="cuda")
+        ll.check(ll.ll_probe_spin(HOLD_TICKS, s), "spin")
+        launch_batch(done, cnt, stamps.data_ptr(), 2 * grid)
+        torch.cuda.synchronize()
+        iv, sp = stamp_stats(stamps, cnt, grid)
+        iv_all.append(iv)
+        sp_all.append(sp)
+        done += cnt
+    return np.concatenate(iv_all), np.concatenate(sp_all)
 
 
 def bench_headline(torch, ll, steps, warmup):
@@ -93,85 +102,77 @@ def bench_headline(torch, ll, steps, warmup):
     reg.init()
     reg.write_inputs(x)
     s = reg.stream_handle()
+    algo = ll.LL_ALGO_AUTO
+    epoch = [1]
 
-    def launch(i):
-        st = reg.allreduce(n, "oneshot")
-        if st != ll.LL_OK:
-            raise RuntimeError(ll.ll_strerror(st))
+    def queue(first, count, stamps_ptr, stride):
+        ll.check(ll.ll_bench_allreduce(reg.base, reg.rank_stride, reg.out_ptr, n, ll.LL_BF16, p, epoch[0], count,
+                                       algo, stamps_ptr, stride, s), "bench_allreduce")
+        epoch[0] += count
 
-    intervals, spans, wall = stamped_loop(torch, ll, launch, steps, warmup, 1)
-    ll.check(ll.ll_check(s), "headline")
-    grid, threads = ll.ll_last_grid()
-    # event-timed mean without stamps, same loop
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    queue(0, warmup, 0, 0)
     torch.cuda.synchronize()
+    grid, threads = ll.ll_last_grid()
+    t0 = time.perf_counter()
+    intervals, spans = gpu_paced(torch, ll, queue, steps, grid)
+    wall = time.perf_counter() - t0
+    ll.check(ll.ll_check(s), "headline")
+    # the same calls launched one at a time from Python (host-paced), for context
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    host_steps = min(steps, 2000)
     ev0.record()
-    for i in range(steps):
-        launch(i)
+    for _ in range(host_steps):
+        ll.check(ll.ll_allreduce(reg.base, reg.rank_stride, reg.out_ptr, n, ll.LL_BF16, ll.LL_SUM, p, epoch[0], s))
+        epoch[0] += 1
     ev1.record()
     torch.cuda.synchronize()
-    ev_mean_us = ev0.elapsed_time(ev1) * 1000.0 / steps
+    host_mean = ev0.elapsed_time(ev1) * 1000.0 / host_steps
     ll.check(ll.ll_check(s), "headline")
-    # parity of the last call
-    import oracle  # the benchmark's check: same oracle as the tests
+    import oracle  # the benchmark's own check of the last result
 
     got = reg.read_out(p * n, np.uint16).reshape(p, n)
     exact = bool(np.array_equal(got, oracle.allreduce(x)))
     return {
         "p50_us": pct(intervals, 50), "p99_us": pct(intervals, 99), "mean_us": float(np.mean(intervals)),
-        "span_p50_us": pct(spans, 50), "event_mean_us": ev_mean_us, "wall_s": wall, "grid": grid,
-        "threads": threads, "bit_exact": exact, "epochs": reg.epoch,
+        "span_p50_us": pct(spans, 50), "python_launched_mean_us": host_mean, "wall_s": wall, "grid": grid,
+        "threads": threads, "bit_exact": exact, "epochs": epoch[0] - 1,
     }
 
 
 def bench_floor(torch, ll, steps, warmup, grid, threads):
-    """Back-to-back floor kernels (same grid), each loading a line nobody has
-    touched for a long time (a 1 GiB table > the 256 MiB last-level cache)."""
+    """Back-to-back floor kernels with the collective's grid, each loading a
+    line nobody has touched for a long time (1 GiB table, larger than the
+    256 MiB last-level cache) and storing it; and empty kernels."""
     words = (1 << 30) // 8
     chase = torch.zeros(words, dtype=torch.int64, device="cuda")
     sink = torch.zeros(16, dtype=torch.int64, device="cuda")
     s = torch.cuda.current_stream().cuda_stream
-    line_words = 16  # 128 bytes
-    stride_lines = 4099
+    step_lines = 4099
+    pos = [0]
 
-    def launch_floor(i):
-        start = ((i * stride_lines) % (words // line_words)) * line_words
-        st = ll.ll_probe_floor(chase.data_ptr(), words, start, sink.data_ptr(), grid, threads, 0, s)
-        if st != ll.LL_OK:
-            raise RuntimeError(ll.ll_strerror(st))
+    def q_floor(first, count, stamps_ptr, stride):
+        ll.check(ll.ll_bench_floor(chase.data_ptr(), words, pos[0], step_lines, sink.data_ptr(), grid, threads, count,
+                                   stamps_ptr, stride, s), "bench_floor")
+        pos[0] += count * step_lines
 
-    def launch_empty(i):
-        st = ll.ll_probe_empty(grid, threads, 0, s)
-        if st != ll.LL_OK:
-            raise RuntimeError(ll.ll_strerror(st))
+    def q_empty(first, count, stamps_ptr, stride):
+        ll.check(ll.ll_bench_empty(grid, threads, count, stamps_ptr, stride, s), "bench_empty")
 
     out = {}
-    for name, fn, probe in (("floor", launch_floor, "floor"), ("empty", launch_empty, "empty")):
-        for i in range(warmup):
-            fn(i)
+    for name, fn in (("floor", q_floor), ("empty", q_empty)):
+        fn(0, warmup, 0, 0)
         torch.cuda.synchronize()
-        stamps = torch.zeros(steps * 2 * grid, dtype=torch.int64, device="cuda")
-        base = stamps.data_ptr()
-        for i in range(steps):
-            if probe == "floor":
-                start = (((warmup + i) * stride_lines) % (words // line_words)) * line_words
-                st = ll.ll_probe_floor(chase.data_ptr(), words, start, sink.data_ptr(), grid, threads,
-                                       base + i * 2 * grid * 8, s)
-            else:
-                st = ll.ll_probe_empty(grid, threads, base + i * 2 * grid * 8, s)
-            if st != ll.LL_OK:
-                raise RuntimeError(ll.ll_strerror(st))
-        torch.cuda.synchronize()
-        arr = stamps.view(steps, 2, grid).cpu().numpy()
-        ends = arr[:, 1, :].max(axis=1)
-        starts = arr[:, 0, :].min(axis=1)
-        iv = np.diff(ends) * TICK_US
-        out[name] = {"p50_us": pct(iv, 50), "p99_us": pct(iv, 99), "span_p50_us": pct((ends - starts) * TICK_US, 50)}
-    # dependent-load latency of the same table (pointer chase of cold lines)
+        iv, sp = gpu_paced(torch, ll, fn, steps, grid)
+        out[name] = {"p50_us": pct(iv, 50), "p99_us": pct(iv, 99), "span_p50_us": pct(sp, 50)}
+    # dependent-load latency of cold lines: chase through a table, after evicting caches
+    line_words = 16
     perm = np.random.default_rng(1).permutation(words // line_words // 64)[:4096] * 64 * line_words
     nxt = np.roll(perm, -1)
-    idx = torch.from_numpy(perm.astype(np.int64)).cuda()
-    chase.index_copy_(0, idx, torch.from_numpy(nxt.astype(np.int64)).cuda())
+    chase.index_copy_(0, torch.from_numpy(perm.astype(np.int64)).cuda(), torch.from_numpy(nxt.astype(np.int64)).cuda())
+    junk = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    junk.fill_(1)
+    del junk
     res = torch.zeros(3, dtype=torch.int64, device="cuda")
     ll.check(ll.ll_probe_chase(chase.data_ptr(), words, int(perm[0]), 2000, res.data_ptr(), s), "chase")
     torch.cuda.synchronize()
@@ -253,6 +254,26 @@ def bench_bandwidth(torch, ll, count, algos, iters=20, warmup=3):
     return res
 
 
+def bench_copy(torch, nbytes=1 << 30, iters=10):
+    """A plain device-to-device copy of `nbytes` (torch's copy kernel): the
+    HBM bandwidth a simple streaming kernel reaches on this GPU."""
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(iters):
+        dst.copy_(src)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1000.0 / iters
+    return {"bytes": nbytes, "kernel_us": us, "gbps": 2.0 * nbytes / us / 1e3}
+
+
 def bench_cpu_baseline(seconds: float):
     import oracle
     from paper_2607_16100_amd import workloads as wl
@@ -292,7 +313,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--bw-iters", type=int, default=20)
-    ap.add_argument("--only", default="", help="comma list of sections: headline,floor,sol,bw,cpu")
+    ap.add_argument("--only", default="", help="comma list of sections: headline,floor,sol,bw,copy,cpu")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs its P virtual ranks on one GPU; --gpus {args.gpus} is not supported "
@@ -331,6 +352,10 @@ def main():
         result["bw"] = bench_bandwidth(torch, ll, 16 << 20, ["twoshot_line", "twoshot", "oneshot_line", "oneshot"],
                                        iters=args.bw_iters)
         log(json.dumps(result["bw"]))
+    if want("copy"):
+        log("device copy reference")
+        result["copy"] = bench_copy(torch)
+        log(json.dumps(result["copy"]))
     if want("cpu"):
         log("cpu baseline")
         result["cpu"] = bench_cpu_baseline(args.cpu_seconds)
@@ -353,14 +378,14 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(h["wall_s"] * 1000.0 / args.steps, 5) if h else None,
+        "ms_per_step": round(h["mean_us"] / 1000.0, 6) if h else None,
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": "AllReduce sum, 8 virtual ranks on one GPU, bf16 batch 1 x hidden 8192 "
-                               "(16 KiB per rank), one-shot 8-byte packets, back-to-back calls",
+                               "(16 KiB per rank), one-shot 8-byte packets (one wave per peer), back-to-back calls",
                    "ranks": 8, "elements_per_rank": 8192, "element_type": "bf16", "accumulate": "f32",
                    "parallelism": "8 virtual ranks / 1 GPU"},
         "p99_us": round(h["p99_us"], 3) if h else None,

@@ -77,7 +77,8 @@ typedef enum {
   LL_ALGO_ONESHOT = 1,       /* one-shot, 8-byte packets (Sec. III-A, Sec. IV "LL") */
   LL_ALGO_TWOSHOT = 2,       /* two-shot (ReduceScatter + AllGather), 8-byte packets */
   LL_ALGO_TWOSHOT_LINE = 3,  /* two-shot, 128-byte line packets */
-  LL_ALGO_ONESHOT_LINE = 4   /* one-shot, 128-byte line packets */
+  LL_ALGO_ONESHOT_LINE = 4,  /* one-shot, 128-byte line packets */
+  LL_ALGO_ONESHOT_WAVES = 5  /* one-shot, 8-byte packets, one wave per peer, LDS staging */
 } ll_algo;
 
 /* Packet format for the stand-alone ReduceScatter / AllGather. */
@@ -154,6 +155,15 @@ const char *ll_strerror(int status);
  * not depend on these settings. */
 int ll_set_launch(int workgroups_per_rank, int threads);
 
+/* Poll pacing for the following calls, in units of 64 shader cycles: idle
+ * time before a lane's first poll of its peers (first_wait) and between
+ * polls (poll_gap), each in [0, 1000].  0 = poll back to back. */
+int ll_set_poll_pacing(int first_wait, int poll_gap);
+
+/* Packet units (16 bytes of packets) per lane of LL_ALGO_ONESHOT_WAVES for
+ * the following calls: 1, 2 or 4; 0 = automatic. */
+int ll_set_wave_units(int units_per_lane);
+
 /* Flag-wait budget in ticks of the 100 MHz constant clock (default 2e8,
  * i.e. 2 s).  Must be >= 1. */
 int ll_set_poll_timeout(uint64_t ticks);
@@ -166,6 +176,14 @@ int ll_debug_mute_rank(int rank);
  * writes each workgroup's start and end time (100 MHz ticks) to
  * stamps[b] and stamps[grid + b].  The pointer is used for one launch only. */
 int ll_debug_stamp_next(uint64_t *stamps);
+
+/* Diagnostics hook: when `phases` (device memory, 4*grid words) is non-NULL,
+ * the next one-shot launch records for thread 0 of each workgroup b and its
+ * last packet unit: phases[4b] = time its input load returned, phases[4b+1] =
+ * time its packet stores were acknowledged (the kernel waits for them only in
+ * this mode), phases[4b+2] = time its wait for peers ended, phases[4b+3] =
+ * number of polls it issued.  Used for one launch only. */
+int ll_debug_phase_next(uint64_t *phases);
 
 /* Grid (total workgroups) of the last launch. */
 int ll_last_grid(int *grid, int *threads);

@@ -58,6 +58,28 @@ int ll_probe_fence_l2(uint32_t *buf4k, int iters, uint64_t *out7, void *stream);
 int ll_probe_pingpong(uint32_t *flags8k, int rounds, int grid, int peer, uint64_t limit_ticks, uint64_t *out3,
                       void *stream);
 
+/* A single lane that waits `ticks` (1 .. 1e8, i.e. at most 1 s) and exits.
+ * Launched first, it holds the stream while the host queues the launches to
+ * be timed, which then run back to back at the GPU's own pace. */
+int ll_probe_spin(uint64_t ticks, void *stream);
+
+/* Back-to-back launch loops run from C (so the host is never the bottleneck).
+ *
+ * ll_bench_allreduce: `calls` AllReduces (ll_allreduce_algo with op = sum) with
+ * epochs first_epoch .. first_epoch+calls-1.  If stamps != NULL, call i writes
+ * its per-workgroup start/end times at stamps + i*stamp_stride (see
+ * ll_debug_stamp_next; stamp_stride >= 2*grid).
+ * ll_bench_floor: `calls` floor kernels; call i loads line
+ * (first_line + i*line_step) mod (chase_len/16) of `chase` (16 words a line).
+ * ll_bench_empty: `calls` empty kernels. */
+int ll_bench_allreduce(void *sym_base, size_t rank_stride, void *out, size_t count, int dt, int nranks,
+                       uint32_t first_epoch, int calls, int algo, uint64_t *stamps, int stamp_stride,
+                       void *stream);
+int ll_bench_floor(const uint64_t *chase, uint64_t chase_len, uint64_t first_line, uint64_t line_step,
+                   uint64_t *sink, int grid, int threads, int calls, uint64_t *stamps, int stamp_stride,
+                   void *stream);
+int ll_bench_empty(int grid, int threads, int calls, uint64_t *stamps, int stamp_stride, void *stream);
+
 /* ids[b] = XCD index of workgroup b. */
 int ll_probe_xcd(uint32_t *ids, int grid, int threads, void *stream);
 

@@ -27,7 +27,8 @@ def comm_volume_per_rank(algo: str, p: int, m: float, proto: str) -> float:
 
 
 def _proto(algo: str) -> tuple[str, str]:
-    base = {"oneshot": "oneshot", "oneshot_line": "oneshot", "twoshot": "twoshot", "twoshot_line": "twoshot"}[algo]
+    base = {"oneshot": "oneshot", "oneshot_line": "oneshot", "oneshot_waves": "oneshot", "twoshot": "twoshot",
+            "twoshot_line": "twoshot"}[algo]
     proto = "line128" if algo.endswith("_line") else "packet8"
     return base, proto
 

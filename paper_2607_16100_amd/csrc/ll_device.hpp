@@ -107,10 +107,14 @@ __device__ __forceinline__ u32x4 load_words(const char *base, int64_t w0, int cn
       uint32_t t[3];
       __builtin_memcpy(t, p, 12);
       v.x = t[0]; v.y = t[1]; v.z = t[2];
-    } else {
+    } else if (cnt == 2) {
       u32x2 t;
       __builtin_memcpy(&t, p, 8);
       v.x = t.x; v.y = t.y;
+    } else {
+      uint32_t t;
+      __builtin_memcpy(&t, p, 4);
+      v.x = t;
     }
     return v;
   }
@@ -142,9 +146,12 @@ __device__ __forceinline__ void store_words(char *base, int64_t w0, int cnt, int
     } else if (cnt == 3) {
       uint32_t t[3] = {v.x, v.y, v.z};
       __builtin_memcpy(p, t, 12);
-    } else {
+    } else if (cnt == 2) {
       u32x2 t = {v.x, v.y};
       __builtin_memcpy(p, &t, 8);
+    } else {
+      const uint32_t t = v.x;
+      __builtin_memcpy(p, &t, 4);
     }
     return;
   }

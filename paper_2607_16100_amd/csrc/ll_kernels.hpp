@@ -32,10 +32,12 @@ struct KArgs {
   uint64_t slot;      // bytes per slot
   uint64_t timeout;   // flag-wait budget, 100 MHz ticks
   uint64_t *stamps;   // optional per-workgroup start/end times
+  uint64_t *phases;   // optional per-workgroup phase times (diagnostics)
   uint32_t epoch;     // flag value of this call
   int32_t mute;       // rank that publishes nothing (test hook), or -1
   uint32_t al4;       // every element stream of this call starts 4-byte aligned
-  uint32_t pad_;
+  uint16_t first_wait;  // idle time before the first poll, in units of 64 shader cycles
+  uint16_t poll_gap;    // idle time between polls, in units of 64 shader cycles
 };
 
 __device__ __forceinline__ int slot_of(int src, int dst) { return src - (src > dst ? 1 : 0); }
@@ -68,15 +70,20 @@ __device__ __forceinline__ void stamp_end(const KArgs &a) {
 // flag equals the epoch.  All pending loads of an iteration are issued before
 // any is checked (parallel polling across ranks, Sec. VII Obs. 1); a lane
 // re-loads only the peers it has not yet heard from.
+__device__ __forceinline__ void idle64(int units) {
+  for (int i = 0; i < units; ++i) __builtin_amdgcn_s_sleep(1);
+}
+
 template <class Pr, int P>
-__device__ __forceinline__ void poll_all(char *area_r, uint64_t slot, uint32_t off, int r, uint32_t epoch,
-                                         uint64_t deadline, u32x4 *got) {
+__device__ __forceinline__ int poll_all(char *area_r, uint64_t slot, uint32_t off, int r, uint32_t epoch,
+                                         uint64_t deadline, u32x4 *got, int first_wait = 0, int poll_gap = 0) {
   // One resource covers the P-1 slots; the slot is selected by the scalar offset.
   const rsrc_t rs = make_rsrc(area_r, (uint32_t)((uint64_t)(P - 1) * slot));
   uint32_t pend = ((1u << P) - 1u) & ~(1u << r);
 #pragma unroll
   for (int q = 0; q < P; ++q) got[q] = u32x4{0u, 0u, 0u, 0u};
-  int spins = 0;
+  int spins = 1;
+  idle64(first_wait);
   while (true) {
     compiler_fence();
 #pragma unroll
@@ -91,11 +98,13 @@ __device__ __forceinline__ void poll_all(char *area_r, uint64_t slot, uint32_t o
       if ((pend & (1u << q)) && rdy) pend &= ~(1u << q);
     }
     if (pend == 0) break;
-    if ((++spins & 15) == 0 && now_ticks() > deadline) {
+    idle64(poll_gap);
+    if ((spins++ & 15) == 0 && now_ticks() > deadline) {
       report_timeout(r, pend, epoch);
       break;
     }
   }
+  return spins;
 }
 
 // Store one packet to slot (q <- r) of every peer q, starting with r+1 so
@@ -171,13 +180,136 @@ __global__ __launch_bounds__(1024) void k_oneshot(KArgs a) {
     const int cnt = Pr::count(sub);
     const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
     const u32x4 own = load_words<DT>(slice_r, w0, cnt, n, true);
+    uint64_t t_loaded = 0, t_acked = 0;
+    if (a.phases != nullptr) t_loaded = now_ticks() + (own.x & 0u);
     if (publish) bcast<P>(a, a.area, r, off, Pr::pack(own, a.epoch, sub));
+    if (a.phases != nullptr) {
+      __asm__ __volatile__("s_waitcnt vmcnt(0)" ::: "memory");
+      t_acked = now_ticks();
+    }
     u32x4 got[P];
-    poll_all<Pr, P>(area_r, a.slot, off, r, a.epoch, deadline, got);
+    const int spins = poll_all<Pr, P>(area_r, a.slot, off, r, a.epoch, deadline, got, a.first_wait, a.poll_gap);
+    if (a.phases != nullptr && threadIdx.x == 0) {
+      const uint64_t t_polled = now_ticks() + (got[(r + 1) % P].x & 0u);
+      a.phases[4 * blockIdx.x + 0] = t_loaded;
+      a.phases[4 * blockIdx.x + 1] = t_acked;
+      a.phases[4 * blockIdx.x + 2] = t_polled;
+      a.phases[4 * blockIdx.x + 3] = (uint64_t)spins;
+    }
 #pragma unroll
     for (int q = 0; q < P; ++q) got[q] = Pr::unpack(got[q], sub);
     const u32x4 res = reduce_ordered<Pr, DT, P>(got, own, r);
     store_words<DT>(out_r, w0, cnt, n, a.al4 != 0, res);
+  }
+  stamp_end(a);
+}
+
+// ---------------------------------------------------------------------------
+// One-shot AllReduce, one wave per peer, with LDS staging (8-byte packets).
+//
+// A workgroup has P waves and handles tiles of 64*U packet units (each unit
+// = 2 payload words; lane l owns units l, l+64, ..., l+64(U-1) of the tile,
+// so every memory instruction of a wave covers 1 KiB of packets).  For a
+// tile, wave q != r sends the rank's packets to peer q only and then polls
+// only the packets peer q sent to this rank; wave r keeps the rank's own
+// values.  Each wave stages its rank's values, widened to binary32, in LDS
+// row q; after a workgroup barrier the rows are summed in ascending rank
+// order and rounded once.  Compared with one lane talking to all P-1 peers, a
+// wave's poll never waits for more than its own U stores (the memory counter
+// covers stores and loads alike on this chip) and a poll is U loads, not
+// U*(P-1).
+template <int DT, int P, int U>
+__global__ __launch_bounds__(512) void k_oneshot_waves(KArgs a) {
+  stamp_start(a);
+  constexpr int E = Elem<DT>::kBytes;
+  constexpr int K = Elem<DT>::kPerWord;
+  constexpr int EPU = 2 * K;   // elements per 8-byte-packet unit
+  constexpr int TW = 128 * U;  // payload words per tile
+  __shared__ float stage[P][TW * K];
+  const Part pt = part_of_block<P>();
+  const int r = pt.r;
+  const int wv = (int)uniform_u32(threadIdx.x >> 6);  // the same in every lane of a wave
+  const int lane = (int)(threadIdx.x & 63);
+  const uint64_t deadline = now_ticks() + a.timeout;
+  char *const slice_r = a.sym + (uint64_t)r * a.stride;
+  const int64_t n = a.n;
+  const int64_t words = (n * E + 3) / 4;
+  const int64_t units = ProtoLL::units(words);
+  const int64_t tiles = (units + 64 * U - 1) / (64 * U);
+  char *const out_r = a.out + (uint64_t)r * (uint64_t)n * E;
+  const bool publish = (r != a.mute);
+  const int q = wv;  // the peer this wave talks to (q == r: the own values)
+  char *const dst = a.sym + (uint64_t)q * a.stride + a.area + (uint64_t)slot_of(r, q) * a.slot;
+  char *const src = slice_r + a.area + (uint64_t)slot_of(q, r) * a.slot;
+
+  for (int64_t tile = pt.w; tile < tiles; tile += pt.W) {
+    u32x4 v[U];
+    u32x4 own[U];
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const int64_t u = tile * 64 * U + k * 64 + lane;
+      v[k] = u32x4{0u, 0u, 0u, 0u};
+      own[k] = u < units ? load_words<DT>(slice_r, 2 * u, 2, n, true) : u32x4{0u, 0u, 0u, 0u};
+    }
+    if (q == r) {
+#pragma unroll
+      for (int k = 0; k < U; ++k) v[k] = own[k];
+    } else {
+      const rsrc_t rd = make_rsrc(dst, (uint32_t)a.slot);
+      const rsrc_t rs = make_rsrc(src, (uint32_t)a.slot);
+      uint32_t pend = 0;
+#pragma unroll
+      for (int k = 0; k < U; ++k) {
+        const int64_t u = tile * 64 * U + k * 64 + lane;
+        if (u < units) {
+          pend |= 1u << k;
+          if (publish) st_pkt(rd, (uint32_t)(u * ProtoLL::kUnitBytes), ProtoLL::pack(own[k], a.epoch, 0));
+        }
+      }
+      int spins = 1;
+      while (pend != 0) {
+        compiler_fence();
+        u32x4 pk[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+          const int64_t u = tile * 64 * U + k * 64 + lane;
+          if (pend & (1u << k)) pk[k] = ld_pkt(rs, (uint32_t)(u * ProtoLL::kUnitBytes));
+        }
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+          if ((pend & (1u << k)) && ProtoLL::ready(pk[k], a.epoch)) {
+            v[k] = ProtoLL::unpack(pk[k], 0);
+            pend &= ~(1u << k);
+          }
+        }
+        if (pend != 0 && (spins++ & 15) == 0 && now_ticks() > deadline) {
+          report_timeout(r, 1u << q, a.epoch);
+          break;
+        }
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      float f[EPU];
+      Elem<DT>::widen(v[k].x, f);
+      Elem<DT>::widen(v[k].y, f + K);
+#pragma unroll
+      for (int e = 0; e < EPU; ++e) stage[q][(k * 64 + lane) * EPU + e] = f[e];
+    }
+    __syncthreads();
+    for (int j = (int)threadIdx.x; j < TW; j += (int)blockDim.x) {
+      float acc[K];
+#pragma unroll
+      for (int e = 0; e < K; ++e) acc[e] = stage[0][j * K + e];
+#pragma unroll
+      for (int p = 1; p < P; ++p) {
+#pragma unroll
+        for (int e = 0; e < K; ++e) acc[e] = acc[e] + stage[p][j * K + e];
+      }
+      const u32x4 res = {Elem<DT>::narrow(acc), 0u, 0u, 0u};
+      store_words<DT>(out_r, tile * TW + j, 1, n, a.al4 != 0, res);
+    }
+    __syncthreads();
   }
   stamp_end(a);
 }

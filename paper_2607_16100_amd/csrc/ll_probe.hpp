@@ -143,6 +143,18 @@ __global__ void k_probe_pingpong(uint32_t *flags, int rounds, int peer, uint64_t
   }
 }
 
+// One lane waits until `ticks` of the constant clock have passed since it
+// started (at most 1 s), so that the host can queue launches behind it and
+// they then run back to back without waiting for the host.
+__global__ void k_probe_spin(uint64_t ticks) {
+  if (blockIdx.x != 0 || threadIdx.x != 0) return;
+  const uint64_t t0 = now_ticks();
+  const uint64_t limit = ticks < 100000000ull ? ticks : 100000000ull;
+  while (now_ticks() - t0 < limit) {
+    __builtin_amdgcn_s_sleep(8);
+  }
+}
+
 // XCD id (bits 3:0 of the XCC_ID hardware register) of every workgroup.
 __global__ void k_probe_xcd(uint32_t *ids) {
   if (threadIdx.x == 0) ids[blockIdx.x] = __builtin_amdgcn_s_getreg(0xf814) & 0xfu;

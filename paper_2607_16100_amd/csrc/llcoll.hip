@@ -30,7 +30,11 @@ std::atomic<int> g_wg_per_rank{0};
 std::atomic<int> g_threads{0};
 std::atomic<uint64_t> g_timeout{200000000ull};  // 2 s of the 100 MHz clock
 std::atomic<int> g_mute{-1};
+std::atomic<int> g_first_wait{0};
+std::atomic<int> g_poll_gap{0};
+std::atomic<int> g_wave_units{0};  // 0 = automatic, else 1, 2 or 4
 std::atomic<uint64_t *> g_stamps{nullptr};
+std::atomic<uint64_t *> g_phases{nullptr};
 std::atomic<int> g_last_grid{0};
 std::atomic<int> g_last_threads{0};
 thread_local int t_last_hip = 0;
@@ -43,7 +47,8 @@ TimeoutInfo g_last_timeout;
 std::mutex g_mu;
 
 // ---------------------------------------------------------------- kernels
-enum Kind { K_ONESHOT = 0, K_TWOSHOT = 1, K_RS = 2, K_AG = 3, K_KINDS = 4 };
+enum Kind { K_ONESHOT = 0, K_TWOSHOT = 1, K_RS = 2, K_AG = 3, K_ONESHOT_WAVES = 4, K_KINDS = 5 };
+constexpr int kWaveUnits[3] = {1, 2, 4};  // units per lane of the wave-per-peer kernels
 enum Proto { PR_LL = 0, PR_LINE = 1, PR_COUNT = 2 };
 
 typedef void (*kernel_fn)(KArgs);
@@ -54,13 +59,16 @@ void fill_row(kernel_fn *row) {
   row[K_TWOSHOT] = k_twoshot<Pr, DT, P>;
   row[K_RS] = k_reduce_scatter<Pr, DT, P>;
   row[K_AG] = k_allgather<Pr, DT, P>;
+  row[K_ONESHOT_WAVES] = nullptr;
 }
 
 // table[proto][dtype][P][kind]
 struct Table {
   kernel_fn k[PR_COUNT][2][LL_MAX_RANKS + 1][K_KINDS];
+  kernel_fn waves[3][2][LL_MAX_RANKS + 1];  // [log2 U][dtype][P]
   Table() {
     memset(k, 0, sizeof k);
+    memset(waves, 0, sizeof waves);
     fill<2>();
     fill<3>();
     fill<4>();
@@ -75,6 +83,12 @@ struct Table {
     fill_row<ProtoLL, 1, P>(k[PR_LL][1][P]);
     fill_row<ProtoLine, 0, P>(k[PR_LINE][0][P]);
     fill_row<ProtoLine, 1, P>(k[PR_LINE][1][P]);
+    waves[0][0][P] = k_oneshot_waves<0, P, 1>;
+    waves[0][1][P] = k_oneshot_waves<1, P, 1>;
+    waves[1][0][P] = k_oneshot_waves<0, P, 2>;
+    waves[1][1][P] = k_oneshot_waves<1, P, 2>;
+    waves[2][0][P] = k_oneshot_waves<0, P, 4>;
+    waves[2][1][P] = k_oneshot_waves<1, P, 4>;
   }
 };
 
@@ -159,12 +173,32 @@ struct Plan {
   int64_t units;  // packet units per stream
 };
 
+// Units per lane of the wave-per-peer one-shot: fewer, fuller workgroups as
+// messages grow.
+int wave_units_log2(int64_t units) {
+  const int forced = g_wave_units.load();
+  if (forced == 1) return 0;
+  if (forced == 2) return 1;
+  if (forced == 4) return 2;
+  if (units <= 64 * 64) return 0;
+  return 1;
+}
+
 int launch(const Plan &pl, void *stream) {
-  const kernel_fn fn = table().k[pl.proto][pl.dt][pl.P][pl.kind];
+  const int wlog = pl.kind == K_ONESHOT_WAVES ? wave_units_log2(pl.units) : 0;
+  const kernel_fn fn = pl.kind == K_ONESHOT_WAVES ? table().waves[wlog][pl.dt][pl.P]
+                                                   : table().k[pl.proto][pl.dt][pl.P][pl.kind];
   if (fn == nullptr) return LL_ERR_UNSUPPORTED;
   int threads = g_threads.load();
   if (threads == 0) threads = 256;
-  const int lanes_per_unit = pl.proto == PR_LINE ? ProtoLine::kLanes : ProtoLL::kLanes;
+  int lanes_per_unit = pl.proto == PR_LINE ? ProtoLine::kLanes : ProtoLL::kLanes;
+  int64_t work_units = pl.units;
+  if (pl.kind == K_ONESHOT_WAVES) {  // one wave per rank, 64*U units per workgroup and step
+    threads = 64 * pl.P;
+    const int64_t tile = 64 * kWaveUnits[wlog];
+    work_units = (pl.units + tile - 1) / tile;
+    lanes_per_unit = threads;
+  }
   int cap_grid = 0;
   int st = resident_grid(fn, threads, &cap_grid);
   if (st != LL_OK) return st;
@@ -172,7 +206,7 @@ int launch(const Plan &pl, void *stream) {
   if (wmax < 1) return LL_ERR_UNSUPPORTED;
   int W = g_wg_per_rank.load();
   if (W == 0) {
-    const int64_t lanes = pl.units * lanes_per_unit;
+    const int64_t lanes = work_units * lanes_per_unit;
     int64_t want = (lanes + threads - 1) / threads;
     if (want < 1) want = 1;
     W = (int)(want < wmax ? want : wmax);
@@ -183,7 +217,10 @@ int launch(const Plan &pl, void *stream) {
   KArgs a = pl.a;
   a.timeout = g_timeout.load();
   a.mute = g_mute.load();
+  a.first_wait = (uint16_t)g_first_wait.load();
+  a.poll_gap = (uint16_t)g_poll_gap.load();
   a.stamps = g_stamps.exchange(nullptr);
+  a.phases = g_phases.exchange(nullptr);
   hipLaunchKernelGGL(fn, dim3(grid), dim3(threads), 0, (hipStream_t)stream, a);
   hipError_t e = hipGetLastError();
   g_last_grid.store(grid);
@@ -223,9 +260,13 @@ KArgs base_args(void *sym_base, size_t rank_stride, void *out, uint32_t epoch) {
   return a;
 }
 
+// Size thresholds measured on MI355X with 8 ranks (latency of back-to-back
+// calls per algorithm and message size).
 ll_algo auto_algo(uint64_t in_bytes, int P) {
   (void)P;
-  if (in_bytes <= (256u << 10)) return LL_ALGO_ONESHOT;
+  if (in_bytes <= (32u << 10)) return LL_ALGO_ONESHOT_WAVES;
+  if (in_bytes <= (128u << 10)) return LL_ALGO_ONESHOT_LINE;
+  if (in_bytes <= (1u << 20)) return LL_ALGO_TWOSHOT;
   return LL_ALGO_TWOSHOT_LINE;
 }
 
@@ -285,7 +326,7 @@ int ll_allreduce_algo(void *sym_base, size_t rank_stride, void *out, size_t coun
   if (st != LL_OK) return st;
   st = check_dtype_op((int)dt, (int)op);
   if (st != LL_OK) return st;
-  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_ONESHOT_LINE) return LL_ERR_INVALID;
+  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_ONESHOT_WAVES) return LL_ERR_INVALID;
   const int es = esize_of(dt);
   const uint64_t in_bytes = (uint64_t)count * es;
   if (count > L::kMaxInputBytes) return LL_ERR_UNSUPPORTED;
@@ -303,10 +344,11 @@ int ll_allreduce_algo(void *sym_base, size_t rank_stride, void *out, size_t coun
   pl.a.n = (int64_t)count;
   pl.a.al4 = (in_bytes % 4 == 0) ? 1u : 0u;
   const bool line = (algo == LL_ALGO_TWOSHOT_LINE || algo == LL_ALGO_ONESHOT_LINE);
+  const bool waves = (algo == LL_ALGO_ONESHOT_WAVES);
   pl.proto = line ? PR_LINE : PR_LL;
   pl.a.area = line ? rg.cap + rg.a8 : rg.cap;
-  if (algo == LL_ALGO_ONESHOT || algo == LL_ALGO_ONESHOT_LINE) {
-    pl.kind = K_ONESHOT;
+  if (algo == LL_ALGO_ONESHOT || algo == LL_ALGO_ONESHOT_LINE || waves) {
+    pl.kind = waves ? K_ONESHOT_WAVES : K_ONESHOT;
     pl.a.slot = line ? L::slot128(in_bytes) : L::slot8(in_bytes);
     const int64_t words = (int64_t)L::ceil_div(in_bytes, 4);
     pl.units = line ? ProtoLine::units(words) : ProtoLL::units(words);
@@ -464,6 +506,19 @@ int ll_set_launch(int workgroups_per_rank, int threads) {
   return LL_OK;
 }
 
+int ll_set_poll_pacing(int first_wait, int poll_gap) {
+  if (first_wait < 0 || first_wait > 1000 || poll_gap < 0 || poll_gap > 1000) return LL_ERR_INVALID;
+  g_first_wait.store(first_wait);
+  g_poll_gap.store(poll_gap);
+  return LL_OK;
+}
+
+int ll_set_wave_units(int units_per_lane) {
+  if (units_per_lane != 0 && units_per_lane != 1 && units_per_lane != 2 && units_per_lane != 4) return LL_ERR_INVALID;
+  g_wave_units.store(units_per_lane);
+  return LL_OK;
+}
+
 int ll_set_poll_timeout(uint64_t ticks) {
   if (ticks == 0) return LL_ERR_INVALID;
   g_timeout.store(ticks);
@@ -478,6 +533,11 @@ int ll_debug_mute_rank(int rank) {
 
 int ll_debug_stamp_next(uint64_t *stamps) {
   g_stamps.store(stamps);
+  return LL_OK;
+}
+
+int ll_debug_phase_next(uint64_t *phases) {
+  g_phases.store(phases);
   return LL_OK;
 }
 
@@ -539,6 +599,58 @@ int ll_probe_pingpong(uint32_t *flags8k, int rounds, int grid, int peer, uint64_
     return LL_ERR_INVALID;
   hipLaunchKernelGGL(k_probe_pingpong, dim3(grid), dim3(64), 0, (hipStream_t)stream, flags8k, rounds, peer,
                      limit_ticks, out3);
+  return hip_status();
+}
+
+int ll_probe_spin(uint64_t ticks, void *stream) {
+  if (ticks == 0 || ticks > 100000000ull) return LL_ERR_INVALID;
+  hipLaunchKernelGGL(k_probe_spin, dim3(1), dim3(64), 0, (hipStream_t)stream, ticks);
+  return hip_status();
+}
+
+int ll_bench_allreduce(void *sym_base, size_t rank_stride, void *out, size_t count, int dt, int nranks,
+                       uint32_t first_epoch, int calls, int algo, uint64_t *stamps, int stamp_stride,
+                       void *stream) {
+  if (calls < 1 || first_epoch == 0 || (uint64_t)first_epoch + (uint64_t)calls - 1 > 0xFFFFFFFFull)
+    return LL_ERR_INVALID;
+  if (stamps != nullptr && stamp_stride < 1) return LL_ERR_INVALID;
+  for (int i = 0; i < calls; ++i) {
+    if (stamps != nullptr) g_stamps.store(stamps + (size_t)i * (size_t)stamp_stride);
+    const int st = ll_allreduce_algo(sym_base, rank_stride, out, count, (ll_dtype)dt, LL_SUM, nranks,
+                                     first_epoch + (uint32_t)i, stream, (ll_algo)algo);
+    if (st != LL_OK) {
+      g_stamps.store(nullptr);
+      return st;
+    }
+  }
+  return LL_OK;
+}
+
+int ll_bench_floor(const uint64_t *chase, uint64_t chase_len, uint64_t first_line, uint64_t line_step,
+                   uint64_t *sink, int grid, int threads, int calls, uint64_t *stamps, int stamp_stride,
+                   void *stream) {
+  int st = probe_launch_check(grid, threads);
+  if (st != LL_OK) return st;
+  if (chase == nullptr || sink == nullptr || calls < 1 || chase_len < 16) return LL_ERR_INVALID;
+  if (stamps != nullptr && stamp_stride < 2 * grid) return LL_ERR_INVALID;
+  const uint64_t lines = chase_len / 16;
+  for (int i = 0; i < calls; ++i) {
+    const uint64_t start = ((first_line + (uint64_t)i * line_step) % lines) * 16;
+    hipLaunchKernelGGL(k_probe_floor, dim3(grid), dim3(threads), 0, (hipStream_t)stream, chase, start, sink,
+                       stamps ? stamps + (size_t)i * (size_t)stamp_stride : nullptr);
+  }
+  return hip_status();
+}
+
+int ll_bench_empty(int grid, int threads, int calls, uint64_t *stamps, int stamp_stride, void *stream) {
+  int st = probe_launch_check(grid, threads);
+  if (st != LL_OK) return st;
+  if (calls < 1) return LL_ERR_INVALID;
+  if (stamps != nullptr && stamp_stride < 2 * grid) return LL_ERR_INVALID;
+  for (int i = 0; i < calls; ++i) {
+    hipLaunchKernelGGL(k_probe_empty, dim3(grid), dim3(threads), 0, (hipStream_t)stream,
+                       stamps ? stamps + (size_t)i * (size_t)stamp_stride : nullptr);
+  }
   return hip_status();
 }
 

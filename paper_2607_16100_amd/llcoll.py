@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(_HERE, "libllcoll.so")
 LL_F32, LL_BF16 = 0, 1
 LL_SUM = 0
 LL_ALGO_AUTO, LL_ALGO_ONESHOT, LL_ALGO_TWOSHOT, LL_ALGO_TWOSHOT_LINE, LL_ALGO_ONESHOT_LINE = 0, 1, 2, 3, 4
+LL_ALGO_ONESHOT_WAVES = 5
 LL_PROTO_AUTO, LL_PROTO_PACKET8, LL_PROTO_LINE128 = 0, 1, 2
 
 LL_OK = 0
@@ -28,6 +29,7 @@ LL_ERR_TIMEOUT = -5
 ALGOS = {
     "auto": LL_ALGO_AUTO, "oneshot": LL_ALGO_ONESHOT, "twoshot": LL_ALGO_TWOSHOT,
     "twoshot_line": LL_ALGO_TWOSHOT_LINE, "oneshot_line": LL_ALGO_ONESHOT_LINE,
+    "oneshot_waves": LL_ALGO_ONESHOT_WAVES,
 }
 PROTOS = {"auto": LL_PROTO_AUTO, "packet8": LL_PROTO_PACKET8, "line128": LL_PROTO_LINE128}
 DTYPES = {"f32": LL_F32, "bf16": LL_BF16}
@@ -48,21 +50,34 @@ _SIGS = {
     "ll_last_timeout": (_i, [ctypes.POINTER(_i), ctypes.POINTER(_u32), ctypes.POINTER(_u32)]),
     "ll_strerror": (ctypes.c_char_p, [_i]),
     "ll_set_launch": (_i, [_i, _i]),
+    "ll_set_poll_pacing": (_i, [_i, _i]),
+    "ll_set_wave_units": (_i, [_i]),
     "ll_set_poll_timeout": (_i, [_u64]),
     "ll_debug_mute_rank": (_i, [_i]),
     "ll_debug_stamp_next": (_i, [_vp]),
+    "ll_debug_phase_next": (_i, [_vp]),
     "ll_last_grid": (_i, [ctypes.POINTER(_i), ctypes.POINTER(_i)]),
     "ll_probe_empty": (_i, [_i, _i, _vp, _vp]),
     "ll_probe_floor": (_i, [_vp, _u64, _u64, _vp, _i, _i, _vp, _vp]),
     "ll_probe_chase": (_i, [_vp, _u64, _u64, _i, _vp, _vp]),
     "ll_probe_fence_l2": (_i, [_vp, _i, _vp, _vp]),
     "ll_probe_pingpong": (_i, [_vp, _i, _i, _i, _u64, _vp, _vp]),
+    "ll_probe_spin": (_i, [_u64, _vp]),
+    "ll_bench_allreduce": (_i, [_vp, _sz, _vp, _sz, _i, _i, _u32, _i, _i, _vp, _i, _vp]),
+    "ll_bench_floor": (_i, [_vp, _u64, _u64, _u64, _vp, _i, _i, _i, _vp, _i, _vp]),
+    "ll_bench_empty": (_i, [_i, _i, _i, _vp, _i, _vp]),
     "ll_probe_xcd": (_i, [_vp, _i, _i, _vp]),
     "ll_probe_litmus": (_i, [_vp, _sz, _i, _i, _i, _i, _i, _vp, _vp]),
 }
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"llcoll HIP library not built ({LIB_PATH}); run __graft_entry__.build()")
+# torch ships its own HIP runtime and loads it from its own directory.  Load
+# torch first so that the library's dependency on libamdhip64.so.7 resolves to
+# that same, already loaded runtime; loading the library first would put two
+# HIP runtimes into one process.
+import torch  # noqa: E402,F401
+
 _lib = ctypes.CDLL(LIB_PATH)
 for _name, (_res, _args) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -149,6 +164,14 @@ def ll_set_launch(workgroups_per_rank: int, threads: int):
     return _lib.ll_set_launch(workgroups_per_rank, threads)
 
 
+def ll_set_poll_pacing(first_wait: int, poll_gap: int):
+    return _lib.ll_set_poll_pacing(first_wait, poll_gap)
+
+
+def ll_set_wave_units(units_per_lane: int):
+    return _lib.ll_set_wave_units(units_per_lane)
+
+
 def ll_set_poll_timeout(ticks: int):
     return _lib.ll_set_poll_timeout(ticks)
 
@@ -159,6 +182,10 @@ def ll_debug_mute_rank(rank: int):
 
 def ll_debug_stamp_next(stamps):
     return _lib.ll_debug_stamp_next(stamps)
+
+
+def ll_debug_phase_next(phases):
+    return _lib.ll_debug_phase_next(phases)
 
 
 def ll_last_grid():
@@ -185,6 +212,26 @@ def ll_probe_fence_l2(buf4k, iters, out7, stream):
 
 def ll_probe_pingpong(flags8k, rounds, grid, peer, limit_ticks, out3, stream):
     return _lib.ll_probe_pingpong(flags8k, rounds, grid, peer, limit_ticks, out3, stream)
+
+
+def ll_probe_spin(ticks, stream):
+    return _lib.ll_probe_spin(ticks, stream)
+
+
+def ll_bench_allreduce(sym_base, rank_stride, out, count, dt, nranks, first_epoch, calls, algo, stamps,
+                       stamp_stride, stream):
+    return _lib.ll_bench_allreduce(sym_base, rank_stride, out, count, dt, nranks, first_epoch, calls, algo, stamps,
+                                   stamp_stride, stream)
+
+
+def ll_bench_floor(chase, chase_len, first_line, line_step, sink, grid, threads, calls, stamps, stamp_stride,
+                   stream):
+    return _lib.ll_bench_floor(chase, chase_len, first_line, line_step, sink, grid, threads, calls, stamps,
+                               stamp_stride, stream)
+
+
+def ll_bench_empty(grid, threads, calls, stamps, stamp_stride, stream):
+    return _lib.ll_bench_empty(grid, threads, calls, stamps, stamp_stride, stream)
 
 
 def ll_probe_xcd(ids, grid, threads, stream):

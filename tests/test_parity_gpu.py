@@ -24,7 +24,7 @@ if torch.cuda.is_available():
 else:  # pragma: no cover
     pytest.skip("no GPU", allow_module_level=True)
 
-AR_ALGOS = ["oneshot", "twoshot", "twoshot_line", "oneshot_line"]
+AR_ALGOS = ["oneshot", "twoshot", "twoshot_line", "oneshot_line", "oneshot_waves", "auto"]
 PROTOS = ["packet8", "line128"]
 NP = {"f32": np.uint32, "bf16": np.uint16}
 
@@ -64,6 +64,7 @@ TEST_TIMEOUT_TICKS = 20_000_000  # 200 ms per flag wait: thousands of times a co
 
 @pytest.fixture(autouse=True)
 def _reset_settings():
+    ll.ll_set_wave_units(0)
     ll.ll_set_launch(0, 0)
     ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
     ll.ll_debug_mute_rank(-1)
@@ -251,8 +252,11 @@ def test_result_independent_of_launch_shape(algo):
     reg.init()
     for wg, threads in [(1, 64), (1, 1024), (3, 256), (16, 128), (0, 0)]:
         ll.ll_set_launch(wg, threads)
-        say(f"launch {algo} wg={wg} threads={threads}")
-        assert_bits_equal(run_allreduce(reg, x, algo), want, f"{algo} wg={wg} t={threads}")
+        for units in ([1, 2, 4, 0] if algo == "oneshot_waves" else [0]):
+            ll.ll_set_wave_units(units)
+            say(f"launch {algo} wg={wg} threads={threads} units={units}")
+            assert_bits_equal(run_allreduce(reg, x, algo), want, f"{algo} wg={wg} t={threads} u={units}")
+    ll.ll_set_wave_units(0)
 
 
 def test_large_epochs_and_reinit():
@@ -264,7 +268,7 @@ def test_large_epochs_and_reinit():
     reg = SymRegion(p, n, "f32")
     reg.init()
     reg.write_inputs(x)
-    for algo, e in zip(AR_ALGOS, (0x7FFFFFFF, 0x80000000, 0xFFFFFFFE, 0xFFFFFFFF)):
+    for algo, e in zip(AR_ALGOS, (0x7FFFFFFF, 0x80000000, 0xFFFFFFFC, 0xFFFFFFFD, 0xFFFFFFFE, 0xFFFFFFFF)):
         check_ok(reg.allreduce(n, algo, epoch=e), f"epoch {e:#x}")
         assert_bits_equal(reg.read_out(p * n, np.uint32).reshape(p, n), want, f"{algo} epoch {e:#x}")
     reg.init()
@@ -285,7 +289,8 @@ def test_count_zero_is_a_no_op():
 @pytest.mark.parametrize("algo", ["oneshot", "twoshot_line"])
 def test_missing_peer_times_out_and_is_reported(algo):
     """Rank 3 publishes nothing; its peers' bounded waits expire (after 2 ms),
-    every kernel still finishes, and ll_check reports the timeout."""
+    every kernel still finishes, and ll_check reports the timeout.  (In two-shot
+    the peers then publish late, so rank 3 may be the first to give up.)"""
     p, n = 8, 4096
     x = wl.uniform(p, n, "f32", seed=1)
     reg = SymRegion(p, n, "f32")
@@ -297,7 +302,10 @@ def test_missing_peer_times_out_and_is_reported(algo):
     assert st == ll.LL_OK
     assert ll.ll_check(stream()) == ll.LL_ERR_TIMEOUT
     rank, missing, epoch = ll.ll_last_timeout()
-    assert rank != 3 and missing == (1 << 3) and epoch == reg.epoch
+    assert epoch == reg.epoch and missing != 0
+    if algo == "oneshot":
+        # only rank 3's packets are missing; the first rank to give up names it
+        assert rank != 3 and missing == (1 << 3)
     ll.ll_debug_mute_rank(-1)
     ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
     reg.init()
