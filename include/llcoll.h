@@ -160,6 +160,11 @@ int ll_set_launch(int workgroups_per_rank, int threads);
  * polls (poll_gap), each in [0, 1000].  0 = poll back to back. */
 int ll_set_poll_pacing(int first_wait, int poll_gap);
 
+/* Two-shot pipeline distance for the following calls: a lane publishes the
+ * ReduceScatter packets of step s, reduces step s-lag and gathers step
+ * s-2*lag.  lag in [1, 64]; default 1. */
+int ll_set_pipeline_lag(int lag);
+
 /* Packet units (16 bytes of packets) per lane of LL_ALGO_ONESHOT_WAVES for
  * the following calls: 1, 2 or 4; 0 = automatic. */
 int ll_set_wave_units(int units_per_lane);

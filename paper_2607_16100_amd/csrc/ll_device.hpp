@@ -4,7 +4,9 @@
 //   * 8-byte packet  = {payload u32, flag u32}.  A lane moves two packets in
 //     one 16-byte store, so a wave writes 1 KiB contiguous per instruction.
 //   * 128-byte line  = 8 lanes x 16 bytes.  The last dword of each 64-byte
-//     half is the flag, the other 30 dwords are payload (120 of 128 bytes).
+//     half is the flag, the other 30 dwords are payload (120 of 128 bytes);
+//     which payload word goes where is chosen so that every access to the
+//     input and output is 16-byte aligned (ProtoLine below).
 // The flag is the call's epoch.  A receiver accepts a packet once every flag
 // covering it equals the epoch; zeroed scratch (flag 0) never matches.
 //
@@ -94,6 +96,16 @@ template <> struct Elem<1> {  // bfloat16
 // stream covers elements [k*kPerWord, (k+1)*kPerWord).  `al4` says the base is
 // 4-byte aligned; otherwise (bfloat16 streams that start on an odd element)
 // elements are moved one at a time.
+// Inputs are read once and outputs written once per call: load and store them
+// with the streaming (non-temporal) hint so they do not displace the packets,
+// which are read back soon after they are written.
+#ifndef LLCOLL_NT_IN
+#define LLCOLL_NT_IN 1
+#endif
+#ifndef LLCOLL_NT_OUT
+#define LLCOLL_NT_OUT 1
+#endif
+
 template <int DT>
 __device__ __forceinline__ u32x4 load_words(const char *base, int64_t w0, int cnt, int64_t nelem, bool al4) {
   constexpr int K = Elem<DT>::kPerWord;
@@ -101,7 +113,13 @@ __device__ __forceinline__ u32x4 load_words(const char *base, int64_t w0, int cn
   const int64_t e0 = w0 * K;
   if (al4 && e0 + (int64_t)cnt * K <= nelem) {
     const char *p = base + w0 * 4;
-    if (cnt == 4) {
+    if (LLCOLL_NT_IN && cnt == 4 && ((uintptr_t)p & 15) == 0) {
+      v = __builtin_nontemporal_load((const u32x4 *)p);
+    } else if (LLCOLL_NT_IN && cnt == 2 && ((uintptr_t)p & 7) == 0) {
+      const u32x2 t = __builtin_nontemporal_load((const u32x2 *)p);
+      v.x = t.x;
+      v.y = t.y;
+    } else if (cnt == 4) {
       __builtin_memcpy(&v, p, 16);
     } else if (cnt == 3) {
       uint32_t t[3];
@@ -141,7 +159,12 @@ __device__ __forceinline__ void store_words(char *base, int64_t w0, int cnt, int
   const int64_t e0 = w0 * K;
   if (al4 && e0 + (int64_t)cnt * K <= nelem) {
     char *p = base + w0 * 4;
-    if (cnt == 4) {
+    if (LLCOLL_NT_OUT && cnt == 4 && ((uintptr_t)p & 15) == 0) {
+      __builtin_nontemporal_store(v, (u32x4 *)p);
+    } else if (LLCOLL_NT_OUT && cnt == 2 && ((uintptr_t)p & 7) == 0) {
+      const u32x2 t = {v.x, v.y};
+      __builtin_nontemporal_store(t, (u32x2 *)p);
+    } else if (cnt == 4) {
       __builtin_memcpy(p, &v, 16);
     } else if (cnt == 3) {
       uint32_t t[3] = {v.x, v.y, v.z};
@@ -170,16 +193,25 @@ __device__ __forceinline__ void store_words(char *base, int64_t w0, int cnt, int
 }
 
 // ---------------------------------------------------------------------------
-// Packet formats.  `sub` is the lane's position inside a unit (0 for 8-byte
-// packets, 0..7 for a line); a unit is what one group of lanes moves with one
-// 16-byte store each.
+// Packet formats.  A unit is what one group of lanes moves with one 16-byte
+// packet store each; `sub` is the lane's position in its group.  Each format
+// says which payload words of a stream a lane carries (load/store), how they
+// sit in its 16 bytes of packet (pack/unpack) and when they have arrived
+// (ready).
 struct ProtoLL {
+  // 8-byte packets {payload, flag}: a lane carries payload words 2u, 2u+1.
   static constexpr int kLanes = 1;        // lanes per unit
-  static constexpr int kUnitBytes = 16;   // bytes per unit in a slot
+  static constexpr int kUnitBytes = 16;   // packet bytes per unit in a slot
   static constexpr int kUnitWords = 2;    // payload words per unit
   static constexpr int kMaxWords = 2;     // payload words per lane
-  __device__ static __forceinline__ int64_t word0(int64_t u, int /*sub*/) { return 2 * u; }
-  __device__ static __forceinline__ int count(int /*sub*/) { return 2; }
+  template <int DT>
+  __device__ static __forceinline__ u32x4 load(const char *base, int64_t u, int /*sub*/, int64_t nelem, bool al4) {
+    return load_words<DT>(base, 2 * u, 2, nelem, al4);
+  }
+  template <int DT>
+  __device__ static __forceinline__ void store(char *base, int64_t u, int /*sub*/, int64_t nelem, bool al4, u32x4 w) {
+    store_words<DT>(base, 2 * u, 2, nelem, al4, w);
+  }
   __device__ static __forceinline__ u32x4 pack(u32x4 w, uint32_t epoch, int /*sub*/) {
     u32x4 p = {w.x, epoch, w.y, epoch};
     return p;
@@ -192,21 +224,75 @@ struct ProtoLL {
   static constexpr __host__ __device__ int64_t units(int64_t words) { return (words + 1) / 2; }
 };
 
+// 128-byte line packets: 8 lanes x 16 bytes a line, the last dword of each
+// 64-byte quarter-wave group ("quad", 4 lanes) is the flag, so a line carries
+// 30 payload dwords and two flags.  A wave's 64 lanes (8 lines, 1 KiB) form
+// one unit carrying 240 payload words:
+//   * data lanes 0..59 carry the 16-byte-aligned words 4*sub .. 4*sub+3 of the
+//     unit, except that the flag lane of each quad (sub % 4 == 3) leaves its
+//     last word out -- the flag takes its place;
+//   * the extra lanes 60..63 carry those 15 displaced words: lane 60+i holds
+//     words 64i+16c+15, c = 0..3, of quads 4i+c (lane 63's last dword is the
+//     quad's flag).
+// Every load and store of payload is thus one 16-byte aligned access per data
+// lane; the displaced words move between lanes through the LDS crossbar
+// (ds_bpermute), not through memory.  This is the displacement of the
+// paper's LL128 design (Sec. IV), with the extra lanes in the role of its
+// extra threads.
 struct ProtoLine {
-  static constexpr int kLanes = 8;
-  static constexpr int kUnitBytes = 128;
-  static constexpr int kUnitWords = 30;
+  static constexpr int kLanes = 64;
+  static constexpr int kUnitBytes = 1024;
+  static constexpr int kUnitWords = 240;
   static constexpr int kMaxWords = 4;
-  __device__ static __forceinline__ int64_t word0(int64_t u, int sub) {
-    return 30 * u + 15 * (sub >> 2) + 4 * (sub & 3);
+  // Lane `src`'s value of v, for every lane (all 64 lanes must be active).
+  __device__ static __forceinline__ uint32_t from_lane(int src, uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_ds_bpermute(src * 4, (int)v);
   }
-  __device__ static __forceinline__ int count(int sub) { return (sub & 3) == 3 ? 3 : 4; }
+  // Called with the whole wave active (a unit is one wave).
+  template <int DT>
+  __device__ static __forceinline__ u32x4 load(const char *base, int64_t u, int sub, int64_t nelem, bool al4) {
+    const int64_t w0 = 240 * u;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (sub < 60) v = load_words<DT>(base, w0 + 4 * sub, 4, nelem, al4);
+    // extra lane 60+i collects the last word of the flag lanes of quads 4i..4i+3
+    const int i = (sub - 60) & 3;
+    const uint32_t d0 = from_lane(16 * i + 3, v.w);
+    const uint32_t d1 = from_lane(16 * i + 7, v.w);
+    const uint32_t d2 = from_lane(16 * i + 11, v.w);
+    const uint32_t d3 = from_lane((16 * i + 15) & 63, v.w);
+    if (sub >= 60) {
+      v.x = d0;
+      v.y = d1;
+      v.z = d2;
+      v.w = i < 3 ? d3 : 0u;
+    }
+    return v;
+  }
+  // Called with the whole wave active; w is in packet order.
+  template <int DT>
+  __device__ static __forceinline__ void store(char *base, int64_t u, int sub, int64_t nelem, bool al4, u32x4 w) {
+    const int64_t w0 = 240 * u;
+    // the flag lane of quad j takes its last word back from extra lane 60 + j/4
+    const int j = (sub >> 2) & 15;
+    const int src = 60 + (j >> 2);
+    const uint32_t c0 = from_lane(src, w.x);
+    const uint32_t c1 = from_lane(src, w.y);
+    const uint32_t c2 = from_lane(src, w.z);
+    const uint32_t c3 = from_lane(src, w.w);
+    if (sub < 60) {
+      if ((sub & 3) == 3) {
+        const int c = j & 3;
+        w.w = c == 0 ? c0 : (c == 1 ? c1 : (c == 2 ? c2 : c3));
+      }
+      store_words<DT>(base, w0 + 4 * sub, 4, nelem, al4, w);
+    }
+  }
   __device__ static __forceinline__ u32x4 pack(u32x4 w, uint32_t epoch, int sub) {
     if ((sub & 3) == 3) w.w = epoch;
     return w;
   }
-  // The flag of a 64-byte half sits in lane 3 of its quad; broadcast it to the
-  // quad with DPP.  All four lanes of a quad are always active together.
+  // The flag of a quad sits in its lane 3; broadcast it to the quad with DPP.
+  // All four lanes of a quad are always active together.
   __device__ static __forceinline__ bool ready(u32x4 p, uint32_t epoch) {
     uint32_t f = (uint32_t)__builtin_amdgcn_mov_dpp((int)p.w, 0xFF /* quad_perm:[3,3,3,3] */, 0xF, 0xF, false);
     return f == epoch;
@@ -215,7 +301,7 @@ struct ProtoLine {
     if ((sub & 3) == 3) p.w = 0u;
     return p;
   }
-  static constexpr __host__ __device__ int64_t units(int64_t words) { return (words + 29) / 30; }
+  static constexpr __host__ __device__ int64_t units(int64_t words) { return (words + 239) / 240; }
 };
 
 // ---------------------------------------------------------------------------

@@ -38,6 +38,8 @@ struct KArgs {
   uint32_t al4;       // every element stream of this call starts 4-byte aligned
   uint16_t first_wait;  // idle time before the first poll, in units of 64 shader cycles
   uint16_t poll_gap;    // idle time between polls, in units of 64 shader cycles
+  uint32_t lag;         // two-shot pipeline distance between publish, reduce and gather (>= 1)
+  uint32_t pad2_;
 };
 
 __device__ __forceinline__ int slot_of(int src, int dst) { return src - (src > dst ? 1 : 0); }
@@ -176,10 +178,8 @@ __global__ __launch_bounds__(1024) void k_oneshot(KArgs a) {
   const int64_t ustep = (int64_t)pt.W * blockDim.x / Pr::kLanes;
 
   for (int64_t u = g / Pr::kLanes; u < units; u += ustep) {
-    const int64_t w0 = Pr::word0(u, sub);
-    const int cnt = Pr::count(sub);
     const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
-    const u32x4 own = load_words<DT>(slice_r, w0, cnt, n, true);
+    const u32x4 own = Pr::template load<DT>(slice_r, u, sub, n, true);
     uint64_t t_loaded = 0, t_acked = 0;
     if (a.phases != nullptr) t_loaded = now_ticks() + (own.x & 0u);
     if (publish) bcast<P>(a, a.area, r, off, Pr::pack(own, a.epoch, sub));
@@ -199,7 +199,7 @@ __global__ __launch_bounds__(1024) void k_oneshot(KArgs a) {
 #pragma unroll
     for (int q = 0; q < P; ++q) got[q] = Pr::unpack(got[q], sub);
     const u32x4 res = reduce_ordered<Pr, DT, P>(got, own, r);
-    store_words<DT>(out_r, w0, cnt, n, a.al4 != 0, res);
+    Pr::template store<DT>(out_r, u, sub, n, a.al4 != 0, res);
   }
   stamp_end(a);
 }
@@ -317,89 +317,109 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs a) {
 // ---------------------------------------------------------------------------
 // Two-shot AllReduce (Sec. III-A): ReduceScatter then AllGather, fused in one
 // kernel.  The input is cut into P chunks of `chunk` elements (the last ones
-// may be short or empty); rank c owns chunk c.
-//   phase 1  send chunk c to slot (c <- r) of its owner, for every c != r
-//   phase 2  reduce own chunk r from the P-1 received copies and the own
-//            input, store it, and send the result to slot (q <- r) of every
-//            peer's AllGather area
-//   phase 3  receive every other reduced chunk and store it
-// RS slots occupy the first P-1 slots of the area, AG slots the next P-1.
+// may be short or empty); rank c owns chunk c.  For a packet unit u (the same
+// offset in every chunk) a lane runs three steps:
+//   publish  send unit u of chunk c to slot (c <- r) of its owner, c != r
+//   reduce   reduce unit u of the own chunk r from the P-1 received copies
+//            and the own input, store it, and send it to slot (q <- r) of
+//            every peer's AllGather area
+//   gather   receive unit u of every other reduced chunk and store it
+// The steps of successive units are software-pipelined: at step s a lane
+// publishes unit s, reduces unit s - lag and gathers unit s - 2*lag, so a
+// packet is read back soon after it was written (while it is still in the
+// memory-side cache) and the wait for peers overlaps the next unit's work.
+// Every wait is for an earlier step of the same lane on another rank, so the
+// pipeline cannot deadlock.  RS slots occupy the first P-1 slots of the
+// area, AG slots the next P-1.
 template <class Pr, int DT, int P>
-__global__ __launch_bounds__(1024) void k_twoshot(KArgs a) {
+struct TwoShot {
+  static constexpr int E = Elem<DT>::kBytes;
+  const KArgs &a;
+  int r;
+  char *slice_r;
+  char *out_r;
+  int64_t n, C;
+  uint64_t ag_area;
+  uint64_t deadline;
+  bool publish, al4;
+
+  __device__ __forceinline__ int64_t chunk_len(int c) const {
+    const int64_t left = n - (int64_t)c * C;
+    return left < 0 ? 0 : (left < C ? left : C);
+  }
+
+  __device__ __forceinline__ void step_publish(int64_t u, int sub) const {
+    const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+    u32x4 v[P];
+#pragma unroll
+    for (int k = 1; k < P; ++k) {
+      const int c = (r + k) % P;
+      v[k] = Pr::template load<DT>(slice_r + c * C * E, u, sub, chunk_len(c), true);
+    }
+#pragma unroll
+    for (int k = 1; k < P; ++k) {
+      const int c = (r + k) % P;
+      char *dst = a.sym + (uint64_t)c * a.stride + a.area + (uint64_t)slot_of(r, c) * a.slot;
+      st_pkt(make_rsrc(dst, (uint32_t)a.slot), off, Pr::pack(v[k], a.epoch, sub));
+    }
+  }
+
+  __device__ __forceinline__ void step_reduce(int64_t u, int sub) const {
+    const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+    const int64_t nr = chunk_len(r);
+    const u32x4 own = Pr::template load<DT>(slice_r + r * C * E, u, sub, nr, true);
+    u32x4 got[P];
+    poll_all<Pr, P>(slice_r + a.area, a.slot, off, r, a.epoch, deadline, got);
+#pragma unroll
+    for (int q = 0; q < P; ++q) got[q] = Pr::unpack(got[q], sub);
+    const u32x4 res = reduce_ordered<Pr, DT, P>(got, own, r);
+    Pr::template store<DT>(out_r + r * C * E, u, sub, nr, al4, res);
+    if (publish) bcast<P>(a, ag_area, r, off, Pr::pack(res, a.epoch, sub));
+  }
+
+  __device__ __forceinline__ void step_gather(int64_t u, int sub) const {
+    const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+    u32x4 got[P];
+    poll_all<Pr, P>(slice_r + ag_area, a.slot, off, r, a.epoch, deadline, got);
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      if (q == r) continue;
+      Pr::template store<DT>(out_r + q * C * E, u, sub, chunk_len(q), al4, Pr::unpack(got[q], sub));
+    }
+  }
+};
+
+#ifndef LLCOLL_TWOSHOT_WAVES_PER_EU
+#define LLCOLL_TWOSHOT_WAVES_PER_EU 1
+#endif
+
+template <class Pr, int DT, int P>
+__global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(LLCOLL_TWOSHOT_WAVES_PER_EU))) void k_twoshot(
+    KArgs a) {
   stamp_start(a);
   const Part pt = part_of_block<P>();
-  const int r = pt.r;
+  TwoShot<Pr, DT, P> t{a};
+  t.r = pt.r;
   constexpr int E = Elem<DT>::kBytes;
-  const uint64_t deadline = now_ticks() + a.timeout;
-  char *const slice_r = a.sym + (uint64_t)r * a.stride;
-  const int64_t n = a.n;
-  const int64_t C = a.chunk;
-  const int64_t units = Pr::units((C * E + 3) / 4);
-  char *const out_r = a.out + (uint64_t)r * (uint64_t)n * E;
-  const uint64_t ag_area = a.area + (uint64_t)(P - 1) * a.slot;
-  const bool publish = (r != a.mute);
-  const bool al4 = a.al4 != 0;
-
+  t.deadline = now_ticks() + a.timeout;
+  t.slice_r = a.sym + (uint64_t)t.r * a.stride;
+  t.n = a.n;
+  t.C = a.chunk;
+  t.out_r = a.out + (uint64_t)t.r * (uint64_t)t.n * E;
+  t.ag_area = a.area + (uint64_t)(P - 1) * a.slot;
+  t.publish = (t.r != a.mute);
+  t.al4 = a.al4 != 0;
+  const int64_t units = Pr::units((t.C * E + 3) / 4);
   const int64_t g = (int64_t)pt.w * blockDim.x + threadIdx.x;
   const int sub = (int)(g % Pr::kLanes);
   const int64_t u0 = g / Pr::kLanes;
   const int64_t ustep = (int64_t)pt.W * blockDim.x / Pr::kLanes;
-
-  // phase 1: scatter the other ranks' chunks to their owners
-  if (publish) {
-    for (int64_t u = u0; u < units; u += ustep) {
-      const int64_t w0 = Pr::word0(u, sub);
-      const int cnt = Pr::count(sub);
-      const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
-      u32x4 v[P];
-#pragma unroll
-      for (int k = 1; k < P; ++k) {
-        const int c = (r + k) % P;
-        const int64_t nc = n - c * C < C ? (n - c * C > 0 ? n - c * C : 0) : C;
-        v[k] = load_words<DT>(slice_r + c * C * E, w0, cnt, nc, true);
-      }
-#pragma unroll
-      for (int k = 1; k < P; ++k) {
-        const int c = (r + k) % P;
-        char *dst = a.sym + (uint64_t)c * a.stride + a.area + (uint64_t)slot_of(r, c) * a.slot;
-        st_pkt(make_rsrc(dst, (uint32_t)a.slot), off, Pr::pack(v[k], a.epoch, sub));
-      }
-    }
-  }
-
-  // phase 2: reduce the own chunk and publish it to every peer
-  {
-    const int64_t nr = n - r * C < C ? (n - r * C > 0 ? n - r * C : 0) : C;
-    for (int64_t u = u0; u < units; u += ustep) {
-      const int64_t w0 = Pr::word0(u, sub);
-      const int cnt = Pr::count(sub);
-      const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
-      const u32x4 own = load_words<DT>(slice_r + r * C * E, w0, cnt, nr, true);
-      u32x4 got[P];
-      poll_all<Pr, P>(slice_r + a.area, a.slot, off, r, a.epoch, deadline, got);
-#pragma unroll
-      for (int q = 0; q < P; ++q) got[q] = Pr::unpack(got[q], sub);
-      const u32x4 res = reduce_ordered<Pr, DT, P>(got, own, r);
-      store_words<DT>(out_r + r * C * E, w0, cnt, nr, al4, res);
-      if (publish) bcast<P>(a, ag_area, r, off, Pr::pack(res, a.epoch, sub));
-    }
-  }
-
-  // phase 3: gather every other reduced chunk
-  {
-    for (int64_t u = u0; u < units; u += ustep) {
-      const int64_t w0 = Pr::word0(u, sub);
-      const int cnt = Pr::count(sub);
-      const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
-      u32x4 got[P];
-      poll_all<Pr, P>(slice_r + ag_area, a.slot, off, r, a.epoch, deadline, got);
-#pragma unroll
-      for (int q = 0; q < P; ++q) {
-        if (q == r) continue;
-        const int64_t nq = n - q * C < C ? (n - q * C > 0 ? n - q * C : 0) : C;
-        store_words<DT>(out_r + q * C * E, w0, cnt, nq, al4, Pr::unpack(got[q], sub));
-      }
-    }
+  const int64_t steps = u0 < units ? (units - u0 + ustep - 1) / ustep : 0;
+  const int64_t lag = a.lag > 0 ? a.lag : 1;
+  for (int64_t s = 0; s < steps + 2 * lag; ++s) {
+    if (s < steps && t.publish) t.step_publish(u0 + s * ustep, sub);
+    if (s >= lag && s - lag < steps) t.step_reduce(u0 + (s - lag) * ustep, sub);
+    if (s >= 2 * lag && s - 2 * lag < steps) t.step_gather(u0 + (s - 2 * lag) * ustep, sub);
   }
   stamp_end(a);
 }
@@ -427,14 +447,12 @@ __global__ __launch_bounds__(1024) void k_reduce_scatter(KArgs a) {
 
   if (publish) {
     for (int64_t u = u0; u < units; u += ustep) {
-      const int64_t w0 = Pr::word0(u, sub);
-      const int cnt = Pr::count(sub);
       const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
       u32x4 v[P];
 #pragma unroll
       for (int k = 1; k < P; ++k) {
         const int c = (r + k) % P;
-        v[k] = load_words<DT>(slice_r + c * m * E, w0, cnt, m, al4);
+        v[k] = Pr::template load<DT>(slice_r + c * m * E, u, sub, m, al4);
       }
 #pragma unroll
       for (int k = 1; k < P; ++k) {
@@ -447,16 +465,14 @@ __global__ __launch_bounds__(1024) void k_reduce_scatter(KArgs a) {
 
   char *const out_r = a.out + (uint64_t)r * (uint64_t)m * E;
   for (int64_t u = u0; u < units; u += ustep) {
-    const int64_t w0 = Pr::word0(u, sub);
-    const int cnt = Pr::count(sub);
     const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
-    const u32x4 own = load_words<DT>(slice_r + r * m * E, w0, cnt, m, al4);
+    const u32x4 own = Pr::template load<DT>(slice_r + r * m * E, u, sub, m, al4);
     u32x4 got[P];
     poll_all<Pr, P>(slice_r + a.area, a.slot, off, r, a.epoch, deadline, got);
 #pragma unroll
     for (int q = 0; q < P; ++q) got[q] = Pr::unpack(got[q], sub);
     const u32x4 res = reduce_ordered<Pr, DT, P>(got, own, r);
-    store_words<DT>(out_r, w0, cnt, m, al4, res);
+    Pr::template store<DT>(out_r, u, sub, m, al4, res);
   }
   stamp_end(a);
 }
@@ -483,18 +499,16 @@ __global__ __launch_bounds__(1024) void k_allgather(KArgs a) {
   const int64_t ustep = (int64_t)pt.W * blockDim.x / Pr::kLanes;
 
   for (int64_t u = g / Pr::kLanes; u < units; u += ustep) {
-    const int64_t w0 = Pr::word0(u, sub);
-    const int cnt = Pr::count(sub);
     const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
-    const u32x4 own = load_words<DT>(slice_r, w0, cnt, s, true);
+    const u32x4 own = Pr::template load<DT>(slice_r, u, sub, s, true);
     if (publish) bcast<P>(a, a.area, r, off, Pr::pack(own, a.epoch, sub));
-    store_words<DT>(out_r + r * s * E, w0, cnt, s, al4, own);
+    Pr::template store<DT>(out_r + r * s * E, u, sub, s, al4, own);
     u32x4 got[P];
     poll_all<Pr, P>(slice_r + a.area, a.slot, off, r, a.epoch, deadline, got);
 #pragma unroll
     for (int q = 0; q < P; ++q) {
       if (q == r) continue;
-      store_words<DT>(out_r + q * s * E, w0, cnt, s, al4, Pr::unpack(got[q], sub));
+      Pr::template store<DT>(out_r + q * s * E, u, sub, s, al4, Pr::unpack(got[q], sub));
     }
   }
   stamp_end(a);

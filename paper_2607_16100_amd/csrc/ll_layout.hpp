@@ -35,7 +35,8 @@ inline uint64_t ceil_div(uint64_t x, uint64_t m) { return (x + m - 1) / m; }
 
 // Slot bytes for a payload of `bytes`.
 inline uint64_t slot8(uint64_t bytes) { return roundup(ceil_div(bytes, 4) * 8, kAlign); }
-inline uint64_t slot128(uint64_t bytes) { return roundup(ceil_div(ceil_div(bytes, 4), 30) * 128, kAlign); }
+// Line packets travel in 1 KiB units (a wave of 8 lines) carrying 240 payload words.
+inline uint64_t slot128(uint64_t bytes) { return roundup(ceil_div(ceil_div(bytes, 4), 240) * 1024, kAlign); }
 
 // Two-shot chunk length in elements: ceil(n / P) rounded up to 16 bytes.
 inline uint64_t twoshot_chunk(uint64_t n, int P, int esize) {

@@ -33,6 +33,7 @@ std::atomic<int> g_mute{-1};
 std::atomic<int> g_first_wait{0};
 std::atomic<int> g_poll_gap{0};
 std::atomic<int> g_wave_units{0};  // 0 = automatic, else 1, 2 or 4
+std::atomic<int> g_lag{1};
 std::atomic<uint64_t *> g_stamps{nullptr};
 std::atomic<uint64_t *> g_phases{nullptr};
 std::atomic<int> g_last_grid{0};
@@ -219,6 +220,7 @@ int launch(const Plan &pl, void *stream) {
   a.mute = g_mute.load();
   a.first_wait = (uint16_t)g_first_wait.load();
   a.poll_gap = (uint16_t)g_poll_gap.load();
+  a.lag = (uint32_t)g_lag.load();
   a.stamps = g_stamps.exchange(nullptr);
   a.phases = g_phases.exchange(nullptr);
   hipLaunchKernelGGL(fn, dim3(grid), dim3(threads), 0, (hipStream_t)stream, a);
@@ -510,6 +512,12 @@ int ll_set_poll_pacing(int first_wait, int poll_gap) {
   if (first_wait < 0 || first_wait > 1000 || poll_gap < 0 || poll_gap > 1000) return LL_ERR_INVALID;
   g_first_wait.store(first_wait);
   g_poll_gap.store(poll_gap);
+  return LL_OK;
+}
+
+int ll_set_pipeline_lag(int lag) {
+  if (lag < 1 || lag > 64) return LL_ERR_INVALID;
+  g_lag.store(lag);
   return LL_OK;
 }
 

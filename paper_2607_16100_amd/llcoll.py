@@ -11,7 +11,9 @@ import ctypes
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libllcoll.so")
+# LLCOLL_LIBRARY may name another build of the same library (e.g. one built
+# with different compile-time options); by default the in-tree build is used.
+LIB_PATH = os.environ.get("LLCOLL_LIBRARY") or os.path.join(_HERE, "libllcoll.so")
 
 LL_F32, LL_BF16 = 0, 1
 LL_SUM = 0
@@ -51,6 +53,7 @@ _SIGS = {
     "ll_strerror": (ctypes.c_char_p, [_i]),
     "ll_set_launch": (_i, [_i, _i]),
     "ll_set_poll_pacing": (_i, [_i, _i]),
+    "ll_set_pipeline_lag": (_i, [_i]),
     "ll_set_wave_units": (_i, [_i]),
     "ll_set_poll_timeout": (_i, [_u64]),
     "ll_debug_mute_rank": (_i, [_i]),
@@ -166,6 +169,10 @@ def ll_set_launch(workgroups_per_rank: int, threads: int):
 
 def ll_set_poll_pacing(first_wait: int, poll_gap: int):
     return _lib.ll_set_poll_pacing(first_wait, poll_gap)
+
+
+def ll_set_pipeline_lag(lag: int):
+    return _lib.ll_set_pipeline_lag(lag)
 
 
 def ll_set_wave_units(units_per_lane: int):
