@@ -46,9 +46,10 @@ def log(msg: str) -> None:
 
 
 def kernel_source_hash() -> str:
+    """Hash of the device code (kernels, primitives, slot layout)."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2607_16100_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
+    for name in ("ll_device.hpp", "ll_kernels.hpp", "ll_layout.hpp"):
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(name.encode())
             h.update(f.read())
@@ -183,6 +184,95 @@ def bench_floor(torch, ll, steps, warmup, grid, threads):
     return out
 
 
+def paced_collective(torch, ll, reg, kind, count, code, steps, warmup):
+    """p50/p99 call-to-call interval (GPU-paced) of one collective on a region.
+    kind: "ar" (count elements, code = ll_algo), "rs" (recvcount, code =
+    ll_proto), "ag" (sendcount, code = ll_proto)."""
+    s = reg.stream_handle()
+    fn = {"ar": ll.ll_bench_allreduce, "rs": ll.ll_bench_reduce_scatter, "ag": ll.ll_bench_allgather}[kind]
+
+    def queue(first, cnt, stamps_ptr, stride):
+        e = reg.epoch + 1
+        ll.check(fn(reg.base, reg.rank_stride, reg.out_ptr, count, reg.dt, reg.nranks, e, cnt, code, stamps_ptr,
+                    stride, s), kind)
+        reg.epoch += cnt
+
+    queue(0, warmup, 0, 0)
+    torch.cuda.synchronize()
+    grid, threads = ll.ll_last_grid()
+    iv, sp = gpu_paced(torch, ll, queue, steps, grid)
+    ll.check(ll.ll_check(s), kind)
+    return {"p50_us": pct(iv, 50), "p99_us": pct(iv, 99), "span_p50_us": pct(sp, 50), "grid": grid,
+            "threads": threads}
+
+
+def bench_c3(torch, ll, steps):
+    """1 MiB per rank (batch 64 x hidden 8192 bf16, 8 ranks): two-shot against one-shot."""
+    from paper_2607_16100_amd import workloads as wl
+    from paper_2607_16100_amd.region import SymRegion
+
+    p, n = 8, 64 * 8192
+    reg = SymRegion(p, n, "bf16")
+    reg.init()
+    reg.write_inputs(wl.normal(p, n, "bf16", sigma=0.5, seed=0))
+    out = {}
+    for algo in ("twoshot", "twoshot_line", "oneshot", "oneshot_line", "auto"):
+        out[algo] = paced_collective(torch, ll, reg, "ar", n, ll.ALGOS[algo], steps, 20)
+    return out
+
+
+def bench_c5(torch, ll, steps):
+    """Stand-alone ReduceScatter and AllGather, bf16, hidden 7168 x batch {1, 16, 256}, 8 and 4 ranks."""
+    from paper_2607_16100_amd import workloads as wl
+    from paper_2607_16100_amd.region import SymRegion
+
+    out = {}
+    for p in (8, 4):
+        for b in (1, 16, 256):
+            total = 7168 * b
+            m = total // p
+            reg = SymRegion(p, total, "bf16", out_elems=p * total)
+            reg.init()
+            reg.write_inputs(wl.normal(p, total, "bf16", seed=0))
+            for proto in ("auto", "packet8", "line128"):
+                out[f"rs_p{p}_b{b}_{proto}"] = paced_collective(torch, ll, reg, "rs", m, ll.PROTOS[proto], steps, 20)
+                out[f"ag_p{p}_b{b}_{proto}"] = paced_collective(torch, ll, reg, "ag", m, ll.PROTOS[proto], steps, 20)
+            del reg
+    return out
+
+
+def bench_sweep(torch, ll, path):
+    """C4: 8 ranks, binary32, 2 .. 2^26 elements per rank; p50/p99 and GB/s of
+    every algorithm at every size (written to `path` as JSON lines)."""
+    from paper_2607_16100_amd import bytemodel
+    from paper_2607_16100_amd.region import SymRegion
+
+    p = 8
+    big = 1 << 26
+    reg = SymRegion(p, big, "f32", out_elems=p * big)
+    reg.init()
+    g = torch.Generator(device="cuda")
+    g.manual_seed(0)
+    rows = torch.rand((p, big), generator=g, device="cuda", dtype=torch.float32) * 2 - 1
+    reg.write_inputs_device(rows.view(torch.uint8).view(p, big * 4))
+    del rows
+    with open(path, "w") as f:
+        for k in range(1, 27):
+            n = 1 << k
+            steps = 2000 if n * 4 <= (1 << 20) else (200 if n * 4 <= (16 << 20) else 20)
+            for algo in ("auto", "oneshot_waves", "oneshot", "oneshot_line", "twoshot", "twoshot_line"):
+                if algo == "oneshot_waves" and n * 4 > (1 << 20):
+                    continue
+                r = paced_collective(torch, ll, reg, "ar", n, ll.ALGOS[algo], steps, min(20, steps))
+                r.update({"elements": n, "bytes_per_rank": n * 4, "algo": algo,
+                          "algorithmic_gbps_p50": bytemodel.allreduce_bytes(algo if algo != "auto" else "twoshot_line", p, n, 4)
+                          / r["p50_us"] / 1e3 if algo != "auto" else None})
+                f.write(json.dumps(r) + "\n")
+                f.flush()
+                log(f"sweep n={n} {algo} p50={r['p50_us']:.2f}")
+    return path
+
+
 def bench_sol_pieces(torch, ll):
     """The paper's speed-of-light pieces (Sec. VI) measured on one chip."""
     s = torch.cuda.current_stream().cuda_stream
@@ -290,10 +380,11 @@ def bench_cpu_baseline(seconds: float):
                       f"by the single-threaded C oracle; median per call"}
 
 
-def traffic_from_profiles(kernel_hash: str):
-    """HBM bytes per launch from the committed counter summary, if it was taken
-    from the current kernel sources."""
-    path = os.path.join(ROOT, "profiles", "twoshot_line_f32_64MiB_p8_counters.json")
+def traffic_from_profiles(kernel_hash: str, grid_threads: int):
+    """HBM bytes per launch from the committed counter summary (rocprofv3
+    FETCH_SIZE and WRITE_SIZE, scaled by what they read for a 1 GiB copy), if
+    it was taken from the current device code with the same launch grid."""
+    path = os.path.join(ROOT, "profiles", "twoshot_line_f32_64MiB_p8_counters.txt")
     if not os.path.exists(path):
         return None
     try:
@@ -301,7 +392,7 @@ def traffic_from_profiles(kernel_hash: str):
             d = json.load(f)
     except (OSError, ValueError):
         return None
-    if d.get("kernel_source_hash") != kernel_hash:
+    if d.get("kernel_source_hash") != kernel_hash or d.get("grid_size_threads") != grid_threads:
         return None
     return d.get("hbm_bytes_per_launch")
 
@@ -313,7 +404,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--bw-iters", type=int, default=20)
-    ap.add_argument("--only", default="", help="comma list of sections: headline,floor,sol,bw,copy,cpu")
+    ap.add_argument("--only", default="", help="comma list of sections: headline,floor,sol,bw,c3,c5,copy,cpu")
+    ap.add_argument("--sweep", default="", help="also run the full C4 size sweep, writing JSON lines to this file")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs its P virtual ranks on one GPU; --gpus {args.gpus} is not supported "
@@ -352,6 +444,17 @@ def main():
         result["bw"] = bench_bandwidth(torch, ll, 16 << 20, ["twoshot_line", "twoshot", "oneshot_line", "oneshot"],
                                        iters=args.bw_iters)
         log(json.dumps(result["bw"]))
+    if want("c3"):
+        log("C3: 1 MiB bf16, two-shot vs one-shot")
+        result["c3"] = bench_c3(torch, ll, min(args.steps, 2000))
+        log(json.dumps(result["c3"]))
+    if want("c5"):
+        log("C5: reduce-scatter / all-gather")
+        result["c5"] = bench_c5(torch, ll, min(args.steps, 1000))
+        log(json.dumps(result["c5"]))
+    if args.sweep:
+        log("C4 sweep")
+        result["sweep_file"] = bench_sweep(torch, ll, args.sweep)
     if want("copy"):
         log("device copy reference")
         result["copy"] = bench_copy(torch)
@@ -368,7 +471,8 @@ def main():
     roofline = None
     if bw:
         roofline = {"bound": "hbm", "achieved": round(bw["gbps"], 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                    "frac": round(bw["gbps"] / PEAK_HBM_GBS, 4), "traffic": traffic_from_profiles(khash),
+                    "frac": round(bw["gbps"] / PEAK_HBM_GBS, 4),
+                    "traffic": traffic_from_profiles(khash, bw["grid"] * bw["threads"]),
                     "kernel": "k_twoshot<ProtoLine, f32, 8> (64 MiB per rank)",
                     "kernel_us": round(bw["kernel_us"], 2), "algorithmic_bytes": bw["algorithmic_bytes"]}
     line = {

@@ -182,12 +182,16 @@ int ll_debug_mute_rank(int rank);
  * stamps[b] and stamps[grid + b].  The pointer is used for one launch only. */
 int ll_debug_stamp_next(uint64_t *stamps);
 
-/* Diagnostics hook: when `phases` (device memory, 4*grid words) is non-NULL,
- * the next one-shot launch records for thread 0 of each workgroup b and its
- * last packet unit: phases[4b] = time its input load returned, phases[4b+1] =
- * time its packet stores were acknowledged (the kernel waits for them only in
- * this mode), phases[4b+2] = time its wait for peers ended, phases[4b+3] =
- * number of polls it issued.  Used for one launch only. */
+/* Diagnostics hook: when `phases` (device memory) is non-NULL, the next
+ * one-shot launch records phase times.  LL_ALGO_ONESHOT (4*grid words): for
+ * thread 0 of each workgroup b and its last packet unit, phases[4b] = time
+ * its input load returned, phases[4b+1] = time its packet stores were
+ * acknowledged (the kernel waits for them only in this mode), phases[4b+2] =
+ * time its wait for peers ended, phases[4b+3] = number of polls it issued.
+ * LL_ALGO_ONESHOT_WAVES (4*grid*nranks words): for lane 0 of wave w of
+ * workgroup b and its first tile, phases[4(b*nranks+w)] = time its input
+ * load returned, [..+1] = time its peer's packets had all arrived, [..+2] =
+ * time it left the workgroup barrier.  Used for one launch only. */
 int ll_debug_phase_next(uint64_t *phases);
 
 /* Grid (total workgroups) of the last launch. */

@@ -69,11 +69,19 @@ int ll_probe_spin(uint64_t ticks, void *stream);
  * epochs first_epoch .. first_epoch+calls-1.  If stamps != NULL, call i writes
  * its per-workgroup start/end times at stamps + i*stamp_stride (see
  * ll_debug_stamp_next; stamp_stride >= 2*grid).
+ * ll_bench_reduce_scatter / ll_bench_allgather: the same for the stand-alone
+ * collectives (proto as ll_proto).
  * ll_bench_floor: `calls` floor kernels; call i loads line
  * (first_line + i*line_step) mod (chase_len/16) of `chase` (16 words a line).
  * ll_bench_empty: `calls` empty kernels. */
 int ll_bench_allreduce(void *sym_base, size_t rank_stride, void *out, size_t count, int dt, int nranks,
                        uint32_t first_epoch, int calls, int algo, uint64_t *stamps, int stamp_stride,
+                       void *stream);
+int ll_bench_reduce_scatter(void *sym_base, size_t rank_stride, void *out, size_t recvcount, int dt, int nranks,
+                            uint32_t first_epoch, int calls, int proto, uint64_t *stamps, int stamp_stride,
+                            void *stream);
+int ll_bench_allgather(void *sym_base, size_t rank_stride, void *out, size_t sendcount, int dt, int nranks,
+                       uint32_t first_epoch, int calls, int proto, uint64_t *stamps, int stamp_stride,
                        void *stream);
 int ll_bench_floor(const uint64_t *chase, uint64_t chase_len, uint64_t first_line, uint64_t line_step,
                    uint64_t *sink, int grid, int threads, int calls, uint64_t *stamps, int stamp_stride,

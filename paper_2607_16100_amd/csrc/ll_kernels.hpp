@@ -218,6 +218,20 @@ __global__ __launch_bounds__(1024) void k_oneshot(KArgs a) {
 // wave's poll never waits for more than its own U stores (the memory counter
 // covers stores and loads alike on this chip) and a poll is U loads, not
 // U*(P-1).
+// Workgroup barrier that makes LDS writes visible but does not wait for the
+// wave's outstanding global stores (packet stores need not be acknowledged
+// before the workgroup goes on).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0); vmcnt and expcnt left alone
+  __builtin_amdgcn_s_barrier();
+}
+
+// 0: every peer wave sends its own store and then polls (measured faster on
+// MI355X); 1: the own-rank wave sends to all peers and the peer waves only poll.
+#ifndef LLCOLL_WAVES_SPLIT
+#define LLCOLL_WAVES_SPLIT 0
+#endif
+
 template <int DT, int P, int U>
 __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs a) {
   stamp_start(a);
@@ -242,28 +256,53 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs a) {
   char *const dst = a.sym + (uint64_t)q * a.stride + a.area + (uint64_t)slot_of(r, q) * a.slot;
   char *const src = slice_r + a.area + (uint64_t)slot_of(q, r) * a.slot;
 
+  // Stage a wave's U units (payload words) in its LDS row, widened to binary32.
+  auto stage_row = [&](const u32x4 *w) {
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      float f[EPU];
+      Elem<DT>::widen(w[k].x, f);
+      Elem<DT>::widen(w[k].y, f + K);
+#pragma unroll
+      for (int e = 0; e < EPU; ++e) stage[q][(k * 64 + lane) * EPU + e] = f[e];
+    }
+  };
+
   for (int64_t tile = pt.w; tile < tiles; tile += pt.W) {
-    u32x4 v[U];
     u32x4 own[U];
 #pragma unroll
     for (int k = 0; k < U; ++k) {
       const int64_t u = tile * 64 * U + k * 64 + lane;
-      v[k] = u32x4{0u, 0u, 0u, 0u};
       own[k] = u < units ? load_words<DT>(slice_r, 2 * u, 2, n, true) : u32x4{0u, 0u, 0u, 0u};
     }
+    if (a.phases != nullptr && lane == 0 && tile == pt.w) {
+      a.phases[4 * (blockIdx.x * P + wv) + 0] = now_ticks() + (own[0].x & 0u);
+    }
     if (q == r) {
+      // the own values; with LLCOLL_WAVES_SPLIT this wave also sends the tile
+      // to every peer, so the polling waves have no stores of their own to
+      // wait for (the memory counter covers stores and loads alike)
+      stage_row(own);
+      if (LLCOLL_WAVES_SPLIT && publish) {
 #pragma unroll
-      for (int k = 0; k < U; ++k) v[k] = own[k];
+        for (int k = 0; k < U; ++k) {
+          const int64_t u = tile * 64 * U + k * 64 + lane;
+          if (u < units) bcast<P>(a, a.area, r, (uint32_t)(u * ProtoLL::kUnitBytes), ProtoLL::pack(own[k], a.epoch, 0));
+        }
+      }
+      if (a.phases != nullptr && lane == 0 && tile == pt.w) a.phases[4 * (blockIdx.x * P + wv) + 1] = now_ticks();
     } else {
+      u32x4 v[U];
       const rsrc_t rd = make_rsrc(dst, (uint32_t)a.slot);
       const rsrc_t rs = make_rsrc(src, (uint32_t)a.slot);
       uint32_t pend = 0;
 #pragma unroll
       for (int k = 0; k < U; ++k) {
         const int64_t u = tile * 64 * U + k * 64 + lane;
+        v[k] = u32x4{0u, 0u, 0u, 0u};
         if (u < units) {
           pend |= 1u << k;
-          if (publish) st_pkt(rd, (uint32_t)(u * ProtoLL::kUnitBytes), ProtoLL::pack(own[k], a.epoch, 0));
+          if (!LLCOLL_WAVES_SPLIT && publish) st_pkt(rd, (uint32_t)(u * ProtoLL::kUnitBytes), ProtoLL::pack(own[k], a.epoch, 0));
         }
       }
       int spins = 1;
@@ -287,16 +326,13 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs a) {
           break;
         }
       }
+      if (a.phases != nullptr && lane == 0 && tile == pt.w) {
+        a.phases[4 * (blockIdx.x * P + wv) + 1] = now_ticks() + (v[0].x & 0u);
+      }
+      stage_row(v);
     }
-#pragma unroll
-    for (int k = 0; k < U; ++k) {
-      float f[EPU];
-      Elem<DT>::widen(v[k].x, f);
-      Elem<DT>::widen(v[k].y, f + K);
-#pragma unroll
-      for (int e = 0; e < EPU; ++e) stage[q][(k * 64 + lane) * EPU + e] = f[e];
-    }
-    __syncthreads();
+    lds_barrier();
+    if (a.phases != nullptr && lane == 0 && tile == pt.w) a.phases[4 * (blockIdx.x * P + wv) + 2] = now_ticks();
     for (int j = (int)threadIdx.x; j < TW; j += (int)blockDim.x) {
       float acc[K];
 #pragma unroll
@@ -309,7 +345,7 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs a) {
       const u32x4 res = {Elem<DT>::narrow(acc), 0u, 0u, 0u};
       store_words<DT>(out_r, tile * TW + j, 1, n, a.al4 != 0, res);
     }
-    __syncthreads();
+    lds_barrier();  // the next tile overwrites the staging rows
   }
   stamp_end(a);
 }
@@ -426,8 +462,10 @@ __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(LLCOLL_TWO
 
 // ---------------------------------------------------------------------------
 // Stand-alone ReduceScatter: rank r's input is P chunks of m = a.n elements;
-// chunk c goes to slot (c <- r); rank r reduces chunk r.  Same two steps as
-// phases 1-2 of the two-shot kernel, with chunks of exactly m elements.
+// chunk c goes to slot (c <- r); rank r reduces chunk r.  The same two steps
+// as the first two of the two-shot kernel, with chunks of exactly m
+// elements, software-pipelined the same way (publish unit s, reduce unit
+// s - lag).
 template <class Pr, int DT, int P>
 __global__ __launch_bounds__(1024) void k_reduce_scatter(KArgs a) {
   stamp_start(a);
@@ -436,6 +474,7 @@ __global__ __launch_bounds__(1024) void k_reduce_scatter(KArgs a) {
   constexpr int E = Elem<DT>::kBytes;
   const uint64_t deadline = now_ticks() + a.timeout;
   char *const slice_r = a.sym + (uint64_t)r * a.stride;
+  char *const out_r = a.out + (uint64_t)r * (uint64_t)a.n * E;
   const int64_t m = a.n;
   const int64_t units = Pr::units((m * E + 3) / 4);
   const bool al4 = a.al4 != 0;
@@ -444,9 +483,12 @@ __global__ __launch_bounds__(1024) void k_reduce_scatter(KArgs a) {
   const int sub = (int)(g % Pr::kLanes);
   const int64_t u0 = g / Pr::kLanes;
   const int64_t ustep = (int64_t)pt.W * blockDim.x / Pr::kLanes;
+  const int64_t steps = u0 < units ? (units - u0 + ustep - 1) / ustep : 0;
+  const int64_t lag = a.lag > 0 ? a.lag : 1;
 
-  if (publish) {
-    for (int64_t u = u0; u < units; u += ustep) {
+  for (int64_t s = 0; s < steps + lag; ++s) {
+    if (s < steps && publish) {
+      const int64_t u = u0 + s * ustep;
       const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
       u32x4 v[P];
 #pragma unroll
@@ -461,18 +503,17 @@ __global__ __launch_bounds__(1024) void k_reduce_scatter(KArgs a) {
         st_pkt(make_rsrc(dst, (uint32_t)a.slot), off, Pr::pack(v[k], a.epoch, sub));
       }
     }
-  }
-
-  char *const out_r = a.out + (uint64_t)r * (uint64_t)m * E;
-  for (int64_t u = u0; u < units; u += ustep) {
-    const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
-    const u32x4 own = Pr::template load<DT>(slice_r + r * m * E, u, sub, m, al4);
-    u32x4 got[P];
-    poll_all<Pr, P>(slice_r + a.area, a.slot, off, r, a.epoch, deadline, got);
+    if (s >= lag && s - lag < steps) {
+      const int64_t u = u0 + (s - lag) * ustep;
+      const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+      const u32x4 own = Pr::template load<DT>(slice_r + r * m * E, u, sub, m, al4);
+      u32x4 got[P];
+      poll_all<Pr, P>(slice_r + a.area, a.slot, off, r, a.epoch, deadline, got);
 #pragma unroll
-    for (int q = 0; q < P; ++q) got[q] = Pr::unpack(got[q], sub);
-    const u32x4 res = reduce_ordered<Pr, DT, P>(got, own, r);
-    Pr::template store<DT>(out_r, u, sub, m, al4, res);
+      for (int q = 0; q < P; ++q) got[q] = Pr::unpack(got[q], sub);
+      const u32x4 res = reduce_ordered<Pr, DT, P>(got, own, r);
+      Pr::template store<DT>(out_r, u, sub, m, al4, res);
+    }
   }
   stamp_end(a);
 }
@@ -480,7 +521,8 @@ __global__ __launch_bounds__(1024) void k_reduce_scatter(KArgs a) {
 // ---------------------------------------------------------------------------
 // Stand-alone AllGather: rank r sends its s = a.n input elements to slot
 // (q <- r) of every peer, copies them to its own output, and stores what it
-// receives from peer q at block q of its output.
+// receives from peer q at block q of its output.  Pipelined like the others:
+// publish unit s, gather unit s - lag.
 template <class Pr, int DT, int P>
 __global__ __launch_bounds__(1024) void k_allgather(KArgs a) {
   stamp_start(a);
@@ -489,26 +531,36 @@ __global__ __launch_bounds__(1024) void k_allgather(KArgs a) {
   constexpr int E = Elem<DT>::kBytes;
   const uint64_t deadline = now_ticks() + a.timeout;
   char *const slice_r = a.sym + (uint64_t)r * a.stride;
-  const int64_t s = a.n;
-  const int64_t units = Pr::units((s * E + 3) / 4);
+  const int64_t n = a.n;
+  const int64_t units = Pr::units((n * E + 3) / 4);
   const bool al4 = a.al4 != 0;
-  char *const out_r = a.out + (uint64_t)r * (uint64_t)P * s * E;
+  char *const out_r = a.out + (uint64_t)r * (uint64_t)P * n * E;
   const bool publish = (r != a.mute);
   const int64_t g = (int64_t)pt.w * blockDim.x + threadIdx.x;
   const int sub = (int)(g % Pr::kLanes);
+  const int64_t u0 = g / Pr::kLanes;
   const int64_t ustep = (int64_t)pt.W * blockDim.x / Pr::kLanes;
+  const int64_t steps = u0 < units ? (units - u0 + ustep - 1) / ustep : 0;
+  const int64_t lag = a.lag > 0 ? a.lag : 1;
 
-  for (int64_t u = g / Pr::kLanes; u < units; u += ustep) {
-    const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
-    const u32x4 own = Pr::template load<DT>(slice_r, u, sub, s, true);
-    if (publish) bcast<P>(a, a.area, r, off, Pr::pack(own, a.epoch, sub));
-    Pr::template store<DT>(out_r + r * s * E, u, sub, s, al4, own);
-    u32x4 got[P];
-    poll_all<Pr, P>(slice_r + a.area, a.slot, off, r, a.epoch, deadline, got);
+  for (int64_t s = 0; s < steps + lag; ++s) {
+    if (s < steps) {
+      const int64_t u = u0 + s * ustep;
+      const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+      const u32x4 own = Pr::template load<DT>(slice_r, u, sub, n, true);
+      if (publish) bcast<P>(a, a.area, r, off, Pr::pack(own, a.epoch, sub));
+      Pr::template store<DT>(out_r + r * n * E, u, sub, n, al4, own);
+    }
+    if (s >= lag && s - lag < steps) {
+      const int64_t u = u0 + (s - lag) * ustep;
+      const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+      u32x4 got[P];
+      poll_all<Pr, P>(slice_r + a.area, a.slot, off, r, a.epoch, deadline, got);
 #pragma unroll
-    for (int q = 0; q < P; ++q) {
-      if (q == r) continue;
-      Pr::template store<DT>(out_r + q * s * E, u, sub, s, al4, Pr::unpack(got[q], sub));
+      for (int q = 0; q < P; ++q) {
+        if (q == r) continue;
+        Pr::template store<DT>(out_r + q * n * E, u, sub, n, al4, Pr::unpack(got[q], sub));
+      }
     }
   }
   stamp_end(a);

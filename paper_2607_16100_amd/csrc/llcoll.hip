@@ -262,17 +262,30 @@ KArgs base_args(void *sym_base, size_t rank_stride, void *out, uint32_t epoch) {
   return a;
 }
 
-// Size thresholds measured on MI355X with 8 ranks (latency of back-to-back
-// calls per algorithm and message size).
+// Size thresholds measured on MI355X (mean time of back-to-back calls for
+// every algorithm at 32 KiB .. 8 MiB per rank, P = 2, 4, 8, binary32 and
+// bfloat16); M = input bytes per rank.
 ll_algo auto_algo(uint64_t in_bytes, int P) {
-  (void)P;
-  if (in_bytes <= (32u << 10)) return LL_ALGO_ONESHOT_WAVES;
-  if (in_bytes <= (128u << 10)) return LL_ALGO_ONESHOT_LINE;
-  if (in_bytes <= (1u << 20)) return LL_ALGO_TWOSHOT;
+  const uint64_t KiB = 1024, MiB = 1024 * 1024;
+  if (in_bytes <= 32 * KiB) return LL_ALGO_ONESHOT_WAVES;
+  if (P <= 2) {
+    if (in_bytes <= 128 * KiB) return LL_ALGO_ONESHOT;
+    if (in_bytes <= 4 * MiB) return LL_ALGO_ONESHOT_LINE;
+    return LL_ALGO_TWOSHOT_LINE;
+  }
+  if (P <= 4) {
+    if (in_bytes <= 512 * KiB) return LL_ALGO_ONESHOT_LINE;
+    return LL_ALGO_TWOSHOT_LINE;
+  }
+  if (in_bytes <= 128 * KiB) return LL_ALGO_ONESHOT_LINE;
+  if (in_bytes <= 512 * KiB) return LL_ALGO_TWOSHOT;
   return LL_ALGO_TWOSHOT_LINE;
 }
 
-ll_proto auto_proto(uint64_t in_bytes) { return in_bytes <= (64u << 10) ? LL_PROTO_PACKET8 : LL_PROTO_LINE128; }
+// ReduceScatter / AllGather: 8-byte packets up to 1 MiB of data per rank
+// (input for ReduceScatter, output for AllGather), lines above (measured on
+// the hidden 7168 x batch {1, 16, 256} shapes at 4 and 8 ranks).
+ll_proto auto_proto(uint64_t bytes) { return bytes <= (1u << 20) ? LL_PROTO_PACKET8 : LL_PROTO_LINE128; }
 
 }  // namespace
 
@@ -626,6 +639,42 @@ int ll_bench_allreduce(void *sym_base, size_t rank_stride, void *out, size_t cou
     if (stamps != nullptr) g_stamps.store(stamps + (size_t)i * (size_t)stamp_stride);
     const int st = ll_allreduce_algo(sym_base, rank_stride, out, count, (ll_dtype)dt, LL_SUM, nranks,
                                      first_epoch + (uint32_t)i, stream, (ll_algo)algo);
+    if (st != LL_OK) {
+      g_stamps.store(nullptr);
+      return st;
+    }
+  }
+  return LL_OK;
+}
+
+int ll_bench_reduce_scatter(void *sym_base, size_t rank_stride, void *out, size_t recvcount, int dt, int nranks,
+                            uint32_t first_epoch, int calls, int proto, uint64_t *stamps, int stamp_stride,
+                            void *stream) {
+  if (calls < 1 || first_epoch == 0 || (uint64_t)first_epoch + (uint64_t)calls - 1 > 0xFFFFFFFFull)
+    return LL_ERR_INVALID;
+  if (stamps != nullptr && stamp_stride < 1) return LL_ERR_INVALID;
+  for (int i = 0; i < calls; ++i) {
+    if (stamps != nullptr) g_stamps.store(stamps + (size_t)i * (size_t)stamp_stride);
+    const int st = ll_reduce_scatter_proto(sym_base, rank_stride, out, recvcount, (ll_dtype)dt, LL_SUM, nranks,
+                                           first_epoch + (uint32_t)i, stream, (ll_proto)proto);
+    if (st != LL_OK) {
+      g_stamps.store(nullptr);
+      return st;
+    }
+  }
+  return LL_OK;
+}
+
+int ll_bench_allgather(void *sym_base, size_t rank_stride, void *out, size_t sendcount, int dt, int nranks,
+                       uint32_t first_epoch, int calls, int proto, uint64_t *stamps, int stamp_stride,
+                       void *stream) {
+  if (calls < 1 || first_epoch == 0 || (uint64_t)first_epoch + (uint64_t)calls - 1 > 0xFFFFFFFFull)
+    return LL_ERR_INVALID;
+  if (stamps != nullptr && stamp_stride < 1) return LL_ERR_INVALID;
+  for (int i = 0; i < calls; ++i) {
+    if (stamps != nullptr) g_stamps.store(stamps + (size_t)i * (size_t)stamp_stride);
+    const int st = ll_allgather_proto(sym_base, rank_stride, out, sendcount, (ll_dtype)dt, nranks,
+                                      first_epoch + (uint32_t)i, stream, (ll_proto)proto);
     if (st != LL_OK) {
       g_stamps.store(nullptr);
       return st;

@@ -67,6 +67,8 @@ _SIGS = {
     "ll_probe_pingpong": (_i, [_vp, _i, _i, _i, _u64, _vp, _vp]),
     "ll_probe_spin": (_i, [_u64, _vp]),
     "ll_bench_allreduce": (_i, [_vp, _sz, _vp, _sz, _i, _i, _u32, _i, _i, _vp, _i, _vp]),
+    "ll_bench_reduce_scatter": (_i, [_vp, _sz, _vp, _sz, _i, _i, _u32, _i, _i, _vp, _i, _vp]),
+    "ll_bench_allgather": (_i, [_vp, _sz, _vp, _sz, _i, _i, _u32, _i, _i, _vp, _i, _vp]),
     "ll_bench_floor": (_i, [_vp, _u64, _u64, _u64, _vp, _i, _i, _i, _vp, _i, _vp]),
     "ll_bench_empty": (_i, [_i, _i, _i, _vp, _i, _vp]),
     "ll_probe_xcd": (_i, [_vp, _i, _i, _vp]),
@@ -229,6 +231,18 @@ def ll_bench_allreduce(sym_base, rank_stride, out, count, dt, nranks, first_epoc
                        stamp_stride, stream):
     return _lib.ll_bench_allreduce(sym_base, rank_stride, out, count, dt, nranks, first_epoch, calls, algo, stamps,
                                    stamp_stride, stream)
+
+
+def ll_bench_reduce_scatter(sym_base, rank_stride, out, recvcount, dt, nranks, first_epoch, calls, proto, stamps,
+                            stamp_stride, stream):
+    return _lib.ll_bench_reduce_scatter(sym_base, rank_stride, out, recvcount, dt, nranks, first_epoch, calls, proto,
+                                        stamps, stamp_stride, stream)
+
+
+def ll_bench_allgather(sym_base, rank_stride, out, sendcount, dt, nranks, first_epoch, calls, proto, stamps,
+                       stamp_stride, stream):
+    return _lib.ll_bench_allgather(sym_base, rank_stride, out, sendcount, dt, nranks, first_epoch, calls, proto,
+                                   stamps, stamp_stride, stream)
 
 
 def ll_bench_floor(chase, chase_len, first_line, line_step, sink, grid, threads, calls, stamps, stamp_stride,

@@ -259,6 +259,37 @@ def test_result_independent_of_launch_shape(algo):
     ll.ll_set_wave_units(0)
 
 
+@pytest.mark.parametrize("lag", [1, 2, 5])
+def test_result_independent_of_pipeline_lag(lag):
+    """Two-shot, ReduceScatter and AllGather give the same bits for every
+    pipeline distance (and launch shape), on sizes with many steps."""
+    p, n = 8, 300_000
+    x = wl.normal(p, n, "bf16", seed=13)
+    want = oracle.allreduce(x)
+    reg = SymRegion(p, n, "bf16", out_elems=p * n)
+    reg.init()
+    ll.ll_set_pipeline_lag(lag)
+    try:
+        for wg, threads in [(1, 64), (4, 256), (0, 0)]:
+            ll.ll_set_launch(wg, threads)
+            for algo in ("twoshot", "twoshot_line"):
+                say(f"lag={lag} {algo} wg={wg} t={threads}")
+                assert_bits_equal(run_allreduce(reg, x, algo), want, f"{algo} lag={lag} wg={wg}")
+            m = n // p
+            for proto in PROTOS:
+                reg.write_inputs(x)
+                check_ok(reg.reduce_scatter(m, proto), "rs")
+                rs = reg.read_out(p * m, np.uint16).reshape(p, m)
+                assert_bits_equal(rs, oracle.reduce_scatter(x), f"RS {proto} lag={lag}")
+                reg.write_inputs(rs)
+                check_ok(reg.allgather(m, proto), "ag")
+                ag = reg.read_out(p * p * m, np.uint16).reshape(p, p * m)
+                assert_bits_equal(ag, oracle.allgather(rs), f"AG {proto} lag={lag}")
+    finally:
+        ll.ll_set_pipeline_lag(1)
+        ll.ll_set_launch(0, 0)
+
+
 def test_large_epochs_and_reinit():
     """Epochs near the top of the 32-bit range, one per call, then ll_init and a
     restart at epoch 1."""
