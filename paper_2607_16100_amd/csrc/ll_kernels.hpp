@@ -306,6 +306,7 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs a) {
         }
       }
       int spins = 1;
+      idle64(a.first_wait);
       while (pend != 0) {
         compiler_fence();
         u32x4 pk[U];
