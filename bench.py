@@ -216,8 +216,14 @@ def bench_c3(torch, ll, steps):
     reg.init()
     reg.write_inputs(wl.normal(p, n, "bf16", sigma=0.5, seed=0))
     out = {}
-    for algo in ("twoshot", "twoshot_line", "oneshot", "oneshot_line", "auto"):
+    for algo in ("twoshot", "twoshot_line", "twoshot_sentinel", "twoshot_sentinel_out", "oneshot", "oneshot_line",
+                 "oneshot_sentinel", "auto"):
         out[algo] = paced_collective(torch, ll, reg, "ar", n, ll.ALGOS[algo], steps, 20)
+    ll.check(ll.ll_set_auto_sentinel(1), "auto sentinel")
+    try:
+        out["auto_sentinel_allowed"] = paced_collective(torch, ll, reg, "ar", n, ll.ALGOS["auto"], steps, 20)
+    finally:
+        ll.ll_set_auto_sentinel(0)
     return out
 
 
@@ -234,7 +240,7 @@ def bench_c5(torch, ll, steps):
             reg = SymRegion(p, total, "bf16", out_elems=p * total)
             reg.init()
             reg.write_inputs(wl.normal(p, total, "bf16", seed=0))
-            for proto in ("auto", "packet8", "line128"):
+            for proto in ("auto", "packet8", "line128", "sentinel"):
                 out[f"rs_p{p}_b{b}_{proto}"] = paced_collective(torch, ll, reg, "rs", m, ll.PROTOS[proto], steps, 20)
                 out[f"ag_p{p}_b{b}_{proto}"] = paced_collective(torch, ll, reg, "ag", m, ll.PROTOS[proto], steps, 20)
             del reg
@@ -260,7 +266,8 @@ def bench_sweep(torch, ll, path):
         for k in range(1, 27):
             n = 1 << k
             steps = 2000 if n * 4 <= (1 << 20) else (200 if n * 4 <= (16 << 20) else 20)
-            for algo in ("auto", "oneshot_waves", "oneshot", "oneshot_line", "twoshot", "twoshot_line"):
+            for algo in ("auto", "oneshot_waves", "oneshot", "oneshot_line", "oneshot_sentinel", "twoshot",
+                         "twoshot_line", "twoshot_sentinel", "twoshot_sentinel_out"):
                 if algo == "oneshot_waves" and n * 4 > (1 << 20):
                     continue
                 r = paced_collective(torch, ll, reg, "ar", n, ll.ALGOS[algo], steps, min(20, steps))
@@ -441,7 +448,8 @@ def main():
         log(json.dumps(result["sol"]))
     if want("bw"):
         log("bandwidth at 64 MiB per rank")
-        result["bw"] = bench_bandwidth(torch, ll, 16 << 20, ["twoshot_line", "twoshot", "oneshot_line", "oneshot"],
+        result["bw"] = bench_bandwidth(torch, ll, 16 << 20, ["twoshot_line", "twoshot", "twoshot_sentinel", "oneshot_line",
+                                                                "oneshot", "oneshot_sentinel"],
                                        iters=args.bw_iters)
         log(json.dumps(result["bw"]))
     if want("c3"):

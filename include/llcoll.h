@@ -27,6 +27,7 @@
  *   [0, cap)                      input area: the rank's input, at offset 0
  *   [cap, cap + A8)               8-byte packet area {payload u32, flag u32}
  *   [cap + A8, cap + A8 + A128)   128-byte line area
+ *   [.., .. + AS)                 sentinel area (payload only)
  * cap (the input capacity, a multiple of 256 bytes) is the largest input for
  * which both packet areas fit every algorithm; ll_input_capacity reports it.
  *
@@ -37,7 +38,8 @@
  *
  * Epochs.  The flag carried by every packet is the caller's `epoch`, which
  * must be >= 1 and must strictly increase over all calls on one region (any
- * entry point); 0 marks zeroed scratch (ll_init).  After epoch 0xFFFFFFFF,
+ * entry point); 0 marks zeroed scratch (ll_init).  Sentinel-mode calls check
+ * the epoch like the others but do not use it.  After epoch 0xFFFFFFFF,
  * call ll_init again and restart at 1.  (The paper's buffer object keeps this
  * counter internally and advances it itself, Sec. V; here the caller owns it.)
  *
@@ -78,11 +80,34 @@ typedef enum {
   LL_ALGO_TWOSHOT = 2,       /* two-shot (ReduceScatter + AllGather), 8-byte packets */
   LL_ALGO_TWOSHOT_LINE = 3,  /* two-shot, 128-byte line packets */
   LL_ALGO_ONESHOT_LINE = 4,  /* one-shot, 128-byte line packets */
-  LL_ALGO_ONESHOT_WAVES = 5  /* one-shot, 8-byte packets, one wave per peer, LDS staging */
+  LL_ALGO_ONESHOT_WAVES = 5,  /* one-shot, 8-byte packets, one wave per peer, LDS staging */
+  LL_ALGO_ONESHOT_SENTINEL = 6, /* one-shot, sentinel synchronisation (Sec. IV, "Sentinel") */
+  LL_ALGO_TWOSHOT_SENTINEL = 7, /* two-shot, sentinel synchronisation */
+  LL_ALGO_TWOSHOT_SENTINEL_OUT = 8 /* two-shot, sentinel; AllGather straight into the
+                                      peers' sentinel-filled outputs (see ll_fill_sentinel) */
 } ll_algo;
 
 /* Packet format for the stand-alone ReduceScatter / AllGather. */
-typedef enum { LL_PROTO_AUTO = 0, LL_PROTO_PACKET8 = 1, LL_PROTO_LINE128 = 2 } ll_proto;
+typedef enum { LL_PROTO_AUTO = 0, LL_PROTO_PACKET8 = 1, LL_PROTO_LINE128 = 2, LL_PROTO_SENTINEL = 3 } ll_proto;
+
+/* Sentinel mode (LL_ALGO_*_SENTINEL, LL_PROTO_SENTINEL).  Receive slots hold
+ * the dword 0xFFFFFFFF until payload overwrites them; the receiver polls until
+ * every dword differs from it and then writes the sentinel back.  Payload
+ * travels without flags (4 bytes of payload per 4 bytes stored).  Input data
+ * must not contain the dword 0xFFFFFFFF (binary32: that negative NaN;
+ * bfloat16: two adjacent 0xFFFF negative NaNs starting at an even index);
+ * such a call times out (LL_ERR_TIMEOUT) instead of completing.  After a
+ * timed-out call, ll_init restores the sentinels.
+ *
+ * LL_ALGO_TWOSHOT_SENTINEL_OUT keeps only the ReduceScatter slots in scratch
+ * (Table I: scratch D rather than 2D): the owner of each chunk stores the
+ * reduced chunk directly into every peer's output, and each rank polls its
+ * own output until those blocks no longer hold the sentinel (Sec. IV, the
+ * sentinel-initialised output of the two-shot variants).  Preconditions:
+ * every element of the nranks*count outputs holds the sentinel
+ * (ll_fill_sentinel on the same stream, once before every call), and
+ * count*esize is a multiple of 16 (else LL_ERR_UNSUPPORTED).  A call on an
+ * output that was not refilled may return the previous call's blocks. */
 
 /* Status codes. */
 #define LL_OK 0
@@ -106,11 +131,21 @@ int ll_slice_bytes(size_t count, ll_dtype dt, int nranks, size_t *min_rank_strid
 /* Input capacity in bytes of a region with this rank_stride and rank count. */
 int ll_input_capacity(size_t rank_stride, int nranks, size_t *capacity_bytes);
 
-/* Zero both packet areas of every slice (flag 0 = nothing received), on
- * `stream`.  Call once after allocating a region, and again before reusing it
+/* Byte offsets, within every slice, of the areas of the slice layout:
+ * offsets5 = {input area (0), 8-byte packet area, line area, sentinel area,
+ * end of the sentinel area}.  Host-only; errors as ll_input_capacity. */
+int ll_slice_layout(size_t rank_stride, int nranks, size_t *offsets5);
+
+/* Zero both flagged packet areas of every slice (flag 0 = nothing received)
+ * and fill the sentinel area with the sentinel, on `stream`.  Call once after allocating a region, and again before reusing it
  * after epoch 0xFFFFFFFF or after a timed-out call.  Sec. V: the LL reset
  * value is zero. */
 int ll_init(void *sym_base, size_t rank_stride, int nranks, void *stream);
+
+/* Set the nranks*count elements of `out` (16-byte aligned device memory) to
+ * the sentinel of `dt` (every byte 0xFF), on `stream`: the precondition of
+ * LL_ALGO_TWOSHOT_SENTINEL_OUT (Sec. V, sentinel initialisation). */
+int ll_fill_sentinel(void *out, size_t count, ll_dtype dt, int nranks, void *stream);
 
 /* AllReduce (sum) of `count` elements per rank, algorithm chosen by size.
  * Input of rank r: sym_base + r*rank_stride, count elements.  One kernel
@@ -149,6 +184,11 @@ int ll_last_timeout(int *rank, uint32_t *missing_peers, uint32_t *epoch);
 const char *ll_strerror(int status);
 
 /* ---- tuning and test hooks (process-wide settings; not thread-safe) ---- */
+
+/* Whether the automatic choices (LL_ALGO_AUTO, LL_PROTO_AUTO) may use sentinel
+ * mode, for callers whose data never holds the sentinel dword (0 = no, the
+ * default; 1 = yes).  Never selects LL_ALGO_TWOSHOT_SENTINEL_OUT. */
+int ll_set_auto_sentinel(int allow);
 
 /* Workgroups per rank and threads per workgroup for the following calls;
  * 0 = automatic.  threads must be a multiple of 64 in [64, 1024].  Results do

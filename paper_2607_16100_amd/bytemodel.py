@@ -13,7 +13,10 @@ from __future__ import annotations
 
 import math
 
-EXPANSION = {"packet8": 2.0, "line128": 128.0 / 120.0}
+EXPANSION = {"packet8": 2.0, "line128": 128.0 / 120.0, "sentinel": 1.0}
+# bytes moved per payload byte of one packet copy: written by the sender,
+# read by the receiver, and (sentinel mode) written back with the sentinel
+COPY_FACTOR = {"packet8": 2 * 2.0, "line128": 2 * 128.0 / 120.0, "sentinel": 3.0}
 
 
 def comm_volume_per_rank(algo: str, p: int, m: float, proto: str) -> float:
@@ -27,9 +30,10 @@ def comm_volume_per_rank(algo: str, p: int, m: float, proto: str) -> float:
 
 
 def _proto(algo: str) -> tuple[str, str]:
-    base = {"oneshot": "oneshot", "oneshot_line": "oneshot", "oneshot_waves": "oneshot", "twoshot": "twoshot",
-            "twoshot_line": "twoshot"}[algo]
-    proto = "line128" if algo.endswith("_line") else "packet8"
+    base = {"oneshot": "oneshot", "oneshot_line": "oneshot", "oneshot_waves": "oneshot",
+            "oneshot_sentinel": "oneshot", "twoshot": "twoshot", "twoshot_line": "twoshot",
+            "twoshot_sentinel": "twoshot"}[algo]
+    proto = "line128" if algo.endswith("_line") else ("sentinel" if algo.endswith("_sentinel") else "packet8")
     return base, proto
 
 
@@ -37,28 +41,26 @@ def allreduce_bytes(algo: str, p: int, count: int, esize: int) -> float:
     """HBM bytes moved by one AllReduce call of `count` elements per rank."""
     m = count * esize
     base, proto = _proto(algo)
-    e = EXPANSION[proto]
+    f = COPY_FACTOR[proto]
     if base == "oneshot":
-        # read input M; write (P-1) packet copies; read them back; write output M
-        per_rank = m + 2 * e * (p - 1) * m + m
+        # read input M; (P-1) packet copies written and read back; write output M
+        per_rank = m + f * (p - 1) * m + m
     else:
-        # RS: read input M, write and read (P-1) chunk packets; AG: write and
-        # read (P-1) reduced-chunk packets; write output M
+        # RS: read input M, (P-1) chunk packet copies; AG: (P-1) reduced-chunk
+        # packet copies; write output M
         c = math.ceil(count / p) * esize
-        per_rank = m + 4 * e * (p - 1) * c + m
+        per_rank = m + 2 * f * (p - 1) * c + m
     return p * per_rank
 
 
 def reduce_scatter_bytes(proto: str, p: int, recvcount: int, esize: int) -> float:
     c = recvcount * esize
-    e = EXPANSION[proto]
-    return p * (p * c + 2 * e * (p - 1) * c + c)
+    return p * (p * c + COPY_FACTOR[proto] * (p - 1) * c + c)
 
 
 def allgather_bytes(proto: str, p: int, sendcount: int, esize: int) -> float:
     s = sendcount * esize
-    e = EXPANSION[proto]
-    return p * (s + 2 * e * (p - 1) * s + p * s)
+    return p * (s + COPY_FACTOR[proto] * (p - 1) * s + p * s)
 
 
 def useful_bytes(p: int, count: int, esize: int) -> float:

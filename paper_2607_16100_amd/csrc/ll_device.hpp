@@ -47,6 +47,9 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t bytes) {
 __device__ __forceinline__ void st_pkt(rsrc_t rs, uint32_t off, u32x4 v) {
   __builtin_amdgcn_raw_buffer_store_b128(v, rs, (int)off, 0, kSC1);
 }
+__device__ __forceinline__ void st_pkt_at(rsrc_t rs, uint32_t off, uint32_t soff, u32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, rs, (int)off, (int)soff, kSC1);
+}
 __device__ __forceinline__ u32x4 ld_pkt(rsrc_t rs, uint32_t off, uint32_t soff = 0) {
   return __builtin_amdgcn_raw_buffer_load_b128(rs, (int)off, (int)soff, kSC1);
 }
@@ -303,6 +306,40 @@ struct ProtoLine {
   }
   static constexpr __host__ __device__ int64_t units(int64_t words) { return (words + 239) / 240; }
 };
+
+// Sentinel mode (Sec. IV, "Sentinel"): no flag at all.  A receive slot holds
+// the sentinel 0xFFFFFFFF in every dword (a negative NaN as binary32, a pair
+// of negative NaNs as bfloat16) until the sender's payload overwrites it; a
+// lane moves 4 payload words per 16-byte store, so the full store bandwidth
+// carries data.  The receiver resets every slot it has read back to the
+// sentinel.  A payload dword that equals the sentinel can never be detected:
+// such data is not supported (the wait times out).
+struct ProtoSent {
+  static constexpr int kLanes = 1;
+  static constexpr int kUnitBytes = 16;
+  static constexpr int kUnitWords = 4;
+  static constexpr int kMaxWords = 4;
+  static constexpr bool kReset = true;
+  static constexpr uint32_t kSentinel = 0xFFFFFFFFu;
+  template <int DT>
+  __device__ static __forceinline__ u32x4 load(const char *base, int64_t u, int /*sub*/, int64_t nelem, bool al4) {
+    return load_words<DT>(base, 4 * u, 4, nelem, al4);
+  }
+  template <int DT>
+  __device__ static __forceinline__ void store(char *base, int64_t u, int /*sub*/, int64_t nelem, bool al4, u32x4 w) {
+    store_words<DT>(base, 4 * u, 4, nelem, al4, w);
+  }
+  __device__ static __forceinline__ u32x4 pack(u32x4 w, uint32_t /*epoch*/, int /*sub*/) { return w; }
+  __device__ static __forceinline__ bool ready(u32x4 p, uint32_t /*epoch*/) {
+    return p.x != kSentinel && p.y != kSentinel && p.z != kSentinel && p.w != kSentinel;
+  }
+  __device__ static __forceinline__ u32x4 unpack(u32x4 p, int /*sub*/) { return p; }
+  static constexpr __host__ __device__ int64_t units(int64_t words) { return (words + 3) / 4; }
+};
+
+// Whether a packet format resets the slots it has read.
+template <class Pr> struct ResetsSlots { static constexpr bool value = false; };
+template <> struct ResetsSlots<ProtoSent> { static constexpr bool value = true; };
 
 // ---------------------------------------------------------------------------
 // Status word shared by all kernels of the library: [0] = error code (0 = ok),

@@ -106,6 +106,15 @@ __device__ __forceinline__ int poll_all(char *area_r, uint64_t slot, uint32_t of
       break;
     }
   }
+  if (ResetsSlots<Pr>::value) {
+    // sentinel mode: give every slot read back to its next sender
+    const u32x4 sent = {ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel};
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      if (q == r) continue;
+      st_pkt_at(rs, off, uniform_u32((uint32_t)((uint64_t)slot_of(q, r) * slot)), sent);
+    }
+  }
   return spins;
 }
 
@@ -368,7 +377,40 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs a) {
 // Every wait is for an earlier step of the same lane on another rank, so the
 // pipeline cannot deadlock.  RS slots occupy the first P-1 slots of the
 // area, AG slots the next P-1.
-template <class Pr, int DT, int P>
+//
+// Direct (sentinel mode only): the AllGather skips scratch.  The owner of
+// chunk c stores its reduced units straight into block c of every peer's
+// output, which the caller has filled with the sentinel beforehand, and each
+// rank polls its own output until the peers' blocks no longer hold it
+// (Sec. IV: sentinel-initialised output; Table I: scratch D instead of 2D).
+// Every unit of a chunk is a full 16 bytes (the caller guarantees
+// n * esize % 16 == 0), so units past a short last chunk are simply skipped.
+template <int P>
+__device__ __forceinline__ void poll_out(char *out_r, uint32_t out_bytes, uint32_t chunk_bytes, uint32_t off,
+                                         uint32_t pend, int r, uint32_t epoch, uint64_t deadline) {
+  const rsrc_t rs = make_rsrc(out_r, out_bytes);
+  int spins = 1;
+  while (pend != 0) {
+    compiler_fence();
+    u32x4 got[P];
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      got[q] = u32x4{0u, 0u, 0u, 0u};
+      if (pend & (1u << q)) got[q] = ld_pkt(rs, off, uniform_u32((uint32_t)q * chunk_bytes));
+    }
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      if ((pend & (1u << q)) && ProtoSent::ready(got[q], epoch)) pend &= ~(1u << q);
+    }
+    if (pend == 0) break;
+    if ((spins++ & 15) == 0 && now_ticks() > deadline) {
+      report_timeout(r, pend, epoch);
+      break;
+    }
+  }
+}
+
+template <class Pr, int DT, int P, bool Direct = false>
 struct TwoShot {
   static constexpr int E = Elem<DT>::kBytes;
   const KArgs &a;
@@ -411,11 +453,30 @@ struct TwoShot {
     for (int q = 0; q < P; ++q) got[q] = Pr::unpack(got[q], sub);
     const u32x4 res = reduce_ordered<Pr, DT, P>(got, own, r);
     Pr::template store<DT>(out_r + r * C * E, u, sub, nr, al4, res);
-    if (publish) bcast<P>(a, ag_area, r, off, Pr::pack(res, a.epoch, sub));
+    if (!publish) return;
+    if constexpr (Direct) {
+      if ((int64_t)off >= nr * E) return;  // past a short last chunk
+      const uint32_t at = uniform_u32((uint32_t)(r * C * E));
+#pragma unroll
+      for (int k = 1; k < P; ++k) {
+        const int q = (r + k) % P;
+        st_pkt_at(make_rsrc(a.out + (uint64_t)q * (uint64_t)n * E, (uint32_t)(n * E)), off, at, res);
+      }
+    } else {
+      bcast<P>(a, ag_area, r, off, Pr::pack(res, a.epoch, sub));
+    }
   }
 
   __device__ __forceinline__ void step_gather(int64_t u, int sub) const {
     const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+    if constexpr (Direct) {
+      uint32_t pend = 0;
+#pragma unroll
+      for (int q = 0; q < P; ++q)
+        if (q != r && (int64_t)off < chunk_len(q) * E) pend |= 1u << q;
+      poll_out<P>(out_r, (uint32_t)(n * E), (uint32_t)(C * E), off, pend, r, a.epoch, deadline);
+      return;
+    }
     u32x4 got[P];
     poll_all<Pr, P>(slice_r + ag_area, a.slot, off, r, a.epoch, deadline, got);
 #pragma unroll
@@ -430,12 +491,12 @@ struct TwoShot {
 #define LLCOLL_TWOSHOT_WAVES_PER_EU 1
 #endif
 
-template <class Pr, int DT, int P>
+template <class Pr, int DT, int P, bool Direct = false>
 __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(LLCOLL_TWOSHOT_WAVES_PER_EU))) void k_twoshot(
     KArgs a) {
   stamp_start(a);
   const Part pt = part_of_block<P>();
-  TwoShot<Pr, DT, P> t{a};
+  TwoShot<Pr, DT, P, Direct> t{a};
   t.r = pt.r;
   constexpr int E = Elem<DT>::kBytes;
   t.deadline = now_ticks() + a.timeout;
@@ -567,11 +628,22 @@ __global__ __launch_bounds__(1024) void k_allgather(KArgs a) {
   stamp_end(a);
 }
 
-// Zero the packet areas [lo, hi) of every slice.
-__global__ __launch_bounds__(256) void k_zero_areas(char *sym, uint64_t stride, int nranks, uint64_t lo, uint64_t hi) {
+// Set `bytes` bytes at `dst` (16-byte aligned) to 0xFF: the sentinel of
+// every element type.
+__global__ __launch_bounds__(256) void k_fill_ones(char *dst, uint64_t bytes) {
+  const uint64_t full = bytes / 16;
+  const u32x4 ones = {0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
+  const uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  for (uint64_t i = t; i < full; i += (uint64_t)gridDim.x * blockDim.x) *(u32x4 *)(dst + i * 16) = ones;
+  if (t < bytes % 16) dst[full * 16 + t] = (char)0xFF;
+}
+
+// Fill bytes [lo, hi) of every slice with the dword `value`.
+__global__ __launch_bounds__(256) void k_fill_areas(char *sym, uint64_t stride, int nranks, uint64_t lo, uint64_t hi,
+                                                  uint32_t value) {
   const uint64_t per = (hi - lo) / 16;
   const uint64_t total = per * (uint64_t)nranks;
-  const u32x4 z = {0u, 0u, 0u, 0u};
+  const u32x4 z = {value, value, value, value};
   for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (uint64_t)gridDim.x * blockDim.x) {
     const uint64_t rk = i / per;
     const uint64_t k = i % per;

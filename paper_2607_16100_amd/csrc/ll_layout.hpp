@@ -4,11 +4,13 @@
 //   [0, cap)                   input area (the rank's input at offset 0)
 //   [cap, cap + A8)            8-byte packet area
 //   [cap + A8, cap + A8 + A128) 128-byte line area
+//   [.., .. + AS)              sentinel area (payload only, reset after use)
 // where cap is the largest multiple of 256 for which both areas, sized for
 // the most demanding algorithm at an input of cap bytes, fit in the slice.
 // The layout therefore depends only on (stride, P): a byte that holds input
 // in one call is never read as a flag in another, and the two packet formats
-// never share bytes, so a stale payload word can never pose as a flag.
+// never share bytes, so a stale payload word can never pose as a flag.  The
+// sentinel area holds nothing but payload and sentinels.
 //
 // Within an area a call places its slots from the area's start:
 //   one-shot / AllGather   P-1 slots, each holding a full input
@@ -58,7 +60,15 @@ inline uint64_t area128(uint64_t M, int P) {
   return std::max(p1 * slot128(M), 2 * p1 * slot128(chunk_bound(M, P)));
 }
 
-inline uint64_t slice_for(uint64_t cap, int P) { return cap + area8(cap, P) + area128(cap, P); }
+// Sentinel slots carry payload only: a 16-byte unit holds 4 payload words.
+inline uint64_t slotS(uint64_t bytes) { return roundup(ceil_div(bytes, 16) * 16, kAlign); }
+
+inline uint64_t areaS(uint64_t M, int P) {
+  const uint64_t p1 = (uint64_t)(P - 1);
+  return std::max(p1 * slotS(M), 2 * p1 * slotS(chunk_bound(M, P)));
+}
+
+inline uint64_t slice_for(uint64_t cap, int P) { return cap + area8(cap, P) + area128(cap, P) + areaS(cap, P); }
 
 // Largest cap (multiple of 256, at most kMaxInputBytes) with slice_for(cap) <= stride.
 inline uint64_t capacity(uint64_t stride, int P) {

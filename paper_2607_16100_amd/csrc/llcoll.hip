@@ -6,8 +6,10 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <atomic>
 #include <mutex>
+#include <type_traits>
 
 #include "../../include/llcoll.h"
 #include "../../include/llprobe.h"
@@ -34,6 +36,7 @@ std::atomic<int> g_first_wait{0};
 std::atomic<int> g_poll_gap{0};
 std::atomic<int> g_wave_units{0};  // 0 = automatic, else 1, 2 or 4
 std::atomic<int> g_lag{1};
+std::atomic<int> g_auto_sentinel{0};
 std::atomic<uint64_t *> g_stamps{nullptr};
 std::atomic<uint64_t *> g_phases{nullptr};
 std::atomic<int> g_last_grid{0};
@@ -48,9 +51,9 @@ TimeoutInfo g_last_timeout;
 std::mutex g_mu;
 
 // ---------------------------------------------------------------- kernels
-enum Kind { K_ONESHOT = 0, K_TWOSHOT = 1, K_RS = 2, K_AG = 3, K_ONESHOT_WAVES = 4, K_KINDS = 5 };
+enum Kind { K_ONESHOT = 0, K_TWOSHOT = 1, K_RS = 2, K_AG = 3, K_ONESHOT_WAVES = 4, K_TWOSHOT_OUT = 5, K_KINDS = 6 };
 constexpr int kWaveUnits[3] = {1, 2, 4};  // units per lane of the wave-per-peer kernels
-enum Proto { PR_LL = 0, PR_LINE = 1, PR_COUNT = 2 };
+enum Proto { PR_LL = 0, PR_LINE = 1, PR_SENT = 2, PR_COUNT = 3 };
 
 typedef void (*kernel_fn)(KArgs);
 
@@ -61,6 +64,8 @@ void fill_row(kernel_fn *row) {
   row[K_RS] = k_reduce_scatter<Pr, DT, P>;
   row[K_AG] = k_allgather<Pr, DT, P>;
   row[K_ONESHOT_WAVES] = nullptr;
+  row[K_TWOSHOT_OUT] = nullptr;
+  if constexpr (std::is_same<Pr, ProtoSent>::value) row[K_TWOSHOT_OUT] = k_twoshot<ProtoSent, DT, P, true>;
 }
 
 // table[proto][dtype][P][kind]
@@ -84,6 +89,8 @@ struct Table {
     fill_row<ProtoLL, 1, P>(k[PR_LL][1][P]);
     fill_row<ProtoLine, 0, P>(k[PR_LINE][0][P]);
     fill_row<ProtoLine, 1, P>(k[PR_LINE][1][P]);
+    fill_row<ProtoSent, 0, P>(k[PR_SENT][0][P]);
+    fill_row<ProtoSent, 1, P>(k[PR_SENT][1][P]);
     waves[0][0][P] = k_oneshot_waves<0, P, 1>;
     waves[0][1][P] = k_oneshot_waves<1, P, 1>;
     waves[1][0][P] = k_oneshot_waves<0, P, 2>;
@@ -192,7 +199,7 @@ int launch(const Plan &pl, void *stream) {
   if (fn == nullptr) return LL_ERR_UNSUPPORTED;
   int threads = g_threads.load();
   if (threads == 0) threads = 256;
-  int lanes_per_unit = pl.proto == PR_LINE ? ProtoLine::kLanes : ProtoLL::kLanes;
+  int lanes_per_unit = pl.proto == PR_LINE ? ProtoLine::kLanes : 1;
   int64_t work_units = pl.units;
   if (pl.kind == K_ONESHOT_WAVES) {  // one wave per rank, 64*U units per workgroup and step
     threads = 64 * pl.P;
@@ -237,8 +244,20 @@ int launch(const Plan &pl, void *stream) {
 // Region geometry of one call; fails with LL_ERR_SCRATCH when the input does
 // not fit the region's input capacity.
 struct Region {
-  uint64_t cap, a8, a128;
+  uint64_t cap, a8, a128, as;
+  uint64_t area_of(int proto) const {
+    return proto == PR_LINE ? cap + a8 : (proto == PR_SENT ? cap + a8 + a128 : cap);
+  }
 };
+
+// Slot bytes and packet units for a payload of `bytes` in format `proto`.
+uint64_t slot_bytes(int proto, uint64_t bytes) {
+  return proto == PR_LINE ? L::slot128(bytes) : (proto == PR_SENT ? L::slotS(bytes) : L::slot8(bytes));
+}
+int64_t units_of(int proto, uint64_t bytes) {
+  const int64_t words = (int64_t)L::ceil_div(bytes, 4);
+  return proto == PR_LINE ? ProtoLine::units(words) : (proto == PR_SENT ? ProtoSent::units(words) : ProtoLL::units(words));
+}
 
 int region_of(size_t rank_stride, int P, uint64_t in_bytes, Region *rg) {
   const uint64_t cap = L::capacity(rank_stride, P);
@@ -248,6 +267,7 @@ int region_of(size_t rank_stride, int P, uint64_t in_bytes, Region *rg) {
   rg->cap = cap;
   rg->a8 = L::area8(cap, P);
   rg->a128 = L::area128(cap, P);
+  rg->as = L::areaS(cap, P);
   return LL_OK;
 }
 
@@ -262,12 +282,26 @@ KArgs base_args(void *sym_base, size_t rank_stride, void *out, uint32_t epoch) {
   return a;
 }
 
-// Size thresholds measured on MI355X (mean time of back-to-back calls for
-// every algorithm at 32 KiB .. 8 MiB per rank, P = 2, 4, 8, binary32 and
-// bfloat16); M = input bytes per rank.
-ll_algo auto_algo(uint64_t in_bytes, int P) {
+// Size thresholds measured on MI355X (mean time of back-to-back calls of
+// every algorithm at 4 KiB .. 64 MiB per rank, P = 2, 4, 8, binary32 and
+// bfloat16; both element types cross over at the same byte sizes);
+// M = input bytes per rank.  Flags only unless the caller allows sentinel
+// mode, which wins from 64 KiB (one-shot) and from 512 KiB at 8 ranks
+// (two-shot), as the paper observes for larger messages and rank counts.
+ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
   const uint64_t KiB = 1024, MiB = 1024 * 1024;
   if (in_bytes <= 32 * KiB) return LL_ALGO_ONESHOT_WAVES;
+  if (sentinel_ok) {
+    if (P <= 2) {
+      if (in_bytes <= 64 * KiB) return LL_ALGO_ONESHOT;
+      if (in_bytes <= 4 * MiB) return LL_ALGO_ONESHOT_SENTINEL;
+      if (in_bytes <= 8 * MiB) return LL_ALGO_TWOSHOT_SENTINEL;
+      return LL_ALGO_TWOSHOT_LINE;
+    }
+    if (in_bytes <= (P <= 4 ? 512 : 256) * KiB) return LL_ALGO_ONESHOT_SENTINEL;
+    if (in_bytes <= 4 * MiB) return LL_ALGO_TWOSHOT_SENTINEL;
+    return LL_ALGO_TWOSHOT_LINE;
+  }
   if (P <= 2) {
     if (in_bytes <= 128 * KiB) return LL_ALGO_ONESHOT;
     if (in_bytes <= 4 * MiB) return LL_ALGO_ONESHOT_LINE;
@@ -282,10 +316,20 @@ ll_algo auto_algo(uint64_t in_bytes, int P) {
   return LL_ALGO_TWOSHOT_LINE;
 }
 
-// ReduceScatter / AllGather: 8-byte packets up to 1 MiB of data per rank
-// (input for ReduceScatter, output for AllGather), lines above (measured on
-// the hidden 7168 x batch {1, 16, 256} shapes at 4 and 8 ranks).
-ll_proto auto_proto(uint64_t bytes) { return bytes <= (1u << 20) ? LL_PROTO_PACKET8 : LL_PROTO_LINE128; }
+// ReduceScatter / AllGather, by the bytes of data per rank (input for
+// ReduceScatter, output for AllGather), measured the same way at 4 KiB ..
+// 16 MiB: 8-byte packets up to 512 KiB, lines above; with sentinel mode
+// allowed, sentinel from 128 KiB (256 KiB at 8 ranks) up to 4 MiB (8 ranks),
+// 8 MiB (3-4 ranks) or 16 MiB (2 ranks).
+ll_proto auto_proto(uint64_t bytes, int P, bool sentinel_ok) {
+  const uint64_t KiB = 1024, MiB = 1024 * 1024;
+  if (sentinel_ok) {
+    if (bytes <= (P >= 5 ? 128 : 64) * KiB) return LL_PROTO_PACKET8;
+    if (bytes <= (P >= 5 ? 4 : (P >= 3 ? 8 : 16)) * MiB) return LL_PROTO_SENTINEL;
+    return LL_PROTO_LINE128;
+  }
+  return bytes <= 512 * KiB ? LL_PROTO_PACKET8 : LL_PROTO_LINE128;
+}
 
 }  // namespace
 
@@ -313,6 +357,20 @@ int ll_input_capacity(size_t rank_stride, int nranks, size_t *capacity_bytes) {
   return LL_OK;
 }
 
+int ll_slice_layout(size_t rank_stride, int nranks, size_t *offsets5) {
+  if (offsets5 == nullptr) return LL_ERR_INVALID;
+  size_t cap = 0;
+  const int st = ll_input_capacity(rank_stride, nranks, &cap);
+  if (st != LL_OK) return st;
+  const uint64_t a8 = L::area8(cap, nranks), a128 = L::area128(cap, nranks), as = L::areaS(cap, nranks);
+  offsets5[0] = 0;
+  offsets5[1] = cap;
+  offsets5[2] = cap + a8;
+  offsets5[3] = cap + a8 + a128;
+  offsets5[4] = cap + a8 + a128 + as;
+  return LL_OK;
+}
+
 int ll_init(void *sym_base, size_t rank_stride, int nranks, void *stream) {
   if (sym_base == nullptr) return LL_ERR_INVALID;
   if (nranks < 2 || nranks > LL_MAX_RANKS) return LL_ERR_INVALID;
@@ -320,13 +378,39 @@ int ll_init(void *sym_base, size_t rank_stride, int nranks, void *stream) {
   Region rg;
   int st = region_of(rank_stride, nranks, 0, &rg);
   if (st != LL_OK) return st;
-  const uint64_t lo = rg.cap, hi = rg.cap + rg.a8 + rg.a128;
-  if (hi == lo) return LL_OK;
   DevInfo d;
   st = device_info(&d);
   if (st != LL_OK) return st;
-  hipLaunchKernelGGL(k_zero_areas, dim3(d.cus * 4), dim3(256), 0, (hipStream_t)stream, (char *)sym_base,
-                     (uint64_t)rank_stride, nranks, lo, hi);
+  // flags start at 0 (never a valid epoch); sentinel slots start at the sentinel
+  const uint64_t lo = rg.cap, mid = rg.cap + rg.a8 + rg.a128, hi = mid + rg.as;
+  if (mid > lo)
+    hipLaunchKernelGGL(k_fill_areas, dim3(d.cus * 4), dim3(256), 0, (hipStream_t)stream, (char *)sym_base,
+                       (uint64_t)rank_stride, nranks, lo, mid, 0u);
+  if (hi > mid)
+    hipLaunchKernelGGL(k_fill_areas, dim3(d.cus * 4), dim3(256), 0, (hipStream_t)stream, (char *)sym_base,
+                       (uint64_t)rank_stride, nranks, mid, hi, ProtoSent::kSentinel);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    t_last_hip = (int)e;
+    return LL_ERR_HIP;
+  }
+  return LL_OK;
+}
+
+int ll_fill_sentinel(void *out, size_t count, ll_dtype dt, int nranks, void *stream) {
+  if (out == nullptr || ((uintptr_t)out % 16) != 0) return LL_ERR_INVALID;
+  if (nranks < 2 || nranks > LL_MAX_RANKS) return LL_ERR_INVALID;
+  if (dt != LL_F32 && dt != LL_BF16) return LL_ERR_UNSUPPORTED;
+  const uint64_t es = (uint64_t)esize_of(dt);
+  if (count > L::kMaxInputBytes / es) return LL_ERR_UNSUPPORTED;
+  const uint64_t bytes = (uint64_t)count * es * (uint64_t)nranks;
+  if (bytes == 0) return LL_OK;
+  DevInfo d;
+  const int st = device_info(&d);
+  if (st != LL_OK) return st;
+  const uint64_t want = L::ceil_div(L::ceil_div(bytes, 16), 256);
+  const int grid = (int)std::max<uint64_t>(1, std::min<uint64_t>(want, (uint64_t)d.cus * 8));
+  hipLaunchKernelGGL(k_fill_ones, dim3(grid), dim3(256), 0, (hipStream_t)stream, (char *)out, bytes);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) {
     t_last_hip = (int)e;
@@ -341,16 +425,17 @@ int ll_allreduce_algo(void *sym_base, size_t rank_stride, void *out, size_t coun
   if (st != LL_OK) return st;
   st = check_dtype_op((int)dt, (int)op);
   if (st != LL_OK) return st;
-  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_ONESHOT_WAVES) return LL_ERR_INVALID;
+  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_TWOSHOT_SENTINEL_OUT) return LL_ERR_INVALID;
   const int es = esize_of(dt);
   const uint64_t in_bytes = (uint64_t)count * es;
+  if (algo == LL_ALGO_TWOSHOT_SENTINEL_OUT && in_bytes % 16 != 0) return LL_ERR_UNSUPPORTED;
   if (count > L::kMaxInputBytes) return LL_ERR_UNSUPPORTED;
   if (overlaps(out, in_bytes * nranks, sym_base, (uint64_t)rank_stride * nranks)) return LL_ERR_INVALID;
   Region rg;
   st = region_of(rank_stride, nranks, in_bytes, &rg);
   if (st != LL_OK) return st;
   if (count == 0) return LL_OK;
-  if (algo == LL_ALGO_AUTO) algo = auto_algo(in_bytes, nranks);
+  if (algo == LL_ALGO_AUTO) algo = auto_algo(in_bytes, nranks, g_auto_sentinel.load() != 0);
 
   Plan pl;
   pl.dt = (int)dt;
@@ -359,21 +444,21 @@ int ll_allreduce_algo(void *sym_base, size_t rank_stride, void *out, size_t coun
   pl.a.n = (int64_t)count;
   pl.a.al4 = (in_bytes % 4 == 0) ? 1u : 0u;
   const bool line = (algo == LL_ALGO_TWOSHOT_LINE || algo == LL_ALGO_ONESHOT_LINE);
+  const bool sent = (algo == LL_ALGO_ONESHOT_SENTINEL || algo == LL_ALGO_TWOSHOT_SENTINEL ||
+                     algo == LL_ALGO_TWOSHOT_SENTINEL_OUT);
   const bool waves = (algo == LL_ALGO_ONESHOT_WAVES);
-  pl.proto = line ? PR_LINE : PR_LL;
-  pl.a.area = line ? rg.cap + rg.a8 : rg.cap;
-  if (algo == LL_ALGO_ONESHOT || algo == LL_ALGO_ONESHOT_LINE || waves) {
+  pl.proto = line ? PR_LINE : (sent ? PR_SENT : PR_LL);
+  pl.a.area = rg.area_of(pl.proto);
+  if (algo == LL_ALGO_ONESHOT || algo == LL_ALGO_ONESHOT_LINE || algo == LL_ALGO_ONESHOT_SENTINEL || waves) {
     pl.kind = waves ? K_ONESHOT_WAVES : K_ONESHOT;
-    pl.a.slot = line ? L::slot128(in_bytes) : L::slot8(in_bytes);
-    const int64_t words = (int64_t)L::ceil_div(in_bytes, 4);
-    pl.units = line ? ProtoLine::units(words) : ProtoLL::units(words);
+    pl.a.slot = slot_bytes(pl.proto, in_bytes);
+    pl.units = units_of(pl.proto, in_bytes);
   } else {
-    pl.kind = K_TWOSHOT;
+    pl.kind = algo == LL_ALGO_TWOSHOT_SENTINEL_OUT ? K_TWOSHOT_OUT : K_TWOSHOT;
     const uint64_t C = L::twoshot_chunk(count, nranks, es);
     pl.a.chunk = (int64_t)C;
-    pl.a.slot = line ? L::slot128(C * es) : L::slot8(C * es);
-    const int64_t words = (int64_t)L::ceil_div(C * es, 4);
-    pl.units = line ? ProtoLine::units(words) : ProtoLL::units(words);
+    pl.a.slot = slot_bytes(pl.proto, C * es);
+    pl.units = units_of(pl.proto, C * es);
   }
   return launch(pl, stream);
 }
@@ -389,7 +474,7 @@ int ll_reduce_scatter_proto(void *sym_base, size_t rank_stride, void *out, size_
   if (st != LL_OK) return st;
   st = check_dtype_op((int)dt, (int)op);
   if (st != LL_OK) return st;
-  if ((int)proto < LL_PROTO_AUTO || (int)proto > LL_PROTO_LINE128) return LL_ERR_INVALID;
+  if ((int)proto < LL_PROTO_AUTO || (int)proto > LL_PROTO_SENTINEL) return LL_ERR_INVALID;
   const int es = esize_of(dt);
   if (recvcount > L::kMaxInputBytes) return LL_ERR_UNSUPPORTED;
   const uint64_t chunk_bytes = (uint64_t)recvcount * es;
@@ -399,19 +484,18 @@ int ll_reduce_scatter_proto(void *sym_base, size_t rank_stride, void *out, size_
   st = region_of(rank_stride, nranks, in_bytes, &rg);
   if (st != LL_OK) return st;
   if (recvcount == 0) return LL_OK;
-  if (proto == LL_PROTO_AUTO) proto = auto_proto(in_bytes);
+  if (proto == LL_PROTO_AUTO) proto = auto_proto(in_bytes, nranks, g_auto_sentinel.load() != 0);
   Plan pl;
   pl.kind = K_RS;
   pl.dt = (int)dt;
   pl.P = nranks;
-  pl.proto = proto == LL_PROTO_LINE128 ? PR_LINE : PR_LL;
+  pl.proto = proto == LL_PROTO_LINE128 ? PR_LINE : (proto == LL_PROTO_SENTINEL ? PR_SENT : PR_LL);
   pl.a = base_args(sym_base, rank_stride, out, epoch);
   pl.a.n = (int64_t)recvcount;
   pl.a.al4 = (chunk_bytes % 4 == 0) ? 1u : 0u;
-  pl.a.area = pl.proto == PR_LINE ? rg.cap + rg.a8 : rg.cap;
-  pl.a.slot = pl.proto == PR_LINE ? L::slot128(chunk_bytes) : L::slot8(chunk_bytes);
-  const int64_t words = (int64_t)L::ceil_div(chunk_bytes, 4);
-  pl.units = pl.proto == PR_LINE ? ProtoLine::units(words) : ProtoLL::units(words);
+  pl.a.area = rg.area_of(pl.proto);
+  pl.a.slot = slot_bytes(pl.proto, chunk_bytes);
+  pl.units = units_of(pl.proto, chunk_bytes);
   return launch(pl, stream);
 }
 
@@ -427,7 +511,7 @@ int ll_allgather_proto(void *sym_base, size_t rank_stride, void *out, size_t sen
   if (st != LL_OK) return st;
   st = check_dtype_op((int)dt, LL_SUM);
   if (st != LL_OK) return st;
-  if ((int)proto < LL_PROTO_AUTO || (int)proto > LL_PROTO_LINE128) return LL_ERR_INVALID;
+  if ((int)proto < LL_PROTO_AUTO || (int)proto > LL_PROTO_SENTINEL) return LL_ERR_INVALID;
   const int es = esize_of(dt);
   if (sendcount > L::kMaxInputBytes) return LL_ERR_UNSUPPORTED;
   const uint64_t in_bytes = (uint64_t)sendcount * es;
@@ -436,19 +520,18 @@ int ll_allgather_proto(void *sym_base, size_t rank_stride, void *out, size_t sen
   st = region_of(rank_stride, nranks, in_bytes, &rg);
   if (st != LL_OK) return st;
   if (sendcount == 0) return LL_OK;
-  if (proto == LL_PROTO_AUTO) proto = auto_proto(in_bytes * nranks);
+  if (proto == LL_PROTO_AUTO) proto = auto_proto(in_bytes * nranks, nranks, g_auto_sentinel.load() != 0);
   Plan pl;
   pl.kind = K_AG;
   pl.dt = (int)dt;
   pl.P = nranks;
-  pl.proto = proto == LL_PROTO_LINE128 ? PR_LINE : PR_LL;
+  pl.proto = proto == LL_PROTO_LINE128 ? PR_LINE : (proto == LL_PROTO_SENTINEL ? PR_SENT : PR_LL);
   pl.a = base_args(sym_base, rank_stride, out, epoch);
   pl.a.n = (int64_t)sendcount;
   pl.a.al4 = (in_bytes % 4 == 0) ? 1u : 0u;
-  pl.a.area = pl.proto == PR_LINE ? rg.cap + rg.a8 : rg.cap;
-  pl.a.slot = pl.proto == PR_LINE ? L::slot128(in_bytes) : L::slot8(in_bytes);
-  const int64_t words = (int64_t)L::ceil_div(in_bytes, 4);
-  pl.units = pl.proto == PR_LINE ? ProtoLine::units(words) : ProtoLL::units(words);
+  pl.a.area = rg.area_of(pl.proto);
+  pl.a.slot = slot_bytes(pl.proto, in_bytes);
+  pl.units = units_of(pl.proto, in_bytes);
   return launch(pl, stream);
 }
 
@@ -531,6 +614,12 @@ int ll_set_poll_pacing(int first_wait, int poll_gap) {
 int ll_set_pipeline_lag(int lag) {
   if (lag < 1 || lag > 64) return LL_ERR_INVALID;
   g_lag.store(lag);
+  return LL_OK;
+}
+
+int ll_set_auto_sentinel(int allow) {
+  if (allow != 0 && allow != 1) return LL_ERR_INVALID;
+  g_auto_sentinel.store(allow);
   return LL_OK;
 }
 
@@ -636,6 +725,10 @@ int ll_bench_allreduce(void *sym_base, size_t rank_stride, void *out, size_t cou
     return LL_ERR_INVALID;
   if (stamps != nullptr && stamp_stride < 1) return LL_ERR_INVALID;
   for (int i = 0; i < calls; ++i) {
+    if (algo == LL_ALGO_TWOSHOT_SENTINEL_OUT) {  // its precondition, timed with it
+      const int sf = ll_fill_sentinel(out, count, (ll_dtype)dt, nranks, stream);
+      if (sf != LL_OK) return sf;
+    }
     if (stamps != nullptr) g_stamps.store(stamps + (size_t)i * (size_t)stamp_stride);
     const int st = ll_allreduce_algo(sym_base, rank_stride, out, count, (ll_dtype)dt, LL_SUM, nranks,
                                      first_epoch + (uint32_t)i, stream, (ll_algo)algo);

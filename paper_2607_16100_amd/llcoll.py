@@ -19,7 +19,8 @@ LL_F32, LL_BF16 = 0, 1
 LL_SUM = 0
 LL_ALGO_AUTO, LL_ALGO_ONESHOT, LL_ALGO_TWOSHOT, LL_ALGO_TWOSHOT_LINE, LL_ALGO_ONESHOT_LINE = 0, 1, 2, 3, 4
 LL_ALGO_ONESHOT_WAVES = 5
-LL_PROTO_AUTO, LL_PROTO_PACKET8, LL_PROTO_LINE128 = 0, 1, 2
+LL_ALGO_ONESHOT_SENTINEL, LL_ALGO_TWOSHOT_SENTINEL, LL_ALGO_TWOSHOT_SENTINEL_OUT = 6, 7, 8
+LL_PROTO_AUTO, LL_PROTO_PACKET8, LL_PROTO_LINE128, LL_PROTO_SENTINEL = 0, 1, 2, 3
 
 LL_OK = 0
 LL_ERR_INVALID = -1
@@ -32,8 +33,11 @@ ALGOS = {
     "auto": LL_ALGO_AUTO, "oneshot": LL_ALGO_ONESHOT, "twoshot": LL_ALGO_TWOSHOT,
     "twoshot_line": LL_ALGO_TWOSHOT_LINE, "oneshot_line": LL_ALGO_ONESHOT_LINE,
     "oneshot_waves": LL_ALGO_ONESHOT_WAVES,
+    "oneshot_sentinel": LL_ALGO_ONESHOT_SENTINEL, "twoshot_sentinel": LL_ALGO_TWOSHOT_SENTINEL,
+    "twoshot_sentinel_out": LL_ALGO_TWOSHOT_SENTINEL_OUT,
 }
-PROTOS = {"auto": LL_PROTO_AUTO, "packet8": LL_PROTO_PACKET8, "line128": LL_PROTO_LINE128}
+PROTOS = {"auto": LL_PROTO_AUTO, "packet8": LL_PROTO_PACKET8, "line128": LL_PROTO_LINE128,
+          "sentinel": LL_PROTO_SENTINEL}
 DTYPES = {"f32": LL_F32, "bf16": LL_BF16}
 
 # name -> (restype, argtypes)
@@ -41,7 +45,10 @@ _vp, _sz, _i, _u32, _u64 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctype
 _SIGS = {
     "ll_slice_bytes": (_i, [_sz, _i, _i, ctypes.POINTER(_sz)]),
     "ll_input_capacity": (_i, [_sz, _i, ctypes.POINTER(_sz)]),
+    "ll_slice_layout": (_i, [_sz, _i, ctypes.POINTER(_sz)]),
     "ll_init": (_i, [_vp, _sz, _i, _vp]),
+    "ll_fill_sentinel": (_i, [_vp, _sz, _i, _i, _vp]),
+    "ll_set_auto_sentinel": (_i, [_i]),
     "ll_allreduce": (_i, [_vp, _sz, _vp, _sz, _i, _i, _i, _u32, _vp]),
     "ll_allreduce_algo": (_i, [_vp, _sz, _vp, _sz, _i, _i, _i, _u32, _vp, _i]),
     "ll_reduce_scatter": (_i, [_vp, _sz, _vp, _sz, _i, _i, _i, _u32, _vp]),
@@ -123,6 +130,13 @@ def ll_input_capacity(rank_stride: int, nranks: int):
     return st, out.value
 
 
+def ll_slice_layout(rank_stride: int, nranks: int):
+    """(status, [input, packet8 area, line area, sentinel area, end]) byte offsets."""
+    out = (ctypes.c_size_t * 5)()
+    st = _lib.ll_slice_layout(rank_stride, nranks, out)
+    return st, list(out)
+
+
 def ll_init(sym_base, rank_stride, nranks, stream):
     return _lib.ll_init(sym_base, rank_stride, nranks, stream)
 
@@ -175,6 +189,14 @@ def ll_set_poll_pacing(first_wait: int, poll_gap: int):
 
 def ll_set_pipeline_lag(lag: int):
     return _lib.ll_set_pipeline_lag(lag)
+
+
+def ll_fill_sentinel(out, count, dt, nranks, stream):
+    return _lib.ll_fill_sentinel(out, count, dt, nranks, stream)
+
+
+def ll_set_auto_sentinel(allow: int):
+    return _lib.ll_set_auto_sentinel(allow)
 
 
 def ll_set_wave_units(units_per_lane: int):

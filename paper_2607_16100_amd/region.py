@@ -91,13 +91,32 @@ class SymRegion:
         view = self.sym.view(self.nranks, self.rank_stride)[:, :rows.shape[1]]
         view.copy_(rows)
 
+    def read_area(self, area: int) -> np.ndarray:
+        """Raw uint32 words of layout area `area` (1 = 8-byte packets, 2 =
+        lines, 3 = sentinel) of every slice, shape [P, area_bytes / 4]."""
+        st, offs = ll.ll_slice_layout(self.rank_stride, self.nranks)
+        ll.check(st, "ll_slice_layout")
+        lo, hi = offs[area], offs[area + 1]
+        v = self.sym.view(self.nranks, self.rank_stride)[:, lo:hi]
+        return v.cpu().numpy().copy().view(np.uint32)
+
     def read_out(self, nelems_total: int, np_dtype) -> np.ndarray:
         nbytes = nelems_total * np.dtype(np_dtype).itemsize
         return self.out[:nbytes].cpu().numpy().view(np_dtype).copy()
 
     # -- collectives (one launch each, on the given stream)
+    def fill_out_sentinel(self, count: int, stream=None) -> int:
+        """Fill the P outputs of `count` elements with the sentinel."""
+        return ll.ll_fill_sentinel(self.out_ptr, count, self.dt, self.nranks, self.stream_handle(stream))
+
     def allreduce(self, count: int, algo: str = "auto", stream=None, epoch: int | None = None) -> int:
+        """One AllReduce.  For "twoshot_sentinel_out" the outputs are first
+        refilled with the sentinel (its precondition), on the same stream."""
         e = self.next_epoch() if epoch is None else epoch
+        if algo == "twoshot_sentinel_out" and count > 0:
+            st = self.fill_out_sentinel(count, stream)
+            if st != ll.LL_OK:
+                return st
         return ll.ll_allreduce_algo(self.base, self.rank_stride, self.out_ptr, count, self.dt, ll.LL_SUM,
                                     self.nranks, e, self.stream_handle(stream), ll.ALGOS[algo])
 

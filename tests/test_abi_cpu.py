@@ -65,6 +65,8 @@ def ar(count=1024, dt=F32, p=4, base=GOOD_BASE, stride=None, out=GOOD_OUT, epoch
     (dict(dt=7), ll.LL_ERR_UNSUPPORTED),
     (dict(op=1), ll.LL_ERR_UNSUPPORTED),
     (dict(algo=9), ll.LL_ERR_INVALID),
+    (dict(algo=8, count=1001), ll.LL_ERR_UNSUPPORTED),  # direct output needs count*esize % 16 == 0
+    (dict(algo=-1), ll.LL_ERR_INVALID),
     (dict(stride=256), ll.LL_ERR_SCRATCH),
     (dict(count=1 << 29, stride=1 << 20), ll.LL_ERR_UNSUPPORTED),
     (dict(out=GOOD_BASE + 512), ll.LL_ERR_INVALID),   # out overlaps the region
@@ -95,6 +97,17 @@ def test_rs_ag_argument_checks():
     assert ag(GOOD_BASE, stride, GOOD_OUT, 0, BF16, 8, 1, 0, 0) == ll.LL_OK
 
 
+def test_fill_sentinel_and_auto_sentinel_argument_checks():
+    assert ll.ll_fill_sentinel(0, 16, F32, 4, 0) == ll.LL_ERR_INVALID
+    assert ll.ll_fill_sentinel(GOOD_OUT + 8, 16, F32, 4, 0) == ll.LL_ERR_INVALID
+    assert ll.ll_fill_sentinel(GOOD_OUT, 16, F32, 9, 0) == ll.LL_ERR_INVALID
+    assert ll.ll_fill_sentinel(GOOD_OUT, 16, 4, 4, 0) == ll.LL_ERR_UNSUPPORTED
+    assert ll.ll_fill_sentinel(GOOD_OUT, 0, BF16, 4, 0) == ll.LL_OK
+    assert ll.ll_set_auto_sentinel(2) == ll.LL_ERR_INVALID
+    assert ll.ll_set_auto_sentinel(1) == ll.LL_OK
+    assert ll.ll_set_auto_sentinel(0) == ll.LL_OK
+
+
 def test_init_argument_checks():
     assert ll.ll_init(0, 4096, 4, 0) == ll.LL_ERR_INVALID
     assert ll.ll_init(GOOD_BASE, 4096, 1, 0) == ll.LL_ERR_INVALID
@@ -114,8 +127,10 @@ def test_slice_bytes_gives_enough_capacity(dt, es, p):
         st, cap = ll.ll_input_capacity(stride, p)
         assert st == ll.LL_OK
         assert cap >= count * es and cap % 256 == 0
-        # the region is not much larger than the input plus the slots it needs
-        assert stride <= 24 * max(cap, 256) + 4 * 1024 * p
+        # the region is not much larger than the input plus the slots it needs:
+        # P-1 one-shot slots per area at 2x (8-byte packets), 128/120x (lines)
+        # and 1x (sentinel) the input, plus per-slot rounding
+        assert stride <= (1 + (p - 1) * (2 + 128 / 120 + 1) * 1.02) * max(cap, 256) + 8 * 1024 * p
 
 
 def test_slice_bytes_argument_checks():
@@ -123,6 +138,22 @@ def test_slice_bytes_argument_checks():
     assert ll.ll_slice_bytes(10, 5, 4)[0] == ll.LL_ERR_UNSUPPORTED
     assert ll.ll_slice_bytes((256 << 20) // 4 + 1, F32, 4)[0] == ll.LL_ERR_UNSUPPORTED
     assert ll.ll_input_capacity(1000, 4)[0] == ll.LL_ERR_INVALID
+
+
+@pytest.mark.parametrize("p", [2, 5, 8])
+def test_slice_layout_areas_are_ordered_and_fit(p):
+    for count in [1, 1000, 7168, 1 << 20]:
+        stride = ll.ll_slice_bytes(count, F32, p)[1] + 512
+        st, offs = ll.ll_slice_layout(stride, p)
+        assert st == ll.LL_OK
+        assert offs[0] == 0 and offs[1] == ll.ll_input_capacity(stride, p)[1]
+        assert all(a < b for a, b in zip(offs, offs[1:])) and offs[4] <= stride
+        assert all(o % 256 == 0 for o in offs)
+        # every 16-byte sentinel slot of one rank pair holds count*4 bytes
+        assert offs[4] - offs[3] >= 2 * (p - 1) * ((count * 4 + p - 1) // p)
+        assert offs[4] - offs[3] >= (p - 1) * count * 4
+    assert ll.ll_slice_layout(1000, p)[0] == ll.LL_ERR_INVALID
+    assert ll.ll_slice_layout(256, p)[0] == ll.LL_ERR_SCRATCH
 
 
 def test_capacity_is_a_function_of_stride_and_ranks_only():

@@ -24,8 +24,9 @@ if torch.cuda.is_available():
 else:  # pragma: no cover
     pytest.skip("no GPU", allow_module_level=True)
 
-AR_ALGOS = ["oneshot", "twoshot", "twoshot_line", "oneshot_line", "oneshot_waves", "auto"]
-PROTOS = ["packet8", "line128"]
+AR_ALGOS = ["oneshot", "twoshot", "twoshot_line", "oneshot_line", "oneshot_waves", "oneshot_sentinel",
+            "twoshot_sentinel", "auto"]
+PROTOS = ["packet8", "line128", "sentinel"]
 NP = {"f32": np.uint32, "bf16": np.uint16}
 
 
@@ -252,6 +253,9 @@ def test_result_independent_of_launch_shape(algo):
     reg.init()
     for wg, threads in [(1, 64), (1, 1024), (3, 256), (16, 128), (0, 0)]:
         ll.ll_set_launch(wg, threads)
+        if algo == "twoshot_sentinel":  # the direct-output variant shares the launch shapes
+            say(f"launch twoshot_sentinel_out wg={wg} threads={threads}")
+            assert_bits_equal(run_allreduce(reg, x, "twoshot_sentinel_out"), want, f"direct wg={wg} t={threads}")
         for units in ([1, 2, 4, 0] if algo == "oneshot_waves" else [0]):
             ll.ll_set_wave_units(units)
             say(f"launch {algo} wg={wg} threads={threads} units={units}")
@@ -272,7 +276,7 @@ def test_result_independent_of_pipeline_lag(lag):
     try:
         for wg, threads in [(1, 64), (4, 256), (0, 0)]:
             ll.ll_set_launch(wg, threads)
-            for algo in ("twoshot", "twoshot_line"):
+            for algo in ("twoshot", "twoshot_line", "twoshot_sentinel", "twoshot_sentinel_out"):
                 say(f"lag={lag} {algo} wg={wg} t={threads}")
                 assert_bits_equal(run_allreduce(reg, x, algo), want, f"{algo} lag={lag} wg={wg}")
             m = n // p
@@ -299,7 +303,9 @@ def test_large_epochs_and_reinit():
     reg = SymRegion(p, n, "f32")
     reg.init()
     reg.write_inputs(x)
-    for algo, e in zip(AR_ALGOS, (0x7FFFFFFF, 0x80000000, 0xFFFFFFFC, 0xFFFFFFFD, 0xFFFFFFFE, 0xFFFFFFFF)):
+    epochs = (0x7FFFFFFF, 0x80000000, 0xFFFFFFF8, 0xFFFFFFF9, 0xFFFFFFFA, 0xFFFFFFFC, 0xFFFFFFFE, 0xFFFFFFFF)
+    assert len(epochs) == len(AR_ALGOS)
+    for algo, e in zip(AR_ALGOS, epochs):
         check_ok(reg.allreduce(n, algo, epoch=e), f"epoch {e:#x}")
         assert_bits_equal(reg.read_out(p * n, np.uint32).reshape(p, n), want, f"{algo} epoch {e:#x}")
     reg.init()
@@ -317,7 +323,7 @@ def test_count_zero_is_a_no_op():
 
 
 # ------------------------------------------------------------ failure handling
-@pytest.mark.parametrize("algo", ["oneshot", "twoshot_line"])
+@pytest.mark.parametrize("algo", ["oneshot", "twoshot_line", "oneshot_sentinel", "twoshot_sentinel"])
 def test_missing_peer_times_out_and_is_reported(algo):
     """Rank 3 publishes nothing; its peers' bounded waits expire (after 2 ms),
     every kernel still finishes, and ll_check reports the timeout.  (In two-shot
@@ -334,7 +340,7 @@ def test_missing_peer_times_out_and_is_reported(algo):
     assert ll.ll_check(stream()) == ll.LL_ERR_TIMEOUT
     rank, missing, epoch = ll.ll_last_timeout()
     assert epoch == reg.epoch and missing != 0
-    if algo == "oneshot":
+    if algo.startswith("oneshot"):
         # only rank 3's packets are missing; the first rank to give up names it
         assert rank != 3 and missing == (1 << 3)
     ll.ll_debug_mute_rank(-1)
@@ -358,3 +364,164 @@ def test_next_epoch_sees_new_inputs():
     reg.write_inputs(b)
     check_ok(reg.allreduce(n, "oneshot", epoch=6), "b")
     assert_bits_equal(reg.read_out(p * n, np.uint32).reshape(p, n), oracle.allreduce(b), "epoch 6")
+
+
+# ------------------------------------------------------------ sentinel mode
+SENT = 0xFFFFFFFF
+
+
+@pytest.mark.parametrize("algo", ["oneshot_sentinel", "twoshot_sentinel"])
+def test_sentinel_slots_are_restored_after_every_call(algo):
+    """Sentinel mode resets every slot it has read (Sec. IV, Sentinel): after
+    a call the sentinel area holds only the sentinel again, and the flagged
+    packet areas are untouched by sentinel calls."""
+    p, n = 8, 40_000
+    x = wl.normal(p, n, "bf16", seed=21)
+    reg = SymRegion(p, n, "bf16")
+    reg.init()
+    assert (reg.read_area(3) == SENT).all() and (reg.read_area(1) == 0).all() and (reg.read_area(2) == 0).all()
+    for k in range(3):
+        say(f"sentinel restore {algo} call {k}")
+        assert_bits_equal(run_allreduce(reg, x, algo), oracle.allreduce(x), f"{algo} call {k}")
+        area = reg.read_area(3)
+        assert (area == SENT).all(), f"{algo}: {(area != SENT).sum()} words not reset after call {k}"
+    assert (reg.read_area(1) == 0).all() and (reg.read_area(2) == 0).all()
+    m = n // p
+    for proto_call in ("rs", "ag"):
+        reg.write_inputs(x)
+        st = reg.reduce_scatter(m, "sentinel") if proto_call == "rs" else reg.allgather(m, "sentinel")
+        check_ok(st, proto_call)
+        assert (reg.read_area(3) == SENT).all(), f"{proto_call}: slots not reset"
+
+
+@pytest.mark.parametrize("algo", ["oneshot_sentinel", "twoshot_sentinel"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_data_equal_to_sentinel_times_out_and_reinit_recovers(algo, dtype):
+    """A payload word equal to the sentinel is never seen as arrived (the
+    hazard of Sec. IV, Sentinel): the waits on it expire, ll_check reports
+    the timeout, and after ll_init a call on clean data is exact again.  The
+    flagged protocols carry the same data without trouble."""
+    p, n = 4, 2048
+    x = wl.uniform(p, n, dtype, seed=5)
+    bad = x.copy()
+    if dtype == "f32":
+        bad[2, 17] = SENT
+    else:
+        bad[2, 16] = bad[2, 17] = 0xFFFF  # one dword of two -NaN halves
+    reg = SymRegion(p, n, dtype)
+    reg.init()
+    reg.write_inputs(bad)
+    ll.ll_set_poll_timeout(200_000)  # 2 ms
+    say(f"sentinel-valued data {algo} {dtype}")
+    assert reg.allreduce(n, algo) == ll.LL_OK
+    assert ll.ll_check(stream()) == ll.LL_ERR_TIMEOUT
+    rank, missing, _ = ll.ll_last_timeout()
+    assert missing != 0
+    if algo == "oneshot_sentinel":
+        assert rank != 2 and missing == (1 << 2)
+    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
+    # the flagged one-shot handles the same words (NaN propagates through the sum)
+    reg.init()
+    check_ok(reg.allreduce(n, "oneshot"), "flagged on sentinel-valued data")
+    got = reg.read_out(p * n, NP[dtype]).reshape(p, n)
+    want = oracle.allreduce(bad)
+    ok = np.ones(n, bool)
+    ok[16:18] = False
+    assert np.array_equal(got[:, ok], want[:, ok])
+    reg.init()
+    reg.write_inputs(x)
+    check_ok(reg.allreduce(n, algo), "after re-init")
+    assert_bits_equal(reg.read_out(p * n, NP[dtype]).reshape(p, n), oracle.allreduce(x), f"{algo} after re-init")
+
+
+def test_sentinel_and_flagged_calls_interleave():
+    """Sentinel and flagged calls share one region call after call (each
+    protocol keeps to its own area), 50 calls, inputs changing every call."""
+    p, n = 8, 7168
+    reg = SymRegion(p, n, "bf16")
+    reg.init()
+    algos = ["oneshot_sentinel", "oneshot", "twoshot_sentinel", "twoshot_line", "oneshot_waves"]
+    for k in range(50):
+        x = wl.uniform(p, n, "bf16", seed=1000 + k)
+        algo = algos[k % len(algos)]
+        assert_bits_equal(run_allreduce(reg, x, algo), oracle.allreduce(x), f"interleave {algo} call {k}")
+
+
+# ------------------------------------------------ sentinel-initialised output
+DIRECT_CASES = [(2, 4, "f32"), (3, 300, "f32"), (4, 12, "f32"), (5, 1004, "f32"), (8, 4, "f32"), (8, 1000, "f32"),
+                (8, 8192, "f32"), (8, 65544, "f32"), (8, 8, "bf16"), (8, 7168, "bf16"), (8, 8192, "bf16"),
+                (7, 4000, "bf16"), (8, 1 << 19, "bf16"), (4, 96, "bf16")]
+
+
+def test_direct_output_twoshot_parity():
+    """Two-shot sentinel with the AllGather stored straight into the peers'
+    sentinel-filled outputs: bit-exact on sizes that leave the last chunk
+    short or some chunks empty, several calls in a row on one region."""
+    for p, n, dtype in DIRECT_CASES:
+        x = wl.normal(p, n, dtype, seed=n + p)
+        want = oracle.allreduce(x)
+        reg = SymRegion(p, n, dtype)
+        reg.init()
+        for k in range(2):
+            say(f"direct P={p} n={n} {dtype} call {k}")
+            assert_bits_equal(run_allreduce(reg, x, "twoshot_sentinel_out"), want, f"direct P={p} n={n} {dtype}")
+        assert (reg.read_area(3) == SENT).all()
+
+
+def test_direct_output_needs_16_byte_rows():
+    x = wl.uniform(4, 1001, "f32", seed=3)  # (fresh device memory may hold the sentinel)
+    reg = SymRegion(4, 1001, "f32")
+    reg.init()
+    reg.write_inputs(x)
+    assert reg.allreduce(1001, "twoshot_sentinel_out") == ll.LL_ERR_UNSUPPORTED
+    check_ok(reg.allreduce(1000, "twoshot_sentinel_out"), "1000 elements")
+    assert_bits_equal(reg.read_out(4 * 1000, np.uint32).reshape(4, 1000), oracle.allreduce(x[:, :1000].copy()),
+                      "1000 elements")
+
+
+def test_fill_sentinel_sets_exactly_the_outputs():
+    p, n = 4, 1001
+    reg = SymRegion(p, n, "bf16", out_elems=p * n + 64)
+    reg.out.zero_()
+    check_ok(ll.ll_fill_sentinel(reg.out_ptr, n, ll.LL_BF16, p, stream()), "fill")
+    b = reg.out.cpu().numpy()
+    assert (b[:p * n * 2] == 0xFF).all() and (b[p * n * 2:] == 0).all()
+
+
+def test_direct_output_missing_peer_times_out():
+    p, n = 8, 4096
+    x = wl.uniform(p, n, "f32", seed=1)
+    reg = SymRegion(p, n, "f32")
+    reg.init()
+    reg.write_inputs(x)
+    ll.ll_set_poll_timeout(200_000)
+    ll.ll_debug_mute_rank(5)
+    assert reg.allreduce(n, "twoshot_sentinel_out") == ll.LL_OK
+    assert ll.ll_check(stream()) == ll.LL_ERR_TIMEOUT
+    ll.ll_debug_mute_rank(-1)
+    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
+    reg.init()
+    check_ok(reg.allreduce(n, "twoshot_sentinel_out"), "after timeout")
+    assert_bits_equal(reg.read_out(p * n, np.uint32).reshape(p, n), oracle.allreduce(x), "after timeout")
+
+
+@pytest.mark.parametrize("p", [2, 4, 8])
+def test_auto_with_sentinel_allowed(p):
+    """With sentinel mode allowed, AUTO gives the same bits at every size."""
+    ll.ll_set_auto_sentinel(1)
+    try:
+        for n in [7, 4096, 20_000, 300_000, 3_000_001]:
+            x = wl.normal(p, n, "bf16", seed=n)
+            reg = SymRegion(p, n, "bf16")
+            reg.init()
+            say(f"auto+sentinel P={p} n={n}")
+            assert_bits_equal(run_allreduce(reg, x, "auto"), oracle.allreduce(x), f"auto+sentinel P={p} n={n}")
+            m = n // p
+            if m:
+                reg.write_inputs(x)
+                check_ok(reg.reduce_scatter(m, "auto"), "rs auto")
+                rs = reg.read_out(p * m, np.uint16).reshape(p, m)
+                assert_bits_equal(rs, oracle.reduce_scatter(x[:, :p * m].copy()), f"RS auto+sentinel P={p} m={m}")
+            del reg
+    finally:
+        ll.ll_set_auto_sentinel(0)
