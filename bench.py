@@ -247,6 +247,42 @@ def bench_c5(torch, ll, steps):
     return out
 
 
+def bench_scratch(torch, ll, iters=10, warmup=3):
+    """The paper's scratch-size study (Sec. VIII, "Impact of Scratch
+    Buffer"): a 32 MiB f32 message per rank over 8 ranks through bounded
+    scratch regions whose iterations hold 256 KiB .. 32 MiB per rank; mean
+    time per call (HIP events on the launch stream)."""
+    from paper_2607_16100_amd.region import ScratchRegion
+
+    p, n = 8, (32 << 20) // 4
+    out = {}
+    for it_kib in (256, 512, 1024, 2048, 4096, 8192, 16384, 32768):
+        reg = ScratchRegion(p, n, "f32", iter_bytes=it_kib << 10)
+        reg.init()
+        g = torch.Generator(device="cuda")
+        g.manual_seed(0)
+        reg.inp.view(torch.float32).copy_(torch.rand(p * n, generator=g, device="cuda") * 2 - 1)
+        stream = torch.cuda.current_stream()
+        row = {"iter_kib": it_kib, "scratch_slice_bytes": reg.scratch_stride}
+        for algo in ("oneshot", "oneshot_line", "oneshot_sentinel", "twoshot", "twoshot_line", "twoshot_sentinel"):
+            for _ in range(warmup):
+                ll.check(reg.allreduce(n, algo), algo)
+            ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            ev0.record(stream)
+            for _ in range(iters):
+                ll.check(reg.allreduce(n, algo), algo)
+            ev1.record(stream)
+            torch.cuda.synchronize()
+            ll.check(ll.ll_check(stream.cuda_stream), algo)
+            row[algo] = round(ev0.elapsed_time(ev1) * 1000.0 / iters, 2)
+            row["iterations"] = reg.last_iters
+        out[f"{it_kib}KiB"] = row
+        log(json.dumps(row))
+        del reg
+    return out
+
+
 def bench_sweep(torch, ll, path):
     """C4: 8 ranks, binary32, 2 .. 2^26 elements per rank; p50/p99 and GB/s of
     every algorithm at every size (written to `path` as JSON lines)."""
@@ -411,7 +447,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--bw-iters", type=int, default=20)
-    ap.add_argument("--only", default="", help="comma list of sections: headline,floor,sol,bw,c3,c5,copy,cpu")
+    ap.add_argument("--only", default="", help="comma list of sections: headline,floor,sol,bw,c3,c5,scratch,copy,cpu")
     ap.add_argument("--sweep", default="", help="also run the full C4 size sweep, writing JSON lines to this file")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -460,6 +496,9 @@ def main():
         log("C5: reduce-scatter / all-gather")
         result["c5"] = bench_c5(torch, ll, min(args.steps, 1000))
         log(json.dumps(result["c5"]))
+    if want("scratch"):
+        log("scratch-size study: 32 MiB f32, 8 ranks")
+        result["scratch"] = bench_scratch(torch, ll)
     if args.sweep:
         log("C4 sweep")
         result["sweep_file"] = bench_sweep(torch, ll, args.sweep)

@@ -172,6 +172,52 @@ int ll_allgather(void *sym_base, size_t rank_stride, void *out, size_t sendcount
 int ll_allgather_proto(void *sym_base, size_t rank_stride, void *out, size_t sendcount,
                        ll_dtype dt, int nranks, uint32_t epoch, void *stream, ll_proto proto);
 
+/* ---- bounded scratch: multi-iteration AllReduce with double buffering ----
+ *
+ * Sec. IV ("Bidirectional Communication & Double Buffering") and Sec. V
+ * (round-robin sub-buffers).  The inputs live outside the scratch region:
+ * rank r's input is `count` elements at in + r*count*esize, its output at
+ * out + r*count*esize (in == out is an in-place AllReduce).  The scratch
+ * region is nranks slices of scratch_stride bytes; each slice holds, per
+ * packet format, two sub-buffers for an iteration of D bytes per rank
+ * (ll_scratch_iter_bytes).  A call of M = count*esize bytes per rank runs in
+ * k = ceil(M / D) iterations inside one kernel: iteration i moves elements
+ * [i*D/esize, (i+1)*D/esize) of every rank through sub-buffer i % 2 with the
+ * flag epoch + i.  No barrier separates iterations: a lane writes a peer's
+ * sub-buffer again only after it has received that peer's packets of the
+ * previous iteration, which the peer sends only after it has read the
+ * sub-buffer (each receive is the credit for the next send).  In sentinel
+ * mode every lane also waits for its slot resets to be acknowledged before
+ * the next iteration.
+ *
+ * Epochs: such a call uses the k epochs epoch .. epoch+k-1 (*epochs_used =
+ * k, 0 when count is 0); the next call on the same scratch region must use an
+ * epoch above epoch+k-1.  Packet areas are never shared with a region of the
+ * other kind: scratch regions have their own init (ll_scratch_init). */
+
+/* Minimum scratch_stride (bytes, multiple of 256) for iterations of
+ * `iter_bytes` bytes per rank (1 .. 256 MiB). */
+int ll_scratch_bytes(size_t iter_bytes, int nranks, size_t *min_scratch_stride);
+
+/* Iteration size D (bytes per rank, a multiple of 256) of a scratch region;
+ * LL_ERR_SCRATCH if the stride holds no iteration at all. */
+int ll_scratch_iter_bytes(size_t scratch_stride, int nranks, size_t *iter_bytes);
+
+/* Zero the flagged sub-buffers and fill the sentinel sub-buffers of every
+ * scratch slice, on `stream`.  Call after allocating, after epoch
+ * 0xFFFFFFFF, and after a timed-out call. */
+int ll_scratch_init(void *scratch_base, size_t scratch_stride, int nranks, void *stream);
+
+/* AllReduce (sum) through a bounded scratch region.  in, out: 16-byte
+ * aligned device memory, equal (in place) or disjoint, neither overlapping
+ * the scratch region; scratch_base 256-byte aligned.  algo as for
+ * ll_allreduce_algo (LL_ALGO_ONESHOT_WAVES only for one iteration;
+ * LL_ALGO_TWOSHOT_SENTINEL_OUT not in place).  count*esize at most 16 GiB.
+ * epochs_used may be NULL.  One kernel launch on `stream`. */
+int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, ll_op op, int nranks,
+                          void *scratch_base, size_t scratch_stride, uint32_t epoch, void *stream, ll_algo algo,
+                          uint32_t *epochs_used);
+
 /* Synchronise `stream`, then report and clear the device status word:
  * LL_OK, LL_ERR_TIMEOUT, or LL_ERR_HIP. */
 int ll_check(void *stream);

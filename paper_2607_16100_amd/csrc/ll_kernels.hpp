@@ -39,8 +39,24 @@ struct KArgs {
   uint16_t first_wait;  // idle time before the first poll, in units of 64 shader cycles
   uint16_t poll_gap;    // idle time between polls, in units of 64 shader cycles
   uint32_t lag;         // two-shot pipeline distance between publish, reduce and gather (>= 1)
-  uint32_t pad2_;
+  uint32_t in_al4;      // every rank's input starts 4-byte aligned
+  const char *in;       // rank r's input at in + r * in_stride
+  uint64_t in_stride;
+  // Multi-iteration calls (bounded scratch, Sec. IV "Bidirectional
+  // Communication & Double Buffering"): iteration i covers elements
+  // [i * iter_n, (i+1) * iter_n) of every rank, uses sub-buffer i % 2 of the
+  // area (sub_bytes apart) and the flag epoch + i.  One iteration: iters = 1,
+  // iter_n = n.
+  int64_t iter_n;
+  uint64_t sub_bytes;
+  uint32_t iters;
+  uint32_t pad3_;
 };
+
+// Wait until every store this wave has issued is acknowledged.  Used between
+// iterations in sentinel mode: a slot reset must be complete before the
+// next iteration's packets, which let a peer refill that slot, go out.
+__device__ __forceinline__ void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0x0f70); }  // vmcnt(0)
 
 __device__ __forceinline__ int slot_of(int src, int dst) { return src - (src > dst ? 1 : 0); }
 
@@ -176,39 +192,48 @@ __global__ __launch_bounds__(1024) void k_oneshot(KArgs a) {
   constexpr int E = Elem<DT>::kBytes;
   const uint64_t deadline = now_ticks() + a.timeout;
   char *const slice_r = a.sym + (uint64_t)r * a.stride;
-  const int64_t n = a.n;
-  const int64_t units = Pr::units((n * E + 3) / 4);
-  char *const out_r = a.out + (uint64_t)r * (uint64_t)n * E;
-
-  char *const area_r = slice_r + a.area;
+  const char *const in_r = a.in + (uint64_t)r * a.in_stride;
+  char *const out_r = a.out + (uint64_t)r * (uint64_t)a.n * E;
   const bool publish = (r != a.mute);
+  const bool in_al4 = a.in_al4 != 0;
   const int64_t g = (int64_t)pt.w * blockDim.x + threadIdx.x;
   const int sub = (int)(g % Pr::kLanes);
   const int64_t ustep = (int64_t)pt.W * blockDim.x / Pr::kLanes;
 
-  for (int64_t u = g / Pr::kLanes; u < units; u += ustep) {
-    const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
-    const u32x4 own = Pr::template load<DT>(slice_r, u, sub, n, true);
-    uint64_t t_loaded = 0, t_acked = 0;
-    if (a.phases != nullptr) t_loaded = now_ticks() + (own.x & 0u);
-    if (publish) bcast<P>(a, a.area, r, off, Pr::pack(own, a.epoch, sub));
-    if (a.phases != nullptr) {
-      __asm__ __volatile__("s_waitcnt vmcnt(0)" ::: "memory");
-      t_acked = now_ticks();
-    }
-    u32x4 got[P];
-    const int spins = poll_all<Pr, P>(area_r, a.slot, off, r, a.epoch, deadline, got, a.first_wait, a.poll_gap);
-    if (a.phases != nullptr && threadIdx.x == 0) {
-      const uint64_t t_polled = now_ticks() + (got[(r + 1) % P].x & 0u);
-      a.phases[4 * blockIdx.x + 0] = t_loaded;
-      a.phases[4 * blockIdx.x + 1] = t_acked;
-      a.phases[4 * blockIdx.x + 2] = t_polled;
-      a.phases[4 * blockIdx.x + 3] = (uint64_t)spins;
-    }
+  for (uint32_t it = 0; it < a.iters; ++it) {
+    const int64_t e0 = (int64_t)it * a.iter_n;
+    const int64_t n = a.n - e0 < a.iter_n ? a.n - e0 : a.iter_n;
+    const int64_t units = Pr::units((n * E + 3) / 4);
+    const uint64_t area = a.area + (uint64_t)(it & 1u) * a.sub_bytes;
+    const uint32_t epoch = a.epoch + it;
+    char *const area_r = slice_r + area;
+    const char *const in_i = in_r + e0 * E;
+    char *const out_i = out_r + e0 * E;
+    for (int64_t u = g / Pr::kLanes; u < units; u += ustep) {
+      const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+      const u32x4 own = Pr::template load<DT>(in_i, u, sub, n, in_al4);
+      uint64_t t_loaded = 0, t_acked = 0;
+      if (a.phases != nullptr) t_loaded = now_ticks() + (own.x & 0u);
+      if (publish) bcast<P>(a, area, r, off, Pr::pack(own, epoch, sub));
+      if (a.phases != nullptr) {
+        __asm__ __volatile__("s_waitcnt vmcnt(0)" ::: "memory");
+        t_acked = now_ticks();
+      }
+      u32x4 got[P];
+      const int spins = poll_all<Pr, P>(area_r, a.slot, off, r, epoch, deadline, got, a.first_wait, a.poll_gap);
+      if (a.phases != nullptr && threadIdx.x == 0) {
+        const uint64_t t_polled = now_ticks() + (got[(r + 1) % P].x & 0u);
+        a.phases[4 * blockIdx.x + 0] = t_loaded;
+        a.phases[4 * blockIdx.x + 1] = t_acked;
+        a.phases[4 * blockIdx.x + 2] = t_polled;
+        a.phases[4 * blockIdx.x + 3] = (uint64_t)spins;
+      }
 #pragma unroll
-    for (int q = 0; q < P; ++q) got[q] = Pr::unpack(got[q], sub);
-    const u32x4 res = reduce_ordered<Pr, DT, P>(got, own, r);
-    Pr::template store<DT>(out_r, u, sub, n, a.al4 != 0, res);
+      for (int q = 0; q < P; ++q) got[q] = Pr::unpack(got[q], sub);
+      const u32x4 res = reduce_ordered<Pr, DT, P>(got, own, r);
+      Pr::template store<DT>(out_i, u, sub, n, a.al4 != 0, res);
+    }
+    if (ResetsSlots<Pr>::value && it + 1 < a.iters) wait_vm_all();
   }
   stamp_end(a);
 }
@@ -255,6 +280,7 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs a) {
   const int lane = (int)(threadIdx.x & 63);
   const uint64_t deadline = now_ticks() + a.timeout;
   char *const slice_r = a.sym + (uint64_t)r * a.stride;
+  const char *const in_r = a.in + (uint64_t)r * a.in_stride;
   const int64_t n = a.n;
   const int64_t words = (n * E + 3) / 4;
   const int64_t units = ProtoLL::units(words);
@@ -282,7 +308,7 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs a) {
 #pragma unroll
     for (int k = 0; k < U; ++k) {
       const int64_t u = tile * 64 * U + k * 64 + lane;
-      own[k] = u < units ? load_words<DT>(slice_r, 2 * u, 2, n, true) : u32x4{0u, 0u, 0u, 0u};
+      own[k] = u < units ? load_words<DT>(in_r, 2 * u, 2, n, a.in_al4 != 0) : u32x4{0u, 0u, 0u, 0u};
     }
     if (a.phases != nullptr && lane == 0 && tile == pt.w) {
       a.phases[4 * (blockIdx.x * P + wv) + 0] = now_ticks() + (own[0].x & 0u);
@@ -416,11 +442,16 @@ struct TwoShot {
   const KArgs &a;
   int r;
   char *slice_r;
+  // the current iteration: its input and output (rank r), its elements, its
+  // chunk length, its RS and AG slot offsets and its flag
+  const char *in_r;
   char *out_r;
+  uint64_t out_off;  // byte offset of the iteration within every rank's output
   int64_t n, C;
-  uint64_t ag_area;
+  uint64_t rs_area, ag_area;
+  uint32_t epoch;
   uint64_t deadline;
-  bool publish, al4;
+  bool publish, al4, in_al4;
 
   __device__ __forceinline__ int64_t chunk_len(int c) const {
     const int64_t left = n - (int64_t)c * C;
@@ -433,22 +464,22 @@ struct TwoShot {
 #pragma unroll
     for (int k = 1; k < P; ++k) {
       const int c = (r + k) % P;
-      v[k] = Pr::template load<DT>(slice_r + c * C * E, u, sub, chunk_len(c), true);
+      v[k] = Pr::template load<DT>(in_r + c * C * E, u, sub, chunk_len(c), in_al4);
     }
 #pragma unroll
     for (int k = 1; k < P; ++k) {
       const int c = (r + k) % P;
-      char *dst = a.sym + (uint64_t)c * a.stride + a.area + (uint64_t)slot_of(r, c) * a.slot;
-      st_pkt(make_rsrc(dst, (uint32_t)a.slot), off, Pr::pack(v[k], a.epoch, sub));
+      char *dst = a.sym + (uint64_t)c * a.stride + rs_area + (uint64_t)slot_of(r, c) * a.slot;
+      st_pkt(make_rsrc(dst, (uint32_t)a.slot), off, Pr::pack(v[k], epoch, sub));
     }
   }
 
   __device__ __forceinline__ void step_reduce(int64_t u, int sub) const {
     const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
     const int64_t nr = chunk_len(r);
-    const u32x4 own = Pr::template load<DT>(slice_r + r * C * E, u, sub, nr, true);
+    const u32x4 own = Pr::template load<DT>(in_r + r * C * E, u, sub, nr, in_al4);
     u32x4 got[P];
-    poll_all<Pr, P>(slice_r + a.area, a.slot, off, r, a.epoch, deadline, got);
+    poll_all<Pr, P>(slice_r + rs_area, a.slot, off, r, epoch, deadline, got);
 #pragma unroll
     for (int q = 0; q < P; ++q) got[q] = Pr::unpack(got[q], sub);
     const u32x4 res = reduce_ordered<Pr, DT, P>(got, own, r);
@@ -460,10 +491,11 @@ struct TwoShot {
 #pragma unroll
       for (int k = 1; k < P; ++k) {
         const int q = (r + k) % P;
-        st_pkt_at(make_rsrc(a.out + (uint64_t)q * (uint64_t)n * E, (uint32_t)(n * E)), off, at, res);
+        char *out_q = a.out + (uint64_t)q * (uint64_t)a.n * E + out_off;
+        st_pkt_at(make_rsrc(out_q, (uint32_t)(n * E)), off, at, res);
       }
     } else {
-      bcast<P>(a, ag_area, r, off, Pr::pack(res, a.epoch, sub));
+      bcast<P>(a, ag_area, r, off, Pr::pack(res, epoch, sub));
     }
   }
 
@@ -474,11 +506,11 @@ struct TwoShot {
 #pragma unroll
       for (int q = 0; q < P; ++q)
         if (q != r && (int64_t)off < chunk_len(q) * E) pend |= 1u << q;
-      poll_out<P>(out_r, (uint32_t)(n * E), (uint32_t)(C * E), off, pend, r, a.epoch, deadline);
+      poll_out<P>(out_r, (uint32_t)(n * E), (uint32_t)(C * E), off, pend, r, epoch, deadline);
       return;
     }
     u32x4 got[P];
-    poll_all<Pr, P>(slice_r + ag_area, a.slot, off, r, a.epoch, deadline, got);
+    poll_all<Pr, P>(slice_r + ag_area, a.slot, off, r, epoch, deadline, got);
 #pragma unroll
     for (int q = 0; q < P; ++q) {
       if (q == r) continue;
@@ -491,6 +523,13 @@ struct TwoShot {
 #define LLCOLL_TWOSHOT_WAVES_PER_EU 1
 #endif
 
+// Two-shot chunk of an iteration of n elements: ceil(n / P) rounded up to 16 bytes.
+template <int P, int E>
+__device__ __forceinline__ int64_t chunk_of(int64_t n) {
+  constexpr int64_t g = 16 / E;
+  return ((n + P - 1) / P + g - 1) / g * g;
+}
+
 template <class Pr, int DT, int P, bool Direct = false>
 __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(LLCOLL_TWOSHOT_WAVES_PER_EU))) void k_twoshot(
     KArgs a) {
@@ -501,23 +540,34 @@ __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(LLCOLL_TWO
   constexpr int E = Elem<DT>::kBytes;
   t.deadline = now_ticks() + a.timeout;
   t.slice_r = a.sym + (uint64_t)t.r * a.stride;
-  t.n = a.n;
-  t.C = a.chunk;
-  t.out_r = a.out + (uint64_t)t.r * (uint64_t)t.n * E;
-  t.ag_area = a.area + (uint64_t)(P - 1) * a.slot;
   t.publish = (t.r != a.mute);
   t.al4 = a.al4 != 0;
-  const int64_t units = Pr::units((t.C * E + 3) / 4);
+  t.in_al4 = a.in_al4 != 0;
+  const char *const in_r = a.in + (uint64_t)t.r * a.in_stride;
+  char *const out_r = a.out + (uint64_t)t.r * (uint64_t)a.n * E;
   const int64_t g = (int64_t)pt.w * blockDim.x + threadIdx.x;
   const int sub = (int)(g % Pr::kLanes);
   const int64_t u0 = g / Pr::kLanes;
   const int64_t ustep = (int64_t)pt.W * blockDim.x / Pr::kLanes;
-  const int64_t steps = u0 < units ? (units - u0 + ustep - 1) / ustep : 0;
   const int64_t lag = a.lag > 0 ? a.lag : 1;
-  for (int64_t s = 0; s < steps + 2 * lag; ++s) {
-    if (s < steps && t.publish) t.step_publish(u0 + s * ustep, sub);
-    if (s >= lag && s - lag < steps) t.step_reduce(u0 + (s - lag) * ustep, sub);
-    if (s >= 2 * lag && s - 2 * lag < steps) t.step_gather(u0 + (s - 2 * lag) * ustep, sub);
+  for (uint32_t it = 0; it < a.iters; ++it) {
+    const int64_t e0 = (int64_t)it * a.iter_n;
+    t.n = a.n - e0 < a.iter_n ? a.n - e0 : a.iter_n;
+    t.C = a.iters == 1 ? a.chunk : chunk_of<P, E>(t.n);
+    t.in_r = in_r + e0 * E;
+    t.out_off = (uint64_t)e0 * E;
+    t.out_r = out_r + t.out_off;
+    t.rs_area = a.area + (uint64_t)(it & 1u) * a.sub_bytes;
+    t.ag_area = t.rs_area + (uint64_t)(P - 1) * a.slot;
+    t.epoch = a.epoch + it;
+    const int64_t units = Pr::units((t.C * E + 3) / 4);
+    const int64_t steps = u0 < units ? (units - u0 + ustep - 1) / ustep : 0;
+    for (int64_t s = 0; s < steps + 2 * lag; ++s) {
+      if (s < steps && t.publish) t.step_publish(u0 + s * ustep, sub);
+      if (s >= lag && s - lag < steps) t.step_reduce(u0 + (s - lag) * ustep, sub);
+      if (s >= 2 * lag && s - 2 * lag < steps) t.step_gather(u0 + (s - 2 * lag) * ustep, sub);
+    }
+    if (ResetsSlots<Pr>::value && it + 1 < a.iters) wait_vm_all();
   }
   stamp_end(a);
 }
@@ -536,6 +586,8 @@ __global__ __launch_bounds__(1024) void k_reduce_scatter(KArgs a) {
   constexpr int E = Elem<DT>::kBytes;
   const uint64_t deadline = now_ticks() + a.timeout;
   char *const slice_r = a.sym + (uint64_t)r * a.stride;
+  const char *const in_r = a.in + (uint64_t)r * a.in_stride;
+  const bool in_al4 = a.in_al4 != 0;
   char *const out_r = a.out + (uint64_t)r * (uint64_t)a.n * E;
   const int64_t m = a.n;
   const int64_t units = Pr::units((m * E + 3) / 4);
@@ -556,7 +608,7 @@ __global__ __launch_bounds__(1024) void k_reduce_scatter(KArgs a) {
 #pragma unroll
       for (int k = 1; k < P; ++k) {
         const int c = (r + k) % P;
-        v[k] = Pr::template load<DT>(slice_r + c * m * E, u, sub, m, al4);
+        v[k] = Pr::template load<DT>(in_r + c * m * E, u, sub, m, in_al4);
       }
 #pragma unroll
       for (int k = 1; k < P; ++k) {
@@ -568,7 +620,7 @@ __global__ __launch_bounds__(1024) void k_reduce_scatter(KArgs a) {
     if (s >= lag && s - lag < steps) {
       const int64_t u = u0 + (s - lag) * ustep;
       const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
-      const u32x4 own = Pr::template load<DT>(slice_r + r * m * E, u, sub, m, al4);
+      const u32x4 own = Pr::template load<DT>(in_r + r * m * E, u, sub, m, in_al4);
       u32x4 got[P];
       poll_all<Pr, P>(slice_r + a.area, a.slot, off, r, a.epoch, deadline, got);
 #pragma unroll
@@ -593,6 +645,7 @@ __global__ __launch_bounds__(1024) void k_allgather(KArgs a) {
   constexpr int E = Elem<DT>::kBytes;
   const uint64_t deadline = now_ticks() + a.timeout;
   char *const slice_r = a.sym + (uint64_t)r * a.stride;
+  const char *const in_r = a.in + (uint64_t)r * a.in_stride;
   const int64_t n = a.n;
   const int64_t units = Pr::units((n * E + 3) / 4);
   const bool al4 = a.al4 != 0;
@@ -609,7 +662,7 @@ __global__ __launch_bounds__(1024) void k_allgather(KArgs a) {
     if (s < steps) {
       const int64_t u = u0 + s * ustep;
       const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
-      const u32x4 own = Pr::template load<DT>(slice_r, u, sub, n, true);
+      const u32x4 own = Pr::template load<DT>(in_r, u, sub, n, a.in_al4 != 0);
       if (publish) bcast<P>(a, a.area, r, off, Pr::pack(own, a.epoch, sub));
       Pr::template store<DT>(out_r + r * n * E, u, sub, n, al4, own);
     }

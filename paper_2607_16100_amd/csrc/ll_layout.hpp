@@ -31,6 +31,7 @@ namespace layout {
 
 constexpr uint64_t kAlign = 256;
 constexpr uint64_t kMaxInputBytes = 256ull << 20;  // keeps every call's P-1 slots within 4 GiB
+constexpr uint64_t kMaxBufferedBytes = 16ull << 30;  // per-rank message of a bounded-scratch call
 
 inline uint64_t roundup(uint64_t x, uint64_t m) { return (x + m - 1) / m * m; }
 inline uint64_t ceil_div(uint64_t x, uint64_t m) { return (x + m - 1) / m; }
@@ -76,6 +77,30 @@ inline uint64_t capacity(uint64_t stride, int P) {
   while (lo < hi) {
     const uint64_t mid = (lo + hi + 1) / 2;
     if (slice_for(mid * kAlign, P) <= stride) {
+      lo = mid;
+    } else {
+      hi = mid - 1;
+    }
+  }
+  return lo * kAlign;
+}
+
+// Bounded scratch (multi-iteration calls with an input outside the region).
+// A scratch slice holds, per packet format, two sub-buffers, each sized like
+// that format's area for an input of D bytes; a call of M bytes per rank runs
+// in ceil(M / D) iterations alternating between the sub-buffers:
+//   [0, 2*A8(D))                 8-byte packet sub-buffers 0 and 1
+//   [2*A8(D), .. + 2*A128(D))    line sub-buffers 0 and 1
+//   [.., .. + 2*AS(D))           sentinel sub-buffers 0 and 1
+inline uint64_t scratch_for(uint64_t D, int P) { return 2 * (area8(D, P) + area128(D, P) + areaS(D, P)); }
+
+// Largest iteration size D (multiple of 256, at most kMaxInputBytes) whose
+// scratch fits in `stride` bytes; 0 if none does.
+inline uint64_t iter_capacity(uint64_t stride, int P) {
+  uint64_t lo = 0, hi = std::min(stride, kMaxInputBytes) / kAlign;
+  while (lo < hi) {
+    const uint64_t mid = (lo + hi + 1) / 2;
+    if (scratch_for(mid * kAlign, P) <= stride) {
       lo = mid;
     } else {
       hi = mid - 1;

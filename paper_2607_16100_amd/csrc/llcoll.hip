@@ -223,6 +223,15 @@ int launch(const Plan &pl, void *stream) {
   }
   const int grid = W * pl.P;
   KArgs a = pl.a;
+  if (a.in == nullptr) {  // input inside the region, at offset 0 of every slice
+    a.in = a.sym;
+    a.in_stride = a.stride;
+    a.in_al4 = 1;
+  }
+  if (a.iters == 0) {
+    a.iters = 1;
+    a.iter_n = a.n;
+  }
   a.timeout = g_timeout.load();
   a.mute = g_mute.load();
   a.first_wait = (uint16_t)g_first_wait.load();
@@ -329,6 +338,33 @@ ll_proto auto_proto(uint64_t bytes, int P, bool sentinel_ok) {
     return LL_PROTO_LINE128;
   }
   return bytes <= 512 * KiB ? LL_PROTO_PACKET8 : LL_PROTO_LINE128;
+}
+
+// Kernel, packet format, slot size and unit count of an AllReduce of `count`
+// elements per rank whose iterations hold `iter_count` elements.
+// area_of(proto) gives the offset of that packet format's area in a slice.
+template <class AreaOf>
+void plan_allreduce(Plan *pl, ll_algo algo, uint64_t count, int es, int nranks, uint64_t iter_count,
+                    AreaOf area_of) {
+  const uint64_t it_bytes = iter_count * (uint64_t)es;
+  const bool line = (algo == LL_ALGO_TWOSHOT_LINE || algo == LL_ALGO_ONESHOT_LINE);
+  const bool sent = (algo == LL_ALGO_ONESHOT_SENTINEL || algo == LL_ALGO_TWOSHOT_SENTINEL ||
+                     algo == LL_ALGO_TWOSHOT_SENTINEL_OUT);
+  const bool waves = (algo == LL_ALGO_ONESHOT_WAVES);
+  pl->proto = line ? PR_LINE : (sent ? PR_SENT : PR_LL);
+  pl->a.area = area_of(pl->proto);
+  if (algo == LL_ALGO_ONESHOT || algo == LL_ALGO_ONESHOT_LINE || algo == LL_ALGO_ONESHOT_SENTINEL || waves) {
+    pl->kind = waves ? K_ONESHOT_WAVES : K_ONESHOT;
+    pl->a.slot = slot_bytes(pl->proto, it_bytes);
+    pl->units = units_of(pl->proto, it_bytes);
+  } else {
+    pl->kind = algo == LL_ALGO_TWOSHOT_SENTINEL_OUT ? K_TWOSHOT_OUT : K_TWOSHOT;
+    const uint64_t C = L::twoshot_chunk(iter_count, nranks, es);
+    pl->a.chunk = (int64_t)C;
+    pl->a.slot = slot_bytes(pl->proto, C * es);
+    pl->units = units_of(pl->proto, C * es);
+  }
+  (void)count;
 }
 
 }  // namespace
@@ -443,29 +479,115 @@ int ll_allreduce_algo(void *sym_base, size_t rank_stride, void *out, size_t coun
   pl.a = base_args(sym_base, rank_stride, out, epoch);
   pl.a.n = (int64_t)count;
   pl.a.al4 = (in_bytes % 4 == 0) ? 1u : 0u;
-  const bool line = (algo == LL_ALGO_TWOSHOT_LINE || algo == LL_ALGO_ONESHOT_LINE);
-  const bool sent = (algo == LL_ALGO_ONESHOT_SENTINEL || algo == LL_ALGO_TWOSHOT_SENTINEL ||
-                     algo == LL_ALGO_TWOSHOT_SENTINEL_OUT);
-  const bool waves = (algo == LL_ALGO_ONESHOT_WAVES);
-  pl.proto = line ? PR_LINE : (sent ? PR_SENT : PR_LL);
-  pl.a.area = rg.area_of(pl.proto);
-  if (algo == LL_ALGO_ONESHOT || algo == LL_ALGO_ONESHOT_LINE || algo == LL_ALGO_ONESHOT_SENTINEL || waves) {
-    pl.kind = waves ? K_ONESHOT_WAVES : K_ONESHOT;
-    pl.a.slot = slot_bytes(pl.proto, in_bytes);
-    pl.units = units_of(pl.proto, in_bytes);
-  } else {
-    pl.kind = algo == LL_ALGO_TWOSHOT_SENTINEL_OUT ? K_TWOSHOT_OUT : K_TWOSHOT;
-    const uint64_t C = L::twoshot_chunk(count, nranks, es);
-    pl.a.chunk = (int64_t)C;
-    pl.a.slot = slot_bytes(pl.proto, C * es);
-    pl.units = units_of(pl.proto, C * es);
-  }
+  plan_allreduce(&pl, algo, count, es, nranks, count, [&](int proto) { return rg.area_of(proto); });
   return launch(pl, stream);
 }
 
 int ll_allreduce(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt, ll_op op, int nranks,
                  uint32_t epoch, void *stream) {
   return ll_allreduce_algo(sym_base, rank_stride, out, count, dt, op, nranks, epoch, stream, LL_ALGO_AUTO);
+}
+
+// ---------------------------------------------------------------- bounded scratch
+int ll_scratch_bytes(size_t iter_bytes, int nranks, size_t *min_scratch_stride) {
+  if (min_scratch_stride == nullptr) return LL_ERR_INVALID;
+  if (nranks < 2 || nranks > LL_MAX_RANKS) return LL_ERR_INVALID;
+  if (iter_bytes == 0 || iter_bytes > L::kMaxInputBytes) return LL_ERR_INVALID;
+  *min_scratch_stride = (size_t)L::scratch_for(L::roundup(iter_bytes, L::kAlign), nranks);
+  return LL_OK;
+}
+
+int ll_scratch_iter_bytes(size_t scratch_stride, int nranks, size_t *iter_bytes) {
+  if (iter_bytes == nullptr) return LL_ERR_INVALID;
+  if (nranks < 2 || nranks > LL_MAX_RANKS) return LL_ERR_INVALID;
+  if (scratch_stride == 0 || scratch_stride % LL_ALIGN != 0) return LL_ERR_INVALID;
+  const uint64_t D = L::iter_capacity(scratch_stride, nranks);
+  if (D == 0) return LL_ERR_SCRATCH;
+  *iter_bytes = (size_t)D;
+  return LL_OK;
+}
+
+int ll_scratch_init(void *scratch_base, size_t scratch_stride, int nranks, void *stream) {
+  if (scratch_base == nullptr || ((uintptr_t)scratch_base % LL_ALIGN) != 0) return LL_ERR_INVALID;
+  size_t D = 0;
+  int st = ll_scratch_iter_bytes(scratch_stride, nranks, &D);
+  if (st != LL_OK) return st;
+  DevInfo d;
+  st = device_info(&d);
+  if (st != LL_OK) return st;
+  const uint64_t mid = 2 * (L::area8(D, nranks) + L::area128(D, nranks));
+  const uint64_t hi = mid + 2 * L::areaS(D, nranks);
+  hipLaunchKernelGGL(k_fill_areas, dim3(d.cus * 4), dim3(256), 0, (hipStream_t)stream, (char *)scratch_base,
+                     (uint64_t)scratch_stride, nranks, (uint64_t)0, mid, 0u);
+  hipLaunchKernelGGL(k_fill_areas, dim3(d.cus * 4), dim3(256), 0, (hipStream_t)stream, (char *)scratch_base,
+                     (uint64_t)scratch_stride, nranks, mid, hi, ProtoSent::kSentinel);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    t_last_hip = (int)e;
+    return LL_ERR_HIP;
+  }
+  return LL_OK;
+}
+
+int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, ll_op op, int nranks,
+                          void *scratch_base, size_t scratch_stride, uint32_t epoch, void *stream, ll_algo algo,
+                          uint32_t *epochs_used) {
+  if (epochs_used != nullptr) *epochs_used = 0;
+  if (in == nullptr || out == nullptr || scratch_base == nullptr) return LL_ERR_INVALID;
+  if (((uintptr_t)in % 16) != 0 || ((uintptr_t)out % 16) != 0) return LL_ERR_INVALID;
+  if (((uintptr_t)scratch_base % LL_ALIGN) != 0) return LL_ERR_INVALID;
+  if (nranks < 2 || nranks > LL_MAX_RANKS) return LL_ERR_INVALID;
+  if (epoch == 0) return LL_ERR_INVALID;
+  int st = check_dtype_op((int)dt, (int)op);
+  if (st != LL_OK) return st;
+  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_TWOSHOT_SENTINEL_OUT) return LL_ERR_INVALID;
+  size_t D = 0;
+  st = ll_scratch_iter_bytes(scratch_stride, nranks, &D);
+  if (st != LL_OK) return st;
+  const int es = esize_of(dt);
+  if (count > (L::kMaxBufferedBytes / (uint64_t)es)) return LL_ERR_UNSUPPORTED;
+  const uint64_t in_bytes = (uint64_t)count * es;
+  if (algo == LL_ALGO_TWOSHOT_SENTINEL_OUT && in_bytes % 16 != 0) return LL_ERR_UNSUPPORTED;
+  if (algo == LL_ALGO_TWOSHOT_SENTINEL_OUT && in == out) return LL_ERR_INVALID;  // its output starts as sentinels
+  const uint64_t all = in_bytes * (uint64_t)nranks, sbytes = (uint64_t)scratch_stride * nranks;
+  if (in != out && overlaps(in, all, out, all)) return LL_ERR_INVALID;  // in place, or apart
+  if (overlaps(in, all, scratch_base, sbytes) || overlaps(out, all, scratch_base, sbytes)) return LL_ERR_INVALID;
+  if (count == 0) return LL_OK;
+  const uint64_t iter_count = std::min<uint64_t>(count, D / (uint64_t)es);
+  const uint64_t iters = (count + iter_count - 1) / iter_count;
+  if ((uint64_t)epoch + iters - 1 > 0xFFFFFFFFull) return LL_ERR_INVALID;
+  if (algo == LL_ALGO_AUTO) {
+    // With several small iterations, two-shot pays its second exchange per
+    // iteration; one-shot lines win below 512 KiB per iteration (measured,
+    // 32 MiB at 8 ranks, the paper's scratch study shape).
+    if (iters > 1 && iter_count * es < (512u << 10)) {
+      algo = LL_ALGO_ONESHOT_LINE;
+    } else {
+      algo = auto_algo(iter_count * es, nranks, g_auto_sentinel.load() != 0);
+      if (iters > 1 && algo == LL_ALGO_ONESHOT_WAVES) algo = LL_ALGO_ONESHOT;
+    }
+  }
+  if (iters > 1 && algo == LL_ALGO_ONESHOT_WAVES) return LL_ERR_UNSUPPORTED;
+
+  Plan pl;
+  pl.dt = (int)dt;
+  pl.P = nranks;
+  pl.a = base_args(scratch_base, scratch_stride, out, epoch);
+  pl.a.in = (const char *)in;
+  pl.a.in_stride = in_bytes;
+  pl.a.in_al4 = (in_bytes % 4 == 0) ? 1u : 0u;
+  pl.a.n = (int64_t)count;
+  pl.a.al4 = (in_bytes % 4 == 0) ? 1u : 0u;
+  pl.a.iters = (uint32_t)iters;
+  pl.a.iter_n = (int64_t)iter_count;
+  const uint64_t a8 = L::area8(D, nranks), a128 = L::area128(D, nranks), as = L::areaS(D, nranks);
+  plan_allreduce(&pl, algo, count, es, nranks, iter_count, [&](int proto) {
+    return proto == PR_LINE ? 2 * a8 : (proto == PR_SENT ? 2 * (a8 + a128) : (uint64_t)0);
+  });
+  pl.a.sub_bytes = pl.proto == PR_LINE ? a128 : (pl.proto == PR_SENT ? as : a8);
+  st = launch(pl, stream);
+  if (st == LL_OK && epochs_used != nullptr) *epochs_used = (uint32_t)iters;
+  return st;
 }
 
 int ll_reduce_scatter_proto(void *sym_base, size_t rank_stride, void *out, size_t recvcount, ll_dtype dt,

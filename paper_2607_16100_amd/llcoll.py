@@ -48,6 +48,10 @@ _SIGS = {
     "ll_slice_layout": (_i, [_sz, _i, ctypes.POINTER(_sz)]),
     "ll_init": (_i, [_vp, _sz, _i, _vp]),
     "ll_fill_sentinel": (_i, [_vp, _sz, _i, _i, _vp]),
+    "ll_scratch_bytes": (_i, [_sz, _i, ctypes.POINTER(_sz)]),
+    "ll_scratch_iter_bytes": (_i, [_sz, _i, ctypes.POINTER(_sz)]),
+    "ll_scratch_init": (_i, [_vp, _sz, _i, _vp]),
+    "ll_allreduce_buffered": (_i, [_vp, _vp, _sz, _i, _i, _i, _vp, _sz, _u32, _vp, _i, ctypes.POINTER(_u32)]),
     "ll_set_auto_sentinel": (_i, [_i]),
     "ll_allreduce": (_i, [_vp, _sz, _vp, _sz, _i, _i, _i, _u32, _vp]),
     "ll_allreduce_algo": (_i, [_vp, _sz, _vp, _sz, _i, _i, _i, _u32, _vp, _i]),
@@ -189,6 +193,30 @@ def ll_set_poll_pacing(first_wait: int, poll_gap: int):
 
 def ll_set_pipeline_lag(lag: int):
     return _lib.ll_set_pipeline_lag(lag)
+
+
+def ll_scratch_bytes(iter_bytes: int, nranks: int):
+    out = ctypes.c_size_t(0)
+    st = _lib.ll_scratch_bytes(iter_bytes, nranks, ctypes.byref(out))
+    return st, out.value
+
+
+def ll_scratch_iter_bytes(scratch_stride: int, nranks: int):
+    out = ctypes.c_size_t(0)
+    st = _lib.ll_scratch_iter_bytes(scratch_stride, nranks, ctypes.byref(out))
+    return st, out.value
+
+
+def ll_scratch_init(scratch_base, scratch_stride, nranks, stream):
+    return _lib.ll_scratch_init(scratch_base, scratch_stride, nranks, stream)
+
+
+def ll_allreduce_buffered(inp, out, count, dt, op, nranks, scratch_base, scratch_stride, epoch, stream, algo):
+    """(status, epochs used)."""
+    used = ctypes.c_uint32(0)
+    st = _lib.ll_allreduce_buffered(inp, out, count, dt, op, nranks, scratch_base, scratch_stride, epoch, stream,
+                                    algo, ctypes.byref(used))
+    return st, used.value
 
 
 def ll_fill_sentinel(out, count, dt, nranks, stream):

@@ -129,3 +129,64 @@ class SymRegion:
         e = self.next_epoch() if epoch is None else epoch
         return ll.ll_allgather_proto(self.base, self.rank_stride, self.out_ptr, sendcount, self.dt, self.nranks, e,
                                      self.stream_handle(stream), ll.PROTOS[proto])
+
+
+class ScratchRegion:
+    """Bounded scratch for multi-iteration AllReduce: P scratch slices of
+    ``scratch_stride`` bytes (sized for iterations of ``iter_bytes`` bytes
+    per rank), plus separate input and output buffers of P x ``max_count``
+    elements.  ``in_place=True`` makes the output the input buffer."""
+
+    def __init__(self, nranks: int, max_count: int, dtype: str, iter_bytes: int, device="cuda:0",
+                 in_place: bool = False):
+        self.nranks = nranks
+        self.dtype = dtype
+        self.dt = ll.DTYPES[dtype]
+        self.esize = 4 if dtype == "f32" else 2
+        st, self.scratch_stride = ll.ll_scratch_bytes(iter_bytes, nranks)
+        ll.check(st, "ll_scratch_bytes")
+        st, self.iter_bytes = ll.ll_scratch_iter_bytes(self.scratch_stride, nranks)
+        ll.check(st, "ll_scratch_iter_bytes")
+        self.device = torch.device(device)
+        self._scr, pad = _aligned(nranks * self.scratch_stride, self.device)
+        self.scratch = self._scr[pad:pad + nranks * self.scratch_stride]
+        nbytes = nranks * max(max_count, 1) * self.esize
+        self._in, ipad = _aligned(nbytes, self.device)
+        self.inp = self._in[ipad:ipad + nbytes]
+        if in_place:
+            self.out = self.inp
+        else:
+            self._out, opad = _aligned(nbytes, self.device)
+            self.out = self._out[opad:opad + nbytes]
+        self.epoch = 0
+
+    def init(self, stream=None) -> None:
+        ll.check(ll.ll_scratch_init(self.scratch.data_ptr(), self.scratch_stride, self.nranks,
+                                    SymRegion.stream_handle(stream)), "ll_scratch_init")
+        self.epoch = 0
+
+    def write_inputs(self, bits: np.ndarray) -> None:
+        """Rank r's raw element bits (row r of a [P, n] array) at in + r*n*esize."""
+        assert bits.shape[0] == self.nranks
+        host = _np_to_u8(bits)
+        self.inp[:host.numel()].copy_(host.to(self.device, non_blocking=False))
+
+    def read_out(self, nelems_total: int, np_dtype) -> np.ndarray:
+        nbytes = nelems_total * np.dtype(np_dtype).itemsize
+        return self.out[:nbytes].cpu().numpy().view(np_dtype).copy()
+
+    def allreduce(self, count: int, algo: str = "auto", stream=None) -> int:
+        """One call; advances the epoch by the iterations it used.  For
+        "twoshot_sentinel_out" the outputs are refilled with the sentinel first."""
+        s = SymRegion.stream_handle(stream)
+        if algo == "twoshot_sentinel_out" and count > 0:
+            st = ll.ll_fill_sentinel(self.out.data_ptr(), count, self.dt, self.nranks, s)
+            if st != ll.LL_OK:
+                return st
+        st, used = ll.ll_allreduce_buffered(self.inp.data_ptr(), self.out.data_ptr(), count, self.dt, ll.LL_SUM,
+                                            self.nranks, self.scratch.data_ptr(), self.scratch_stride,
+                                            self.epoch + 1, s, ll.ALGOS[algo])
+        if st == ll.LL_OK:
+            self.epoch += used
+        self.last_iters = used
+        return st

@@ -108,6 +108,45 @@ def test_fill_sentinel_and_auto_sentinel_argument_checks():
     assert ll.ll_set_auto_sentinel(0) == ll.LL_OK
 
 
+@pytest.mark.parametrize("p", [2, 4, 8])
+def test_scratch_sizing_round_trips(p):
+    for d in [1, 256, 4096, 5000, 1 << 20, 64 << 20]:
+        st, stride = ll.ll_scratch_bytes(d, p)
+        assert st == ll.LL_OK and stride % 256 == 0
+        st, it = ll.ll_scratch_iter_bytes(stride, p)
+        assert st == ll.LL_OK and it >= d and it % 256 == 0
+        assert ll.ll_scratch_iter_bytes(stride - 256, p)[1] < it  # minimal
+    assert ll.ll_scratch_bytes(0, p)[0] == ll.LL_ERR_INVALID
+    assert ll.ll_scratch_bytes((256 << 20) + 1, p)[0] == ll.LL_ERR_INVALID
+    assert ll.ll_scratch_iter_bytes(256, p)[0] == ll.LL_ERR_SCRATCH
+    assert ll.ll_scratch_iter_bytes(1000, p)[0] == ll.LL_ERR_INVALID
+
+
+def test_buffered_argument_checks():
+    stride = ll.ll_scratch_bytes(4096, 4)[1]
+    scr = 1 << 42
+    IN, OUT = GOOD_BASE, GOOD_OUT
+
+    def b(inp=IN, out=OUT, count=4096, dt=F32, op=0, p=4, base=scr, s=stride, epoch=1, algo=0):
+        return ll.ll_allreduce_buffered(inp, out, count, dt, op, p, base, s, epoch, 0, algo)
+
+    assert b(inp=0)[0] == ll.LL_ERR_INVALID
+    assert b(out=OUT + 8)[0] == ll.LL_ERR_INVALID
+    assert b(base=scr + 64)[0] == ll.LL_ERR_INVALID
+    assert b(epoch=0)[0] == ll.LL_ERR_INVALID
+    assert b(p=1)[0] == ll.LL_ERR_INVALID
+    assert b(op=1)[0] == ll.LL_ERR_UNSUPPORTED
+    assert b(algo=9)[0] == ll.LL_ERR_INVALID
+    assert b(s=256)[0] == ll.LL_ERR_SCRATCH
+    assert b(out=IN + 16)[0] == ll.LL_ERR_INVALID            # partial overlap of in and out
+    assert b(out=scr + 4096)[0] == ll.LL_ERR_INVALID         # output inside the scratch region
+    assert b(algo=ll.LL_ALGO_ONESHOT_WAVES, count=1 << 20)[0] == ll.LL_ERR_UNSUPPORTED  # waves: one iteration
+    assert b(algo=ll.LL_ALGO_TWOSHOT_SENTINEL_OUT, out=IN)[0] == ll.LL_ERR_INVALID
+    assert b(algo=ll.LL_ALGO_TWOSHOT_SENTINEL_OUT, count=1001)[0] == ll.LL_ERR_UNSUPPORTED
+    assert b(epoch=0xFFFFFFFF, count=4096)[0] == ll.LL_ERR_INVALID  # 4 iterations would pass 2^32 - 1
+    assert b(count=0) == (ll.LL_OK, 0)
+
+
 def test_init_argument_checks():
     assert ll.ll_init(0, 4096, 4, 0) == ll.LL_ERR_INVALID
     assert ll.ll_init(GOOD_BASE, 4096, 1, 0) == ll.LL_ERR_INVALID

@@ -1,0 +1,185 @@
+"""GPU parity of the bounded-scratch AllReduce (multi-iteration, double
+buffering): every algorithm, 1 .. 64 iterations, ragged last iterations,
+in place, back-to-back calls, against the CPU oracle at 0 ulp."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+import oracle  # noqa: E402
+from paper_2607_16100_amd import workloads as wl  # noqa: E402
+
+if torch.cuda.is_available():
+    from paper_2607_16100_amd import llcoll as ll  # noqa: E402
+    from paper_2607_16100_amd.region import ScratchRegion  # noqa: E402
+else:  # pragma: no cover
+    pytest.skip("no GPU", allow_module_level=True)
+
+ALGOS = ["oneshot", "oneshot_line", "oneshot_sentinel", "twoshot", "twoshot_line", "twoshot_sentinel",
+         "twoshot_sentinel_out", "auto"]
+NP = {"f32": np.uint32, "bf16": np.uint16}
+TEST_TIMEOUT_TICKS = 20_000_000
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def check_ok(st, what):
+    assert st == ll.LL_OK, f"{what}: {ll.ll_strerror(st)}"
+    st2 = ll.ll_check(stream())
+    assert st2 == ll.LL_OK, f"{what}: ll_check says {ll.ll_strerror(st2)}"
+
+
+def assert_bits_equal(got, want, what):
+    if not np.array_equal(got, want):
+        bad = np.argwhere(got != want)
+        r, i = bad[0]
+        raise AssertionError(f"{what}: {len(bad)} elements differ; first at rank {r} index {i}: "
+                             f"got {int(got[r, i]):#x} want {int(want[r, i]):#x}")
+
+
+@pytest.fixture(autouse=True)
+def _reset_settings():
+    ll.ll_set_launch(0, 0)
+    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
+    ll.ll_debug_mute_rank(-1)
+    yield
+    ll.ll_set_launch(0, 0)
+    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
+    ll.ll_debug_mute_rank(-1)
+
+
+def run(reg, x, algo):
+    p, n = x.shape
+    reg.write_inputs(x)
+    check_ok(reg.allreduce(n, algo), f"buffered {algo} P={p} n={n}")
+    return reg.read_out(p * n, x.dtype).reshape(p, n)
+
+
+def usable(algo, n, esize, iters):
+    if algo == "twoshot_sentinel_out" and (n * esize) % 16:
+        return False
+    return True
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("p", [2, 3, 8])
+def test_iterations_parity(dtype, p):
+    """Iteration size 4 KiB; messages of 1, 2, 3 and 7+ iterations with a
+    ragged last iteration, every algorithm, two calls in a row."""
+    es = 4 if dtype == "f32" else 2
+    reg = ScratchRegion(p, 40_000, dtype, iter_bytes=4096)
+    reg.init()
+    d = reg.iter_bytes // es
+    for n in [5, d, d + 8, 2 * d, 3 * d - 8, 7 * d + 8, 40_000]:
+        x = wl.normal(p, n, dtype, seed=n + p)
+        want = oracle.allreduce(x)
+        for algo in ALGOS:
+            if not usable(algo, n, es, 0):
+                continue
+            for k in range(2):
+                say(f"buffered {algo} P={p} {dtype} n={n} call {k}")
+                got = run(reg, x, algo)
+                assert reg.last_iters == -(-n // d)
+                assert_bits_equal(got, want, f"{algo} P={p} {dtype} n={n} call {k}")
+
+
+def test_waves_one_iteration_only():
+    reg = ScratchRegion(8, 10_000, "bf16", iter_bytes=4096)
+    reg.init()
+    x = wl.normal(8, 1000, "bf16", seed=4)
+    assert_bits_equal(run(reg, x, "oneshot_waves"), oracle.allreduce(x), "waves, one iteration")
+    reg.write_inputs(wl.normal(8, 10_000, "bf16", seed=5))
+    assert reg.allreduce(10_000, "oneshot_waves") == ll.LL_ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("algo", [a for a in ALGOS if a != "twoshot_sentinel_out"] + ["oneshot_waves"])
+def test_in_place(algo):
+    """in == out: each rank's input is overwritten by its result."""
+    p, n = 8, 30_000
+    reg = ScratchRegion(p, n, "bf16", iter_bytes=16384 if algo != "oneshot_waves" else 1 << 20, in_place=True)
+    reg.init()
+    for k in range(2):
+        x = wl.uniform(p, n, "bf16", seed=50 + k)
+        say(f"in place {algo} call {k}")
+        assert_bits_equal(run(reg, x, algo), oracle.allreduce(x), f"in place {algo} call {k}")
+
+
+def test_direct_output_rejects_in_place():
+    reg = ScratchRegion(4, 1024, "f32", iter_bytes=4096, in_place=True)
+    reg.init()
+    assert reg.allreduce(1024, "twoshot_sentinel_out") == ll.LL_ERR_INVALID
+
+
+@pytest.mark.parametrize("algo", ["oneshot", "twoshot_line", "oneshot_sentinel", "twoshot_sentinel"])
+def test_many_iterations_small_grids(algo):
+    """64 iterations with one small workgroup per rank (each lane serves many
+    units per iteration) and with the automatic grid."""
+    p, n = 8, 64 * 1024
+    reg = ScratchRegion(p, n, "f32", iter_bytes=4096)
+    reg.init()
+    x = wl.normal(p, n, "f32", seed=77)
+    want = oracle.allreduce(x)
+    for wg, threads in [(1, 64), (2, 256), (0, 0)]:
+        ll.ll_set_launch(wg, threads)
+        say(f"64 iterations {algo} wg={wg} t={threads}")
+        assert_bits_equal(run(reg, x, algo), want, f"{algo} wg={wg} t={threads}")
+        assert reg.last_iters == 64
+
+
+def test_epochs_advance_by_iterations():
+    p, n = 4, 10_000
+    reg = ScratchRegion(p, n, "f32", iter_bytes=4096)
+    reg.init()
+    x = wl.uniform(p, n, "f32", seed=8)
+    run(reg, x, "twoshot")
+    assert reg.epoch == reg.last_iters == -(-n * 4 // reg.iter_bytes)
+    # a call that would run past epoch 0xFFFFFFFF is refused before launching
+    st, _ = ll.ll_allreduce_buffered(reg.inp.data_ptr(), reg.out.data_ptr(), n, ll.LL_F32, ll.LL_SUM, p,
+                                     reg.scratch.data_ptr(), reg.scratch_stride, 0xFFFFFFFF, stream(),
+                                     ll.LL_ALGO_TWOSHOT)
+    assert st == ll.LL_ERR_INVALID
+
+
+def test_e4_scale_32mib_message():
+    """The paper's scratch study shape: 32 MiB per rank, 8 ranks, iterations
+    of 4 MiB (8 iterations) and 1 MiB (32), one-shot and two-shot."""
+    p, n = 8, (32 << 20) // 4
+    x = wl.uniform(p, n, "f32", seed=32)
+    want = oracle.allreduce(x)
+    for it_bytes in (4 << 20, 1 << 20):
+        reg = ScratchRegion(p, n, "f32", iter_bytes=it_bytes)
+        reg.init()
+        for algo in ("oneshot_line", "twoshot_line", "twoshot_sentinel"):
+            say(f"32 MiB {algo} iterations of {it_bytes >> 10} KiB")
+            assert_bits_equal(run(reg, x, algo), want, f"32 MiB {algo} {it_bytes}")
+        del reg
+
+
+@pytest.mark.parametrize("algo", ["oneshot", "twoshot_sentinel"])
+def test_missing_peer_times_out_and_scratch_init_recovers(algo):
+    p, n = 8, 8192
+    reg = ScratchRegion(p, n, "f32", iter_bytes=4096)
+    reg.init()
+    x = wl.uniform(p, n, "f32", seed=2)
+    reg.write_inputs(x)
+    ll.ll_set_poll_timeout(200_000)
+    ll.ll_debug_mute_rank(6)
+    assert reg.allreduce(n, algo) == ll.LL_OK
+    assert ll.ll_check(stream()) == ll.LL_ERR_TIMEOUT
+    ll.ll_debug_mute_rank(-1)
+    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
+    reg.init()
+    assert_bits_equal(run(reg, x, algo), oracle.allreduce(x), f"{algo} after timeout")
