@@ -216,8 +216,8 @@ def bench_c3(torch, ll, steps):
     reg.init()
     reg.write_inputs(wl.normal(p, n, "bf16", sigma=0.5, seed=0))
     out = {}
-    for algo in ("twoshot", "twoshot_line", "twoshot_sentinel", "twoshot_sentinel_out", "oneshot", "oneshot_line",
-                 "oneshot_sentinel", "auto"):
+    for algo in ("twoshot", "twoshot_line", "twoshot_sentinel", "twoshot_sentinel_out", "twoshot_atomic", "oneshot",
+                 "oneshot_line", "oneshot_sentinel", "auto"):
         out[algo] = paced_collective(torch, ll, reg, "ar", n, ll.ALGOS[algo], steps, 20)
     ll.check(ll.ll_set_auto_sentinel(1), "auto sentinel")
     try:
@@ -303,7 +303,7 @@ def bench_sweep(torch, ll, path):
             n = 1 << k
             steps = 2000 if n * 4 <= (1 << 20) else (200 if n * 4 <= (16 << 20) else 20)
             for algo in ("auto", "oneshot_waves", "oneshot", "oneshot_line", "oneshot_sentinel", "twoshot",
-                         "twoshot_line", "twoshot_sentinel", "twoshot_sentinel_out"):
+                         "twoshot_line", "twoshot_sentinel", "twoshot_sentinel_out", "twoshot_atomic"):
                 if algo == "oneshot_waves" and n * 4 > (1 << 20):
                     continue
                 r = paced_collective(torch, ll, reg, "ar", n, ll.ALGOS[algo], steps, min(20, steps))
@@ -484,8 +484,9 @@ def main():
         log(json.dumps(result["sol"]))
     if want("bw"):
         log("bandwidth at 64 MiB per rank")
-        result["bw"] = bench_bandwidth(torch, ll, 16 << 20, ["twoshot_line", "twoshot", "twoshot_sentinel", "oneshot_line",
-                                                                "oneshot", "oneshot_sentinel"],
+        result["bw"] = bench_bandwidth(torch, ll, 16 << 20, ["twoshot_line", "twoshot", "twoshot_sentinel",
+                                                                "twoshot_sentinel_out", "twoshot_atomic",
+                                                                "oneshot_line", "oneshot", "oneshot_sentinel"],
                                        iters=args.bw_iters)
         log(json.dumps(result["bw"]))
     if want("c3"):

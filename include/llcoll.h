@@ -27,6 +27,7 @@
  *   [0, cap)                      input area: the rank's input, at offset 0
  *   [cap, cap + A8)               8-byte packet area {payload u32, flag u32}
  *   [cap + A8, cap + A8 + A128)   128-byte line area
+ *   [.., .. + AA)                 binary32 accumulators and tile counters (atomic two-shot)
  *   [.., .. + AS)                 sentinel area (payload only)
  * cap (the input capacity, a multiple of 256 bytes) is the largest input for
  * which both packet areas fit every algorithm; ll_input_capacity reports it.
@@ -83,9 +84,26 @@ typedef enum {
   LL_ALGO_ONESHOT_WAVES = 5,  /* one-shot, 8-byte packets, one wave per peer, LDS staging */
   LL_ALGO_ONESHOT_SENTINEL = 6, /* one-shot, sentinel synchronisation (Sec. IV, "Sentinel") */
   LL_ALGO_TWOSHOT_SENTINEL = 7, /* two-shot, sentinel synchronisation */
-  LL_ALGO_TWOSHOT_SENTINEL_OUT = 8 /* two-shot, sentinel; AllGather straight into the
-                                      peers' sentinel-filled outputs (see ll_fill_sentinel) */
+  LL_ALGO_TWOSHOT_SENTINEL_OUT = 8, /* two-shot, sentinel; AllGather straight into the
+                                       peers' sentinel-filled outputs (see ll_fill_sentinel) */
+  LL_ALGO_TWOSHOT_ATOMIC = 9        /* two-shot with atomic accumulation (Sec. IV, "LL128
+                                       Atomic"): NOT deterministic, see below */
 } ll_algo;
+
+/* LL_ALGO_TWOSHOT_ATOMIC, the analogue of the paper's two-shot LL128 atomic
+ * AllReduce.  Every rank adds its chunk c, widened to binary32, into an
+ * accumulator in rank c's slice with device-scope float atomic adds.  The
+ * chip does not add a 128-byte line atomically, so the paper's in-line flag
+ * becomes a per-tile counter (one per 1 KiB of chunk input) that each rank
+ * bumps after its adds, with release ordering.  The owner waits until the
+ * counter reaches nranks, rounds once and stores the result into every
+ * rank's output.  Scratch per slice is about 2*count*esize/nranks.
+ * Preconditions and errors are those of LL_ALGO_TWOSHOT_SENTINEL_OUT:
+ * sentinel-filled outputs and count*esize % 16 == 0.  The summation order
+ * depends on timing, so results differ from the ordered sum by up to
+ * gamma_{P-1} * sum |x_i| (binary32, end of Sec. IV), plus one rounding to
+ * bfloat16.  Every rank receives the same bits.  Not available through
+ * ll_allreduce_buffered, and never chosen by AUTO. */
 
 /* Packet format for the stand-alone ReduceScatter / AllGather. */
 typedef enum { LL_PROTO_AUTO = 0, LL_PROTO_PACKET8 = 1, LL_PROTO_LINE128 = 2, LL_PROTO_SENTINEL = 3 } ll_proto;
@@ -132,12 +150,14 @@ int ll_slice_bytes(size_t count, ll_dtype dt, int nranks, size_t *min_rank_strid
 int ll_input_capacity(size_t rank_stride, int nranks, size_t *capacity_bytes);
 
 /* Byte offsets, within every slice, of the areas of the slice layout:
- * offsets5 = {input area (0), 8-byte packet area, line area, sentinel area,
- * end of the sentinel area}.  Host-only; errors as ll_input_capacity. */
-int ll_slice_layout(size_t rank_stride, int nranks, size_t *offsets5);
+ * offsets6 = {input area (0), 8-byte packet area, line area, atomic
+ * accumulator area, sentinel area, end of the sentinel area}.  Host-only;
+ * errors as ll_input_capacity. */
+int ll_slice_layout(size_t rank_stride, int nranks, size_t *offsets6);
 
-/* Zero both flagged packet areas of every slice (flag 0 = nothing received)
- * and fill the sentinel area with the sentinel, on `stream`.  Call once after allocating a region, and again before reusing it
+/* Zero both flagged packet areas and the accumulator area of every slice
+ * (flag 0 = nothing received) and fill the sentinel area with the sentinel,
+ * on `stream`.  Call once after allocating a region, and again before reusing it
  * after epoch 0xFFFFFFFF or after a timed-out call.  Sec. V: the LL reset
  * value is zero. */
 int ll_init(void *sym_base, size_t rank_stride, int nranks, void *stream);

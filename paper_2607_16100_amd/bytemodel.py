@@ -39,6 +39,10 @@ def _proto(algo: str) -> tuple[str, str]:
 
 def allreduce_bytes(algo: str, p: int, count: int, esize: int) -> float:
     """HBM bytes moved by one AllReduce call of `count` elements per rank."""
+    if algo == "twoshot_atomic":
+        return twoshot_atomic_bytes(p, count, esize)
+    if algo == "twoshot_sentinel_out":
+        return twoshot_sentinel_out_bytes(p, count, esize)
     m = count * esize
     base, proto = _proto(algo)
     f = COPY_FACTOR[proto]
@@ -50,6 +54,30 @@ def allreduce_bytes(algo: str, p: int, count: int, esize: int) -> float:
         # packet copies; write output M
         c = math.ceil(count / p) * esize
         per_rank = m + 2 * f * (p - 1) * c + m
+    return p * per_rank
+
+
+def twoshot_sentinel_out_bytes(p: int, count: int, esize: int) -> float:
+    """Two-shot sentinel with the AllGather stored into the peers' outputs:
+    per rank, the input M, the ReduceScatter's (P-1) chunk copies (written,
+    read, reset), the output M (own chunk plus the peers' direct stores), the
+    poll of the (P-1) peer chunks, and the sentinel fill of the output (M)."""
+    m = count * esize
+    c = math.ceil(count / p) * esize
+    return p * (m + COPY_FACTOR["sentinel"] * (p - 1) * c + m + (p - 1) * c + m)
+
+
+def twoshot_atomic_bytes(p: int, count: int, esize: int) -> float:
+    """Atomic-accumulation two-shot: per rank, read the input M; P chunk
+    contributions added into binary32 accumulators (each add reads and writes
+    4 bytes per element); the owner reads and zeroes its accumulator; every
+    output receives M (own chunk plus the peers' direct stores), is polled
+    for the (P-1) peer chunks, and was filled with the sentinel before the
+    call (M)."""
+    m = count * esize
+    c = math.ceil(count / p) * esize
+    acc = 4.0 / esize  # accumulator bytes per input byte
+    per_rank = m + 2 * acc * m + 2 * acc * c + m + (p - 1) * c + m
     return p * per_rank
 
 

@@ -573,6 +573,155 @@ __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(LLCOLL_TWO
 }
 
 // ---------------------------------------------------------------------------
+// Two-shot AllReduce with atomic accumulation: the gfx950 analogue of the
+// paper's two-shot LL128 atomic algorithm (Sec. IV, "LL128 Atomic AllReduce";
+// Fig. 5).
+//
+// ReduceScatter.  Every rank adds its chunk c, widened to binary32, into an
+// accumulator in rank c's slice with device-scope float atomic adds (its own
+// chunk included).  The hardware gives no 128-byte line atomicity, so the
+// flag cannot ride inside the data: after the adds of a tile (one wave's 64
+// lanes x 16 input bytes) a wave bumps that tile's counter with a
+// release-ordered atomic add.  Owner c waits (acquire) until the counter
+// reaches P, then reads the accumulated tile, rounds once to the element type
+// and resets accumulator and counter to zero for the next call.
+// AllGather.  The owner stores the result into its own output and straight
+// into every peer's output, which the caller has filled with the sentinel
+// (as in the paper's Fig. 5); each rank polls its own output until the peers'
+// blocks no longer hold it.
+// Like the paper's algorithm it is not deterministic: the order of the
+// atomic adds, and with it the binary32 rounding, varies from call to call
+// (the result obeys the gamma_{P-1} bound of the end of Sec. IV, checked by
+// the tests).  Every rank still receives the same bits, because each element
+// is rounded once, by its owner.
+// Slice layout of the area: accumulator (a.slot bytes: binary32 for every
+// element of the chunk's whole tiles), then one u32 counter per tile.  The
+// caller guarantees 16-byte aligned rows (count * esize % 16 == 0), so every
+// lane's 16 input bytes are wholly inside or wholly outside a chunk.
+template <int DT, int P>
+__global__ __launch_bounds__(1024) void k_twoshot_atomic(KArgs a) {
+  stamp_start(a);
+  constexpr int E = Elem<DT>::kBytes;
+  constexpr int EL = 16 / E;  // elements per lane: 16 input bytes
+  constexpr int TE = 64 * EL; // elements per tile (one wave)
+  const Part pt = part_of_block<P>();
+  const int r = pt.r;
+  const int lane = (int)(threadIdx.x & 63);
+  const int64_t gw = ((int64_t)pt.w * blockDim.x + threadIdx.x) >> 6;
+  const int64_t GW = ((int64_t)pt.W * blockDim.x) >> 6;
+  const int64_t n = a.n, C = a.chunk;
+  const int64_t tiles = (C + TE - 1) / TE;
+  const uint64_t deadline = now_ticks() + a.timeout;
+  const char *const in_r = a.in + (uint64_t)r * a.in_stride;
+  char *const out_r = a.out + (uint64_t)r * (uint64_t)n * E;
+  const bool publish = (r != a.mute);
+  auto chunk_len = [&](int c) -> int64_t {
+    const int64_t left = n - (int64_t)c * C;
+    return left < 0 ? 0 : (left < C ? left : C);
+  };
+  auto acc_of = [&](int c) -> float * { return (float *)(a.sym + (uint64_t)c * a.stride + a.area); };
+  auto cnt_of = [&](int c) -> uint32_t * { return (uint32_t *)(a.sym + (uint64_t)c * a.stride + a.area + a.slot); };
+
+  auto step_add = [&](int64_t t) {
+    const int64_t e0 = t * TE + (int64_t)lane * EL;
+    // Branch-free: all P loads first (a lane's 16 bytes lie wholly inside or
+    // wholly outside a chunk), then all adds back to back.  The memory
+    // counter covers loads and atomics alike, so any wait between the adds
+    // would serialise them.  Lanes past a chunk's end add zeros into the
+    // accumulator's tile padding, which is never read.
+    u32x4 w[P];
+#pragma unroll
+    for (int k = 1; k <= P; ++k) {
+      const int c = (r + k) % P;  // own chunk last
+      const bool ok = e0 < chunk_len(c);
+      const char *src = ok ? in_r + ((uint64_t)c * C + e0) * E : in_r;
+      const u32x4 v = __builtin_nontemporal_load((const u32x4 *)src);
+      w[k - 1] = ok ? v : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int k = 1; k <= P; ++k) {
+      const int c = (r + k) % P;
+      const uint32_t wv[4] = {w[k - 1].x, w[k - 1].y, w[k - 1].z, w[k - 1].w};
+      float *acc = acc_of(c) + e0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float f[Elem<DT>::kPerWord];
+        Elem<DT>::widen(wv[j], f);
+#pragma unroll
+        for (int h = 0; h < Elem<DT>::kPerWord; ++h)
+          __hip_atomic_fetch_add(acc + j * Elem<DT>::kPerWord + h, f[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+    // the wave's adds of this tile are performed before its counters move
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    if (lane == 0) {
+#pragma unroll
+      for (int k = 1; k <= P; ++k) {
+        const int c = (r + k) % P;
+        if (t * TE < chunk_len(c))
+          __hip_atomic_fetch_add(cnt_of(c) + t, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+  };
+
+  auto step_reduce = [&](int64_t t) {
+    const int64_t len = chunk_len(r);
+    if (t * TE >= len) return;
+    uint32_t *cnt = cnt_of(r) + t;
+    int spins = 1;
+    while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != (uint32_t)P) {
+      if ((spins++ & 15) == 0 && now_ticks() > deadline) {
+        report_timeout(r, ((1u << P) - 1u) & ~(1u << r), a.epoch);
+        break;
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    const int64_t e0 = t * TE + (int64_t)lane * EL;
+    if (e0 < len) {
+      float *acc = acc_of(r) + e0;
+      float f[EL];
+#pragma unroll
+      for (int j = 0; j < EL; ++j) f[j] = __hip_atomic_load(acc + j, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      uint32_t res[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) res[j] = Elem<DT>::narrow(&f[j * Elem<DT>::kPerWord]);
+      const u32x4 v = {res[0], res[1], res[2], res[3]};
+      store_words<DT>(out_r + (uint64_t)r * C * E, e0 / Elem<DT>::kPerWord, 4, len, true, v);
+      if (publish) {
+        const uint32_t at = uniform_u32((uint32_t)(r * C * E));
+#pragma unroll
+        for (int k = 1; k < P; ++k) {
+          const int q = (r + k) % P;
+          st_pkt_at(make_rsrc(a.out + (uint64_t)q * (uint64_t)n * E, (uint32_t)(n * E)), (uint32_t)(e0 * E), at, v);
+        }
+      }
+      // back to zero for the next call (ordered by the kernel boundary)
+#pragma unroll
+      for (int j = 0; j < EL; ++j) __hip_atomic_store(acc + j, 0.0f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (lane == 0) __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  };
+
+  auto step_gather = [&](int64_t t) {
+    const int64_t e0 = t * TE + (int64_t)lane * EL;
+    uint32_t pend = 0;
+#pragma unroll
+    for (int q = 0; q < P; ++q)
+      if (q != r && e0 < chunk_len(q)) pend |= 1u << q;
+    poll_out<P>(out_r, (uint32_t)(n * E), (uint32_t)(C * E), (uint32_t)(e0 * E), pend, r, a.epoch, deadline);
+  };
+
+  const int64_t steps = gw < tiles ? (tiles - gw + GW - 1) / GW : 0;
+  const int64_t lag = a.lag > 0 ? a.lag : 1;
+  for (int64_t s = 0; s < steps + 2 * lag; ++s) {
+    if (s < steps && publish) step_add(gw + s * GW);
+    if (s >= lag && s - lag < steps) step_reduce(gw + (s - lag) * GW);
+    if (s >= 2 * lag && s - 2 * lag < steps) step_gather(gw + (s - 2 * lag) * GW);
+  }
+  stamp_end(a);
+}
+
+// ---------------------------------------------------------------------------
 // Stand-alone ReduceScatter: rank r's input is P chunks of m = a.n elements;
 // chunk c goes to slot (c <- r); rank r reduces chunk r.  The same two steps
 // as the first two of the two-shot kernel, with chunks of exactly m

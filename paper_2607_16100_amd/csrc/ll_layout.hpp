@@ -4,6 +4,7 @@
 //   [0, cap)                   input area (the rank's input at offset 0)
 //   [cap, cap + A8)            8-byte packet area
 //   [cap + A8, cap + A8 + A128) 128-byte line area
+//   [.., .. + AA)              atomic accumulator and tile counters
 //   [.., .. + AS)              sentinel area (payload only, reset after use)
 // where cap is the largest multiple of 256 for which both areas, sized for
 // the most demanding algorithm at an input of cap bytes, fit in the slice.
@@ -69,7 +70,20 @@ inline uint64_t areaS(uint64_t M, int P) {
   return std::max(p1 * slotS(M), 2 * p1 * slotS(chunk_bound(M, P)));
 }
 
-inline uint64_t slice_for(uint64_t cap, int P) { return cap + area8(cap, P) + area128(cap, P) + areaS(cap, P); }
+// Atomic-accumulation two-shot: a binary32 accumulator covering the rank's
+// chunk in whole tiles of 1 KiB of input (4 KiB of accumulator for binary32
+// tiles, 8 KiB for bfloat16), and one u32 counter per tile.
+inline uint64_t atomic_acc_bytes(uint64_t chunk_bytes, int esize) {
+  return roundup(ceil_div(chunk_bytes, 1024) * 4096 / (uint64_t)esize, kAlign);
+}
+inline uint64_t areaA(uint64_t M, int P) {
+  const uint64_t cb = chunk_bound(M, P);
+  return atomic_acc_bytes(cb, 2) + roundup(4 * ceil_div(cb, 1024), kAlign);
+}
+
+inline uint64_t slice_for(uint64_t cap, int P) {
+  return cap + area8(cap, P) + area128(cap, P) + areaA(cap, P) + areaS(cap, P);
+}
 
 // Largest cap (multiple of 256, at most kMaxInputBytes) with slice_for(cap) <= stride.
 inline uint64_t capacity(uint64_t stride, int P) {

@@ -51,7 +51,16 @@ TimeoutInfo g_last_timeout;
 std::mutex g_mu;
 
 // ---------------------------------------------------------------- kernels
-enum Kind { K_ONESHOT = 0, K_TWOSHOT = 1, K_RS = 2, K_AG = 3, K_ONESHOT_WAVES = 4, K_TWOSHOT_OUT = 5, K_KINDS = 6 };
+enum Kind {
+  K_ONESHOT = 0,
+  K_TWOSHOT = 1,
+  K_RS = 2,
+  K_AG = 3,
+  K_ONESHOT_WAVES = 4,
+  K_TWOSHOT_OUT = 5,
+  K_TWOSHOT_ATOMIC = 6,
+  K_KINDS = 7
+};
 constexpr int kWaveUnits[3] = {1, 2, 4};  // units per lane of the wave-per-peer kernels
 enum Proto { PR_LL = 0, PR_LINE = 1, PR_SENT = 2, PR_COUNT = 3 };
 
@@ -65,7 +74,11 @@ void fill_row(kernel_fn *row) {
   row[K_AG] = k_allgather<Pr, DT, P>;
   row[K_ONESHOT_WAVES] = nullptr;
   row[K_TWOSHOT_OUT] = nullptr;
-  if constexpr (std::is_same<Pr, ProtoSent>::value) row[K_TWOSHOT_OUT] = k_twoshot<ProtoSent, DT, P, true>;
+  row[K_TWOSHOT_ATOMIC] = nullptr;
+  if constexpr (std::is_same<Pr, ProtoSent>::value) {
+    row[K_TWOSHOT_OUT] = k_twoshot<ProtoSent, DT, P, true>;
+    row[K_TWOSHOT_ATOMIC] = k_twoshot_atomic<DT, P>;
+  }
 }
 
 // table[proto][dtype][P][kind]
@@ -253,10 +266,11 @@ int launch(const Plan &pl, void *stream) {
 // Region geometry of one call; fails with LL_ERR_SCRATCH when the input does
 // not fit the region's input capacity.
 struct Region {
-  uint64_t cap, a8, a128, as;
+  uint64_t cap, a8, a128, aa, as;
   uint64_t area_of(int proto) const {
-    return proto == PR_LINE ? cap + a8 : (proto == PR_SENT ? cap + a8 + a128 : cap);
+    return proto == PR_LINE ? cap + a8 : (proto == PR_SENT ? cap + a8 + a128 + aa : cap);
   }
+  uint64_t atomic_area() const { return cap + a8 + a128; }
 };
 
 // Slot bytes and packet units for a payload of `bytes` in format `proto`.
@@ -276,6 +290,7 @@ int region_of(size_t rank_stride, int P, uint64_t in_bytes, Region *rg) {
   rg->cap = cap;
   rg->a8 = L::area8(cap, P);
   rg->a128 = L::area128(cap, P);
+  rg->aa = L::areaA(cap, P);
   rg->as = L::areaS(cap, P);
   return LL_OK;
 }
@@ -340,6 +355,9 @@ ll_proto auto_proto(uint64_t bytes, int P, bool sentinel_ok) {
   return bytes <= 512 * KiB ? LL_PROTO_PACKET8 : LL_PROTO_LINE128;
 }
 
+// Algorithms whose AllGather stores into the peers' sentinel-filled outputs.
+bool fills_output(ll_algo algo) { return algo == LL_ALGO_TWOSHOT_SENTINEL_OUT || algo == LL_ALGO_TWOSHOT_ATOMIC; }
+
 // Kernel, packet format, slot size and unit count of an AllReduce of `count`
 // elements per rank whose iterations hold `iter_count` elements.
 // area_of(proto) gives the offset of that packet format's area in a slice.
@@ -393,17 +411,18 @@ int ll_input_capacity(size_t rank_stride, int nranks, size_t *capacity_bytes) {
   return LL_OK;
 }
 
-int ll_slice_layout(size_t rank_stride, int nranks, size_t *offsets5) {
-  if (offsets5 == nullptr) return LL_ERR_INVALID;
+int ll_slice_layout(size_t rank_stride, int nranks, size_t *offsets6) {
+  if (offsets6 == nullptr) return LL_ERR_INVALID;
   size_t cap = 0;
   const int st = ll_input_capacity(rank_stride, nranks, &cap);
   if (st != LL_OK) return st;
-  const uint64_t a8 = L::area8(cap, nranks), a128 = L::area128(cap, nranks), as = L::areaS(cap, nranks);
-  offsets5[0] = 0;
-  offsets5[1] = cap;
-  offsets5[2] = cap + a8;
-  offsets5[3] = cap + a8 + a128;
-  offsets5[4] = cap + a8 + a128 + as;
+  const uint64_t a8 = L::area8(cap, nranks), a128 = L::area128(cap, nranks), aa = L::areaA(cap, nranks);
+  offsets6[0] = 0;
+  offsets6[1] = cap;
+  offsets6[2] = cap + a8;
+  offsets6[3] = cap + a8 + a128;
+  offsets6[4] = cap + a8 + a128 + aa;
+  offsets6[5] = cap + a8 + a128 + aa + L::areaS(cap, nranks);
   return LL_OK;
 }
 
@@ -418,7 +437,7 @@ int ll_init(void *sym_base, size_t rank_stride, int nranks, void *stream) {
   st = device_info(&d);
   if (st != LL_OK) return st;
   // flags start at 0 (never a valid epoch); sentinel slots start at the sentinel
-  const uint64_t lo = rg.cap, mid = rg.cap + rg.a8 + rg.a128, hi = mid + rg.as;
+  const uint64_t lo = rg.cap, mid = rg.cap + rg.a8 + rg.a128 + rg.aa, hi = mid + rg.as;
   if (mid > lo)
     hipLaunchKernelGGL(k_fill_areas, dim3(d.cus * 4), dim3(256), 0, (hipStream_t)stream, (char *)sym_base,
                        (uint64_t)rank_stride, nranks, lo, mid, 0u);
@@ -461,10 +480,10 @@ int ll_allreduce_algo(void *sym_base, size_t rank_stride, void *out, size_t coun
   if (st != LL_OK) return st;
   st = check_dtype_op((int)dt, (int)op);
   if (st != LL_OK) return st;
-  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_TWOSHOT_SENTINEL_OUT) return LL_ERR_INVALID;
+  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_TWOSHOT_ATOMIC) return LL_ERR_INVALID;
   const int es = esize_of(dt);
   const uint64_t in_bytes = (uint64_t)count * es;
-  if (algo == LL_ALGO_TWOSHOT_SENTINEL_OUT && in_bytes % 16 != 0) return LL_ERR_UNSUPPORTED;
+  if (fills_output(algo) && in_bytes % 16 != 0) return LL_ERR_UNSUPPORTED;
   if (count > L::kMaxInputBytes) return LL_ERR_UNSUPPORTED;
   if (overlaps(out, in_bytes * nranks, sym_base, (uint64_t)rank_stride * nranks)) return LL_ERR_INVALID;
   Region rg;
@@ -479,6 +498,16 @@ int ll_allreduce_algo(void *sym_base, size_t rank_stride, void *out, size_t coun
   pl.a = base_args(sym_base, rank_stride, out, epoch);
   pl.a.n = (int64_t)count;
   pl.a.al4 = (in_bytes % 4 == 0) ? 1u : 0u;
+  if (algo == LL_ALGO_TWOSHOT_ATOMIC) {
+    pl.kind = K_TWOSHOT_ATOMIC;
+    pl.proto = PR_SENT;
+    const uint64_t C = L::twoshot_chunk(count, nranks, es);
+    pl.a.chunk = (int64_t)C;
+    pl.a.area = rg.atomic_area();
+    pl.a.slot = L::atomic_acc_bytes(C * es, es);  // binary32 accumulator in whole tiles
+    pl.units = (int64_t)L::ceil_div(C * es, 1024) * 64;  // one lane per 16 input bytes
+    return launch(pl, stream);
+  }
   plan_allreduce(&pl, algo, count, es, nranks, count, [&](int proto) { return rg.area_of(proto); });
   return launch(pl, stream);
 }
@@ -540,7 +569,8 @@ int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, 
   if (epoch == 0) return LL_ERR_INVALID;
   int st = check_dtype_op((int)dt, (int)op);
   if (st != LL_OK) return st;
-  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_TWOSHOT_SENTINEL_OUT) return LL_ERR_INVALID;
+  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_TWOSHOT_ATOMIC) return LL_ERR_INVALID;
+  if (algo == LL_ALGO_TWOSHOT_ATOMIC) return LL_ERR_UNSUPPORTED;  // single-iteration regions only
   size_t D = 0;
   st = ll_scratch_iter_bytes(scratch_stride, nranks, &D);
   if (st != LL_OK) return st;
@@ -847,7 +877,7 @@ int ll_bench_allreduce(void *sym_base, size_t rank_stride, void *out, size_t cou
     return LL_ERR_INVALID;
   if (stamps != nullptr && stamp_stride < 1) return LL_ERR_INVALID;
   for (int i = 0; i < calls; ++i) {
-    if (algo == LL_ALGO_TWOSHOT_SENTINEL_OUT) {  // its precondition, timed with it
+    if (fills_output((ll_algo)algo)) {  // its precondition, timed with it
       const int sf = ll_fill_sentinel(out, count, (ll_dtype)dt, nranks, stream);
       if (sf != LL_OK) return sf;
     }

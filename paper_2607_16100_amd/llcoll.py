@@ -20,6 +20,7 @@ LL_SUM = 0
 LL_ALGO_AUTO, LL_ALGO_ONESHOT, LL_ALGO_TWOSHOT, LL_ALGO_TWOSHOT_LINE, LL_ALGO_ONESHOT_LINE = 0, 1, 2, 3, 4
 LL_ALGO_ONESHOT_WAVES = 5
 LL_ALGO_ONESHOT_SENTINEL, LL_ALGO_TWOSHOT_SENTINEL, LL_ALGO_TWOSHOT_SENTINEL_OUT = 6, 7, 8
+LL_ALGO_TWOSHOT_ATOMIC = 9
 LL_PROTO_AUTO, LL_PROTO_PACKET8, LL_PROTO_LINE128, LL_PROTO_SENTINEL = 0, 1, 2, 3
 
 LL_OK = 0
@@ -34,7 +35,7 @@ ALGOS = {
     "twoshot_line": LL_ALGO_TWOSHOT_LINE, "oneshot_line": LL_ALGO_ONESHOT_LINE,
     "oneshot_waves": LL_ALGO_ONESHOT_WAVES,
     "oneshot_sentinel": LL_ALGO_ONESHOT_SENTINEL, "twoshot_sentinel": LL_ALGO_TWOSHOT_SENTINEL,
-    "twoshot_sentinel_out": LL_ALGO_TWOSHOT_SENTINEL_OUT,
+    "twoshot_sentinel_out": LL_ALGO_TWOSHOT_SENTINEL_OUT, "twoshot_atomic": LL_ALGO_TWOSHOT_ATOMIC,
 }
 PROTOS = {"auto": LL_PROTO_AUTO, "packet8": LL_PROTO_PACKET8, "line128": LL_PROTO_LINE128,
           "sentinel": LL_PROTO_SENTINEL}
@@ -135,8 +136,8 @@ def ll_input_capacity(rank_stride: int, nranks: int):
 
 
 def ll_slice_layout(rank_stride: int, nranks: int):
-    """(status, [input, packet8 area, line area, sentinel area, end]) byte offsets."""
-    out = (ctypes.c_size_t * 5)()
+    """(status, [input, packet8 area, line area, atomic area, sentinel area, end]) byte offsets."""
+    out = (ctypes.c_size_t * 6)()
     st = _lib.ll_slice_layout(rank_stride, nranks, out)
     return st, list(out)
 

@@ -93,7 +93,8 @@ class SymRegion:
 
     def read_area(self, area: int) -> np.ndarray:
         """Raw uint32 words of layout area `area` (1 = 8-byte packets, 2 =
-        lines, 3 = sentinel) of every slice, shape [P, area_bytes / 4]."""
+        lines, 3 = atomic accumulators, 4 = sentinel) of every slice, shape
+        [P, area_bytes / 4]."""
         st, offs = ll.ll_slice_layout(self.rank_stride, self.nranks)
         ll.check(st, "ll_slice_layout")
         lo, hi = offs[area], offs[area + 1]
@@ -110,10 +111,11 @@ class SymRegion:
         return ll.ll_fill_sentinel(self.out_ptr, count, self.dt, self.nranks, self.stream_handle(stream))
 
     def allreduce(self, count: int, algo: str = "auto", stream=None, epoch: int | None = None) -> int:
-        """One AllReduce.  For "twoshot_sentinel_out" the outputs are first
-        refilled with the sentinel (its precondition), on the same stream."""
+        """One AllReduce.  For "twoshot_sentinel_out" and "twoshot_atomic" the
+        outputs are first refilled with the sentinel (their precondition), on
+        the same stream."""
         e = self.next_epoch() if epoch is None else epoch
-        if algo == "twoshot_sentinel_out" and count > 0:
+        if algo in ("twoshot_sentinel_out", "twoshot_atomic") and count > 0:
             st = self.fill_out_sentinel(count, stream)
             if st != ll.LL_OK:
                 return st

@@ -64,7 +64,8 @@ def ar(count=1024, dt=F32, p=4, base=GOOD_BASE, stride=None, out=GOOD_OUT, epoch
     (dict(epoch=0), ll.LL_ERR_INVALID),
     (dict(dt=7), ll.LL_ERR_UNSUPPORTED),
     (dict(op=1), ll.LL_ERR_UNSUPPORTED),
-    (dict(algo=9), ll.LL_ERR_INVALID),
+    (dict(algo=10), ll.LL_ERR_INVALID),
+    (dict(algo=9, count=1001), ll.LL_ERR_UNSUPPORTED),  # atomic two-shot: count*esize % 16 == 0
     (dict(algo=8, count=1001), ll.LL_ERR_UNSUPPORTED),  # direct output needs count*esize % 16 == 0
     (dict(algo=-1), ll.LL_ERR_INVALID),
     (dict(stride=256), ll.LL_ERR_SCRATCH),
@@ -136,7 +137,8 @@ def test_buffered_argument_checks():
     assert b(epoch=0)[0] == ll.LL_ERR_INVALID
     assert b(p=1)[0] == ll.LL_ERR_INVALID
     assert b(op=1)[0] == ll.LL_ERR_UNSUPPORTED
-    assert b(algo=9)[0] == ll.LL_ERR_INVALID
+    assert b(algo=10)[0] == ll.LL_ERR_INVALID
+    assert b(algo=ll.LL_ALGO_TWOSHOT_ATOMIC)[0] == ll.LL_ERR_UNSUPPORTED
     assert b(s=256)[0] == ll.LL_ERR_SCRATCH
     assert b(out=IN + 16)[0] == ll.LL_ERR_INVALID            # partial overlap of in and out
     assert b(out=scr + 4096)[0] == ll.LL_ERR_INVALID         # output inside the scratch region
@@ -169,7 +171,7 @@ def test_slice_bytes_gives_enough_capacity(dt, es, p):
         # the region is not much larger than the input plus the slots it needs:
         # P-1 one-shot slots per area at 2x (8-byte packets), 128/120x (lines)
         # and 1x (sentinel) the input, plus per-slot rounding
-        assert stride <= (1 + (p - 1) * (2 + 128 / 120 + 1) * 1.02) * max(cap, 256) + 8 * 1024 * p
+        assert stride <= (1 + (p - 1) * (2 + 128 / 120 + 1) * 1.02 + 2.1) * max(cap, 256) + 8 * 1024 * p
 
 
 def test_slice_bytes_argument_checks():
@@ -186,11 +188,13 @@ def test_slice_layout_areas_are_ordered_and_fit(p):
         st, offs = ll.ll_slice_layout(stride, p)
         assert st == ll.LL_OK
         assert offs[0] == 0 and offs[1] == ll.ll_input_capacity(stride, p)[1]
-        assert all(a < b for a, b in zip(offs, offs[1:])) and offs[4] <= stride
+        assert all(a < b for a, b in zip(offs, offs[1:])) and offs[5] <= stride
         assert all(o % 256 == 0 for o in offs)
         # every 16-byte sentinel slot of one rank pair holds count*4 bytes
-        assert offs[4] - offs[3] >= 2 * (p - 1) * ((count * 4 + p - 1) // p)
-        assert offs[4] - offs[3] >= (p - 1) * count * 4
+        assert offs[5] - offs[4] >= 2 * (p - 1) * ((count * 4 + p - 1) // p)
+        assert offs[5] - offs[4] >= (p - 1) * count * 4
+        # the accumulator holds a bfloat16 chunk in binary32, plus counters
+        assert offs[4] - offs[3] >= 2 * ((count * 4 + p - 1) // p)
     assert ll.ll_slice_layout(1000, p)[0] == ll.LL_ERR_INVALID
     assert ll.ll_slice_layout(256, p)[0] == ll.LL_ERR_SCRATCH
 

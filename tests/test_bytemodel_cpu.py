@@ -42,3 +42,14 @@ def test_rs_ag_bytes():
     assert bm.reduce_scatter_bytes("sentinel", p, c, es) == p * (p * b + 3 * (p - 1) * b + b)
     assert bm.allgather_bytes("packet8", p, c, es) == p * (b + 4 * (p - 1) * b + p * b)
     assert bm.useful_bytes(p, c, es) == 2 * p * b
+
+
+def test_direct_output_variants():
+    p, count, es = 8, 1 << 20, 4
+    m, c = count * es, count * es // p
+    assert bm.allreduce_bytes("twoshot_sentinel_out", p, count, es) == p * (3 * m + 4 * (p - 1) * c)
+    # atomic: input, adds (read + write of a binary32 accumulator), accumulator
+    # read and reset, output, poll, fill
+    assert bm.allreduce_bytes("twoshot_atomic", p, count, es) == p * (m + 2 * m + 2 * c + m + (p - 1) * c + m)
+    assert bm.allreduce_bytes("twoshot_atomic", p, count, 2) == p * (count * 2 * 3 + 4 * count * 2 + 4 * c // 2
+                                                                     + (p - 1) * c // 2)

@@ -17,6 +17,7 @@ torch = pytest.importorskip("torch")
 
 import oracle  # noqa: E402
 from paper_2607_16100_amd import workloads as wl  # noqa: E402
+from sumbound import assert_within_summation_bound  # noqa: E402
 
 if torch.cuda.is_available():
     from paper_2607_16100_amd import llcoll as ll  # noqa: E402
@@ -379,11 +380,11 @@ def test_sentinel_slots_are_restored_after_every_call(algo):
     x = wl.normal(p, n, "bf16", seed=21)
     reg = SymRegion(p, n, "bf16")
     reg.init()
-    assert (reg.read_area(3) == SENT).all() and (reg.read_area(1) == 0).all() and (reg.read_area(2) == 0).all()
+    assert (reg.read_area(4) == SENT).all() and (reg.read_area(1) == 0).all() and (reg.read_area(2) == 0).all()
     for k in range(3):
         say(f"sentinel restore {algo} call {k}")
         assert_bits_equal(run_allreduce(reg, x, algo), oracle.allreduce(x), f"{algo} call {k}")
-        area = reg.read_area(3)
+        area = reg.read_area(4)
         assert (area == SENT).all(), f"{algo}: {(area != SENT).sum()} words not reset after call {k}"
     assert (reg.read_area(1) == 0).all() and (reg.read_area(2) == 0).all()
     m = n // p
@@ -391,7 +392,7 @@ def test_sentinel_slots_are_restored_after_every_call(algo):
         reg.write_inputs(x)
         st = reg.reduce_scatter(m, "sentinel") if proto_call == "rs" else reg.allgather(m, "sentinel")
         check_ok(st, proto_call)
-        assert (reg.read_area(3) == SENT).all(), f"{proto_call}: slots not reset"
+        assert (reg.read_area(4) == SENT).all(), f"{proto_call}: slots not reset"
 
 
 @pytest.mark.parametrize("algo", ["oneshot_sentinel", "twoshot_sentinel"])
@@ -465,7 +466,7 @@ def test_direct_output_twoshot_parity():
         for k in range(2):
             say(f"direct P={p} n={n} {dtype} call {k}")
             assert_bits_equal(run_allreduce(reg, x, "twoshot_sentinel_out"), want, f"direct P={p} n={n} {dtype}")
-        assert (reg.read_area(3) == SENT).all()
+        assert (reg.read_area(4) == SENT).all()
 
 
 def test_direct_output_needs_16_byte_rows():
@@ -525,3 +526,61 @@ def test_auto_with_sentinel_allowed(p):
             del reg
     finally:
         ll.ll_set_auto_sentinel(0)
+
+
+# ------------------------------------------------ atomic-accumulation two-shot
+ATOMIC_CASES = [(2, 4, "f32"), (3, 300, "f32"), (4, 1024, "f32"), (5, 1004, "f32"), (8, 8, "f32"),
+                (8, 8192, "f32"), (8, 100_000, "f32"), (8, 8, "bf16"), (8, 8192, "bf16"), (7, 4000, "bf16"),
+                (8, 64 * 8192, "bf16"), (4, 7168 * 16, "bf16"), (8, 1 << 20, "f32")]
+
+
+def test_atomic_twoshot_within_bound_and_identical_on_all_ranks():
+    for p, n, dtype in ATOMIC_CASES:
+        x = wl.normal(p, n, dtype, seed=7 * n + p)
+        reg = SymRegion(p, n, dtype)
+        reg.init()
+        for k in range(3):  # accumulators and counters must be back at zero after each call
+            say(f"atomic P={p} n={n} {dtype} call {k}")
+            got = run_allreduce(reg, x, "twoshot_atomic")
+            assert_within_summation_bound(got, x, dtype, f"atomic P={p} n={n} {dtype} call {k}")
+        assert (reg.read_area(3) == 0).all(), "accumulators or counters not reset"
+        assert (reg.read_area(4) == SENT).all()
+
+
+def test_atomic_twoshot_adversarial_sums():
+    """The C5 adversarial recipe (near-cancelling rank pairs) still meets the
+    bound; with binary32 accumulation cancellation is what stresses it."""
+    for p in (4, 8):
+        n = 7168 * 16
+        x = wl.adversarial(p, n, seed=11)
+        reg = SymRegion(p, n, "bf16")
+        reg.init()
+        assert_within_summation_bound(run_allreduce(reg, x, "twoshot_atomic"), x, "bf16", f"adversarial P={p}")
+
+
+def test_atomic_twoshot_launch_shapes():
+    p, n = 8, 50_000
+    x = wl.uniform(p, n, "f32", seed=31)
+    reg = SymRegion(p, n, "f32")
+    reg.init()
+    for wg, threads in [(1, 64), (3, 256), (16, 128), (0, 0)]:
+        ll.ll_set_launch(wg, threads)
+        say(f"atomic launch wg={wg} threads={threads}")
+        assert_within_summation_bound(run_allreduce(reg, x, "twoshot_atomic"), x, "f32", f"atomic wg={wg}")
+    ll.ll_set_launch(0, 0)
+
+
+def test_atomic_twoshot_missing_peer_times_out():
+    p, n = 8, 4096
+    x = wl.uniform(p, n, "f32", seed=1)
+    reg = SymRegion(p, n, "f32")
+    reg.init()
+    reg.write_inputs(x)
+    ll.ll_set_poll_timeout(200_000)
+    ll.ll_debug_mute_rank(2)
+    assert reg.allreduce(n, "twoshot_atomic") == ll.LL_OK
+    assert ll.ll_check(stream()) == ll.LL_ERR_TIMEOUT
+    ll.ll_debug_mute_rank(-1)
+    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
+    reg.init()
+    assert_within_summation_bound(run_allreduce(reg, x, "twoshot_atomic"), x, "f32", "after timeout")
