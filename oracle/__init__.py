@@ -66,6 +66,10 @@ def _load():
             fn = getattr(lib, name)
             fn.argtypes = [vp, vp, sz, ci, ci]
             fn.restype = ci
+        for name in ("ref_broadcast", "ref_reduce"):
+            fn = getattr(lib, name)
+            fn.argtypes = [vp, vp, sz, ci, ci, ci]
+            fn.restype = ci
         lib.ref_bf16_from_f32_bits.argtypes = [ctypes.c_uint32]
         lib.ref_bf16_from_f32_bits.restype = ctypes.c_uint16
         lib.ref_f32_bits_from_bf16.argtypes = [ctypes.c_uint16]
@@ -121,6 +125,28 @@ def allgather(x: np.ndarray) -> np.ndarray:
     rc = _load().ref_allgather(x.ctypes.data, out.ctypes.data, s, _dtype_code(x), p)
     if rc != 0:
         raise ValueError("ref_allgather rejected its arguments")
+    return out
+
+
+def broadcast(x: np.ndarray, root: int) -> np.ndarray:
+    """x is [P, n]; out[r] is x[root] for every rank r."""
+    x = _prep(x)
+    p, n = x.shape
+    out = np.empty_like(x)
+    rc = _load().ref_broadcast(x.ctypes.data, out.ctypes.data, n, _dtype_code(x), p, root)
+    if rc != 0:
+        raise ValueError("ref_broadcast rejected its arguments")
+    return out
+
+
+def reduce(x: np.ndarray, root: int) -> np.ndarray:
+    """x is [P, n]; the root's result: the ordered sum of the P rows, rounded once."""
+    x = _prep(x)
+    p, n = x.shape
+    out = np.empty(n, dtype=x.dtype)
+    rc = _load().ref_reduce(x.ctypes.data, out.ctypes.data, n, _dtype_code(x), p, root)
+    if rc != 0:
+        raise ValueError("ref_reduce rejected its arguments")
     return out
 
 

@@ -23,6 +23,11 @@
  *   AllGather (Sec. III-A, two-shot): rank r ends with the concatenation of
  *   every rank's input, in rank order.
  *
+ *   Broadcast and Reduce (Sec. V, the artifact's further low-latency
+ *   collectives; their meaning is the usual one): Broadcast gives every rank
+ *   a copy of the root's input; Reduce gives the root alone the reduced
+ *   value, the same ascending-rank binary32 sum as AllReduce.
+ *
  * Element types: dtype 0 = IEEE binary32, dtype 1 = bfloat16.  Values are
  * passed as raw bit patterns so nothing on the Python side reinterprets them.
  * bfloat16 -> binary32 is exact (shift left by 16); binary32 -> bfloat16 is
@@ -39,6 +44,8 @@
  *   ref_allreduce      in [P][count]          out [P][count]
  *   ref_reduce_scatter in [P][P*recvcount]    out [P][recvcount]
  *   ref_allgather      in [P][sendcount]      out [P][P*sendcount]
+ *   ref_broadcast      in [P][count]          out [P][count]
+ *   ref_reduce         in [P][count]          out [count]       (the root's result)
  *
  * Return value: 0 on success, -1 on a bad argument.
  */
@@ -190,6 +197,23 @@ int ref_allgather(const void *in, void *out, size_t sendcount, int dtype, int nr
       memcpy(obase + ((size_t)r * nranks + q) * block, ibase + (size_t)q * block, block);
     }
   }
+  return 0;
+}
+
+int ref_broadcast(const void *in, void *out, size_t count, int dtype, int nranks, int root) {
+  if (bad_args(in, out, dtype, nranks) || root < 0 || root >= nranks) return -1;
+  size_t block = count * elem_size(dtype);
+  const unsigned char *src = (const unsigned char *)in + (size_t)root * block;
+  unsigned char *obase = (unsigned char *)out;
+  for (int r = 0; r < nranks; ++r) memcpy(obase + (size_t)r * block, src, block);
+  return 0;
+}
+
+int ref_reduce(const void *in, void *out, size_t count, int dtype, int nranks, int root) {
+  if (bad_args(in, out, dtype, nranks) || root < 0 || root >= nranks) return -1;
+  unsigned int env = fpenv_enter();
+  for (size_t i = 0; i < count; ++i) store_elem(out, i, dtype, reduce_elem(in, count, i, dtype, nranks));
+  fpenv_leave(env);
   return 0;
 }
 

@@ -40,7 +40,13 @@ def as_f32(bits_row):
     return npref.widen(np.asarray(bits_row))
 
 
-ORACLES = [("c", oracle.allreduce), ("numpy", npref.allreduce)]
+def _reduce_on_every_rank(x):
+    """The C oracle's Reduce (root = last rank), laid out like an AllReduce
+    so that every AllReduce pin below applies to it unchanged."""
+    return np.tile(oracle.reduce(x, x.shape[0] - 1), (x.shape[0], 1))
+
+
+ORACLES = [("c", oracle.allreduce), ("numpy", npref.allreduce), ("c_reduce", _reduce_on_every_rank)]
 
 
 # ---------------------------------------------------------------- wrong oracles
@@ -358,6 +364,43 @@ def test_allgather_of_reduce_scatter_is_allreduce(dtype, p):
     rs = oracle.reduce_scatter(x)
     ag = oracle.allgather(rs)
     assert np.array_equal(ag, oracle.allreduce(x))
+
+
+# ---------------------------------------------------------------- Broadcast and Reduce
+@pytest.mark.parametrize("dtype", [wl.F32, wl.BF16])
+@pytest.mark.parametrize("p", [2, 3, 8])
+def test_broadcast_is_the_roots_block_of_allgather(dtype, p):
+    """Every rank's Broadcast result is block `root` of its AllGather result
+    (AllGather is pinned above); with rank-index fills it is the root's index."""
+    n = 77
+    x = wl.uniform(p, n, dtype, seed=12)
+    ag = oracle.allgather(x)
+    for root in range(p):
+        bc = oracle.broadcast(x, root)
+        for r in range(p):
+            assert bc[r].tobytes() == ag[r, root * n:(root + 1) * n].tobytes()
+    idx = wl.rank_index(p, 9, dtype)
+    assert np.all(npref.widen(oracle.broadcast(idx, p - 1)) == np.float32(p - 1))
+    # a Broadcast that sent rank 0's data whatever the root would fail
+    assert not np.array_equal(oracle.broadcast(x, p - 1), np.tile(x[0], (p, 1)))
+
+
+@pytest.mark.parametrize("dtype", [wl.F32, wl.BF16])
+@pytest.mark.parametrize("p", [2, 5, 8])
+def test_reduce_is_a_row_of_allreduce_for_every_root(dtype, p):
+    x = wl.adversarial(p, 999, seed=3) if dtype == wl.BF16 else wl.normal(p, 999, dtype, seed=3)
+    ar = oracle.allreduce(x)
+    for root in range(p):
+        assert np.array_equal(oracle.reduce(x, root), ar[root])
+
+
+def test_broadcast_and_reduce_reject_bad_roots():
+    x = wl.ones(4, 8, wl.F32)
+    for fn in (oracle.broadcast, oracle.reduce):
+        with pytest.raises(ValueError):
+            fn(x, 4)
+        with pytest.raises(ValueError):
+            fn(x, -1)
 
 
 def test_empty_inputs():
