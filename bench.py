@@ -206,6 +206,35 @@ def paced_collective(torch, ll, reg, kind, count, code, steps, warmup):
             "threads": threads}
 
 
+def bench_rooted(torch, ll, steps):
+    """Broadcast and Reduce, 8 ranks, bf16, 16 KiB and 1 MiB per rank, root 0."""
+    from paper_2607_16100_amd import workloads as wl
+    from paper_2607_16100_amd.region import SymRegion
+
+    out = {}
+    p = 8
+    for n in (8192, 1 << 19):
+        reg = SymRegion(p, n, "bf16")
+        reg.init()
+        reg.write_inputs(wl.normal(p, n, "bf16", seed=0))
+        s = reg.stream_handle()
+        for kind, code in (("broadcast", 0), ("reduce", 1)):
+            for proto in ("packet8", "line128", "sentinel"):
+                def queue(first, cnt, stamps_ptr, stride, code=code, proto=proto):
+                    ll.check(ll.ll_bench_rooted(code, reg.base, reg.rank_stride, reg.out_ptr, n, reg.dt, 0, p,
+                                                reg.epoch + 1, cnt, ll.PROTOS[proto], stamps_ptr, stride, s), kind)
+                    reg.epoch += cnt
+
+                queue(0, 20, 0, 0)
+                torch.cuda.synchronize()
+                grid, threads = ll.ll_last_grid()
+                iv, sp = gpu_paced(torch, ll, queue, steps, grid)
+                ll.check(ll.ll_check(s), kind)
+                out[f"{kind}_{n * 2 >> 10}KiB_{proto}"] = {"p50_us": pct(iv, 50), "p99_us": pct(iv, 99)}
+        del reg
+    return out
+
+
 def bench_c3(torch, ll, steps):
     """1 MiB per rank (batch 64 x hidden 8192 bf16, 8 ranks): two-shot against one-shot."""
     from paper_2607_16100_amd import workloads as wl
@@ -447,7 +476,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--bw-iters", type=int, default=20)
-    ap.add_argument("--only", default="", help="comma list of sections: headline,floor,sol,bw,c3,c5,scratch,copy,cpu")
+    ap.add_argument("--only", default="", help="comma list of sections: headline,floor,sol,bw,c3,c5,rooted,scratch,copy,cpu")
     ap.add_argument("--sweep", default="", help="also run the full C4 size sweep, writing JSON lines to this file")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -497,6 +526,10 @@ def main():
         log("C5: reduce-scatter / all-gather")
         result["c5"] = bench_c5(torch, ll, min(args.steps, 1000))
         log(json.dumps(result["c5"]))
+    if want("rooted"):
+        log("Broadcast / Reduce")
+        result["rooted"] = bench_rooted(torch, ll, min(args.steps, 1000))
+        log(json.dumps(result["rooted"]))
     if want("scratch"):
         log("scratch-size study: 32 MiB f32, 8 ranks")
         result["scratch"] = bench_scratch(torch, ll)

@@ -238,6 +238,22 @@ int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, 
                           void *scratch_base, size_t scratch_stride, uint32_t epoch, void *stream, ll_algo algo,
                           uint32_t *epochs_used);
 
+/* Broadcast: every rank receives the root's `count` input elements; rank r's
+ * copy at out + r*count*esize (the root's own copy included).  One exchange:
+ * the root stores packets into one slot of every peer (the paper lists
+ * Broadcast among the collectives built from the same primitives, Sec. V).
+ * root in [0, nranks).  proto as for ReduceScatter (AUTO: 8-byte packets up
+ * to 64 KiB, then lines, or sentinel when allowed). */
+int ll_broadcast(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt, int root, int nranks,
+                 uint32_t epoch, void *stream, ll_proto proto);
+
+/* Reduce (sum): the root receives the AllReduce result, `count` elements at
+ * `out` (only the root's result is written).  Every other rank stores its
+ * input as packets into its slot of the root, which sums in ascending rank
+ * order and rounds once, as ll_allreduce. */
+int ll_reduce(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt, ll_op op, int root,
+              int nranks, uint32_t epoch, void *stream, ll_proto proto);
+
 /* Synchronise `stream`, then report and clear the device status word:
  * LL_OK, LL_ERR_TIMEOUT, or LL_ERR_HIP. */
 int ll_check(void *stream);

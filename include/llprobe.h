@@ -83,6 +83,10 @@ int ll_bench_reduce_scatter(void *sym_base, size_t rank_stride, void *out, size_
 int ll_bench_allgather(void *sym_base, size_t rank_stride, void *out, size_t sendcount, int dt, int nranks,
                        uint32_t first_epoch, int calls, int proto, uint64_t *stamps, int stamp_stride,
                        void *stream);
+/* ll_bench_rooted: `calls` Broadcasts (kind 0) or Reduces (kind 1). */
+int ll_bench_rooted(int kind, void *sym_base, size_t rank_stride, void *out, size_t count, int dt, int root,
+                    int nranks, uint32_t first_epoch, int calls, int proto, uint64_t *stamps, int stamp_stride,
+                    void *stream);
 int ll_bench_floor(const uint64_t *chase, uint64_t chase_len, uint64_t first_line, uint64_t line_step,
                    uint64_t *sink, int grid, int threads, int calls, uint64_t *stamps, int stamp_stride,
                    void *stream);

@@ -50,7 +50,7 @@ struct KArgs {
   int64_t iter_n;
   uint64_t sub_bytes;
   uint32_t iters;
-  uint32_t pad3_;
+  int32_t root;         // Broadcast / Reduce root rank
 };
 
 // Wait until every store this wave has issued is acknowledged.  Used between
@@ -94,10 +94,12 @@ __device__ __forceinline__ void idle64(int units) {
 
 template <class Pr, int P>
 __device__ __forceinline__ int poll_all(char *area_r, uint64_t slot, uint32_t off, int r, uint32_t epoch,
-                                         uint64_t deadline, u32x4 *got, int first_wait = 0, int poll_gap = 0) {
+                                         uint64_t deadline, u32x4 *got, int first_wait = 0, int poll_gap = 0,
+                                         uint32_t peers = 0xFFFFFFFFu) {
   // One resource covers the P-1 slots; the slot is selected by the scalar offset.
   const rsrc_t rs = make_rsrc(area_r, (uint32_t)((uint64_t)(P - 1) * slot));
-  uint32_t pend = ((1u << P) - 1u) & ~(1u << r);
+  const uint32_t want = ((1u << P) - 1u) & ~(1u << r) & peers;
+  uint32_t pend = want;
 #pragma unroll
   for (int q = 0; q < P; ++q) got[q] = u32x4{0u, 0u, 0u, 0u};
   int spins = 1;
@@ -127,7 +129,7 @@ __device__ __forceinline__ int poll_all(char *area_r, uint64_t slot, uint32_t of
     const u32x4 sent = {ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel};
 #pragma unroll
     for (int q = 0; q < P; ++q) {
-      if (q == r) continue;
+      if (!(want & (1u << q))) continue;
       st_pkt_at(rs, off, uniform_u32((uint32_t)((uint64_t)slot_of(q, r) * slot)), sent);
     }
   }
@@ -717,6 +719,89 @@ __global__ __launch_bounds__(1024) void k_twoshot_atomic(KArgs a) {
     if (s < steps && publish) step_add(gw + s * GW);
     if (s >= lag && s - lag < steps) step_reduce(gw + (s - lag) * GW);
     if (s >= 2 * lag && s - 2 * lag < steps) step_gather(gw + (s - 2 * lag) * GW);
+  }
+  stamp_end(a);
+}
+
+// ---------------------------------------------------------------------------
+// Broadcast and Reduce (the artifact's further collectives, Sec. V), one
+// exchange each, from the same packet primitives.
+//
+// Broadcast: the root stores its input units into slot (q <- root) of every
+// peer q and copies them to its own output; every other rank polls that one
+// slot and stores what arrives.  Output: every rank's copy, back to back.
+template <class Pr, int DT, int P>
+__global__ __launch_bounds__(1024) void k_broadcast(KArgs a) {
+  stamp_start(a);
+  const Part pt = part_of_block<P>();
+  const int r = pt.r, root = a.root;
+  constexpr int E = Elem<DT>::kBytes;
+  const uint64_t deadline = now_ticks() + a.timeout;
+  const int64_t n = a.n;
+  const int64_t units = Pr::units((n * E + 3) / 4);
+  char *const out_r = a.out + (uint64_t)r * (uint64_t)n * E;
+  const int64_t g = (int64_t)pt.w * blockDim.x + threadIdx.x;
+  const int sub = (int)(g % Pr::kLanes);
+  const int64_t ustep = (int64_t)pt.W * blockDim.x / Pr::kLanes;
+  if (r == root) {
+    const char *const in_r = a.in + (uint64_t)r * a.in_stride;
+    for (int64_t u = g / Pr::kLanes; u < units; u += ustep) {
+      const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+      const u32x4 own = Pr::template load<DT>(in_r, u, sub, n, a.in_al4 != 0);
+      if (r != a.mute) bcast<P>(a, a.area, r, off, Pr::pack(own, a.epoch, sub));
+      Pr::template store<DT>(out_r, u, sub, n, a.al4 != 0, own);
+    }
+  } else {
+    char *const area_r = a.sym + (uint64_t)r * a.stride + a.area;
+    for (int64_t u = g / Pr::kLanes; u < units; u += ustep) {
+      const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+      u32x4 got[P];
+      poll_all<Pr, P>(area_r, a.slot, off, r, a.epoch, deadline, got, 0, 0, 1u << root);
+      Pr::template store<DT>(out_r, u, sub, n, a.al4 != 0, Pr::unpack(got[root], sub));
+    }
+  }
+  stamp_end(a);
+}
+
+// Reduce: every rank but the root stores its input units into slot
+// (root <- q) of the root; the root polls its P-1 slots and sums all P
+// contributions in ascending rank order, rounding once (as AllReduce).
+// Output: the root's result only, `n` elements at `out`.
+template <class Pr, int DT, int P>
+__global__ __launch_bounds__(1024) void k_reduce(KArgs a) {
+  stamp_start(a);
+  const Part pt = part_of_block<P>();
+  const int r = pt.r, root = a.root;
+  constexpr int E = Elem<DT>::kBytes;
+  const uint64_t deadline = now_ticks() + a.timeout;
+  const int64_t n = a.n;
+  const int64_t units = Pr::units((n * E + 3) / 4);
+  const char *const in_r = a.in + (uint64_t)r * a.in_stride;
+  const int64_t g = (int64_t)pt.w * blockDim.x + threadIdx.x;
+  const int sub = (int)(g % Pr::kLanes);
+  const int64_t ustep = (int64_t)pt.W * blockDim.x / Pr::kLanes;
+  if (r != root) {
+    if (r == a.mute) {
+      stamp_end(a);
+      return;
+    }
+    char *const dst = a.sym + (uint64_t)root * a.stride + a.area + (uint64_t)slot_of(r, root) * a.slot;
+    const rsrc_t rs = make_rsrc(dst, (uint32_t)a.slot);
+    for (int64_t u = g / Pr::kLanes; u < units; u += ustep) {
+      const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+      st_pkt(rs, off, Pr::pack(Pr::template load<DT>(in_r, u, sub, n, a.in_al4 != 0), a.epoch, sub));
+    }
+  } else {
+    char *const area_r = a.sym + (uint64_t)r * a.stride + a.area;
+    for (int64_t u = g / Pr::kLanes; u < units; u += ustep) {
+      const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+      const u32x4 own = Pr::template load<DT>(in_r, u, sub, n, a.in_al4 != 0);
+      u32x4 got[P];
+      poll_all<Pr, P>(area_r, a.slot, off, r, a.epoch, deadline, got);
+#pragma unroll
+      for (int q = 0; q < P; ++q) got[q] = Pr::unpack(got[q], sub);
+      Pr::template store<DT>(a.out, u, sub, n, a.al4 != 0, reduce_ordered<Pr, DT, P>(got, own, r));
+    }
   }
   stamp_end(a);
 }

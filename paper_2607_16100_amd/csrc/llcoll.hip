@@ -59,7 +59,9 @@ enum Kind {
   K_ONESHOT_WAVES = 4,
   K_TWOSHOT_OUT = 5,
   K_TWOSHOT_ATOMIC = 6,
-  K_KINDS = 7
+  K_BCAST = 7,
+  K_REDUCE = 8,
+  K_KINDS = 9
 };
 constexpr int kWaveUnits[3] = {1, 2, 4};  // units per lane of the wave-per-peer kernels
 enum Proto { PR_LL = 0, PR_LINE = 1, PR_SENT = 2, PR_COUNT = 3 };
@@ -73,6 +75,8 @@ void fill_row(kernel_fn *row) {
   row[K_RS] = k_reduce_scatter<Pr, DT, P>;
   row[K_AG] = k_allgather<Pr, DT, P>;
   row[K_ONESHOT_WAVES] = nullptr;
+  row[K_BCAST] = k_broadcast<Pr, DT, P>;
+  row[K_REDUCE] = k_reduce<Pr, DT, P>;
   row[K_TWOSHOT_OUT] = nullptr;
   row[K_TWOSHOT_ATOMIC] = nullptr;
   if constexpr (std::is_same<Pr, ProtoSent>::value) {
@@ -353,6 +357,13 @@ ll_proto auto_proto(uint64_t bytes, int P, bool sentinel_ok) {
     return LL_PROTO_LINE128;
   }
   return bytes <= 512 * KiB ? LL_PROTO_PACKET8 : LL_PROTO_LINE128;
+}
+
+// Broadcast / Reduce: 8-byte packets up to 64 KiB per rank, lines above, or
+// sentinel above 64 KiB when allowed.
+ll_proto auto_proto_rooted(uint64_t bytes, bool sentinel_ok) {
+  if (bytes <= (64u << 10)) return LL_PROTO_PACKET8;
+  return sentinel_ok ? LL_PROTO_SENTINEL : LL_PROTO_LINE128;
 }
 
 // Algorithms whose AllGather stores into the peers' sentinel-filled outputs.
@@ -692,6 +703,52 @@ int ll_allgather(void *sym_base, size_t rank_stride, void *out, size_t sendcount
   return ll_allgather_proto(sym_base, rank_stride, out, sendcount, dt, nranks, epoch, stream, LL_PROTO_AUTO);
 }
 
+// Broadcast / Reduce: one exchange in the one-shot slots of the chosen format.
+static int rooted_call(Kind kind, void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt, int root,
+                       int nranks, uint32_t epoch, void *stream, ll_proto proto) {
+  int st = check_common(sym_base, rank_stride, out, nranks, epoch);
+  if (st != LL_OK) return st;
+  if (root < 0 || root >= nranks) return LL_ERR_INVALID;
+  if ((int)proto < LL_PROTO_AUTO || (int)proto > LL_PROTO_SENTINEL) return LL_ERR_INVALID;
+  const int es = esize_of(dt);
+  if (count > L::kMaxInputBytes) return LL_ERR_UNSUPPORTED;
+  const uint64_t in_bytes = (uint64_t)count * es;
+  const uint64_t out_bytes = kind == K_BCAST ? in_bytes * nranks : in_bytes;
+  if (overlaps(out, out_bytes, sym_base, (uint64_t)rank_stride * nranks)) return LL_ERR_INVALID;
+  Region rg;
+  st = region_of(rank_stride, nranks, in_bytes, &rg);
+  if (st != LL_OK) return st;
+  if (count == 0) return LL_OK;
+  if (proto == LL_PROTO_AUTO) proto = auto_proto_rooted(in_bytes, g_auto_sentinel.load() != 0);
+  Plan pl;
+  pl.kind = kind;
+  pl.dt = (int)dt;
+  pl.P = nranks;
+  pl.proto = proto == LL_PROTO_LINE128 ? PR_LINE : (proto == LL_PROTO_SENTINEL ? PR_SENT : PR_LL);
+  pl.a = base_args(sym_base, rank_stride, out, epoch);
+  pl.a.n = (int64_t)count;
+  pl.a.al4 = (in_bytes % 4 == 0) ? 1u : 0u;
+  pl.a.root = root;
+  pl.a.area = rg.area_of(pl.proto);
+  pl.a.slot = slot_bytes(pl.proto, in_bytes);
+  pl.units = units_of(pl.proto, in_bytes);
+  return launch(pl, stream);
+}
+
+int ll_broadcast(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt, int root, int nranks,
+                 uint32_t epoch, void *stream, ll_proto proto) {
+  const int st = check_dtype_op((int)dt, LL_SUM);
+  if (st != LL_OK) return st;
+  return rooted_call(K_BCAST, sym_base, rank_stride, out, count, dt, root, nranks, epoch, stream, proto);
+}
+
+int ll_reduce(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt, ll_op op, int root,
+              int nranks, uint32_t epoch, void *stream, ll_proto proto) {
+  const int st = check_dtype_op((int)dt, (int)op);
+  if (st != LL_OK) return st;
+  return rooted_call(K_REDUCE, sym_base, rank_stride, out, count, dt, root, nranks, epoch, stream, proto);
+}
+
 int ll_check(void *stream) {
   hipError_t e = hipStreamSynchronize((hipStream_t)stream);
   if (e != hipSuccess) {
@@ -884,6 +941,28 @@ int ll_bench_allreduce(void *sym_base, size_t rank_stride, void *out, size_t cou
     if (stamps != nullptr) g_stamps.store(stamps + (size_t)i * (size_t)stamp_stride);
     const int st = ll_allreduce_algo(sym_base, rank_stride, out, count, (ll_dtype)dt, LL_SUM, nranks,
                                      first_epoch + (uint32_t)i, stream, (ll_algo)algo);
+    if (st != LL_OK) {
+      g_stamps.store(nullptr);
+      return st;
+    }
+  }
+  return LL_OK;
+}
+
+int ll_bench_rooted(int kind, void *sym_base, size_t rank_stride, void *out, size_t count, int dt, int root,
+                    int nranks, uint32_t first_epoch, int calls, int proto, uint64_t *stamps, int stamp_stride,
+                    void *stream) {
+  if (kind != 0 && kind != 1) return LL_ERR_INVALID;
+  if (calls < 1 || first_epoch == 0 || (uint64_t)first_epoch + (uint64_t)calls - 1 > 0xFFFFFFFFull)
+    return LL_ERR_INVALID;
+  if (stamps != nullptr && stamp_stride < 1) return LL_ERR_INVALID;
+  for (int i = 0; i < calls; ++i) {
+    if (stamps != nullptr) g_stamps.store(stamps + (size_t)i * (size_t)stamp_stride);
+    const uint32_t e = first_epoch + (uint32_t)i;
+    const int st = kind == 0 ? ll_broadcast(sym_base, rank_stride, out, count, (ll_dtype)dt, root, nranks, e, stream,
+                                            (ll_proto)proto)
+                             : ll_reduce(sym_base, rank_stride, out, count, (ll_dtype)dt, LL_SUM, root, nranks, e,
+                                         stream, (ll_proto)proto);
     if (st != LL_OK) {
       g_stamps.store(nullptr);
       return st;

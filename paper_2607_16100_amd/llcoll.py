@@ -49,6 +49,9 @@ _SIGS = {
     "ll_slice_layout": (_i, [_sz, _i, ctypes.POINTER(_sz)]),
     "ll_init": (_i, [_vp, _sz, _i, _vp]),
     "ll_fill_sentinel": (_i, [_vp, _sz, _i, _i, _vp]),
+    "ll_broadcast": (_i, [_vp, _sz, _vp, _sz, _i, _i, _i, _u32, _vp, _i]),
+    "ll_reduce": (_i, [_vp, _sz, _vp, _sz, _i, _i, _i, _i, _u32, _vp, _i]),
+    "ll_bench_rooted": (_i, [_i, _vp, _sz, _vp, _sz, _i, _i, _i, _u32, _i, _i, _vp, _i, _vp]),
     "ll_scratch_bytes": (_i, [_sz, _i, ctypes.POINTER(_sz)]),
     "ll_scratch_iter_bytes": (_i, [_sz, _i, ctypes.POINTER(_sz)]),
     "ll_scratch_init": (_i, [_vp, _sz, _i, _vp]),
@@ -218,6 +221,20 @@ def ll_allreduce_buffered(inp, out, count, dt, op, nranks, scratch_base, scratch
     st = _lib.ll_allreduce_buffered(inp, out, count, dt, op, nranks, scratch_base, scratch_stride, epoch, stream,
                                     algo, ctypes.byref(used))
     return st, used.value
+
+
+def ll_broadcast(sym_base, rank_stride, out, count, dt, root, nranks, epoch, stream, proto):
+    return _lib.ll_broadcast(sym_base, rank_stride, out, count, dt, root, nranks, epoch, stream, proto)
+
+
+def ll_reduce(sym_base, rank_stride, out, count, dt, op, root, nranks, epoch, stream, proto):
+    return _lib.ll_reduce(sym_base, rank_stride, out, count, dt, op, root, nranks, epoch, stream, proto)
+
+
+def ll_bench_rooted(kind, sym_base, rank_stride, out, count, dt, root, nranks, first_epoch, calls, proto, stamps,
+                    stamp_stride, stream):
+    return _lib.ll_bench_rooted(kind, sym_base, rank_stride, out, count, dt, root, nranks, first_epoch, calls, proto,
+                                stamps, stamp_stride, stream)
 
 
 def ll_fill_sentinel(out, count, dt, nranks, stream):

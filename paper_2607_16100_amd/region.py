@@ -106,6 +106,16 @@ class SymRegion:
         return self.out[:nbytes].cpu().numpy().view(np_dtype).copy()
 
     # -- collectives (one launch each, on the given stream)
+    def broadcast(self, count: int, root: int, proto: str = "auto", stream=None, epoch: int | None = None) -> int:
+        e = self.next_epoch() if epoch is None else epoch
+        return ll.ll_broadcast(self.base, self.rank_stride, self.out_ptr, count, self.dt, root, self.nranks, e,
+                               self.stream_handle(stream), ll.PROTOS[proto])
+
+    def reduce(self, count: int, root: int, proto: str = "auto", stream=None, epoch: int | None = None) -> int:
+        e = self.next_epoch() if epoch is None else epoch
+        return ll.ll_reduce(self.base, self.rank_stride, self.out_ptr, count, self.dt, ll.LL_SUM, root, self.nranks,
+                            e, self.stream_handle(stream), ll.PROTOS[proto])
+
     def fill_out_sentinel(self, count: int, stream=None) -> int:
         """Fill the P outputs of `count` elements with the sentinel."""
         return ll.ll_fill_sentinel(self.out_ptr, count, self.dt, self.nranks, self.stream_handle(stream))

@@ -149,6 +149,22 @@ def test_buffered_argument_checks():
     assert b(count=0) == (ll.LL_OK, 0)
 
 
+def test_broadcast_reduce_argument_checks():
+    stride = stride_for(1000, F32, 4)
+    bc, rd = ll.ll_broadcast, ll.ll_reduce
+    assert bc(GOOD_BASE, stride, GOOD_OUT, 1000, F32, 4, 4, 1, 0, 0) == ll.LL_ERR_INVALID   # root >= P
+    assert bc(GOOD_BASE, stride, GOOD_OUT, 1000, F32, -1, 4, 1, 0, 0) == ll.LL_ERR_INVALID
+    assert bc(GOOD_BASE, stride, GOOD_OUT, 1000, F32, 0, 4, 0, 0, 0) == ll.LL_ERR_INVALID   # epoch 0
+    assert bc(GOOD_BASE, stride, GOOD_OUT, 1000, F32, 0, 4, 1, 0, 4) == ll.LL_ERR_INVALID   # proto
+    assert bc(GOOD_BASE, stride, GOOD_OUT, 100_000, F32, 0, 4, 1, 0, 0) == ll.LL_ERR_SCRATCH
+    assert bc(GOOD_BASE, stride, GOOD_BASE + 256, 10, F32, 0, 4, 1, 0, 0) == ll.LL_ERR_INVALID  # out in region
+    assert bc(GOOD_BASE, stride, GOOD_OUT, 0, F32, 0, 4, 1, 0, 0) == ll.LL_OK
+    assert rd(GOOD_BASE, stride, GOOD_OUT, 1000, F32, 1, 0, 4, 1, 0, 0) == ll.LL_ERR_UNSUPPORTED  # op
+    assert rd(GOOD_BASE, stride, GOOD_OUT, 1000, 3, 0, 0, 4, 1, 0, 0) == ll.LL_ERR_UNSUPPORTED   # dtype
+    assert rd(GOOD_BASE, stride, GOOD_OUT, 1000, F32, 0, 9, 4, 1, 0, 0) == ll.LL_ERR_INVALID
+    assert rd(GOOD_BASE, stride, GOOD_OUT, 0, F32, 0, 0, 4, 1, 0, 0) == ll.LL_OK
+
+
 def test_init_argument_checks():
     assert ll.ll_init(0, 4096, 4, 0) == ll.LL_ERR_INVALID
     assert ll.ll_init(GOOD_BASE, 4096, 1, 0) == ll.LL_ERR_INVALID

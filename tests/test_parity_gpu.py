@@ -584,3 +584,59 @@ def test_atomic_twoshot_missing_peer_times_out():
     ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
     reg.init()
     assert_within_summation_bound(run_allreduce(reg, x, "twoshot_atomic"), x, "f32", "after timeout")
+
+
+# ------------------------------------------------ Broadcast and Reduce
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("p", [2, 3, 5, 8])
+def test_broadcast_and_reduce_parity(dtype, p):
+    reg = SymRegion(p, 70_001, dtype)
+    reg.init()
+    for n in [1, 3, 255, 4096, 70_001]:
+        x = wl.normal(p, n, dtype, seed=3 * n + p)
+        reg.write_inputs(x)
+        for root in sorted({0, p - 1, p // 2}):
+            for proto in PROTOS + ["auto"]:
+                say(f"broadcast/reduce P={p} {dtype} n={n} root={root} {proto}")
+                check_ok(reg.broadcast(n, root, proto), "broadcast")
+                got = reg.read_out(p * n, NP[dtype]).reshape(p, n)
+                assert_bits_equal(got, oracle.broadcast(x, root), f"broadcast {proto} root={root} n={n}")
+                check_ok(reg.reduce(n, root, proto), "reduce")
+                got = reg.read_out(n, NP[dtype]).reshape(1, n)
+                assert_bits_equal(got, oracle.reduce(x, root).reshape(1, n), f"reduce {proto} root={root} n={n}")
+    assert (reg.read_area(4) == SENT).all()
+
+
+def test_broadcast_reduce_compose_to_allreduce():
+    """Reduce to a root, then Broadcast of the root's result, equals AllReduce."""
+    p, n = 8, 30_000
+    x = wl.adversarial(p, n, seed=4)
+    reg = SymRegion(p, n, "bf16")
+    reg.init()
+    reg.write_inputs(x)
+    check_ok(reg.reduce(n, 5, "line128"), "reduce")
+    red = reg.read_out(n, np.uint16)
+    reg.write_inputs(np.tile(red, (p, 1)))
+    check_ok(reg.broadcast(n, 5, "packet8"), "broadcast")
+    assert_bits_equal(reg.read_out(p * n, np.uint16).reshape(p, n), oracle.allreduce(x), "reduce+broadcast")
+
+
+@pytest.mark.parametrize("kind", ["broadcast", "reduce"])
+def test_rooted_missing_rank_times_out(kind):
+    p, n = 8, 4096
+    x = wl.uniform(p, n, "f32", seed=6)
+    reg = SymRegion(p, n, "f32")
+    reg.init()
+    reg.write_inputs(x)
+    ll.ll_set_poll_timeout(200_000)
+    ll.ll_debug_mute_rank(2 if kind == "broadcast" else 6)  # the root, or a contributor
+    st = reg.broadcast(n, 2, "packet8") if kind == "broadcast" else reg.reduce(n, 2, "packet8")
+    assert st == ll.LL_OK
+    assert ll.ll_check(stream()) == ll.LL_ERR_TIMEOUT
+    rank, missing, _ = ll.ll_last_timeout()
+    assert missing == (1 << (2 if kind == "broadcast" else 6))
+    ll.ll_debug_mute_rank(-1)
+    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
+    reg.init()
+    check_ok(reg.reduce(n, 2, "packet8"), "after timeout")
+    assert_bits_equal(reg.read_out(n, np.uint32).reshape(1, n), oracle.reduce(x, 2).reshape(1, n), "after timeout")
