@@ -86,8 +86,11 @@ typedef enum {
   LL_ALGO_TWOSHOT_SENTINEL = 7, /* two-shot, sentinel synchronisation */
   LL_ALGO_TWOSHOT_SENTINEL_OUT = 8, /* two-shot, sentinel; AllGather straight into the
                                        peers' sentinel-filled outputs (see ll_fill_sentinel) */
-  LL_ALGO_TWOSHOT_ATOMIC = 9        /* two-shot with atomic accumulation (Sec. IV, "LL128
+  LL_ALGO_TWOSHOT_ATOMIC = 9,       /* two-shot with atomic accumulation (Sec. IV, "LL128
                                        Atomic"): NOT deterministic, see below */
+  LL_ALGO_TWOSHOT_WAVES = 10,       /* two-shot, 8-byte packets, one wave per peer, partial
+                                       sums staged in LDS (single iteration only) */
+  LL_ALGO_TWOSHOT_SENTINEL_WAVES = 11 /* the same with sentinel units */
 } ll_algo;
 
 /* LL_ALGO_TWOSHOT_ATOMIC, the analogue of the paper's two-shot LL128 atomic
@@ -271,6 +274,13 @@ const char *ll_strerror(int status);
  * mode, for callers whose data never holds the sentinel dword (0 = no, the
  * default; 1 = yes).  Never selects LL_ALGO_TWOSHOT_SENTINEL_OUT. */
 int ll_set_auto_sentinel(int allow);
+
+/* Kernel family of the stand-alone ReduceScatter / AllGather with 8-byte
+ * packets or sentinel units: 0 = by size (one wave per peer with LDS staging
+ * up to 1 MiB of data per rank at 5-8 ranks and 2 MiB below, one lane per
+ * packet unit above), 1 = one lane per unit always, 2 = one wave per peer
+ * always.  Results do not depend on it. */
+int ll_set_wave_kernels(int mode);
 
 /* Workgroups per rank and threads per workgroup for the following calls;
  * 0 = automatic.  threads must be a multiple of 64 in [64, 1024].  Results do

@@ -575,6 +575,193 @@ __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(LLCOLL_TWO
 }
 
 // ---------------------------------------------------------------------------
+// Two-shot AllReduce, one wave per peer, with LDS staging of the partial sums
+// (8-byte packets or sentinel units); its two halves serve as the
+// stand-alone ReduceScatter (Mode 1) and AllGather (Mode 2).
+//
+// A workgroup has P waves and handles one tile of 64*U packet units at the
+// same offset in every chunk (lane l owns units l, l+64, ... of the tile).
+// ReduceScatter: wave q != r sends the tile of chunk q to its owner q (one
+// store per unit) and polls the tile of chunk r that peer q sent to this
+// rank; wave r loads its own chunk r.  Each wave stages its values, widened
+// to binary32, in LDS row q.  After a workgroup barrier every wave forms the
+// ordered sum of the rows for its lanes' units (all waves compute the same
+// sums) and rounds once.  AllGather: wave q != r sends the reduced tile (for
+// Mode 2: the own input) to peer q and polls the tile of chunk q that peer q
+// sends back, and stores it; wave r stores the own chunk.  As in the one-shot
+// wave kernel, a wave's polls never wait for more than its own U stores.
+//
+// Chunks: Mode 0 cuts the n-element input into chunks of a.chunk elements
+// (the last ones may be short); Mode 1 takes P chunks of a.n elements;
+// Mode 2 has one a.n-element input per rank.  Outputs: Mode 0, rank r's n
+// elements; Mode 1, rank r's chunk; Mode 2, the P blocks of rank r.
+template <class Pr, int DT, int P, int U, int Mode = 0>
+__global__ __launch_bounds__(512) void k_twoshot_waves(KArgs a) {
+  stamp_start(a);
+  constexpr int E = Elem<DT>::kBytes;
+  constexpr int K = Elem<DT>::kPerWord;
+  constexpr int WPU = Pr::kUnitWords;  // payload words per unit
+  constexpr int EPU = WPU * K;         // elements per unit
+  constexpr bool kRS = Mode != 2, kAG = Mode != 1;
+  __shared__ float stage[kRS ? P : 1][64 * U * EPU];
+  const Part pt = part_of_block<P>();
+  const int r = pt.r;
+  const int q = (int)uniform_u32(threadIdx.x >> 6);  // this wave's peer (q == r: the own values)
+  const int lane = (int)(threadIdx.x & 63);
+  const uint64_t deadline = now_ticks() + a.timeout;
+  const int64_t C = Mode == 0 ? a.chunk : a.n;
+  const int64_t n_all = Mode == 0 ? a.n : (int64_t)P * a.n;
+  const bool publish = (r != a.mute);
+  const bool al4 = a.al4 != 0, in_al4 = a.in_al4 != 0;
+  char *const slice_r = a.sym + (uint64_t)r * a.stride;
+  const char *const in_r = a.in + (uint64_t)r * a.in_stride;
+  // where this rank's result for chunk c goes
+  auto out_chunk = [&](int c) -> char * {
+    if (Mode == 1) return a.out + (uint64_t)r * (uint64_t)C * E;
+    return a.out + (uint64_t)r * (uint64_t)n_all * E + (uint64_t)c * C * E;
+  };
+  auto in_chunk = [&](int c) -> const char * { return Mode == 2 ? in_r : in_r + (uint64_t)c * C * E; };
+  const uint64_t ag_area = Mode == 2 ? a.area : a.area + (uint64_t)(P - 1) * a.slot;
+  auto chunk_len = [&](int c) -> int64_t {
+    const int64_t left = n_all - (int64_t)c * C;
+    return left < 0 ? 0 : (left < C ? left : C);
+  };
+  const int64_t units = Pr::units((C * E + 3) / 4);
+  const int64_t tiles = (units + 64 * U - 1) / (64 * U);
+  // slot (q <- r) in peer q's slice and slot (r <- q) in this rank's slice
+  const uint64_t slot_out = (uint64_t)slot_of(r, q) * a.slot, slot_in = (uint64_t)slot_of(q, r) * a.slot;
+  char *const peer_slice = a.sym + (uint64_t)q * a.stride;
+
+  auto stage_row = [&](const u32x4 *w) {
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const uint32_t wv[4] = {w[k].x, w[k].y, w[k].z, w[k].w};
+#pragma unroll
+      for (int j = 0; j < WPU; ++j) {
+        float f[K];
+        Elem<DT>::widen(wv[j], f);
+#pragma unroll
+        for (int e = 0; e < K; ++e) stage[kRS ? q : 0][(k * 64 + lane) * EPU + j * K + e] = f[e];
+      }
+    }
+  };
+
+  // Poll U units of slot `src` (this rank's slice) from peer q; sentinel
+  // units are given back to the sentinel once read.
+  auto poll_peer = [&](char *src, int64_t tile_u0, u32x4 *v) {
+    const rsrc_t rs = make_rsrc(src, (uint32_t)a.slot);
+    uint32_t pend = 0;
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      v[k] = u32x4{0u, 0u, 0u, 0u};
+      if (tile_u0 + k * 64 + lane < units) pend |= 1u << k;
+    }
+    const uint32_t want = pend;
+    int spins = 1;
+    while (pend != 0) {
+      compiler_fence();
+      u32x4 pk[U];
+#pragma unroll
+      for (int k = 0; k < U; ++k)
+        if (pend & (1u << k)) pk[k] = ld_pkt(rs, (uint32_t)((tile_u0 + k * 64 + lane) * Pr::kUnitBytes));
+#pragma unroll
+      for (int k = 0; k < U; ++k) {
+        if ((pend & (1u << k)) && Pr::ready(pk[k], a.epoch)) {
+          v[k] = Pr::unpack(pk[k], 0);
+          pend &= ~(1u << k);
+        }
+      }
+      if (pend != 0 && (spins++ & 15) == 0 && now_ticks() > deadline) {
+        report_timeout(r, 1u << q, a.epoch);
+        break;
+      }
+    }
+    if (ResetsSlots<Pr>::value) {
+      const u32x4 sent = {ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel};
+#pragma unroll
+      for (int k = 0; k < U; ++k)
+        if (want & (1u << k)) st_pkt(rs, (uint32_t)((tile_u0 + k * 64 + lane) * Pr::kUnitBytes), sent);
+    }
+  };
+
+  for (int64_t tile = pt.w; tile < tiles; tile += pt.W) {
+    const int64_t u0 = tile * 64 * U;
+    u32x4 res[U];
+    if constexpr (kRS) {
+      // ---- ReduceScatter of this tile
+      if (q == r) {
+        u32x4 own[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) own[k] = Pr::template load<DT>(in_chunk(r), u0 + k * 64 + lane, 0, chunk_len(r),
+                                                                  in_al4);
+        stage_row(own);
+      } else {
+        if (publish) {
+          const rsrc_t rd = make_rsrc(peer_slice + a.area + slot_out, (uint32_t)a.slot);
+#pragma unroll
+          for (int k = 0; k < U; ++k) {
+            const int64_t u = u0 + k * 64 + lane;
+            if (u < units) {
+              const u32x4 w = Pr::template load<DT>(in_chunk(q), u, 0, chunk_len(q), in_al4);
+              st_pkt(rd, (uint32_t)(u * Pr::kUnitBytes), Pr::pack(w, a.epoch, 0));
+            }
+          }
+        }
+        u32x4 v[U];
+        poll_peer(slice_r + a.area + slot_in, u0, v);
+        stage_row(v);
+      }
+      lds_barrier();
+      // ---- the ordered sum of the tile (every wave computes the same values)
+#pragma unroll
+      for (int k = 0; k < U; ++k) {
+        uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int j = 0; j < WPU; ++j) {
+          float acc[K];
+#pragma unroll
+          for (int e = 0; e < K; ++e) acc[e] = stage[0][(k * 64 + lane) * EPU + j * K + e];
+#pragma unroll
+          for (int p = 1; p < P; ++p) {
+#pragma unroll
+            for (int e = 0; e < K; ++e) acc[e] = acc[e] + stage[p][(k * 64 + lane) * EPU + j * K + e];
+          }
+          w[j] = Elem<DT>::narrow(acc);
+        }
+        res[k] = u32x4{w[0], w[1], w[2], w[3]};
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < U; ++k) res[k] = Pr::template load<DT>(in_chunk(r), u0 + k * 64 + lane, 0, C, in_al4);
+    }
+    // ---- AllGather of this tile
+    if (q == r || !kAG) {
+      if (q == r) {
+#pragma unroll
+        for (int k = 0; k < U; ++k)
+          Pr::template store<DT>(out_chunk(r), u0 + k * 64 + lane, 0, chunk_len(r), al4, res[k]);
+      }
+    } else {
+      if (publish) {
+        const rsrc_t rd = make_rsrc(peer_slice + ag_area + slot_out, (uint32_t)a.slot);
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+          const int64_t u = u0 + k * 64 + lane;
+          if (u < units) st_pkt(rd, (uint32_t)(u * Pr::kUnitBytes), Pr::pack(res[k], a.epoch, 0));
+        }
+      }
+      u32x4 v[U];
+      poll_peer(slice_r + ag_area + slot_in, u0, v);
+#pragma unroll
+      for (int k = 0; k < U; ++k)
+        Pr::template store<DT>(out_chunk(q), u0 + k * 64 + lane, 0, chunk_len(q), al4, v[k]);
+    }
+    if constexpr (kRS) lds_barrier();  // the next tile overwrites the staging rows
+  }
+  stamp_end(a);
+}
+
+// ---------------------------------------------------------------------------
 // Two-shot AllReduce with atomic accumulation: the gfx950 analogue of the
 // paper's two-shot LL128 atomic algorithm (Sec. IV, "LL128 Atomic AllReduce";
 // Fig. 5).

@@ -37,6 +37,7 @@ std::atomic<int> g_poll_gap{0};
 std::atomic<int> g_wave_units{0};  // 0 = automatic, else 1, 2 or 4
 std::atomic<int> g_lag{1};
 std::atomic<int> g_auto_sentinel{0};
+std::atomic<int> g_wave_kernels{0};  // stand-alone RS/AG: 0 = by size, 1 = never, 2 = always
 std::atomic<uint64_t *> g_stamps{nullptr};
 std::atomic<uint64_t *> g_phases{nullptr};
 std::atomic<int> g_last_grid{0};
@@ -61,7 +62,10 @@ enum Kind {
   K_TWOSHOT_ATOMIC = 6,
   K_BCAST = 7,
   K_REDUCE = 8,
-  K_KINDS = 9
+  K_TWOSHOT_WAVES = 9,
+  K_RS_WAVES = 10,
+  K_AG_WAVES = 11,
+  K_KINDS = 12
 };
 constexpr int kWaveUnits[3] = {1, 2, 4};  // units per lane of the wave-per-peer kernels
 enum Proto { PR_LL = 0, PR_LINE = 1, PR_SENT = 2, PR_COUNT = 3 };
@@ -89,9 +93,11 @@ void fill_row(kernel_fn *row) {
 struct Table {
   kernel_fn k[PR_COUNT][2][LL_MAX_RANKS + 1][K_KINDS];
   kernel_fn waves[3][2][LL_MAX_RANKS + 1];  // [log2 U][dtype][P]
+  kernel_fn twaves[3][3][2][2][LL_MAX_RANKS + 1];  // [AR, RS, AG][log2 U][8-byte packets, sentinel][dtype][P]
   Table() {
     memset(k, 0, sizeof k);
     memset(waves, 0, sizeof waves);
+    memset(twaves, 0, sizeof twaves);
     fill<2>();
     fill<3>();
     fill<4>();
@@ -99,6 +105,21 @@ struct Table {
     fill<6>();
     fill<7>();
     fill<8>();
+  }
+  template <int M, int P>
+  void fill_twaves() {
+    twaves[M][0][0][0][P] = k_twoshot_waves<ProtoLL, 0, P, 1, M>;
+    twaves[M][0][0][1][P] = k_twoshot_waves<ProtoLL, 1, P, 1, M>;
+    twaves[M][1][0][0][P] = k_twoshot_waves<ProtoLL, 0, P, 2, M>;
+    twaves[M][1][0][1][P] = k_twoshot_waves<ProtoLL, 1, P, 2, M>;
+    twaves[M][2][0][0][P] = k_twoshot_waves<ProtoLL, 0, P, 4, M>;
+    twaves[M][2][0][1][P] = k_twoshot_waves<ProtoLL, 1, P, 4, M>;
+    twaves[M][0][1][0][P] = k_twoshot_waves<ProtoSent, 0, P, 1, M>;
+    twaves[M][0][1][1][P] = k_twoshot_waves<ProtoSent, 1, P, 1, M>;
+    twaves[M][1][1][0][P] = k_twoshot_waves<ProtoSent, 0, P, 2, M>;
+    twaves[M][1][1][1][P] = k_twoshot_waves<ProtoSent, 1, P, 2, M>;
+    twaves[M][2][1][0][P] = k_twoshot_waves<ProtoSent, 0, P, 4, M>;
+    twaves[M][2][1][1][P] = k_twoshot_waves<ProtoSent, 1, P, 4, M>;
   }
   template <int P>
   void fill() {
@@ -114,6 +135,9 @@ struct Table {
     waves[1][1][P] = k_oneshot_waves<1, P, 2>;
     waves[2][0][P] = k_oneshot_waves<0, P, 4>;
     waves[2][1][P] = k_oneshot_waves<1, P, 4>;
+    fill_twaves<0, P>();
+    fill_twaves<1, P>();
+    fill_twaves<2, P>();
   }
 };
 
@@ -210,15 +234,25 @@ int wave_units_log2(int64_t units) {
 }
 
 int launch(const Plan &pl, void *stream) {
-  const int wlog = pl.kind == K_ONESHOT_WAVES ? wave_units_log2(pl.units) : 0;
-  const kernel_fn fn = pl.kind == K_ONESHOT_WAVES ? table().waves[wlog][pl.dt][pl.P]
-                                                   : table().k[pl.proto][pl.dt][pl.P][pl.kind];
+  const bool two_waves = pl.kind == K_TWOSHOT_WAVES || pl.kind == K_RS_WAVES || pl.kind == K_AG_WAVES;
+  const bool wave_kernel = pl.kind == K_ONESHOT_WAVES || two_waves;
+  const int wlog = wave_kernel ? wave_units_log2(pl.units) : 0;
+  kernel_fn fn = nullptr;
+  if (pl.kind == K_ONESHOT_WAVES) {
+    fn = table().waves[wlog][pl.dt][pl.P];
+  } else if (two_waves) {
+    if (pl.proto == PR_LINE) return LL_ERR_UNSUPPORTED;
+    const int mode = pl.kind == K_TWOSHOT_WAVES ? 0 : (pl.kind == K_RS_WAVES ? 1 : 2);
+    fn = table().twaves[mode][wlog][pl.proto == PR_SENT ? 1 : 0][pl.dt][pl.P];
+  } else {
+    fn = table().k[pl.proto][pl.dt][pl.P][pl.kind];
+  }
   if (fn == nullptr) return LL_ERR_UNSUPPORTED;
   int threads = g_threads.load();
   if (threads == 0) threads = 256;
   int lanes_per_unit = pl.proto == PR_LINE ? ProtoLine::kLanes : 1;
   int64_t work_units = pl.units;
-  if (pl.kind == K_ONESHOT_WAVES) {  // one wave per rank, 64*U units per workgroup and step
+  if (wave_kernel) {  // one wave per rank, 64*U units per workgroup and step
     threads = 64 * pl.P;
     const int64_t tile = 64 * kWaveUnits[wlog];
     work_units = (pl.units + tile - 1) / tile;
@@ -314,49 +348,46 @@ KArgs base_args(void *sym_base, size_t rank_stride, void *out, uint32_t epoch) {
 // every algorithm at 4 KiB .. 64 MiB per rank, P = 2, 4, 8, binary32 and
 // bfloat16; both element types cross over at the same byte sizes);
 // M = input bytes per rank.  Flags only unless the caller allows sentinel
-// mode, which wins from 64 KiB (one-shot) and from 512 KiB at 8 ranks
-// (two-shot), as the paper observes for larger messages and rank counts.
+// mode, which wins for mid sizes, as the paper observes for larger messages
+// and rank counts.
 ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
   const uint64_t KiB = 1024, MiB = 1024 * 1024;
-  if (in_bytes <= 32 * KiB) return LL_ALGO_ONESHOT_WAVES;
-  if (sentinel_ok) {
-    if (P <= 2) {
-      if (in_bytes <= 64 * KiB) return LL_ALGO_ONESHOT;
-      if (in_bytes <= 4 * MiB) return LL_ALGO_ONESHOT_SENTINEL;
-      if (in_bytes <= 8 * MiB) return LL_ALGO_TWOSHOT_SENTINEL;
+  if (P <= 2) {
+    if (in_bytes <= 32 * KiB) return LL_ALGO_ONESHOT_WAVES;
+    if (sentinel_ok) {
+      if (in_bytes <= 2 * MiB) return LL_ALGO_ONESHOT_SENTINEL;
+      if (in_bytes <= 16 * MiB) return LL_ALGO_TWOSHOT_SENTINEL_WAVES;
       return LL_ALGO_TWOSHOT_LINE;
     }
-    if (in_bytes <= (P <= 4 ? 512 : 256) * KiB) return LL_ALGO_ONESHOT_SENTINEL;
-    if (in_bytes <= 4 * MiB) return LL_ALGO_TWOSHOT_SENTINEL;
-    return LL_ALGO_TWOSHOT_LINE;
-  }
-  if (P <= 2) {
     if (in_bytes <= 128 * KiB) return LL_ALGO_ONESHOT;
     if (in_bytes <= 4 * MiB) return LL_ALGO_ONESHOT_LINE;
     return LL_ALGO_TWOSHOT_LINE;
   }
-  if (P <= 4) {
-    if (in_bytes <= 512 * KiB) return LL_ALGO_ONESHOT_LINE;
+  if (in_bytes <= (P <= 4 ? 64 : 16) * KiB) return LL_ALGO_ONESHOT_WAVES;
+  if (sentinel_ok) {
+    if (in_bytes <= 128 * KiB) return LL_ALGO_TWOSHOT_WAVES;
+    if (P <= 4 && in_bytes <= 256 * KiB) return LL_ALGO_ONESHOT_SENTINEL;
+    if (in_bytes <= 4 * MiB) return LL_ALGO_TWOSHOT_SENTINEL_WAVES;
     return LL_ALGO_TWOSHOT_LINE;
   }
-  if (in_bytes <= 128 * KiB) return LL_ALGO_ONESHOT_LINE;
-  if (in_bytes <= 512 * KiB) return LL_ALGO_TWOSHOT;
+  if (in_bytes <= 1 * MiB) return LL_ALGO_TWOSHOT_WAVES;
   return LL_ALGO_TWOSHOT_LINE;
 }
 
 // ReduceScatter / AllGather, by the bytes of data per rank (input for
 // ReduceScatter, output for AllGather), measured the same way at 4 KiB ..
-// 16 MiB: 8-byte packets up to 512 KiB, lines above; with sentinel mode
-// allowed, sentinel from 128 KiB (256 KiB at 8 ranks) up to 4 MiB (8 ranks),
-// 8 MiB (3-4 ranks) or 16 MiB (2 ranks).
+// 16 MiB at 4 and 8 ranks: 8-byte packets up to 1 MiB, lines above; with
+// sentinel mode allowed, sentinel units from 128 KiB (256 KiB at 3-4 ranks,
+// where 8-byte packets stay as fast a little longer) up to 4 MiB (8 MiB at
+// 2-4 ranks).
 ll_proto auto_proto(uint64_t bytes, int P, bool sentinel_ok) {
   const uint64_t KiB = 1024, MiB = 1024 * 1024;
   if (sentinel_ok) {
-    if (bytes <= (P >= 5 ? 128 : 64) * KiB) return LL_PROTO_PACKET8;
-    if (bytes <= (P >= 5 ? 4 : (P >= 3 ? 8 : 16)) * MiB) return LL_PROTO_SENTINEL;
+    if (bytes <= (P >= 5 ? 64 : 128) * KiB) return LL_PROTO_PACKET8;
+    if (bytes <= (P >= 5 ? 4 : 8) * MiB) return LL_PROTO_SENTINEL;
     return LL_PROTO_LINE128;
   }
-  return bytes <= 512 * KiB ? LL_PROTO_PACKET8 : LL_PROTO_LINE128;
+  return bytes <= 1 * MiB ? LL_PROTO_PACKET8 : LL_PROTO_LINE128;
 }
 
 // Broadcast / Reduce: 8-byte packets up to 64 KiB per rank, lines above, or
@@ -364,6 +395,16 @@ ll_proto auto_proto(uint64_t bytes, int P, bool sentinel_ok) {
 ll_proto auto_proto_rooted(uint64_t bytes, bool sentinel_ok) {
   if (bytes <= (64u << 10)) return LL_PROTO_PACKET8;
   return sentinel_ok ? LL_PROTO_SENTINEL : LL_PROTO_LINE128;
+}
+
+// Stand-alone ReduceScatter / AllGather: the wave-per-peer kernels serve
+// 8-byte packets and sentinel units up to 1 MiB of data per rank at 5-8
+// ranks and 2 MiB below (measured; forced on or off by ll_set_wave_kernels).
+bool use_wave_kernel(ll_proto proto, uint64_t bytes, int P) {
+  if (proto == LL_PROTO_LINE128) return false;
+  const int m = g_wave_kernels.load();
+  if (m != 0) return m == 2;
+  return bytes <= (P >= 5 ? (1u << 20) : (2u << 20));
 }
 
 // Algorithms whose AllGather stores into the peers' sentinel-filled outputs.
@@ -378,7 +419,7 @@ void plan_allreduce(Plan *pl, ll_algo algo, uint64_t count, int es, int nranks, 
   const uint64_t it_bytes = iter_count * (uint64_t)es;
   const bool line = (algo == LL_ALGO_TWOSHOT_LINE || algo == LL_ALGO_ONESHOT_LINE);
   const bool sent = (algo == LL_ALGO_ONESHOT_SENTINEL || algo == LL_ALGO_TWOSHOT_SENTINEL ||
-                     algo == LL_ALGO_TWOSHOT_SENTINEL_OUT);
+                     algo == LL_ALGO_TWOSHOT_SENTINEL_OUT || algo == LL_ALGO_TWOSHOT_SENTINEL_WAVES);
   const bool waves = (algo == LL_ALGO_ONESHOT_WAVES);
   pl->proto = line ? PR_LINE : (sent ? PR_SENT : PR_LL);
   pl->a.area = area_of(pl->proto);
@@ -388,6 +429,7 @@ void plan_allreduce(Plan *pl, ll_algo algo, uint64_t count, int es, int nranks, 
     pl->units = units_of(pl->proto, it_bytes);
   } else {
     pl->kind = algo == LL_ALGO_TWOSHOT_SENTINEL_OUT ? K_TWOSHOT_OUT : K_TWOSHOT;
+    if (algo == LL_ALGO_TWOSHOT_WAVES || algo == LL_ALGO_TWOSHOT_SENTINEL_WAVES) pl->kind = K_TWOSHOT_WAVES;
     const uint64_t C = L::twoshot_chunk(iter_count, nranks, es);
     pl->a.chunk = (int64_t)C;
     pl->a.slot = slot_bytes(pl->proto, C * es);
@@ -491,7 +533,7 @@ int ll_allreduce_algo(void *sym_base, size_t rank_stride, void *out, size_t coun
   if (st != LL_OK) return st;
   st = check_dtype_op((int)dt, (int)op);
   if (st != LL_OK) return st;
-  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_TWOSHOT_ATOMIC) return LL_ERR_INVALID;
+  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_TWOSHOT_SENTINEL_WAVES) return LL_ERR_INVALID;
   const int es = esize_of(dt);
   const uint64_t in_bytes = (uint64_t)count * es;
   if (fills_output(algo) && in_bytes % 16 != 0) return LL_ERR_UNSUPPORTED;
@@ -580,7 +622,7 @@ int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, 
   if (epoch == 0) return LL_ERR_INVALID;
   int st = check_dtype_op((int)dt, (int)op);
   if (st != LL_OK) return st;
-  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_TWOSHOT_ATOMIC) return LL_ERR_INVALID;
+  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_TWOSHOT_SENTINEL_WAVES) return LL_ERR_INVALID;
   if (algo == LL_ALGO_TWOSHOT_ATOMIC) return LL_ERR_UNSUPPORTED;  // single-iteration regions only
   size_t D = 0;
   st = ll_scratch_iter_bytes(scratch_stride, nranks, &D);
@@ -606,9 +648,13 @@ int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, 
     } else {
       algo = auto_algo(iter_count * es, nranks, g_auto_sentinel.load() != 0);
       if (iters > 1 && algo == LL_ALGO_ONESHOT_WAVES) algo = LL_ALGO_ONESHOT;
+      if (iters > 1 && algo == LL_ALGO_TWOSHOT_WAVES) algo = LL_ALGO_TWOSHOT;
+      if (iters > 1 && algo == LL_ALGO_TWOSHOT_SENTINEL_WAVES) algo = LL_ALGO_TWOSHOT_SENTINEL;
     }
   }
-  if (iters > 1 && algo == LL_ALGO_ONESHOT_WAVES) return LL_ERR_UNSUPPORTED;
+  if (iters > 1 && (algo == LL_ALGO_ONESHOT_WAVES || algo == LL_ALGO_TWOSHOT_WAVES ||
+                    algo == LL_ALGO_TWOSHOT_SENTINEL_WAVES))
+    return LL_ERR_UNSUPPORTED;
 
   Plan pl;
   pl.dt = (int)dt;
@@ -649,7 +695,7 @@ int ll_reduce_scatter_proto(void *sym_base, size_t rank_stride, void *out, size_
   if (recvcount == 0) return LL_OK;
   if (proto == LL_PROTO_AUTO) proto = auto_proto(in_bytes, nranks, g_auto_sentinel.load() != 0);
   Plan pl;
-  pl.kind = K_RS;
+  pl.kind = use_wave_kernel(proto, in_bytes, nranks) ? K_RS_WAVES : K_RS;
   pl.dt = (int)dt;
   pl.P = nranks;
   pl.proto = proto == LL_PROTO_LINE128 ? PR_LINE : (proto == LL_PROTO_SENTINEL ? PR_SENT : PR_LL);
@@ -685,7 +731,7 @@ int ll_allgather_proto(void *sym_base, size_t rank_stride, void *out, size_t sen
   if (sendcount == 0) return LL_OK;
   if (proto == LL_PROTO_AUTO) proto = auto_proto(in_bytes * nranks, nranks, g_auto_sentinel.load() != 0);
   Plan pl;
-  pl.kind = K_AG;
+  pl.kind = use_wave_kernel(proto, in_bytes * nranks, nranks) ? K_AG_WAVES : K_AG;
   pl.dt = (int)dt;
   pl.P = nranks;
   pl.proto = proto == LL_PROTO_LINE128 ? PR_LINE : (proto == LL_PROTO_SENTINEL ? PR_SENT : PR_LL);
@@ -823,6 +869,12 @@ int ll_set_poll_pacing(int first_wait, int poll_gap) {
 int ll_set_pipeline_lag(int lag) {
   if (lag < 1 || lag > 64) return LL_ERR_INVALID;
   g_lag.store(lag);
+  return LL_OK;
+}
+
+int ll_set_wave_kernels(int mode) {
+  if (mode < 0 || mode > 2) return LL_ERR_INVALID;
+  g_wave_kernels.store(mode);
   return LL_OK;
 }
 

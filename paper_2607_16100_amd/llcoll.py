@@ -21,6 +21,7 @@ LL_ALGO_AUTO, LL_ALGO_ONESHOT, LL_ALGO_TWOSHOT, LL_ALGO_TWOSHOT_LINE, LL_ALGO_ON
 LL_ALGO_ONESHOT_WAVES = 5
 LL_ALGO_ONESHOT_SENTINEL, LL_ALGO_TWOSHOT_SENTINEL, LL_ALGO_TWOSHOT_SENTINEL_OUT = 6, 7, 8
 LL_ALGO_TWOSHOT_ATOMIC = 9
+LL_ALGO_TWOSHOT_WAVES, LL_ALGO_TWOSHOT_SENTINEL_WAVES = 10, 11
 LL_PROTO_AUTO, LL_PROTO_PACKET8, LL_PROTO_LINE128, LL_PROTO_SENTINEL = 0, 1, 2, 3
 
 LL_OK = 0
@@ -36,6 +37,7 @@ ALGOS = {
     "oneshot_waves": LL_ALGO_ONESHOT_WAVES,
     "oneshot_sentinel": LL_ALGO_ONESHOT_SENTINEL, "twoshot_sentinel": LL_ALGO_TWOSHOT_SENTINEL,
     "twoshot_sentinel_out": LL_ALGO_TWOSHOT_SENTINEL_OUT, "twoshot_atomic": LL_ALGO_TWOSHOT_ATOMIC,
+    "twoshot_waves": LL_ALGO_TWOSHOT_WAVES, "twoshot_sentinel_waves": LL_ALGO_TWOSHOT_SENTINEL_WAVES,
 }
 PROTOS = {"auto": LL_PROTO_AUTO, "packet8": LL_PROTO_PACKET8, "line128": LL_PROTO_LINE128,
           "sentinel": LL_PROTO_SENTINEL}
@@ -57,6 +59,7 @@ _SIGS = {
     "ll_scratch_init": (_i, [_vp, _sz, _i, _vp]),
     "ll_allreduce_buffered": (_i, [_vp, _vp, _sz, _i, _i, _i, _vp, _sz, _u32, _vp, _i, ctypes.POINTER(_u32)]),
     "ll_set_auto_sentinel": (_i, [_i]),
+    "ll_set_wave_kernels": (_i, [_i]),
     "ll_allreduce": (_i, [_vp, _sz, _vp, _sz, _i, _i, _i, _u32, _vp]),
     "ll_allreduce_algo": (_i, [_vp, _sz, _vp, _sz, _i, _i, _i, _u32, _vp, _i]),
     "ll_reduce_scatter": (_i, [_vp, _sz, _vp, _sz, _i, _i, _i, _u32, _vp]),
@@ -239,6 +242,10 @@ def ll_bench_rooted(kind, sym_base, rank_stride, out, count, dt, root, nranks, f
 
 def ll_fill_sentinel(out, count, dt, nranks, stream):
     return _lib.ll_fill_sentinel(out, count, dt, nranks, stream)
+
+
+def ll_set_wave_kernels(mode: int):
+    return _lib.ll_set_wave_kernels(mode)
 
 
 def ll_set_auto_sentinel(allow: int):

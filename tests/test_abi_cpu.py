@@ -64,7 +64,7 @@ def ar(count=1024, dt=F32, p=4, base=GOOD_BASE, stride=None, out=GOOD_OUT, epoch
     (dict(epoch=0), ll.LL_ERR_INVALID),
     (dict(dt=7), ll.LL_ERR_UNSUPPORTED),
     (dict(op=1), ll.LL_ERR_UNSUPPORTED),
-    (dict(algo=10), ll.LL_ERR_INVALID),
+    (dict(algo=12), ll.LL_ERR_INVALID),
     (dict(algo=9, count=1001), ll.LL_ERR_UNSUPPORTED),  # atomic two-shot: count*esize % 16 == 0
     (dict(algo=8, count=1001), ll.LL_ERR_UNSUPPORTED),  # direct output needs count*esize % 16 == 0
     (dict(algo=-1), ll.LL_ERR_INVALID),
@@ -104,6 +104,8 @@ def test_fill_sentinel_and_auto_sentinel_argument_checks():
     assert ll.ll_fill_sentinel(GOOD_OUT, 16, F32, 9, 0) == ll.LL_ERR_INVALID
     assert ll.ll_fill_sentinel(GOOD_OUT, 16, 4, 4, 0) == ll.LL_ERR_UNSUPPORTED
     assert ll.ll_fill_sentinel(GOOD_OUT, 0, BF16, 4, 0) == ll.LL_OK
+    assert ll.ll_set_wave_kernels(3) == ll.LL_ERR_INVALID
+    assert ll.ll_set_wave_kernels(0) == ll.LL_OK
     assert ll.ll_set_auto_sentinel(2) == ll.LL_ERR_INVALID
     assert ll.ll_set_auto_sentinel(1) == ll.LL_OK
     assert ll.ll_set_auto_sentinel(0) == ll.LL_OK
@@ -137,7 +139,8 @@ def test_buffered_argument_checks():
     assert b(epoch=0)[0] == ll.LL_ERR_INVALID
     assert b(p=1)[0] == ll.LL_ERR_INVALID
     assert b(op=1)[0] == ll.LL_ERR_UNSUPPORTED
-    assert b(algo=10)[0] == ll.LL_ERR_INVALID
+    assert b(algo=12)[0] == ll.LL_ERR_INVALID
+    assert b(algo=ll.LL_ALGO_TWOSHOT_WAVES, count=1 << 20)[0] == ll.LL_ERR_UNSUPPORTED  # one iteration only
     assert b(algo=ll.LL_ALGO_TWOSHOT_ATOMIC)[0] == ll.LL_ERR_UNSUPPORTED
     assert b(s=256)[0] == ll.LL_ERR_SCRATCH
     assert b(out=IN + 16)[0] == ll.LL_ERR_INVALID            # partial overlap of in and out

@@ -26,7 +26,7 @@ else:  # pragma: no cover
     pytest.skip("no GPU", allow_module_level=True)
 
 AR_ALGOS = ["oneshot", "twoshot", "twoshot_line", "oneshot_line", "oneshot_waves", "oneshot_sentinel",
-            "twoshot_sentinel", "auto"]
+            "twoshot_sentinel", "twoshot_waves", "twoshot_sentinel_waves", "auto"]
 PROTOS = ["packet8", "line128", "sentinel"]
 NP = {"f32": np.uint32, "bf16": np.uint16}
 
@@ -67,10 +67,12 @@ TEST_TIMEOUT_TICKS = 20_000_000  # 200 ms per flag wait: thousands of times a co
 @pytest.fixture(autouse=True)
 def _reset_settings():
     ll.ll_set_wave_units(0)
+    ll.ll_set_wave_kernels(0)
     ll.ll_set_launch(0, 0)
     ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
     ll.ll_debug_mute_rank(-1)
     yield
+    ll.ll_set_wave_kernels(0)
     ll.ll_set_launch(0, 0)
     ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
     ll.ll_debug_mute_rank(-1)
@@ -212,36 +214,44 @@ def test_c5_reduce_scatter_and_allgather(p, b, kind):
     want_rs = oracle.reduce_scatter(x)
     reg = SymRegion(p, total, "bf16", out_elems=p * total)
     reg.init()
-    for proto in PROTOS:
-        say(f"C5 RS {kind} P={p} b={b} {proto}")
+    for proto, wk in [(pr, w) for pr in PROTOS for w in (1, 2)] + [("auto", 0)]:
+        ll.ll_set_wave_kernels(wk)
+        say(f"C5 RS {kind} P={p} b={b} {proto} kernels={wk}")
         reg.write_inputs(x)
         check_ok(reg.reduce_scatter(m, proto), "reduce_scatter")
         got_rs = reg.read_out(p * m, np.uint16).reshape(p, m)
-        assert_bits_equal(got_rs, want_rs, f"RS {proto}")
-        say(f"C5 AG {kind} P={p} b={b} {proto}")
+        assert_bits_equal(got_rs, want_rs, f"RS {proto} kernels={wk}")
+        say(f"C5 AG {kind} P={p} b={b} {proto} kernels={wk}")
         reg.write_inputs(got_rs)
         check_ok(reg.allgather(m, proto), "allgather")
         got_ag = reg.read_out(p * p * m, np.uint16).reshape(p, p * m)
-        assert_bits_equal(got_ag, oracle.allgather(got_rs), f"AG {proto}")
-        assert_bits_equal(got_ag, oracle.allreduce(x), f"AG(RS) == AR {proto}")
+        assert_bits_equal(got_ag, oracle.allgather(got_rs), f"AG {proto} kernels={wk}")
+        assert_bits_equal(got_ag, oracle.allreduce(x), f"AG(RS) == AR {proto} kernels={wk}")
+    ll.ll_set_wave_kernels(0)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("proto", PROTOS)
 @pytest.mark.parametrize("p,m", [(2, 1), (3, 7), (4, 33), (8, 5), (8, 61), (5, 250)])
 def test_rs_ag_ragged(dtype, proto, p, m):
-    """Chunks whose byte offsets are not 4-byte aligned (odd bfloat16 counts)."""
+    """Chunks whose byte offsets are not 4-byte aligned (odd bfloat16 counts),
+    with both kernel families."""
     x = wl.uniform(p, p * m, dtype, seed=7)
     reg = SymRegion(p, p * m, dtype, out_elems=p * p * m)
     reg.init()
-    reg.write_inputs(x)
-    check_ok(reg.reduce_scatter(m, proto), "rs")
-    rs = reg.read_out(p * m, NP[dtype]).reshape(p, m)
-    assert_bits_equal(rs, oracle.reduce_scatter(x), f"RS ragged {proto}")
-    reg.write_inputs(x[:, :m].copy())
-    check_ok(reg.allgather(m, proto), "ag")
-    ag = reg.read_out(p * p * m, NP[dtype]).reshape(p, p * m)
-    assert_bits_equal(ag, oracle.allgather(x[:, :m].copy()), f"AG ragged {proto}")
+    try:
+        for wk in (1, 2):
+            ll.ll_set_wave_kernels(wk)
+            reg.write_inputs(x)
+            check_ok(reg.reduce_scatter(m, proto), "rs")
+            rs = reg.read_out(p * m, NP[dtype]).reshape(p, m)
+            assert_bits_equal(rs, oracle.reduce_scatter(x), f"RS ragged {proto} kernels={wk}")
+            reg.write_inputs(x[:, :m].copy())
+            check_ok(reg.allgather(m, proto), "ag")
+            ag = reg.read_out(p * p * m, NP[dtype]).reshape(p, p * m)
+            assert_bits_equal(ag, oracle.allgather(x[:, :m].copy()), f"AG ragged {proto} kernels={wk}")
+    finally:
+        ll.ll_set_wave_kernels(0)
 
 
 # ------------------------------------------------------------ invariants
@@ -257,7 +267,7 @@ def test_result_independent_of_launch_shape(algo):
         if algo == "twoshot_sentinel":  # the direct-output variant shares the launch shapes
             say(f"launch twoshot_sentinel_out wg={wg} threads={threads}")
             assert_bits_equal(run_allreduce(reg, x, "twoshot_sentinel_out"), want, f"direct wg={wg} t={threads}")
-        for units in ([1, 2, 4, 0] if algo == "oneshot_waves" else [0]):
+        for units in ([1, 2, 4, 0] if algo.endswith("_waves") else [0]):
             ll.ll_set_wave_units(units)
             say(f"launch {algo} wg={wg} threads={threads} units={units}")
             assert_bits_equal(run_allreduce(reg, x, algo), want, f"{algo} wg={wg} t={threads} u={units}")
@@ -304,7 +314,8 @@ def test_large_epochs_and_reinit():
     reg = SymRegion(p, n, "f32")
     reg.init()
     reg.write_inputs(x)
-    epochs = (0x7FFFFFFF, 0x80000000, 0xFFFFFFF8, 0xFFFFFFF9, 0xFFFFFFFA, 0xFFFFFFFC, 0xFFFFFFFE, 0xFFFFFFFF)
+    epochs = (0x7FFFFFFF, 0x80000000, 0xFFFFFFF4, 0xFFFFFFF6, 0xFFFFFFF8, 0xFFFFFFF9, 0xFFFFFFFA, 0xFFFFFFFC,
+              0xFFFFFFFE, 0xFFFFFFFF)
     assert len(epochs) == len(AR_ALGOS)
     for algo, e in zip(AR_ALGOS, epochs):
         check_ok(reg.allreduce(n, algo, epoch=e), f"epoch {e:#x}")
@@ -324,7 +335,8 @@ def test_count_zero_is_a_no_op():
 
 
 # ------------------------------------------------------------ failure handling
-@pytest.mark.parametrize("algo", ["oneshot", "twoshot_line", "oneshot_sentinel", "twoshot_sentinel"])
+@pytest.mark.parametrize("algo", ["oneshot", "twoshot_line", "oneshot_sentinel", "twoshot_sentinel", "twoshot_waves",
+                                  "twoshot_sentinel_waves"])
 def test_missing_peer_times_out_and_is_reported(algo):
     """Rank 3 publishes nothing; its peers' bounded waits expire (after 2 ms),
     every kernel still finishes, and ll_check reports the timeout.  (In two-shot
@@ -371,7 +383,7 @@ def test_next_epoch_sees_new_inputs():
 SENT = 0xFFFFFFFF
 
 
-@pytest.mark.parametrize("algo", ["oneshot_sentinel", "twoshot_sentinel"])
+@pytest.mark.parametrize("algo", ["oneshot_sentinel", "twoshot_sentinel", "twoshot_sentinel_waves"])
 def test_sentinel_slots_are_restored_after_every_call(algo):
     """Sentinel mode resets every slot it has read (Sec. IV, Sentinel): after
     a call the sentinel area holds only the sentinel again, and the flagged
@@ -640,3 +652,44 @@ def test_rooted_missing_rank_times_out(kind):
     reg.init()
     check_ok(reg.reduce(n, 2, "packet8"), "after timeout")
     assert_bits_equal(reg.read_out(n, np.uint32).reshape(1, n), oracle.reduce(x, 2).reshape(1, n), "after timeout")
+
+
+@pytest.mark.parametrize("proto", ["packet8", "sentinel"])
+def test_rs_ag_wave_kernels_launch_shapes_and_timeouts(proto):
+    """The wave-per-peer ReduceScatter / AllGather at several workgroup counts
+    and units per lane, then a muted rank that makes the waits expire."""
+    p, m = 8, 40_000
+    x = wl.normal(p, p * m, "bf16", seed=17)
+    reg = SymRegion(p, p * m, "bf16", out_elems=p * p * m)
+    reg.init()
+    ll.ll_set_wave_kernels(2)
+    for wg in (1, 3, 0):
+        for units in (1, 2, 4, 0):
+            ll.ll_set_launch(wg, 0)
+            ll.ll_set_wave_units(units)
+            say(f"RS/AG waves {proto} wg={wg} units={units}")
+            reg.write_inputs(x)
+            check_ok(reg.reduce_scatter(m, proto), "rs")
+            rs = reg.read_out(p * m, np.uint16).reshape(p, m)
+            assert_bits_equal(rs, oracle.reduce_scatter(x), f"RS waves wg={wg} u={units}")
+            reg.write_inputs(rs)
+            check_ok(reg.allgather(m, proto), "ag")
+            assert_bits_equal(reg.read_out(p * p * m, np.uint16).reshape(p, p * m), oracle.allgather(rs),
+                              f"AG waves wg={wg} u={units}")
+    ll.ll_set_launch(0, 0)
+    ll.ll_set_wave_units(0)
+    ll.ll_set_poll_timeout(200_000)
+    ll.ll_debug_mute_rank(4)
+    reg.write_inputs(x)
+    assert reg.reduce_scatter(m, proto) == ll.LL_OK
+    assert ll.ll_check(stream()) == ll.LL_ERR_TIMEOUT
+    assert reg.allgather(m, proto) == ll.LL_OK
+    assert ll.ll_check(stream()) == ll.LL_ERR_TIMEOUT
+    ll.ll_debug_mute_rank(-1)
+    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
+    reg.init()
+    reg.write_inputs(x)
+    check_ok(reg.reduce_scatter(m, proto), "rs after timeout")
+    assert_bits_equal(reg.read_out(p * m, np.uint16).reshape(p, m), oracle.reduce_scatter(x), "RS after timeout")
+    if proto == "sentinel":
+        assert (reg.read_area(4) == SENT).all()
