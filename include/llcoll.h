@@ -90,7 +90,9 @@ typedef enum {
                                        Atomic"): NOT deterministic, see below */
   LL_ALGO_TWOSHOT_WAVES = 10,       /* two-shot, 8-byte packets, one wave per peer, partial
                                        sums staged in LDS (single iteration only) */
-  LL_ALGO_TWOSHOT_SENTINEL_WAVES = 11 /* the same with sentinel units */
+  LL_ALGO_TWOSHOT_SENTINEL_WAVES = 11, /* the same with sentinel units */
+  LL_ALGO_ONESHOT_SENTINEL_WAVES = 12  /* one-shot, sentinel units, one wave per peer (single
+                                          iteration only) */
 } ll_algo;
 
 /* LL_ALGO_TWOSHOT_ATOMIC, the analogue of the paper's two-shot LL128 atomic

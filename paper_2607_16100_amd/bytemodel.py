@@ -32,7 +32,8 @@ def comm_volume_per_rank(algo: str, p: int, m: float, proto: str) -> float:
 def _proto(algo: str) -> tuple[str, str]:
     base = {"oneshot": "oneshot", "oneshot_line": "oneshot", "oneshot_waves": "oneshot",
             "oneshot_sentinel": "oneshot", "twoshot": "twoshot", "twoshot_line": "twoshot",
-            "twoshot_sentinel": "twoshot", "twoshot_waves": "twoshot", "twoshot_sentinel_waves": "twoshot"}[algo]
+            "twoshot_sentinel": "twoshot", "twoshot_waves": "twoshot", "twoshot_sentinel_waves": "twoshot",
+            "oneshot_sentinel_waves": "oneshot"}[algo]
     proto = "line128" if algo.endswith("_line") else ("sentinel" if "_sentinel" in algo else "packet8")
     return base, proto
 

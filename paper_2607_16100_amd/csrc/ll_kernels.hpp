@@ -241,19 +241,19 @@ __global__ __launch_bounds__(1024) void k_oneshot(KArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// One-shot AllReduce, one wave per peer, with LDS staging (8-byte packets).
+// One-shot AllReduce, one wave per peer, with LDS staging (8-byte packets or
+// sentinel units).
 //
-// A workgroup has P waves and handles tiles of 64*U packet units (each unit
-// = 2 payload words; lane l owns units l, l+64, ..., l+64(U-1) of the tile,
-// so every memory instruction of a wave covers 1 KiB of packets).  For a
-// tile, wave q != r sends the rank's packets to peer q only and then polls
-// only the packets peer q sent to this rank; wave r keeps the rank's own
-// values.  Each wave stages its rank's values, widened to binary32, in LDS
-// row q; after a workgroup barrier the rows are summed in ascending rank
-// order and rounded once.  Compared with one lane talking to all P-1 peers, a
-// wave's poll never waits for more than its own U stores (the memory counter
-// covers stores and loads alike on this chip) and a poll is U loads, not
-// U*(P-1).
+// A workgroup has P waves and handles tiles of 64*U packet units (lane l owns
+// units l, l+64, ..., l+64(U-1) of the tile, so every memory instruction of a
+// wave covers 64 units).  For a tile, wave q != r sends the rank's units to
+// peer q only and then polls only the units peer q sent to this rank; wave r
+// keeps the rank's own values.  Each wave stages its rank's values, widened
+// to binary32, in LDS row q; after a workgroup barrier the rows are summed in
+// ascending rank order and rounded once.  Compared with one lane talking to
+// all P-1 peers, a wave's poll never waits for more than its own U stores
+// (the memory counter covers stores and loads alike on this chip) and a poll
+// is U loads, not U*(P-1).
 // Workgroup barrier that makes LDS writes visible but does not wait for the
 // wave's outstanding global stores (packet stores need not be acknowledged
 // before the workgroup goes on).
@@ -262,19 +262,14 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_s_barrier();
 }
 
-// 0: every peer wave sends its own store and then polls (measured faster on
-// MI355X); 1: the own-rank wave sends to all peers and the peer waves only poll.
-#ifndef LLCOLL_WAVES_SPLIT
-#define LLCOLL_WAVES_SPLIT 0
-#endif
-
-template <int DT, int P, int U>
+template <class Pr, int DT, int P, int U>
 __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs a) {
   stamp_start(a);
   constexpr int E = Elem<DT>::kBytes;
   constexpr int K = Elem<DT>::kPerWord;
-  constexpr int EPU = 2 * K;   // elements per 8-byte-packet unit
-  constexpr int TW = 128 * U;  // payload words per tile
+  constexpr int WPU = Pr::kUnitWords;  // payload words per unit
+  constexpr int EPU = WPU * K;         // elements per unit
+  constexpr int TW = 64 * U * WPU;     // payload words per tile
   __shared__ float stage[P][TW * K];
   const Part pt = part_of_block<P>();
   const int r = pt.r;
@@ -285,7 +280,7 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs a) {
   const char *const in_r = a.in + (uint64_t)r * a.in_stride;
   const int64_t n = a.n;
   const int64_t words = (n * E + 3) / 4;
-  const int64_t units = ProtoLL::units(words);
+  const int64_t units = Pr::units(words);
   const int64_t tiles = (units + 64 * U - 1) / (64 * U);
   char *const out_r = a.out + (uint64_t)r * (uint64_t)n * E;
   const bool publish = (r != a.mute);
@@ -297,11 +292,14 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs a) {
   auto stage_row = [&](const u32x4 *w) {
 #pragma unroll
     for (int k = 0; k < U; ++k) {
-      float f[EPU];
-      Elem<DT>::widen(w[k].x, f);
-      Elem<DT>::widen(w[k].y, f + K);
+      const uint32_t wv4[4] = {w[k].x, w[k].y, w[k].z, w[k].w};
 #pragma unroll
-      for (int e = 0; e < EPU; ++e) stage[q][(k * 64 + lane) * EPU + e] = f[e];
+      for (int j = 0; j < WPU; ++j) {
+        float f[K];
+        Elem<DT>::widen(wv4[j], f);
+#pragma unroll
+        for (int e = 0; e < K; ++e) stage[q][(k * 64 + lane) * EPU + j * K + e] = f[e];
+      }
     }
   };
 
@@ -310,23 +308,13 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs a) {
 #pragma unroll
     for (int k = 0; k < U; ++k) {
       const int64_t u = tile * 64 * U + k * 64 + lane;
-      own[k] = u < units ? load_words<DT>(in_r, 2 * u, 2, n, a.in_al4 != 0) : u32x4{0u, 0u, 0u, 0u};
+      own[k] = u < units ? Pr::template load<DT>(in_r, u, 0, n, a.in_al4 != 0) : u32x4{0u, 0u, 0u, 0u};
     }
     if (a.phases != nullptr && lane == 0 && tile == pt.w) {
       a.phases[4 * (blockIdx.x * P + wv) + 0] = now_ticks() + (own[0].x & 0u);
     }
     if (q == r) {
-      // the own values; with LLCOLL_WAVES_SPLIT this wave also sends the tile
-      // to every peer, so the polling waves have no stores of their own to
-      // wait for (the memory counter covers stores and loads alike)
       stage_row(own);
-      if (LLCOLL_WAVES_SPLIT && publish) {
-#pragma unroll
-        for (int k = 0; k < U; ++k) {
-          const int64_t u = tile * 64 * U + k * 64 + lane;
-          if (u < units) bcast<P>(a, a.area, r, (uint32_t)(u * ProtoLL::kUnitBytes), ProtoLL::pack(own[k], a.epoch, 0));
-        }
-      }
       if (a.phases != nullptr && lane == 0 && tile == pt.w) a.phases[4 * (blockIdx.x * P + wv) + 1] = now_ticks();
     } else {
       u32x4 v[U];
@@ -339,9 +327,10 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs a) {
         v[k] = u32x4{0u, 0u, 0u, 0u};
         if (u < units) {
           pend |= 1u << k;
-          if (!LLCOLL_WAVES_SPLIT && publish) st_pkt(rd, (uint32_t)(u * ProtoLL::kUnitBytes), ProtoLL::pack(own[k], a.epoch, 0));
+          if (publish) st_pkt(rd, (uint32_t)(u * Pr::kUnitBytes), Pr::pack(own[k], a.epoch, 0));
         }
       }
+      const uint32_t want = pend;
       int spins = 1;
       idle64(a.first_wait);
       while (pend != 0) {
@@ -350,18 +339,26 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs a) {
 #pragma unroll
         for (int k = 0; k < U; ++k) {
           const int64_t u = tile * 64 * U + k * 64 + lane;
-          if (pend & (1u << k)) pk[k] = ld_pkt(rs, (uint32_t)(u * ProtoLL::kUnitBytes));
+          if (pend & (1u << k)) pk[k] = ld_pkt(rs, (uint32_t)(u * Pr::kUnitBytes));
         }
 #pragma unroll
         for (int k = 0; k < U; ++k) {
-          if ((pend & (1u << k)) && ProtoLL::ready(pk[k], a.epoch)) {
-            v[k] = ProtoLL::unpack(pk[k], 0);
+          if ((pend & (1u << k)) && Pr::ready(pk[k], a.epoch)) {
+            v[k] = Pr::unpack(pk[k], 0);
             pend &= ~(1u << k);
           }
         }
         if (pend != 0 && (spins++ & 15) == 0 && now_ticks() > deadline) {
           report_timeout(r, 1u << q, a.epoch);
           break;
+        }
+      }
+      if (ResetsSlots<Pr>::value) {
+        const u32x4 sent = {ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel};
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+          const int64_t u = tile * 64 * U + k * 64 + lane;
+          if (want & (1u << k)) st_pkt(rs, (uint32_t)(u * Pr::kUnitBytes), sent);
         }
       }
       if (a.phases != nullptr && lane == 0 && tile == pt.w) {

@@ -92,7 +92,7 @@ void fill_row(kernel_fn *row) {
 // table[proto][dtype][P][kind]
 struct Table {
   kernel_fn k[PR_COUNT][2][LL_MAX_RANKS + 1][K_KINDS];
-  kernel_fn waves[3][2][LL_MAX_RANKS + 1];  // [log2 U][dtype][P]
+  kernel_fn waves[3][2][2][LL_MAX_RANKS + 1];  // [log2 U][8-byte packets, sentinel][dtype][P]
   kernel_fn twaves[3][3][2][2][LL_MAX_RANKS + 1];  // [AR, RS, AG][log2 U][8-byte packets, sentinel][dtype][P]
   Table() {
     memset(k, 0, sizeof k);
@@ -129,12 +129,18 @@ struct Table {
     fill_row<ProtoLine, 1, P>(k[PR_LINE][1][P]);
     fill_row<ProtoSent, 0, P>(k[PR_SENT][0][P]);
     fill_row<ProtoSent, 1, P>(k[PR_SENT][1][P]);
-    waves[0][0][P] = k_oneshot_waves<0, P, 1>;
-    waves[0][1][P] = k_oneshot_waves<1, P, 1>;
-    waves[1][0][P] = k_oneshot_waves<0, P, 2>;
-    waves[1][1][P] = k_oneshot_waves<1, P, 2>;
-    waves[2][0][P] = k_oneshot_waves<0, P, 4>;
-    waves[2][1][P] = k_oneshot_waves<1, P, 4>;
+    waves[0][0][0][P] = k_oneshot_waves<ProtoLL, 0, P, 1>;
+    waves[0][0][1][P] = k_oneshot_waves<ProtoLL, 1, P, 1>;
+    waves[1][0][0][P] = k_oneshot_waves<ProtoLL, 0, P, 2>;
+    waves[1][0][1][P] = k_oneshot_waves<ProtoLL, 1, P, 2>;
+    waves[2][0][0][P] = k_oneshot_waves<ProtoLL, 0, P, 4>;
+    waves[2][0][1][P] = k_oneshot_waves<ProtoLL, 1, P, 4>;
+    waves[0][1][0][P] = k_oneshot_waves<ProtoSent, 0, P, 1>;
+    waves[0][1][1][P] = k_oneshot_waves<ProtoSent, 1, P, 1>;
+    waves[1][1][0][P] = k_oneshot_waves<ProtoSent, 0, P, 2>;
+    waves[1][1][1][P] = k_oneshot_waves<ProtoSent, 1, P, 2>;
+    waves[2][1][0][P] = k_oneshot_waves<ProtoSent, 0, P, 4>;
+    waves[2][1][1][P] = k_oneshot_waves<ProtoSent, 1, P, 4>;
     fill_twaves<0, P>();
     fill_twaves<1, P>();
     fill_twaves<2, P>();
@@ -239,7 +245,8 @@ int launch(const Plan &pl, void *stream) {
   const int wlog = wave_kernel ? wave_units_log2(pl.units) : 0;
   kernel_fn fn = nullptr;
   if (pl.kind == K_ONESHOT_WAVES) {
-    fn = table().waves[wlog][pl.dt][pl.P];
+    if (pl.proto == PR_LINE) return LL_ERR_UNSUPPORTED;
+    fn = table().waves[wlog][pl.proto == PR_SENT ? 1 : 0][pl.dt][pl.P];
   } else if (two_waves) {
     if (pl.proto == PR_LINE) return LL_ERR_UNSUPPORTED;
     const int mode = pl.kind == K_TWOSHOT_WAVES ? 0 : (pl.kind == K_RS_WAVES ? 1 : 2);
@@ -355,6 +362,7 @@ ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
   if (P <= 2) {
     if (in_bytes <= 32 * KiB) return LL_ALGO_ONESHOT_WAVES;
     if (sentinel_ok) {
+      if (in_bytes <= 512 * KiB) return LL_ALGO_ONESHOT_SENTINEL_WAVES;
       if (in_bytes <= 2 * MiB) return LL_ALGO_ONESHOT_SENTINEL;
       if (in_bytes <= 16 * MiB) return LL_ALGO_TWOSHOT_SENTINEL_WAVES;
       return LL_ALGO_TWOSHOT_LINE;
@@ -363,13 +371,13 @@ ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
     if (in_bytes <= 4 * MiB) return LL_ALGO_ONESHOT_LINE;
     return LL_ALGO_TWOSHOT_LINE;
   }
-  if (in_bytes <= (P <= 4 ? 64 : 16) * KiB) return LL_ALGO_ONESHOT_WAVES;
   if (sentinel_ok) {
-    if (in_bytes <= 128 * KiB) return LL_ALGO_TWOSHOT_WAVES;
-    if (P <= 4 && in_bytes <= 256 * KiB) return LL_ALGO_ONESHOT_SENTINEL;
+    if (in_bytes <= (P <= 4 ? 32 : 8) * KiB) return LL_ALGO_ONESHOT_WAVES;
+    if (in_bytes <= (P <= 4 ? 128 : 64) * KiB) return LL_ALGO_ONESHOT_SENTINEL_WAVES;
     if (in_bytes <= 4 * MiB) return LL_ALGO_TWOSHOT_SENTINEL_WAVES;
     return LL_ALGO_TWOSHOT_LINE;
   }
+  if (in_bytes <= (P <= 4 ? 64 : 16) * KiB) return LL_ALGO_ONESHOT_WAVES;
   if (in_bytes <= 1 * MiB) return LL_ALGO_TWOSHOT_WAVES;
   return LL_ALGO_TWOSHOT_LINE;
 }
@@ -419,8 +427,9 @@ void plan_allreduce(Plan *pl, ll_algo algo, uint64_t count, int es, int nranks, 
   const uint64_t it_bytes = iter_count * (uint64_t)es;
   const bool line = (algo == LL_ALGO_TWOSHOT_LINE || algo == LL_ALGO_ONESHOT_LINE);
   const bool sent = (algo == LL_ALGO_ONESHOT_SENTINEL || algo == LL_ALGO_TWOSHOT_SENTINEL ||
-                     algo == LL_ALGO_TWOSHOT_SENTINEL_OUT || algo == LL_ALGO_TWOSHOT_SENTINEL_WAVES);
-  const bool waves = (algo == LL_ALGO_ONESHOT_WAVES);
+                     algo == LL_ALGO_TWOSHOT_SENTINEL_OUT || algo == LL_ALGO_TWOSHOT_SENTINEL_WAVES ||
+                     algo == LL_ALGO_ONESHOT_SENTINEL_WAVES);
+  const bool waves = (algo == LL_ALGO_ONESHOT_WAVES || algo == LL_ALGO_ONESHOT_SENTINEL_WAVES);
   pl->proto = line ? PR_LINE : (sent ? PR_SENT : PR_LL);
   pl->a.area = area_of(pl->proto);
   if (algo == LL_ALGO_ONESHOT || algo == LL_ALGO_ONESHOT_LINE || algo == LL_ALGO_ONESHOT_SENTINEL || waves) {
@@ -533,7 +542,7 @@ int ll_allreduce_algo(void *sym_base, size_t rank_stride, void *out, size_t coun
   if (st != LL_OK) return st;
   st = check_dtype_op((int)dt, (int)op);
   if (st != LL_OK) return st;
-  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_TWOSHOT_SENTINEL_WAVES) return LL_ERR_INVALID;
+  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_ONESHOT_SENTINEL_WAVES) return LL_ERR_INVALID;
   const int es = esize_of(dt);
   const uint64_t in_bytes = (uint64_t)count * es;
   if (fills_output(algo) && in_bytes % 16 != 0) return LL_ERR_UNSUPPORTED;
@@ -622,7 +631,7 @@ int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, 
   if (epoch == 0) return LL_ERR_INVALID;
   int st = check_dtype_op((int)dt, (int)op);
   if (st != LL_OK) return st;
-  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_TWOSHOT_SENTINEL_WAVES) return LL_ERR_INVALID;
+  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_ONESHOT_SENTINEL_WAVES) return LL_ERR_INVALID;
   if (algo == LL_ALGO_TWOSHOT_ATOMIC) return LL_ERR_UNSUPPORTED;  // single-iteration regions only
   size_t D = 0;
   st = ll_scratch_iter_bytes(scratch_stride, nranks, &D);
@@ -650,10 +659,11 @@ int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, 
       if (iters > 1 && algo == LL_ALGO_ONESHOT_WAVES) algo = LL_ALGO_ONESHOT;
       if (iters > 1 && algo == LL_ALGO_TWOSHOT_WAVES) algo = LL_ALGO_TWOSHOT;
       if (iters > 1 && algo == LL_ALGO_TWOSHOT_SENTINEL_WAVES) algo = LL_ALGO_TWOSHOT_SENTINEL;
+      if (iters > 1 && algo == LL_ALGO_ONESHOT_SENTINEL_WAVES) algo = LL_ALGO_ONESHOT_SENTINEL;
     }
   }
   if (iters > 1 && (algo == LL_ALGO_ONESHOT_WAVES || algo == LL_ALGO_TWOSHOT_WAVES ||
-                    algo == LL_ALGO_TWOSHOT_SENTINEL_WAVES))
+                    algo == LL_ALGO_TWOSHOT_SENTINEL_WAVES || algo == LL_ALGO_ONESHOT_SENTINEL_WAVES))
     return LL_ERR_UNSUPPORTED;
 
   Plan pl;

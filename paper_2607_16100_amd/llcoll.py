@@ -21,7 +21,7 @@ LL_ALGO_AUTO, LL_ALGO_ONESHOT, LL_ALGO_TWOSHOT, LL_ALGO_TWOSHOT_LINE, LL_ALGO_ON
 LL_ALGO_ONESHOT_WAVES = 5
 LL_ALGO_ONESHOT_SENTINEL, LL_ALGO_TWOSHOT_SENTINEL, LL_ALGO_TWOSHOT_SENTINEL_OUT = 6, 7, 8
 LL_ALGO_TWOSHOT_ATOMIC = 9
-LL_ALGO_TWOSHOT_WAVES, LL_ALGO_TWOSHOT_SENTINEL_WAVES = 10, 11
+LL_ALGO_TWOSHOT_WAVES, LL_ALGO_TWOSHOT_SENTINEL_WAVES, LL_ALGO_ONESHOT_SENTINEL_WAVES = 10, 11, 12
 LL_PROTO_AUTO, LL_PROTO_PACKET8, LL_PROTO_LINE128, LL_PROTO_SENTINEL = 0, 1, 2, 3
 
 LL_OK = 0
@@ -38,6 +38,7 @@ ALGOS = {
     "oneshot_sentinel": LL_ALGO_ONESHOT_SENTINEL, "twoshot_sentinel": LL_ALGO_TWOSHOT_SENTINEL,
     "twoshot_sentinel_out": LL_ALGO_TWOSHOT_SENTINEL_OUT, "twoshot_atomic": LL_ALGO_TWOSHOT_ATOMIC,
     "twoshot_waves": LL_ALGO_TWOSHOT_WAVES, "twoshot_sentinel_waves": LL_ALGO_TWOSHOT_SENTINEL_WAVES,
+    "oneshot_sentinel_waves": LL_ALGO_ONESHOT_SENTINEL_WAVES,
 }
 PROTOS = {"auto": LL_PROTO_AUTO, "packet8": LL_PROTO_PACKET8, "line128": LL_PROTO_LINE128,
           "sentinel": LL_PROTO_SENTINEL}

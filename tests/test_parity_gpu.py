@@ -26,7 +26,7 @@ else:  # pragma: no cover
     pytest.skip("no GPU", allow_module_level=True)
 
 AR_ALGOS = ["oneshot", "twoshot", "twoshot_line", "oneshot_line", "oneshot_waves", "oneshot_sentinel",
-            "twoshot_sentinel", "twoshot_waves", "twoshot_sentinel_waves", "auto"]
+            "twoshot_sentinel", "twoshot_waves", "twoshot_sentinel_waves", "oneshot_sentinel_waves", "auto"]
 PROTOS = ["packet8", "line128", "sentinel"]
 NP = {"f32": np.uint32, "bf16": np.uint16}
 
@@ -314,8 +314,8 @@ def test_large_epochs_and_reinit():
     reg = SymRegion(p, n, "f32")
     reg.init()
     reg.write_inputs(x)
-    epochs = (0x7FFFFFFF, 0x80000000, 0xFFFFFFF4, 0xFFFFFFF6, 0xFFFFFFF8, 0xFFFFFFF9, 0xFFFFFFFA, 0xFFFFFFFC,
-              0xFFFFFFFE, 0xFFFFFFFF)
+    epochs = (0x7FFFFFFF, 0x80000000, 0xFFFFFFF2, 0xFFFFFFF4, 0xFFFFFFF6, 0xFFFFFFF8, 0xFFFFFFF9, 0xFFFFFFFA,
+              0xFFFFFFFC, 0xFFFFFFFE, 0xFFFFFFFF)
     assert len(epochs) == len(AR_ALGOS)
     for algo, e in zip(AR_ALGOS, epochs):
         check_ok(reg.allreduce(n, algo, epoch=e), f"epoch {e:#x}")
@@ -336,7 +336,7 @@ def test_count_zero_is_a_no_op():
 
 # ------------------------------------------------------------ failure handling
 @pytest.mark.parametrize("algo", ["oneshot", "twoshot_line", "oneshot_sentinel", "twoshot_sentinel", "twoshot_waves",
-                                  "twoshot_sentinel_waves"])
+                                  "twoshot_sentinel_waves", "oneshot_waves", "oneshot_sentinel_waves"])
 def test_missing_peer_times_out_and_is_reported(algo):
     """Rank 3 publishes nothing; its peers' bounded waits expire (after 2 ms),
     every kernel still finishes, and ll_check reports the timeout.  (In two-shot
@@ -383,7 +383,8 @@ def test_next_epoch_sees_new_inputs():
 SENT = 0xFFFFFFFF
 
 
-@pytest.mark.parametrize("algo", ["oneshot_sentinel", "twoshot_sentinel", "twoshot_sentinel_waves"])
+@pytest.mark.parametrize("algo", ["oneshot_sentinel", "twoshot_sentinel", "twoshot_sentinel_waves",
+                                  "oneshot_sentinel_waves"])
 def test_sentinel_slots_are_restored_after_every_call(algo):
     """Sentinel mode resets every slot it has read (Sec. IV, Sentinel): after
     a call the sentinel area holds only the sentinel again, and the flagged
