@@ -51,7 +51,49 @@ struct KArgs {
   uint64_t sub_bytes;
   uint32_t iters;
   int32_t root;         // Broadcast / Reduce root rank
+  uint32_t grid;        // workgroups in the launch (gridDim.x, without its memory load)
+  uint32_t block;       // threads per workgroup (blockDim.x, likewise)
 };
+
+// Kernel arguments live in memory and reach a wave through scalar loads.  Left
+// alone, the compiler loads the fields used inside a loop only after the loop
+// test, a second round trip on the way to the first packet.  pin_args loads
+// every field up front, in one batch.
+template <class T>
+__device__ __forceinline__ T in_sgpr(T v) {
+  asm volatile("" : "+s"(v));
+  return v;
+}
+
+__device__ __forceinline__ KArgs pin_args(const KArgs &k) {
+  KArgs a;
+  a.sym = in_sgpr(k.sym);
+  a.stride = in_sgpr(k.stride);
+  a.out = in_sgpr(k.out);
+  a.n = in_sgpr(k.n);
+  a.chunk = in_sgpr(k.chunk);
+  a.area = in_sgpr(k.area);
+  a.slot = in_sgpr(k.slot);
+  a.timeout = in_sgpr(k.timeout);
+  a.stamps = in_sgpr(k.stamps);
+  a.phases = in_sgpr(k.phases);
+  a.epoch = in_sgpr(k.epoch);
+  a.mute = in_sgpr(k.mute);
+  a.al4 = in_sgpr(k.al4);
+  a.first_wait = (uint16_t)in_sgpr((uint32_t)k.first_wait);
+  a.poll_gap = (uint16_t)in_sgpr((uint32_t)k.poll_gap);
+  a.lag = in_sgpr(k.lag);
+  a.in_al4 = in_sgpr(k.in_al4);
+  a.in = in_sgpr(k.in);
+  a.in_stride = in_sgpr(k.in_stride);
+  a.iter_n = in_sgpr(k.iter_n);
+  a.sub_bytes = in_sgpr(k.sub_bytes);
+  a.iters = in_sgpr(k.iters);
+  a.root = in_sgpr(k.root);
+  a.grid = in_sgpr(k.grid);
+  a.block = in_sgpr(k.block);
+  return a;
+}
 
 // Wait until every store this wave has issued is acknowledged.  Used between
 // iterations in sentinel mode: a slot reset must be complete before the
@@ -65,22 +107,26 @@ struct Part {
 };
 
 template <int P>
-__device__ __forceinline__ Part part_of_block() {
+__device__ __forceinline__ Part part_of_block(const KArgs &a) {
   Part p;
   p.r = (int)(blockIdx.x % P);
   p.w = (int)(blockIdx.x / P);
-  p.W = (int)(gridDim.x / P);
+  p.W = (int)(a.grid / P);
   return p;
 }
 
-__device__ __forceinline__ void stamp_start(const KArgs &a) {
-  if (a.stamps != nullptr && threadIdx.x == 0) a.stamps[blockIdx.x] = now_ticks();
-}
+// Per-workgroup start and end times (diagnostics).  The start time is kept in
+// a register and stored together with the end time: a store at kernel entry
+// would delay the first load, since one memory counter covers both.
+__device__ __forceinline__ uint64_t stamp_start(const KArgs &a) { return a.stamps != nullptr ? now_ticks() : 0; }
 
-__device__ __forceinline__ void stamp_end(const KArgs &a) {
+__device__ __forceinline__ void stamp_end(const KArgs &a, uint64_t t_start) {
   if (a.stamps != nullptr) {
     __syncthreads();
-    if (threadIdx.x == 0) a.stamps[gridDim.x + blockIdx.x] = now_ticks();
+    if (threadIdx.x == 0) {
+      a.stamps[blockIdx.x] = t_start;
+      a.stamps[a.grid + blockIdx.x] = now_ticks();
+    }
   }
 }
 
@@ -187,9 +233,10 @@ __device__ __forceinline__ u32x4 reduce_ordered(const u32x4 *got, u32x4 own, int
 // One-shot AllReduce (Sec. III-A; the per-thread load -> bcast -> recvReduce
 // -> store sequence of Sec. V).  Slot (d <- s) holds all of s's input.
 template <class Pr, int DT, int P>
-__global__ __launch_bounds__(1024) void k_oneshot(KArgs a) {
-  stamp_start(a);
-  const Part pt = part_of_block<P>();
+__global__ __launch_bounds__(1024) void k_oneshot(KArgs ka) {
+  const KArgs a = pin_args(ka);
+  const uint64_t t_start = stamp_start(a);
+  const Part pt = part_of_block<P>(a);
   const int r = pt.r;
   constexpr int E = Elem<DT>::kBytes;
   const uint64_t deadline = now_ticks() + a.timeout;
@@ -198,9 +245,9 @@ __global__ __launch_bounds__(1024) void k_oneshot(KArgs a) {
   char *const out_r = a.out + (uint64_t)r * (uint64_t)a.n * E;
   const bool publish = (r != a.mute);
   const bool in_al4 = a.in_al4 != 0;
-  const int64_t g = (int64_t)pt.w * blockDim.x + threadIdx.x;
+  const int64_t g = (int64_t)pt.w * a.block + threadIdx.x;
   const int sub = (int)(g % Pr::kLanes);
-  const int64_t ustep = (int64_t)pt.W * blockDim.x / Pr::kLanes;
+  const int64_t ustep = (int64_t)pt.W * a.block / Pr::kLanes;
 
   for (uint32_t it = 0; it < a.iters; ++it) {
     const int64_t e0 = (int64_t)it * a.iter_n;
@@ -237,7 +284,7 @@ __global__ __launch_bounds__(1024) void k_oneshot(KArgs a) {
     }
     if (ResetsSlots<Pr>::value && it + 1 < a.iters) wait_vm_all();
   }
-  stamp_end(a);
+  stamp_end(a, t_start);
 }
 
 // ---------------------------------------------------------------------------
@@ -263,15 +310,16 @@ __device__ __forceinline__ void lds_barrier() {
 }
 
 template <class Pr, int DT, int P, int U>
-__global__ __launch_bounds__(512) void k_oneshot_waves(KArgs a) {
-  stamp_start(a);
+__global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
+  const KArgs a = pin_args(ka);
+  const uint64_t t_start = stamp_start(a);
   constexpr int E = Elem<DT>::kBytes;
   constexpr int K = Elem<DT>::kPerWord;
   constexpr int WPU = Pr::kUnitWords;  // payload words per unit
   constexpr int EPU = WPU * K;         // elements per unit
   constexpr int TW = 64 * U * WPU;     // payload words per tile
   __shared__ float stage[P][TW * K];
-  const Part pt = part_of_block<P>();
+  const Part pt = part_of_block<P>(a);
   const int r = pt.r;
   const int wv = (int)uniform_u32(threadIdx.x >> 6);  // the same in every lane of a wave
   const int lane = (int)(threadIdx.x & 63);
@@ -352,6 +400,7 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs a) {
           report_timeout(r, 1u << q, a.epoch);
           break;
         }
+        if (pend != 0) idle64(a.poll_gap);
       }
       if (ResetsSlots<Pr>::value) {
         const u32x4 sent = {ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel};
@@ -368,7 +417,7 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs a) {
     }
     lds_barrier();
     if (a.phases != nullptr && lane == 0 && tile == pt.w) a.phases[4 * (blockIdx.x * P + wv) + 2] = now_ticks();
-    for (int j = (int)threadIdx.x; j < TW; j += (int)blockDim.x) {
+    for (int j = (int)threadIdx.x; j < TW; j += (int)a.block) {
       float acc[K];
 #pragma unroll
       for (int e = 0; e < K; ++e) acc[e] = stage[0][j * K + e];
@@ -382,7 +431,7 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs a) {
     }
     lds_barrier();  // the next tile overwrites the staging rows
   }
-  stamp_end(a);
+  stamp_end(a, t_start);
 }
 
 // ---------------------------------------------------------------------------
@@ -531,9 +580,10 @@ __device__ __forceinline__ int64_t chunk_of(int64_t n) {
 
 template <class Pr, int DT, int P, bool Direct = false>
 __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(LLCOLL_TWOSHOT_WAVES_PER_EU))) void k_twoshot(
-    KArgs a) {
-  stamp_start(a);
-  const Part pt = part_of_block<P>();
+    KArgs ka) {
+  const KArgs a = pin_args(ka);
+  const uint64_t t_start = stamp_start(a);
+  const Part pt = part_of_block<P>(a);
   TwoShot<Pr, DT, P, Direct> t{a};
   t.r = pt.r;
   constexpr int E = Elem<DT>::kBytes;
@@ -544,10 +594,10 @@ __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(LLCOLL_TWO
   t.in_al4 = a.in_al4 != 0;
   const char *const in_r = a.in + (uint64_t)t.r * a.in_stride;
   char *const out_r = a.out + (uint64_t)t.r * (uint64_t)a.n * E;
-  const int64_t g = (int64_t)pt.w * blockDim.x + threadIdx.x;
+  const int64_t g = (int64_t)pt.w * a.block + threadIdx.x;
   const int sub = (int)(g % Pr::kLanes);
   const int64_t u0 = g / Pr::kLanes;
-  const int64_t ustep = (int64_t)pt.W * blockDim.x / Pr::kLanes;
+  const int64_t ustep = (int64_t)pt.W * a.block / Pr::kLanes;
   const int64_t lag = a.lag > 0 ? a.lag : 1;
   for (uint32_t it = 0; it < a.iters; ++it) {
     const int64_t e0 = (int64_t)it * a.iter_n;
@@ -568,7 +618,7 @@ __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(LLCOLL_TWO
     }
     if (ResetsSlots<Pr>::value && it + 1 < a.iters) wait_vm_all();
   }
-  stamp_end(a);
+  stamp_end(a, t_start);
 }
 
 // ---------------------------------------------------------------------------
@@ -593,15 +643,16 @@ __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(LLCOLL_TWO
 // Mode 2 has one a.n-element input per rank.  Outputs: Mode 0, rank r's n
 // elements; Mode 1, rank r's chunk; Mode 2, the P blocks of rank r.
 template <class Pr, int DT, int P, int U, int Mode = 0>
-__global__ __launch_bounds__(512) void k_twoshot_waves(KArgs a) {
-  stamp_start(a);
+__global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
+  const KArgs a = pin_args(ka);
+  const uint64_t t_start = stamp_start(a);
   constexpr int E = Elem<DT>::kBytes;
   constexpr int K = Elem<DT>::kPerWord;
   constexpr int WPU = Pr::kUnitWords;  // payload words per unit
   constexpr int EPU = WPU * K;         // elements per unit
   constexpr bool kRS = Mode != 2, kAG = Mode != 1;
   __shared__ float stage[kRS ? P : 1][64 * U * EPU];
-  const Part pt = part_of_block<P>();
+  const Part pt = part_of_block<P>(a);
   const int r = pt.r;
   const int q = (int)uniform_u32(threadIdx.x >> 6);  // this wave's peer (q == r: the own values)
   const int lane = (int)(threadIdx.x & 63);
@@ -755,7 +806,7 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs a) {
     }
     if constexpr (kRS) lds_barrier();  // the next tile overwrites the staging rows
   }
-  stamp_end(a);
+  stamp_end(a, t_start);
 }
 
 // ---------------------------------------------------------------------------
@@ -785,16 +836,17 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs a) {
 // caller guarantees 16-byte aligned rows (count * esize % 16 == 0), so every
 // lane's 16 input bytes are wholly inside or wholly outside a chunk.
 template <int DT, int P>
-__global__ __launch_bounds__(1024) void k_twoshot_atomic(KArgs a) {
-  stamp_start(a);
+__global__ __launch_bounds__(1024) void k_twoshot_atomic(KArgs ka) {
+  const KArgs a = pin_args(ka);
+  const uint64_t t_start = stamp_start(a);
   constexpr int E = Elem<DT>::kBytes;
   constexpr int EL = 16 / E;  // elements per lane: 16 input bytes
   constexpr int TE = 64 * EL; // elements per tile (one wave)
-  const Part pt = part_of_block<P>();
+  const Part pt = part_of_block<P>(a);
   const int r = pt.r;
   const int lane = (int)(threadIdx.x & 63);
-  const int64_t gw = ((int64_t)pt.w * blockDim.x + threadIdx.x) >> 6;
-  const int64_t GW = ((int64_t)pt.W * blockDim.x) >> 6;
+  const int64_t gw = ((int64_t)pt.w * a.block + threadIdx.x) >> 6;
+  const int64_t GW = ((int64_t)pt.W * a.block) >> 6;
   const int64_t n = a.n, C = a.chunk;
   const int64_t tiles = (C + TE - 1) / TE;
   const uint64_t deadline = now_ticks() + a.timeout;
@@ -904,7 +956,7 @@ __global__ __launch_bounds__(1024) void k_twoshot_atomic(KArgs a) {
     if (s >= lag && s - lag < steps) step_reduce(gw + (s - lag) * GW);
     if (s >= 2 * lag && s - 2 * lag < steps) step_gather(gw + (s - 2 * lag) * GW);
   }
-  stamp_end(a);
+  stamp_end(a, t_start);
 }
 
 // ---------------------------------------------------------------------------
@@ -915,18 +967,19 @@ __global__ __launch_bounds__(1024) void k_twoshot_atomic(KArgs a) {
 // peer q and copies them to its own output; every other rank polls that one
 // slot and stores what arrives.  Output: every rank's copy, back to back.
 template <class Pr, int DT, int P>
-__global__ __launch_bounds__(1024) void k_broadcast(KArgs a) {
-  stamp_start(a);
-  const Part pt = part_of_block<P>();
+__global__ __launch_bounds__(1024) void k_broadcast(KArgs ka) {
+  const KArgs a = pin_args(ka);
+  const uint64_t t_start = stamp_start(a);
+  const Part pt = part_of_block<P>(a);
   const int r = pt.r, root = a.root;
   constexpr int E = Elem<DT>::kBytes;
   const uint64_t deadline = now_ticks() + a.timeout;
   const int64_t n = a.n;
   const int64_t units = Pr::units((n * E + 3) / 4);
   char *const out_r = a.out + (uint64_t)r * (uint64_t)n * E;
-  const int64_t g = (int64_t)pt.w * blockDim.x + threadIdx.x;
+  const int64_t g = (int64_t)pt.w * a.block + threadIdx.x;
   const int sub = (int)(g % Pr::kLanes);
-  const int64_t ustep = (int64_t)pt.W * blockDim.x / Pr::kLanes;
+  const int64_t ustep = (int64_t)pt.W * a.block / Pr::kLanes;
   if (r == root) {
     const char *const in_r = a.in + (uint64_t)r * a.in_stride;
     for (int64_t u = g / Pr::kLanes; u < units; u += ustep) {
@@ -944,7 +997,7 @@ __global__ __launch_bounds__(1024) void k_broadcast(KArgs a) {
       Pr::template store<DT>(out_r, u, sub, n, a.al4 != 0, Pr::unpack(got[root], sub));
     }
   }
-  stamp_end(a);
+  stamp_end(a, t_start);
 }
 
 // Reduce: every rank but the root stores its input units into slot
@@ -952,21 +1005,22 @@ __global__ __launch_bounds__(1024) void k_broadcast(KArgs a) {
 // contributions in ascending rank order, rounding once (as AllReduce).
 // Output: the root's result only, `n` elements at `out`.
 template <class Pr, int DT, int P>
-__global__ __launch_bounds__(1024) void k_reduce(KArgs a) {
-  stamp_start(a);
-  const Part pt = part_of_block<P>();
+__global__ __launch_bounds__(1024) void k_reduce(KArgs ka) {
+  const KArgs a = pin_args(ka);
+  const uint64_t t_start = stamp_start(a);
+  const Part pt = part_of_block<P>(a);
   const int r = pt.r, root = a.root;
   constexpr int E = Elem<DT>::kBytes;
   const uint64_t deadline = now_ticks() + a.timeout;
   const int64_t n = a.n;
   const int64_t units = Pr::units((n * E + 3) / 4);
   const char *const in_r = a.in + (uint64_t)r * a.in_stride;
-  const int64_t g = (int64_t)pt.w * blockDim.x + threadIdx.x;
+  const int64_t g = (int64_t)pt.w * a.block + threadIdx.x;
   const int sub = (int)(g % Pr::kLanes);
-  const int64_t ustep = (int64_t)pt.W * blockDim.x / Pr::kLanes;
+  const int64_t ustep = (int64_t)pt.W * a.block / Pr::kLanes;
   if (r != root) {
     if (r == a.mute) {
-      stamp_end(a);
+      stamp_end(a, t_start);
       return;
     }
     char *const dst = a.sym + (uint64_t)root * a.stride + a.area + (uint64_t)slot_of(r, root) * a.slot;
@@ -987,7 +1041,7 @@ __global__ __launch_bounds__(1024) void k_reduce(KArgs a) {
       Pr::template store<DT>(a.out, u, sub, n, a.al4 != 0, reduce_ordered<Pr, DT, P>(got, own, r));
     }
   }
-  stamp_end(a);
+  stamp_end(a, t_start);
 }
 
 // ---------------------------------------------------------------------------
@@ -997,9 +1051,10 @@ __global__ __launch_bounds__(1024) void k_reduce(KArgs a) {
 // elements, software-pipelined the same way (publish unit s, reduce unit
 // s - lag).
 template <class Pr, int DT, int P>
-__global__ __launch_bounds__(1024) void k_reduce_scatter(KArgs a) {
-  stamp_start(a);
-  const Part pt = part_of_block<P>();
+__global__ __launch_bounds__(1024) void k_reduce_scatter(KArgs ka) {
+  const KArgs a = pin_args(ka);
+  const uint64_t t_start = stamp_start(a);
+  const Part pt = part_of_block<P>(a);
   const int r = pt.r;
   constexpr int E = Elem<DT>::kBytes;
   const uint64_t deadline = now_ticks() + a.timeout;
@@ -1011,10 +1066,10 @@ __global__ __launch_bounds__(1024) void k_reduce_scatter(KArgs a) {
   const int64_t units = Pr::units((m * E + 3) / 4);
   const bool al4 = a.al4 != 0;
   const bool publish = (r != a.mute);
-  const int64_t g = (int64_t)pt.w * blockDim.x + threadIdx.x;
+  const int64_t g = (int64_t)pt.w * a.block + threadIdx.x;
   const int sub = (int)(g % Pr::kLanes);
   const int64_t u0 = g / Pr::kLanes;
-  const int64_t ustep = (int64_t)pt.W * blockDim.x / Pr::kLanes;
+  const int64_t ustep = (int64_t)pt.W * a.block / Pr::kLanes;
   const int64_t steps = u0 < units ? (units - u0 + ustep - 1) / ustep : 0;
   const int64_t lag = a.lag > 0 ? a.lag : 1;
 
@@ -1047,7 +1102,7 @@ __global__ __launch_bounds__(1024) void k_reduce_scatter(KArgs a) {
       Pr::template store<DT>(out_r, u, sub, m, al4, res);
     }
   }
-  stamp_end(a);
+  stamp_end(a, t_start);
 }
 
 // ---------------------------------------------------------------------------
@@ -1056,9 +1111,10 @@ __global__ __launch_bounds__(1024) void k_reduce_scatter(KArgs a) {
 // receives from peer q at block q of its output.  Pipelined like the others:
 // publish unit s, gather unit s - lag.
 template <class Pr, int DT, int P>
-__global__ __launch_bounds__(1024) void k_allgather(KArgs a) {
-  stamp_start(a);
-  const Part pt = part_of_block<P>();
+__global__ __launch_bounds__(1024) void k_allgather(KArgs ka) {
+  const KArgs a = pin_args(ka);
+  const uint64_t t_start = stamp_start(a);
+  const Part pt = part_of_block<P>(a);
   const int r = pt.r;
   constexpr int E = Elem<DT>::kBytes;
   const uint64_t deadline = now_ticks() + a.timeout;
@@ -1069,10 +1125,10 @@ __global__ __launch_bounds__(1024) void k_allgather(KArgs a) {
   const bool al4 = a.al4 != 0;
   char *const out_r = a.out + (uint64_t)r * (uint64_t)P * n * E;
   const bool publish = (r != a.mute);
-  const int64_t g = (int64_t)pt.w * blockDim.x + threadIdx.x;
+  const int64_t g = (int64_t)pt.w * a.block + threadIdx.x;
   const int sub = (int)(g % Pr::kLanes);
   const int64_t u0 = g / Pr::kLanes;
-  const int64_t ustep = (int64_t)pt.W * blockDim.x / Pr::kLanes;
+  const int64_t ustep = (int64_t)pt.W * a.block / Pr::kLanes;
   const int64_t steps = u0 < units ? (units - u0 + ustep - 1) / ustep : 0;
   const int64_t lag = a.lag > 0 ? a.lag : 1;
 
@@ -1096,7 +1152,7 @@ __global__ __launch_bounds__(1024) void k_allgather(KArgs a) {
       }
     }
   }
-  stamp_end(a);
+  stamp_end(a, t_start);
 }
 
 // Set `bytes` bytes at `dst` (16-byte aligned) to 0xFF: the sentinel of

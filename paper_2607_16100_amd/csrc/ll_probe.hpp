@@ -18,25 +18,33 @@
 
 namespace llc {
 
+// Start times are kept in a register and stored with the end times, as in the
+// collectives, so that no store precedes the first load.
 __global__ void k_probe_empty(uint64_t *stamps) {
   if (stamps != nullptr) {
-    if (threadIdx.x == 0) stamps[blockIdx.x] = now_ticks();
+    const uint64_t t0 = now_ticks();
     __syncthreads();
-    if (threadIdx.x == 0) stamps[gridDim.x + blockIdx.x] = now_ticks();
+    if (threadIdx.x == 0) {
+      stamps[blockIdx.x] = t0;
+      stamps[gridDim.x + blockIdx.x] = now_ticks();
+    }
   }
 }
 
 // One dependent HBM round trip: lane 0 of workgroup 0 loads chase[start]
 // (a line nobody has touched recently) and stores the value.
 __global__ void k_probe_floor(const uint64_t *chase, uint64_t start, uint64_t *sink, uint64_t *stamps) {
-  if (stamps != nullptr && threadIdx.x == 0) stamps[blockIdx.x] = now_ticks();
+  const uint64_t t0 = stamps != nullptr ? now_ticks() : 0;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     const uint64_t v = __builtin_nontemporal_load(chase + start);
     sink[0] = v;
   }
   if (stamps != nullptr) {
     __syncthreads();
-    if (threadIdx.x == 0) stamps[gridDim.x + blockIdx.x] = now_ticks();
+    if (threadIdx.x == 0) {
+      stamps[blockIdx.x] = t0;
+      stamps[gridDim.x + blockIdx.x] = now_ticks();
+    }
   }
 }
 

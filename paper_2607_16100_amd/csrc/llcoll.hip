@@ -37,7 +37,8 @@ std::atomic<int> g_poll_gap{0};
 std::atomic<int> g_wave_units{0};  // 0 = automatic, else 1, 2 or 4
 std::atomic<int> g_lag{1};
 std::atomic<int> g_auto_sentinel{0};
-std::atomic<int> g_wave_kernels{0};  // stand-alone RS/AG: 0 = by size, 1 = never, 2 = always
+std::atomic<int> g_wave_kernels{0};
+std::atomic<int> g_probe{0};  // stand-alone RS/AG: 0 = by size, 1 = never, 2 = always
 std::atomic<uint64_t *> g_stamps{nullptr};
 std::atomic<uint64_t *> g_phases{nullptr};
 std::atomic<int> g_last_grid{0};
@@ -295,6 +296,8 @@ int launch(const Plan &pl, void *stream) {
   a.first_wait = (uint16_t)g_first_wait.load();
   a.poll_gap = (uint16_t)g_poll_gap.load();
   a.lag = (uint32_t)g_lag.load();
+  a.grid = (uint32_t)grid;
+  a.block = (uint32_t)threads;
   a.stamps = g_stamps.exchange(nullptr);
   a.phases = g_phases.exchange(nullptr);
   hipLaunchKernelGGL(fn, dim3(grid), dim3(threads), 0, (hipStream_t)stream, a);
