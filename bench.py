@@ -313,9 +313,10 @@ def bench_scratch(torch, ll, iters=10, warmup=3):
     return out
 
 
-def bench_sweep(torch, ll, path):
+def bench_sweep(torch, ll, path, floor_p50_us=None):
     """C4: 8 ranks, binary32, 2 .. 2^26 elements per rank; p50/p99 and GB/s of
-    every algorithm at every size (written to `path` as JSON lines)."""
+    every algorithm at every size (written to `path` as JSON lines), each with
+    its ratio to the latency floor and its fraction of the HBM peak."""
     from paper_2607_16100_amd import bytemodel
     from paper_2607_16100_amd.region import SymRegion
 
@@ -340,9 +341,10 @@ def bench_sweep(torch, ll, path):
                 if algo in ("twoshot_atomic", "twoshot_sentinel_out") and n < 4:
                     continue
                 r = paced_collective(torch, ll, reg, "ar", n, ll.ALGOS[algo], steps, min(20, steps))
-                r.update({"elements": n, "bytes_per_rank": n * 4, "algo": algo,
-                          "algorithmic_gbps_p50": bytemodel.allreduce_bytes(algo if algo != "auto" else "twoshot_line", p, n, 4)
-                          / r["p50_us"] / 1e3 if algo != "auto" else None})
+                gbps = (bytemodel.allreduce_bytes(algo, p, n, 4) / r["p50_us"] / 1e3) if algo != "auto" else None
+                r.update({"elements": n, "bytes_per_rank": n * 4, "algo": algo, "algorithmic_gbps_p50": gbps,
+                          "hbm_frac_p50": gbps / PEAK_HBM_GBS if gbps else None,
+                          "ratio_to_floor": r["p50_us"] / floor_p50_us if floor_p50_us else None})
                 f.write(json.dumps(r) + "\n")
                 f.flush()
                 log(f"sweep n={n} {algo} p50={r['p50_us']:.2f}")
@@ -452,9 +454,12 @@ def bench_cpu_baseline(seconds: float):
         t0 = time.perf_counter()
         want = oracle.allreduce(x)
         times.append(time.perf_counter() - t0)
-    res = {"value": float(np.median(times)) * 1e6, "unit": "us", "cores": 1, "kind": "oracle",
+    med = float(np.median(times))
+    res = {"value": med * 1e6, "unit": "us", "cores": 1, "kind": "oracle",
            "sample": f"8 ranks x 8192 bf16 (the 16 KiB workload) reduced {len(times)} times in ~{seconds:.0f} s "
-                     f"by the single-threaded C oracle; median per call"}
+                     f"by the single-threaded C oracle; median per call",
+           "gbps_read_inputs_write_output": (8 * 8192 * 2 + 8192 * 2) / med / 1e9,
+           "host_cores_available": len(os.sched_getaffinity(0))}
     got = HEADLINE_OUTPUT.get("bits")
     if got is not None:  # the headline's last GPU result against the oracle's
         res["headline_bit_exact"] = bool(np.array_equal(got, want))
@@ -504,8 +509,11 @@ def main():
     torch.cuda.set_device(0)
     props = torch.cuda.get_device_properties(0)
     log(f"device: {props.name} {getattr(props, 'gcnArchName', '')} CUs={props.multi_processor_count}")
-    ll.ll_set_poll_timeout(200_000_000)
     result = {}
+    result["device"] = {"name": props.name, "arch": getattr(props, "gcnArchName", ""),
+                        "compute_units": props.multi_processor_count, "hbm_bytes": props.total_memory,
+                        "hip_runtime": getattr(torch.version, "hip", None), "torch": torch.__version__}
+    ll.ll_set_poll_timeout(200_000_000)
     if want("headline"):
         log("headline: 16 KiB bf16 one-shot, 8 ranks")
         result["headline"] = bench_headline(torch, ll, args.steps, args.warmup)
@@ -544,7 +552,8 @@ def main():
         result["scratch"] = bench_scratch(torch, ll)
     if args.sweep:
         log("C4 sweep")
-        result["sweep_file"] = bench_sweep(torch, ll, args.sweep)
+        fl0 = result.get("floor", {}).get("floor", {}).get("p50_us")
+        result["sweep_file"] = bench_sweep(torch, ll, args.sweep, fl0)
     if want("copy"):
         log("device copy reference")
         result["copy"] = bench_copy(torch)
