@@ -132,9 +132,11 @@ def test_allreduce_special_values(algo, dtype):
 
 
 # ------------------------------------------------------------ configuration C2
-def test_c2_oneshot_bf16_16k_10k_calls():
+@pytest.mark.parametrize("algo", ["oneshot", "auto"])
+def test_c2_oneshot_bf16_16k_10k_calls(algo):
     """8 ranks, bfloat16, 8192 normal(0,1) elements per rank, one-shot with
-    8-byte packets, 10,000 back-to-back calls with the epoch incremented."""
+    8-byte packets (AUTO: the wave-per-peer kernel the benchmark times),
+    10,000 back-to-back calls with the epoch incremented."""
     p, n = 8, 8192
     x = wl.normal(p, n, "bf16", sigma=1.0, seed=0)
     want = oracle.allreduce(x)
@@ -143,7 +145,7 @@ def test_c2_oneshot_bf16_16k_10k_calls():
     reg.write_inputs(x)
     s = stream()
     for i in range(10_000):
-        st = reg.allreduce(n, "oneshot")
+        st = reg.allreduce(n, algo)
         assert st == ll.LL_OK
         if i % 1000 == 999:
             assert ll.ll_check(s) == ll.LL_OK, f"C2: status after call {i}"
