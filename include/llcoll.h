@@ -91,8 +91,10 @@ typedef enum {
   LL_ALGO_TWOSHOT_WAVES = 10,       /* two-shot, 8-byte packets, one wave per peer, partial
                                        sums staged in LDS (single iteration only) */
   LL_ALGO_TWOSHOT_SENTINEL_WAVES = 11, /* the same with sentinel units */
-  LL_ALGO_ONESHOT_SENTINEL_WAVES = 12  /* one-shot, sentinel units, one wave per peer (single
+  LL_ALGO_ONESHOT_SENTINEL_WAVES = 12, /* one-shot, sentinel units, one wave per peer (single
                                           iteration only) */
+  LL_ALGO_ONESHOT_LINE_WAVES = 13,     /* one-shot, 128-byte lines, one wave per peer */
+  LL_ALGO_TWOSHOT_LINE_WAVES = 14      /* two-shot, 128-byte lines, one wave per peer */
 } ll_algo;
 
 /* LL_ALGO_TWOSHOT_ATOMIC, the analogue of the paper's two-shot LL128 atomic

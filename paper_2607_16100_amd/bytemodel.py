@@ -33,8 +33,9 @@ def _proto(algo: str) -> tuple[str, str]:
     base = {"oneshot": "oneshot", "oneshot_line": "oneshot", "oneshot_waves": "oneshot",
             "oneshot_sentinel": "oneshot", "twoshot": "twoshot", "twoshot_line": "twoshot",
             "twoshot_sentinel": "twoshot", "twoshot_waves": "twoshot", "twoshot_sentinel_waves": "twoshot",
-            "oneshot_sentinel_waves": "oneshot"}[algo]
-    proto = "line128" if algo.endswith("_line") else ("sentinel" if "_sentinel" in algo else "packet8")
+            "oneshot_sentinel_waves": "oneshot", "oneshot_line_waves": "oneshot",
+            "twoshot_line_waves": "twoshot"}[algo]
+    proto = "line128" if "_line" in algo else ("sentinel" if "_sentinel" in algo else "packet8")
     return base, proto
 
 

@@ -309,27 +309,46 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_s_barrier();
 }
 
+// Unit addressing of the wave-per-peer kernels.  A tile is 64*U units of a
+// one-lane format (lane l owns units l, l+64, ...) or U units of the 64-lane
+// line format (the whole wave owns each unit; lane l is its part `sub`).
+// Either way a lane holds kMaxWords payload words per unit slot k.
+template <class Pr, int U>
+struct WaveUnits {
+  static constexpr bool kWave = Pr::kLanes == 64;
+  static constexpr int64_t kPerTile = kWave ? U : 64 * U;
+  __device__ static __forceinline__ int64_t unit(int64_t tile, int k, int lane) {
+    return kWave ? tile * U + k : tile * 64 * U + k * 64 + lane;
+  }
+  __device__ static __forceinline__ int sub(int lane) { return kWave ? lane : 0; }
+  __device__ static __forceinline__ uint32_t off(int64_t u, int lane) {
+    return (uint32_t)(u * Pr::kUnitBytes + sub(lane) * 16);
+  }
+};
+
 template <class Pr, int DT, int P, int U>
 __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
   const KArgs a = pin_args(ka);
   const uint64_t t_start = stamp_start(a);
   constexpr int E = Elem<DT>::kBytes;
   constexpr int K = Elem<DT>::kPerWord;
-  constexpr int WPU = Pr::kUnitWords;  // payload words per unit
-  constexpr int EPU = WPU * K;         // elements per unit
-  constexpr int TW = 64 * U * WPU;     // payload words per tile
+  using WU = WaveUnits<Pr, U>;
+  constexpr int WPU = Pr::kMaxWords;  // payload words per lane and unit slot
+  constexpr int EPU = WPU * K;        // elements per lane and unit slot
+  constexpr int TW = 64 * U * WPU;    // payload words per tile
   __shared__ float stage[P][TW * K];
   const Part pt = part_of_block<P>(a);
   const int r = pt.r;
   const int wv = (int)uniform_u32(threadIdx.x >> 6);  // the same in every lane of a wave
   const int lane = (int)(threadIdx.x & 63);
+  const int sub = WU::sub(lane);
   const uint64_t deadline = now_ticks() + a.timeout;
   char *const slice_r = a.sym + (uint64_t)r * a.stride;
   const char *const in_r = a.in + (uint64_t)r * a.in_stride;
   const int64_t n = a.n;
   const int64_t words = (n * E + 3) / 4;
   const int64_t units = Pr::units(words);
-  const int64_t tiles = (units + 64 * U - 1) / (64 * U);
+  const int64_t tiles = (units + WU::kPerTile - 1) / WU::kPerTile;
   char *const out_r = a.out + (uint64_t)r * (uint64_t)n * E;
   const bool publish = (r != a.mute);
   const int q = wv;  // the peer this wave talks to (q == r: the own values)
@@ -355,8 +374,8 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
     u32x4 own[U];
 #pragma unroll
     for (int k = 0; k < U; ++k) {
-      const int64_t u = tile * 64 * U + k * 64 + lane;
-      own[k] = u < units ? Pr::template load<DT>(in_r, u, 0, n, a.in_al4 != 0) : u32x4{0u, 0u, 0u, 0u};
+      const int64_t u = WU::unit(tile, k, lane);
+      own[k] = u < units ? Pr::template load<DT>(in_r, u, sub, n, a.in_al4 != 0) : u32x4{0u, 0u, 0u, 0u};
     }
     if (a.phases != nullptr && lane == 0 && tile == pt.w) {
       a.phases[4 * (blockIdx.x * P + wv) + 0] = now_ticks() + (own[0].x & 0u);
@@ -371,11 +390,11 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
       uint32_t pend = 0;
 #pragma unroll
       for (int k = 0; k < U; ++k) {
-        const int64_t u = tile * 64 * U + k * 64 + lane;
+        const int64_t u = WU::unit(tile, k, lane);
         v[k] = u32x4{0u, 0u, 0u, 0u};
         if (u < units) {
           pend |= 1u << k;
-          if (publish) st_pkt(rd, (uint32_t)(u * Pr::kUnitBytes), Pr::pack(own[k], a.epoch, 0));
+          if (publish) st_pkt(rd, WU::off(u, lane), Pr::pack(own[k], a.epoch, sub));
         }
       }
       const uint32_t want = pend;
@@ -386,13 +405,13 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
         u32x4 pk[U];
 #pragma unroll
         for (int k = 0; k < U; ++k) {
-          const int64_t u = tile * 64 * U + k * 64 + lane;
-          if (pend & (1u << k)) pk[k] = ld_pkt(rs, (uint32_t)(u * Pr::kUnitBytes));
+          const int64_t u = WU::unit(tile, k, lane);
+          if (pend & (1u << k)) pk[k] = ld_pkt(rs, WU::off(u, lane));
         }
 #pragma unroll
         for (int k = 0; k < U; ++k) {
           if ((pend & (1u << k)) && Pr::ready(pk[k], a.epoch)) {
-            v[k] = Pr::unpack(pk[k], 0);
+            v[k] = Pr::unpack(pk[k], sub);
             pend &= ~(1u << k);
           }
         }
@@ -406,8 +425,8 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
         const u32x4 sent = {ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel};
 #pragma unroll
         for (int k = 0; k < U; ++k) {
-          const int64_t u = tile * 64 * U + k * 64 + lane;
-          if (want & (1u << k)) st_pkt(rs, (uint32_t)(u * Pr::kUnitBytes), sent);
+          const int64_t u = WU::unit(tile, k, lane);
+          if (want & (1u << k)) st_pkt(rs, WU::off(u, lane), sent);
         }
       }
       if (a.phases != nullptr && lane == 0 && tile == pt.w) {
@@ -417,17 +436,41 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
     }
     lds_barrier();
     if (a.phases != nullptr && lane == 0 && tile == pt.w) a.phases[4 * (blockIdx.x * P + wv) + 2] = now_ticks();
-    for (int j = (int)threadIdx.x; j < TW; j += (int)a.block) {
-      float acc[K];
+    if constexpr (WU::kWave) {
+      // line units are in packet order: the own-rank wave sums its lanes'
+      // words and stores whole units (the store puts displaced words back)
+      if (q == r) {
 #pragma unroll
-      for (int e = 0; e < K; ++e) acc[e] = stage[0][j * K + e];
+        for (int k = 0; k < U; ++k) {
+          uint32_t w[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
-      for (int p = 1; p < P; ++p) {
+          for (int j = 0; j < WPU; ++j) {
+            float acc[K];
 #pragma unroll
-        for (int e = 0; e < K; ++e) acc[e] = acc[e] + stage[p][j * K + e];
+            for (int e = 0; e < K; ++e) acc[e] = stage[0][(k * 64 + lane) * EPU + j * K + e];
+#pragma unroll
+            for (int p = 1; p < P; ++p) {
+#pragma unroll
+              for (int e = 0; e < K; ++e) acc[e] = acc[e] + stage[p][(k * 64 + lane) * EPU + j * K + e];
+            }
+            w[j] = Elem<DT>::narrow(acc);
+          }
+          Pr::template store<DT>(out_r, WU::unit(tile, k, lane), sub, n, a.al4 != 0, u32x4{w[0], w[1], w[2], w[3]});
+        }
       }
-      const u32x4 res = {Elem<DT>::narrow(acc), 0u, 0u, 0u};
-      store_words<DT>(out_r, tile * TW + j, 1, n, a.al4 != 0, res);
+    } else {
+      for (int j = (int)threadIdx.x; j < TW; j += (int)a.block) {
+        float acc[K];
+#pragma unroll
+        for (int e = 0; e < K; ++e) acc[e] = stage[0][j * K + e];
+#pragma unroll
+        for (int p = 1; p < P; ++p) {
+#pragma unroll
+          for (int e = 0; e < K; ++e) acc[e] = acc[e] + stage[p][j * K + e];
+        }
+        const u32x4 res = {Elem<DT>::narrow(acc), 0u, 0u, 0u};
+        store_words<DT>(out_r, tile * TW + j, 1, n, a.al4 != 0, res);
+      }
     }
     lds_barrier();  // the next tile overwrites the staging rows
   }
@@ -648,14 +691,16 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
   const uint64_t t_start = stamp_start(a);
   constexpr int E = Elem<DT>::kBytes;
   constexpr int K = Elem<DT>::kPerWord;
-  constexpr int WPU = Pr::kUnitWords;  // payload words per unit
-  constexpr int EPU = WPU * K;         // elements per unit
+  using WU = WaveUnits<Pr, U>;
+  constexpr int WPU = Pr::kMaxWords;  // payload words per lane and unit slot
+  constexpr int EPU = WPU * K;        // elements per lane and unit slot
   constexpr bool kRS = Mode != 2, kAG = Mode != 1;
   __shared__ float stage[kRS ? P : 1][64 * U * EPU];
   const Part pt = part_of_block<P>(a);
   const int r = pt.r;
   const int q = (int)uniform_u32(threadIdx.x >> 6);  // this wave's peer (q == r: the own values)
   const int lane = (int)(threadIdx.x & 63);
+  const int sub = WU::sub(lane);
   const uint64_t deadline = now_ticks() + a.timeout;
   const int64_t C = Mode == 0 ? a.chunk : a.n;
   const int64_t n_all = Mode == 0 ? a.n : (int64_t)P * a.n;
@@ -675,7 +720,7 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
     return left < 0 ? 0 : (left < C ? left : C);
   };
   const int64_t units = Pr::units((C * E + 3) / 4);
-  const int64_t tiles = (units + 64 * U - 1) / (64 * U);
+  const int64_t tiles = (units + WU::kPerTile - 1) / WU::kPerTile;
   // slot (q <- r) in peer q's slice and slot (r <- q) in this rank's slice
   const uint64_t slot_out = (uint64_t)slot_of(r, q) * a.slot, slot_in = (uint64_t)slot_of(q, r) * a.slot;
   char *const peer_slice = a.sym + (uint64_t)q * a.stride;
@@ -696,13 +741,13 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
 
   // Poll U units of slot `src` (this rank's slice) from peer q; sentinel
   // units are given back to the sentinel once read.
-  auto poll_peer = [&](char *src, int64_t tile_u0, u32x4 *v) {
+  auto poll_peer = [&](char *src, int64_t tile, u32x4 *v) {
     const rsrc_t rs = make_rsrc(src, (uint32_t)a.slot);
     uint32_t pend = 0;
 #pragma unroll
     for (int k = 0; k < U; ++k) {
       v[k] = u32x4{0u, 0u, 0u, 0u};
-      if (tile_u0 + k * 64 + lane < units) pend |= 1u << k;
+      if (WU::unit(tile, k, lane) < units) pend |= 1u << k;
     }
     const uint32_t want = pend;
     int spins = 1;
@@ -711,11 +756,11 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
       u32x4 pk[U];
 #pragma unroll
       for (int k = 0; k < U; ++k)
-        if (pend & (1u << k)) pk[k] = ld_pkt(rs, (uint32_t)((tile_u0 + k * 64 + lane) * Pr::kUnitBytes));
+        if (pend & (1u << k)) pk[k] = ld_pkt(rs, WU::off(WU::unit(tile, k, lane), lane));
 #pragma unroll
       for (int k = 0; k < U; ++k) {
         if ((pend & (1u << k)) && Pr::ready(pk[k], a.epoch)) {
-          v[k] = Pr::unpack(pk[k], 0);
+          v[k] = Pr::unpack(pk[k], sub);
           pend &= ~(1u << k);
         }
       }
@@ -728,35 +773,34 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
       const u32x4 sent = {ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel};
 #pragma unroll
       for (int k = 0; k < U; ++k)
-        if (want & (1u << k)) st_pkt(rs, (uint32_t)((tile_u0 + k * 64 + lane) * Pr::kUnitBytes), sent);
+        if (want & (1u << k)) st_pkt(rs, WU::off(WU::unit(tile, k, lane), lane), sent);
     }
   };
 
   for (int64_t tile = pt.w; tile < tiles; tile += pt.W) {
-    const int64_t u0 = tile * 64 * U;
     u32x4 res[U];
     if constexpr (kRS) {
       // ---- ReduceScatter of this tile
       if (q == r) {
         u32x4 own[U];
 #pragma unroll
-        for (int k = 0; k < U; ++k) own[k] = Pr::template load<DT>(in_chunk(r), u0 + k * 64 + lane, 0, chunk_len(r),
-                                                                  in_al4);
+        for (int k = 0; k < U; ++k) own[k] = Pr::template load<DT>(in_chunk(r), WU::unit(tile, k, lane), sub,
+                                                                  chunk_len(r), in_al4);
         stage_row(own);
       } else {
         if (publish) {
           const rsrc_t rd = make_rsrc(peer_slice + a.area + slot_out, (uint32_t)a.slot);
 #pragma unroll
           for (int k = 0; k < U; ++k) {
-            const int64_t u = u0 + k * 64 + lane;
+            const int64_t u = WU::unit(tile, k, lane);
             if (u < units) {
-              const u32x4 w = Pr::template load<DT>(in_chunk(q), u, 0, chunk_len(q), in_al4);
-              st_pkt(rd, (uint32_t)(u * Pr::kUnitBytes), Pr::pack(w, a.epoch, 0));
+              const u32x4 w = Pr::template load<DT>(in_chunk(q), u, sub, chunk_len(q), in_al4);
+              st_pkt(rd, WU::off(u, lane), Pr::pack(w, a.epoch, sub));
             }
           }
         }
         u32x4 v[U];
-        poll_peer(slice_r + a.area + slot_in, u0, v);
+        poll_peer(slice_r + a.area + slot_in, tile, v);
         stage_row(v);
       }
       lds_barrier();
@@ -780,29 +824,29 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
       }
     } else {
 #pragma unroll
-      for (int k = 0; k < U; ++k) res[k] = Pr::template load<DT>(in_chunk(r), u0 + k * 64 + lane, 0, C, in_al4);
+      for (int k = 0; k < U; ++k) res[k] = Pr::template load<DT>(in_chunk(r), WU::unit(tile, k, lane), sub, C, in_al4);
     }
     // ---- AllGather of this tile
     if (q == r || !kAG) {
       if (q == r) {
 #pragma unroll
         for (int k = 0; k < U; ++k)
-          Pr::template store<DT>(out_chunk(r), u0 + k * 64 + lane, 0, chunk_len(r), al4, res[k]);
+          Pr::template store<DT>(out_chunk(r), WU::unit(tile, k, lane), sub, chunk_len(r), al4, res[k]);
       }
     } else {
       if (publish) {
         const rsrc_t rd = make_rsrc(peer_slice + ag_area + slot_out, (uint32_t)a.slot);
 #pragma unroll
         for (int k = 0; k < U; ++k) {
-          const int64_t u = u0 + k * 64 + lane;
-          if (u < units) st_pkt(rd, (uint32_t)(u * Pr::kUnitBytes), Pr::pack(res[k], a.epoch, 0));
+          const int64_t u = WU::unit(tile, k, lane);
+          if (u < units) st_pkt(rd, WU::off(u, lane), Pr::pack(res[k], a.epoch, sub));
         }
       }
       u32x4 v[U];
-      poll_peer(slice_r + ag_area + slot_in, u0, v);
+      poll_peer(slice_r + ag_area + slot_in, tile, v);
 #pragma unroll
       for (int k = 0; k < U; ++k)
-        Pr::template store<DT>(out_chunk(q), u0 + k * 64 + lane, 0, chunk_len(q), al4, v[k]);
+        Pr::template store<DT>(out_chunk(q), WU::unit(tile, k, lane), sub, chunk_len(q), al4, v[k]);
     }
     if constexpr (kRS) lds_barrier();  // the next tile overwrites the staging rows
   }

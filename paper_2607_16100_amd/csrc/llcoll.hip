@@ -93,8 +93,8 @@ void fill_row(kernel_fn *row) {
 // table[proto][dtype][P][kind]
 struct Table {
   kernel_fn k[PR_COUNT][2][LL_MAX_RANKS + 1][K_KINDS];
-  kernel_fn waves[3][2][2][LL_MAX_RANKS + 1];  // [log2 U][8-byte packets, sentinel][dtype][P]
-  kernel_fn twaves[3][3][2][2][LL_MAX_RANKS + 1];  // [AR, RS, AG][log2 U][8-byte packets, sentinel][dtype][P]
+  kernel_fn waves[3][3][2][LL_MAX_RANKS + 1];  // [log2 U][8-byte packets, sentinel, lines][dtype][P]
+  kernel_fn twaves[3][3][3][2][LL_MAX_RANKS + 1];  // [AR, RS, AG][log2 U][8-byte, sentinel, lines][dtype][P]
   Table() {
     memset(k, 0, sizeof k);
     memset(waves, 0, sizeof waves);
@@ -121,6 +121,12 @@ struct Table {
     twaves[M][1][1][1][P] = k_twoshot_waves<ProtoSent, 1, P, 2, M>;
     twaves[M][2][1][0][P] = k_twoshot_waves<ProtoSent, 0, P, 4, M>;
     twaves[M][2][1][1][P] = k_twoshot_waves<ProtoSent, 1, P, 4, M>;
+    twaves[M][0][2][0][P] = k_twoshot_waves<ProtoLine, 0, P, 1, M>;
+    twaves[M][0][2][1][P] = k_twoshot_waves<ProtoLine, 1, P, 1, M>;
+    twaves[M][1][2][0][P] = k_twoshot_waves<ProtoLine, 0, P, 2, M>;
+    twaves[M][1][2][1][P] = k_twoshot_waves<ProtoLine, 1, P, 2, M>;
+    twaves[M][2][2][0][P] = k_twoshot_waves<ProtoLine, 0, P, 4, M>;
+    twaves[M][2][2][1][P] = k_twoshot_waves<ProtoLine, 1, P, 4, M>;
   }
   template <int P>
   void fill() {
@@ -142,6 +148,12 @@ struct Table {
     waves[1][1][1][P] = k_oneshot_waves<ProtoSent, 1, P, 2>;
     waves[2][1][0][P] = k_oneshot_waves<ProtoSent, 0, P, 4>;
     waves[2][1][1][P] = k_oneshot_waves<ProtoSent, 1, P, 4>;
+    waves[0][2][0][P] = k_oneshot_waves<ProtoLine, 0, P, 1>;
+    waves[0][2][1][P] = k_oneshot_waves<ProtoLine, 1, P, 1>;
+    waves[1][2][0][P] = k_oneshot_waves<ProtoLine, 0, P, 2>;
+    waves[1][2][1][P] = k_oneshot_waves<ProtoLine, 1, P, 2>;
+    waves[2][2][0][P] = k_oneshot_waves<ProtoLine, 0, P, 4>;
+    waves[2][2][1][P] = k_oneshot_waves<ProtoLine, 1, P, 4>;
     fill_twaves<0, P>();
     fill_twaves<1, P>();
     fill_twaves<2, P>();
@@ -245,13 +257,12 @@ int launch(const Plan &pl, void *stream) {
   const bool wave_kernel = pl.kind == K_ONESHOT_WAVES || two_waves;
   const int wlog = wave_kernel ? wave_units_log2(pl.units) : 0;
   kernel_fn fn = nullptr;
+  const int wpr = pl.proto == PR_SENT ? 1 : (pl.proto == PR_LINE ? 2 : 0);
   if (pl.kind == K_ONESHOT_WAVES) {
-    if (pl.proto == PR_LINE) return LL_ERR_UNSUPPORTED;
-    fn = table().waves[wlog][pl.proto == PR_SENT ? 1 : 0][pl.dt][pl.P];
+    fn = table().waves[wlog][wpr][pl.dt][pl.P];
   } else if (two_waves) {
-    if (pl.proto == PR_LINE) return LL_ERR_UNSUPPORTED;
     const int mode = pl.kind == K_TWOSHOT_WAVES ? 0 : (pl.kind == K_RS_WAVES ? 1 : 2);
-    fn = table().twaves[mode][wlog][pl.proto == PR_SENT ? 1 : 0][pl.dt][pl.P];
+    fn = table().twaves[mode][wlog][wpr][pl.dt][pl.P];
   } else {
     fn = table().k[pl.proto][pl.dt][pl.P][pl.kind];
   }
@@ -260,9 +271,9 @@ int launch(const Plan &pl, void *stream) {
   if (threads == 0) threads = 256;
   int lanes_per_unit = pl.proto == PR_LINE ? ProtoLine::kLanes : 1;
   int64_t work_units = pl.units;
-  if (wave_kernel) {  // one wave per rank, 64*U units per workgroup and step
+  if (wave_kernel) {  // one wave per rank; 64*U one-lane units (U line units) per workgroup and step
     threads = 64 * pl.P;
-    const int64_t tile = 64 * kWaveUnits[wlog];
+    const int64_t tile = (pl.proto == PR_LINE ? 1 : 64) * kWaveUnits[wlog];
     work_units = (pl.units + tile - 1) / tile;
     lanes_per_unit = threads;
   }
@@ -377,11 +388,13 @@ ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
   if (sentinel_ok) {
     if (in_bytes <= (P <= 4 ? 32 : 8) * KiB) return LL_ALGO_ONESHOT_WAVES;
     if (in_bytes <= (P <= 4 ? 128 : 64) * KiB) return LL_ALGO_ONESHOT_SENTINEL_WAVES;
-    if (in_bytes <= 4 * MiB) return LL_ALGO_TWOSHOT_SENTINEL_WAVES;
+    if (in_bytes <= (P <= 4 ? 2 : 1) * MiB) return LL_ALGO_TWOSHOT_SENTINEL_WAVES;
+    if (in_bytes <= 4 * MiB) return LL_ALGO_TWOSHOT_LINE_WAVES;
     return LL_ALGO_TWOSHOT_LINE;
   }
-  if (in_bytes <= (P <= 4 ? 64 : 16) * KiB) return LL_ALGO_ONESHOT_WAVES;
-  if (in_bytes <= 1 * MiB) return LL_ALGO_TWOSHOT_WAVES;
+  if (in_bytes <= (P <= 4 ? 32 : 16) * KiB) return LL_ALGO_ONESHOT_WAVES;
+  if (in_bytes <= 128 * KiB) return LL_ALGO_TWOSHOT_WAVES;
+  if (in_bytes <= 4 * MiB) return LL_ALGO_TWOSHOT_LINE_WAVES;
   return LL_ALGO_TWOSHOT_LINE;
 }
 
@@ -418,6 +431,12 @@ bool use_wave_kernel(ll_proto proto, uint64_t bytes, int P) {
   return bytes <= (P >= 5 ? (1u << 20) : (2u << 20));
 }
 
+// The wave-per-peer AllReduce kernels (single iteration only).
+bool is_wave_algo(ll_algo a) {
+  return a == LL_ALGO_ONESHOT_WAVES || a == LL_ALGO_ONESHOT_SENTINEL_WAVES || a == LL_ALGO_ONESHOT_LINE_WAVES ||
+         a == LL_ALGO_TWOSHOT_WAVES || a == LL_ALGO_TWOSHOT_SENTINEL_WAVES || a == LL_ALGO_TWOSHOT_LINE_WAVES;
+}
+
 // Algorithms whose AllGather stores into the peers' sentinel-filled outputs.
 bool fills_output(ll_algo algo) { return algo == LL_ALGO_TWOSHOT_SENTINEL_OUT || algo == LL_ALGO_TWOSHOT_ATOMIC; }
 
@@ -428,11 +447,13 @@ template <class AreaOf>
 void plan_allreduce(Plan *pl, ll_algo algo, uint64_t count, int es, int nranks, uint64_t iter_count,
                     AreaOf area_of) {
   const uint64_t it_bytes = iter_count * (uint64_t)es;
-  const bool line = (algo == LL_ALGO_TWOSHOT_LINE || algo == LL_ALGO_ONESHOT_LINE);
+  const bool line = (algo == LL_ALGO_TWOSHOT_LINE || algo == LL_ALGO_ONESHOT_LINE ||
+                     algo == LL_ALGO_ONESHOT_LINE_WAVES || algo == LL_ALGO_TWOSHOT_LINE_WAVES);
   const bool sent = (algo == LL_ALGO_ONESHOT_SENTINEL || algo == LL_ALGO_TWOSHOT_SENTINEL ||
                      algo == LL_ALGO_TWOSHOT_SENTINEL_OUT || algo == LL_ALGO_TWOSHOT_SENTINEL_WAVES ||
                      algo == LL_ALGO_ONESHOT_SENTINEL_WAVES);
-  const bool waves = (algo == LL_ALGO_ONESHOT_WAVES || algo == LL_ALGO_ONESHOT_SENTINEL_WAVES);
+  const bool waves = (algo == LL_ALGO_ONESHOT_WAVES || algo == LL_ALGO_ONESHOT_SENTINEL_WAVES ||
+                      algo == LL_ALGO_ONESHOT_LINE_WAVES);
   pl->proto = line ? PR_LINE : (sent ? PR_SENT : PR_LL);
   pl->a.area = area_of(pl->proto);
   if (algo == LL_ALGO_ONESHOT || algo == LL_ALGO_ONESHOT_LINE || algo == LL_ALGO_ONESHOT_SENTINEL || waves) {
@@ -441,7 +462,8 @@ void plan_allreduce(Plan *pl, ll_algo algo, uint64_t count, int es, int nranks, 
     pl->units = units_of(pl->proto, it_bytes);
   } else {
     pl->kind = algo == LL_ALGO_TWOSHOT_SENTINEL_OUT ? K_TWOSHOT_OUT : K_TWOSHOT;
-    if (algo == LL_ALGO_TWOSHOT_WAVES || algo == LL_ALGO_TWOSHOT_SENTINEL_WAVES) pl->kind = K_TWOSHOT_WAVES;
+    if (algo == LL_ALGO_TWOSHOT_WAVES || algo == LL_ALGO_TWOSHOT_SENTINEL_WAVES || algo == LL_ALGO_TWOSHOT_LINE_WAVES)
+      pl->kind = K_TWOSHOT_WAVES;
     const uint64_t C = L::twoshot_chunk(iter_count, nranks, es);
     pl->a.chunk = (int64_t)C;
     pl->a.slot = slot_bytes(pl->proto, C * es);
@@ -545,7 +567,7 @@ int ll_allreduce_algo(void *sym_base, size_t rank_stride, void *out, size_t coun
   if (st != LL_OK) return st;
   st = check_dtype_op((int)dt, (int)op);
   if (st != LL_OK) return st;
-  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_ONESHOT_SENTINEL_WAVES) return LL_ERR_INVALID;
+  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_TWOSHOT_LINE_WAVES) return LL_ERR_INVALID;
   const int es = esize_of(dt);
   const uint64_t in_bytes = (uint64_t)count * es;
   if (fills_output(algo) && in_bytes % 16 != 0) return LL_ERR_UNSUPPORTED;
@@ -634,7 +656,7 @@ int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, 
   if (epoch == 0) return LL_ERR_INVALID;
   int st = check_dtype_op((int)dt, (int)op);
   if (st != LL_OK) return st;
-  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_ONESHOT_SENTINEL_WAVES) return LL_ERR_INVALID;
+  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_TWOSHOT_LINE_WAVES) return LL_ERR_INVALID;
   if (algo == LL_ALGO_TWOSHOT_ATOMIC) return LL_ERR_UNSUPPORTED;  // single-iteration regions only
   size_t D = 0;
   st = ll_scratch_iter_bytes(scratch_stride, nranks, &D);
@@ -663,10 +685,10 @@ int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, 
       if (iters > 1 && algo == LL_ALGO_TWOSHOT_WAVES) algo = LL_ALGO_TWOSHOT;
       if (iters > 1 && algo == LL_ALGO_TWOSHOT_SENTINEL_WAVES) algo = LL_ALGO_TWOSHOT_SENTINEL;
       if (iters > 1 && algo == LL_ALGO_ONESHOT_SENTINEL_WAVES) algo = LL_ALGO_ONESHOT_SENTINEL;
+      if (iters > 1 && algo == LL_ALGO_TWOSHOT_LINE_WAVES) algo = LL_ALGO_TWOSHOT_LINE;
     }
   }
-  if (iters > 1 && (algo == LL_ALGO_ONESHOT_WAVES || algo == LL_ALGO_TWOSHOT_WAVES ||
-                    algo == LL_ALGO_TWOSHOT_SENTINEL_WAVES || algo == LL_ALGO_ONESHOT_SENTINEL_WAVES))
+  if (iters > 1 && is_wave_algo(algo))
     return LL_ERR_UNSUPPORTED;
 
   Plan pl;

@@ -22,6 +22,7 @@ LL_ALGO_ONESHOT_WAVES = 5
 LL_ALGO_ONESHOT_SENTINEL, LL_ALGO_TWOSHOT_SENTINEL, LL_ALGO_TWOSHOT_SENTINEL_OUT = 6, 7, 8
 LL_ALGO_TWOSHOT_ATOMIC = 9
 LL_ALGO_TWOSHOT_WAVES, LL_ALGO_TWOSHOT_SENTINEL_WAVES, LL_ALGO_ONESHOT_SENTINEL_WAVES = 10, 11, 12
+LL_ALGO_ONESHOT_LINE_WAVES, LL_ALGO_TWOSHOT_LINE_WAVES = 13, 14
 LL_PROTO_AUTO, LL_PROTO_PACKET8, LL_PROTO_LINE128, LL_PROTO_SENTINEL = 0, 1, 2, 3
 
 LL_OK = 0
@@ -39,6 +40,7 @@ ALGOS = {
     "twoshot_sentinel_out": LL_ALGO_TWOSHOT_SENTINEL_OUT, "twoshot_atomic": LL_ALGO_TWOSHOT_ATOMIC,
     "twoshot_waves": LL_ALGO_TWOSHOT_WAVES, "twoshot_sentinel_waves": LL_ALGO_TWOSHOT_SENTINEL_WAVES,
     "oneshot_sentinel_waves": LL_ALGO_ONESHOT_SENTINEL_WAVES,
+    "oneshot_line_waves": LL_ALGO_ONESHOT_LINE_WAVES, "twoshot_line_waves": LL_ALGO_TWOSHOT_LINE_WAVES,
 }
 PROTOS = {"auto": LL_PROTO_AUTO, "packet8": LL_PROTO_PACKET8, "line128": LL_PROTO_LINE128,
           "sentinel": LL_PROTO_SENTINEL}

@@ -64,7 +64,7 @@ def ar(count=1024, dt=F32, p=4, base=GOOD_BASE, stride=None, out=GOOD_OUT, epoch
     (dict(epoch=0), ll.LL_ERR_INVALID),
     (dict(dt=7), ll.LL_ERR_UNSUPPORTED),
     (dict(op=1), ll.LL_ERR_UNSUPPORTED),
-    (dict(algo=13), ll.LL_ERR_INVALID),
+    (dict(algo=15), ll.LL_ERR_INVALID),
     (dict(algo=9, count=1001), ll.LL_ERR_UNSUPPORTED),  # atomic two-shot: count*esize % 16 == 0
     (dict(algo=8, count=1001), ll.LL_ERR_UNSUPPORTED),  # direct output needs count*esize % 16 == 0
     (dict(algo=-1), ll.LL_ERR_INVALID),
@@ -139,7 +139,7 @@ def test_buffered_argument_checks():
     assert b(epoch=0)[0] == ll.LL_ERR_INVALID
     assert b(p=1)[0] == ll.LL_ERR_INVALID
     assert b(op=1)[0] == ll.LL_ERR_UNSUPPORTED
-    assert b(algo=13)[0] == ll.LL_ERR_INVALID
+    assert b(algo=15)[0] == ll.LL_ERR_INVALID
     assert b(algo=ll.LL_ALGO_TWOSHOT_WAVES, count=1 << 20)[0] == ll.LL_ERR_UNSUPPORTED  # one iteration only
     assert b(algo=ll.LL_ALGO_TWOSHOT_ATOMIC)[0] == ll.LL_ERR_UNSUPPORTED
     assert b(s=256)[0] == ll.LL_ERR_SCRATCH

@@ -26,7 +26,8 @@ else:  # pragma: no cover
     pytest.skip("no GPU", allow_module_level=True)
 
 AR_ALGOS = ["oneshot", "twoshot", "twoshot_line", "oneshot_line", "oneshot_waves", "oneshot_sentinel",
-            "twoshot_sentinel", "twoshot_waves", "twoshot_sentinel_waves", "oneshot_sentinel_waves", "auto"]
+            "twoshot_sentinel", "twoshot_waves", "twoshot_sentinel_waves", "oneshot_sentinel_waves",
+            "oneshot_line_waves", "twoshot_line_waves", "auto"]
 PROTOS = ["packet8", "line128", "sentinel"]
 NP = {"f32": np.uint32, "bf16": np.uint16}
 
@@ -316,8 +317,8 @@ def test_large_epochs_and_reinit():
     reg = SymRegion(p, n, "f32")
     reg.init()
     reg.write_inputs(x)
-    epochs = (0x7FFFFFFF, 0x80000000, 0xFFFFFFF2, 0xFFFFFFF4, 0xFFFFFFF6, 0xFFFFFFF8, 0xFFFFFFF9, 0xFFFFFFFA,
-              0xFFFFFFFC, 0xFFFFFFFE, 0xFFFFFFFF)
+    epochs = (0x7FFFFFFF, 0x80000000, 0xFFFFFFEE, 0xFFFFFFF0, 0xFFFFFFF2, 0xFFFFFFF4, 0xFFFFFFF6, 0xFFFFFFF8,
+              0xFFFFFFF9, 0xFFFFFFFA, 0xFFFFFFFC, 0xFFFFFFFE, 0xFFFFFFFF)
     assert len(epochs) == len(AR_ALGOS)
     for algo, e in zip(AR_ALGOS, epochs):
         check_ok(reg.allreduce(n, algo, epoch=e), f"epoch {e:#x}")
@@ -338,7 +339,8 @@ def test_count_zero_is_a_no_op():
 
 # ------------------------------------------------------------ failure handling
 @pytest.mark.parametrize("algo", ["oneshot", "twoshot_line", "oneshot_sentinel", "twoshot_sentinel", "twoshot_waves",
-                                  "twoshot_sentinel_waves", "oneshot_waves", "oneshot_sentinel_waves"])
+                                  "twoshot_sentinel_waves", "oneshot_waves", "oneshot_sentinel_waves",
+                                  "oneshot_line_waves", "twoshot_line_waves"])
 def test_missing_peer_times_out_and_is_reported(algo):
     """Rank 3 publishes nothing; its peers' bounded waits expire (after 2 ms),
     every kernel still finishes, and ll_check reports the timeout.  (In two-shot
