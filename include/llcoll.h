@@ -279,11 +279,10 @@ const char *ll_strerror(int status);
  * default; 1 = yes).  Never selects LL_ALGO_TWOSHOT_SENTINEL_OUT. */
 int ll_set_auto_sentinel(int allow);
 
-/* Kernel family of the stand-alone ReduceScatter / AllGather with 8-byte
- * packets or sentinel units: 0 = by size (one wave per peer with LDS staging
- * up to 1 MiB of data per rank at 5-8 ranks and 2 MiB below, one lane per
- * packet unit above), 1 = one lane per unit always, 2 = one wave per peer
- * always.  Results do not depend on it. */
+/* Kernel family of the stand-alone ReduceScatter / AllGather: 0 = by size
+ * (one wave per peer with LDS staging up to 1-2 MiB of data per rank, one
+ * lane per packet unit above), 1 = one lane per unit always, 2 = one wave per
+ * peer always.  Results do not depend on it. */
 int ll_set_wave_kernels(int mode);
 
 /* Workgroups per rank and threads per workgroup for the following calls;

@@ -400,18 +400,17 @@ ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
 
 // ReduceScatter / AllGather, by the bytes of data per rank (input for
 // ReduceScatter, output for AllGather), measured the same way at 4 KiB ..
-// 16 MiB at 4 and 8 ranks: 8-byte packets up to 1 MiB, lines above; with
-// sentinel mode allowed, sentinel units from 128 KiB (256 KiB at 3-4 ranks,
-// where 8-byte packets stay as fast a little longer) up to 4 MiB (8 MiB at
-// 2-4 ranks).
+// 16 MiB at 4 and 8 ranks: 8-byte packets up to 256 KiB (128 KiB at 2-4
+// ranks), lines above; with sentinel mode allowed, sentinel units from 128
+// KiB up to 4 MiB.
 ll_proto auto_proto(uint64_t bytes, int P, bool sentinel_ok) {
   const uint64_t KiB = 1024, MiB = 1024 * 1024;
   if (sentinel_ok) {
-    if (bytes <= (P >= 5 ? 64 : 128) * KiB) return LL_PROTO_PACKET8;
-    if (bytes <= (P >= 5 ? 4 : 8) * MiB) return LL_PROTO_SENTINEL;
+    if (bytes <= 64 * KiB) return LL_PROTO_PACKET8;
+    if (bytes <= 4 * MiB) return LL_PROTO_SENTINEL;
     return LL_PROTO_LINE128;
   }
-  return bytes <= 1 * MiB ? LL_PROTO_PACKET8 : LL_PROTO_LINE128;
+  return bytes <= (P >= 5 ? 256 : 128) * KiB ? LL_PROTO_PACKET8 : LL_PROTO_LINE128;
 }
 
 // Broadcast / Reduce: 8-byte packets up to 64 KiB per rank, lines above, or
@@ -422,13 +421,17 @@ ll_proto auto_proto_rooted(uint64_t bytes, bool sentinel_ok) {
 }
 
 // Stand-alone ReduceScatter / AllGather: the wave-per-peer kernels serve
-// 8-byte packets and sentinel units up to 1 MiB of data per rank at 5-8
-// ranks and 2 MiB below (measured; forced on or off by ll_set_wave_kernels).
+// each format up to the size where the one-lane-per-unit kernels catch up
+// (measured at 4 and 8 ranks): 8-byte packets up to 1 MiB of data per rank
+// (2 MiB at 2-4 ranks), lines up to 2 MiB, sentinel units up to 1 MiB
+// (512 KiB at 2-4 ranks).  ll_set_wave_kernels forces either family.
 bool use_wave_kernel(ll_proto proto, uint64_t bytes, int P) {
-  if (proto == LL_PROTO_LINE128) return false;
   const int m = g_wave_kernels.load();
   if (m != 0) return m == 2;
-  return bytes <= (P >= 5 ? (1u << 20) : (2u << 20));
+  const uint64_t KiB = 1024, MiB = 1024 * 1024;
+  if (proto == LL_PROTO_LINE128) return bytes <= 2 * MiB;
+  if (proto == LL_PROTO_SENTINEL) return bytes <= (P >= 5 ? 1 * MiB : 512 * KiB);
+  return bytes <= (P >= 5 ? 1 * MiB : 2 * MiB);
 }
 
 // The wave-per-peer AllReduce kernels (single iteration only).

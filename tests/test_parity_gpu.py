@@ -659,7 +659,7 @@ def test_rooted_missing_rank_times_out(kind):
     assert_bits_equal(reg.read_out(n, np.uint32).reshape(1, n), oracle.reduce(x, 2).reshape(1, n), "after timeout")
 
 
-@pytest.mark.parametrize("proto", ["packet8", "sentinel"])
+@pytest.mark.parametrize("proto", ["packet8", "sentinel", "line128"])
 def test_rs_ag_wave_kernels_launch_shapes_and_timeouts(proto):
     """The wave-per-peer ReduceScatter / AllGather at several workgroup counts
     and units per lane, then a muted rank that makes the waits expire."""
