@@ -294,7 +294,8 @@ def bench_scratch(torch, ll, iters=10, warmup=3):
         reg.inp.view(torch.float32).copy_(torch.rand(p * n, generator=g, device="cuda") * 2 - 1)
         stream = torch.cuda.current_stream()
         row = {"iter_kib": it_kib, "scratch_slice_bytes": reg.scratch_stride}
-        for algo in ("oneshot", "oneshot_line", "oneshot_sentinel", "twoshot", "twoshot_line", "twoshot_sentinel"):
+        for algo in ("oneshot", "oneshot_line", "oneshot_sentinel", "twoshot", "twoshot_line", "twoshot_sentinel",
+                     "twoshot_waves", "twoshot_line_waves", "twoshot_sentinel_waves", "auto"):
             for _ in range(warmup):
                 ll.check(reg.allreduce(n, algo), algo)
             ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)

@@ -89,7 +89,7 @@ typedef enum {
   LL_ALGO_TWOSHOT_ATOMIC = 9,       /* two-shot with atomic accumulation (Sec. IV, "LL128
                                        Atomic"): NOT deterministic, see below */
   LL_ALGO_TWOSHOT_WAVES = 10,       /* two-shot, 8-byte packets, one wave per peer, partial
-                                       sums staged in LDS (single iteration only) */
+                                       sums staged in LDS */
   LL_ALGO_TWOSHOT_SENTINEL_WAVES = 11, /* the same with sentinel units */
   LL_ALGO_ONESHOT_SENTINEL_WAVES = 12, /* one-shot, sentinel units, one wave per peer (single
                                           iteration only) */
@@ -238,8 +238,9 @@ int ll_scratch_init(void *scratch_base, size_t scratch_stride, int nranks, void 
 /* AllReduce (sum) through a bounded scratch region.  in, out: 16-byte
  * aligned device memory, equal (in place) or disjoint, neither overlapping
  * the scratch region; scratch_base 256-byte aligned.  algo as for
- * ll_allreduce_algo (LL_ALGO_ONESHOT_WAVES only for one iteration;
- * LL_ALGO_TWOSHOT_SENTINEL_OUT not in place).  count*esize at most 16 GiB.
+ * ll_allreduce_algo (the one-shot wave-per-peer algorithms only for one
+ * iteration; LL_ALGO_TWOSHOT_SENTINEL_OUT not in place; not
+ * LL_ALGO_TWOSHOT_ATOMIC).  count*esize at most 16 GiB.
  * epochs_used may be NULL.  One kernel launch on `stream`. */
 int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, ll_op op, int nranks,
                           void *scratch_base, size_t scratch_stride, uint32_t epoch, void *stream, ll_algo algo,

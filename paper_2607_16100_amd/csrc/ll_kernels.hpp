@@ -702,25 +702,32 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
   const int lane = (int)(threadIdx.x & 63);
   const int sub = WU::sub(lane);
   const uint64_t deadline = now_ticks() + a.timeout;
-  const int64_t C = Mode == 0 ? a.chunk : a.n;
-  const int64_t n_all = Mode == 0 ? a.n : (int64_t)P * a.n;
   const bool publish = (r != a.mute);
   const bool al4 = a.al4 != 0, in_al4 = a.in_al4 != 0;
   char *const slice_r = a.sym + (uint64_t)r * a.stride;
   const char *const in_r = a.in + (uint64_t)r * a.in_stride;
+  // rank r's output: Mode 0 all n elements, Mode 1 its chunk, Mode 2 its P blocks
+  char *const out_rank = a.out + (uint64_t)r * (uint64_t)(Mode == 0 ? a.n : (Mode == 1 ? a.n : (int64_t)P * a.n)) * E;
+  // The current iteration (Mode 0 calls may run several, each through
+  // sub-buffer it % 2 with the flag epoch + it): its elements, chunk length,
+  // input, output offset, packet area and flag.
+  int64_t n_all = Mode == 0 ? a.n : (int64_t)P * a.n;
+  int64_t C = Mode == 0 ? a.chunk : a.n;
+  const char *in_it = in_r;
+  uint64_t out_off = 0;
+  uint64_t area = a.area;
+  uint32_t epoch = a.epoch;
   // where this rank's result for chunk c goes
   auto out_chunk = [&](int c) -> char * {
-    if (Mode == 1) return a.out + (uint64_t)r * (uint64_t)C * E;
-    return a.out + (uint64_t)r * (uint64_t)n_all * E + (uint64_t)c * C * E;
+    if (Mode == 1) return out_rank;
+    return out_rank + out_off + (uint64_t)c * C * E;
   };
-  auto in_chunk = [&](int c) -> const char * { return Mode == 2 ? in_r : in_r + (uint64_t)c * C * E; };
-  const uint64_t ag_area = Mode == 2 ? a.area : a.area + (uint64_t)(P - 1) * a.slot;
+  auto in_chunk = [&](int c) -> const char * { return Mode == 2 ? in_it : in_it + (uint64_t)c * C * E; };
   auto chunk_len = [&](int c) -> int64_t {
     const int64_t left = n_all - (int64_t)c * C;
     return left < 0 ? 0 : (left < C ? left : C);
   };
-  const int64_t units = Pr::units((C * E + 3) / 4);
-  const int64_t tiles = (units + WU::kPerTile - 1) / WU::kPerTile;
+  int64_t units = Pr::units((C * E + 3) / 4);
   // slot (q <- r) in peer q's slice and slot (r <- q) in this rank's slice
   const uint64_t slot_out = (uint64_t)slot_of(r, q) * a.slot, slot_in = (uint64_t)slot_of(q, r) * a.slot;
   char *const peer_slice = a.sym + (uint64_t)q * a.stride;
@@ -759,13 +766,13 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
         if (pend & (1u << k)) pk[k] = ld_pkt(rs, WU::off(WU::unit(tile, k, lane), lane));
 #pragma unroll
       for (int k = 0; k < U; ++k) {
-        if ((pend & (1u << k)) && Pr::ready(pk[k], a.epoch)) {
+        if ((pend & (1u << k)) && Pr::ready(pk[k], epoch)) {
           v[k] = Pr::unpack(pk[k], sub);
           pend &= ~(1u << k);
         }
       }
       if (pend != 0 && (spins++ & 15) == 0 && now_ticks() > deadline) {
-        report_timeout(r, 1u << q, a.epoch);
+        report_timeout(r, 1u << q, epoch);
         break;
       }
     }
@@ -777,78 +784,94 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
     }
   };
 
-  for (int64_t tile = pt.w; tile < tiles; tile += pt.W) {
-    u32x4 res[U];
-    if constexpr (kRS) {
-      // ---- ReduceScatter of this tile
-      if (q == r) {
-        u32x4 own[U];
+  const uint32_t iters = Mode == 0 ? a.iters : 1u;
+  for (uint32_t it = 0; it < iters; ++it) {
+    if (Mode == 0 && iters > 1) {
+      const int64_t e0 = (int64_t)it * a.iter_n;
+      n_all = a.n - e0 < a.iter_n ? a.n - e0 : a.iter_n;
+      C = chunk_of<P, E>(n_all);
+      in_it = in_r + e0 * E;
+      out_off = (uint64_t)e0 * E;
+      area = a.area + (uint64_t)(it & 1u) * a.sub_bytes;
+      epoch = a.epoch + it;
+      units = Pr::units((C * E + 3) / 4);
+    }
+    const uint64_t ag_area = Mode == 2 ? area : area + (uint64_t)(P - 1) * a.slot;
+    const int64_t tiles = (units + WU::kPerTile - 1) / WU::kPerTile;
+    for (int64_t tile = pt.w; tile < tiles; tile += pt.W) {
+      u32x4 res[U];
+      if constexpr (kRS) {
+        // ---- ReduceScatter of this tile
+        if (q == r) {
+          u32x4 own[U];
 #pragma unroll
-        for (int k = 0; k < U; ++k) own[k] = Pr::template load<DT>(in_chunk(r), WU::unit(tile, k, lane), sub,
-                                                                  chunk_len(r), in_al4);
-        stage_row(own);
+          for (int k = 0; k < U; ++k) own[k] = Pr::template load<DT>(in_chunk(r), WU::unit(tile, k, lane), sub,
+                                                                    chunk_len(r), in_al4);
+          stage_row(own);
+        } else {
+          if (publish) {
+            const rsrc_t rd = make_rsrc(peer_slice + area + slot_out, (uint32_t)a.slot);
+#pragma unroll
+            for (int k = 0; k < U; ++k) {
+              const int64_t u = WU::unit(tile, k, lane);
+              if (u < units) {
+                const u32x4 w = Pr::template load<DT>(in_chunk(q), u, sub, chunk_len(q), in_al4);
+                st_pkt(rd, WU::off(u, lane), Pr::pack(w, epoch, sub));
+              }
+            }
+          }
+          u32x4 v[U];
+          poll_peer(slice_r + area + slot_in, tile, v);
+          stage_row(v);
+        }
+        lds_barrier();
+        // ---- the ordered sum of the tile (every wave computes the same values)
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+          uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+          for (int j = 0; j < WPU; ++j) {
+            float acc[K];
+#pragma unroll
+            for (int e = 0; e < K; ++e) acc[e] = stage[0][(k * 64 + lane) * EPU + j * K + e];
+#pragma unroll
+            for (int p = 1; p < P; ++p) {
+#pragma unroll
+              for (int e = 0; e < K; ++e) acc[e] = acc[e] + stage[p][(k * 64 + lane) * EPU + j * K + e];
+            }
+            w[j] = Elem<DT>::narrow(acc);
+          }
+          res[k] = u32x4{w[0], w[1], w[2], w[3]};
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < U; ++k) res[k] = Pr::template load<DT>(in_chunk(r), WU::unit(tile, k, lane), sub, C, in_al4);
+      }
+      // ---- AllGather of this tile
+      if (q == r || !kAG) {
+        if (q == r) {
+#pragma unroll
+          for (int k = 0; k < U; ++k)
+            Pr::template store<DT>(out_chunk(r), WU::unit(tile, k, lane), sub, chunk_len(r), al4, res[k]);
+        }
       } else {
         if (publish) {
-          const rsrc_t rd = make_rsrc(peer_slice + a.area + slot_out, (uint32_t)a.slot);
+          const rsrc_t rd = make_rsrc(peer_slice + ag_area + slot_out, (uint32_t)a.slot);
 #pragma unroll
           for (int k = 0; k < U; ++k) {
             const int64_t u = WU::unit(tile, k, lane);
-            if (u < units) {
-              const u32x4 w = Pr::template load<DT>(in_chunk(q), u, sub, chunk_len(q), in_al4);
-              st_pkt(rd, WU::off(u, lane), Pr::pack(w, a.epoch, sub));
-            }
+            if (u < units) st_pkt(rd, WU::off(u, lane), Pr::pack(res[k], epoch, sub));
           }
         }
         u32x4 v[U];
-        poll_peer(slice_r + a.area + slot_in, tile, v);
-        stage_row(v);
-      }
-      lds_barrier();
-      // ---- the ordered sum of the tile (every wave computes the same values)
-#pragma unroll
-      for (int k = 0; k < U; ++k) {
-        uint32_t w[4] = {0u, 0u, 0u, 0u};
-#pragma unroll
-        for (int j = 0; j < WPU; ++j) {
-          float acc[K];
-#pragma unroll
-          for (int e = 0; e < K; ++e) acc[e] = stage[0][(k * 64 + lane) * EPU + j * K + e];
-#pragma unroll
-          for (int p = 1; p < P; ++p) {
-#pragma unroll
-            for (int e = 0; e < K; ++e) acc[e] = acc[e] + stage[p][(k * 64 + lane) * EPU + j * K + e];
-          }
-          w[j] = Elem<DT>::narrow(acc);
-        }
-        res[k] = u32x4{w[0], w[1], w[2], w[3]};
-      }
-    } else {
-#pragma unroll
-      for (int k = 0; k < U; ++k) res[k] = Pr::template load<DT>(in_chunk(r), WU::unit(tile, k, lane), sub, C, in_al4);
-    }
-    // ---- AllGather of this tile
-    if (q == r || !kAG) {
-      if (q == r) {
+        poll_peer(slice_r + ag_area + slot_in, tile, v);
 #pragma unroll
         for (int k = 0; k < U; ++k)
-          Pr::template store<DT>(out_chunk(r), WU::unit(tile, k, lane), sub, chunk_len(r), al4, res[k]);
+          Pr::template store<DT>(out_chunk(q), WU::unit(tile, k, lane), sub, chunk_len(q), al4, v[k]);
       }
-    } else {
-      if (publish) {
-        const rsrc_t rd = make_rsrc(peer_slice + ag_area + slot_out, (uint32_t)a.slot);
-#pragma unroll
-        for (int k = 0; k < U; ++k) {
-          const int64_t u = WU::unit(tile, k, lane);
-          if (u < units) st_pkt(rd, WU::off(u, lane), Pr::pack(res[k], a.epoch, sub));
-        }
-      }
-      u32x4 v[U];
-      poll_peer(slice_r + ag_area + slot_in, tile, v);
-#pragma unroll
-      for (int k = 0; k < U; ++k)
-        Pr::template store<DT>(out_chunk(q), WU::unit(tile, k, lane), sub, chunk_len(q), al4, v[k]);
+      if constexpr (kRS) lds_barrier();  // the next tile overwrites the staging rows
     }
-    if constexpr (kRS) lds_barrier();  // the next tile overwrites the staging rows
+    if (ResetsSlots<Pr>::value && it + 1 < iters) wait_vm_all();
   }
   stamp_end(a, t_start);
 }

@@ -434,10 +434,9 @@ bool use_wave_kernel(ll_proto proto, uint64_t bytes, int P) {
   return bytes <= (P >= 5 ? 1 * MiB : 2 * MiB);
 }
 
-// The wave-per-peer AllReduce kernels (single iteration only).
+// The wave-per-peer one-shot kernels run a single iteration only.
 bool is_wave_algo(ll_algo a) {
-  return a == LL_ALGO_ONESHOT_WAVES || a == LL_ALGO_ONESHOT_SENTINEL_WAVES || a == LL_ALGO_ONESHOT_LINE_WAVES ||
-         a == LL_ALGO_TWOSHOT_WAVES || a == LL_ALGO_TWOSHOT_SENTINEL_WAVES || a == LL_ALGO_TWOSHOT_LINE_WAVES;
+  return a == LL_ALGO_ONESHOT_WAVES || a == LL_ALGO_ONESHOT_SENTINEL_WAVES || a == LL_ALGO_ONESHOT_LINE_WAVES;
 }
 
 // Algorithms whose AllGather stores into the peers' sentinel-filled outputs.
@@ -677,19 +676,13 @@ int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, 
   const uint64_t iters = (count + iter_count - 1) / iter_count;
   if ((uint64_t)epoch + iters - 1 > 0xFFFFFFFFull) return LL_ERR_INVALID;
   if (algo == LL_ALGO_AUTO) {
-    // With several small iterations, two-shot pays its second exchange per
-    // iteration; one-shot lines win below 512 KiB per iteration (measured,
-    // 32 MiB at 8 ranks, the paper's scratch study shape).
-    if (iters > 1 && iter_count * es < (512u << 10)) {
-      algo = LL_ALGO_ONESHOT_LINE;
-    } else {
-      algo = auto_algo(iter_count * es, nranks, g_auto_sentinel.load() != 0);
-      if (iters > 1 && algo == LL_ALGO_ONESHOT_WAVES) algo = LL_ALGO_ONESHOT;
-      if (iters > 1 && algo == LL_ALGO_TWOSHOT_WAVES) algo = LL_ALGO_TWOSHOT;
-      if (iters > 1 && algo == LL_ALGO_TWOSHOT_SENTINEL_WAVES) algo = LL_ALGO_TWOSHOT_SENTINEL;
-      if (iters > 1 && algo == LL_ALGO_ONESHOT_SENTINEL_WAVES) algo = LL_ALGO_ONESHOT_SENTINEL;
-      if (iters > 1 && algo == LL_ALGO_TWOSHOT_LINE_WAVES) algo = LL_ALGO_TWOSHOT_LINE;
-    }
+    // by the iteration size; the one-shot wave kernels run one iteration
+    // only, and the two-shot wave kernels take their place (measured on the
+    // paper's scratch study shape, 32 MiB at 8 ranks in 256 KiB .. 32 MiB
+    // iterations)
+    algo = auto_algo(iter_count * es, nranks, g_auto_sentinel.load() != 0);
+    if (iters > 1 && algo == LL_ALGO_ONESHOT_WAVES) algo = LL_ALGO_TWOSHOT_WAVES;
+    if (iters > 1 && algo == LL_ALGO_ONESHOT_SENTINEL_WAVES) algo = LL_ALGO_TWOSHOT_SENTINEL_WAVES;
   }
   if (iters > 1 && is_wave_algo(algo))
     return LL_ERR_UNSUPPORTED;

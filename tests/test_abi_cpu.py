@@ -140,7 +140,7 @@ def test_buffered_argument_checks():
     assert b(p=1)[0] == ll.LL_ERR_INVALID
     assert b(op=1)[0] == ll.LL_ERR_UNSUPPORTED
     assert b(algo=15)[0] == ll.LL_ERR_INVALID
-    assert b(algo=ll.LL_ALGO_TWOSHOT_WAVES, count=1 << 20)[0] == ll.LL_ERR_UNSUPPORTED  # one iteration only
+    assert b(algo=ll.LL_ALGO_ONESHOT_LINE_WAVES, count=1 << 20)[0] == ll.LL_ERR_UNSUPPORTED  # one iteration only
     assert b(algo=ll.LL_ALGO_TWOSHOT_ATOMIC)[0] == ll.LL_ERR_UNSUPPORTED
     assert b(s=256)[0] == ll.LL_ERR_SCRATCH
     assert b(out=IN + 16)[0] == ll.LL_ERR_INVALID            # partial overlap of in and out

@@ -22,7 +22,7 @@ else:  # pragma: no cover
     pytest.skip("no GPU", allow_module_level=True)
 
 ALGOS = ["oneshot", "oneshot_line", "oneshot_sentinel", "twoshot", "twoshot_line", "twoshot_sentinel",
-         "twoshot_sentinel_out", "auto"]
+         "twoshot_sentinel_out", "twoshot_waves", "twoshot_sentinel_waves", "twoshot_line_waves", "auto"]
 NP = {"f32": np.uint32, "bf16": np.uint16}
 TEST_TIMEOUT_TICKS = 20_000_000
 
@@ -123,7 +123,8 @@ def test_direct_output_rejects_in_place():
     assert reg.allreduce(1024, "twoshot_sentinel_out") == ll.LL_ERR_INVALID
 
 
-@pytest.mark.parametrize("algo", ["oneshot", "twoshot_line", "oneshot_sentinel", "twoshot_sentinel"])
+@pytest.mark.parametrize("algo", ["oneshot", "twoshot_line", "oneshot_sentinel", "twoshot_sentinel", "twoshot_waves",
+                                  "twoshot_sentinel_waves", "twoshot_line_waves"])
 def test_many_iterations_small_grids(algo):
     """64 iterations with one small workgroup per rank (each lane serves many
     units per iteration) and with the automatic grid."""
@@ -162,13 +163,13 @@ def test_e4_scale_32mib_message():
     for it_bytes in (4 << 20, 1 << 20):
         reg = ScratchRegion(p, n, "f32", iter_bytes=it_bytes)
         reg.init()
-        for algo in ("oneshot_line", "twoshot_line", "twoshot_sentinel"):
+        for algo in ("oneshot_line", "twoshot_line", "twoshot_sentinel", "twoshot_line_waves", "twoshot_sentinel_waves"):
             say(f"32 MiB {algo} iterations of {it_bytes >> 10} KiB")
             assert_bits_equal(run(reg, x, algo), want, f"32 MiB {algo} {it_bytes}")
         del reg
 
 
-@pytest.mark.parametrize("algo", ["oneshot", "twoshot_sentinel"])
+@pytest.mark.parametrize("algo", ["oneshot", "twoshot_sentinel", "twoshot_line_waves", "twoshot_sentinel_waves"])
 def test_missing_peer_times_out_and_scratch_init_recovers(algo):
     p, n = 8, 8192
     reg = ScratchRegion(p, n, "f32", iter_bytes=4096)
