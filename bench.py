@@ -334,10 +334,10 @@ def bench_sweep(torch, ll, path, floor_p50_us=None):
         for k in range(1, 27):
             n = 1 << k
             steps = 2000 if n * 4 <= (1 << 20) else (200 if n * 4 <= (16 << 20) else 20)
-            for algo in ("auto", "oneshot_waves", "oneshot_sentinel_waves", "oneshot", "oneshot_line",
-                         "oneshot_sentinel", "twoshot_waves", "twoshot_sentinel_waves", "twoshot", "twoshot_line",
+            for algo in ("auto", "oneshot_waves", "oneshot_sentinel_waves", "oneshot_line_waves", "oneshot", "oneshot_line",
+                         "oneshot_sentinel", "twoshot_waves", "twoshot_sentinel_waves", "twoshot_line_waves", "twoshot", "twoshot_line",
                          "twoshot_sentinel", "twoshot_sentinel_out", "twoshot_atomic"):
-                if algo in ("oneshot_waves", "oneshot_sentinel_waves") and n * 4 > (1 << 20):
+                if algo in ("oneshot_waves", "oneshot_sentinel_waves", "oneshot_line_waves") and n * 4 > (1 << 20):
                     continue
                 if algo in ("twoshot_atomic", "twoshot_sentinel_out") and n < 4:
                     continue
