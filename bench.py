@@ -464,7 +464,44 @@ def bench_cpu_baseline(seconds: float):
     got = HEADLINE_OUTPUT.get("bits")
     if got is not None:  # the headline's last GPU result against the oracle's
         res["headline_bit_exact"] = bool(np.array_equal(got, want))
+    res["bandwidth_workload"] = bench_cpu_all_cores(seconds / 2)
     return res
+
+
+def bench_cpu_all_cores(seconds: float):
+    """The same C oracle on the 64 MiB-per-rank binary32 workload (8 ranks),
+    once on one thread and then on every host core: the elements are split
+    into contiguous column blocks, one per thread, and each block is reduced
+    by an unchanged oracle call, so the per-element order is untouched and the
+    result is bit-identical.  ctypes releases the GIL for the calls."""
+    import oracle
+    from concurrent.futures import ThreadPoolExecutor
+    from paper_2607_16100_amd import workloads as wl
+
+    p, n = 8, 16 << 20
+    x = wl.uniform(p, n, "f32", seed=0)
+    t0 = time.perf_counter()
+    one = oracle.allreduce(x)
+    t_one = time.perf_counter() - t0
+    cores = max(1, min(16, len(os.sched_getaffinity(0))))
+    edges = [(n * i // cores) // 64 * 64 for i in range(cores)] + [n]
+    blocks = [np.ascontiguousarray(x[:, edges[i]:edges[i + 1]]) for i in range(cores)]
+    del x
+    times, outs = [], None
+    with ThreadPoolExecutor(max_workers=cores) as pool:
+        t_end = time.perf_counter() + seconds
+        while time.perf_counter() < t_end or not times:
+            t0 = time.perf_counter()
+            outs = list(pool.map(oracle.allreduce, blocks))
+            times.append(time.perf_counter() - t0)
+    same = all(np.array_equal(outs[i], one[:, edges[i]:edges[i + 1]]) for i in range(cores))
+    med = float(np.median(times))
+    traffic = (p * n * 4 + n * 4) / 1e9  # every input read once, one output row written
+    return {"bytes_per_rank": n * 4, "one_core_us": t_one * 1e6, "one_core_gbps": traffic / t_one,
+            "all_cores_us": med * 1e6, "all_cores_gbps": traffic / med, "cores": cores,
+            "calls": len(times), "bit_identical": bool(same),
+            "sample": "8 ranks x 16 Mi binary32 uniform[-1,1); one single-threaded call, then the median "
+                      "of repeated calls split into one contiguous column block per core"}
 
 
 def traffic_from_profiles(kernel_hash: str, grid_threads: int):
