@@ -532,8 +532,8 @@ def main():
     ap.add_argument("--sweep", default="", help="also run the full C4 size sweep, writing JSON lines to this file")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs its P virtual ranks on one GPU; --gpus {args.gpus} is not supported "
-              f"(the multi-GPU design is described but not built)", file=sys.stderr)
+        print(f"bench.py: the P virtual ranks share one GPU; --gpus {args.gpus} is not supported "
+              f"(only one GPU is used; sharding over several GPUs is a design, not code)", file=sys.stderr)
         sys.exit(2)
     only = set(x for x in args.only.split(",") if x)
 

@@ -101,7 +101,10 @@ template <> struct Elem<1> {  // bfloat16
 // elements are moved one at a time.
 // Inputs are read once and outputs written once per call: load and store them
 // with the streaming (non-temporal) hint so they do not displace the packets,
-// which are read back soon after they are written.
+// which are read back soon after they are written.  A kernel whose waves all
+// read the same input words (the one-wave-per-peer one-shot) loads them
+// through the cache instead (NT = false), so that the waves share one memory
+// read.
 #ifndef LLCOLL_NT_IN
 #define LLCOLL_NT_IN 1
 #endif
@@ -109,16 +112,17 @@ template <> struct Elem<1> {  // bfloat16
 #define LLCOLL_NT_OUT 1
 #endif
 
-template <int DT>
+template <int DT, bool NT = true>
 __device__ __forceinline__ u32x4 load_words(const char *base, int64_t w0, int cnt, int64_t nelem, bool al4) {
   constexpr int K = Elem<DT>::kPerWord;
+  constexpr bool kNT = LLCOLL_NT_IN && NT;
   u32x4 v = {0u, 0u, 0u, 0u};
   const int64_t e0 = w0 * K;
   if (al4 && e0 + (int64_t)cnt * K <= nelem) {
     const char *p = base + w0 * 4;
-    if (LLCOLL_NT_IN && cnt == 4 && ((uintptr_t)p & 15) == 0) {
+    if (kNT && cnt == 4 && ((uintptr_t)p & 15) == 0) {
       v = __builtin_nontemporal_load((const u32x4 *)p);
-    } else if (LLCOLL_NT_IN && cnt == 2 && ((uintptr_t)p & 7) == 0) {
+    } else if (kNT && cnt == 2 && ((uintptr_t)p & 7) == 0) {
       const u32x2 t = __builtin_nontemporal_load((const u32x2 *)p);
       v.x = t.x;
       v.y = t.y;
@@ -207,9 +211,9 @@ struct ProtoLL {
   static constexpr int kUnitBytes = 16;   // packet bytes per unit in a slot
   static constexpr int kUnitWords = 2;    // payload words per unit
   static constexpr int kMaxWords = 2;     // payload words per lane
-  template <int DT>
+  template <int DT, bool NT = true>
   __device__ static __forceinline__ u32x4 load(const char *base, int64_t u, int /*sub*/, int64_t nelem, bool al4) {
-    return load_words<DT>(base, 2 * u, 2, nelem, al4);
+    return load_words<DT, NT>(base, 2 * u, 2, nelem, al4);
   }
   template <int DT>
   __device__ static __forceinline__ void store(char *base, int64_t u, int /*sub*/, int64_t nelem, bool al4, u32x4 w) {
@@ -252,11 +256,11 @@ struct ProtoLine {
     return (uint32_t)__builtin_amdgcn_ds_bpermute(src * 4, (int)v);
   }
   // Called with the whole wave active (a unit is one wave).
-  template <int DT>
+  template <int DT, bool NT = true>
   __device__ static __forceinline__ u32x4 load(const char *base, int64_t u, int sub, int64_t nelem, bool al4) {
     const int64_t w0 = 240 * u;
     u32x4 v = {0u, 0u, 0u, 0u};
-    if (sub < 60) v = load_words<DT>(base, w0 + 4 * sub, 4, nelem, al4);
+    if (sub < 60) v = load_words<DT, NT>(base, w0 + 4 * sub, 4, nelem, al4);
     // extra lane 60+i collects the last word of the flag lanes of quads 4i..4i+3
     const int i = (sub - 60) & 3;
     const uint32_t d0 = from_lane(16 * i + 3, v.w);
@@ -321,9 +325,9 @@ struct ProtoSent {
   static constexpr int kMaxWords = 4;
   static constexpr bool kReset = true;
   static constexpr uint32_t kSentinel = 0xFFFFFFFFu;
-  template <int DT>
+  template <int DT, bool NT = true>
   __device__ static __forceinline__ u32x4 load(const char *base, int64_t u, int /*sub*/, int64_t nelem, bool al4) {
-    return load_words<DT>(base, 4 * u, 4, nelem, al4);
+    return load_words<DT, NT>(base, 4 * u, 4, nelem, al4);
   }
   template <int DT>
   __device__ static __forceinline__ void store(char *base, int64_t u, int /*sub*/, int64_t nelem, bool al4, u32x4 w) {

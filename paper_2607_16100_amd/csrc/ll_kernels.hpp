@@ -375,7 +375,7 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
 #pragma unroll
     for (int k = 0; k < U; ++k) {
       const int64_t u = WU::unit(tile, k, lane);
-      own[k] = u < units ? Pr::template load<DT>(in_r, u, sub, n, a.in_al4 != 0) : u32x4{0u, 0u, 0u, 0u};
+      own[k] = u < units ? Pr::template load<DT, false>(in_r, u, sub, n, a.in_al4 != 0) : u32x4{0u, 0u, 0u, 0u};
     }
     if (a.phases != nullptr && lane == 0 && tile == pt.w) {
       a.phases[4 * (blockIdx.x * P + wv) + 0] = now_ticks() + (own[0].x & 0u);

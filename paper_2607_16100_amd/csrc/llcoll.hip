@@ -38,7 +38,6 @@ std::atomic<int> g_wave_units{0};  // 0 = automatic, else 1, 2 or 4
 std::atomic<int> g_lag{1};
 std::atomic<int> g_auto_sentinel{0};
 std::atomic<int> g_wave_kernels{0};
-std::atomic<int> g_probe{0};  // stand-alone RS/AG: 0 = by size, 1 = never, 2 = always
 std::atomic<uint64_t *> g_stamps{nullptr};
 std::atomic<uint64_t *> g_phases{nullptr};
 std::atomic<int> g_last_grid{0};
