@@ -53,6 +53,7 @@ struct KArgs {
   int32_t root;         // Broadcast / Reduce root rank
   uint32_t grid;        // workgroups in the launch (gridDim.x, without its memory load)
   uint32_t block;       // threads per workgroup (blockDim.x, likewise)
+  int64_t units;        // packet units of the call's stream (one-shot wave kernel)
 };
 
 // Kernel arguments live in memory and reach a wave through scalar loads.  Left
@@ -92,6 +93,7 @@ __device__ __forceinline__ KArgs pin_args(const KArgs &k) {
   a.root = in_sgpr(k.root);
   a.grid = in_sgpr(k.grid);
   a.block = in_sgpr(k.block);
+  a.units = in_sgpr(k.units);
   return a;
 }
 
@@ -326,6 +328,13 @@ struct WaveUnits {
   }
 };
 
+// Phase stamps of the wave-per-peer one-shot are compiled in only on request
+// (-DLLCOLL_WAVE_PHASES=1): every instruction on the way from kernel entry to
+// the output store adds to the call's latency.
+#ifndef LLCOLL_WAVE_PHASES
+#define LLCOLL_WAVE_PHASES 0
+#endif
+
 template <class Pr, int DT, int P, int U>
 __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
   const KArgs a = pin_args(ka);
@@ -336,30 +345,59 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
   constexpr int WPU = Pr::kMaxWords;  // payload words per lane and unit slot
   constexpr int EPU = WPU * K;        // elements per lane and unit slot
   constexpr int TW = 64 * U * WPU;    // payload words per tile
+  constexpr uint32_t kTileShift = WU::kPerTile == 1 ? 0 : (WU::kPerTile == 2 ? 1 : (WU::kPerTile == 4 ? 2 :
+                                  (WU::kPerTile == 64 ? 6 : (WU::kPerTile == 128 ? 7 : 8))));
+  static_assert((1 << kTileShift) == WU::kPerTile, "tiles hold a power-of-two number of units");
   __shared__ float stage[P][TW * K];
-  const Part pt = part_of_block<P>(a);
-  const int r = pt.r;
+  const uint32_t r = blockIdx.x % P;
+  const uint32_t w = blockIdx.x / P;
   const int wv = (int)uniform_u32(threadIdx.x >> 6);  // the same in every lane of a wave
   const int lane = (int)(threadIdx.x & 63);
   const int sub = WU::sub(lane);
-  const uint64_t deadline = now_ticks() + a.timeout;
-  char *const slice_r = a.sym + (uint64_t)r * a.stride;
   const char *const in_r = a.in + (uint64_t)r * a.in_stride;
   const int64_t n = a.n;
-  const int64_t words = (n * E + 3) / 4;
-  const int64_t units = Pr::units(words);
-  const int64_t tiles = (units + WU::kPerTile - 1) / WU::kPerTile;
-  char *const out_r = a.out + (uint64_t)r * (uint64_t)n * E;
-  const bool publish = (r != a.mute);
-  const int q = wv;  // the peer this wave talks to (q == r: the own values)
-  char *const dst = a.sym + (uint64_t)q * a.stride + a.area + (uint64_t)slot_of(r, q) * a.slot;
-  char *const src = slice_r + a.area + (uint64_t)slot_of(q, r) * a.slot;
+  // unit and tile indices fit 32 bits: a call's P-1 slots span less than 4 GiB
+  const uint32_t units = (uint32_t)a.units;
+  const bool in_al4 = a.in_al4 != 0;
 
-  // Stage a wave's U units (payload words) in its LDS row, widened to binary32.
-  auto stage_row = [&](const u32x4 *w) {
+  // The input of a tile, loaded by every wave of the workgroup.  The first
+  // tile's load is issued before the rest of the set-up below, which would
+  // otherwise stand between kernel entry and the first packet store (a wave
+  // issues at most one instruction every few cycles, and a workgroup's waves
+  // share the scalar unit).  The host launches no more workgroups per rank
+  // than there are tiles; a workgroup past the last tile (a forced launch
+  // shape) loads and stores nothing, since every access is guarded by the
+  // unit count.
+  auto load_tile = [&](uint32_t tile, u32x4 *own) {
 #pragma unroll
     for (int k = 0; k < U; ++k) {
-      const uint32_t wv4[4] = {w[k].x, w[k].y, w[k].z, w[k].w};
+      const uint32_t u = (uint32_t)WU::unit(tile, k, lane);
+      own[k] = u < units ? Pr::template load<DT, false>(in_r, u, sub, n, in_al4) : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  uint32_t tile = w;
+  u32x4 own[U];
+  load_tile(tile, own);
+
+  const uint32_t W = a.grid / P;
+  const uint32_t tiles = (units + (uint32_t)WU::kPerTile - 1u) >> kTileShift;
+  // the wait budget starts at the first timeout check, so that no clock read
+  // (a scalar memory round trip) sits on the way to the first store
+  uint64_t deadline = 0;
+  char *const out_r = a.out + (uint64_t)r * (uint64_t)n * E;
+  const bool publish = (int)r != a.mute;
+  const uint32_t q = (uint32_t)wv;  // the peer this wave talks to (q == r: the own values)
+  const uint32_t slot = (uint32_t)a.slot;
+  char *const dst = a.sym + a.area + (uint64_t)q * a.stride + (r - (r > q ? 1u : 0u)) * slot;
+  char *const src = a.sym + a.area + (uint64_t)r * a.stride + (q - (q > r ? 1u : 0u)) * slot;
+  const rsrc_t rd = make_rsrc(dst, slot);
+  const rsrc_t rs = make_rsrc(src, slot);
+
+  // Stage a wave's U units (payload words) in its LDS row, widened to binary32.
+  auto stage_row = [&](const u32x4 *v) {
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const uint32_t wv4[4] = {v[k].x, v[k].y, v[k].z, v[k].w};
 #pragma unroll
       for (int j = 0; j < WPU; ++j) {
         float f[K];
@@ -369,45 +407,48 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
       }
     }
   };
+// Diagnostics: the time of phase k of the first tile, for lane 0 of each wave.
+#define LL_WAVE_PHASE(k, expr)                                              \
+  do {                                                                      \
+    if (LLCOLL_WAVE_PHASES && a.phases != nullptr && lane == 0 && tile == w) \
+      a.phases[4 * (blockIdx.x * P + wv) + (k)] = (expr);                   \
+  } while (0)
 
-  for (int64_t tile = pt.w; tile < tiles; tile += pt.W) {
-    u32x4 own[U];
-#pragma unroll
-    for (int k = 0; k < U; ++k) {
-      const int64_t u = WU::unit(tile, k, lane);
-      own[k] = u < units ? Pr::template load<DT, false>(in_r, u, sub, n, a.in_al4 != 0) : u32x4{0u, 0u, 0u, 0u};
-    }
-    if (a.phases != nullptr && lane == 0 && tile == pt.w) {
-      a.phases[4 * (blockIdx.x * P + wv) + 0] = now_ticks() + (own[0].x & 0u);
-    }
+  while (true) {
+    LL_WAVE_PHASE(0, now_ticks() + (own[0].x & 0u));
     if (q == r) {
       stage_row(own);
-      if (a.phases != nullptr && lane == 0 && tile == pt.w) a.phases[4 * (blockIdx.x * P + wv) + 1] = now_ticks();
+      LL_WAVE_PHASE(1, now_ticks());
     } else {
+      // The packet stores are not branched around: a unit past the end (or
+      // every unit, for a muted rank) is stored at an offset past the slot,
+      // which the buffer resource discards.  A branch here would leave the
+      // input load pending on one path, and the compiler would then wait for
+      // every outstanding memory operation, this store's acknowledgement
+      // included, before the first poll.
+      constexpr uint32_t kNowhere = 0xFFFFFFF0u;
       u32x4 v[U];
-      const rsrc_t rd = make_rsrc(dst, (uint32_t)a.slot);
-      const rsrc_t rs = make_rsrc(src, (uint32_t)a.slot);
       uint32_t pend = 0;
 #pragma unroll
       for (int k = 0; k < U; ++k) {
-        const int64_t u = WU::unit(tile, k, lane);
+        const uint32_t u = (uint32_t)WU::unit(tile, k, lane);
         v[k] = u32x4{0u, 0u, 0u, 0u};
-        if (u < units) {
-          pend |= 1u << k;
-          if (publish) st_pkt(rd, WU::off(u, lane), Pr::pack(own[k], a.epoch, sub));
-        }
+        const bool valid = u < units;
+        pend |= (valid ? 1u : 0u) << k;
+        st_pkt(rd, valid && publish ? WU::off(u, lane) : kNowhere, Pr::pack(own[k], a.epoch, sub));
       }
       const uint32_t want = pend;
-      int spins = 1;
       idle64(a.first_wait);
-      while (pend != 0) {
+      // The poll loop runs while any lane of the wave still waits (a wave vote
+      // ends it), and every round re-loads all U units: the few extra loads of
+      // lanes already done cost less than per-lane branching, which would add
+      // instructions to every round.
+      uint32_t spins = 0;
+      while (true) {
         compiler_fence();
         u32x4 pk[U];
 #pragma unroll
-        for (int k = 0; k < U; ++k) {
-          const int64_t u = WU::unit(tile, k, lane);
-          if (pend & (1u << k)) pk[k] = ld_pkt(rs, WU::off(u, lane));
-        }
+        for (int k = 0; k < U; ++k) pk[k] = ld_pkt(rs, WU::off(WU::unit(tile, k, lane), lane));
 #pragma unroll
         for (int k = 0; k < U; ++k) {
           if ((pend & (1u << k)) && Pr::ready(pk[k], a.epoch)) {
@@ -415,34 +456,37 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
             pend &= ~(1u << k);
           }
         }
-        if (pend != 0 && (spins++ & 15) == 0 && now_ticks() > deadline) {
-          report_timeout(r, 1u << q, a.epoch);
-          break;
+        if (__builtin_amdgcn_ballot_w64(pend != 0) == 0) break;
+        if ((++spins & 15) == 0) {
+          const uint64_t t = now_ticks();
+          if (deadline == 0) {
+            deadline = t + a.timeout;
+          } else if (t > deadline) {
+            if (pend != 0) report_timeout((int)r, 1u << q, a.epoch);
+            break;
+          }
         }
-        if (pend != 0) idle64(a.poll_gap);
+        idle64(a.poll_gap);
       }
       if (ResetsSlots<Pr>::value) {
         const u32x4 sent = {ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel};
 #pragma unroll
         for (int k = 0; k < U; ++k) {
-          const int64_t u = WU::unit(tile, k, lane);
-          if (want & (1u << k)) st_pkt(rs, WU::off(u, lane), sent);
+          if (want & (1u << k)) st_pkt(rs, WU::off(WU::unit(tile, k, lane), lane), sent);
         }
       }
-      if (a.phases != nullptr && lane == 0 && tile == pt.w) {
-        a.phases[4 * (blockIdx.x * P + wv) + 1] = now_ticks() + (v[0].x & 0u);
-      }
+      LL_WAVE_PHASE(1, now_ticks() + (v[0].x & 0u));
       stage_row(v);
     }
     lds_barrier();
-    if (a.phases != nullptr && lane == 0 && tile == pt.w) a.phases[4 * (blockIdx.x * P + wv) + 2] = now_ticks();
+    LL_WAVE_PHASE(2, now_ticks());
     if constexpr (WU::kWave) {
       // line units are in packet order: the own-rank wave sums its lanes'
       // words and stores whole units (the store puts displaced words back)
       if (q == r) {
 #pragma unroll
         for (int k = 0; k < U; ++k) {
-          uint32_t w[4] = {0u, 0u, 0u, 0u};
+          uint32_t o[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
           for (int j = 0; j < WPU; ++j) {
             float acc[K];
@@ -453,9 +497,9 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
 #pragma unroll
               for (int e = 0; e < K; ++e) acc[e] = acc[e] + stage[p][(k * 64 + lane) * EPU + j * K + e];
             }
-            w[j] = Elem<DT>::narrow(acc);
+            o[j] = Elem<DT>::narrow(acc);
           }
-          Pr::template store<DT>(out_r, WU::unit(tile, k, lane), sub, n, a.al4 != 0, u32x4{w[0], w[1], w[2], w[3]});
+          Pr::template store<DT>(out_r, WU::unit(tile, k, lane), sub, n, a.al4 != 0, u32x4{o[0], o[1], o[2], o[3]});
         }
       }
     } else {
@@ -469,13 +513,17 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
           for (int e = 0; e < K; ++e) acc[e] = acc[e] + stage[p][j * K + e];
         }
         const u32x4 res = {Elem<DT>::narrow(acc), 0u, 0u, 0u};
-        store_words<DT>(out_r, tile * TW + j, 1, n, a.al4 != 0, res);
+        store_words<DT>(out_r, (int64_t)tile * TW + j, 1, n, a.al4 != 0, res);
       }
     }
+    tile += W;
+    if (tile >= tiles) break;
     lds_barrier();  // the next tile overwrites the staging rows
+    load_tile(tile, own);
   }
   stamp_end(a, t_start);
 }
+#undef LL_WAVE_PHASE
 
 // ---------------------------------------------------------------------------
 // Two-shot AllReduce (Sec. III-A): ReduceScatter then AllGather, fused in one

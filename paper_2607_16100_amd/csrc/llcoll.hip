@@ -308,6 +308,7 @@ int launch(const Plan &pl, void *stream) {
   a.lag = (uint32_t)g_lag.load();
   a.grid = (uint32_t)grid;
   a.block = (uint32_t)threads;
+  a.units = pl.units;
   a.stamps = g_stamps.exchange(nullptr);
   a.phases = g_phases.exchange(nullptr);
   hipLaunchKernelGGL(fn, dim3(grid), dim3(threads), 0, (hipStream_t)stream, a);
