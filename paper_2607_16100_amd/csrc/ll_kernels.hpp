@@ -379,19 +379,34 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
   u32x4 own[U];
   load_tile(tile, own);
 
+  // Then the tile's packet stores, again ahead of the set-up the polls and
+  // the reduction need.  Every wave stores (the own-rank wave and, for a muted
+  // rank, every wave, at an offset past the slot, which the buffer resource
+  // discards), and no store is branched around: a branch would leave the
+  // input load pending on one path, and the compiler would then wait for
+  // every outstanding memory operation, this store's acknowledgement
+  // included, before the first poll.
+  constexpr uint32_t kNowhere = 0xFFFFFFF0u;
+  const uint32_t q = (uint32_t)wv;  // the peer this wave talks to (q == r: the own values)
+  const uint32_t slot = (uint32_t)a.slot;
+  const bool publish = (int)r != a.mute && q != r;
+  const rsrc_t rd = make_rsrc(a.sym + a.area + (uint64_t)q * a.stride + (r - (r > q ? 1u : 0u)) * slot, slot);
+  auto store_tile = [&](uint32_t tile, const u32x4 *own) {
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const uint32_t u = (uint32_t)WU::unit(tile, k, lane);
+      st_pkt(rd, u < units && publish ? WU::off(u, lane) : kNowhere, Pr::pack(own[k], a.epoch, sub));
+    }
+  };
+  store_tile(tile, own);
+
   const uint32_t W = a.grid / P;
   const uint32_t tiles = (units + (uint32_t)WU::kPerTile - 1u) >> kTileShift;
   // the wait budget starts at the first timeout check, so that no clock read
   // (a scalar memory round trip) sits on the way to the first store
   uint64_t deadline = 0;
   char *const out_r = a.out + (uint64_t)r * (uint64_t)n * E;
-  const bool publish = (int)r != a.mute;
-  const uint32_t q = (uint32_t)wv;  // the peer this wave talks to (q == r: the own values)
-  const uint32_t slot = (uint32_t)a.slot;
-  char *const dst = a.sym + a.area + (uint64_t)q * a.stride + (r - (r > q ? 1u : 0u)) * slot;
-  char *const src = a.sym + a.area + (uint64_t)r * a.stride + (q - (q > r ? 1u : 0u)) * slot;
-  const rsrc_t rd = make_rsrc(dst, slot);
-  const rsrc_t rs = make_rsrc(src, slot);
+  const rsrc_t rs = make_rsrc(a.sym + a.area + (uint64_t)r * a.stride + (q - (q > r ? 1u : 0u)) * slot, slot);
 
   // Stage a wave's U units (payload words) in its LDS row, widened to binary32.
   auto stage_row = [&](const u32x4 *v) {
@@ -420,22 +435,12 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
       stage_row(own);
       LL_WAVE_PHASE(1, now_ticks());
     } else {
-      // The packet stores are not branched around: a unit past the end (or
-      // every unit, for a muted rank) is stored at an offset past the slot,
-      // which the buffer resource discards.  A branch here would leave the
-      // input load pending on one path, and the compiler would then wait for
-      // every outstanding memory operation, this store's acknowledgement
-      // included, before the first poll.
-      constexpr uint32_t kNowhere = 0xFFFFFFF0u;
       u32x4 v[U];
       uint32_t pend = 0;
 #pragma unroll
       for (int k = 0; k < U; ++k) {
-        const uint32_t u = (uint32_t)WU::unit(tile, k, lane);
         v[k] = u32x4{0u, 0u, 0u, 0u};
-        const bool valid = u < units;
-        pend |= (valid ? 1u : 0u) << k;
-        st_pkt(rd, valid && publish ? WU::off(u, lane) : kNowhere, Pr::pack(own[k], a.epoch, sub));
+        pend |= ((uint32_t)WU::unit(tile, k, lane) < units ? 1u : 0u) << k;
       }
       const uint32_t want = pend;
       idle64(a.first_wait);
@@ -520,6 +525,7 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
     if (tile >= tiles) break;
     lds_barrier();  // the next tile overwrites the staging rows
     load_tile(tile, own);
+    store_tile(tile, own);
   }
   stamp_end(a, t_start);
 }
