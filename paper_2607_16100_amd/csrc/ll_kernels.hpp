@@ -749,47 +749,84 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
   constexpr int WPU = Pr::kMaxWords;  // payload words per lane and unit slot
   constexpr int EPU = WPU * K;        // elements per lane and unit slot
   constexpr bool kRS = Mode != 2, kAG = Mode != 1;
+  constexpr uint32_t kNowhere = 0xFFFFFFF0u;  // past every slot: the buffer resource discards the store
   __shared__ float stage[kRS ? P : 1][64 * U * EPU];
-  const Part pt = part_of_block<P>(a);
-  const int r = pt.r;
-  const int q = (int)uniform_u32(threadIdx.x >> 6);  // this wave's peer (q == r: the own values)
+  const uint32_t r = blockIdx.x % P;
+  const uint32_t w = blockIdx.x / P;
+  const uint32_t q = (uint32_t)uniform_u32(threadIdx.x >> 6);  // this wave's peer (q == r: the own values)
   const int lane = (int)(threadIdx.x & 63);
   const int sub = WU::sub(lane);
-  const uint64_t deadline = now_ticks() + a.timeout;
-  const bool publish = (r != a.mute);
-  const bool al4 = a.al4 != 0, in_al4 = a.in_al4 != 0;
-  char *const slice_r = a.sym + (uint64_t)r * a.stride;
+  const bool in_al4 = a.in_al4 != 0;
   const char *const in_r = a.in + (uint64_t)r * a.in_stride;
-  // rank r's output: Mode 0 all n elements, Mode 1 its chunk, Mode 2 its P blocks
-  char *const out_rank = a.out + (uint64_t)r * (uint64_t)(Mode == 0 ? a.n : (Mode == 1 ? a.n : (int64_t)P * a.n)) * E;
+  const uint32_t slot = (uint32_t)a.slot;
   // The current iteration (Mode 0 calls may run several, each through
   // sub-buffer it % 2 with the flag epoch + it): its elements, chunk length,
   // input, output offset, packet area and flag.
   int64_t n_all = Mode == 0 ? a.n : (int64_t)P * a.n;
   int64_t C = Mode == 0 ? a.chunk : a.n;
   const char *in_it = in_r;
-  uint64_t out_off = 0;
   uint64_t area = a.area;
   uint32_t epoch = a.epoch;
-  // where this rank's result for chunk c goes
-  auto out_chunk = [&](int c) -> char * {
-    if (Mode == 1) return out_rank;
-    return out_rank + out_off + (uint64_t)c * C * E;
-  };
-  auto in_chunk = [&](int c) -> const char * { return Mode == 2 ? in_it : in_it + (uint64_t)c * C * E; };
-  auto chunk_len = [&](int c) -> int64_t {
+  auto in_chunk = [&](uint32_t c) -> const char * { return Mode == 2 ? in_it : in_it + (uint64_t)c * C * E; };
+  auto chunk_len = [&](uint32_t c) -> int64_t {
     const int64_t left = n_all - (int64_t)c * C;
     return left < 0 ? 0 : (left < C ? left : C);
   };
-  int64_t units = Pr::units((C * E + 3) / 4);
-  // slot (q <- r) in peer q's slice and slot (r <- q) in this rank's slice
-  const uint64_t slot_out = (uint64_t)slot_of(r, q) * a.slot, slot_in = (uint64_t)slot_of(q, r) * a.slot;
-  char *const peer_slice = a.sym + (uint64_t)q * a.stride;
-
-  auto stage_row = [&](const u32x4 *w) {
+  // unit and tile indices fit 32 bits: a call's slots span less than 4 GiB
+  uint32_t units = (uint32_t)Pr::units((C * E + 3) / 4);
+  // Every packet store is issued, at an offset past the slot when there is
+  // nothing to send (the own rank, a unit past the end, a muted rank), and no
+  // store is branched around: a branch would leave the input load pending on
+  // one path, and the compiler would then wait for every outstanding memory
+  // operation, the store's acknowledgement included, before the next poll.
+  const bool publish = (int)r != a.mute && q != r;
+  auto store_units = [&](char *dst, uint32_t tile, const u32x4 *v) {
+    const rsrc_t rd = make_rsrc(dst, slot);
 #pragma unroll
     for (int k = 0; k < U; ++k) {
-      const uint32_t wv[4] = {w[k].x, w[k].y, w[k].z, w[k].w};
+      const uint32_t u = (uint32_t)WU::unit(tile, k, lane);
+      st_pkt(rd, u < units && publish ? WU::off(u, lane) : kNowhere, Pr::pack(v[k], epoch, sub));
+    }
+  };
+  // slot (q <- r) in peer q's slice and slot (r <- q) in this rank's slice
+  char *const slot_out = a.sym + (uint64_t)q * a.stride + (r - (r > q ? 1u : 0u)) * slot;
+  char *const slot_in = a.sym + (uint64_t)r * a.stride + (q - (q > r ? 1u : 0u)) * slot;
+  const uint64_t ag_off = Mode == 2 ? 0 : (uint64_t)(P - 1) * slot;  // AllGather slots follow the RS slots
+
+  // The first step of the first tile goes out before the rest of the set-up:
+  // each wave loads the tile of chunk q (Mode 2: of its own input) and sends
+  // it to peer q, the ReduceScatter packets (Mode 2: the AllGather packets).
+  // The host launches no more workgroups per rank than there are tiles; a
+  // workgroup past the last tile (a forced launch shape) loads and stores
+  // nothing, since every access is guarded by the unit count.
+  auto load_units = [&](const char *src, int64_t len, uint32_t tile, u32x4 *v) {
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const uint32_t u = (uint32_t)WU::unit(tile, k, lane);
+      v[k] = u < units ? Pr::template load<DT>(src, u, sub, len, in_al4) : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  u32x4 first[U];
+  load_units(in_chunk(Mode == 2 ? r : q), chunk_len(Mode == 2 ? r : q), w, first);
+  store_units(slot_out + area + (Mode == 2 ? ag_off : 0), w, first);
+
+  const bool al4 = a.al4 != 0;
+  // the wait budget starts at the first timeout check, so that no clock read
+  // (a scalar memory round trip) sits on the way to the first store
+  uint64_t deadline = 0;
+  // rank r's output: Mode 0 all n elements, Mode 1 its chunk, Mode 2 its P blocks
+  char *const out_rank = a.out + (uint64_t)r * (uint64_t)(Mode == 2 ? (int64_t)P * a.n : a.n) * E;
+  uint64_t out_off = 0;
+  // where this rank's result for chunk c goes
+  auto out_chunk = [&](uint32_t c) -> char * {
+    if (Mode == 1) return out_rank;
+    return out_rank + out_off + (uint64_t)c * C * E;
+  };
+
+  auto stage_row = [&](const u32x4 *v) {
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      const uint32_t wv[4] = {v[k].x, v[k].y, v[k].z, v[k].w};
 #pragma unroll
       for (int j = 0; j < WPU; ++j) {
         float f[K];
@@ -801,23 +838,24 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
   };
 
   // Poll U units of slot `src` (this rank's slice) from peer q; sentinel
-  // units are given back to the sentinel once read.
-  auto poll_peer = [&](char *src, int64_t tile, u32x4 *v) {
-    const rsrc_t rs = make_rsrc(src, (uint32_t)a.slot);
+  // units are given back to the sentinel once read.  The loop runs while any
+  // lane of the wave still waits (a wave vote ends it) and re-loads every
+  // unit each round.
+  auto poll_peer = [&](char *src, uint32_t tile, u32x4 *v) {
+    const rsrc_t rs = make_rsrc(src, slot);
     uint32_t pend = 0;
 #pragma unroll
     for (int k = 0; k < U; ++k) {
       v[k] = u32x4{0u, 0u, 0u, 0u};
-      if (WU::unit(tile, k, lane) < units) pend |= 1u << k;
+      pend |= ((uint32_t)WU::unit(tile, k, lane) < units ? 1u : 0u) << k;
     }
     const uint32_t want = pend;
-    int spins = 1;
-    while (pend != 0) {
+    uint32_t spins = 0;
+    while (true) {
       compiler_fence();
       u32x4 pk[U];
 #pragma unroll
-      for (int k = 0; k < U; ++k)
-        if (pend & (1u << k)) pk[k] = ld_pkt(rs, WU::off(WU::unit(tile, k, lane), lane));
+      for (int k = 0; k < U; ++k) pk[k] = ld_pkt(rs, WU::off(WU::unit(tile, k, lane), lane));
 #pragma unroll
       for (int k = 0; k < U; ++k) {
         if ((pend & (1u << k)) && Pr::ready(pk[k], epoch)) {
@@ -825,9 +863,15 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
           pend &= ~(1u << k);
         }
       }
-      if (pend != 0 && (spins++ & 15) == 0 && now_ticks() > deadline) {
-        report_timeout(r, 1u << q, epoch);
-        break;
+      if (__builtin_amdgcn_ballot_w64(pend != 0) == 0) break;
+      if ((++spins & 15) == 0) {
+        const uint64_t t = now_ticks();
+        if (deadline == 0) {
+          deadline = t + a.timeout;
+        } else if (t > deadline) {
+          if (pend != 0) report_timeout((int)r, 1u << q, epoch);
+          break;
+        }
       }
     }
     if (ResetsSlots<Pr>::value) {
@@ -839,8 +883,9 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
   };
 
   const uint32_t iters = Mode == 0 ? a.iters : 1u;
+  const uint32_t W = a.grid / P;
   for (uint32_t it = 0; it < iters; ++it) {
-    if (Mode == 0 && iters > 1) {
+    if (Mode == 0 && it > 0) {
       const int64_t e0 = (int64_t)it * a.iter_n;
       n_all = a.n - e0 < a.iter_n ? a.n - e0 : a.iter_n;
       C = chunk_of<P, E>(n_all);
@@ -848,41 +893,35 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
       out_off = (uint64_t)e0 * E;
       area = a.area + (uint64_t)(it & 1u) * a.sub_bytes;
       epoch = a.epoch + it;
-      units = Pr::units((C * E + 3) / 4);
+      units = (uint32_t)Pr::units((C * E + 3) / 4);
     }
-    const uint64_t ag_area = Mode == 2 ? area : area + (uint64_t)(P - 1) * a.slot;
-    const int64_t tiles = (units + WU::kPerTile - 1) / WU::kPerTile;
-    for (int64_t tile = pt.w; tile < tiles; tile += pt.W) {
+    const uint32_t tiles = (uint32_t)((units + WU::kPerTile - 1) / WU::kPerTile);
+    for (uint32_t tile = w; tile < tiles; tile += W) {
+      const bool sent_already = it == 0 && tile == w;  // the first step of the first tile went out above
       u32x4 res[U];
       if constexpr (kRS) {
-        // ---- ReduceScatter of this tile
-        if (q == r) {
-          u32x4 own[U];
+        // ---- ReduceScatter of this tile: wave q sends chunk q's tile to
+        // peer q (above, for the first tile), then polls what peer q sent
+        u32x4 mine[U];
+        if (sent_already) {
 #pragma unroll
-          for (int k = 0; k < U; ++k) own[k] = Pr::template load<DT>(in_chunk(r), WU::unit(tile, k, lane), sub,
-                                                                    chunk_len(r), in_al4);
-          stage_row(own);
+          for (int k = 0; k < U; ++k) mine[k] = first[k];
         } else {
-          if (publish) {
-            const rsrc_t rd = make_rsrc(peer_slice + area + slot_out, (uint32_t)a.slot);
-#pragma unroll
-            for (int k = 0; k < U; ++k) {
-              const int64_t u = WU::unit(tile, k, lane);
-              if (u < units) {
-                const u32x4 w = Pr::template load<DT>(in_chunk(q), u, sub, chunk_len(q), in_al4);
-                st_pkt(rd, WU::off(u, lane), Pr::pack(w, epoch, sub));
-              }
-            }
-          }
+          load_units(in_chunk(q), chunk_len(q), tile, mine);
+          store_units(slot_out + area, tile, mine);
+        }
+        if (q == r) {
+          stage_row(mine);
+        } else {
           u32x4 v[U];
-          poll_peer(slice_r + area + slot_in, tile, v);
+          poll_peer(slot_in + area, tile, v);
           stage_row(v);
         }
         lds_barrier();
         // ---- the ordered sum of the tile (every wave computes the same values)
 #pragma unroll
         for (int k = 0; k < U; ++k) {
-          uint32_t w[4] = {0u, 0u, 0u, 0u};
+          uint32_t o[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
           for (int j = 0; j < WPU; ++j) {
             float acc[K];
@@ -893,35 +932,40 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
 #pragma unroll
               for (int e = 0; e < K; ++e) acc[e] = acc[e] + stage[p][(k * 64 + lane) * EPU + j * K + e];
             }
-            w[j] = Elem<DT>::narrow(acc);
+            o[j] = Elem<DT>::narrow(acc);
           }
-          res[k] = u32x4{w[0], w[1], w[2], w[3]};
+          res[k] = u32x4{o[0], o[1], o[2], o[3]};
         }
       } else {
+        if (sent_already) {
 #pragma unroll
-        for (int k = 0; k < U; ++k) res[k] = Pr::template load<DT>(in_chunk(r), WU::unit(tile, k, lane), sub, C, in_al4);
+          for (int k = 0; k < U; ++k) res[k] = first[k];
+        } else {
+          load_units(in_chunk(r), C, tile, res);
+        }
       }
-      // ---- AllGather of this tile
-      if (q == r || !kAG) {
+      // ---- AllGather of this tile: wave q sends the reduced tile to peer q
+      // (Mode 2: above, for the first tile) and stores what peer q sent; the
+      // own-rank wave stores the rank's own result
+      if constexpr (kAG) {
+        if (!(Mode == 2 && sent_already)) store_units(slot_out + area + ag_off, tile, res);
+        if (q == r) {
+#pragma unroll
+          for (int k = 0; k < U; ++k)
+            Pr::template store<DT>(out_chunk(r), WU::unit(tile, k, lane), sub, chunk_len(r), al4, res[k]);
+        } else {
+          u32x4 v[U];
+          poll_peer(slot_in + area + ag_off, tile, v);
+#pragma unroll
+          for (int k = 0; k < U; ++k)
+            Pr::template store<DT>(out_chunk(q), WU::unit(tile, k, lane), sub, chunk_len(q), al4, v[k]);
+        }
+      } else {
         if (q == r) {
 #pragma unroll
           for (int k = 0; k < U; ++k)
             Pr::template store<DT>(out_chunk(r), WU::unit(tile, k, lane), sub, chunk_len(r), al4, res[k]);
         }
-      } else {
-        if (publish) {
-          const rsrc_t rd = make_rsrc(peer_slice + ag_area + slot_out, (uint32_t)a.slot);
-#pragma unroll
-          for (int k = 0; k < U; ++k) {
-            const int64_t u = WU::unit(tile, k, lane);
-            if (u < units) st_pkt(rd, WU::off(u, lane), Pr::pack(res[k], epoch, sub));
-          }
-        }
-        u32x4 v[U];
-        poll_peer(slice_r + ag_area + slot_in, tile, v);
-#pragma unroll
-        for (int k = 0; k < U; ++k)
-          Pr::template store<DT>(out_chunk(q), WU::unit(tile, k, lane), sub, chunk_len(q), al4, v[k]);
       }
       if constexpr (kRS) lds_barrier();  // the next tile overwrites the staging rows
     }
