@@ -365,52 +365,47 @@ KArgs base_args(void *sym_base, size_t rank_stride, void *out, uint32_t epoch) {
   return a;
 }
 
-// Size thresholds measured on MI355X (mean time of back-to-back calls of
-// every algorithm at 4 KiB .. 64 MiB per rank, P = 2, 4, 8, binary32 and
-// bfloat16; both element types cross over at the same byte sizes);
-// M = input bytes per rank.  Flags only unless the caller allows sentinel
-// mode, which wins for mid sizes, as the paper observes for larger messages
-// and rank counts.
+// Size thresholds measured on MI355X (p50 of back-to-back calls of every
+// algorithm at 1 KiB .. 8 MiB per rank, P = 2, 4, 8, bfloat16; binary32
+// crosses over at the same byte sizes); M = input bytes per rank.  Flags only
+// unless the caller allows sentinel mode, which wins from the smallest sizes
+// up to a few MiB, as the paper observes for larger messages and rank counts.
 ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
   const uint64_t KiB = 1024, MiB = 1024 * 1024;
   if (P <= 2) {
-    if (in_bytes <= 32 * KiB) return LL_ALGO_ONESHOT_WAVES;
     if (sentinel_ok) {
-      if (in_bytes <= 512 * KiB) return LL_ALGO_ONESHOT_SENTINEL_WAVES;
+      if (in_bytes <= 1 * MiB) return LL_ALGO_ONESHOT_SENTINEL_WAVES;
       if (in_bytes <= 2 * MiB) return LL_ALGO_ONESHOT_SENTINEL;
       if (in_bytes <= 16 * MiB) return LL_ALGO_TWOSHOT_SENTINEL_WAVES;
       return LL_ALGO_TWOSHOT_LINE;
     }
-    if (in_bytes <= 128 * KiB) return LL_ALGO_ONESHOT;
+    if (in_bytes <= 64 * KiB) return LL_ALGO_ONESHOT_WAVES;
+    if (in_bytes <= 256 * KiB) return LL_ALGO_ONESHOT;
+    if (in_bytes <= 1 * MiB) return LL_ALGO_ONESHOT_LINE_WAVES;
     if (in_bytes <= 4 * MiB) return LL_ALGO_ONESHOT_LINE;
     return LL_ALGO_TWOSHOT_LINE;
   }
   if (sentinel_ok) {
-    if (in_bytes <= (P <= 4 ? 32 : 8) * KiB) return LL_ALGO_ONESHOT_WAVES;
-    if (in_bytes <= (P <= 4 ? 128 : 64) * KiB) return LL_ALGO_ONESHOT_SENTINEL_WAVES;
-    if (in_bytes <= (P <= 4 ? 2 : 1) * MiB) return LL_ALGO_TWOSHOT_SENTINEL_WAVES;
+    if (in_bytes <= (P <= 4 ? 256 : 64) * KiB) return LL_ALGO_ONESHOT_SENTINEL_WAVES;
+    if (in_bytes <= (P <= 4 ? 4 : 2) * MiB) return LL_ALGO_TWOSHOT_SENTINEL_WAVES;
     if (in_bytes <= 4 * MiB) return LL_ALGO_TWOSHOT_LINE_WAVES;
     return LL_ALGO_TWOSHOT_LINE;
   }
-  if (in_bytes <= (P <= 4 ? 32 : 16) * KiB) return LL_ALGO_ONESHOT_WAVES;
+  if (in_bytes <= (P <= 4 ? 64 : 32) * KiB) return LL_ALGO_ONESHOT_WAVES;
   if (in_bytes <= 128 * KiB) return LL_ALGO_TWOSHOT_WAVES;
-  if (in_bytes <= 4 * MiB) return LL_ALGO_TWOSHOT_LINE_WAVES;
+  if (in_bytes <= (P <= 4 ? 2 : 4) * MiB) return LL_ALGO_TWOSHOT_LINE_WAVES;
   return LL_ALGO_TWOSHOT_LINE;
 }
 
 // ReduceScatter / AllGather, by the bytes of data per rank (input for
 // ReduceScatter, output for AllGather), measured the same way at 4 KiB ..
-// 16 MiB at 4 and 8 ranks: 8-byte packets up to 256 KiB (128 KiB at 2-4
-// ranks), lines above; with sentinel mode allowed, sentinel units from 128
-// KiB up to 4 MiB.
+// 8 MiB at 4 and 8 ranks: 8-byte packets up to 128 KiB (256 KiB at 2-4
+// ranks), lines above; with sentinel mode allowed, sentinel units up to 2 MiB
+// (4 MiB at 2-4 ranks).
 ll_proto auto_proto(uint64_t bytes, int P, bool sentinel_ok) {
   const uint64_t KiB = 1024, MiB = 1024 * 1024;
-  if (sentinel_ok) {
-    if (bytes <= 64 * KiB) return LL_PROTO_PACKET8;
-    if (bytes <= 4 * MiB) return LL_PROTO_SENTINEL;
-    return LL_PROTO_LINE128;
-  }
-  return bytes <= (P >= 5 ? 256 : 128) * KiB ? LL_PROTO_PACKET8 : LL_PROTO_LINE128;
+  if (sentinel_ok) return bytes <= (P >= 5 ? 2 : 4) * MiB ? LL_PROTO_SENTINEL : LL_PROTO_LINE128;
+  return bytes <= (P >= 5 ? 128 : 256) * KiB ? LL_PROTO_PACKET8 : LL_PROTO_LINE128;
 }
 
 // Broadcast / Reduce: 8-byte packets up to 64 KiB per rank, lines above, or
@@ -422,16 +417,15 @@ ll_proto auto_proto_rooted(uint64_t bytes, bool sentinel_ok) {
 
 // Stand-alone ReduceScatter / AllGather: the wave-per-peer kernels serve
 // each format up to the size where the one-lane-per-unit kernels catch up
-// (measured at 4 and 8 ranks): 8-byte packets up to 1 MiB of data per rank
-// (2 MiB at 2-4 ranks), lines up to 2 MiB, sentinel units up to 1 MiB
-// (512 KiB at 2-4 ranks).  ll_set_wave_kernels forces either family.
+// (measured at 4 and 8 ranks): 8-byte packets up to 2 MiB of data per rank,
+// lines up to 4 MiB (8 MiB at 2-4 ranks), sentinel units up to 2 MiB.
+// ll_set_wave_kernels forces either family.
 bool use_wave_kernel(ll_proto proto, uint64_t bytes, int P) {
   const int m = g_wave_kernels.load();
   if (m != 0) return m == 2;
-  const uint64_t KiB = 1024, MiB = 1024 * 1024;
-  if (proto == LL_PROTO_LINE128) return bytes <= 2 * MiB;
-  if (proto == LL_PROTO_SENTINEL) return bytes <= (P >= 5 ? 1 * MiB : 512 * KiB);
-  return bytes <= (P >= 5 ? 1 * MiB : 2 * MiB);
+  const uint64_t MiB = 1024 * 1024;
+  if (proto == LL_PROTO_LINE128) return bytes <= (P >= 5 ? 4 : 8) * MiB;
+  return bytes <= 2 * MiB;
 }
 
 // The wave-per-peer one-shot kernels run a single iteration only.
@@ -683,6 +677,7 @@ int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, 
     algo = auto_algo(iter_count * es, nranks, g_auto_sentinel.load() != 0);
     if (iters > 1 && algo == LL_ALGO_ONESHOT_WAVES) algo = LL_ALGO_TWOSHOT_WAVES;
     if (iters > 1 && algo == LL_ALGO_ONESHOT_SENTINEL_WAVES) algo = LL_ALGO_TWOSHOT_SENTINEL_WAVES;
+    if (iters > 1 && algo == LL_ALGO_ONESHOT_LINE_WAVES) algo = LL_ALGO_TWOSHOT_LINE_WAVES;
   }
   if (iters > 1 && is_wave_algo(algo))
     return LL_ERR_UNSUPPORTED;
