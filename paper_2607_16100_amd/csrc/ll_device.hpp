@@ -63,6 +63,27 @@ __device__ __forceinline__ void compiler_fence() { __asm__ __volatile__("" ::: "
 
 __device__ __forceinline__ uint64_t now_ticks() { return __builtin_amdgcn_s_memrealtime(); }
 
+// Budget of a call's flag waits, in ticks of the 100 MHz constant clock.  The
+// clock is read for the first time at a wait's first timeout check, not at
+// kernel entry: a clock read is a scalar memory round trip, and at entry it
+// would stand between the kernel's start and its first loads and stores.
+// The budget therefore starts when a wait first runs long, which is all a
+// bound on waiting needs.
+struct WaitBudget {
+  uint64_t budget = 0;
+  uint64_t deadline = 0;
+  __device__ WaitBudget() {}
+  __device__ explicit WaitBudget(uint64_t ticks) : budget(ticks) {}
+  __device__ __forceinline__ bool expired() {
+    const uint64_t t = now_ticks();
+    if (deadline == 0) {
+      deadline = t + budget;
+      return false;
+    }
+    return t > deadline;
+  }
+};
+
 // ---------------------------------------------------------------------------
 // Element types.  A payload word holds one binary32 or two bfloat16 values
 // (element 2k in the low half).

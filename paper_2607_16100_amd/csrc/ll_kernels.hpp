@@ -142,7 +142,7 @@ __device__ __forceinline__ void idle64(int units) {
 
 template <class Pr, int P>
 __device__ __forceinline__ int poll_all(char *area_r, uint64_t slot, uint32_t off, int r, uint32_t epoch,
-                                         uint64_t deadline, u32x4 *got, int first_wait = 0, int poll_gap = 0,
+                                         WaitBudget &budget, u32x4 *got, int first_wait = 0, int poll_gap = 0,
                                          uint32_t peers = 0xFFFFFFFFu) {
   // One resource covers the P-1 slots; the slot is selected by the scalar offset.
   const rsrc_t rs = make_rsrc(area_r, (uint32_t)((uint64_t)(P - 1) * slot));
@@ -167,7 +167,7 @@ __device__ __forceinline__ int poll_all(char *area_r, uint64_t slot, uint32_t of
     }
     if (pend == 0) break;
     idle64(poll_gap);
-    if ((spins++ & 15) == 0 && now_ticks() > deadline) {
+    if ((spins++ & 15) == 0 && budget.expired()) {
       report_timeout(r, pend, epoch);
       break;
     }
@@ -241,7 +241,7 @@ __global__ __launch_bounds__(1024) void k_oneshot(KArgs ka) {
   const Part pt = part_of_block<P>(a);
   const int r = pt.r;
   constexpr int E = Elem<DT>::kBytes;
-  const uint64_t deadline = now_ticks() + a.timeout;
+  WaitBudget budget(a.timeout);
   char *const slice_r = a.sym + (uint64_t)r * a.stride;
   const char *const in_r = a.in + (uint64_t)r * a.in_stride;
   char *const out_r = a.out + (uint64_t)r * (uint64_t)a.n * E;
@@ -271,7 +271,7 @@ __global__ __launch_bounds__(1024) void k_oneshot(KArgs ka) {
         t_acked = now_ticks();
       }
       u32x4 got[P];
-      const int spins = poll_all<Pr, P>(area_r, a.slot, off, r, epoch, deadline, got, a.first_wait, a.poll_gap);
+      const int spins = poll_all<Pr, P>(area_r, a.slot, off, r, epoch, budget, got, a.first_wait, a.poll_gap);
       if (a.phases != nullptr && threadIdx.x == 0) {
         const uint64_t t_polled = now_ticks() + (got[(r + 1) % P].x & 0u);
         a.phases[4 * blockIdx.x + 0] = t_loaded;
@@ -402,9 +402,7 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
 
   const uint32_t W = a.grid / P;
   const uint32_t tiles = (units + (uint32_t)WU::kPerTile - 1u) >> kTileShift;
-  // the wait budget starts at the first timeout check, so that no clock read
-  // (a scalar memory round trip) sits on the way to the first store
-  uint64_t deadline = 0;
+  WaitBudget budget(a.timeout);
   char *const out_r = a.out + (uint64_t)r * (uint64_t)n * E;
   const rsrc_t rs = make_rsrc(a.sym + a.area + (uint64_t)r * a.stride + (q - (q > r ? 1u : 0u)) * slot, slot);
 
@@ -462,14 +460,9 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
           }
         }
         if (__builtin_amdgcn_ballot_w64(pend != 0) == 0) break;
-        if ((++spins & 15) == 0) {
-          const uint64_t t = now_ticks();
-          if (deadline == 0) {
-            deadline = t + a.timeout;
-          } else if (t > deadline) {
-            if (pend != 0) report_timeout((int)r, 1u << q, a.epoch);
-            break;
-          }
+        if ((++spins & 15) == 0 && budget.expired()) {
+          if (pend != 0) report_timeout((int)r, 1u << q, a.epoch);
+          break;
         }
         idle64(a.poll_gap);
       }
@@ -558,7 +551,7 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
 // n * esize % 16 == 0), so units past a short last chunk are simply skipped.
 template <int P>
 __device__ __forceinline__ void poll_out(char *out_r, uint32_t out_bytes, uint32_t chunk_bytes, uint32_t off,
-                                         uint32_t pend, int r, uint32_t epoch, uint64_t deadline) {
+                                         uint32_t pend, int r, uint32_t epoch, WaitBudget &budget) {
   const rsrc_t rs = make_rsrc(out_r, out_bytes);
   int spins = 1;
   while (pend != 0) {
@@ -574,7 +567,7 @@ __device__ __forceinline__ void poll_out(char *out_r, uint32_t out_bytes, uint32
       if ((pend & (1u << q)) && ProtoSent::ready(got[q], epoch)) pend &= ~(1u << q);
     }
     if (pend == 0) break;
-    if ((spins++ & 15) == 0 && now_ticks() > deadline) {
+    if ((spins++ & 15) == 0 && budget.expired()) {
       report_timeout(r, pend, epoch);
       break;
     }
@@ -595,7 +588,7 @@ struct TwoShot {
   int64_t n, C;
   uint64_t rs_area, ag_area;
   uint32_t epoch;
-  uint64_t deadline;
+  mutable WaitBudget budget;
   bool publish, al4, in_al4;
 
   __device__ __forceinline__ int64_t chunk_len(int c) const {
@@ -624,7 +617,7 @@ struct TwoShot {
     const int64_t nr = chunk_len(r);
     const u32x4 own = Pr::template load<DT>(in_r + r * C * E, u, sub, nr, in_al4);
     u32x4 got[P];
-    poll_all<Pr, P>(slice_r + rs_area, a.slot, off, r, epoch, deadline, got);
+    poll_all<Pr, P>(slice_r + rs_area, a.slot, off, r, epoch, budget, got);
 #pragma unroll
     for (int q = 0; q < P; ++q) got[q] = Pr::unpack(got[q], sub);
     const u32x4 res = reduce_ordered<Pr, DT, P>(got, own, r);
@@ -651,11 +644,11 @@ struct TwoShot {
 #pragma unroll
       for (int q = 0; q < P; ++q)
         if (q != r && (int64_t)off < chunk_len(q) * E) pend |= 1u << q;
-      poll_out<P>(out_r, (uint32_t)(n * E), (uint32_t)(C * E), off, pend, r, epoch, deadline);
+      poll_out<P>(out_r, (uint32_t)(n * E), (uint32_t)(C * E), off, pend, r, epoch, budget);
       return;
     }
     u32x4 got[P];
-    poll_all<Pr, P>(slice_r + ag_area, a.slot, off, r, epoch, deadline, got);
+    poll_all<Pr, P>(slice_r + ag_area, a.slot, off, r, epoch, budget, got);
 #pragma unroll
     for (int q = 0; q < P; ++q) {
       if (q == r) continue;
@@ -684,7 +677,7 @@ __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(LLCOLL_TWO
   TwoShot<Pr, DT, P, Direct> t{a};
   t.r = pt.r;
   constexpr int E = Elem<DT>::kBytes;
-  t.deadline = now_ticks() + a.timeout;
+  t.budget = WaitBudget(a.timeout);
   t.slice_r = a.sym + (uint64_t)t.r * a.stride;
   t.publish = (t.r != a.mute);
   t.al4 = a.al4 != 0;
@@ -811,9 +804,7 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
   store_units(slot_out + area + (Mode == 2 ? ag_off : 0), w, first);
 
   const bool al4 = a.al4 != 0;
-  // the wait budget starts at the first timeout check, so that no clock read
-  // (a scalar memory round trip) sits on the way to the first store
-  uint64_t deadline = 0;
+  WaitBudget budget(a.timeout);
   // rank r's output: Mode 0 all n elements, Mode 1 its chunk, Mode 2 its P blocks
   char *const out_rank = a.out + (uint64_t)r * (uint64_t)(Mode == 2 ? (int64_t)P * a.n : a.n) * E;
   uint64_t out_off = 0;
@@ -864,14 +855,9 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
         }
       }
       if (__builtin_amdgcn_ballot_w64(pend != 0) == 0) break;
-      if ((++spins & 15) == 0) {
-        const uint64_t t = now_ticks();
-        if (deadline == 0) {
-          deadline = t + a.timeout;
-        } else if (t > deadline) {
-          if (pend != 0) report_timeout((int)r, 1u << q, epoch);
-          break;
-        }
+      if ((++spins & 15) == 0 && budget.expired()) {
+        if (pend != 0) report_timeout((int)r, 1u << q, epoch);
+        break;
       }
     }
     if (ResetsSlots<Pr>::value) {
@@ -1014,7 +1000,7 @@ __global__ __launch_bounds__(1024) void k_twoshot_atomic(KArgs ka) {
   const int64_t GW = ((int64_t)pt.W * a.block) >> 6;
   const int64_t n = a.n, C = a.chunk;
   const int64_t tiles = (C + TE - 1) / TE;
-  const uint64_t deadline = now_ticks() + a.timeout;
+  WaitBudget budget(a.timeout);
   const char *const in_r = a.in + (uint64_t)r * a.in_stride;
   char *const out_r = a.out + (uint64_t)r * (uint64_t)n * E;
   const bool publish = (r != a.mute);
@@ -1073,7 +1059,7 @@ __global__ __launch_bounds__(1024) void k_twoshot_atomic(KArgs ka) {
     uint32_t *cnt = cnt_of(r) + t;
     int spins = 1;
     while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != (uint32_t)P) {
-      if ((spins++ & 15) == 0 && now_ticks() > deadline) {
+      if ((spins++ & 15) == 0 && budget.expired()) {
         report_timeout(r, ((1u << P) - 1u) & ~(1u << r), a.epoch);
         break;
       }
@@ -1111,7 +1097,7 @@ __global__ __launch_bounds__(1024) void k_twoshot_atomic(KArgs ka) {
 #pragma unroll
     for (int q = 0; q < P; ++q)
       if (q != r && e0 < chunk_len(q)) pend |= 1u << q;
-    poll_out<P>(out_r, (uint32_t)(n * E), (uint32_t)(C * E), (uint32_t)(e0 * E), pend, r, a.epoch, deadline);
+    poll_out<P>(out_r, (uint32_t)(n * E), (uint32_t)(C * E), (uint32_t)(e0 * E), pend, r, a.epoch, budget);
   };
 
   const int64_t steps = gw < tiles ? (tiles - gw + GW - 1) / GW : 0;
@@ -1135,30 +1121,36 @@ template <class Pr, int DT, int P>
 __global__ __launch_bounds__(1024) void k_broadcast(KArgs ka) {
   const KArgs a = pin_args(ka);
   const uint64_t t_start = stamp_start(a);
-  const Part pt = part_of_block<P>(a);
-  const int r = pt.r, root = a.root;
   constexpr int E = Elem<DT>::kBytes;
-  const uint64_t deadline = now_ticks() + a.timeout;
+  const uint32_t r = blockIdx.x % P, w = blockIdx.x / P;
+  const uint32_t root = (uint32_t)a.root;
   const int64_t n = a.n;
-  const int64_t units = Pr::units((n * E + 3) / 4);
-  char *const out_r = a.out + (uint64_t)r * (uint64_t)n * E;
-  const int64_t g = (int64_t)pt.w * a.block + threadIdx.x;
+  // unit indices fit 32 bits: a call's P-1 slots span less than 4 GiB
+  const uint32_t units = (uint32_t)a.units;
+  const uint32_t g = w * a.block + threadIdx.x;
   const int sub = (int)(g % Pr::kLanes);
-  const int64_t ustep = (int64_t)pt.W * a.block / Pr::kLanes;
+  const uint32_t ustep = (a.grid / P) * a.block / Pr::kLanes;
   if (r == root) {
+    // The root's first unit is loaded and sent before the rest of its
+    // set-up; a lane past the end stores at an offset past the slot, which
+    // the buffer resource discards, so no store is branched around.
+    constexpr uint32_t kNowhere = 0xFFFFFFF0u;
     const char *const in_r = a.in + (uint64_t)r * a.in_stride;
-    for (int64_t u = g / Pr::kLanes; u < units; u += ustep) {
-      const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+    const bool publish = (int)r != a.mute;
+    for (uint32_t u = g / Pr::kLanes; u < units; u += ustep) {
+      const uint32_t off = u * Pr::kUnitBytes + sub * 16;
       const u32x4 own = Pr::template load<DT>(in_r, u, sub, n, a.in_al4 != 0);
-      if (r != a.mute) bcast<P>(a, a.area, r, off, Pr::pack(own, a.epoch, sub));
-      Pr::template store<DT>(out_r, u, sub, n, a.al4 != 0, own);
+      bcast<P>(a, a.area, (int)r, publish ? off : kNowhere, Pr::pack(own, a.epoch, sub));
+      Pr::template store<DT>(a.out + (uint64_t)r * (uint64_t)n * E, u, sub, n, a.al4 != 0, own);
     }
   } else {
     char *const area_r = a.sym + (uint64_t)r * a.stride + a.area;
-    for (int64_t u = g / Pr::kLanes; u < units; u += ustep) {
-      const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+    char *const out_r = a.out + (uint64_t)r * (uint64_t)n * E;
+    WaitBudget budget(a.timeout);
+    for (uint32_t u = g / Pr::kLanes; u < units; u += ustep) {
+      const uint32_t off = u * Pr::kUnitBytes + sub * 16;
       u32x4 got[P];
-      poll_all<Pr, P>(area_r, a.slot, off, r, a.epoch, deadline, got, 0, 0, 1u << root);
+      poll_all<Pr, P>(area_r, a.slot, off, (int)r, a.epoch, budget, got, 0, 0, 1u << root);
       Pr::template store<DT>(out_r, u, sub, n, a.al4 != 0, Pr::unpack(got[root], sub));
     }
   }
@@ -1173,37 +1165,36 @@ template <class Pr, int DT, int P>
 __global__ __launch_bounds__(1024) void k_reduce(KArgs ka) {
   const KArgs a = pin_args(ka);
   const uint64_t t_start = stamp_start(a);
-  const Part pt = part_of_block<P>(a);
-  const int r = pt.r, root = a.root;
-  constexpr int E = Elem<DT>::kBytes;
-  const uint64_t deadline = now_ticks() + a.timeout;
+  const uint32_t r = blockIdx.x % P, w = blockIdx.x / P;
+  const uint32_t root = (uint32_t)a.root;
   const int64_t n = a.n;
-  const int64_t units = Pr::units((n * E + 3) / 4);
+  const uint32_t units = (uint32_t)a.units;
   const char *const in_r = a.in + (uint64_t)r * a.in_stride;
-  const int64_t g = (int64_t)pt.w * a.block + threadIdx.x;
+  const uint32_t g = w * a.block + threadIdx.x;
   const int sub = (int)(g % Pr::kLanes);
-  const int64_t ustep = (int64_t)pt.W * a.block / Pr::kLanes;
+  const uint32_t ustep = (a.grid / P) * a.block / Pr::kLanes;
   if (r != root) {
-    if (r == a.mute) {
-      stamp_end(a, t_start);
-      return;
-    }
-    char *const dst = a.sym + (uint64_t)root * a.stride + a.area + (uint64_t)slot_of(r, root) * a.slot;
-    const rsrc_t rs = make_rsrc(dst, (uint32_t)a.slot);
-    for (int64_t u = g / Pr::kLanes; u < units; u += ustep) {
-      const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
-      st_pkt(rs, off, Pr::pack(Pr::template load<DT>(in_r, u, sub, n, a.in_al4 != 0), a.epoch, sub));
+    // a sender: load and store, nothing else; a muted rank stores at an
+    // offset past the slot, which the buffer resource discards
+    constexpr uint32_t kNowhere = 0xFFFFFFF0u;
+    const bool publish = (int)r != a.mute;
+    const uint32_t slot = (uint32_t)a.slot;
+    const rsrc_t rs = make_rsrc(a.sym + (uint64_t)root * a.stride + a.area + (r - (r > root ? 1u : 0u)) * slot, slot);
+    for (uint32_t u = g / Pr::kLanes; u < units; u += ustep) {
+      const uint32_t off = u * Pr::kUnitBytes + sub * 16;
+      st_pkt(rs, publish ? off : kNowhere, Pr::pack(Pr::template load<DT>(in_r, u, sub, n, a.in_al4 != 0), a.epoch, sub));
     }
   } else {
     char *const area_r = a.sym + (uint64_t)r * a.stride + a.area;
-    for (int64_t u = g / Pr::kLanes; u < units; u += ustep) {
-      const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+    WaitBudget budget(a.timeout);
+    for (uint32_t u = g / Pr::kLanes; u < units; u += ustep) {
+      const uint32_t off = u * Pr::kUnitBytes + sub * 16;
       const u32x4 own = Pr::template load<DT>(in_r, u, sub, n, a.in_al4 != 0);
       u32x4 got[P];
-      poll_all<Pr, P>(area_r, a.slot, off, r, a.epoch, deadline, got);
+      poll_all<Pr, P>(area_r, a.slot, off, (int)r, a.epoch, budget, got);
 #pragma unroll
       for (int q = 0; q < P; ++q) got[q] = Pr::unpack(got[q], sub);
-      Pr::template store<DT>(a.out, u, sub, n, a.al4 != 0, reduce_ordered<Pr, DT, P>(got, own, r));
+      Pr::template store<DT>(a.out, u, sub, n, a.al4 != 0, reduce_ordered<Pr, DT, P>(got, own, (int)r));
     }
   }
   stamp_end(a, t_start);
@@ -1222,7 +1213,7 @@ __global__ __launch_bounds__(1024) void k_reduce_scatter(KArgs ka) {
   const Part pt = part_of_block<P>(a);
   const int r = pt.r;
   constexpr int E = Elem<DT>::kBytes;
-  const uint64_t deadline = now_ticks() + a.timeout;
+  WaitBudget budget(a.timeout);
   char *const slice_r = a.sym + (uint64_t)r * a.stride;
   const char *const in_r = a.in + (uint64_t)r * a.in_stride;
   const bool in_al4 = a.in_al4 != 0;
@@ -1260,7 +1251,7 @@ __global__ __launch_bounds__(1024) void k_reduce_scatter(KArgs ka) {
       const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
       const u32x4 own = Pr::template load<DT>(in_r + r * m * E, u, sub, m, in_al4);
       u32x4 got[P];
-      poll_all<Pr, P>(slice_r + a.area, a.slot, off, r, a.epoch, deadline, got);
+      poll_all<Pr, P>(slice_r + a.area, a.slot, off, r, a.epoch, budget, got);
 #pragma unroll
       for (int q = 0; q < P; ++q) got[q] = Pr::unpack(got[q], sub);
       const u32x4 res = reduce_ordered<Pr, DT, P>(got, own, r);
@@ -1282,7 +1273,7 @@ __global__ __launch_bounds__(1024) void k_allgather(KArgs ka) {
   const Part pt = part_of_block<P>(a);
   const int r = pt.r;
   constexpr int E = Elem<DT>::kBytes;
-  const uint64_t deadline = now_ticks() + a.timeout;
+  WaitBudget budget(a.timeout);
   char *const slice_r = a.sym + (uint64_t)r * a.stride;
   const char *const in_r = a.in + (uint64_t)r * a.in_stride;
   const int64_t n = a.n;
@@ -1309,7 +1300,7 @@ __global__ __launch_bounds__(1024) void k_allgather(KArgs ka) {
       const int64_t u = u0 + (s - lag) * ustep;
       const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
       u32x4 got[P];
-      poll_all<Pr, P>(slice_r + a.area, a.slot, off, r, a.epoch, deadline, got);
+      poll_all<Pr, P>(slice_r + a.area, a.slot, off, r, a.epoch, budget, got);
 #pragma unroll
       for (int q = 0; q < P; ++q) {
         if (q == r) continue;
