@@ -240,13 +240,17 @@ struct Plan {
   int64_t units;  // packet units per stream
 };
 
-// Units per lane of the wave-per-peer one-shot: fewer, fuller workgroups as
-// messages grow.
-int wave_units_log2(int64_t units) {
+// Units per lane of the wave-per-peer kernels: fewer, fuller workgroups as
+// messages grow (measured at 64 KiB .. 8 MiB per rank, 2-8 ranks).  A line
+// unit is a whole wave; the two-shot AllReduce over lines takes two units
+// per lane once the P tiles of a step hold more than 1536 line units, the
+// other line kernels keep one.
+int wave_units_log2(int64_t units, int proto, bool twoshot_allreduce, int P) {
   const int forced = g_wave_units.load();
   if (forced == 1) return 0;
   if (forced == 2) return 1;
   if (forced == 4) return 2;
+  if (proto == PR_LINE && twoshot_allreduce) return units * P <= 1536 ? 0 : 1;
   if (units <= 64 * 64) return 0;
   return 1;
 }
@@ -254,7 +258,7 @@ int wave_units_log2(int64_t units) {
 int launch(const Plan &pl, void *stream) {
   const bool two_waves = pl.kind == K_TWOSHOT_WAVES || pl.kind == K_RS_WAVES || pl.kind == K_AG_WAVES;
   const bool wave_kernel = pl.kind == K_ONESHOT_WAVES || two_waves;
-  const int wlog = wave_kernel ? wave_units_log2(pl.units) : 0;
+  const int wlog = wave_kernel ? wave_units_log2(pl.units, pl.proto, pl.kind == K_TWOSHOT_WAVES, pl.P) : 0;
   kernel_fn fn = nullptr;
   const int wpr = pl.proto == PR_SENT ? 1 : (pl.proto == PR_LINE ? 2 : 0);
   if (pl.kind == K_ONESHOT_WAVES) {
@@ -387,13 +391,13 @@ ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
   }
   if (sentinel_ok) {
     if (in_bytes <= (P <= 4 ? 256 : 64) * KiB) return LL_ALGO_ONESHOT_SENTINEL_WAVES;
-    if (in_bytes <= (P <= 4 ? 4 : 2) * MiB) return LL_ALGO_TWOSHOT_SENTINEL_WAVES;
+    if (in_bytes <= 2 * MiB) return LL_ALGO_TWOSHOT_SENTINEL_WAVES;
     if (in_bytes <= 4 * MiB) return LL_ALGO_TWOSHOT_LINE_WAVES;
     return LL_ALGO_TWOSHOT_LINE;
   }
   if (in_bytes <= (P <= 4 ? 64 : 32) * KiB) return LL_ALGO_ONESHOT_WAVES;
   if (in_bytes <= 128 * KiB) return LL_ALGO_TWOSHOT_WAVES;
-  if (in_bytes <= (P <= 4 ? 2 : 4) * MiB) return LL_ALGO_TWOSHOT_LINE_WAVES;
+  if (in_bytes <= 4 * MiB) return LL_ALGO_TWOSHOT_LINE_WAVES;
   return LL_ALGO_TWOSHOT_LINE;
 }
 
