@@ -277,6 +277,61 @@ def test_result_independent_of_launch_shape(algo):
     ll.ll_set_wave_units(0)
 
 
+WAVE_ALGOS = ["oneshot_waves", "oneshot_sentinel_waves", "oneshot_line_waves", "twoshot_waves",
+              "twoshot_sentinel_waves", "twoshot_line_waves"]
+
+
+@pytest.mark.parametrize("algo", WAVE_ALGOS)
+@pytest.mark.parametrize("n", [5, 300])
+def test_workgroups_past_the_last_tile(algo, n):
+    """A forced launch with more workgroups per rank than there are tiles: the
+    wave kernels issue their first loads and stores before they look at the
+    tile count, so a workgroup past the last tile must load and store nothing.
+    The result is exact and the output past P*n elements is untouched."""
+    p = 8
+    x = wl.normal(p, n, "bf16", seed=n)
+    reg = SymRegion(p, n, "bf16")
+    reg.init()
+    guard = np.uint8(0xA5)
+    reg.out.fill_(int(guard))
+    ll.ll_set_launch(16, 0)
+    try:
+        got = run_allreduce(reg, x, algo)
+    finally:
+        ll.ll_set_launch(0, 0)
+    assert_bits_equal(got, oracle.allreduce(x), f"{algo} n={n} W=16")
+    tail = reg.out[p * n * 2:].cpu().numpy()
+    assert (tail == guard).all(), f"{algo}: {int((tail != guard).sum())} bytes written past the output"
+
+
+@pytest.mark.parametrize("proto", PROTOS)
+def test_rs_ag_workgroups_past_the_last_tile(proto):
+    """The same for the wave-per-peer ReduceScatter and AllGather."""
+    p, m = 8, 37
+    x = wl.normal(p, p * m, "bf16", seed=5)
+    reg = SymRegion(p, p * m, "bf16", out_elems=p * p * m + 4096)
+    reg.init()
+    guard = np.uint8(0x5A)
+    ll.ll_set_wave_kernels(2)
+    ll.ll_set_launch(16, 0)
+    try:
+        reg.out.fill_(int(guard))
+        reg.write_inputs(x)
+        check_ok(reg.reduce_scatter(m, proto), "rs")
+        rs = reg.read_out(p * m, np.uint16).reshape(p, m)
+        assert (reg.out[p * m * 2:].cpu().numpy() == guard).all(), "RS wrote past its output"
+        reg.out.fill_(int(guard))
+        reg.write_inputs(rs)
+        check_ok(reg.allgather(m, proto), "ag")
+        ag = reg.read_out(p * p * m, np.uint16).reshape(p, p * m)
+        assert (reg.out[p * p * m * 2:].cpu().numpy() == guard).all(), "AG wrote past its output"
+    finally:
+        ll.ll_set_launch(0, 0)
+        ll.ll_set_wave_kernels(0)
+    assert_bits_equal(rs, oracle.reduce_scatter(x), f"RS {proto} W=16")
+    assert_bits_equal(ag, oracle.allgather(rs), f"AG {proto} W=16")
+
+
 @pytest.mark.parametrize("lag", [1, 2, 5])
 def test_result_independent_of_pipeline_lag(lag):
     """Two-shot, ReduceScatter and AllGather give the same bits for every
