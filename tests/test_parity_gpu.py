@@ -168,6 +168,62 @@ def test_changing_inputs_never_return_stale_packets(algo):
         assert_bits_equal(run_allreduce(reg, x, algo), oracle.allreduce(x), f"{algo} change {k}")
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_random_call_sequence_on_one_region(dtype):
+    """One region, 150 calls in a seeded random order: every deterministic
+    AllReduce algorithm and AUTO at random sizes (1 element .. 96 Ki),
+    ReduceScatter / AllGather with every format, and Broadcast / Reduce with a
+    random root, each with new inputs.  Whatever the previous call left in the
+    packet areas (other sizes, formats, kernels, iteration layouts), no stale
+    packet may ever be accepted."""
+    p, nmax = 8, 96 * 1024
+    rng = np.random.default_rng(20261202 if dtype == "bf16" else 7)
+    reg = SymRegion(p, nmax, dtype, out_elems=p * nmax)
+    reg.init()
+    algos = AR_ALGOS
+    for k in range(150):
+        kind = rng.choice(["ar", "ar", "ar", "rs", "ag", "bcast", "reduce"])
+        n = int(rng.integers(1, nmax + 1)) if rng.random() < 0.5 else int(rng.integers(1, 2048))
+        seed = 10_000 + 1000 * k
+        if kind == "ar":
+            algo = str(rng.choice(algos))
+            x = wl.normal(p, n, dtype, seed=seed)
+            say(f"seq {k}: allreduce {algo} n={n}")
+            assert_bits_equal(run_allreduce(reg, x, algo), oracle.allreduce(x), f"seq {k} {algo} n={n}")
+        elif kind in ("rs", "ag"):
+            proto = str(rng.choice(PROTOS))
+            m = max(1, n // p)
+            if kind == "rs":
+                x = wl.normal(p, p * m, dtype, seed=seed)
+                reg.write_inputs(x)
+                say(f"seq {k}: reduce_scatter {proto} m={m}")
+                check_ok(reg.reduce_scatter(m, proto), f"seq {k} rs")
+                assert_bits_equal(reg.read_out(p * m, NP[dtype]).reshape(p, m), oracle.reduce_scatter(x),
+                                  f"seq {k} rs {proto} m={m}")
+            else:
+                x = wl.normal(p, m, dtype, seed=seed)
+                reg.write_inputs(x)
+                say(f"seq {k}: allgather {proto} m={m}")
+                check_ok(reg.allgather(m, proto), f"seq {k} ag")
+                assert_bits_equal(reg.read_out(p * p * m, NP[dtype]).reshape(p, p * m), oracle.allgather(x),
+                                  f"seq {k} ag {proto} m={m}")
+        else:
+            proto = str(rng.choice(PROTOS))
+            root = int(rng.integers(0, p))
+            x = wl.normal(p, n, dtype, seed=seed)
+            reg.write_inputs(x)
+            if kind == "bcast":
+                say(f"seq {k}: broadcast {proto} root={root} n={n}")
+                check_ok(reg.broadcast(n, root, proto), f"seq {k} bcast")
+                assert_bits_equal(reg.read_out(p * n, NP[dtype]).reshape(p, n), oracle.broadcast(x, root),
+                                  f"seq {k} bcast {proto} n={n}")
+            else:
+                say(f"seq {k}: reduce {proto} root={root} n={n}")
+                check_ok(reg.reduce(n, root, proto), f"seq {k} reduce")
+                got = reg.read_out(n, NP[dtype]).reshape(1, n)
+                assert_bits_equal(got, oracle.reduce(x, root).reshape(1, n), f"seq {k} reduce {proto} n={n}")
+
+
 # ------------------------------------------------------------ configuration C3
 def test_c3_twoshot_bf16_1mib_vs_oneshot():
     """8 ranks, bfloat16, 64 x 8192 normal(0, 0.5) per rank: two-shot (both
