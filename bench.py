@@ -103,7 +103,8 @@ def bench_headline(torch, ll, steps, warmup):
     reg.init()
     reg.write_inputs(x)
     s = reg.stream_handle()
-    algo = ll.LL_ALGO_AUTO
+    # the configuration's path, named explicitly (it is also what AUTO picks here)
+    algo = ll.LL_ALGO_ONESHOT_WAVES
     epoch = [1]
 
     def queue(first, count, stamps_ptr, stride):
@@ -124,7 +125,8 @@ def bench_headline(torch, ll, steps, warmup):
     host_steps = min(steps, 2000)
     ev0.record()
     for _ in range(host_steps):
-        ll.check(ll.ll_allreduce(reg.base, reg.rank_stride, reg.out_ptr, n, ll.LL_BF16, ll.LL_SUM, p, epoch[0], s))
+        ll.check(ll.ll_allreduce_algo(reg.base, reg.rank_stride, reg.out_ptr, n, ll.LL_BF16, ll.LL_SUM, p, epoch[0], s,
+                                      algo))
         epoch[0] += 1
     ev1.record()
     torch.cuda.synchronize()
@@ -132,10 +134,18 @@ def bench_headline(torch, ll, steps, warmup):
     ll.check(ll.ll_check(s), "headline")
     # the last call's output, checked against the oracle by the CPU-baseline leg
     HEADLINE_OUTPUT["bits"] = reg.read_out(p * n, np.uint16).reshape(p, n)
+    # the same workload through AUTO and the other packet formats (context);
+    # their epochs continue after the ones used above
+    reg.epoch = epoch[0] - 1
+    variants = {}
+    for name in ("auto", "oneshot_sentinel_waves", "oneshot_line_waves", "twoshot_waves"):
+        r = paced_collective(torch, ll, reg, "ar", n, ll.ALGOS[name], min(steps, 5000), 100)
+        variants[name] = {"p50_us": r["p50_us"], "p99_us": r["p99_us"]}
     return {
+        "algorithm": "oneshot_waves", "variants": variants,
         "p50_us": pct(intervals, 50), "p99_us": pct(intervals, 99), "mean_us": float(np.mean(intervals)),
         "span_p50_us": pct(spans, 50), "python_launched_mean_us": host_mean, "wall_s": wall, "grid": grid,
-        "threads": threads, "epochs": epoch[0] - 1,
+        "threads": threads, "epochs": reg.epoch,
     }
 
 
