@@ -319,16 +319,18 @@ int ll_debug_mute_rank(int rank);
 int ll_debug_stamp_next(uint64_t *stamps);
 
 /* Diagnostics hook: when `phases` (device memory) is non-NULL, the next
- * one-shot launch records phase times.  LL_ALGO_ONESHOT (4*grid words): for
+ * one-shot launch records phase times.  The stamps exist only in a library
+ * built for it (the default build leaves them out of the kernels' critical
+ * paths); otherwise `phases` is ignored.
+ * LL_ALGO_ONESHOT, built with -DLLCOLL_ONESHOT_PHASES=1 (4*grid words): for
  * thread 0 of each workgroup b and its last packet unit, phases[4b] = time
  * its input load returned, phases[4b+1] = time its packet stores were
  * acknowledged (the kernel waits for them only in this mode), phases[4b+2] =
  * time its wait for peers ended, phases[4b+3] = number of polls it issued.
- * LL_ALGO_ONESHOT_WAVES (4*grid*nranks words), only in a library built with
- * -DLLCOLL_WAVE_PHASES=1 (the default build leaves the stamps out of that
- * kernel's critical path): for lane 0 of wave w of workgroup b and its first
- * tile, phases[4(b*nranks+w)] = time its input load returned, [..+1] = time
- * its peer's packets had all arrived, [..+2] = time it left the workgroup
+ * LL_ALGO_ONESHOT_WAVES, built with -DLLCOLL_WAVE_PHASES=1 (4*grid*nranks
+ * words): for lane 0 of wave w of workgroup b and its first tile,
+ * phases[4(b*nranks+w)] = time its input load returned, [..+1] = time its
+ * peer's packets had all arrived, [..+2] = time it left the workgroup
  * barrier.  Used for one launch only. */
 int ll_debug_phase_next(uint64_t *phases);
 

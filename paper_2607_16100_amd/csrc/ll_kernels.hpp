@@ -234,45 +234,55 @@ __device__ __forceinline__ u32x4 reduce_ordered(const u32x4 *got, u32x4 own, int
 // ---------------------------------------------------------------------------
 // One-shot AllReduce (Sec. III-A; the per-thread load -> bcast -> recvReduce
 // -> store sequence of Sec. V).  Slot (d <- s) holds all of s's input.
+// Phase stamps of the one-lane one-shot are compiled in only on request
+// (-DLLCOLL_ONESHOT_PHASES=1), like those of the wave kernel.
+#ifndef LLCOLL_ONESHOT_PHASES
+#define LLCOLL_ONESHOT_PHASES 0
+#endif
+
 template <class Pr, int DT, int P>
 __global__ __launch_bounds__(1024) void k_oneshot(KArgs ka) {
   const KArgs a = pin_args(ka);
   const uint64_t t_start = stamp_start(a);
-  const Part pt = part_of_block<P>(a);
-  const int r = pt.r;
   constexpr int E = Elem<DT>::kBytes;
+  constexpr uint32_t kNowhere = 0xFFFFFFF0u;  // past every slot: the buffer resource discards the store
+  const uint32_t r = blockIdx.x % P, w = blockIdx.x / P;
+  const char *const in_r = a.in + (uint64_t)r * a.in_stride;
+  const bool in_al4 = a.in_al4 != 0;
+  // unit indices fit 32 bits: a call's P-1 slots span less than 4 GiB
+  const uint32_t g = w * a.block + threadIdx.x;
+  const int sub = (int)(g % Pr::kLanes);
+  const uint32_t ustep = (a.grid / P) * a.block / Pr::kLanes;
+  // A muted rank (test hook) stores at an offset past the slots, which the
+  // buffer resource discards: no store is branched around, so the compiler
+  // never has to wait for the stores' acknowledgements before the polls.
+  const bool publish = (int)r != a.mute;
   WaitBudget budget(a.timeout);
   char *const slice_r = a.sym + (uint64_t)r * a.stride;
-  const char *const in_r = a.in + (uint64_t)r * a.in_stride;
   char *const out_r = a.out + (uint64_t)r * (uint64_t)a.n * E;
-  const bool publish = (r != a.mute);
-  const bool in_al4 = a.in_al4 != 0;
-  const int64_t g = (int64_t)pt.w * a.block + threadIdx.x;
-  const int sub = (int)(g % Pr::kLanes);
-  const int64_t ustep = (int64_t)pt.W * a.block / Pr::kLanes;
 
   for (uint32_t it = 0; it < a.iters; ++it) {
     const int64_t e0 = (int64_t)it * a.iter_n;
     const int64_t n = a.n - e0 < a.iter_n ? a.n - e0 : a.iter_n;
-    const int64_t units = Pr::units((n * E + 3) / 4);
+    const uint32_t units = (uint32_t)Pr::units((n * E + 3) / 4);
     const uint64_t area = a.area + (uint64_t)(it & 1u) * a.sub_bytes;
     const uint32_t epoch = a.epoch + it;
     char *const area_r = slice_r + area;
     const char *const in_i = in_r + e0 * E;
     char *const out_i = out_r + e0 * E;
-    for (int64_t u = g / Pr::kLanes; u < units; u += ustep) {
-      const uint32_t off = (uint32_t)(u * Pr::kUnitBytes + sub * 16);
+    for (uint32_t u = g / Pr::kLanes; u < units; u += ustep) {
+      const uint32_t off = u * Pr::kUnitBytes + sub * 16;
       const u32x4 own = Pr::template load<DT>(in_i, u, sub, n, in_al4);
       uint64_t t_loaded = 0, t_acked = 0;
-      if (a.phases != nullptr) t_loaded = now_ticks() + (own.x & 0u);
-      if (publish) bcast<P>(a, area, r, off, Pr::pack(own, epoch, sub));
-      if (a.phases != nullptr) {
+      if (LLCOLL_ONESHOT_PHASES && a.phases != nullptr) t_loaded = now_ticks() + (own.x & 0u);
+      bcast<P>(a, area, (int)r, publish ? off : kNowhere, Pr::pack(own, epoch, sub));
+      if (LLCOLL_ONESHOT_PHASES && a.phases != nullptr) {
         __asm__ __volatile__("s_waitcnt vmcnt(0)" ::: "memory");
         t_acked = now_ticks();
       }
       u32x4 got[P];
-      const int spins = poll_all<Pr, P>(area_r, a.slot, off, r, epoch, budget, got, a.first_wait, a.poll_gap);
-      if (a.phases != nullptr && threadIdx.x == 0) {
+      const int spins = poll_all<Pr, P>(area_r, a.slot, off, (int)r, epoch, budget, got, a.first_wait, a.poll_gap);
+      if (LLCOLL_ONESHOT_PHASES && a.phases != nullptr && threadIdx.x == 0) {
         const uint64_t t_polled = now_ticks() + (got[(r + 1) % P].x & 0u);
         a.phases[4 * blockIdx.x + 0] = t_loaded;
         a.phases[4 * blockIdx.x + 1] = t_acked;
@@ -281,7 +291,7 @@ __global__ __launch_bounds__(1024) void k_oneshot(KArgs ka) {
       }
 #pragma unroll
       for (int q = 0; q < P; ++q) got[q] = Pr::unpack(got[q], sub);
-      const u32x4 res = reduce_ordered<Pr, DT, P>(got, own, r);
+      const u32x4 res = reduce_ordered<Pr, DT, P>(got, own, (int)r);
       Pr::template store<DT>(out_i, u, sub, n, a.al4 != 0, res);
     }
     if (ResetsSlots<Pr>::value && it + 1 < a.iters) wait_vm_all();
