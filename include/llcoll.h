@@ -298,7 +298,9 @@ int ll_set_poll_pacing(int first_wait, int poll_gap);
 
 /* Two-shot pipeline distance for the following calls: a lane publishes the
  * ReduceScatter packets of step s, reduces step s-lag and gathers step
- * s-2*lag.  lag in [1, 64]; default 1. */
+ * s-2*lag; lag 0 does all three for one step before the next (each wait is
+ * then for the same step of a peer's lane, which publishes before it waits).
+ * lag in [0, 64]; default 1. */
 int ll_set_pipeline_lag(int lag);
 
 /* Packet units (16 bytes of packets) per lane of LL_ALGO_ONESHOT_WAVES for

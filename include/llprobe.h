@@ -95,6 +95,16 @@ int ll_bench_empty(int grid, int threads, int calls, uint64_t *stamps, int stamp
 /* ids[b] = XCD index of workgroup b. */
 int ll_probe_xcd(uint32_t *ids, int grid, int threads, void *stream);
 
+/* Streaming bandwidth: a grid-stride kernel over bytes/16 16-byte words with
+ * non-temporal loads and stores.  mode 0 copies src to dst, mode 1 only reads
+ * src (dst must hold at least 16 bytes and is normally left untouched), mode 2
+ * only writes dst (src unused, may be NULL).  bytes > 0 and a multiple of 16;
+ * src and dst 16-byte aligned and bytes long; grid 1..65536, threads a
+ * multiple of 64 up to 1024.  Sweeping grid gives the HBM bandwidth that a
+ * simple streaming kernel reaches, the practical ceiling under the published
+ * peak. */
+int ll_probe_stream(const void *src, void *dst, size_t bytes, int mode, int grid, int threads, void *stream);
+
 /* Torn-packet litmus across XCDs.  grid/2 writer workgroups each rewrite
  * `lines` 128-byte lines `iters` times; grid/2 reader workgroups read another
  * writer's lines `reads` times.  layout 0 = 8-byte packets, 1 = 128-byte lines

@@ -38,7 +38,7 @@ struct KArgs {
   uint32_t al4;       // every element stream of this call starts 4-byte aligned
   uint16_t first_wait;  // idle time before the first poll, in units of 64 shader cycles
   uint16_t poll_gap;    // idle time between polls, in units of 64 shader cycles
-  uint32_t lag;         // two-shot pipeline distance between publish, reduce and gather (>= 1)
+  uint32_t lag;         // two-shot pipeline distance between publish, reduce and gather (>= 0)
   uint32_t in_al4;      // every rank's input starts 4-byte aligned
   const char *in;       // rank r's input at in + r * in_stride
   uint64_t in_stride;
@@ -698,7 +698,7 @@ __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(LLCOLL_TWO
   const int sub = (int)(g % Pr::kLanes);
   const int64_t u0 = g / Pr::kLanes;
   const int64_t ustep = (int64_t)pt.W * a.block / Pr::kLanes;
-  const int64_t lag = a.lag > 0 ? a.lag : 1;
+  const int64_t lag = a.lag;
   for (uint32_t it = 0; it < a.iters; ++it) {
     const int64_t e0 = (int64_t)it * a.iter_n;
     t.n = a.n - e0 < a.iter_n ? a.n - e0 : a.iter_n;
@@ -1111,7 +1111,7 @@ __global__ __launch_bounds__(1024) void k_twoshot_atomic(KArgs ka) {
   };
 
   const int64_t steps = gw < tiles ? (tiles - gw + GW - 1) / GW : 0;
-  const int64_t lag = a.lag > 0 ? a.lag : 1;
+  const int64_t lag = a.lag;
   for (int64_t s = 0; s < steps + 2 * lag; ++s) {
     if (s < steps && publish) step_add(gw + s * GW);
     if (s >= lag && s - lag < steps) step_reduce(gw + (s - lag) * GW);
@@ -1237,7 +1237,7 @@ __global__ __launch_bounds__(1024) void k_reduce_scatter(KArgs ka) {
   const int64_t u0 = g / Pr::kLanes;
   const int64_t ustep = (int64_t)pt.W * a.block / Pr::kLanes;
   const int64_t steps = u0 < units ? (units - u0 + ustep - 1) / ustep : 0;
-  const int64_t lag = a.lag > 0 ? a.lag : 1;
+  const int64_t lag = a.lag;
 
   for (int64_t s = 0; s < steps + lag; ++s) {
     if (s < steps && publish) {
@@ -1296,7 +1296,7 @@ __global__ __launch_bounds__(1024) void k_allgather(KArgs ka) {
   const int64_t u0 = g / Pr::kLanes;
   const int64_t ustep = (int64_t)pt.W * a.block / Pr::kLanes;
   const int64_t steps = u0 < units ? (units - u0 + ustep - 1) / ustep : 0;
-  const int64_t lag = a.lag > 0 ? a.lag : 1;
+  const int64_t lag = a.lag;
 
   for (int64_t s = 0; s < steps + lag; ++s) {
     if (s < steps) {

@@ -12,6 +12,9 @@
 // * XCD map: which XCD each workgroup of a grid runs on.
 // * Litmus: whether 8-byte packets and 64-byte line halves written by one
 //   workgroup are ever observed torn by a reader on another XCD.
+// * Streaming: the HBM bandwidth that a plain kernel of 16-byte streaming
+//   loads and stores reaches (copy, read only, write only), the practical
+//   ceiling for the bandwidth-bound collectives.
 #pragma once
 
 #include "ll_device.hpp"
@@ -257,6 +260,28 @@ __global__ __launch_bounds__(256) void k_probe_litmus(uint32_t *buf, int lines, 
   atomicAdd(&counts[1], torn);
   atomicAdd(&counts[2], split16);
   atomicAdd(&counts[3], splitline);
+}
+
+// Streaming kernel over n16 16-byte words, grid-stride, one word per lane
+// and step, non-temporal loads and stores.  mode 0: dst = src; mode 1: read
+// src only (the xor of all words decides a store that never happens for
+// these inputs, so the loads stay); mode 2: write dst only.
+__global__ __launch_bounds__(1024) void k_probe_stream(const u32x4 *src, u32x4 *dst, uint64_t n16, int mode) {
+  const uint64_t nth = (uint64_t)gridDim.x * blockDim.x;
+  u32x4 acc = {0u, 0u, 0u, 0u};
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += nth) {
+    if (mode == 2) {
+      __builtin_nontemporal_store(u32x4{(uint32_t)i, 1u, 2u, 3u}, &dst[i]);
+      continue;
+    }
+    const u32x4 v = __builtin_nontemporal_load(&src[i]);
+    if (mode == 0) {
+      __builtin_nontemporal_store(v, &dst[i]);
+    } else {
+      acc ^= v;
+    }
+  }
+  if (mode == 1 && acc.x == 0x9E3779B9u && acc.y == 0x7F4A7C15u) dst[0] = acc;
 }
 
 }  // namespace llc

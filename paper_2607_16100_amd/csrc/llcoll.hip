@@ -897,7 +897,7 @@ int ll_set_poll_pacing(int first_wait, int poll_gap) {
 }
 
 int ll_set_pipeline_lag(int lag) {
-  if (lag < 1 || lag > 64) return LL_ERR_INVALID;
+  if (lag < 0 || lag > 64) return LL_ERR_INVALID;
   g_lag.store(lag);
   return LL_OK;
 }
@@ -1122,6 +1122,16 @@ int ll_probe_xcd(uint32_t *ids, int grid, int threads, void *stream) {
   if (st != LL_OK) return st;
   if (ids == nullptr) return LL_ERR_INVALID;
   hipLaunchKernelGGL(k_probe_xcd, dim3(grid), dim3(threads), 0, (hipStream_t)stream, ids);
+  return hip_status();
+}
+
+int ll_probe_stream(const void *src, void *dst, size_t bytes, int mode, int grid, int threads, void *stream) {
+  int st = probe_launch_check(grid, threads);
+  if (st != LL_OK) return st;
+  if (mode < 0 || mode > 2 || dst == nullptr || (mode != 2 && src == nullptr)) return LL_ERR_INVALID;
+  if (bytes == 0 || bytes % 16 != 0 || ((uintptr_t)src | (uintptr_t)dst) % 16 != 0) return LL_ERR_INVALID;
+  hipLaunchKernelGGL(k_probe_stream, dim3(grid), dim3(threads), 0, (hipStream_t)stream, (const u32x4 *)src,
+                     (u32x4 *)dst, (uint64_t)(bytes / 16), mode);
   return hip_status();
 }
 

@@ -94,6 +94,7 @@ _SIGS = {
     "ll_bench_empty": (_i, [_i, _i, _i, _vp, _i, _vp]),
     "ll_probe_xcd": (_i, [_vp, _i, _i, _vp]),
     "ll_probe_litmus": (_i, [_vp, _sz, _i, _i, _i, _i, _i, _vp, _vp]),
+    "ll_probe_stream": (_i, [_vp, _vp, _sz, _i, _i, _i, _vp]),
 }
 
 if not os.path.exists(LIB_PATH):
@@ -335,6 +336,10 @@ def ll_bench_empty(grid, threads, calls, stamps, stamp_stride, stream):
 
 def ll_probe_xcd(ids, grid, threads, stream):
     return _lib.ll_probe_xcd(ids, grid, threads, stream)
+
+
+def ll_probe_stream(src, dst, nbytes, mode, grid, threads, stream):
+    return _lib.ll_probe_stream(src, dst, nbytes, mode, grid, threads, stream)
 
 
 def ll_probe_litmus(buf, buf_bytes, grid, lines, iters, reads, layout, counts4, stream):

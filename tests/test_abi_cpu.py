@@ -234,6 +234,10 @@ def test_setters():
     assert ll.ll_set_poll_timeout(200_000_000) == ll.LL_OK
     assert ll.ll_debug_mute_rank(9) == ll.LL_ERR_INVALID
     assert ll.ll_debug_mute_rank(-1) == ll.LL_OK
+    assert ll.ll_set_pipeline_lag(-1) == ll.LL_ERR_INVALID
+    assert ll.ll_set_pipeline_lag(65) == ll.LL_ERR_INVALID
+    assert ll.ll_set_pipeline_lag(0) == ll.LL_OK
+    assert ll.ll_set_pipeline_lag(1) == ll.LL_OK
 
 
 def test_strerror_covers_every_code():
@@ -249,6 +253,13 @@ def test_probe_argument_checks():
     assert ll.ll_probe_floor(GOOD_BASE, 10, 10, GOOD_OUT, 8, 64, 0, 0) == ll.LL_ERR_INVALID
     assert ll.ll_probe_litmus(GOOD_BASE, 1024, 16, 64, 1, 1, 0, GOOD_OUT, 0) == ll.LL_ERR_INVALID  # buffer too small
     assert ll.ll_probe_pingpong(GOOD_BASE, 10, 8, 8, 100, GOOD_OUT, 0) == ll.LL_ERR_INVALID
+    assert ll.ll_probe_stream(GOOD_BASE, GOOD_OUT, 1024, 3, 8, 64, 0) == ll.LL_ERR_INVALID  # no such mode
+    assert ll.ll_probe_stream(GOOD_BASE, GOOD_OUT, 1000, 0, 8, 64, 0) == ll.LL_ERR_INVALID  # not 16-byte words
+    assert ll.ll_probe_stream(GOOD_BASE, GOOD_OUT, 0, 0, 8, 64, 0) == ll.LL_ERR_INVALID
+    assert ll.ll_probe_stream(0, GOOD_OUT, 1024, 0, 8, 64, 0) == ll.LL_ERR_INVALID  # copy needs a source
+    assert ll.ll_probe_stream(GOOD_BASE, 0, 1024, 2, 8, 64, 0) == ll.LL_ERR_INVALID
+    assert ll.ll_probe_stream(GOOD_BASE + 8, GOOD_OUT, 1024, 0, 8, 64, 0) == ll.LL_ERR_INVALID  # misaligned
+    assert ll.ll_probe_stream(GOOD_BASE, GOOD_OUT, 1024, 0, 8, 96, 0) == ll.LL_ERR_INVALID
 
 
 def test_product_fails_loudly_without_the_library(tmp_path, monkeypatch):

@@ -388,7 +388,7 @@ def test_rs_ag_workgroups_past_the_last_tile(proto):
     assert_bits_equal(ag, oracle.allgather(rs), f"AG {proto} W=16")
 
 
-@pytest.mark.parametrize("lag", [1, 2, 5])
+@pytest.mark.parametrize("lag", [0, 1, 2, 5])
 def test_result_independent_of_pipeline_lag(lag):
     """Two-shot, ReduceScatter and AllGather give the same bits for every
     pipeline distance (and launch shape), on sizes with many steps."""

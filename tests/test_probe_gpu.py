@@ -70,3 +70,31 @@ def test_pingpong_completes():
     ticks, done, cycles = out.cpu().numpy().tolist()
     print(f"pingpong: {done} rounds, {ticks * 10 / max(done, 1):.0f} ns per round", flush=True)
     assert done == 500
+
+
+@pytest.mark.parametrize("grid", [1, 7, 512])
+def test_streaming_probe_moves_exactly_its_bytes(grid):
+    """The streaming probe copies src to dst word for word (mode 0), leaves dst
+    alone when it only reads (mode 1), writes its fill pattern (mode 2), and
+    stops at `bytes`, with grids smaller and larger than the word count."""
+    nbytes = 16 * 1000 + 16 * 37
+    n16 = nbytes // 16
+    g = torch.Generator(device="cuda")
+    g.manual_seed(5)
+    src = torch.randint(-2**31, 2**31 - 1, (n16 * 4,), dtype=torch.int32, device="cuda", generator=g)
+    dst = torch.full((n16 * 4 + 64,), 0x5A5A5A5A, dtype=torch.int32, device="cuda")
+    guard = dst[n16 * 4:].clone()
+    before = dst.clone()
+    assert ll.ll_probe_stream(src.data_ptr(), dst.data_ptr(), nbytes, 1, grid, 256, stream()) == ll.LL_OK
+    torch.cuda.synchronize()
+    assert torch.equal(dst, before)
+    assert ll.ll_probe_stream(src.data_ptr(), dst.data_ptr(), nbytes, 0, grid, 256, stream()) == ll.LL_OK
+    torch.cuda.synchronize()
+    assert torch.equal(dst[:n16 * 4], src)
+    assert torch.equal(dst[n16 * 4:], guard)
+    assert ll.ll_probe_stream(0, dst.data_ptr(), nbytes, 2, grid, 256, stream()) == ll.LL_OK
+    torch.cuda.synchronize()
+    words = dst[:n16 * 4].view(n16, 4).cpu().numpy().astype(np.int64) & 0xFFFFFFFF
+    assert np.array_equal(words[:, 0], np.arange(n16))
+    assert (words[:, 1] == 1).all() and (words[:, 2] == 2).all() and (words[:, 3] == 3).all()
+    assert torch.equal(dst[n16 * 4:], guard)
