@@ -241,26 +241,36 @@ struct Plan {
 };
 
 // Units per lane of the wave-per-peer kernels: fewer, fuller workgroups as
-// messages grow (measured at 64 KiB .. 8 MiB per rank, 2-8 ranks).  A line
-// unit is a whole wave; the two-shot AllReduce over lines takes two units
-// per lane once the P tiles of a step hold more than 1536 line units, the
-// other line kernels keep one.
-int wave_units_log2(int64_t units, int proto, bool twoshot_allreduce, int P) {
+// messages grow (measured at 64 KiB .. 8 MiB per rank, 2-8 ranks).
+//  - Lines (a line unit is a whole wave): the two-shot AllReduce takes two
+//    units per lane once the P tiles of a step hold more than 1536 line
+//    units; the other line kernels keep one.
+//  - Two-shot AllReduce over 8-byte packets or sentinel units: one unit per
+//    lane while every tile of a chunk gets a resident workgroup of its own
+//    (one round of tiles), else two.
+//  - The others: one unit per lane up to 64 tiles of 64 units, else two.
+int wave_units_log2(const Plan &pl, int wpr) {
   const int forced = g_wave_units.load();
   if (forced == 1) return 0;
   if (forced == 2) return 1;
   if (forced == 4) return 2;
-  if (proto == PR_LINE && twoshot_allreduce) return units * P <= 1536 ? 0 : 1;
-  if (units <= 64 * 64) return 0;
+  const bool twoshot_allreduce = pl.kind == K_TWOSHOT_WAVES;
+  if (pl.proto == PR_LINE && twoshot_allreduce) return pl.units * pl.P <= 1536 ? 0 : 1;
+  if (twoshot_allreduce) {
+    int cap = 0;
+    if (resident_grid(table().twaves[0][0][wpr][pl.dt][pl.P], 64 * pl.P, &cap) != LL_OK) return 1;
+    return (pl.units + 63) / 64 <= cap / pl.P ? 0 : 1;
+  }
+  if (pl.units <= 64 * 64) return 0;
   return 1;
 }
 
 int launch(const Plan &pl, void *stream) {
   const bool two_waves = pl.kind == K_TWOSHOT_WAVES || pl.kind == K_RS_WAVES || pl.kind == K_AG_WAVES;
   const bool wave_kernel = pl.kind == K_ONESHOT_WAVES || two_waves;
-  const int wlog = wave_kernel ? wave_units_log2(pl.units, pl.proto, pl.kind == K_TWOSHOT_WAVES, pl.P) : 0;
-  kernel_fn fn = nullptr;
   const int wpr = pl.proto == PR_SENT ? 1 : (pl.proto == PR_LINE ? 2 : 0);
+  const int wlog = wave_kernel ? wave_units_log2(pl, wpr) : 0;
+  kernel_fn fn = nullptr;
   if (pl.kind == K_ONESHOT_WAVES) {
     fn = table().waves[wlog][wpr][pl.dt][pl.P];
   } else if (two_waves) {
@@ -386,18 +396,26 @@ ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
     if (in_bytes <= 64 * KiB) return LL_ALGO_ONESHOT_WAVES;
     if (in_bytes <= 256 * KiB) return LL_ALGO_ONESHOT;
     if (in_bytes <= 1 * MiB) return LL_ALGO_ONESHOT_LINE_WAVES;
-    if (in_bytes <= 4 * MiB) return LL_ALGO_ONESHOT_LINE;
+    if (in_bytes <= 2 * MiB) return LL_ALGO_ONESHOT_LINE;
+    if (in_bytes <= 8 * MiB) return LL_ALGO_TWOSHOT_LINE_WAVES;
     return LL_ALGO_TWOSHOT_LINE;
   }
+  // the line two-shot with one wave per peer serves up to 8 MiB at 3-4 ranks
+  const uint64_t line_waves_max = (P <= 4 ? 8 : 4) * MiB;
   if (sentinel_ok) {
     if (in_bytes <= (P <= 4 ? 256 : 64) * KiB) return LL_ALGO_ONESHOT_SENTINEL_WAVES;
     if (in_bytes <= 2 * MiB) return LL_ALGO_TWOSHOT_SENTINEL_WAVES;
-    if (in_bytes <= 4 * MiB) return LL_ALGO_TWOSHOT_LINE_WAVES;
+    if (in_bytes <= line_waves_max) return LL_ALGO_TWOSHOT_LINE_WAVES;
     return LL_ALGO_TWOSHOT_LINE;
   }
-  if (in_bytes <= (P <= 4 ? 64 : 32) * KiB) return LL_ALGO_ONESHOT_WAVES;
-  if (in_bytes <= 128 * KiB) return LL_ALGO_TWOSHOT_WAVES;
-  if (in_bytes <= 4 * MiB) return LL_ALGO_TWOSHOT_LINE_WAVES;
+  if (P <= 4) {
+    if (in_bytes <= 64 * KiB) return LL_ALGO_ONESHOT_WAVES;
+    if (in_bytes <= 256 * KiB) return LL_ALGO_ONESHOT_LINE_WAVES;
+  } else {
+    if (in_bytes <= 32 * KiB) return LL_ALGO_ONESHOT_WAVES;
+    if (in_bytes <= 128 * KiB) return LL_ALGO_TWOSHOT_WAVES;
+  }
+  if (in_bytes <= line_waves_max) return LL_ALGO_TWOSHOT_LINE_WAVES;
   return LL_ALGO_TWOSHOT_LINE;
 }
 
