@@ -240,29 +240,26 @@ struct Plan {
   int64_t units;  // packet units per stream
 };
 
-// Units per lane of the wave-per-peer kernels: fewer, fuller workgroups as
-// messages grow (measured at 64 KiB .. 8 MiB per rank, 2-8 ranks).
-//  - Lines (a line unit is a whole wave): the two-shot AllReduce takes two
-//    units per lane once the P tiles of a step hold more than 1536 line
-//    units; the other line kernels keep one.
-//  - Two-shot AllReduce over 8-byte packets or sentinel units: one unit per
-//    lane while every tile of a chunk gets a resident workgroup of its own
-//    (one round of tiles), else two.
-//  - The others: one unit per lane up to 64 tiles of 64 units, else two.
+// Units per lane (U) of the wave-per-peer kernels, measured at 16 KiB ..
+// 4 MiB per rank and 2, 4 and 8 ranks.  One unit per lane, except in the
+// two-shot AllReduce once its tiles would need a second round of
+// workgroups, which costs a whole extra exchange:
+//  - lines (a line unit is a whole wave): two units per lane once the P
+//    tiles of a step hold more than 1536 line units;
+//  - 8-byte packets and sentinel units: two once a chunk has more tiles of
+//    64 units than resident workgroups per rank.
+// Elsewhere two units per lane are never more than about 3 % faster and up
+// to 25 % slower.
 int wave_units_log2(const Plan &pl, int wpr) {
   const int forced = g_wave_units.load();
   if (forced == 1) return 0;
   if (forced == 2) return 1;
   if (forced == 4) return 2;
-  const bool twoshot_allreduce = pl.kind == K_TWOSHOT_WAVES;
-  if (pl.proto == PR_LINE && twoshot_allreduce) return pl.units * pl.P <= 1536 ? 0 : 1;
-  if (twoshot_allreduce) {
-    int cap = 0;
-    if (resident_grid(table().twaves[0][0][wpr][pl.dt][pl.P], 64 * pl.P, &cap) != LL_OK) return 1;
-    return (pl.units + 63) / 64 <= cap / pl.P ? 0 : 1;
-  }
-  if (pl.units <= 64 * 64) return 0;
-  return 1;
+  if (pl.kind != K_TWOSHOT_WAVES) return 0;
+  if (pl.proto == PR_LINE) return pl.units * pl.P <= 1536 ? 0 : 1;
+  int cap = 0;
+  if (resident_grid(table().twaves[0][0][wpr][pl.dt][pl.P], 64 * pl.P, &cap) != LL_OK) return 1;
+  return (pl.units + 63) / 64 <= cap / pl.P ? 0 : 1;
 }
 
 int launch(const Plan &pl, void *stream) {
@@ -393,8 +390,7 @@ ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
       if (in_bytes <= 16 * MiB) return LL_ALGO_TWOSHOT_SENTINEL_WAVES;
       return LL_ALGO_TWOSHOT_LINE;
     }
-    if (in_bytes <= 64 * KiB) return LL_ALGO_ONESHOT_WAVES;
-    if (in_bytes <= 256 * KiB) return LL_ALGO_ONESHOT;
+    if (in_bytes <= 256 * KiB) return LL_ALGO_ONESHOT_WAVES;
     if (in_bytes <= 1 * MiB) return LL_ALGO_ONESHOT_LINE_WAVES;
     if (in_bytes <= 2 * MiB) return LL_ALGO_ONESHOT_LINE;
     if (in_bytes <= 8 * MiB) return LL_ALGO_TWOSHOT_LINE_WAVES;
@@ -409,8 +405,8 @@ ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
     return LL_ALGO_TWOSHOT_LINE;
   }
   if (P <= 4) {
-    if (in_bytes <= 64 * KiB) return LL_ALGO_ONESHOT_WAVES;
-    if (in_bytes <= 256 * KiB) return LL_ALGO_ONESHOT_LINE_WAVES;
+    if (in_bytes <= 128 * KiB) return LL_ALGO_ONESHOT_WAVES;
+    if (in_bytes <= 256 * KiB) return LL_ALGO_TWOSHOT_WAVES;
   } else {
     if (in_bytes <= 32 * KiB) return LL_ALGO_ONESHOT_WAVES;
     if (in_bytes <= 128 * KiB) return LL_ALGO_TWOSHOT_WAVES;
