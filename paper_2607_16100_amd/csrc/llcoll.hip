@@ -435,14 +435,15 @@ ll_proto auto_proto_rooted(uint64_t bytes, bool sentinel_ok) {
 
 // Stand-alone ReduceScatter / AllGather: the wave-per-peer kernels serve
 // each format up to the size where the one-lane-per-unit kernels catch up
-// (measured at 4 and 8 ranks): 8-byte packets up to 2 MiB of data per rank,
-// lines up to 4 MiB (8 MiB at 2-4 ranks), sentinel units up to 2 MiB.
-// ll_set_wave_kernels forces either family.
-bool use_wave_kernel(ll_proto proto, uint64_t bytes, int P) {
+// (measured at 4 and 8 ranks): 8-byte packets and sentinel units up to
+// 2 MiB of data per rank; lines up to 8 MiB at 2-4 ranks, and at 5-8 ranks
+// up to 4 MiB (ReduceScatter) or 2 MiB (AllGather).  ll_set_wave_kernels
+// forces either family.
+bool use_wave_kernel(ll_proto proto, uint64_t bytes, int P, bool allgather) {
   const int m = g_wave_kernels.load();
   if (m != 0) return m == 2;
   const uint64_t MiB = 1024 * 1024;
-  if (proto == LL_PROTO_LINE128) return bytes <= (P >= 5 ? 4 : 8) * MiB;
+  if (proto == LL_PROTO_LINE128) return bytes <= (P >= 5 ? (allgather ? 2 : 4) : 8) * MiB;
   return bytes <= 2 * MiB;
 }
 
@@ -739,7 +740,7 @@ int ll_reduce_scatter_proto(void *sym_base, size_t rank_stride, void *out, size_
   if (recvcount == 0) return LL_OK;
   if (proto == LL_PROTO_AUTO) proto = auto_proto(in_bytes, nranks, g_auto_sentinel.load() != 0);
   Plan pl;
-  pl.kind = use_wave_kernel(proto, in_bytes, nranks) ? K_RS_WAVES : K_RS;
+  pl.kind = use_wave_kernel(proto, in_bytes, nranks, false) ? K_RS_WAVES : K_RS;
   pl.dt = (int)dt;
   pl.P = nranks;
   pl.proto = proto == LL_PROTO_LINE128 ? PR_LINE : (proto == LL_PROTO_SENTINEL ? PR_SENT : PR_LL);
@@ -775,7 +776,7 @@ int ll_allgather_proto(void *sym_base, size_t rank_stride, void *out, size_t sen
   if (sendcount == 0) return LL_OK;
   if (proto == LL_PROTO_AUTO) proto = auto_proto(in_bytes * nranks, nranks, g_auto_sentinel.load() != 0);
   Plan pl;
-  pl.kind = use_wave_kernel(proto, in_bytes * nranks, nranks) ? K_AG_WAVES : K_AG;
+  pl.kind = use_wave_kernel(proto, in_bytes * nranks, nranks, true) ? K_AG_WAVES : K_AG;
   pl.dt = (int)dt;
   pl.P = nranks;
   pl.proto = proto == LL_PROTO_LINE128 ? PR_LINE : (proto == LL_PROTO_SENTINEL ? PR_SENT : PR_LL);
