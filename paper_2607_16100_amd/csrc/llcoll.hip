@@ -8,7 +8,9 @@
 
 #include <algorithm>
 #include <atomic>
+#include <map>
 #include <mutex>
+#include <tuple>
 #include <type_traits>
 
 #include "../../include/llcoll.h"
@@ -194,19 +196,34 @@ int device_info(DevInfo *out) {
   return LL_OK;
 }
 
+// Workgroups of `fn` resident per CU with `threads` per workgroup, by device;
+// filled on first use (one occupancy query per kernel shape and device).
+std::map<std::tuple<int, const void *, int>, int> g_per_cu;  // guarded by g_mu
+
 // Largest grid of `fn` that is resident at once with `threads` per workgroup.
 int resident_grid(kernel_fn fn, int threads, int *grid_out) {
   DevInfo d;
   int st = device_info(&d);
   if (st != LL_OK) return st;
-  int per_cu = 0;
-  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(fn), threads, 0);
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) {
     t_last_hip = (int)e;
     return LL_ERR_HIP;
   }
-  if (per_cu < 1) per_cu = 1;
-  *grid_out = per_cu * d.cus;
+  const auto key = std::make_tuple(dev, reinterpret_cast<const void *>(fn), threads);
+  std::lock_guard<std::mutex> lk(g_mu);
+  auto it = g_per_cu.find(key);
+  if (it == g_per_cu.end()) {
+    int per_cu = 0;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(fn), threads, 0);
+    if (e != hipSuccess) {
+      t_last_hip = (int)e;
+      return LL_ERR_HIP;
+    }
+    it = g_per_cu.emplace(key, per_cu < 1 ? 1 : per_cu).first;
+  }
+  *grid_out = it->second * d.cus;
   return LL_OK;
 }
 
