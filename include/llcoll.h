@@ -281,9 +281,10 @@ const char *ll_strerror(int status);
 int ll_set_auto_sentinel(int allow);
 
 /* Kernel family of the stand-alone ReduceScatter / AllGather: 0 = by size
- * (one wave per peer with LDS staging up to 1-2 MiB of data per rank, one
- * lane per packet unit above), 1 = one lane per unit always, 2 = one wave per
- * peer always.  Results do not depend on it. */
+ * (one wave per peer with LDS staging up to 2-8 MiB of data per rank, by
+ * packet format and rank count; one lane per packet unit above), 1 = one lane
+ * per unit always, 2 = one wave per peer always.  Results do not depend on
+ * it. */
 int ll_set_wave_kernels(int mode);
 
 /* Workgroups per rank and threads per workgroup for the following calls;
@@ -303,8 +304,11 @@ int ll_set_poll_pacing(int first_wait, int poll_gap);
  * lag in [0, 64]; default 1. */
 int ll_set_pipeline_lag(int lag);
 
-/* Packet units (16 bytes of packets) per lane of LL_ALGO_ONESHOT_WAVES for
- * the following calls: 1, 2 or 4; 0 = automatic. */
+/* Packet units per lane of the wave-per-peer kernels (one-shot, two-shot,
+ * stand-alone ReduceScatter / AllGather) for the following calls: 1, 2 or 4;
+ * 0 = automatic (one, or two for a two-shot AllReduce whose tiles exceed one
+ * round of resident workgroups).  A unit is one 16-byte store per lane, or a
+ * whole 128-byte-line unit per wave.  Results do not depend on it. */
 int ll_set_wave_units(int units_per_lane);
 
 /* Flag-wait budget in ticks of the 100 MHz constant clock (default 2e8,
