@@ -191,6 +191,9 @@ def bench_floor(torch, ll, steps, warmup, grid, threads):
     r = res.cpu().numpy()
     out["hbm_dependent_load_us"] = float(r[0]) * TICK_US / 2000
     out["hbm_dependent_load_cycles"] = float(r[1]) / 2000
+    # the floor composed from its two parts (empty-kernel interval plus one
+    # dependent HBM load); the directly measured floor above is the denominator
+    out["composed_p50_us"] = out["empty"]["p50_us"] + out["hbm_dependent_load_us"]
     del chase
     return out
 
