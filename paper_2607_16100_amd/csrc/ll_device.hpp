@@ -296,6 +296,18 @@ struct ProtoLine {
     }
     return v;
   }
+  // Payload word `wd` (0..239) of a unit: the lane and word slot that carry
+  // it in packet order.
+  __device__ static __forceinline__ void slot_of_word(int wd, int *lane, int *slot) {
+    const int l = wd >> 2;
+    if ((l & 3) == 3 && (wd & 3) == 3) {
+      *lane = 60 + (l >> 4);
+      *slot = (l >> 2) & 3;
+    } else {
+      *lane = l;
+      *slot = wd & 3;
+    }
+  }
   // Called with the whole wave active; w is in packet order.
   template <int DT>
   __device__ static __forceinline__ void store(char *base, int64_t u, int sub, int64_t nelem, bool al4, u32x4 w) {

@@ -488,9 +488,32 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
     }
     lds_barrier();
     LL_WAVE_PHASE(2, now_ticks());
-    if constexpr (WU::kWave) {
-      // line units are in packet order: the own-rank wave sums its lanes'
-      // words and stores whole units (the store puts displaced words back)
+    if constexpr (WU::kWave && 64 * P >= 240 * U) {
+      // line units are staged in packet order; with a thread per payload
+      // word of the tile (U units of 240 words), thread t forms word t from
+      // the lane and slot that carry it and stores it
+      const int t = (int)threadIdx.x;
+      if (t < 240 * U) {
+        const int k = t / 240;
+        const int wd = t - 240 * k;
+        int sl, sj;
+        Pr::slot_of_word(wd, &sl, &sj);
+        const int at = (k * 64 + sl) * EPU + sj * K;
+        float acc[K];
+#pragma unroll
+        for (int e = 0; e < K; ++e) acc[e] = stage[0][at + e];
+#pragma unroll
+        for (int p = 1; p < P; ++p) {
+#pragma unroll
+          for (int e = 0; e < K; ++e) acc[e] = acc[e] + stage[p][at + e];
+        }
+        const u32x4 res = {Elem<DT>::narrow(acc), 0u, 0u, 0u};
+        store_words<DT>(out_r, (int64_t)WU::unit(tile, k, 0) * 240 + wd, 1, n, a.al4 != 0, res);
+      }
+    } else if constexpr (WU::kWave) {
+      // fewer threads than words: the own-rank wave sums its lanes' words in
+      // packet order and stores whole units (the store puts displaced words
+      // back)
       if (q == r) {
 #pragma unroll
         for (int k = 0; k < U; ++k) {
