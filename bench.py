@@ -103,7 +103,8 @@ def bench_headline(torch, ll, steps, warmup):
     reg.init()
     reg.write_inputs(x)
     s = reg.stream_handle()
-    # the configuration's path, named explicitly (it is also what AUTO picks here)
+    # the configuration's path, named explicitly: one-shot with 8-byte packets
+    # (AUTO takes the line one-shot here, reported below with the other formats)
     algo = ll.LL_ALGO_ONESHOT_WAVES
     epoch = [1]
 

@@ -421,11 +421,14 @@ ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
     if (in_bytes <= line_waves_max) return LL_ALGO_TWOSHOT_LINE_WAVES;
     return LL_ALGO_TWOSHOT_LINE;
   }
+  // the line one-shot sums a word per thread from 4 ranks up (64*P threads
+  // for 240 words), which makes it the faster one-shot from 16 KiB
   if (P <= 4) {
-    if (in_bytes <= 128 * KiB) return LL_ALGO_ONESHOT_WAVES;
-    if (in_bytes <= 256 * KiB) return LL_ALGO_TWOSHOT_WAVES;
+    if (in_bytes <= (P == 4 ? 64 : 128) * KiB) return LL_ALGO_ONESHOT_WAVES;
+    if (in_bytes <= 256 * KiB) return P == 4 ? LL_ALGO_ONESHOT_LINE_WAVES : LL_ALGO_TWOSHOT_WAVES;
   } else {
-    if (in_bytes <= 32 * KiB) return LL_ALGO_ONESHOT_WAVES;
+    if (in_bytes <= 8 * KiB) return LL_ALGO_ONESHOT_WAVES;
+    if (in_bytes <= 32 * KiB) return LL_ALGO_ONESHOT_LINE_WAVES;
     if (in_bytes <= 128 * KiB) return LL_ALGO_TWOSHOT_WAVES;
   }
   if (in_bytes <= line_waves_max) return LL_ALGO_TWOSHOT_LINE_WAVES;

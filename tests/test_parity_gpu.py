@@ -133,11 +133,11 @@ def test_allreduce_special_values(algo, dtype):
 
 
 # ------------------------------------------------------------ configuration C2
-@pytest.mark.parametrize("algo", ["oneshot", "auto"])
+@pytest.mark.parametrize("algo", ["oneshot", "oneshot_waves", "auto"])
 def test_c2_oneshot_bf16_16k_10k_calls(algo):
     """8 ranks, bfloat16, 8192 normal(0,1) elements per rank, one-shot with
-    8-byte packets (AUTO: the wave-per-peer kernel the benchmark times),
-    10,000 back-to-back calls with the epoch incremented."""
+    8-byte packets (and AUTO, which takes the line one-shot with one wave per
+    peer here), 10,000 back-to-back calls with the epoch incremented."""
     p, n = 8, 8192
     x = wl.normal(p, n, "bf16", sigma=1.0, seed=0)
     want = oracle.allreduce(x)
