@@ -300,12 +300,13 @@ __global__ __launch_bounds__(1024) void k_oneshot(KArgs ka) {
 }
 
 // ---------------------------------------------------------------------------
-// One-shot AllReduce, one wave per peer, with LDS staging (8-byte packets or
-// sentinel units).
+// One-shot AllReduce, one wave per peer, with LDS staging (8-byte packets,
+// sentinel units or 128-byte lines).
 //
 // A workgroup has P waves and handles tiles of 64*U packet units (lane l owns
 // units l, l+64, ..., l+64(U-1) of the tile, so every memory instruction of a
-// wave covers 64 units).  For a tile, wave q != r sends the rank's units to
+// wave covers 64 units; with lines a tile is U line units, each a whole
+// wave).  For a tile, wave q != r sends the rank's units to
 // peer q only and then polls only the units peer q sent to this rank; wave r
 // keeps the rank's own values.  Each wave stages its rank's values, widened
 // to binary32, in LDS row q; after a workgroup barrier the rows are summed in
