@@ -184,6 +184,16 @@ int ll_allreduce(void *sym_base, size_t rank_stride, void *out, size_t count, ll
 int ll_allreduce_algo(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt,
                       ll_op op, int nranks, uint32_t epoch, void *stream, ll_algo algo);
 
+/* The algorithm that LL_ALGO_AUTO runs for a single-call AllReduce
+ * (ll_allreduce) of `count` elements of `dt` per rank over `nranks` ranks,
+ * under the current ll_set_auto_sentinel setting, written to *algo.  The
+ * choice follows measured crossovers on the MI355X: one-shot with one wave
+ * per peer for small messages, the two-shot wave kernels for medium ones,
+ * the line two-shot for large ones.  Host only, no HIP call.
+ * LL_ERR_INVALID: algo NULL or nranks outside [2, 8]; LL_ERR_UNSUPPORTED:
+ * unknown dtype. */
+int ll_auto_algo(size_t count, ll_dtype dt, int nranks, ll_algo *algo);
+
 /* ReduceScatter (sum): rank r's input is nranks*recvcount elements; rank r
  * receives elements [r*recvcount, (r+1)*recvcount) of the sum (Sec. III-A). */
 int ll_reduce_scatter(void *sym_base, size_t rank_stride, void *out, size_t recvcount,

@@ -634,6 +634,13 @@ int ll_allreduce_algo(void *sym_base, size_t rank_stride, void *out, size_t coun
   return launch(pl, stream);
 }
 
+int ll_auto_algo(size_t count, ll_dtype dt, int nranks, ll_algo *algo) {
+  if (algo == nullptr || nranks < 2 || nranks > LL_MAX_RANKS) return LL_ERR_INVALID;
+  if ((int)dt != LL_F32 && (int)dt != LL_BF16) return LL_ERR_UNSUPPORTED;
+  *algo = auto_algo((uint64_t)count * esize_of(dt), nranks, g_auto_sentinel.load() != 0);
+  return LL_OK;
+}
+
 int ll_allreduce(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt, ll_op op, int nranks,
                  uint32_t epoch, void *stream) {
   return ll_allreduce_algo(sym_base, rank_stride, out, count, dt, op, nranks, epoch, stream, LL_ALGO_AUTO);

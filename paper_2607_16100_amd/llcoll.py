@@ -65,6 +65,7 @@ _SIGS = {
     "ll_set_wave_kernels": (_i, [_i]),
     "ll_allreduce": (_i, [_vp, _sz, _vp, _sz, _i, _i, _i, _u32, _vp]),
     "ll_allreduce_algo": (_i, [_vp, _sz, _vp, _sz, _i, _i, _i, _u32, _vp, _i]),
+    "ll_auto_algo": (_i, [_sz, _i, _i, _vp]),
     "ll_reduce_scatter": (_i, [_vp, _sz, _vp, _sz, _i, _i, _i, _u32, _vp]),
     "ll_reduce_scatter_proto": (_i, [_vp, _sz, _vp, _sz, _i, _i, _i, _u32, _vp, _i]),
     "ll_allgather": (_i, [_vp, _sz, _vp, _sz, _i, _i, _u32, _vp]),
@@ -162,6 +163,12 @@ def ll_allreduce(sym_base, rank_stride, out, count, dt, op, nranks, epoch, strea
 
 def ll_allreduce_algo(sym_base, rank_stride, out, count, dt, op, nranks, epoch, stream, algo):
     return _lib.ll_allreduce_algo(sym_base, rank_stride, out, count, dt, op, nranks, epoch, stream, algo)
+
+
+def ll_auto_algo(count: int, dt: int, nranks: int):
+    out = ctypes.c_int(-1)
+    st = _lib.ll_auto_algo(count, dt, nranks, ctypes.byref(out))
+    return st, out.value
 
 
 def ll_reduce_scatter(sym_base, rank_stride, out, recvcount, dt, op, nranks, epoch, stream):

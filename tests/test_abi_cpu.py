@@ -275,3 +275,45 @@ def test_product_fails_loudly_without_the_library(tmp_path, monkeypatch):
     mod = importlib.util.module_from_spec(spec)
     with pytest.raises(ImportError):
         spec.loader.exec_module(mod)
+
+
+def test_auto_algo_choices():
+    """AUTO's choice (host logic only): the measured crossovers at the
+    configurations' sizes, and one-way crossovers from one-shot to two-shot as
+    messages grow."""
+    A = ll.ALGOS
+    f32, bf16 = ll.LL_F32, ll.LL_BF16
+    assert ll.ll_set_auto_sentinel(0) == ll.LL_OK
+    assert ll.ll_auto_algo(4096, bf16, 8) == (ll.LL_OK, A["oneshot_waves"])            # 8 KiB
+    assert ll.ll_auto_algo(8192, bf16, 8) == (ll.LL_OK, A["oneshot_line_waves"])       # C2, 16 KiB
+    assert ll.ll_auto_algo(64 * 8192, bf16, 8) == (ll.LL_OK, A["twoshot_line_waves"])  # C3, 1 MiB
+    assert ll.ll_auto_algo(16 << 20, f32, 8) == (ll.LL_OK, A["twoshot_line"])          # C4, 64 MiB
+    assert ll.ll_auto_algo(1024, f32, 4) == (ll.LL_OK, A["oneshot_waves"])             # C1
+    assert ll.ll_set_auto_sentinel(1) == ll.LL_OK
+    try:
+        assert ll.ll_auto_algo(8192, bf16, 8) == (ll.LL_OK, A["oneshot_sentinel_waves"])
+        assert ll.ll_auto_algo(64 * 8192, bf16, 8) == (ll.LL_OK, A["twoshot_sentinel_waves"])
+        assert ll.ll_auto_algo(16 << 20, f32, 8) == (ll.LL_OK, A["twoshot_line"])
+    finally:
+        assert ll.ll_set_auto_sentinel(0) == ll.LL_OK
+    assert ll.ll_auto_algo(1, f32, 1)[0] == ll.LL_ERR_INVALID
+    assert ll.ll_auto_algo(1, f32, 9)[0] == ll.LL_ERR_INVALID
+    assert ll.ll_auto_algo(1, 7, 8)[0] == ll.LL_ERR_UNSUPPORTED
+    names = {v: k for k, v in A.items()}
+    for sentinel in (0, 1):
+        assert ll.ll_set_auto_sentinel(sentinel) == ll.LL_OK
+        for p in range(2, 9):
+            for dt, es in ((f32, 4), (bf16, 2)):
+                seen_twoshot = False
+                for k in range(0, 29):
+                    st, algo = ll.ll_auto_algo((1 << k) // es or 1, dt, p)
+                    assert st == ll.LL_OK
+                    name = names[algo]
+                    assert name not in ("auto", "twoshot_sentinel_out", "twoshot_atomic")
+                    if sentinel == 0:
+                        assert "sentinel" not in name
+                    if name.startswith("twoshot"):
+                        seen_twoshot = True
+                    else:
+                        assert not seen_twoshot, f"P={p} {2**k} bytes: one-shot after two-shot"
+    assert ll.ll_set_auto_sentinel(0) == ll.LL_OK
