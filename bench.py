@@ -648,6 +648,9 @@ def main():
                     "traffic": traffic_from_profiles(khash, bw["grid"] * bw["threads"]),
                     "kernel": "k_twoshot<ProtoLine, f32, 8> (64 MiB per rank)",
                     "kernel_us": round(bw["kernel_us"], 2), "algorithmic_bytes": bw["algorithmic_bytes"]}
+        if roofline["traffic"]:
+            # the counters' bytes (FETCH_SIZE + WRITE_SIZE, calibrated) over the same kernel time
+            roofline["traffic_gbps"] = round(roofline["traffic"] / bw["kernel_us"] / 1e3, 1)
         probe = result.get("copy", {}).get("streaming_probe", {}).get("copy")
         if probe:
             # the best plain streaming copy on the same GPU: what a simple kernel reaches
