@@ -405,6 +405,8 @@ def bench_bandwidth(torch, ll, count, algos, iters=20, warmup=3):
     from paper_2607_16100_amd.region import SymRegion
 
     p = 8
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()  # fresh device allocations, as for the copy reference
     reg = SymRegion(p, count, "f32", out_elems=p * count)
     reg.init()
     # inputs generated on the device from a seeded torch generator (the values
@@ -437,15 +439,23 @@ def bench_bandwidth(torch, ll, count, algos, iters=20, warmup=3):
     return res
 
 
-def bench_copy(torch, ll, nbytes=1 << 30, iters=10):
+def bench_copy(torch, ll, nbytes=1 << 30, iters=20, placements=3):
     """HBM bandwidth of plain streaming kernels over `nbytes`: torch's
     device-to-device copy, and the library's streaming probe (16-byte
     non-temporal loads and stores, grid-stride) as a copy, a read and a write,
-    each at the best of a sweep of grid sizes.  This is the rate a simple
-    kernel reaches on this GPU, the practical ceiling under the 8 TB/s peak."""
-    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
-    dst = torch.empty_like(src)
-    src.fill_(1)
+    each at the best over grid sizes and, for the copy, over `placements`
+    separately allocated source/destination pairs (where the two buffers
+    sit moves a copy's rate by up to 10 %).  This is the rate a simple kernel
+    reaches on this GPU, the practical ceiling under the 8 TB/s peak."""
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()  # fresh device allocations, not blocks the earlier legs left cached
+    pairs = []
+    for _ in range(placements):
+        src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        dst = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        src.fill_(1)
+        pairs.append((src, dst))
+    src, dst = pairs[0]
     for _ in range(3):
         dst.copy_(src)
     torch.cuda.synchronize()
@@ -460,22 +470,26 @@ def bench_copy(torch, ll, nbytes=1 << 30, iters=10):
     res = {"bytes": nbytes, "kernel_us": us, "gbps": 2.0 * nbytes / us / 1e3}
     s = stream.cuda_stream
     probe = {}
+    grids = (512, 768, 1024, 1536, 2048, 4096, 8192, 16384)
     for mode, name, moved in ((0, "copy", 2), (1, "read", 1), (2, "write", 1)):
         best = None
-        for grid in (512, 1024, 2048, 4096, 8192, 16384):
-            ll.check(ll.ll_probe_stream(src.data_ptr(), dst.data_ptr(), nbytes, mode, grid, 256, s), "stream")
+        shapes = [(0, g) for g in grids] + ([(i, g) for i in range(1, placements) for g in (512, 1024, 2048)]
+                                            if mode == 0 else [])
+        for pair, grid in shapes:
+            a, b = pairs[pair]
+            ll.check(ll.ll_probe_stream(a.data_ptr(), b.data_ptr(), nbytes, mode, grid, 256, s), "stream")
             e0.record(stream)
             for _ in range(iters):
-                ll.check(ll.ll_probe_stream(src.data_ptr(), dst.data_ptr(), nbytes, mode, grid, 256, s), "stream")
+                ll.check(ll.ll_probe_stream(a.data_ptr(), b.data_ptr(), nbytes, mode, grid, 256, s), "stream")
             e1.record(stream)
             torch.cuda.synchronize()
             t = e0.elapsed_time(e1) * 1000.0 / iters
             gbps = moved * nbytes / t / 1e3
             if best is None or gbps > best["gbps"]:
-                best = {"gbps": gbps, "kernel_us": t, "grid": grid, "threads": 256}
+                best = {"gbps": gbps, "kernel_us": t, "grid": grid, "threads": 256, "placement": pair}
         probe[name] = best
     res["streaming_probe"] = probe
-    del src, dst
+    del pairs, src, dst
     return res
 
 
@@ -609,6 +623,10 @@ def main():
                                                                 "oneshot_line", "oneshot", "oneshot_sentinel"],
                                        iters=args.bw_iters)
         log(json.dumps(result["bw"]))
+    if want("copy"):
+        log("device copy reference (right after the bandwidth leg, in the same state of the chip)")
+        result["copy"] = bench_copy(torch, ll)
+        log(json.dumps(result["copy"]))
     if want("c3"):
         log("C3: 1 MiB bf16, two-shot vs one-shot")
         result["c3"] = bench_c3(torch, ll, min(args.steps, 2000))
@@ -628,10 +646,6 @@ def main():
         log("C4 sweep")
         fl0 = result.get("floor", {}).get("floor", {}).get("p50_us")
         result["sweep_file"] = bench_sweep(torch, ll, args.sweep, fl0)
-    if want("copy"):
-        log("device copy reference")
-        result["copy"] = bench_copy(torch, ll)
-        log(json.dumps(result["copy"]))
     if want("cpu"):
         log("cpu baseline")
         result["cpu"] = bench_cpu_baseline(args.cpu_seconds)
