@@ -156,6 +156,70 @@ def test_c2_oneshot_bf16_16k_10k_calls(algo):
     assert reg.epoch == 10_000
 
 
+@pytest.mark.parametrize("algo", ["oneshot_waves", "auto", "oneshot_line_waves", "twoshot_line"])
+def test_benchmark_launch_loop_is_exact(algo):
+    """The C-side launch loop the benchmark times (ll_bench_allreduce): 2000
+    back-to-back calls on the 16 KiB, 8-rank workload with epochs 1..2000,
+    the last ten with per-workgroup stamps, leave the oracle's result and no
+    timed-out wait; every stamped workgroup ends after it starts."""
+    p, n = 8, 8192
+    x = wl.normal(p, n, "bf16", sigma=1.0, seed=0)
+    want = oracle.allreduce(x)
+    reg = SymRegion(p, n, "bf16")
+    reg.init()
+    reg.write_inputs(x)
+    s = reg.stream_handle()
+    code = ll.ALGOS[algo]
+    say(f"bench loop {algo}: 1990 calls")
+    st = ll.ll_bench_allreduce(reg.base, reg.rank_stride, reg.out_ptr, n, ll.LL_BF16, p, reg.epoch + 1, 1990, code,
+                               0, 0, s)
+    assert st == ll.LL_OK, ll.ll_strerror(st)
+    reg.epoch += 1990
+    assert ll.ll_check(s) == ll.LL_OK
+    grid, _ = ll.ll_last_grid()
+    stamps = torch.zeros(10 * 2 * grid, dtype=torch.int64, device="cuda")
+    say(f"bench loop {algo}: 10 stamped calls, grid {grid}")
+    st = ll.ll_bench_allreduce(reg.base, reg.rank_stride, reg.out_ptr, n, ll.LL_BF16, p, reg.epoch + 1, 10, code,
+                               stamps.data_ptr(), 2 * grid, s)
+    assert st == ll.LL_OK, ll.ll_strerror(st)
+    reg.epoch += 10
+    assert ll.ll_check(s) == ll.LL_OK
+    got = reg.read_out(p * n, np.uint16).reshape(p, n)
+    assert_bits_equal(got, want, f"bench loop {algo}")
+    t = stamps.view(10, 2, grid).cpu().numpy()
+    assert (t[:, 0] > 0).all() and (t[:, 1] >= t[:, 0]).all()
+
+
+@pytest.mark.parametrize("proto", PROTOS)
+def test_benchmark_rs_ag_loops_are_exact(proto):
+    """ll_bench_reduce_scatter / ll_bench_allgather, 500 calls each at C5's
+    b=1 shape (8 ranks, 7168 bf16 per rank), leave the oracle's result."""
+    p, total = 8, 7168
+    m = total // p
+    x = wl.normal(p, total, "bf16", sigma=1.0, seed=4)
+    reg = SymRegion(p, total, "bf16", out_elems=p * total)
+    reg.init()
+    s = reg.stream_handle()
+    reg.write_inputs(x)
+    say(f"bench RS loop {proto}")
+    st = ll.ll_bench_reduce_scatter(reg.base, reg.rank_stride, reg.out_ptr, m, ll.LL_BF16, p, reg.epoch + 1, 500,
+                                    ll.PROTOS[proto], 0, 0, s)
+    assert st == ll.LL_OK, ll.ll_strerror(st)
+    reg.epoch += 500
+    assert ll.ll_check(s) == ll.LL_OK
+    rs = reg.read_out(p * m, np.uint16).reshape(p, m)
+    assert_bits_equal(rs, oracle.reduce_scatter(x), f"bench RS loop {proto}")
+    reg.write_inputs(rs)
+    say(f"bench AG loop {proto}")
+    st = ll.ll_bench_allgather(reg.base, reg.rank_stride, reg.out_ptr, m, ll.LL_BF16, p, reg.epoch + 1, 500,
+                               ll.PROTOS[proto], 0, 0, s)
+    assert st == ll.LL_OK, ll.ll_strerror(st)
+    reg.epoch += 500
+    assert ll.ll_check(s) == ll.LL_OK
+    ag = reg.read_out(p * p * m, np.uint16).reshape(p, p * m)
+    assert_bits_equal(ag, oracle.allreduce(x), f"bench AG loop {proto}")
+
+
 @pytest.mark.parametrize("algo", AR_ALGOS)
 def test_changing_inputs_never_return_stale_packets(algo):
     """New inputs every call (seed r + 1000 k): a packet left from an earlier
