@@ -276,12 +276,17 @@ struct ProtoLine {
   __device__ static __forceinline__ uint32_t from_lane(int src, uint32_t v) {
     return (uint32_t)__builtin_amdgcn_ds_bpermute(src * 4, (int)v);
   }
-  // Called with the whole wave active (a unit is one wave).
+  // The load in two halves, so that a caller can put independent work
+  // between the memory load and the lane permutes that wait for it: load_raw
+  // loads the data lanes' words, finish_load (whole wave active) moves the
+  // displaced words into the extra lanes.
   template <int DT, bool NT = true>
-  __device__ static __forceinline__ u32x4 load(const char *base, int64_t u, int sub, int64_t nelem, bool al4) {
-    const int64_t w0 = 240 * u;
+  __device__ static __forceinline__ u32x4 load_raw(const char *base, int64_t u, int sub, int64_t nelem, bool al4) {
     u32x4 v = {0u, 0u, 0u, 0u};
-    if (sub < 60) v = load_words<DT, NT>(base, w0 + 4 * sub, 4, nelem, al4);
+    if (sub < 60) v = load_words<DT, NT>(base, 240 * u + 4 * sub, 4, nelem, al4);
+    return v;
+  }
+  __device__ static __forceinline__ u32x4 finish_load(u32x4 v, int sub) {
     // extra lane 60+i collects the last word of the flag lanes of quads 4i..4i+3
     const int i = (sub - 60) & 3;
     const uint32_t d0 = from_lane(16 * i + 3, v.w);
@@ -295,6 +300,11 @@ struct ProtoLine {
       v.w = i < 3 ? d3 : 0u;
     }
     return v;
+  }
+  // Called with the whole wave active (a unit is one wave).
+  template <int DT, bool NT = true>
+  __device__ static __forceinline__ u32x4 load(const char *base, int64_t u, int sub, int64_t nelem, bool al4) {
+    return finish_load(load_raw<DT, NT>(base, u, sub, nelem, al4), sub);
   }
   // Payload word `wd` (0..239) of a unit: the lane and word slot that carry
   // it in packet order.

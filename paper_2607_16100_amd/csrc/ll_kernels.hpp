@@ -379,11 +379,24 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
   // than there are tiles; a workgroup past the last tile (a forced launch
   // shape) loads and stores nothing, since every access is guarded by the
   // unit count.
+  // For lines the load comes in two halves (memory, then lane permutes that
+  // wait for it); the store set-up below goes between them, while the load
+  // is in flight.
   auto load_tile = [&](uint32_t tile, u32x4 *own) {
 #pragma unroll
     for (int k = 0; k < U; ++k) {
       const uint32_t u = (uint32_t)WU::unit(tile, k, lane);
-      own[k] = u < units ? Pr::template load<DT, false>(in_r, u, sub, n, in_al4) : u32x4{0u, 0u, 0u, 0u};
+      if constexpr (WU::kWave) {
+        own[k] = u < units ? Pr::template load_raw<DT, false>(in_r, u, sub, n, in_al4) : u32x4{0u, 0u, 0u, 0u};
+      } else {
+        own[k] = u < units ? Pr::template load<DT, false>(in_r, u, sub, n, in_al4) : u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+  };
+  auto finish_tile = [&](u32x4 *own) {
+    if constexpr (WU::kWave) {
+#pragma unroll
+      for (int k = 0; k < U; ++k) own[k] = Pr::finish_load(own[k], sub);
     }
   };
   uint32_t tile = w;
@@ -409,6 +422,7 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
       st_pkt(rd, u < units && publish ? WU::off(u, lane) : kNowhere, Pr::pack(own[k], a.epoch, sub));
     }
   };
+  finish_tile(own);
   store_tile(tile, own);
 
   const uint32_t W = a.grid / P;
@@ -552,6 +566,7 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
     if (tile >= tiles) break;
     lds_barrier();  // the next tile overwrites the staging rows
     load_tile(tile, own);
+    finish_tile(own);
     store_tile(tile, own);
   }
   stamp_end(a, t_start);
