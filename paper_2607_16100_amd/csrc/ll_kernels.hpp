@@ -809,13 +809,18 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
   const char *in_it = in_r;
   uint64_t area = a.area;
   uint32_t epoch = a.epoch;
-  auto in_chunk = [&](uint32_t c) -> const char * { return Mode == 2 ? in_it : in_it + (uint64_t)c * C * E; };
-  auto chunk_len = [&](uint32_t c) -> int64_t {
-    const int64_t left = n_all - (int64_t)c * C;
-    return left < 0 ? 0 : (left < C ? left : C);
+  // Element counts and chunk byte offsets fit 32 bits (an input is at most
+  // 256 MiB), which keeps the set-up before the first packet store short.
+  auto in_chunk = [&](uint32_t c) -> const char * {
+    return Mode == 2 ? in_it : in_it + (uint64_t)(c * (uint32_t)(C * E));
   };
-  // unit and tile indices fit 32 bits: a call's slots span less than 4 GiB
-  uint32_t units = (uint32_t)Pr::units((C * E + 3) / 4);
+  auto chunk_len = [&](uint32_t c) -> int64_t {
+    const int32_t left = (int32_t)n_all - (int32_t)(c * (uint32_t)C);
+    return left < 0 ? 0 : (left < (int32_t)C ? left : (int32_t)C);
+  };
+  // unit and tile indices fit 32 bits: a call's slots span less than 4 GiB;
+  // the first iteration's unit count comes from the host
+  uint32_t units = (uint32_t)a.units;
   // Every packet store is issued, at an offset past the slot when there is
   // nothing to send (the own rank, a unit past the end, a muted rank), and no
   // store is branched around: a branch would leave the input load pending on
