@@ -809,17 +809,15 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
   const char *in_it = in_r;
   uint64_t area = a.area;
   uint32_t epoch = a.epoch;
-  // Element counts and chunk byte offsets fit 32 bits (an input is at most
-  // 256 MiB), which keeps the set-up before the first packet store short.
-  auto in_chunk = [&](uint32_t c) -> const char * {
-    return Mode == 2 ? in_it : in_it + (uint64_t)(c * (uint32_t)(C * E));
-  };
+  auto in_chunk = [&](uint32_t c) -> const char * { return Mode == 2 ? in_it : in_it + (uint64_t)c * C * E; };
   auto chunk_len = [&](uint32_t c) -> int64_t {
-    const int32_t left = (int32_t)n_all - (int32_t)(c * (uint32_t)C);
-    return left < 0 ? 0 : (left < (int32_t)C ? left : (int32_t)C);
+    const int64_t left = n_all - (int64_t)c * C;
+    return left < 0 ? 0 : (left < C ? left : C);
   };
-  // unit and tile indices fit 32 bits: a call's slots span less than 4 GiB;
-  // the first iteration's unit count comes from the host
+  // unit and tile indices fit 32 bits: a call's slots span less than 4 GiB.
+  // The first step uses the host's unit count and 32-bit chunk arithmetic
+  // (element counts and chunk offsets fit 32 bits, an input being at most
+  // 256 MiB), which keeps the set-up before the first packet store short.
   uint32_t units = (uint32_t)a.units;
   // Every packet store is issued, at an offset past the slot when there is
   // nothing to send (the own rank, a unit past the end, a muted rank), and no
@@ -854,8 +852,14 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
     }
   };
   u32x4 first[U];
-  load_units(in_chunk(Mode == 2 ? r : q), chunk_len(Mode == 2 ? r : q), w, first);
+  {
+    const uint32_t c0 = Mode == 2 ? r : q;
+    const int32_t left = (int32_t)n_all - (int32_t)(c0 * (uint32_t)C);
+    const int64_t len0 = left < 0 ? 0 : (left < (int32_t)C ? left : (int32_t)C);
+    load_units(Mode == 2 ? in_it : in_it + (uint64_t)(c0 * (uint32_t)(C * E)), len0, w, first);
+  }
   store_units(slot_out + area + (Mode == 2 ? ag_off : 0), w, first);
+  units = (uint32_t)Pr::units((C * E + 3) / 4);  // the same count, for the loop below
 
   const bool al4 = a.al4 != 0;
   WaitBudget budget(a.timeout);
