@@ -93,6 +93,25 @@ def gpu_paced(torch, ll, launch_batch, steps, grid, batch=2000):
     return np.concatenate(iv_all), np.concatenate(sp_all)
 
 
+def stamp_free_mean(torch, ll, launch_batch, steps, batch=2000):
+    """Mean time per call of `steps` back-to-back launches without any stamps,
+    queued behind the spin kernel like gpu_paced: HIP events on the launch
+    stream, recorded after the spin kernel and after the last launch."""
+    s = torch.cuda.current_stream()
+    total_ms, done = 0.0, 0
+    while done < steps:
+        cnt = min(batch, steps - done)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ll.check(ll.ll_probe_spin(HOLD_TICKS, s.cuda_stream), "spin")
+        e0.record(s)
+        launch_batch(done, cnt, 0, 0)
+        e1.record(s)
+        torch.cuda.synchronize()
+        total_ms += e0.elapsed_time(e1)
+        done += cnt
+    return total_ms * 1000.0 / steps
+
+
 def bench_headline(torch, ll, steps, warmup):
     from paper_2607_16100_amd import workloads as wl
     from paper_2607_16100_amd.region import SymRegion
@@ -120,6 +139,9 @@ def bench_headline(torch, ll, steps, warmup):
     intervals, spans = gpu_paced(torch, ll, queue, steps, grid)
     wall = time.perf_counter() - t0
     ll.check(ll.ll_check(s), "headline")
+    # the same GPU-paced batch without the per-workgroup stamps (HIP events)
+    stampfree = stamp_free_mean(torch, ll, queue, steps)
+    ll.check(ll.ll_check(s), "headline")
     # the same calls launched one at a time from Python (host-paced), for context
     torch.cuda.synchronize()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -145,9 +167,32 @@ def bench_headline(torch, ll, steps, warmup):
     return {
         "algorithm": "oneshot_waves", "variants": variants,
         "p50_us": pct(intervals, 50), "p99_us": pct(intervals, 99), "mean_us": float(np.mean(intervals)),
-        "span_p50_us": pct(spans, 50), "python_launched_mean_us": host_mean, "wall_s": wall, "grid": grid,
-        "threads": threads, "epochs": reg.epoch,
+        "span_p50_us": pct(spans, 50), "stamp_free_mean_us": stampfree, "python_launched_mean_us": host_mean,
+        "wall_s": wall, "grid": grid, "threads": threads, "epochs": reg.epoch,
+        "exchange_probe": bench_exchange_probe(torch, ll, reg, n, p, steps),
     }
+
+
+def bench_exchange_probe(torch, ll, reg, n, p, steps):
+    """The minimal-exchange probe on the headline's region, grid and packet
+    volume (load, one packet store to one peer, poll, one output store per
+    wave; no LDS, barrier or sum): stamped p50 interval and stamp-free mean,
+    measured like the collective."""
+    s = reg.stream_handle()
+
+    def queue(first, count, stamps_ptr, stride):
+        ll.check(ll.ll_bench_exchange(reg.base, reg.rank_stride, reg.out_ptr, n, ll.LL_BF16, p, reg.epoch + 1,
+                                      count, stamps_ptr, stride, s), "bench_exchange")
+        reg.epoch += count
+
+    queue(0, 200, 0, 0)
+    torch.cuda.synchronize()
+    grid, threads = ll.ll_last_grid()
+    iv, sp = gpu_paced(torch, ll, queue, steps, grid)
+    mean = stamp_free_mean(torch, ll, queue, steps)
+    ll.check(ll.ll_check(s), "exchange probe")
+    return {"p50_us": pct(iv, 50), "p99_us": pct(iv, 99), "span_p50_us": pct(sp, 50), "stamp_free_mean_us": mean,
+            "grid": grid, "threads": threads}
 
 
 HEADLINE_OUTPUT = {}
@@ -177,7 +222,8 @@ def bench_floor(torch, ll, steps, warmup, grid, threads):
         fn(0, warmup, 0, 0)
         torch.cuda.synchronize()
         iv, sp = gpu_paced(torch, ll, fn, steps, grid)
-        out[name] = {"p50_us": pct(iv, 50), "p99_us": pct(iv, 99), "span_p50_us": pct(sp, 50)}
+        out[name] = {"p50_us": pct(iv, 50), "p99_us": pct(iv, 99), "span_p50_us": pct(sp, 50),
+                     "stamp_free_mean_us": stamp_free_mean(torch, ll, fn, steps)}
     # dependent-load latency of cold lines: chase through a table, after evicting caches
     line_words = 16
     perm = np.random.default_rng(1).permutation(words // line_words // 64)[:4096] * 64 * line_words
@@ -670,6 +716,27 @@ def main():
             # the best plain streaming copy on the same GPU: what a simple kernel reaches
             roofline["copy_ceiling_gbps"] = round(probe["gbps"], 1)
             roofline["frac_of_copy_ceiling"] = round(bw["gbps"] / probe["gbps"], 4)
+    if h and fl:
+        ex = h.get("exchange_probe", {})
+        lat = {"bound": "latency floor: back-to-back launches of a kernel with the same grid doing one dependent "
+                        "HBM load (empty-kernel launch + one HBM round trip)",
+               "kernel": "k_oneshot_tile<ProtoLL, bf16, 8> (16 KiB per rank, 8 ranks, one tile per workgroup)",
+               "p50_us": round(h["p50_us"], 3), "floor_p50_us": round(fl["p50_us"], 3),
+               "ratio_to_floor": round(h["p50_us"] / fl["p50_us"], 3), "target_ratio": 1.5,
+               "composed_floor_us": round(result["floor"].get("composed_p50_us", float("nan")), 3),
+               "kernel_span_p50_us": round(h["span_p50_us"], 3),
+               "floor_span_p50_us": round(fl["span_p50_us"], 3),
+               "stamp_free_mean_us": round(h["stamp_free_mean_us"], 3),
+               "floor_stamp_free_mean_us": round(fl["stamp_free_mean_us"], 3),
+               "ratio_to_floor_stamp_free": round(h["stamp_free_mean_us"] / fl["stamp_free_mean_us"], 3)}
+        if ex:
+            lat.update({"exchange_probe_p50_us": round(ex["p50_us"], 3),
+                        "exchange_probe_stamp_free_mean_us": round(ex["stamp_free_mean_us"], 3),
+                        "ratio_to_exchange_probe": round(h["p50_us"] / ex["p50_us"], 3)})
+        if roofline is None:
+            roofline = {"bound": "latency", "achieved": lat["p50_us"], "peak": lat["floor_p50_us"], "unit": "us",
+                        "frac": round(lat["floor_p50_us"] / lat["p50_us"], 4), "traffic": None}
+        roofline["latency"] = lat
     line = {
         "metric": "p50 µs per AllReduce at 16 KB (P=8, bf16) + HBM GB/s at 64 MB",
         "value": round(h["p50_us"], 3) if h else None,

@@ -92,6 +92,23 @@ int ll_bench_floor(const uint64_t *chase, uint64_t chase_len, uint64_t first_lin
                    void *stream);
 int ll_bench_empty(int grid, int threads, int calls, uint64_t *stamps, int stamp_stride, void *stream);
 
+/* Minimal-exchange probe: `calls` launches, epochs first_epoch ..
+ * first_epoch+calls-1, of a kernel with the grid and packet volume of the
+ * one-shot AllReduce with one wave per peer and 8-byte packets (LL_ALGO_
+ * ONESHOT_WAVES, one unit per lane) on `count` elements of `dt` per rank:
+ * per wave one input load, one coherent 16-byte packet store per lane to one
+ * peer, a poll of that peer's packets, one output store; no LDS, barrier or
+ * sum.  It moves the data the one-shot must move and nothing else, so its
+ * call-to-call interval bounds the one-shot's from below (see the probe
+ * kernel).  The region is an AllReduce region of at least `count`
+ * elements (its 8-byte packet slots are used); count*esize must be a
+ * positive multiple of 8 and fit one tile per workgroup with every
+ * workgroup resident.  out receives nranks*count elements: each element of
+ * rank r's output equals that element of some rank's input.  stamps as for
+ * ll_bench_allreduce. */
+int ll_bench_exchange(void *sym_base, size_t rank_stride, void *out, size_t count, int dt, int nranks,
+                      uint32_t first_epoch, int calls, uint64_t *stamps, int stamp_stride, void *stream);
+
 /* ids[b] = XCD index of workgroup b. */
 int ll_probe_xcd(uint32_t *ids, int grid, int threads, void *stream);
 

@@ -63,17 +63,24 @@ __device__ __forceinline__ void compiler_fence() { __asm__ __volatile__("" ::: "
 
 __device__ __forceinline__ uint64_t now_ticks() { return __builtin_amdgcn_s_memrealtime(); }
 
-// Budget of a call's flag waits, in ticks of the 100 MHz constant clock.  The
-// clock is read for the first time at a wait's first timeout check, not at
-// kernel entry: a clock read is a scalar memory round trip, and at entry it
-// would stand between the kernel's start and its first loads and stores.
-// The budget therefore starts when a wait first runs long, which is all a
-// bound on waiting needs.
+// Budget of a call's flag waits, in ticks of the 100 MHz constant clock, and
+// where an expired wait is reported.  The clock is read for the first time at
+// a wait's first timeout check, not at kernel entry: a clock read is a scalar
+// memory round trip, and at entry it would stand between the kernel's start
+// and its first loads and stores.  The budget therefore starts when a wait
+// first runs long, which is all a bound on waiting needs.
+//
+// Status word (4 dwords, owned by the stream the call runs on): [0] = error
+// code (0 = ok), [1] = rank, [2] = mask of peers not heard from, [3] = epoch.
+// The first wait to expire records itself; later ones leave it alone.
+constexpr uint32_t kStatusTimeout = 1;
+
 struct WaitBudget {
   uint64_t budget = 0;
   uint64_t deadline = 0;
+  uint32_t *status = nullptr;
   __device__ WaitBudget() {}
-  __device__ explicit WaitBudget(uint64_t ticks) : budget(ticks) {}
+  __device__ WaitBudget(uint64_t ticks, uint32_t *st) : budget(ticks), status(st) {}
   __device__ __forceinline__ bool expired() {
     const uint64_t t = now_ticks();
     if (deadline == 0) {
@@ -81,6 +88,15 @@ struct WaitBudget {
       return false;
     }
     return t > deadline;
+  }
+  __device__ __forceinline__ void report(int rank, uint32_t pending, uint32_t epoch) const {
+    uint32_t expected = 0;
+    if (__hip_atomic_compare_exchange_strong(&status[0], &expected, kStatusTimeout, __ATOMIC_RELAXED,
+                                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+      __hip_atomic_store(&status[1], (uint32_t)rank, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&status[2], pending, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&status[3], epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
 };
 
@@ -217,6 +233,54 @@ __device__ __forceinline__ void store_words(char *base, int64_t w0, int cnt, int
         *(uint16_t *)(base + e * 2) = (uint16_t)x;
       }
     }
+  }
+}
+
+// Loading / storing a one-lane unit's payload words through a buffer resource
+// (kernels whose streams start 4-byte aligned).  The resource covers the
+// stream's bytes rounded up to whole words, so the hardware range check
+// returns zeros for words past the end and drops stores to them: no branch
+// is needed around the access.  For bfloat16 a last word that holds only one
+// element (an odd count) carries, in its other half, two bytes that lie past
+// the stream but inside the input area; that element is never stored, and
+// clear_tail zeroes it where it matters (sentinel units, where it could
+// complete a sentinel dword).  The clearing is a separate step so that a
+// caller can put independent work between the load and it.
+template <int NW>
+__device__ __forceinline__ u32x4 load_words_rs(rsrc_t rs, uint32_t w0) {
+  u32x4 v = {0u, 0u, 0u, 0u};
+  if constexpr (NW == 2) {
+    const u32x2 t = __builtin_amdgcn_raw_buffer_load_b64(rs, (int)(w0 * 4), 0, 0);
+    v.x = t.x;
+    v.y = t.y;
+  } else {
+    v = __builtin_amdgcn_raw_buffer_load_b128(rs, (int)(w0 * 4), 0, 0);
+  }
+  return v;
+}
+
+template <int DT, int NW>
+__device__ __forceinline__ u32x4 clear_tail(u32x4 v, uint32_t w0, uint32_t nelem) {
+  if constexpr (DT == 1) {
+    // word w holds elements 2w and 2w+1
+    if (2 * w0 + 1 >= nelem) v.x &= 0xFFFFu;
+    if (2 * w0 + 3 >= nelem) v.y &= 0xFFFFu;
+    if constexpr (NW == 4) {
+      if (2 * w0 + 5 >= nelem) v.z &= 0xFFFFu;
+      if (2 * w0 + 7 >= nelem) v.w &= 0xFFFFu;
+    }
+  }
+  return v;
+}
+
+// The matching store of NW words at word w0, for a stream whose byte length
+// is a multiple of 4 (so that no word is partly past the end); streaming hint.
+template <int NW>
+__device__ __forceinline__ void store_words_rs(rsrc_t rs, uint32_t w0, u32x4 v) {
+  if constexpr (NW == 2) {
+    __builtin_amdgcn_raw_buffer_store_b64(u32x2{v.x, v.y}, rs, (int)(w0 * 4), 0, kNT);
+  } else {
+    __builtin_amdgcn_raw_buffer_store_b128(v, rs, (int)(w0 * 4), 0, kNT);
   }
 }
 
@@ -387,22 +451,5 @@ struct ProtoSent {
 // Whether a packet format resets the slots it has read.
 template <class Pr> struct ResetsSlots { static constexpr bool value = false; };
 template <> struct ResetsSlots<ProtoSent> { static constexpr bool value = true; };
-
-// ---------------------------------------------------------------------------
-// Status word shared by all kernels of the library: [0] = error code (0 = ok),
-// [1] = rank, [2] = mask of peers not heard from, [3] = epoch.
-extern __device__ uint32_t g_ll_status[4];
-
-constexpr uint32_t kStatusTimeout = 1;
-
-__device__ __forceinline__ void report_timeout(int rank, uint32_t pending, uint32_t epoch) {
-  uint32_t expected = 0;
-  if (__hip_atomic_compare_exchange_strong(&g_ll_status[0], &expected, kStatusTimeout, __ATOMIC_RELAXED,
-                                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
-    __hip_atomic_store(&g_ll_status[1], (uint32_t)rank, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(&g_ll_status[2], pending, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(&g_ll_status[3], epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-}
 
 }  // namespace llc

@@ -19,6 +19,7 @@
 #pragma once
 
 #include "ll_device.hpp"
+#include "ll_iter.hpp"
 
 namespace llc {
 
@@ -54,6 +55,7 @@ struct KArgs {
   uint32_t grid;        // workgroups in the launch (gridDim.x, without its memory load)
   uint32_t block;       // threads per workgroup (blockDim.x, likewise)
   int64_t units;        // packet units of the call's stream (one-shot wave kernel)
+  uint32_t *status;     // status word of the stream the call runs on (where a timed-out wait reports)
 };
 
 // Kernel arguments live in memory and reach a wave through scalar loads.  Left
@@ -94,6 +96,7 @@ __device__ __forceinline__ KArgs pin_args(const KArgs &k) {
   a.grid = in_sgpr(k.grid);
   a.block = in_sgpr(k.block);
   a.units = in_sgpr(k.units);
+  a.status = in_sgpr(k.status);
   return a;
 }
 
@@ -168,7 +171,7 @@ __device__ __forceinline__ int poll_all(char *area_r, uint64_t slot, uint32_t of
     if (pend == 0) break;
     idle64(poll_gap);
     if ((spins++ & 15) == 0 && budget.expired()) {
-      report_timeout(r, pend, epoch);
+      budget.report(r, pend, epoch);
       break;
     }
   }
@@ -257,13 +260,13 @@ __global__ __launch_bounds__(1024) void k_oneshot(KArgs ka) {
   // buffer resource discards: no store is branched around, so the compiler
   // never has to wait for the stores' acknowledgements before the polls.
   const bool publish = (int)r != a.mute;
-  WaitBudget budget(a.timeout);
+  WaitBudget budget(a.timeout, a.status);
   char *const slice_r = a.sym + (uint64_t)r * a.stride;
   char *const out_r = a.out + (uint64_t)r * (uint64_t)a.n * E;
 
   for (uint32_t it = 0; it < a.iters; ++it) {
-    const int64_t e0 = (int64_t)it * a.iter_n;
-    const int64_t n = a.n - e0 < a.iter_n ? a.n - e0 : a.iter_n;
+    const IterSpan sp = iter_span(a.n, a.iter_n, it, P, E);
+    const int64_t e0 = sp.e0, n = sp.n;
     const uint32_t units = (uint32_t)Pr::units((n * E + 3) / 4);
     const uint64_t area = a.area + (uint64_t)(it & 1u) * a.sub_bytes;
     const uint32_t epoch = a.epoch + it;
@@ -427,7 +430,8 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
 
   const uint32_t W = a.grid / P;
   const uint32_t tiles = (units + (uint32_t)WU::kPerTile - 1u) >> kTileShift;
-  WaitBudget budget(a.timeout);
+
+  WaitBudget budget(a.timeout, a.status);
   char *const out_r = a.out + (uint64_t)r * (uint64_t)n * E;
   const rsrc_t rs = make_rsrc(a.sym + a.area + (uint64_t)r * a.stride + (q - (q > r ? 1u : 0u)) * slot, slot);
 
@@ -452,6 +456,49 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
       a.phases[4 * (blockIdx.x * P + wv) + (k)] = (expr);                   \
   } while (0)
 
+  // Poll the tile's units in slot (r <- q) until the wave has them all; the
+  // loop runs while any lane of the wave still waits (a wave vote ends it),
+  // and every round re-loads all U units: the few extra loads of lanes
+  // already done cost less than per-lane branching, which would add
+  // instructions to every round.  Sentinel units are given back once read.
+  auto poll_tile = [&](uint32_t tile, u32x4 *v) {
+    uint32_t pend = 0;
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      v[k] = u32x4{0u, 0u, 0u, 0u};
+      pend |= ((uint32_t)WU::unit(tile, k, lane) < units ? 1u : 0u) << k;
+    }
+    const uint32_t want = pend;
+    idle64(a.first_wait);
+    uint32_t spins = 0;
+    while (true) {
+      compiler_fence();
+      u32x4 pk[U];
+#pragma unroll
+      for (int k = 0; k < U; ++k) pk[k] = ld_pkt(rs, WU::off(WU::unit(tile, k, lane), lane));
+#pragma unroll
+      for (int k = 0; k < U; ++k) {
+        if ((pend & (1u << k)) && Pr::ready(pk[k], a.epoch)) {
+          v[k] = Pr::unpack(pk[k], sub);
+          pend &= ~(1u << k);
+        }
+      }
+      if (__builtin_amdgcn_ballot_w64(pend != 0) == 0) break;
+      if ((++spins & 15) == 0 && budget.expired()) {
+        if (pend != 0) budget.report((int)r, 1u << q, a.epoch);
+        break;
+      }
+      idle64(a.poll_gap);
+    }
+    if (ResetsSlots<Pr>::value) {
+      const u32x4 sent = {ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel};
+#pragma unroll
+      for (int k = 0; k < U; ++k) {
+        if (want & (1u << k)) st_pkt(rs, WU::off(WU::unit(tile, k, lane), lane), sent);
+      }
+    }
+  };
+
   while (true) {
     LL_WAVE_PHASE(0, now_ticks() + (own[0].x & 0u));
     if (q == r) {
@@ -459,45 +506,7 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
       LL_WAVE_PHASE(1, now_ticks());
     } else {
       u32x4 v[U];
-      uint32_t pend = 0;
-#pragma unroll
-      for (int k = 0; k < U; ++k) {
-        v[k] = u32x4{0u, 0u, 0u, 0u};
-        pend |= ((uint32_t)WU::unit(tile, k, lane) < units ? 1u : 0u) << k;
-      }
-      const uint32_t want = pend;
-      idle64(a.first_wait);
-      // The poll loop runs while any lane of the wave still waits (a wave vote
-      // ends it), and every round re-loads all U units: the few extra loads of
-      // lanes already done cost less than per-lane branching, which would add
-      // instructions to every round.
-      uint32_t spins = 0;
-      while (true) {
-        compiler_fence();
-        u32x4 pk[U];
-#pragma unroll
-        for (int k = 0; k < U; ++k) pk[k] = ld_pkt(rs, WU::off(WU::unit(tile, k, lane), lane));
-#pragma unroll
-        for (int k = 0; k < U; ++k) {
-          if ((pend & (1u << k)) && Pr::ready(pk[k], a.epoch)) {
-            v[k] = Pr::unpack(pk[k], sub);
-            pend &= ~(1u << k);
-          }
-        }
-        if (__builtin_amdgcn_ballot_w64(pend != 0) == 0) break;
-        if ((++spins & 15) == 0 && budget.expired()) {
-          if (pend != 0) report_timeout((int)r, 1u << q, a.epoch);
-          break;
-        }
-        idle64(a.poll_gap);
-      }
-      if (ResetsSlots<Pr>::value) {
-        const u32x4 sent = {ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel};
-#pragma unroll
-        for (int k = 0; k < U; ++k) {
-          if (want & (1u << k)) st_pkt(rs, WU::off(WU::unit(tile, k, lane), lane), sent);
-        }
-      }
+      poll_tile(tile, v);
       LL_WAVE_PHASE(1, now_ticks() + (v[0].x & 0u));
       stage_row(v);
     }
@@ -571,6 +580,109 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
   }
   stamp_end(a, t_start);
 }
+
+// ---------------------------------------------------------------------------
+// One-shot AllReduce for the latency-bound sizes: one wave per peer, one tile
+// per workgroup, one-lane packet formats (8-byte packets or sentinel units),
+// every stream 4-byte aligned.  The same exchange as k_oneshot_waves with
+// U = 1, written as one short straight path: on this chip the code a kernel
+// runs between its start and its last store is paid for in latency (every
+// call starts with cold instruction caches), so this kernel carries no
+// multi-tile loop and no element-wise fallback for unaligned streams.
+//
+// Wave q of the workgroup serving rank r and tile w: lane l owns unit
+// u = 64w + l.  It loads the unit's input words through a buffer resource
+// (words past the input read as zero), stores them as one packet to slot
+// (q <- r) of peer q (the own-rank wave and a muted rank store at an offset
+// past the slot, which the resource discards: no branch around the store),
+// polls slot (r <- q) until the peer's packet carries the epoch, and stages
+// the payload, widened to binary32, in LDS row q.  After one barrier wave 0
+// forms the ordered sum of the P rows for its 64 lanes, rounds once and
+// stores the tile's output, 4*kMaxWords bytes per lane.
+template <class Pr, int DT, int P>
+__global__ __launch_bounds__(512) void k_oneshot_tile(KArgs ka) {
+  static_assert(Pr::kLanes == 1, "one-lane packet formats only");
+  const KArgs a = pin_args(ka);
+  const uint64_t t_start = stamp_start(a);
+  constexpr int E = Elem<DT>::kBytes;
+  constexpr int K = Elem<DT>::kPerWord;
+  constexpr int NW = Pr::kMaxWords;  // payload words per lane
+  constexpr int EPL = NW * K;        // elements per lane
+  __shared__ float stage[P][64 * EPL];
+  const uint32_t r = blockIdx.x % P;
+  const uint32_t w = blockIdx.x / P;
+  const uint32_t q = (uint32_t)uniform_u32(threadIdx.x >> 6);
+  const uint32_t lane = threadIdx.x & 63;
+  const uint32_t u = w * 64 + lane;
+  const uint32_t nb = (uint32_t)(a.n * E);  // input bytes per rank (< 256 MiB)
+  const rsrc_t in_rs = make_rsrc(a.in + (uint64_t)r * a.in_stride, (nb + 3u) & ~3u);
+  u32x4 x = load_words_rs<NW>(in_rs, u * NW);
+  constexpr uint32_t kNowhere = 0xFFFFFFF0u;
+  const uint32_t slot = (uint32_t)a.slot;
+  const bool publish = q != r && u < (uint32_t)a.units && (int)r != a.mute;
+  const rsrc_t rd = make_rsrc(a.sym + a.area + (uint64_t)q * a.stride + (r - (r > q ? 1u : 0u)) * slot, slot);
+  if (ResetsSlots<Pr>::value) x = clear_tail<DT, NW>(x, u * NW, (uint32_t)a.n);
+  st_pkt(rd, publish ? u * 16 : kNowhere, Pr::pack(x, a.epoch, 0));
+  // diagnostics (-DLLCOLL_WAVE_PHASES=1): as in k_oneshot_waves
+  const int wv = (int)q;
+  const uint32_t tile = w;
+  LL_WAVE_PHASE(0, now_ticks() + (x.x & 0u));
+  WaitBudget budget(a.timeout, a.status);
+  u32x4 v = x;
+  if (q != r) {
+    const rsrc_t rs = make_rsrc(a.sym + a.area + (uint64_t)r * a.stride + (q - (q > r ? 1u : 0u)) * slot, slot);
+    bool pend = u < (uint32_t)a.units;
+    uint32_t spins = 0;
+    while (true) {
+      compiler_fence();
+      const u32x4 pk = ld_pkt(rs, u * 16);
+      if (pend && Pr::ready(pk, a.epoch)) {
+        v = Pr::unpack(pk, 0);
+        pend = false;
+      }
+      if (__builtin_amdgcn_ballot_w64(pend) == 0) break;
+      if ((++spins & 15) == 0 && budget.expired()) {
+        if (pend) budget.report((int)r, 1u << q, a.epoch);
+        break;
+      }
+    }
+    if (ResetsSlots<Pr>::value) {
+      const u32x4 sent = {ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel};
+      if (u < (uint32_t)a.units) st_pkt(rs, u * 16, sent);
+    }
+  }
+  LL_WAVE_PHASE(1, now_ticks() + (v.x & 0u));
+  {
+    const uint32_t vw[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int j = 0; j < NW; ++j) {
+      float f[K];
+      Elem<DT>::widen(vw[j], f);
+#pragma unroll
+      for (int e = 0; e < K; ++e) stage[q][lane * EPL + j * K + e] = f[e];
+    }
+  }
+  lds_barrier();
+  LL_WAVE_PHASE(2, now_ticks());
+  if (q == 0) {
+    uint32_t o[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int j = 0; j < NW; ++j) {
+      float acc[K];
+#pragma unroll
+      for (int e = 0; e < K; ++e) acc[e] = stage[0][lane * EPL + j * K + e];
+#pragma unroll
+      for (int p = 1; p < P; ++p) {
+#pragma unroll
+        for (int e = 0; e < K; ++e) acc[e] = acc[e] + stage[p][lane * EPL + j * K + e];
+      }
+      o[j] = Elem<DT>::narrow(acc);
+    }
+    // al4: nb is a whole number of words, so no stored word is partly past the end
+    store_words_rs<NW>(make_rsrc(a.out + (uint64_t)r * nb, nb), u * NW, u32x4{o[0], o[1], o[2], o[3]});
+  }
+  stamp_end(a, t_start);
+}
 #undef LL_WAVE_PHASE
 
 // ---------------------------------------------------------------------------
@@ -617,7 +729,7 @@ __device__ __forceinline__ void poll_out(char *out_r, uint32_t out_bytes, uint32
     }
     if (pend == 0) break;
     if ((spins++ & 15) == 0 && budget.expired()) {
-      report_timeout(r, pend, epoch);
+      budget.report(r, pend, epoch);
       break;
     }
   }
@@ -710,13 +822,6 @@ struct TwoShot {
 #define LLCOLL_TWOSHOT_WAVES_PER_EU 1
 #endif
 
-// Two-shot chunk of an iteration of n elements: ceil(n / P) rounded up to 16 bytes.
-template <int P, int E>
-__device__ __forceinline__ int64_t chunk_of(int64_t n) {
-  constexpr int64_t g = 16 / E;
-  return ((n + P - 1) / P + g - 1) / g * g;
-}
-
 template <class Pr, int DT, int P, bool Direct = false>
 __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(LLCOLL_TWOSHOT_WAVES_PER_EU))) void k_twoshot(
     KArgs ka) {
@@ -726,7 +831,7 @@ __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(LLCOLL_TWO
   TwoShot<Pr, DT, P, Direct> t{a};
   t.r = pt.r;
   constexpr int E = Elem<DT>::kBytes;
-  t.budget = WaitBudget(a.timeout);
+  t.budget = WaitBudget(a.timeout, a.status);
   t.slice_r = a.sym + (uint64_t)t.r * a.stride;
   t.publish = (t.r != a.mute);
   t.al4 = a.al4 != 0;
@@ -739,9 +844,10 @@ __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(LLCOLL_TWO
   const int64_t ustep = (int64_t)pt.W * a.block / Pr::kLanes;
   const int64_t lag = a.lag;
   for (uint32_t it = 0; it < a.iters; ++it) {
-    const int64_t e0 = (int64_t)it * a.iter_n;
-    t.n = a.n - e0 < a.iter_n ? a.n - e0 : a.iter_n;
-    t.C = a.iters == 1 ? a.chunk : chunk_of<P, E>(t.n);
+    const IterSpan sp = iter_span(a.n, a.iter_n, it, P, E);
+    const int64_t e0 = sp.e0;
+    t.n = sp.n;
+    t.C = a.iters == 1 ? a.chunk : sp.chunk;
     t.in_r = in_r + e0 * E;
     t.out_off = (uint64_t)e0 * E;
     t.out_r = out_r + t.out_off;
@@ -804,7 +910,9 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
   // The current iteration (Mode 0 calls may run several, each through
   // sub-buffer it % 2 with the flag epoch + it): its elements, chunk length,
   // input, output offset, packet area and flag.
-  int64_t n_all = Mode == 0 ? a.n : (int64_t)P * a.n;
+  // Iteration 0 of a Mode 0 call holds min(n, iter_n) elements; its chunk
+  // length a.chunk comes from the host (iter_span of iteration 0).
+  int64_t n_all = Mode == 0 ? (a.n < a.iter_n ? a.n : a.iter_n) : (int64_t)P * a.n;
   int64_t C = Mode == 0 ? a.chunk : a.n;
   const char *in_it = in_r;
   uint64_t area = a.area;
@@ -862,7 +970,7 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
   units = (uint32_t)Pr::units((C * E + 3) / 4);  // the same count, for the loop below
 
   const bool al4 = a.al4 != 0;
-  WaitBudget budget(a.timeout);
+  WaitBudget budget(a.timeout, a.status);
   // rank r's output: Mode 0 all n elements, Mode 1 its chunk, Mode 2 its P blocks
   char *const out_rank = a.out + (uint64_t)r * (uint64_t)(Mode == 2 ? (int64_t)P * a.n : a.n) * E;
   uint64_t out_off = 0;
@@ -914,7 +1022,7 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
       }
       if (__builtin_amdgcn_ballot_w64(pend != 0) == 0) break;
       if ((++spins & 15) == 0 && budget.expired()) {
-        if (pend != 0) report_timeout((int)r, 1u << q, epoch);
+        if (pend != 0) budget.report((int)r, 1u << q, epoch);
         break;
       }
     }
@@ -930,9 +1038,10 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
   const uint32_t W = a.grid / P;
   for (uint32_t it = 0; it < iters; ++it) {
     if (Mode == 0 && it > 0) {
-      const int64_t e0 = (int64_t)it * a.iter_n;
-      n_all = a.n - e0 < a.iter_n ? a.n - e0 : a.iter_n;
-      C = chunk_of<P, E>(n_all);
+      const IterSpan sp = iter_span(a.n, a.iter_n, it, P, E);
+      const int64_t e0 = sp.e0;
+      n_all = sp.n;
+      C = sp.chunk;
       in_it = in_r + e0 * E;
       out_off = (uint64_t)e0 * E;
       area = a.area + (uint64_t)(it & 1u) * a.sub_bytes;
@@ -1058,7 +1167,7 @@ __global__ __launch_bounds__(1024) void k_twoshot_atomic(KArgs ka) {
   const int64_t GW = ((int64_t)pt.W * a.block) >> 6;
   const int64_t n = a.n, C = a.chunk;
   const int64_t tiles = (C + TE - 1) / TE;
-  WaitBudget budget(a.timeout);
+  WaitBudget budget(a.timeout, a.status);
   const char *const in_r = a.in + (uint64_t)r * a.in_stride;
   char *const out_r = a.out + (uint64_t)r * (uint64_t)n * E;
   const bool publish = (r != a.mute);
@@ -1118,7 +1227,7 @@ __global__ __launch_bounds__(1024) void k_twoshot_atomic(KArgs ka) {
     int spins = 1;
     while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != (uint32_t)P) {
       if ((spins++ & 15) == 0 && budget.expired()) {
-        report_timeout(r, ((1u << P) - 1u) & ~(1u << r), a.epoch);
+        budget.report(r, ((1u << P) - 1u) & ~(1u << r), a.epoch);
         break;
       }
     }
@@ -1204,7 +1313,7 @@ __global__ __launch_bounds__(1024) void k_broadcast(KArgs ka) {
   } else {
     char *const area_r = a.sym + (uint64_t)r * a.stride + a.area;
     char *const out_r = a.out + (uint64_t)r * (uint64_t)n * E;
-    WaitBudget budget(a.timeout);
+    WaitBudget budget(a.timeout, a.status);
     for (uint32_t u = g / Pr::kLanes; u < units; u += ustep) {
       const uint32_t off = u * Pr::kUnitBytes + sub * 16;
       u32x4 got[P];
@@ -1244,7 +1353,7 @@ __global__ __launch_bounds__(1024) void k_reduce(KArgs ka) {
     }
   } else {
     char *const area_r = a.sym + (uint64_t)r * a.stride + a.area;
-    WaitBudget budget(a.timeout);
+    WaitBudget budget(a.timeout, a.status);
     for (uint32_t u = g / Pr::kLanes; u < units; u += ustep) {
       const uint32_t off = u * Pr::kUnitBytes + sub * 16;
       const u32x4 own = Pr::template load<DT>(in_r, u, sub, n, a.in_al4 != 0);
@@ -1271,7 +1380,7 @@ __global__ __launch_bounds__(1024) void k_reduce_scatter(KArgs ka) {
   const Part pt = part_of_block<P>(a);
   const int r = pt.r;
   constexpr int E = Elem<DT>::kBytes;
-  WaitBudget budget(a.timeout);
+  WaitBudget budget(a.timeout, a.status);
   char *const slice_r = a.sym + (uint64_t)r * a.stride;
   const char *const in_r = a.in + (uint64_t)r * a.in_stride;
   const bool in_al4 = a.in_al4 != 0;
@@ -1331,7 +1440,7 @@ __global__ __launch_bounds__(1024) void k_allgather(KArgs ka) {
   const Part pt = part_of_block<P>(a);
   const int r = pt.r;
   constexpr int E = Elem<DT>::kBytes;
-  WaitBudget budget(a.timeout);
+  WaitBudget budget(a.timeout, a.status);
   char *const slice_r = a.sym + (uint64_t)r * a.stride;
   const char *const in_r = a.in + (uint64_t)r * a.in_stride;
   const int64_t n = a.n;
@@ -1367,29 +1476,6 @@ __global__ __launch_bounds__(1024) void k_allgather(KArgs ka) {
     }
   }
   stamp_end(a, t_start);
-}
-
-// Set `bytes` bytes at `dst` (16-byte aligned) to 0xFF: the sentinel of
-// every element type.
-__global__ __launch_bounds__(256) void k_fill_ones(char *dst, uint64_t bytes) {
-  const uint64_t full = bytes / 16;
-  const u32x4 ones = {0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
-  const uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  for (uint64_t i = t; i < full; i += (uint64_t)gridDim.x * blockDim.x) *(u32x4 *)(dst + i * 16) = ones;
-  if (t < bytes % 16) dst[full * 16 + t] = (char)0xFF;
-}
-
-// Fill bytes [lo, hi) of every slice with the dword `value`.
-__global__ __launch_bounds__(256) void k_fill_areas(char *sym, uint64_t stride, int nranks, uint64_t lo, uint64_t hi,
-                                                  uint32_t value) {
-  const uint64_t per = (hi - lo) / 16;
-  const uint64_t total = per * (uint64_t)nranks;
-  const u32x4 z = {value, value, value, value};
-  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (uint64_t)gridDim.x * blockDim.x) {
-    const uint64_t rk = i / per;
-    const uint64_t k = i % per;
-    *(u32x4 *)(sym + rk * stride + lo + k * 16) = z;
-  }
 }
 
 }  // namespace llc

@@ -15,9 +15,12 @@
 // * Streaming: the HBM bandwidth that a plain kernel of 16-byte streaming
 //   loads and stores reaches (copy, read only, write only), the practical
 //   ceiling for the bandwidth-bound collectives.
+// * Minimal exchange: the data movement of the one-wave-per-peer one-shot
+//   with nothing else, the bound that kernel is measured against.
 #pragma once
 
 #include "ll_device.hpp"
+#include "ll_kernels.hpp"
 
 namespace llc {
 
@@ -282,6 +285,62 @@ __global__ __launch_bounds__(1024) void k_probe_stream(const u32x4 *src, u32x4 *
     }
   }
   if (mode == 1 && acc.x == 0x9E3779B9u && acc.y == 0x7F4A7C15u) dst[0] = acc;
+}
+
+// Minimal exchange with the grid and packet volume of the one-shot with one
+// wave per peer and 8-byte packets (k_oneshot_waves): workgroup b serves rank
+// r = b % P and tile w = b / P of 64 packet units (8 input bytes each); wave
+// q of the workgroup loads the tile's input (each lane 8 bytes), stores it as
+// one 16-byte packet store per lane into slot (q <- r) of peer q, polls the
+// same units of slot (r <- q) in its own slice until both flags of every lane
+// equal the epoch (a wave vote ends the loop), and stores the 8 payload bytes
+// it received to the rank's output tile.  The own-rank wave stores its own
+// input there without an exchange.  No LDS, no barrier, no sum: every wave of
+// a workgroup writes the same output tile, so each output element ends up as
+// one rank's input element (which one is unspecified).  The same instruction
+// order as the collective: input load first, then the packet store with no
+// branch around it.  Waits are bounded and report like the collectives'.
+template <int P>
+__global__ __launch_bounds__(512) void k_probe_exchange(KArgs ka) {
+  const KArgs a = pin_args(ka);
+  const uint64_t t_start = stamp_start(a);
+  const uint32_t r = blockIdx.x % P;
+  const uint32_t w = blockIdx.x / P;
+  const uint32_t q = (uint32_t)uniform_u32(threadIdx.x >> 6);
+  const uint32_t lane = threadIdx.x & 63;
+  const uint32_t units = (uint32_t)a.units;
+  const uint32_t u = w * 64 + lane;
+  const uint32_t in_bytes = (uint32_t)a.n;  // a.n: input bytes per rank
+  const rsrc_t in_rs = make_rsrc(a.sym + (uint64_t)r * a.stride, in_bytes);
+  const u32x2 x = __builtin_amdgcn_raw_buffer_load_b64(in_rs, (int)(u * 8), 0, 0);
+  constexpr uint32_t kNowhere = 0xFFFFFFF0u;
+  const uint32_t slot = (uint32_t)a.slot;
+  const bool publish = q != r && u < units;
+  const rsrc_t rd = make_rsrc(a.sym + a.area + (uint64_t)q * a.stride + (r - (r > q ? 1u : 0u)) * slot, slot);
+  st_pkt(rd, publish ? u * 16 : kNowhere, u32x4{x.x, a.epoch, x.y, a.epoch});
+  WaitBudget budget(a.timeout, a.status);
+  u32x2 v = x;
+  if (q != r) {
+    const rsrc_t rs = make_rsrc(a.sym + a.area + (uint64_t)r * a.stride + (q - (q > r ? 1u : 0u)) * slot, slot);
+    bool pend = u < units;
+    uint32_t spins = 0;
+    while (true) {
+      compiler_fence();
+      const u32x4 pk = ld_pkt(rs, u * 16);
+      if (pend && pk.y == a.epoch && pk.w == a.epoch) {
+        v = u32x2{pk.x, pk.z};
+        pend = false;
+      }
+      if (__builtin_amdgcn_ballot_w64(pend) == 0) break;
+      if ((++spins & 15) == 0 && budget.expired()) {
+        if (pend) budget.report((int)r, 1u << q, a.epoch);
+        break;
+      }
+    }
+  }
+  const rsrc_t out_rs = make_rsrc(a.out + (uint64_t)r * in_bytes, in_bytes);
+  __builtin_amdgcn_raw_buffer_store_b64(v, out_rs, (int)(u * 8), 0, kNT);
+  stamp_end(a, t_start);
 }
 
 }  // namespace llc

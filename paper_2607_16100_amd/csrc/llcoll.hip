@@ -15,14 +15,20 @@
 
 #include "../../include/llcoll.h"
 #include "../../include/llprobe.h"
+#include "../../include/lltune.h"
 #include "ll_device.hpp"
-#include "ll_kernels.hpp"
+#include "ll_fill.hpp"
+#include "ll_iter.hpp"
 #include "ll_layout.hpp"
 #include "ll_probe.hpp"
+#include "ll_table.hpp"
 
 namespace llc {
-__device__ uint32_t g_ll_status[4];
-}
+// Status words, one per stream that has run a call (see status_of); each
+// device holds its own copy of the array.
+constexpr int kStatusSlots = 256;
+__device__ uint32_t g_status[kStatusSlots][4];
+}  // namespace llc
 
 using namespace llc;
 namespace L = llc::layout;
@@ -50,130 +56,38 @@ struct TimeoutInfo {
   int rank = -1;
   uint32_t missing = 0, epoch = 0;
 };
-TimeoutInfo g_last_timeout;
+thread_local TimeoutInfo t_last_timeout;  // the last timeout this thread's ll_check saw
 std::mutex g_mu;
 
 // ---------------------------------------------------------------- kernels
-enum Kind {
-  K_ONESHOT = 0,
-  K_TWOSHOT = 1,
-  K_RS = 2,
-  K_AG = 3,
-  K_ONESHOT_WAVES = 4,
-  K_TWOSHOT_OUT = 5,
-  K_TWOSHOT_ATOMIC = 6,
-  K_BCAST = 7,
-  K_REDUCE = 8,
-  K_TWOSHOT_WAVES = 9,
-  K_RS_WAVES = 10,
-  K_AG_WAVES = 11,
-  K_KINDS = 12
-};
 constexpr int kWaveUnits[3] = {1, 2, 4};  // units per lane of the wave-per-peer kernels
-enum Proto { PR_LL = 0, PR_LINE = 1, PR_SENT = 2, PR_COUNT = 3 };
-
-typedef void (*kernel_fn)(KArgs);
-
-template <class Pr, int DT, int P>
-void fill_row(kernel_fn *row) {
-  row[K_ONESHOT] = k_oneshot<Pr, DT, P>;
-  row[K_TWOSHOT] = k_twoshot<Pr, DT, P>;
-  row[K_RS] = k_reduce_scatter<Pr, DT, P>;
-  row[K_AG] = k_allgather<Pr, DT, P>;
-  row[K_ONESHOT_WAVES] = nullptr;
-  row[K_BCAST] = k_broadcast<Pr, DT, P>;
-  row[K_REDUCE] = k_reduce<Pr, DT, P>;
-  row[K_TWOSHOT_OUT] = nullptr;
-  row[K_TWOSHOT_ATOMIC] = nullptr;
-  if constexpr (std::is_same<Pr, ProtoSent>::value) {
-    row[K_TWOSHOT_OUT] = k_twoshot<ProtoSent, DT, P, true>;
-    row[K_TWOSHOT_ATOMIC] = k_twoshot_atomic<DT, P>;
-  }
-}
-
-// table[proto][dtype][P][kind]
-struct Table {
-  kernel_fn k[PR_COUNT][2][LL_MAX_RANKS + 1][K_KINDS];
-  kernel_fn waves[3][3][2][LL_MAX_RANKS + 1];  // [log2 U][8-byte packets, sentinel, lines][dtype][P]
-  kernel_fn twaves[3][3][3][2][LL_MAX_RANKS + 1];  // [AR, RS, AG][log2 U][8-byte, sentinel, lines][dtype][P]
-  Table() {
-    memset(k, 0, sizeof k);
-    memset(waves, 0, sizeof waves);
-    memset(twaves, 0, sizeof twaves);
-    fill<2>();
-    fill<3>();
-    fill<4>();
-    fill<5>();
-    fill<6>();
-    fill<7>();
-    fill<8>();
-  }
-  template <int M, int P>
-  void fill_twaves() {
-    twaves[M][0][0][0][P] = k_twoshot_waves<ProtoLL, 0, P, 1, M>;
-    twaves[M][0][0][1][P] = k_twoshot_waves<ProtoLL, 1, P, 1, M>;
-    twaves[M][1][0][0][P] = k_twoshot_waves<ProtoLL, 0, P, 2, M>;
-    twaves[M][1][0][1][P] = k_twoshot_waves<ProtoLL, 1, P, 2, M>;
-    twaves[M][2][0][0][P] = k_twoshot_waves<ProtoLL, 0, P, 4, M>;
-    twaves[M][2][0][1][P] = k_twoshot_waves<ProtoLL, 1, P, 4, M>;
-    twaves[M][0][1][0][P] = k_twoshot_waves<ProtoSent, 0, P, 1, M>;
-    twaves[M][0][1][1][P] = k_twoshot_waves<ProtoSent, 1, P, 1, M>;
-    twaves[M][1][1][0][P] = k_twoshot_waves<ProtoSent, 0, P, 2, M>;
-    twaves[M][1][1][1][P] = k_twoshot_waves<ProtoSent, 1, P, 2, M>;
-    twaves[M][2][1][0][P] = k_twoshot_waves<ProtoSent, 0, P, 4, M>;
-    twaves[M][2][1][1][P] = k_twoshot_waves<ProtoSent, 1, P, 4, M>;
-    twaves[M][0][2][0][P] = k_twoshot_waves<ProtoLine, 0, P, 1, M>;
-    twaves[M][0][2][1][P] = k_twoshot_waves<ProtoLine, 1, P, 1, M>;
-    twaves[M][1][2][0][P] = k_twoshot_waves<ProtoLine, 0, P, 2, M>;
-    twaves[M][1][2][1][P] = k_twoshot_waves<ProtoLine, 1, P, 2, M>;
-    twaves[M][2][2][0][P] = k_twoshot_waves<ProtoLine, 0, P, 4, M>;
-    twaves[M][2][2][1][P] = k_twoshot_waves<ProtoLine, 1, P, 4, M>;
-  }
-  template <int P>
-  void fill() {
-    fill_row<ProtoLL, 0, P>(k[PR_LL][0][P]);
-    fill_row<ProtoLL, 1, P>(k[PR_LL][1][P]);
-    fill_row<ProtoLine, 0, P>(k[PR_LINE][0][P]);
-    fill_row<ProtoLine, 1, P>(k[PR_LINE][1][P]);
-    fill_row<ProtoSent, 0, P>(k[PR_SENT][0][P]);
-    fill_row<ProtoSent, 1, P>(k[PR_SENT][1][P]);
-    waves[0][0][0][P] = k_oneshot_waves<ProtoLL, 0, P, 1>;
-    waves[0][0][1][P] = k_oneshot_waves<ProtoLL, 1, P, 1>;
-    waves[1][0][0][P] = k_oneshot_waves<ProtoLL, 0, P, 2>;
-    waves[1][0][1][P] = k_oneshot_waves<ProtoLL, 1, P, 2>;
-    waves[2][0][0][P] = k_oneshot_waves<ProtoLL, 0, P, 4>;
-    waves[2][0][1][P] = k_oneshot_waves<ProtoLL, 1, P, 4>;
-    waves[0][1][0][P] = k_oneshot_waves<ProtoSent, 0, P, 1>;
-    waves[0][1][1][P] = k_oneshot_waves<ProtoSent, 1, P, 1>;
-    waves[1][1][0][P] = k_oneshot_waves<ProtoSent, 0, P, 2>;
-    waves[1][1][1][P] = k_oneshot_waves<ProtoSent, 1, P, 2>;
-    waves[2][1][0][P] = k_oneshot_waves<ProtoSent, 0, P, 4>;
-    waves[2][1][1][P] = k_oneshot_waves<ProtoSent, 1, P, 4>;
-    waves[0][2][0][P] = k_oneshot_waves<ProtoLine, 0, P, 1>;
-    waves[0][2][1][P] = k_oneshot_waves<ProtoLine, 1, P, 1>;
-    waves[1][2][0][P] = k_oneshot_waves<ProtoLine, 0, P, 2>;
-    waves[1][2][1][P] = k_oneshot_waves<ProtoLine, 1, P, 2>;
-    waves[2][2][0][P] = k_oneshot_waves<ProtoLine, 0, P, 4>;
-    waves[2][2][1][P] = k_oneshot_waves<ProtoLine, 1, P, 4>;
-    fill_twaves<0, P>();
-    fill_twaves<1, P>();
-    fill_twaves<2, P>();
-  }
-};
 
 const Table &table() {
-  static const Table t;
+  static const Table t = [] {
+    Table x;
+    memset(&x, 0, sizeof x);
+    fill_table_p2(&x);
+    fill_table_p3(&x);
+    fill_table_p4(&x);
+    fill_table_p5(&x);
+    fill_table_p6(&x);
+    fill_table_p7(&x);
+    fill_table_p8(&x);
+    return x;
+  }();
   return t;
 }
 
-// Per-device facts, queried on first use.
+// Per-device facts, queried on first use: compute units, and the device
+// address of that device's copy of the status array.
 struct DevInfo {
   bool ok = false;
   int cus = 0;
+  uint32_t *status = nullptr;
 };
 DevInfo g_dev[64];
 
-int device_info(DevInfo *out) {
+int device_info(DevInfo *out, int *dev_out = nullptr) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) {
@@ -189,10 +103,55 @@ int device_info(DevInfo *out) {
       t_last_hip = (int)e;
       return LL_ERR_HIP;
     }
+    void *st = nullptr;
+    e = hipGetSymbolAddress(&st, HIP_SYMBOL(llc::g_status));
+    if (e != hipSuccess) {
+      t_last_hip = (int)e;
+      return LL_ERR_HIP;
+    }
     g_dev[dev].cus = cus;
+    g_dev[dev].status = (uint32_t *)st;
     g_dev[dev].ok = true;
   }
   *out = g_dev[dev];
+  if (dev_out) *dev_out = dev;
+  return LL_OK;
+}
+
+// Status slots.  Every stream that runs a call owns one of the device's
+// kStatusSlots status words: a kernel that times out reports into the word of
+// its own stream, and ll_check(stream) reads and clears only that word, so
+// calls on different streams (and different regions) report independently.
+// A stream keeps its slot for the life of the process; if more than
+// kStatusSlots streams of one device run calls, the later ones share slots
+// (their timeouts may then be reported on either stream).
+void *g_slot_owner[64][kStatusSlots];  // guarded by g_mu
+bool g_slot_used[64][kStatusSlots];
+
+int slot_index(int dev, void *stream, bool assign) {
+  const uintptr_t h = ((uintptr_t)stream >> 4) * 0x9E3779B97F4A7C15ull;
+  const int start = (int)((h >> 32) % kStatusSlots);
+  std::lock_guard<std::mutex> lk(g_mu);
+  for (int k = 0; k < kStatusSlots; ++k) {
+    const int i = (start + k) % kStatusSlots;
+    if (g_slot_used[dev][i] && g_slot_owner[dev][i] == stream) return i;
+    if (!g_slot_used[dev][i]) {
+      if (!assign) return -1;
+      g_slot_used[dev][i] = true;
+      g_slot_owner[dev][i] = stream;
+      return i;
+    }
+  }
+  return assign ? start : -1;  // every slot taken: share
+}
+
+// Device address of the status word of `stream` on the current device.
+int status_of(void *stream, uint32_t **out) {
+  DevInfo d;
+  int dev = 0;
+  const int st = device_info(&d, &dev);
+  if (st != LL_OK) return st;
+  *out = d.status + 4 * slot_index(dev, stream, true);
   return LL_OK;
 }
 
@@ -279,6 +238,8 @@ int wave_units_log2(const Plan &pl, int wpr) {
   return (pl.units + 63) / 64 <= cap / pl.P ? 0 : 1;
 }
 
+int launch_kernel(kernel_fn fn, const Plan &pl, int W, int threads, void *stream);
+
 int launch(const Plan &pl, void *stream) {
   const bool two_waves = pl.kind == K_TWOSHOT_WAVES || pl.kind == K_RS_WAVES || pl.kind == K_AG_WAVES;
   const bool wave_kernel = pl.kind == K_ONESHOT_WAVES || two_waves;
@@ -294,6 +255,18 @@ int launch(const Plan &pl, void *stream) {
     fn = table().k[pl.proto][pl.dt][pl.P][pl.kind];
   }
   if (fn == nullptr) return LL_ERR_UNSUPPORTED;
+  // The latency-bound one-shot: one tile of 64 one-lane units per workgroup,
+  // every stream 4-byte aligned, all tiles resident at once, no forced
+  // launch shape -> the straight-line one-tile kernel.
+  if (pl.kind == K_ONESHOT_WAVES && wlog == 0 && pl.proto != PR_LINE && g_wg_per_rank.load() == 0 &&
+      g_threads.load() == 0 && pl.a.al4 != 0 && (pl.a.in == nullptr || pl.a.in_al4 != 0) && pl.a.iters <= 1) {
+    kernel_fn tf = table().tile[pl.proto == PR_SENT ? 1 : 0][pl.dt][pl.P];
+    int cap = 0;
+    const int rc = resident_grid(tf, 64 * pl.P, &cap);
+    if (rc != LL_OK) return rc;
+    const int64_t tiles = (pl.units + 63) / 64;
+    if (tf != nullptr && tiles <= cap / pl.P) return launch_kernel(tf, pl, (int)tiles, 64 * pl.P, stream);
+  }
   int threads = g_threads.load();
   if (threads == 0) threads = 256;
   int lanes_per_unit = pl.proto == PR_LINE ? ProtoLine::kLanes : 1;
@@ -318,6 +291,11 @@ int launch(const Plan &pl, void *stream) {
   } else if (W > wmax) {
     W = wmax;  // never launch more than can be resident: waits depend on co-residency
   }
+  return launch_kernel(fn, pl, W, threads, stream);
+}
+
+// Launch `fn` with W workgroups per rank and `threads` per workgroup.
+int launch_kernel(kernel_fn fn, const Plan &pl, int W, int threads, void *stream) {
   const int grid = W * pl.P;
   KArgs a = pl.a;
   if (a.in == nullptr) {  // input inside the region, at offset 0 of every slice
@@ -337,6 +315,8 @@ int launch(const Plan &pl, void *stream) {
   a.grid = (uint32_t)grid;
   a.block = (uint32_t)threads;
   a.units = pl.units;
+  const int st = status_of(stream, &a.status);
+  if (st != LL_OK) return st;
   a.stamps = g_stamps.exchange(nullptr);
   a.phases = g_phases.exchange(nullptr);
   hipLaunchKernelGGL(fn, dim3(grid), dim3(threads), 0, (hipStream_t)stream, a);
@@ -499,12 +479,11 @@ void plan_allreduce(Plan *pl, ll_algo algo, uint64_t count, int es, int nranks, 
     pl->kind = algo == LL_ALGO_TWOSHOT_SENTINEL_OUT ? K_TWOSHOT_OUT : K_TWOSHOT;
     if (algo == LL_ALGO_TWOSHOT_WAVES || algo == LL_ALGO_TWOSHOT_SENTINEL_WAVES || algo == LL_ALGO_TWOSHOT_LINE_WAVES)
       pl->kind = K_TWOSHOT_WAVES;
-    const uint64_t C = L::twoshot_chunk(iter_count, nranks, es);
+    const uint64_t C = (uint64_t)iter_span((int64_t)count, (int64_t)iter_count, 0, nranks, es).chunk;
     pl->a.chunk = (int64_t)C;
     pl->a.slot = slot_bytes(pl->proto, C * es);
     pl->units = units_of(pl->proto, C * es);
   }
-  (void)count;
 }
 
 }  // namespace
@@ -687,6 +666,40 @@ int ll_scratch_init(void *scratch_base, size_t scratch_stride, int nranks, void 
   return LL_OK;
 }
 
+static void buffered_iterations(uint64_t count, int es, uint64_t D, uint64_t *iter_count, uint64_t *iters) {
+  *iter_count = std::min<uint64_t>(count, D / (uint64_t)es);
+  *iters = *iter_count ? (count + *iter_count - 1) / *iter_count : 0;
+}
+
+int ll_buffered_plan(size_t count, ll_dtype dt, int nranks, size_t scratch_stride, uint32_t *iters,
+                     size_t *iter_count) {
+  if (iters == nullptr || iter_count == nullptr) return LL_ERR_INVALID;
+  int st = check_dtype_op((int)dt, LL_SUM);
+  if (st != LL_OK) return st;
+  size_t D = 0;
+  st = ll_scratch_iter_bytes(scratch_stride, nranks, &D);
+  if (st != LL_OK) return st;
+  const int es = esize_of(dt);
+  if (count > (L::kMaxBufferedBytes / (uint64_t)es)) return LL_ERR_UNSUPPORTED;
+  uint64_t ic = 0, k = 0;
+  buffered_iterations(count, es, D, &ic, &k);
+  if (k > 0xFFFFFFFFull) return LL_ERR_UNSUPPORTED;
+  *iters = (uint32_t)k;
+  *iter_count = (size_t)ic;
+  return LL_OK;
+}
+
+int ll_iteration_span(size_t count, size_t iter_count, uint32_t it, int nranks, ll_dtype dt, int64_t *out3) {
+  if (out3 == nullptr || iter_count == 0 || nranks < 2 || nranks > LL_MAX_RANKS) return LL_ERR_INVALID;
+  const int st = check_dtype_op((int)dt, LL_SUM);
+  if (st != LL_OK) return st;
+  const IterSpan sp = iter_span((int64_t)count, (int64_t)iter_count, it, nranks, esize_of(dt));
+  out3[0] = sp.e0;
+  out3[1] = sp.n;
+  out3[2] = sp.chunk;
+  return LL_OK;
+}
+
 int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, ll_op op, int nranks,
                           void *scratch_base, size_t scratch_stride, uint32_t epoch, void *stream, ll_algo algo,
                           uint32_t *epochs_used) {
@@ -712,8 +725,8 @@ int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, 
   if (in != out && overlaps(in, all, out, all)) return LL_ERR_INVALID;  // in place, or apart
   if (overlaps(in, all, scratch_base, sbytes) || overlaps(out, all, scratch_base, sbytes)) return LL_ERR_INVALID;
   if (count == 0) return LL_OK;
-  const uint64_t iter_count = std::min<uint64_t>(count, D / (uint64_t)es);
-  const uint64_t iters = (count + iter_count - 1) / iter_count;
+  uint64_t iter_count = 0, iters = 0;
+  buffered_iterations(count, es, D, &iter_count, &iters);
   if ((uint64_t)epoch + iters - 1 > 0xFFFFFFFFull) return LL_ERR_INVALID;
   if (algo == LL_ALGO_AUTO) {
     // by the iteration size; the one-shot wave kernels run one iteration
@@ -873,33 +886,38 @@ int ll_check(void *stream) {
     t_last_hip = (int)e;
     return LL_ERR_HIP;
   }
+  DevInfo d;
+  int dev = 0;
+  int rc = device_info(&d, &dev);
+  if (rc != LL_OK) return rc;
+  const int slot = slot_index(dev, stream, false);
+  if (slot < 0) return LL_OK;  // no call has run on this stream
+  uint32_t *word = d.status + 4 * slot;
   uint32_t st[4] = {0, 0, 0, 0};
-  e = hipMemcpyFromSymbol(st, HIP_SYMBOL(llc::g_ll_status), sizeof st, 0, hipMemcpyDeviceToHost);
+  e = hipMemcpyAsync(st, word, sizeof st, hipMemcpyDeviceToHost, (hipStream_t)stream);
+  if (e == hipSuccess) e = hipStreamSynchronize((hipStream_t)stream);
   if (e != hipSuccess) {
     t_last_hip = (int)e;
     return LL_ERR_HIP;
   }
   if (st[0] == 0) return LL_OK;
   const uint32_t zero[4] = {0, 0, 0, 0};
-  e = hipMemcpyToSymbol(HIP_SYMBOL(llc::g_ll_status), zero, sizeof zero, 0, hipMemcpyHostToDevice);
+  e = hipMemcpyAsync(word, zero, sizeof zero, hipMemcpyHostToDevice, (hipStream_t)stream);
+  if (e == hipSuccess) e = hipStreamSynchronize((hipStream_t)stream);
   if (e != hipSuccess) {
     t_last_hip = (int)e;
     return LL_ERR_HIP;
   }
-  {
-    std::lock_guard<std::mutex> lk(g_mu);
-    g_last_timeout.rank = (int)st[1];
-    g_last_timeout.missing = st[2];
-    g_last_timeout.epoch = st[3];
-  }
+  t_last_timeout.rank = (int)st[1];
+  t_last_timeout.missing = st[2];
+  t_last_timeout.epoch = st[3];
   return st[0] == kStatusTimeout ? LL_ERR_TIMEOUT : LL_ERR_HIP;
 }
 
 int ll_last_timeout(int *rank, uint32_t *missing_peers, uint32_t *epoch) {
-  std::lock_guard<std::mutex> lk(g_mu);
-  if (rank) *rank = g_last_timeout.rank;
-  if (missing_peers) *missing_peers = g_last_timeout.missing;
-  if (epoch) *epoch = g_last_timeout.epoch;
+  if (rank) *rank = t_last_timeout.rank;
+  if (missing_peers) *missing_peers = t_last_timeout.missing;
+  if (epoch) *epoch = t_last_timeout.epoch;
   return LL_OK;
 }
 
@@ -1156,6 +1174,58 @@ int ll_bench_empty(int grid, int threads, int calls, uint64_t *stamps, int stamp
     hipLaunchKernelGGL(k_probe_empty, dim3(grid), dim3(threads), 0, (hipStream_t)stream,
                        stamps ? stamps + (size_t)i * (size_t)stamp_stride : nullptr);
   }
+  return hip_status();
+}
+
+int ll_bench_exchange(void *sym_base, size_t rank_stride, void *out, size_t count, int dt, int nranks,
+                      uint32_t first_epoch, int calls, uint64_t *stamps, int stamp_stride, void *stream) {
+  int st = check_common(sym_base, rank_stride, out, nranks, first_epoch);
+  if (st != LL_OK) return st;
+  st = check_dtype_op(dt, LL_SUM);
+  if (st != LL_OK) return st;
+  if (calls < 1 || (uint64_t)first_epoch + (uint64_t)calls - 1 > 0xFFFFFFFFull) return LL_ERR_INVALID;
+  const uint64_t bytes = (uint64_t)count * (uint64_t)esize_of((ll_dtype)dt);
+  if (bytes == 0 || bytes % 8 != 0) return LL_ERR_UNSUPPORTED;
+  if (overlaps(out, bytes * nranks, sym_base, (uint64_t)rank_stride * nranks)) return LL_ERR_INVALID;
+  Region rg;
+  st = region_of(rank_stride, nranks, bytes, &rg);
+  if (st != LL_OK) return st;
+  static kernel_fn const fns[LL_MAX_RANKS + 1] = {nullptr,
+                                                  nullptr,
+                                                  k_probe_exchange<2>,
+                                                  k_probe_exchange<3>,
+                                                  k_probe_exchange<4>,
+                                                  k_probe_exchange<5>,
+                                                  k_probe_exchange<6>,
+                                                  k_probe_exchange<7>,
+                                                  k_probe_exchange<8>};
+  const kernel_fn fn = fns[nranks];
+  const int threads = 64 * nranks;
+  int cap_grid = 0;
+  st = resident_grid(fn, threads, &cap_grid);
+  if (st != LL_OK) return st;
+  const uint64_t units = bytes / 8;
+  const uint64_t W = (units + 63) / 64;
+  if (W > (uint64_t)(cap_grid / nranks)) return LL_ERR_UNSUPPORTED;  // one tile per workgroup, all resident
+  const int grid = (int)W * nranks;
+  if (stamps != nullptr && stamp_stride < 2 * grid) return LL_ERR_INVALID;
+  KArgs a = base_args(sym_base, rank_stride, out, first_epoch);
+  a.n = (int64_t)bytes;
+  a.area = rg.area_of(PR_LL);
+  a.slot = slot_bytes(PR_LL, bytes);
+  a.units = (int64_t)units;
+  a.timeout = g_timeout.load();
+  a.grid = (uint32_t)grid;
+  a.block = (uint32_t)threads;
+  st = status_of(stream, &a.status);
+  if (st != LL_OK) return st;
+  for (int i = 0; i < calls; ++i) {
+    a.epoch = first_epoch + (uint32_t)i;
+    a.stamps = stamps ? stamps + (size_t)i * (size_t)stamp_stride : nullptr;
+    hipLaunchKernelGGL(fn, dim3(grid), dim3(threads), 0, (hipStream_t)stream, a);
+  }
+  g_last_grid.store(grid);
+  g_last_threads.store(threads);
   return hip_status();
 }
 

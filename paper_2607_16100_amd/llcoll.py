@@ -1,4 +1,5 @@
-"""Python binding of the llcoll C ABI (``include/llcoll.h``, ``include/llprobe.h``).
+"""Python binding of the llcoll C ABI (``include/llcoll.h``, ``include/llprobe.h``,
+``include/lltune.h``).
 
 Argument marshalling only: every function has the C name, takes the same
 arguments (device pointers and streams as integers) and returns the C status
@@ -96,6 +97,9 @@ _SIGS = {
     "ll_probe_xcd": (_i, [_vp, _i, _i, _vp]),
     "ll_probe_litmus": (_i, [_vp, _sz, _i, _i, _i, _i, _i, _vp, _vp]),
     "ll_probe_stream": (_i, [_vp, _vp, _sz, _i, _i, _i, _vp]),
+    "ll_bench_exchange": (_i, [_vp, _sz, _vp, _sz, _i, _i, _u32, _i, _vp, _i, _vp]),
+    "ll_buffered_plan": (_i, [_sz, _i, _i, _sz, ctypes.POINTER(_u32), ctypes.POINTER(_sz)]),
+    "ll_iteration_span": (_i, [_sz, _sz, _u32, _i, _i, ctypes.POINTER(ctypes.c_int64)]),
 }
 
 if not os.path.exists(LIB_PATH):
@@ -351,3 +355,22 @@ def ll_probe_stream(src, dst, nbytes, mode, grid, threads, stream):
 
 def ll_probe_litmus(buf, buf_bytes, grid, lines, iters, reads, layout, counts4, stream):
     return _lib.ll_probe_litmus(buf, buf_bytes, grid, lines, iters, reads, layout, counts4, stream)
+
+
+def ll_bench_exchange(sym_base, rank_stride, out, count, dt, nranks, first_epoch, calls, stamps, stamp_stride, stream):
+    return _lib.ll_bench_exchange(sym_base, rank_stride, out, count, dt, nranks, first_epoch, calls, stamps,
+                                  stamp_stride, stream)
+
+
+def ll_buffered_plan(count: int, dt: int, nranks: int, scratch_stride: int):
+    """(status, iterations, elements per iteration)."""
+    k, ic = ctypes.c_uint32(0), ctypes.c_size_t(0)
+    st = _lib.ll_buffered_plan(count, dt, nranks, scratch_stride, ctypes.byref(k), ctypes.byref(ic))
+    return st, k.value, ic.value
+
+
+def ll_iteration_span(count: int, iter_count: int, it: int, nranks: int, dt: int):
+    """(status, (first element, elements, two-shot chunk))."""
+    out = (ctypes.c_int64 * 3)()
+    st = _lib.ll_iteration_span(count, iter_count, it, nranks, dt, out)
+    return st, tuple(out)

@@ -10,7 +10,7 @@ import pytest
 from paper_2607_16100_amd import llcoll as ll
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADERS = [os.path.join(ROOT, "include", h) for h in ("llcoll.h", "llprobe.h")]
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("llcoll.h", "llprobe.h", "lltune.h")]
 
 F32, BF16 = ll.LL_F32, ll.LL_BF16
 GOOD_BASE = 1 << 40          # fake, 256-aligned device addresses: never dereferenced
@@ -317,3 +317,32 @@ def test_auto_algo_choices():
                     else:
                         assert not seen_twoshot, f"P={p} {2**k} bytes: one-shot after two-shot"
     assert ll.ll_set_auto_sentinel(0) == ll.LL_OK
+
+
+@pytest.mark.parametrize("p", [2, 3, 5, 6, 7, 8])
+@pytest.mark.parametrize("dt,es", [(F32, 4), (BF16, 2)])
+def test_iterations_tile_the_message_and_chunks_stay_inside(p, dt, es):
+    """The iteration arithmetic every kernel uses: the iterations of a
+    bounded-scratch call cover [0, count) exactly once, in order, and the P
+    chunks of an iteration never reach past it (rank counts that do not
+    divide the iteration included)."""
+    for iter_bytes in (4096, 65536, 1 << 20):
+        st, stride = ll.ll_scratch_bytes(iter_bytes, p)
+        assert st == ll.LL_OK
+        for count in (1, 5, 1000, iter_bytes // es, iter_bytes // es + 3, 7 * (iter_bytes // es) - 1, 123_457):
+            st, iters, ic = ll.ll_buffered_plan(count, dt, p, stride)
+            assert st == ll.LL_OK
+            assert iters == -(-count // ic) and ic * es <= iter_bytes
+            covered = 0
+            for it in range(iters):
+                st, (e0, n, chunk) = ll.ll_iteration_span(count, ic, it, p, dt)
+                assert st == ll.LL_OK
+                assert e0 == covered and n > 0
+                covered += n
+                assert (chunk * es) % 16 == 0 and chunk * p >= n
+                ends = [min(max(n - c * chunk, 0), chunk) for c in range(p)]
+                assert sum(ends) == n                      # the chunks partition the iteration
+                assert all(ends[c] == 0 or c * chunk + ends[c] <= n for c in range(p))
+            assert covered == count
+            st, (e0, n, _) = ll.ll_iteration_span(count, ic, iters, p, dt)
+            assert st == ll.LL_OK and n == 0               # nothing past the last iteration

@@ -75,7 +75,7 @@ def usable(algo, n, esize, iters):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("p", [2, 3, 8])
+@pytest.mark.parametrize("p", [2, 3, 6, 7, 8])
 def test_iterations_parity(dtype, p):
     """Iteration size 4 KiB; messages of 1, 2, 3 and 7+ iterations with a
     ragged last iteration, every algorithm, two calls in a row."""
@@ -115,6 +115,29 @@ def test_in_place(algo):
         x = wl.uniform(p, n, "bf16", seed=50 + k)
         say(f"in place {algo} call {k}")
         assert_bits_equal(run(reg, x, algo), oracle.allreduce(x), f"in place {algo} call {k}")
+
+
+IN_PLACE_ALGOS = ["auto", "twoshot", "twoshot_line", "twoshot_sentinel", "twoshot_waves", "twoshot_sentinel_waves",
+                  "twoshot_line_waves", "oneshot", "oneshot_line"]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("p", [3, 5, 6, 7])
+def test_in_place_rank_counts_that_do_not_divide_the_iteration(dtype, p):
+    """In place, several iterations, with rank counts whose P chunks of an
+    iteration overrun it (P * chunk > iteration elements): a kernel that cut
+    an iteration by the whole message's count would reduce elements of the
+    next iteration and overwrite its inputs before every rank has read them."""
+    es = 4 if dtype == "f32" else 2
+    reg = ScratchRegion(p, 40_000, dtype, iter_bytes=4096, in_place=True)
+    reg.init()
+    d = reg.iter_bytes // es
+    for n in [3 * d, 5 * d + 7, 40_000]:
+        for algo in IN_PLACE_ALGOS:
+            x = wl.normal(p, n, dtype, seed=n + 31 * p)
+            say(f"in place {algo} P={p} {dtype} n={n} ({-(-n // d)} iterations)")
+            assert_bits_equal(run(reg, x, algo), oracle.allreduce(x), f"in place {algo} P={p} {dtype} n={n}")
+            assert reg.last_iters == -(-n // d)
 
 
 def test_direct_output_rejects_in_place():

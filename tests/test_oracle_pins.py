@@ -184,6 +184,71 @@ def test_subnormals_are_not_flushed(name, fn):
     assert not np.any(out == ftz)
 
 
+# ------------------------------------------------ overflow, infinities, NaN
+# IEEE 754 binary32 addition with round to nearest even, and one rounding to
+# bfloat16: the expected bits below follow from those rules alone.
+BF16_MAX, BF16_INF, BF16_NINF = 0x7F7F, 0x7F80, 0xFF80
+F32_MAX, F32_INF = 0x7F7FFFFF, 0x7F800000
+
+
+def _cols(cols, dtype, p=4):
+    x = np.zeros((p, len(cols)), dtype=np.uint16 if dtype == wl.BF16 else np.uint32)
+    for j, c in enumerate(cols):
+        x[:len(c), j] = c
+    return x
+
+
+def _isnan(v):
+    v = np.asarray(v)
+    if v.dtype == np.uint32:
+        return ((v & 0x7F800000) == 0x7F800000) & ((v & 0x007FFFFF) != 0)
+    return ((v & 0x7F80) == 0x7F80) & ((v & 0x007F) != 0)
+
+
+@pytest.mark.parametrize("name,fn", ORACLES)
+def test_bf16_overflow_rounds_once_to_inf(name, fn):
+    # 0x7B00 = 2^119, half a bfloat16 ulp at bf16 max (2^127 * (2 - 2^-7)).
+    x = _cols([[BF16_MAX, 0x7B00],           # binary32 sum 0x7F7F8000: a tie; bf16 max is odd -> Inf
+               [BF16_MAX, 0x7A80],           # 0x7F7F4000: under the tie -> bf16 max
+               [0xFF7F, 0xFB00],             # the negative tie -> -Inf
+               [BF16_MAX, 0x7B00, 0xFB00],   # back to bf16 max before the only rounding
+               [0x7F7E, 0x7B00],             # 0x7F7E8000: a tie, 0x7F7E is even -> stays
+               [0x7F7E, 0x7B01],             # just over that tie -> 0x7F7F
+               [BF16_MAX, BF16_MAX]],        # binary32 overflow -> Inf
+              wl.BF16)
+    out = fn(x)[0]
+    assert list(out) == [BF16_INF, BF16_MAX, BF16_NINF, BF16_MAX, 0x7F7E, 0x7F7F, BF16_INF]
+    # rounding at every step instead of once gets the fourth column wrong (Inf - 2^119 = Inf)
+    assert wrong_bf16_per_step(x)[3] == BF16_INF
+
+
+@pytest.mark.parametrize("name,fn", ORACLES)
+def test_binary32_overflow_and_infinities(name, fn):
+    x = _cols([[F32_MAX, F32_MAX],                # overflow -> +Inf
+               [F32_MAX | 0x80000000, F32_MAX | 0x80000000],  # -> -Inf
+               [F32_MAX, F32_MAX, F32_MAX | 0x80000000],      # Inf - max stays Inf
+               [F32_INF, 0x3F800000],             # Inf + 1
+               [0x3F800000, 0, 0, 0xFF800000],    # -Inf at the last rank
+               [0x7E967699] * 4],                 # 4 x 1e38 > binary32 max: overflow at the 4th add
+              wl.F32)
+    out = fn(x)[0]
+    assert list(out) == [F32_INF, 0xFF800000, F32_INF, F32_INF, 0xFF800000, F32_INF]
+    # the same columns in descending order would give max for the third
+    assert wrong_descending(x)[2] == F32_MAX
+
+
+@pytest.mark.parametrize("name,fn", ORACLES)
+@pytest.mark.parametrize("dtype", [wl.F32, wl.BF16])
+def test_nan_results(name, fn, dtype):
+    if dtype == wl.F32:
+        cols = [[F32_INF, 0xFF800000], [0x7FC00001, 0x3F800000], [0x3F800000, 0x7F800001],
+                [F32_MAX, F32_MAX, 0xFF800000]]
+    else:
+        cols = [[BF16_INF, BF16_NINF], [0x7FC1, 0x3F80], [0x3F80, 0x7F81], [BF16_MAX, BF16_MAX, BF16_NINF]]
+    out = fn(_cols(cols, dtype))
+    assert _isnan(out).all()  # Inf - Inf, quiet NaN, signalling NaN, overflow then -Inf
+
+
 # ---------------------------------------------------------------- exact model
 def _random_f32_bits(rng: random.Random):
     kind = rng.random()

@@ -96,7 +96,7 @@ SMALL_N = [1, 2, 3, 5, 17, 63, 64, 65, 129, 1000, 4099, 30 * 8 * 3 + 7]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("p", [2, 3, 4, 5, 8])
+@pytest.mark.parametrize("p", [2, 3, 4, 5, 6, 7, 8])
 def test_allreduce_all_algorithms_ragged(dtype, p):
     """All four algorithms on one region, sizes across several units with ragged
     tails, alternating calls (the slice layout keeps every flag position fixed)."""
@@ -355,7 +355,8 @@ def test_c5_reduce_scatter_and_allgather(p, b, kind):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("proto", PROTOS)
-@pytest.mark.parametrize("p,m", [(2, 1), (3, 7), (4, 33), (8, 5), (8, 61), (5, 250)])
+@pytest.mark.parametrize("p,m", [(2, 1), (3, 7), (4, 33), (8, 5), (8, 61), (5, 250), (6, 13), (6, 100), (7, 9),
+                                 (7, 333)])
 def test_rs_ag_ragged(dtype, proto, p, m):
     """Chunks whose byte offsets are not 4-byte aligned (odd bfloat16 counts),
     with both kernel families."""
@@ -698,7 +699,7 @@ def test_direct_output_missing_peer_times_out():
     assert_bits_equal(reg.read_out(p * n, np.uint32).reshape(p, n), oracle.allreduce(x), "after timeout")
 
 
-@pytest.mark.parametrize("p", [2, 4, 8])
+@pytest.mark.parametrize("p", [2, 4, 6, 7, 8])
 def test_auto_with_sentinel_allowed(p):
     """With sentinel mode allowed, AUTO gives the same bits at every size."""
     ll.ll_set_auto_sentinel(1)
@@ -780,7 +781,7 @@ def test_atomic_twoshot_missing_peer_times_out():
 
 # ------------------------------------------------ Broadcast and Reduce
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("p", [2, 3, 5, 8])
+@pytest.mark.parametrize("p", [2, 3, 5, 6, 7, 8])
 def test_broadcast_and_reduce_parity(dtype, p):
     reg = SymRegion(p, 70_001, dtype)
     reg.init()

@@ -19,8 +19,10 @@ def stream():
 
 
 def test_workgroups_are_dealt_round_robin_over_xcds():
-    """Workgroup b runs on XCD b mod 8, so rank r = b mod P of an 8-rank launch
-    owns one XCD and every rank-to-rank packet crosses the fabric."""
+    """Consecutive workgroups run on consecutive XCDs: workgroup b runs on XCD
+    (b + s) mod 8, where s, the XCD of workgroup 0, may differ from launch to
+    launch.  So rank r = b mod P of an 8-rank launch owns one XCD and every
+    rank-to-rank packet crosses the fabric."""
     grid = 256
     ids = torch.full((grid,), 99, dtype=torch.int32, device="cuda")
     assert ll.ll_probe_xcd(ids.data_ptr(), grid, 64, stream()) == ll.LL_OK
@@ -29,7 +31,7 @@ def test_workgroups_are_dealt_round_robin_over_xcds():
     nx = int(x.max()) + 1
     print("XCDs seen:", nx, "first 16:", x[:16].tolist(), flush=True)
     assert nx == 8
-    assert np.array_equal(x, np.arange(grid) % 8)
+    assert np.array_equal(x, (np.arange(grid) + x[0]) % 8)
 
 
 @pytest.mark.parametrize("layout,name", [(0, "8-byte packets"), (1, "128-byte lines, flag per 64-byte half")])
