@@ -256,6 +256,37 @@ int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, 
                           void *scratch_base, size_t scratch_stride, uint32_t epoch, void *stream, ll_algo algo,
                           uint32_t *epochs_used);
 
+/* ---- no allocation: AllReduce through a scratch the library holds ----
+ *
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc).
+ * ll_allreduce_static is ll_allreduce_buffered with the scratch region held
+ * by the library: a file-scope device array of LL_STATIC_SCRATCH_BYTES per
+ * GPU, laid out for LL_MAX_RANKS slices, allocated when the library's code is
+ * loaded on a GPU and held until the process ends.  The call itself
+ * allocates nothing (no hipMalloc, hipFree or allocating library routine) and
+ * takes no epoch: the library keeps one epoch counter per GPU for that GPU's
+ * array.  The first call on a GPU, and the first call after ll_check has
+ * reported a timeout on that GPU, first clears the array's flag areas with a
+ * fill kernel on `stream`.
+ *
+ * in, out, count, dt, op, nranks, epochs_used: as ll_allreduce_buffered; in
+ * and out are 16-byte aligned device memory, equal (in place) or disjoint.
+ * algo: LL_ALGO_AUTO (flagged protocols only) or a flagged algorithm
+ * (8-byte packets or 128-byte lines); sentinel and atomic algorithms return
+ * LL_ERR_UNSUPPORTED (a timed-out sentinel call leaves slots only an
+ * ll_init-style reset restores).  Messages of any size up to 16 GiB per
+ * rank run in iterations of the array's iteration size; larger ones return
+ * LL_ERR_UNSUPPORTED.
+ *
+ * Every call on a GPU shares that GPU's array, which keeps the last call's
+ * packets: calls that overlap in time on one GPU (two streams, two threads)
+ * race and their results are undefined.  Serialise them. */
+#define LL_STATIC_SCRATCH_BYTES (64u << 20)
+
+int ll_allreduce_static(const void *in, void *out, size_t count, ll_dtype dt, ll_op op, int nranks, void *stream,
+                        ll_algo algo, uint32_t *epochs_used);
+
 /* Broadcast: every rank receives the root's `count` input elements; rank r's
  * copy at out + r*count*esize (the root's own copy included).  One exchange:
  * the root stores packets into one slot of every peer (the paper lists

@@ -58,6 +58,7 @@ struct TimeoutInfo {
 };
 thread_local TimeoutInfo t_last_timeout;  // the last timeout this thread's ll_check saw
 std::mutex g_mu;
+std::mutex g_static_mu;  // the static scratch table (ll_allreduce_static)
 
 // ---------------------------------------------------------------- kernels
 constexpr int kWaveUnits[3] = {1, 2, 4};  // units per lane of the wave-per-peer kernels
@@ -700,9 +701,14 @@ int ll_iteration_span(size_t count, size_t iter_count, uint32_t it, int nranks, 
   return LL_OK;
 }
 
-int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, ll_op op, int nranks,
-                          void *scratch_base, size_t scratch_stride, uint32_t epoch, void *stream, ll_algo algo,
-                          uint32_t *epochs_used) {
+// A bounded-scratch AllReduce through the scratch region at scratch_base,
+// laid out for `layout_P` ranks (nranks <= layout_P: a call uses the first
+// nranks slices and the first nranks-1 slots of every area, whose offsets
+// depend on layout_P only).  With flags_only, sentinel algorithms are
+// refused and AUTO picks among the flagged ones.
+static int buffered_call(const void *in, void *out, size_t count, ll_dtype dt, ll_op op, int nranks,
+                         void *scratch_base, size_t scratch_stride, int layout_P, bool flags_only, uint32_t epoch,
+                         void *stream, ll_algo algo, uint32_t *epochs_used) {
   if (epochs_used != nullptr) *epochs_used = 0;
   if (in == nullptr || out == nullptr || scratch_base == nullptr) return LL_ERR_INVALID;
   if (((uintptr_t)in % 16) != 0 || ((uintptr_t)out % 16) != 0) return LL_ERR_INVALID;
@@ -713,8 +719,13 @@ int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, 
   if (st != LL_OK) return st;
   if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_TWOSHOT_LINE_WAVES) return LL_ERR_INVALID;
   if (algo == LL_ALGO_TWOSHOT_ATOMIC) return LL_ERR_UNSUPPORTED;  // single-iteration regions only
+  if (flags_only && (algo == LL_ALGO_ONESHOT_SENTINEL || algo == LL_ALGO_TWOSHOT_SENTINEL ||
+                     algo == LL_ALGO_TWOSHOT_SENTINEL_OUT || algo == LL_ALGO_TWOSHOT_SENTINEL_WAVES ||
+                     algo == LL_ALGO_ONESHOT_SENTINEL_WAVES))
+    return LL_ERR_UNSUPPORTED;
+  if (nranks > layout_P) return LL_ERR_INVALID;
   size_t D = 0;
-  st = ll_scratch_iter_bytes(scratch_stride, nranks, &D);
+  st = ll_scratch_iter_bytes(scratch_stride, layout_P, &D);
   if (st != LL_OK) return st;
   const int es = esize_of(dt);
   if (count > (L::kMaxBufferedBytes / (uint64_t)es)) return LL_ERR_UNSUPPORTED;
@@ -733,7 +744,7 @@ int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, 
     // only, and the two-shot wave kernels take their place (measured on the
     // paper's scratch study shape, 32 MiB at 8 ranks in 256 KiB .. 32 MiB
     // iterations)
-    algo = auto_algo(iter_count * es, nranks, g_auto_sentinel.load() != 0);
+    algo = auto_algo(iter_count * es, nranks, !flags_only && g_auto_sentinel.load() != 0);
     if (iters > 1 && algo == LL_ALGO_ONESHOT_WAVES) algo = LL_ALGO_TWOSHOT_WAVES;
     if (iters > 1 && algo == LL_ALGO_ONESHOT_SENTINEL_WAVES) algo = LL_ALGO_TWOSHOT_SENTINEL_WAVES;
     if (iters > 1 && algo == LL_ALGO_ONESHOT_LINE_WAVES) algo = LL_ALGO_TWOSHOT_LINE_WAVES;
@@ -752,7 +763,7 @@ int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, 
   pl.a.al4 = (in_bytes % 4 == 0) ? 1u : 0u;
   pl.a.iters = (uint32_t)iters;
   pl.a.iter_n = (int64_t)iter_count;
-  const uint64_t a8 = L::area8(D, nranks), a128 = L::area128(D, nranks), as = L::areaS(D, nranks);
+  const uint64_t a8 = L::area8(D, layout_P), a128 = L::area128(D, layout_P), as = L::areaS(D, layout_P);
   plan_allreduce(&pl, algo, count, es, nranks, iter_count, [&](int proto) {
     return proto == PR_LINE ? 2 * a8 : (proto == PR_SENT ? 2 * (a8 + a128) : (uint64_t)0);
   });
@@ -760,6 +771,104 @@ int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, 
   st = launch(pl, stream);
   if (st == LL_OK && epochs_used != nullptr) *epochs_used = (uint32_t)iters;
   return st;
+}
+
+int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, ll_op op, int nranks,
+                          void *scratch_base, size_t scratch_stride, uint32_t epoch, void *stream, ll_algo algo,
+                          uint32_t *epochs_used) {
+  if (nranks < 2 || nranks > LL_MAX_RANKS) {
+    if (epochs_used != nullptr) *epochs_used = 0;
+    return LL_ERR_INVALID;
+  }
+  return buffered_call(in, out, count, dt, op, nranks, scratch_base, scratch_stride, nranks, false, epoch, stream,
+                       algo, epochs_used);
+}
+
+// ---------------------------------------------------------------- no allocation
+// The scratch of ll_allreduce_static: a bounded-scratch region of
+// LL_STATIC_SCRATCH_BYTES laid out for LL_MAX_RANKS slices, one copy per
+// device, held until the process ends.  In host code the name stands for
+// no device address: host code uses only the address that
+// hipGetSymbolAddress reports for the current device (static_scratch_of).
+static __device__ __align__(256) unsigned char scratch[LL_STATIC_SCRATCH_BYTES];
+
+namespace {
+struct StaticScratch {
+  void *ptr = nullptr;      // device address of `scratch` on this device
+  bool init_needed = true;  // flags not yet cleared, or a timeout seen since
+  uint64_t next_epoch = 1;  // epochs of this device's static scratch, shared by all its callers
+};
+StaticScratch g_static[64];  // guarded by g_static_mu
+
+constexpr size_t kStaticStride = LL_STATIC_SCRATCH_BYTES / LL_MAX_RANKS;
+}  // namespace
+
+// Device address of the current device's static scratch (looked up once per
+// device), and the first of `iters` epochs for a call; clears the flag areas
+// on `stream` first when they need it (first use on the device, a timeout
+// reported by ll_check since, or the epochs running out).
+static int static_scratch_of(uint64_t iters, void *stream, void **ptr, uint32_t *epoch) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    t_last_hip = (int)e;
+    return LL_ERR_HIP;
+  }
+  if (dev < 0 || dev >= 64) return LL_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lk(g_static_mu);
+  StaticScratch &ss = g_static[dev];
+  if (ss.ptr == nullptr) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr) {
+      t_last_hip = (int)e;
+      return LL_ERR_HIP;
+    }
+    ss.ptr = p;
+  }
+  if (ss.next_epoch + iters - 1 > 0xFFFFFFFFull) ss.init_needed = true;
+  if (ss.init_needed) {
+    const int st = ll_scratch_init(ss.ptr, kStaticStride, LL_MAX_RANKS, stream);
+    if (st != LL_OK) return st;
+    ss.init_needed = false;
+    ss.next_epoch = 1;
+  }
+  *ptr = ss.ptr;
+  *epoch = (uint32_t)ss.next_epoch;
+  ss.next_epoch += iters;
+  return LL_OK;
+}
+
+int ll_allreduce_static(const void *in, void *out, size_t count, ll_dtype dt, ll_op op, int nranks, void *stream,
+                        ll_algo algo, uint32_t *epochs_used) {
+  if (epochs_used != nullptr) *epochs_used = 0;
+  if (in == nullptr || out == nullptr) return LL_ERR_INVALID;
+  if (((uintptr_t)in % 16) != 0 || ((uintptr_t)out % 16) != 0) return LL_ERR_INVALID;
+  if (nranks < 2 || nranks > LL_MAX_RANKS) return LL_ERR_INVALID;
+  int st = check_dtype_op((int)dt, (int)op);
+  if (st != LL_OK) return st;
+  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_TWOSHOT_LINE_WAVES) return LL_ERR_INVALID;
+  switch (algo) {
+    case LL_ALGO_ONESHOT_SENTINEL: case LL_ALGO_TWOSHOT_SENTINEL: case LL_ALGO_TWOSHOT_SENTINEL_OUT:
+    case LL_ALGO_TWOSHOT_ATOMIC: case LL_ALGO_TWOSHOT_SENTINEL_WAVES: case LL_ALGO_ONESHOT_SENTINEL_WAVES:
+      return LL_ERR_UNSUPPORTED;  // flagged protocols only
+    default:
+      break;
+  }
+  const int es = esize_of(dt);
+  if (count > L::kMaxBufferedBytes / (uint64_t)es) return LL_ERR_UNSUPPORTED;  // beyond the largest message
+  if (count == 0) return LL_OK;
+  // the same iteration plan as buffered_call's, to reserve the epochs
+  const uint64_t D = L::iter_capacity(kStaticStride, LL_MAX_RANKS);
+  uint64_t iter_count = 0, iters = 0;
+  buffered_iterations(count, es, D, &iter_count, &iters);
+  if (iters > 0xFFFFFFFFull - 1) return LL_ERR_UNSUPPORTED;
+  void *base = nullptr;
+  uint32_t epoch = 0;
+  st = static_scratch_of(iters, stream, &base, &epoch);
+  if (st != LL_OK) return st;
+  return buffered_call(in, out, count, dt, op, nranks, base, kStaticStride, LL_MAX_RANKS, true, epoch, stream, algo,
+                       epochs_used);
 }
 
 int ll_reduce_scatter_proto(void *sym_base, size_t rank_stride, void *out, size_t recvcount, ll_dtype dt,
@@ -907,6 +1016,12 @@ int ll_check(void *stream) {
   if (e != hipSuccess) {
     t_last_hip = (int)e;
     return LL_ERR_HIP;
+  }
+  {
+    // a timed-out call may have left packets that a later call on the
+    // device's static scratch could take for its own: clear it first
+    std::lock_guard<std::mutex> lk(g_static_mu);
+    g_static[dev].init_needed = true;
   }
   t_last_timeout.rank = (int)st[1];
   t_last_timeout.missing = st[2];

@@ -98,6 +98,7 @@ _SIGS = {
     "ll_probe_litmus": (_i, [_vp, _sz, _i, _i, _i, _i, _i, _vp, _vp]),
     "ll_probe_stream": (_i, [_vp, _vp, _sz, _i, _i, _i, _vp]),
     "ll_bench_exchange": (_i, [_vp, _sz, _vp, _sz, _i, _i, _u32, _i, _vp, _i, _vp]),
+    "ll_allreduce_static": (_i, [_vp, _vp, _sz, _i, _i, _i, _vp, _i, ctypes.POINTER(_u32)]),
     "ll_buffered_plan": (_i, [_sz, _i, _i, _sz, ctypes.POINTER(_u32), ctypes.POINTER(_sz)]),
     "ll_iteration_span": (_i, [_sz, _sz, _u32, _i, _i, ctypes.POINTER(ctypes.c_int64)]),
 }
@@ -238,6 +239,16 @@ def ll_allreduce_buffered(inp, out, count, dt, op, nranks, scratch_base, scratch
     used = ctypes.c_uint32(0)
     st = _lib.ll_allreduce_buffered(inp, out, count, dt, op, nranks, scratch_base, scratch_stride, epoch, stream,
                                     algo, ctypes.byref(used))
+    return st, used.value
+
+
+LL_STATIC_SCRATCH_BYTES = 64 << 20
+
+
+def ll_allreduce_static(inp, out, count, dt, op, nranks, stream, algo):
+    """(status, epochs used): AllReduce through the library's own scratch (no allocation)."""
+    used = ctypes.c_uint32(0)
+    st = _lib.ll_allreduce_static(inp, out, count, dt, op, nranks, stream, algo, ctypes.byref(used))
     return st, used.value
 
 

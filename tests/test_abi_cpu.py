@@ -346,3 +346,26 @@ def test_iterations_tile_the_message_and_chunks_stay_inside(p, dt, es):
             assert covered == count
             st, (e0, n, _) = ll.ll_iteration_span(count, ic, iters, p, dt)
             assert st == ll.LL_OK and n == 0               # nothing past the last iteration
+
+
+def test_static_entry_point_argument_checks():
+    """ll_allreduce_static rejects bad arguments before any HIP call."""
+    good = dict(inp=GOOD_BASE, out=GOOD_OUT, count=1024, dt=F32, op=ll.LL_SUM, nranks=8, stream=0,
+                algo=ll.LL_ALGO_AUTO)
+
+    def call(**kw):
+        a = dict(good, **kw)
+        return ll.ll_allreduce_static(a["inp"], a["out"], a["count"], a["dt"], a["op"], a["nranks"], a["stream"],
+                                      a["algo"])[0]
+
+    assert call(inp=0) == ll.LL_ERR_INVALID
+    assert call(out=GOOD_OUT + 8) == ll.LL_ERR_INVALID
+    assert call(nranks=1) == ll.LL_ERR_INVALID and call(nranks=9) == ll.LL_ERR_INVALID
+    assert call(dt=5) == ll.LL_ERR_UNSUPPORTED and call(op=2) == ll.LL_ERR_UNSUPPORTED
+    assert call(algo=99) == ll.LL_ERR_INVALID
+    for name in ("oneshot_sentinel", "twoshot_sentinel", "twoshot_sentinel_out", "twoshot_atomic",
+                 "twoshot_sentinel_waves", "oneshot_sentinel_waves"):
+        assert call(algo=ll.ALGOS[name]) == ll.LL_ERR_UNSUPPORTED, name
+    assert call(count=(16 << 30) // 4 + 1) == ll.LL_ERR_UNSUPPORTED
+    assert call(count=0) == ll.LL_OK
+    assert ll.LL_STATIC_SCRATCH_BYTES == 64 << 20
