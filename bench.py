@@ -127,14 +127,16 @@ def bench_headline(torch, ll, steps, warmup):
     algo = ll.LL_ALGO_ONESHOT_WAVES
     epoch = [1]
 
+    shape = ll.Options(report=True)  # collects the launch shape
+
     def queue(first, count, stamps_ptr, stride):
         ll.check(ll.ll_bench_allreduce(reg.base, reg.rank_stride, reg.out_ptr, n, ll.LL_BF16, p, epoch[0], count,
-                                       algo, stamps_ptr, stride, s), "bench_allreduce")
+                                       algo, shape, stamps_ptr, stride, s), "bench_allreduce")
         epoch[0] += count
 
     queue(0, warmup, 0, 0)
     torch.cuda.synchronize()
-    grid, threads = ll.ll_last_grid()
+    grid, threads = shape.grid, shape.threads
     t0 = time.perf_counter()
     intervals, spans = gpu_paced(torch, ll, queue, steps, grid)
     wall = time.perf_counter() - t0
@@ -180,14 +182,17 @@ def bench_exchange_probe(torch, ll, reg, n, p, steps):
     measured like the collective."""
     s = reg.stream_handle()
 
+    shape = {}
+
     def queue(first, count, stamps_ptr, stride):
-        ll.check(ll.ll_bench_exchange(reg.base, reg.rank_stride, reg.out_ptr, n, ll.LL_BF16, p, reg.epoch + 1,
-                                      count, stamps_ptr, stride, s), "bench_exchange")
+        st, shape["grid"] = ll.ll_bench_exchange(reg.base, reg.rank_stride, reg.out_ptr, n, ll.LL_BF16, p,
+                                                 reg.epoch + 1, count, stamps_ptr, stride, s)
+        ll.check(st, "bench_exchange")
         reg.epoch += count
 
     queue(0, 200, 0, 0)
     torch.cuda.synchronize()
-    grid, threads = ll.ll_last_grid()
+    grid, threads = shape["grid"], 64 * p
     iv, sp = gpu_paced(torch, ll, queue, steps, grid)
     mean = stamp_free_mean(torch, ll, queue, steps)
     ll.check(ll.ll_check(s), "exchange probe")
@@ -245,22 +250,23 @@ def bench_floor(torch, ll, steps, warmup, grid, threads):
     return out
 
 
-def paced_collective(torch, ll, reg, kind, count, code, steps, warmup):
+def paced_collective(torch, ll, reg, kind, count, code, steps, warmup, flags=0):
     """p50/p99 call-to-call interval (GPU-paced) of one collective on a region.
     kind: "ar" (count elements, code = ll_algo), "rs" (recvcount, code =
-    ll_proto), "ag" (sendcount, code = ll_proto)."""
+    ll_proto), "ag" (sendcount, code = ll_proto); flags: LL_OPT_* of the calls."""
     s = reg.stream_handle()
     fn = {"ar": ll.ll_bench_allreduce, "rs": ll.ll_bench_reduce_scatter, "ag": ll.ll_bench_allgather}[kind]
+    shape = ll.Options(flags=flags, report=True)
 
     def queue(first, cnt, stamps_ptr, stride):
         e = reg.epoch + 1
-        ll.check(fn(reg.base, reg.rank_stride, reg.out_ptr, count, reg.dt, reg.nranks, e, cnt, code, stamps_ptr,
-                    stride, s), kind)
+        ll.check(fn(reg.base, reg.rank_stride, reg.out_ptr, count, reg.dt, reg.nranks, e, cnt, code, shape,
+                    stamps_ptr, stride, s), kind)
         reg.epoch += cnt
 
     queue(0, warmup, 0, 0)
     torch.cuda.synchronize()
-    grid, threads = ll.ll_last_grid()
+    grid, threads = shape.grid, shape.threads
     iv, sp = gpu_paced(torch, ll, queue, steps, grid)
     ll.check(ll.ll_check(s), kind)
     return {"p50_us": pct(iv, 50), "p99_us": pct(iv, 99), "span_p50_us": pct(sp, 50), "grid": grid,
@@ -281,14 +287,17 @@ def bench_rooted(torch, ll, steps):
         s = reg.stream_handle()
         for kind, code in (("broadcast", 0), ("reduce", 1)):
             for proto in ("packet8", "line128", "sentinel"):
-                def queue(first, cnt, stamps_ptr, stride, code=code, proto=proto):
+                shape = ll.Options(report=True)
+
+                def queue(first, cnt, stamps_ptr, stride, code=code, proto=proto, shape=shape):
                     ll.check(ll.ll_bench_rooted(code, reg.base, reg.rank_stride, reg.out_ptr, n, reg.dt, 0, p,
-                                                reg.epoch + 1, cnt, ll.PROTOS[proto], stamps_ptr, stride, s), kind)
+                                                reg.epoch + 1, cnt, ll.PROTOS[proto], shape, stamps_ptr, stride, s),
+                             kind)
                     reg.epoch += cnt
 
                 queue(0, 20, 0, 0)
                 torch.cuda.synchronize()
-                grid, threads = ll.ll_last_grid()
+                grid, threads = shape.grid, shape.threads
                 iv, sp = gpu_paced(torch, ll, queue, steps, grid)
                 ll.check(ll.ll_check(s), kind)
                 out[f"{kind}_{n * 2 >> 10}KiB_{proto}"] = {"p50_us": pct(iv, 50), "p99_us": pct(iv, 99)}
@@ -309,11 +318,8 @@ def bench_c3(torch, ll, steps):
     for algo in ("twoshot", "twoshot_line", "twoshot_waves", "twoshot_sentinel", "twoshot_sentinel_waves",
                  "twoshot_sentinel_out", "twoshot_atomic", "oneshot", "oneshot_line", "oneshot_sentinel", "auto"):
         out[algo] = paced_collective(torch, ll, reg, "ar", n, ll.ALGOS[algo], steps, 20)
-    ll.check(ll.ll_set_auto_sentinel(1), "auto sentinel")
-    try:
-        out["auto_sentinel_allowed"] = paced_collective(torch, ll, reg, "ar", n, ll.ALGOS["auto"], steps, 20)
-    finally:
-        ll.ll_set_auto_sentinel(0)
+    out["auto_sentinel_allowed"] = paced_collective(torch, ll, reg, "ar", n, ll.ALGOS["auto"], steps, 20,
+                                                    flags=ll.LL_OPT_AUTO_SENTINEL)
     return out
 
 
@@ -465,8 +471,9 @@ def bench_bandwidth(torch, ll, count, algos, iters=20, warmup=3):
     stream = torch.cuda.current_stream()
     res = {}
     for algo in algos:
+        shape = ll.Options(report=True)
         for _ in range(warmup):
-            ll.check(reg.allreduce(count, algo), algo)
+            ll.check(reg.allreduce(count, algo, opt=shape), algo)
         ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         ev0.record(stream)
@@ -478,7 +485,7 @@ def bench_bandwidth(torch, ll, count, algos, iters=20, warmup=3):
         us = ev0.elapsed_time(ev1) * 1000.0 / iters
         nbytes = bytemodel.allreduce_bytes(algo, p, count, 4)
         useful = bytemodel.useful_bytes(p, count, 4)
-        grid, threads = ll.ll_last_grid()
+        grid, threads = shape.grid, shape.threads
         res[algo] = {"kernel_us": us, "algorithmic_bytes": nbytes, "gbps": nbytes / us / 1e3,
                      "useful_gbps": useful / us / 1e3, "grid": grid, "threads": threads}
     del reg
@@ -647,7 +654,6 @@ def main():
     result["device"] = {"name": props.name, "arch": getattr(props, "gcnArchName", ""),
                         "compute_units": props.multi_processor_count, "hbm_bytes": props.total_memory,
                         "hip_runtime": getattr(torch.version, "hip", None), "torch": torch.__version__}
-    ll.ll_set_poll_timeout(200_000_000)
     if want("headline"):
         log("headline: 16 KiB bf16 one-shot, 8 ranks")
         result["headline"] = bench_headline(torch, ll, args.steps, args.warmup)

@@ -29,8 +29,15 @@
  *   [cap + A8, cap + A8 + A128)   128-byte line area
  *   [.., .. + AA)                 binary32 accumulators and tile counters (atomic two-shot)
  *   [.., .. + AS)                 sentinel area (payload only)
- * cap (the input capacity, a multiple of 256 bytes) is the largest input for
- * which both packet areas fit every algorithm; ll_input_capacity reports it.
+ * A region holds the areas of a set of packet formats, encoded in its
+ * stride: (rank_stride / 256) mod 16 has one bit per format (LL_FMT_*), and
+ * 0 means all of them, so every stride that is a multiple of 4 KiB holds all
+ * formats.  ll_slice_bytes returns such a stride for LL_ALGO_AUTO and, for a
+ * named algorithm, the smaller stride of a region that holds that
+ * algorithm's format only.  cap (the input capacity, a multiple of 256
+ * bytes) is the largest input for which the present areas fit every
+ * algorithm of their format; ll_input_capacity reports it.  A call whose
+ * packet format the region does not hold returns LL_ERR_SCRATCH.
  *
  * Element types: binary32 and bfloat16.  The reduction is the sum of the P
  * inputs in ascending rank order, accumulated in binary32, rounded once to the
@@ -52,13 +59,17 @@
  *
  * Ownership.  The caller allocates and frees the symmetric region and `out`,
  * and keeps them alive until the stream has run the call.  The library keeps
- * no per-region state.  Two calls on one region must not run concurrently
+ * no per-region state and no settings: what a call does depends on its
+ * arguments only (and on its ll_options, for the entry points that take
+ * them).  Its only global state is a lazily built, thread-safe table of
+ * kernels and device properties and, per device, the status words of the
+ * streams that ran calls.  Two calls on one region must not run concurrently
  * (use one stream per region).
  *
- * Failure.  Every wait on a flag is bounded (ll_set_poll_timeout).  A wait
- * that expires records LL_ERR_TIMEOUT in a device status word and lets the
- * kernel finish; ll_check reports it.  The outputs of such a call are
- * undefined.
+ * Failure.  Every wait on a flag is bounded (ll_options.poll_timeout,
+ * default 2 s).  A wait that expires records LL_ERR_TIMEOUT in the status
+ * word of the stream the call runs on and lets the kernel finish; ll_check
+ * on that stream reports it.  The outputs of such a call are undefined.
  */
 #ifndef LLCOLL_H
 #define LLCOLL_H
@@ -146,20 +157,57 @@ typedef enum { LL_PROTO_AUTO = 0, LL_PROTO_PACKET8 = 1, LL_PROTO_LINE128 = 2, LL
 #define LL_MAX_RANKS 8
 #define LL_ALIGN 256
 
-/* Minimum rank_stride (bytes, multiple of 256) whose input capacity holds
- * `count` elements of `dt` for nranks ranks.  `count` is the per-rank input
- * length of the largest call the region will serve: count for AllReduce,
- * nranks*recvcount for ReduceScatter, sendcount for AllGather.  This is the
- * host-side sizing helper of Sec. V ("Host-side Functions"). */
-int ll_slice_bytes(size_t count, ll_dtype dt, int nranks, size_t *min_rank_stride);
+/* Packet formats a region holds: bits of (rank_stride / 256) mod 16, where 0
+ * means all formats. */
+#define LL_FMT_PACKET8 1u   /* 8-byte packets */
+#define LL_FMT_LINE128 2u   /* 128-byte lines */
+#define LL_FMT_SENTINEL 4u  /* sentinel units */
+#define LL_FMT_ATOMIC 8u    /* binary32 accumulators of LL_ALGO_TWOSHOT_ATOMIC */
+
+/* Per-call options of the *_ex entry points (and ll_broadcast, ll_reduce,
+ * ll_allreduce_buffered).  NULL means the defaults, which are also what the
+ * entry points without options use.  Fill with ll_options_init, then set
+ * fields. */
+typedef struct ll_tuning ll_tuning; /* benchmark and test hooks: include/lltune.h */
+typedef struct {
+  uint32_t size;            /* sizeof(ll_options), set by ll_options_init */
+  uint32_t flags;           /* LL_OPT_* bits; default 0 */
+  uint64_t poll_timeout;    /* bound of every flag wait, in ticks of the 100 MHz
+                               constant clock; 0 = the default, 2e8 (2 s) */
+  const ll_tuning *tuning;  /* launch-shape and test hooks; NULL = none */
+} ll_options;
+
+/* The automatic choices (LL_ALGO_AUTO, LL_PROTO_AUTO) may use sentinel mode:
+ * for callers whose data never holds the sentinel dword (see below).  Never
+ * selects LL_ALGO_TWOSHOT_SENTINEL_OUT. */
+#define LL_OPT_AUTO_SENTINEL 0x1u
+/* The automatic choices never use 128-byte line packets, whose correctness
+ * rests on a measured, not a guaranteed, property of the chip (a 64-byte
+ * half of a line is never seen torn across XCDs): they take the 8-byte-packet
+ * algorithm of the same shape instead.  Named line algorithms still run. */
+#define LL_OPT_NO_LINES 0x2u
+
+int ll_options_init(ll_options *opt);
+
+/* Minimum rank_stride (bytes, multiple of 256) of a region whose input
+ * capacity holds `count` elements of `dt` for nranks ranks and `algo`.
+ * `count` is the per-rank input length of the largest call the region will
+ * serve: count for AllReduce, nranks*recvcount for ReduceScatter, sendcount
+ * for AllGather.  algo = LL_ALGO_AUTO sizes a region for every algorithm and
+ * packet format (a multiple of 4 KiB); a named algorithm sizes it for that
+ * algorithm's packet format only (the region then serves every call in that
+ * format: ReduceScatter, AllGather, Broadcast and Reduce in it too, and AUTO
+ * chooses within it).  This is the host-side sizing helper of Sec. V
+ * ("Host-side Functions"). */
+int ll_slice_bytes(size_t count, ll_dtype dt, int nranks, ll_algo algo, size_t *min_rank_stride);
 
 /* Input capacity in bytes of a region with this rank_stride and rank count. */
 int ll_input_capacity(size_t rank_stride, int nranks, size_t *capacity_bytes);
 
 /* Byte offsets, within every slice, of the areas of the slice layout:
  * offsets6 = {input area (0), 8-byte packet area, line area, atomic
- * accumulator area, sentinel area, end of the sentinel area}.  Host-only;
- * errors as ll_input_capacity. */
+ * accumulator area, sentinel area, end of the sentinel area}; an area the
+ * region does not hold is empty.  Host-only; errors as ll_input_capacity. */
 int ll_slice_layout(size_t rank_stride, int nranks, size_t *offsets6);
 
 /* Zero both flagged packet areas and the accumulator area of every slice
@@ -184,30 +232,38 @@ int ll_allreduce(void *sym_base, size_t rank_stride, void *out, size_t count, ll
 int ll_allreduce_algo(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt,
                       ll_op op, int nranks, uint32_t epoch, void *stream, ll_algo algo);
 
-/* The algorithm that LL_ALGO_AUTO runs for a single-call AllReduce
- * (ll_allreduce) of `count` elements of `dt` per rank over `nranks` ranks,
- * under the current ll_set_auto_sentinel setting, written to *algo.  The
- * choice follows measured crossovers on the MI355X: one-shot with one wave
- * per peer for small messages, the two-shot wave kernels for medium ones,
- * the line two-shot for large ones.  Host only, no HIP call.
- * LL_ERR_INVALID: algo NULL or nranks outside [2, 8]; LL_ERR_UNSUPPORTED:
- * unknown dtype. */
-int ll_auto_algo(size_t count, ll_dtype dt, int nranks, ll_algo *algo);
+/* Same, with per-call options (opt may be NULL). */
+int ll_allreduce_ex(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt, ll_op op,
+                    int nranks, uint32_t epoch, void *stream, ll_algo algo, const ll_options *opt);
+
+/* The algorithm that LL_ALGO_AUTO runs for a single-call AllReduce of
+ * `count` elements of `dt` per rank over `nranks` ranks on a region whose
+ * stride is `rank_stride` (0: a region of every packet format), with options
+ * `opt` (may be NULL), written to *algo.  The choice follows measured
+ * crossovers on the MI355X: one-shot with one wave per peer for small
+ * messages, the two-shot wave kernels for medium ones, the line two-shot for
+ * large ones; within the region's packet formats and the options.  Host
+ * only, no HIP call.  LL_ERR_INVALID: algo NULL or nranks outside [2, 8];
+ * LL_ERR_UNSUPPORTED: unknown dtype; LL_ERR_SCRATCH: the region holds no
+ * format AUTO may use. */
+int ll_auto_algo(size_t count, ll_dtype dt, int nranks, size_t rank_stride, const ll_options *opt, ll_algo *algo);
 
 /* ReduceScatter (sum): rank r's input is nranks*recvcount elements; rank r
  * receives elements [r*recvcount, (r+1)*recvcount) of the sum (Sec. III-A). */
 int ll_reduce_scatter(void *sym_base, size_t rank_stride, void *out, size_t recvcount,
                       ll_dtype dt, ll_op op, int nranks, uint32_t epoch, void *stream);
-int ll_reduce_scatter_proto(void *sym_base, size_t rank_stride, void *out, size_t recvcount,
-                            ll_dtype dt, ll_op op, int nranks, uint32_t epoch, void *stream,
-                            ll_proto proto);
+/* Same, with the packet format named and per-call options (opt may be NULL). */
+int ll_reduce_scatter_ex(void *sym_base, size_t rank_stride, void *out, size_t recvcount, ll_dtype dt,
+                         ll_op op, int nranks, uint32_t epoch, void *stream, ll_proto proto,
+                         const ll_options *opt);
 
 /* AllGather: rank r's input is sendcount elements; every rank receives the
  * concatenation of all inputs in rank order (Sec. III-A). */
 int ll_allgather(void *sym_base, size_t rank_stride, void *out, size_t sendcount, ll_dtype dt,
                  int nranks, uint32_t epoch, void *stream);
-int ll_allgather_proto(void *sym_base, size_t rank_stride, void *out, size_t sendcount,
-                       ll_dtype dt, int nranks, uint32_t epoch, void *stream, ll_proto proto);
+/* Same, with the packet format named and per-call options (opt may be NULL). */
+int ll_allgather_ex(void *sym_base, size_t rank_stride, void *out, size_t sendcount, ll_dtype dt,
+                    int nranks, uint32_t epoch, void *stream, ll_proto proto, const ll_options *opt);
 
 /* ---- bounded scratch: multi-iteration AllReduce with double buffering ----
  *
@@ -254,7 +310,7 @@ int ll_scratch_init(void *scratch_base, size_t scratch_stride, int nranks, void 
  * epochs_used may be NULL.  One kernel launch on `stream`. */
 int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, ll_op op, int nranks,
                           void *scratch_base, size_t scratch_stride, uint32_t epoch, void *stream, ll_algo algo,
-                          uint32_t *epochs_used);
+                          const ll_options *opt, uint32_t *epochs_used);
 
 /* ---- no allocation: AllReduce through a scratch the library holds ----
  *
@@ -292,97 +348,31 @@ int ll_allreduce_static(const void *in, void *out, size_t count, ll_dtype dt, ll
  * the root stores packets into one slot of every peer (the paper lists
  * Broadcast among the collectives built from the same primitives, Sec. V).
  * root in [0, nranks).  proto as for ReduceScatter (AUTO: 8-byte packets up
- * to 64 KiB, then lines, or sentinel when allowed). */
+ * to 64 KiB, then lines, or sentinel when allowed); opt may be NULL. */
 int ll_broadcast(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt, int root, int nranks,
-                 uint32_t epoch, void *stream, ll_proto proto);
+                 uint32_t epoch, void *stream, ll_proto proto, const ll_options *opt);
 
 /* Reduce (sum): the root receives the AllReduce result, `count` elements at
  * `out` (only the root's result is written).  Every other rank stores its
  * input as packets into its slot of the root, which sums in ascending rank
  * order and rounds once, as ll_allreduce. */
 int ll_reduce(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt, ll_op op, int root,
-              int nranks, uint32_t epoch, void *stream, ll_proto proto);
+              int nranks, uint32_t epoch, void *stream, ll_proto proto, const ll_options *opt);
 
-/* Synchronise `stream`, then report and clear the device status word:
- * LL_OK, LL_ERR_TIMEOUT, or LL_ERR_HIP. */
+/* Synchronise `stream`, then report and clear the status word of that stream
+ * (the word its calls' timed-out waits report into): LL_OK, LL_ERR_TIMEOUT,
+ * or LL_ERR_HIP.  Calls on other streams are not seen.  A stream keeps its
+ * status word for the life of the process; beyond 256 streams per device,
+ * later streams share words. */
 int ll_check(void *stream);
 
-/* Details of the last timeout seen by ll_check: rank, the bit mask of peers
- * not heard from, and the epoch waited for.  Any pointer may be NULL. */
+/* Details of the last timeout ll_check reported in the calling thread: rank,
+ * the bit mask of peers not heard from, and the epoch waited for.  Any
+ * pointer may be NULL. */
 int ll_last_timeout(int *rank, uint32_t *missing_peers, uint32_t *epoch);
 
 /* Human-readable text for a status code. */
 const char *ll_strerror(int status);
-
-/* ---- tuning and test hooks (process-wide settings; not thread-safe) ---- */
-
-/* Whether the automatic choices (LL_ALGO_AUTO, LL_PROTO_AUTO) may use sentinel
- * mode, for callers whose data never holds the sentinel dword (0 = no, the
- * default; 1 = yes).  Never selects LL_ALGO_TWOSHOT_SENTINEL_OUT. */
-int ll_set_auto_sentinel(int allow);
-
-/* Kernel family of the stand-alone ReduceScatter / AllGather: 0 = by size
- * (one wave per peer with LDS staging up to 2-8 MiB of data per rank, by
- * packet format and rank count; one lane per packet unit above), 1 = one lane
- * per unit always, 2 = one wave per peer always.  Results do not depend on
- * it. */
-int ll_set_wave_kernels(int mode);
-
-/* Workgroups per rank and threads per workgroup for the following calls;
- * 0 = automatic.  threads must be a multiple of 64 in [64, 1024].  Results do
- * not depend on these settings. */
-int ll_set_launch(int workgroups_per_rank, int threads);
-
-/* Poll pacing for the following calls, in units of 64 shader cycles: idle
- * time before a lane's first poll of its peers (first_wait) and between
- * polls (poll_gap), each in [0, 1000].  0 = poll back to back. */
-int ll_set_poll_pacing(int first_wait, int poll_gap);
-
-/* Two-shot pipeline distance for the following calls: a lane publishes the
- * ReduceScatter packets of step s, reduces step s-lag and gathers step
- * s-2*lag; lag 0 does all three for one step before the next (each wait is
- * then for the same step of a peer's lane, which publishes before it waits).
- * lag in [0, 64]; default 1. */
-int ll_set_pipeline_lag(int lag);
-
-/* Packet units per lane of the wave-per-peer kernels (one-shot, two-shot,
- * stand-alone ReduceScatter / AllGather) for the following calls: 1, 2 or 4;
- * 0 = automatic (one, or two for a two-shot AllReduce whose tiles exceed one
- * round of resident workgroups).  A unit is one 16-byte store per lane, or a
- * whole 128-byte-line unit per wave.  Results do not depend on it. */
-int ll_set_wave_units(int units_per_lane);
-
-/* Flag-wait budget in ticks of the 100 MHz constant clock (default 2e8,
- * i.e. 2 s).  Must be >= 1. */
-int ll_set_poll_timeout(uint64_t ticks);
-
-/* Test hook: rank `rank` publishes nothing (-1 = off), so its peers' waits
- * expire; used to test timeout reporting. */
-int ll_debug_mute_rank(int rank);
-
-/* Benchmark hook: when `stamps` (device memory) is non-NULL, the next launch
- * writes each workgroup's start and end time (100 MHz ticks) to
- * stamps[b] and stamps[grid + b].  The pointer is used for one launch only. */
-int ll_debug_stamp_next(uint64_t *stamps);
-
-/* Diagnostics hook: when `phases` (device memory) is non-NULL, the next
- * one-shot launch records phase times.  The stamps exist only in a library
- * built for it (the default build leaves them out of the kernels' critical
- * paths); otherwise `phases` is ignored.
- * LL_ALGO_ONESHOT, built with -DLLCOLL_ONESHOT_PHASES=1 (4*grid words): for
- * thread 0 of each workgroup b and its last packet unit, phases[4b] = time
- * its input load returned, phases[4b+1] = time its packet stores were
- * acknowledged (the kernel waits for them only in this mode), phases[4b+2] =
- * time its wait for peers ended, phases[4b+3] = number of polls it issued.
- * LL_ALGO_ONESHOT_WAVES, built with -DLLCOLL_WAVE_PHASES=1 (4*grid*nranks
- * words): for lane 0 of wave w of workgroup b and its first tile,
- * phases[4(b*nranks+w)] = time its input load returned, [..+1] = time its
- * peer's packets had all arrived, [..+2] = time it left the workgroup
- * barrier.  Used for one launch only. */
-int ll_debug_phase_next(uint64_t *phases);
-
-/* Grid (total workgroups) of the last launch. */
-int ll_last_grid(int *grid, int *threads);
 
 #ifdef __cplusplus
 }

@@ -27,6 +27,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "llcoll.h"
+
 #ifdef __cplusplus
 extern "C" {
 #endif
@@ -65,28 +67,28 @@ int ll_probe_spin(uint64_t ticks, void *stream);
 
 /* Back-to-back launch loops run from C (so the host is never the bottleneck).
  *
- * ll_bench_allreduce: `calls` AllReduces (ll_allreduce_algo with op = sum) with
- * epochs first_epoch .. first_epoch+calls-1.  If stamps != NULL, call i writes
- * its per-workgroup start/end times at stamps + i*stamp_stride (see
- * ll_debug_stamp_next; stamp_stride >= 2*grid).
+ * ll_bench_allreduce: `calls` AllReduces (ll_allreduce_ex with op = sum) with
+ * epochs first_epoch .. first_epoch+calls-1 and options `opt` (may be NULL).
+ * If stamps != NULL, call i writes its per-workgroup start/end times at
+ * stamps + i*stamp_stride (see ll_tuning.stamps; stamp_stride >= 2*grid).
  * ll_bench_reduce_scatter / ll_bench_allgather: the same for the stand-alone
  * collectives (proto as ll_proto).
  * ll_bench_floor: `calls` floor kernels; call i loads line
  * (first_line + i*line_step) mod (chase_len/16) of `chase` (16 words a line).
  * ll_bench_empty: `calls` empty kernels. */
 int ll_bench_allreduce(void *sym_base, size_t rank_stride, void *out, size_t count, int dt, int nranks,
-                       uint32_t first_epoch, int calls, int algo, uint64_t *stamps, int stamp_stride,
-                       void *stream);
+                       uint32_t first_epoch, int calls, int algo, const ll_options *opt, uint64_t *stamps,
+                       int stamp_stride, void *stream);
 int ll_bench_reduce_scatter(void *sym_base, size_t rank_stride, void *out, size_t recvcount, int dt, int nranks,
-                            uint32_t first_epoch, int calls, int proto, uint64_t *stamps, int stamp_stride,
-                            void *stream);
+                            uint32_t first_epoch, int calls, int proto, const ll_options *opt, uint64_t *stamps,
+                            int stamp_stride, void *stream);
 int ll_bench_allgather(void *sym_base, size_t rank_stride, void *out, size_t sendcount, int dt, int nranks,
-                       uint32_t first_epoch, int calls, int proto, uint64_t *stamps, int stamp_stride,
-                       void *stream);
+                       uint32_t first_epoch, int calls, int proto, const ll_options *opt, uint64_t *stamps,
+                       int stamp_stride, void *stream);
 /* ll_bench_rooted: `calls` Broadcasts (kind 0) or Reduces (kind 1). */
 int ll_bench_rooted(int kind, void *sym_base, size_t rank_stride, void *out, size_t count, int dt, int root,
-                    int nranks, uint32_t first_epoch, int calls, int proto, uint64_t *stamps, int stamp_stride,
-                    void *stream);
+                    int nranks, uint32_t first_epoch, int calls, int proto, const ll_options *opt,
+                    uint64_t *stamps, int stamp_stride, void *stream);
 int ll_bench_floor(const uint64_t *chase, uint64_t chase_len, uint64_t first_line, uint64_t line_step,
                    uint64_t *sink, int grid, int threads, int calls, uint64_t *stamps, int stamp_stride,
                    void *stream);
@@ -105,9 +107,10 @@ int ll_bench_empty(int grid, int threads, int calls, uint64_t *stamps, int stamp
  * positive multiple of 8 and fit one tile per workgroup with every
  * workgroup resident.  out receives nranks*count elements: each element of
  * rank r's output equals that element of some rank's input.  stamps as for
- * ll_bench_allreduce. */
+ * ll_bench_allreduce; grid_out (NULL or host memory) receives the grid. */
 int ll_bench_exchange(void *sym_base, size_t rank_stride, void *out, size_t count, int dt, int nranks,
-                      uint32_t first_epoch, int calls, uint64_t *stamps, int stamp_stride, void *stream);
+                      uint32_t first_epoch, int calls, uint64_t *stamps, int stamp_stride, int *grid_out,
+                      void *stream);
 
 /* ids[b] = XCD index of workgroup b. */
 int ll_probe_xcd(uint32_t *ids, int grid, int threads, void *stream);

@@ -10,7 +10,9 @@ into ``paper_2607_16100_amd/libllcoll.so`` with hipcc:
 each to an object of its own, in parallel, then linked into one shared
 library.  Extra preprocessor definitions (diagnostic builds) can be passed
 with ``extra_defines``; such a build goes to ``out`` instead of the default
-library path.
+library path.  ``build_phases`` (``--phases``) builds the diagnostic variant
+with the one-shot wave kernels' phase stamps compiled in,
+``libllcoll_phases.so``, which ``timeline.py`` loads.
 """
 from __future__ import annotations
 
@@ -23,6 +25,7 @@ from concurrent.futures import ThreadPoolExecutor
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libllcoll.so")
+PHASES_LIB = os.path.join(HERE, "libllcoll_phases.so")
 ARCH = os.environ.get("LLCOLL_ARCH", "gfx950")
 RANKS = range(2, 9)
 
@@ -79,5 +82,12 @@ def build(verbose: bool = False, extra_defines=(), out: str | None = None, jobs:
     return target
 
 
+def build_phases(verbose: bool = False) -> str:
+    return build(verbose, extra_defines=("LLCOLL_WAVE_PHASES=1",), out=PHASES_LIB)
+
+
 if __name__ == "__main__":
-    print(build(verbose=True))
+    if "--phases" in sys.argv[1:]:
+        print(build_phases(verbose=True))
+    else:
+        print(build(verbose=True))

@@ -6,12 +6,17 @@
 //   [cap + A8, cap + A8 + A128) 128-byte line area
 //   [.., .. + AA)              atomic accumulator and tile counters
 //   [.., .. + AS)              sentinel area (payload only, reset after use)
-// where cap is the largest multiple of 256 for which both areas, sized for
-// the most demanding algorithm at an input of cap bytes, fit in the slice.
-// The layout therefore depends only on (stride, P): a byte that holds input
-// in one call is never read as a flag in another, and the two packet formats
-// never share bytes, so a stale payload word can never pose as a flag.  The
-// sentinel area holds nothing but payload and sentinels.
+// An area is present only if the region holds that packet format: the
+// region's format set is (stride / 256) mod 16, a bit per format (kFmt8,
+// kFmtLine, kFmtSent, kFmtAtomic), where 0 stands for all four -- so any
+// stride that is a multiple of 4 KiB holds every format, and ll_slice_bytes
+// adds the bits of a one-algorithm region to a multiple of 4 KiB.  cap is the
+// largest multiple of 256 for which the present areas, each sized for the most
+// demanding algorithm of its format at an input of cap bytes, fit in the
+// slice.  The layout therefore depends only on (stride, P): a byte that
+// holds input in one call is never read as a flag in another, and two packet
+// formats never share bytes, so a stale payload word can never pose as a
+// flag.  The sentinel area holds nothing but payload and sentinels.
 //
 // Within an area a call places its slots from the area's start:
 //   one-shot / AllGather   P-1 slots, each holding a full input
@@ -81,16 +86,52 @@ inline uint64_t areaA(uint64_t M, int P) {
   return atomic_acc_bytes(cb, 2) + roundup(4 * ceil_div(cb, 1024), kAlign);
 }
 
-inline uint64_t slice_for(uint64_t cap, int P) {
-  return cap + area8(cap, P) + area128(cap, P) + areaA(cap, P) + areaS(cap, P);
+// Packet formats a region holds (bits of the format set).
+constexpr unsigned kFmt8 = 1, kFmtLine = 2, kFmtSent = 4, kFmtAtomic = 8, kFmtAll = 15;
+constexpr uint64_t kFmtUnit = 4096;  // strides with no format bits are multiples of this
+
+// The format set of a region with this stride.
+inline unsigned formats_of(uint64_t stride) {
+  const unsigned m = (unsigned)((stride / kAlign) % 16);
+  return m == 0 ? kFmtAll : m;
 }
 
-// Largest cap (multiple of 256, at most kMaxInputBytes) with slice_for(cap) <= stride.
+// Area sizes of a slice with input capacity cap and format set fmt.
+struct Areas {
+  uint64_t a8, a128, aa, as;
+};
+inline Areas areas(uint64_t cap, int P, unsigned fmt) {
+  Areas a;
+  a.a8 = (fmt & kFmt8) ? area8(cap, P) : 0;
+  a.a128 = (fmt & kFmtLine) ? area128(cap, P) : 0;
+  a.aa = (fmt & kFmtAtomic) ? areaA(cap, P) : 0;
+  a.as = (fmt & kFmtSent) ? areaS(cap, P) : 0;
+  return a;
+}
+
+inline uint64_t slice_for(uint64_t cap, int P, unsigned fmt = kFmtAll) {
+  const Areas a = areas(cap, P, fmt);
+  return cap + a.a8 + a.a128 + a.aa + a.as;
+}
+
+// The smallest stride with format set fmt whose slices hold an input of cap
+// bytes: a multiple of 4 KiB plus the format bits.
+inline uint64_t stride_for(uint64_t cap, int P, unsigned fmt) {
+  const uint64_t need = slice_for(cap, P, fmt);
+  const uint64_t bits = fmt == kFmtAll ? 0 : (uint64_t)fmt * kAlign;
+  uint64_t s = need / kFmtUnit * kFmtUnit + bits;
+  if (s < need) s += kFmtUnit;
+  return s;
+}
+
+// Largest cap (multiple of 256, at most kMaxInputBytes) with
+// slice_for(cap, P, formats_of(stride)) <= stride.
 inline uint64_t capacity(uint64_t stride, int P) {
+  const unsigned fmt = formats_of(stride);
   uint64_t lo = 0, hi = std::min(stride, kMaxInputBytes) / kAlign;
   while (lo < hi) {
     const uint64_t mid = (lo + hi + 1) / 2;
-    if (slice_for(mid * kAlign, P) <= stride) {
+    if (slice_for(mid * kAlign, P, fmt) <= stride) {
       lo = mid;
     } else {
       hi = mid - 1;

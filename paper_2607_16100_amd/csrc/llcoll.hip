@@ -7,7 +7,6 @@
 #include <string.h>
 
 #include <algorithm>
-#include <atomic>
 #include <map>
 #include <mutex>
 #include <tuple>
@@ -35,21 +34,56 @@ namespace L = llc::layout;
 
 namespace {
 
-// ---------------------------------------------------------------- settings
-std::atomic<int> g_wg_per_rank{0};
-std::atomic<int> g_threads{0};
-std::atomic<uint64_t> g_timeout{200000000ull};  // 2 s of the 100 MHz clock
-std::atomic<int> g_mute{-1};
-std::atomic<int> g_first_wait{0};
-std::atomic<int> g_poll_gap{0};
-std::atomic<int> g_wave_units{0};  // 0 = automatic, else 1, 2 or 4
-std::atomic<int> g_lag{1};
-std::atomic<int> g_auto_sentinel{0};
-std::atomic<int> g_wave_kernels{0};
-std::atomic<uint64_t *> g_stamps{nullptr};
-std::atomic<uint64_t *> g_phases{nullptr};
-std::atomic<int> g_last_grid{0};
-std::atomic<int> g_last_threads{0};
+// ---------------------------------------------------------------- per-call options
+constexpr uint64_t kDefaultTimeout = 200000000ull;  // 2 s of the 100 MHz clock
+
+// What one call runs with: its ll_options (and their ll_tuning) resolved
+// against the defaults.  Nothing of it outlives the call.
+struct CallOpts {
+  uint32_t flags = 0;
+  uint64_t timeout = kDefaultTimeout;
+  int wg_per_rank = 0, threads = 0, wave_units = 0, wave_kernels = 0, lag = 1, first_wait = 0, poll_gap = 0;
+  int mute = -1;
+  uint64_t *stamps = nullptr, *phases = nullptr;
+  int *grid_out = nullptr, *threads_out = nullptr;
+  bool sentinel_ok() const { return (flags & LL_OPT_AUTO_SENTINEL) != 0; }
+  bool lines_ok() const { return (flags & LL_OPT_NO_LINES) == 0; }
+  bool forced_shape() const { return wg_per_rank != 0 || threads != 0; }
+};
+
+// Checks and resolves `o` (NULL = defaults); no HIP call.
+int resolve_opts(const ll_options *o, CallOpts *c) {
+  *c = CallOpts();
+  if (o == nullptr) return LL_OK;
+  if (o->size != sizeof(ll_options)) return LL_ERR_INVALID;
+  if ((o->flags & ~(uint32_t)(LL_OPT_AUTO_SENTINEL | LL_OPT_NO_LINES)) != 0) return LL_ERR_INVALID;
+  c->flags = o->flags;
+  if (o->poll_timeout != 0) c->timeout = o->poll_timeout;
+  const ll_tuning *t = o->tuning;
+  if (t == nullptr) return LL_OK;
+  if (t->size != sizeof(ll_tuning)) return LL_ERR_INVALID;
+  if (t->workgroups_per_rank < 0 || t->workgroups_per_rank > 4096) return LL_ERR_INVALID;
+  if (t->threads != 0 && (t->threads < 64 || t->threads > 1024 || t->threads % 64 != 0)) return LL_ERR_INVALID;
+  if (t->wave_units != 0 && t->wave_units != 1 && t->wave_units != 2 && t->wave_units != 4) return LL_ERR_INVALID;
+  if (t->wave_kernels < 0 || t->wave_kernels > 2) return LL_ERR_INVALID;
+  if (t->pipeline_lag < -1 || t->pipeline_lag > 64) return LL_ERR_INVALID;
+  if (t->first_wait < 0 || t->first_wait > 1000 || t->poll_gap < 0 || t->poll_gap > 1000) return LL_ERR_INVALID;
+  if (t->mute_rank < -1 || t->mute_rank >= LL_MAX_RANKS) return LL_ERR_INVALID;
+  c->wg_per_rank = t->workgroups_per_rank;
+  c->threads = t->threads;
+  c->wave_units = t->wave_units;
+  c->wave_kernels = t->wave_kernels;
+  c->lag = t->pipeline_lag < 0 ? 1 : t->pipeline_lag;
+  c->first_wait = t->first_wait;
+  c->poll_gap = t->poll_gap;
+  c->mute = t->mute_rank;
+  c->stamps = t->stamps;
+  c->phases = t->phases;
+  c->grid_out = t->grid_out;
+  c->threads_out = t->threads_out;
+  return LL_OK;
+}
+
 thread_local int t_last_hip = 0;
 thread_local char t_msg[256];
 struct TimeoutInfo {
@@ -215,6 +249,7 @@ struct Plan {
   int dt, P;
   KArgs a;
   int64_t units;  // packet units per stream
+  CallOpts o;     // the call's options
 };
 
 // Units per lane (U) of the wave-per-peer kernels, measured at 16 KiB ..
@@ -228,7 +263,7 @@ struct Plan {
 // Elsewhere two units per lane are never more than about 3 % faster and up
 // to 25 % slower.
 int wave_units_log2(const Plan &pl, int wpr) {
-  const int forced = g_wave_units.load();
+  const int forced = pl.o.wave_units;
   if (forced == 1) return 0;
   if (forced == 2) return 1;
   if (forced == 4) return 2;
@@ -259,8 +294,8 @@ int launch(const Plan &pl, void *stream) {
   // The latency-bound one-shot: one tile of 64 one-lane units per workgroup,
   // every stream 4-byte aligned, all tiles resident at once, no forced
   // launch shape -> the straight-line one-tile kernel.
-  if (pl.kind == K_ONESHOT_WAVES && wlog == 0 && pl.proto != PR_LINE && g_wg_per_rank.load() == 0 &&
-      g_threads.load() == 0 && pl.a.al4 != 0 && (pl.a.in == nullptr || pl.a.in_al4 != 0) && pl.a.iters <= 1) {
+  if (pl.kind == K_ONESHOT_WAVES && wlog == 0 && pl.proto != PR_LINE && !pl.o.forced_shape() && pl.a.al4 != 0 &&
+      (pl.a.in == nullptr || pl.a.in_al4 != 0) && pl.a.iters <= 1) {
     kernel_fn tf = table().tile[pl.proto == PR_SENT ? 1 : 0][pl.dt][pl.P];
     int cap = 0;
     const int rc = resident_grid(tf, 64 * pl.P, &cap);
@@ -268,7 +303,7 @@ int launch(const Plan &pl, void *stream) {
     const int64_t tiles = (pl.units + 63) / 64;
     if (tf != nullptr && tiles <= cap / pl.P) return launch_kernel(tf, pl, (int)tiles, 64 * pl.P, stream);
   }
-  int threads = g_threads.load();
+  int threads = pl.o.threads;
   if (threads == 0) threads = 256;
   int lanes_per_unit = pl.proto == PR_LINE ? ProtoLine::kLanes : 1;
   int64_t work_units = pl.units;
@@ -283,7 +318,7 @@ int launch(const Plan &pl, void *stream) {
   if (st != LL_OK) return st;
   int wmax = cap_grid / pl.P;
   if (wmax < 1) return LL_ERR_UNSUPPORTED;
-  int W = g_wg_per_rank.load();
+  int W = pl.o.wg_per_rank;
   if (W == 0) {
     const int64_t lanes = work_units * lanes_per_unit;
     int64_t want = (lanes + threads - 1) / threads;
@@ -308,22 +343,22 @@ int launch_kernel(kernel_fn fn, const Plan &pl, int W, int threads, void *stream
     a.iters = 1;
     a.iter_n = a.n;
   }
-  a.timeout = g_timeout.load();
-  a.mute = g_mute.load();
-  a.first_wait = (uint16_t)g_first_wait.load();
-  a.poll_gap = (uint16_t)g_poll_gap.load();
-  a.lag = (uint32_t)g_lag.load();
+  a.timeout = pl.o.timeout;
+  a.mute = pl.o.mute;
+  a.first_wait = (uint16_t)pl.o.first_wait;
+  a.poll_gap = (uint16_t)pl.o.poll_gap;
+  a.lag = (uint32_t)pl.o.lag;
   a.grid = (uint32_t)grid;
   a.block = (uint32_t)threads;
   a.units = pl.units;
   const int st = status_of(stream, &a.status);
   if (st != LL_OK) return st;
-  a.stamps = g_stamps.exchange(nullptr);
-  a.phases = g_phases.exchange(nullptr);
+  a.stamps = pl.o.stamps;
+  a.phases = pl.o.phases;
   hipLaunchKernelGGL(fn, dim3(grid), dim3(threads), 0, (hipStream_t)stream, a);
   hipError_t e = hipGetLastError();
-  g_last_grid.store(grid);
-  g_last_threads.store(threads);
+  if (pl.o.grid_out) *pl.o.grid_out = grid;
+  if (pl.o.threads_out) *pl.o.threads_out = threads;
   if (e != hipSuccess) {
     t_last_hip = (int)e;
     return LL_ERR_HIP;
@@ -332,9 +367,11 @@ int launch_kernel(kernel_fn fn, const Plan &pl, int W, int threads, void *stream
 }
 
 // Region geometry of one call; fails with LL_ERR_SCRATCH when the input does
-// not fit the region's input capacity.
+// not fit the region's input capacity.  fmt: the packet formats the region
+// holds (L::kFmt* bits).
 struct Region {
   uint64_t cap, a8, a128, aa, as;
+  unsigned fmt;
   uint64_t area_of(int proto) const {
     return proto == PR_LINE ? cap + a8 : (proto == PR_SENT ? cap + a8 + a128 + aa : cap);
   }
@@ -351,15 +388,18 @@ int64_t units_of(int proto, uint64_t bytes) {
 }
 
 int region_of(size_t rank_stride, int P, uint64_t in_bytes, Region *rg) {
+  const unsigned fmt = L::formats_of(rank_stride);
   const uint64_t cap = L::capacity(rank_stride, P);
-  if (L::slice_for(cap, P) > rank_stride) return LL_ERR_SCRATCH;
+  if (L::slice_for(cap, P, fmt) > rank_stride) return LL_ERR_SCRATCH;
   if (in_bytes > L::kMaxInputBytes) return LL_ERR_UNSUPPORTED;
   if (in_bytes > cap) return LL_ERR_SCRATCH;
+  const L::Areas ar = L::areas(cap, P, fmt);
   rg->cap = cap;
-  rg->a8 = L::area8(cap, P);
-  rg->a128 = L::area128(cap, P);
-  rg->aa = L::areaA(cap, P);
-  rg->as = L::areaS(cap, P);
+  rg->a8 = ar.a8;
+  rg->a128 = ar.a128;
+  rg->aa = ar.aa;
+  rg->as = ar.as;
+  rg->fmt = fmt;
   return LL_OK;
 }
 
@@ -438,10 +478,10 @@ ll_proto auto_proto_rooted(uint64_t bytes, bool sentinel_ok) {
 // each format up to the size where the one-lane-per-unit kernels catch up
 // (measured at 4 and 8 ranks): 8-byte packets and sentinel units up to
 // 2 MiB of data per rank; lines up to 8 MiB at 2-4 ranks, and at 5-8 ranks
-// up to 4 MiB (ReduceScatter) or 2 MiB (AllGather).  ll_set_wave_kernels
+// up to 4 MiB (ReduceScatter) or 2 MiB (AllGather).  ll_tuning.wave_kernels
 // forces either family.
-bool use_wave_kernel(ll_proto proto, uint64_t bytes, int P, bool allgather) {
-  const int m = g_wave_kernels.load();
+bool use_wave_kernel(ll_proto proto, uint64_t bytes, int P, bool allgather, const CallOpts &o) {
+  const int m = o.wave_kernels;
   if (m != 0) return m == 2;
   const uint64_t MiB = 1024 * 1024;
   if (proto == LL_PROTO_LINE128) return bytes <= (P >= 5 ? (allgather ? 2 : 4) : 8) * MiB;
@@ -455,6 +495,86 @@ bool is_wave_algo(ll_algo a) {
 
 // Algorithms whose AllGather stores into the peers' sentinel-filled outputs.
 bool fills_output(ll_algo algo) { return algo == LL_ALGO_TWOSHOT_SENTINEL_OUT || algo == LL_ALGO_TWOSHOT_ATOMIC; }
+
+// The region format an AllReduce algorithm needs.
+unsigned algo_fmt(ll_algo a) {
+  switch (a) {
+    case LL_ALGO_TWOSHOT_LINE: case LL_ALGO_ONESHOT_LINE: case LL_ALGO_ONESHOT_LINE_WAVES:
+    case LL_ALGO_TWOSHOT_LINE_WAVES:
+      return L::kFmtLine;
+    case LL_ALGO_ONESHOT_SENTINEL: case LL_ALGO_TWOSHOT_SENTINEL: case LL_ALGO_TWOSHOT_SENTINEL_OUT:
+    case LL_ALGO_TWOSHOT_SENTINEL_WAVES: case LL_ALGO_ONESHOT_SENTINEL_WAVES:
+      return L::kFmtSent;
+    case LL_ALGO_TWOSHOT_ATOMIC:
+      return L::kFmtAtomic;
+    case LL_ALGO_AUTO:
+      return L::kFmtAll;
+    default:
+      return L::kFmt8;
+  }
+}
+unsigned proto_fmt(ll_proto p) {
+  return p == LL_PROTO_LINE128 ? L::kFmtLine : (p == LL_PROTO_SENTINEL ? L::kFmtSent : L::kFmt8);
+}
+
+// The algorithm of the same shape (one-shot or two-shot, one lane per unit
+// or one wave per peer) in packet format f (kFmt8, kFmtLine or kFmtSent).
+ll_algo in_format(ll_algo a, unsigned f) {
+  int shape;  // 0 one-shot waves, 1 one-shot, 2 two-shot waves, 3 two-shot
+  switch (a) {
+    case LL_ALGO_ONESHOT_WAVES: case LL_ALGO_ONESHOT_LINE_WAVES: case LL_ALGO_ONESHOT_SENTINEL_WAVES: shape = 0; break;
+    case LL_ALGO_ONESHOT: case LL_ALGO_ONESHOT_LINE: case LL_ALGO_ONESHOT_SENTINEL: shape = 1; break;
+    case LL_ALGO_TWOSHOT_WAVES: case LL_ALGO_TWOSHOT_LINE_WAVES: case LL_ALGO_TWOSHOT_SENTINEL_WAVES: shape = 2; break;
+    default: shape = 3; break;
+  }
+  static const ll_algo by[4][3] = {
+      {LL_ALGO_ONESHOT_WAVES, LL_ALGO_ONESHOT_LINE_WAVES, LL_ALGO_ONESHOT_SENTINEL_WAVES},
+      {LL_ALGO_ONESHOT, LL_ALGO_ONESHOT_LINE, LL_ALGO_ONESHOT_SENTINEL},
+      {LL_ALGO_TWOSHOT_WAVES, LL_ALGO_TWOSHOT_LINE_WAVES, LL_ALGO_TWOSHOT_SENTINEL_WAVES},
+      {LL_ALGO_TWOSHOT, LL_ALGO_TWOSHOT_LINE, LL_ALGO_TWOSHOT_SENTINEL}};
+  return by[shape][f == L::kFmt8 ? 0 : (f == L::kFmtLine ? 1 : 2)];
+}
+
+// The formats AUTO may use on a region holding `region_fmt`: the flagged
+// formats the region holds (not lines with LL_OPT_NO_LINES); sentinel units
+// when the options allow them, or when the region holds no flagged format
+// (it was sized for a sentinel algorithm).
+unsigned auto_formats(unsigned region_fmt, const CallOpts &o) {
+  unsigned f = region_fmt & (L::kFmt8 | (o.lines_ok() ? L::kFmtLine : 0u));
+  if ((region_fmt & L::kFmtSent) && (o.sentinel_ok() || f == 0)) f |= L::kFmtSent;
+  return f;
+}
+
+// The first of the formats in `order` that `allowed` holds; 0 if none.
+unsigned first_allowed(const unsigned *order, int n, unsigned allowed) {
+  for (int i = 0; i < n; ++i)
+    if (allowed & order[i]) return order[i];
+  return 0;
+}
+
+// AUTO for an AllReduce of in_bytes per rank: the measured choice among the
+// allowed formats, moved to another allowed format of the same shape when
+// its own is not (8-byte packets first, then lines, then sentinel units; a
+// line choice goes to 8-byte packets first).  LL_ALGO_AUTO if no format is
+// allowed.
+ll_algo auto_choice(uint64_t in_bytes, int P, unsigned allowed) {
+  if (allowed == 0) return LL_ALGO_AUTO;
+  const ll_algo a = auto_algo(in_bytes, P, (allowed & L::kFmtSent) != 0);
+  const unsigned f = algo_fmt(a);
+  if (allowed & f) return a;
+  static const unsigned order[3] = {L::kFmt8, L::kFmtLine, L::kFmtSent};
+  return in_format(a, first_allowed(order, 3, allowed));
+}
+
+// AUTO for the stand-alone and rooted collectives, likewise; LL_PROTO_AUTO
+// if no format is allowed.
+ll_proto proto_choice(ll_proto p, unsigned allowed) {
+  if (allowed == 0) return LL_PROTO_AUTO;
+  if (allowed & proto_fmt(p)) return p;
+  static const unsigned order[3] = {L::kFmt8, L::kFmtLine, L::kFmtSent};
+  const unsigned f = first_allowed(order, 3, allowed);
+  return f == L::kFmt8 ? LL_PROTO_PACKET8 : (f == L::kFmtLine ? LL_PROTO_LINE128 : LL_PROTO_SENTINEL);
+}
 
 // Kernel, packet format, slot size and unit count of an AllReduce of `count`
 // elements per rank whose iterations hold `iter_count` elements.
@@ -492,14 +612,31 @@ void plan_allreduce(Plan *pl, ll_algo algo, uint64_t count, int es, int nranks, 
 // =================================================================== C ABI
 extern "C" {
 
-int ll_slice_bytes(size_t count, ll_dtype dt, int nranks, size_t *min_rank_stride) {
+int ll_options_init(ll_options *opt) {
+  if (opt == nullptr) return LL_ERR_INVALID;
+  memset(opt, 0, sizeof *opt);
+  opt->size = sizeof(ll_options);
+  return LL_OK;
+}
+
+int ll_tuning_init(ll_tuning *t) {
+  if (t == nullptr) return LL_ERR_INVALID;
+  memset(t, 0, sizeof *t);
+  t->size = sizeof(ll_tuning);
+  t->pipeline_lag = -1;
+  t->mute_rank = -1;
+  return LL_OK;
+}
+
+int ll_slice_bytes(size_t count, ll_dtype dt, int nranks, ll_algo algo, size_t *min_rank_stride) {
   if (min_rank_stride == nullptr) return LL_ERR_INVALID;
   if (nranks < 2 || nranks > LL_MAX_RANKS) return LL_ERR_INVALID;
   if (dt != LL_F32 && dt != LL_BF16) return LL_ERR_UNSUPPORTED;
+  if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_TWOSHOT_LINE_WAVES) return LL_ERR_INVALID;
   const uint64_t es = (uint64_t)esize_of(dt);
   if (count > L::kMaxInputBytes / es) return LL_ERR_UNSUPPORTED;
   const uint64_t cap = L::roundup((uint64_t)count * es, L::kAlign);
-  *min_rank_stride = (size_t)L::slice_for(cap, nranks);
+  *min_rank_stride = (size_t)L::stride_for(cap, nranks, algo_fmt(algo));
   return LL_OK;
 }
 
@@ -508,7 +645,7 @@ int ll_input_capacity(size_t rank_stride, int nranks, size_t *capacity_bytes) {
   if (nranks < 2 || nranks > LL_MAX_RANKS) return LL_ERR_INVALID;
   if (rank_stride % LL_ALIGN != 0) return LL_ERR_INVALID;
   const uint64_t cap = L::capacity(rank_stride, nranks);
-  if (L::slice_for(cap, nranks) > rank_stride) return LL_ERR_SCRATCH;
+  if (L::slice_for(cap, nranks, L::formats_of(rank_stride)) > rank_stride) return LL_ERR_SCRATCH;
   *capacity_bytes = (size_t)cap;
   return LL_OK;
 }
@@ -518,13 +655,13 @@ int ll_slice_layout(size_t rank_stride, int nranks, size_t *offsets6) {
   size_t cap = 0;
   const int st = ll_input_capacity(rank_stride, nranks, &cap);
   if (st != LL_OK) return st;
-  const uint64_t a8 = L::area8(cap, nranks), a128 = L::area128(cap, nranks), aa = L::areaA(cap, nranks);
+  const L::Areas ar = L::areas(cap, nranks, L::formats_of(rank_stride));
   offsets6[0] = 0;
   offsets6[1] = cap;
-  offsets6[2] = cap + a8;
-  offsets6[3] = cap + a8 + a128;
-  offsets6[4] = cap + a8 + a128 + aa;
-  offsets6[5] = cap + a8 + a128 + aa + L::areaS(cap, nranks);
+  offsets6[2] = cap + ar.a8;
+  offsets6[3] = cap + ar.a8 + ar.a128;
+  offsets6[4] = cap + ar.a8 + ar.a128 + ar.aa;
+  offsets6[5] = cap + ar.a8 + ar.a128 + ar.aa + ar.as;
   return LL_OK;
 }
 
@@ -576,13 +713,16 @@ int ll_fill_sentinel(void *out, size_t count, ll_dtype dt, int nranks, void *str
   return LL_OK;
 }
 
-int ll_allreduce_algo(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt, ll_op op,
-                      int nranks, uint32_t epoch, void *stream, ll_algo algo) {
+int ll_allreduce_ex(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt, ll_op op, int nranks,
+                    uint32_t epoch, void *stream, ll_algo algo, const ll_options *opt) {
   int st = check_common(sym_base, rank_stride, out, nranks, epoch);
   if (st != LL_OK) return st;
   st = check_dtype_op((int)dt, (int)op);
   if (st != LL_OK) return st;
   if ((int)algo < LL_ALGO_AUTO || (int)algo > LL_ALGO_TWOSHOT_LINE_WAVES) return LL_ERR_INVALID;
+  CallOpts o;
+  st = resolve_opts(opt, &o);
+  if (st != LL_OK) return st;
   const int es = esize_of(dt);
   const uint64_t in_bytes = (uint64_t)count * es;
   if (fills_output(algo) && in_bytes % 16 != 0) return LL_ERR_UNSUPPORTED;
@@ -591,12 +731,17 @@ int ll_allreduce_algo(void *sym_base, size_t rank_stride, void *out, size_t coun
   Region rg;
   st = region_of(rank_stride, nranks, in_bytes, &rg);
   if (st != LL_OK) return st;
+  if (algo == LL_ALGO_AUTO) {
+    algo = auto_choice(in_bytes, nranks, auto_formats(rg.fmt, o));
+    if (algo == LL_ALGO_AUTO) return LL_ERR_SCRATCH;  // no format AUTO may use
+  }
+  if ((rg.fmt & algo_fmt(algo)) == 0) return LL_ERR_SCRATCH;  // the region holds no area for this format
   if (count == 0) return LL_OK;
-  if (algo == LL_ALGO_AUTO) algo = auto_algo(in_bytes, nranks, g_auto_sentinel.load() != 0);
 
   Plan pl;
   pl.dt = (int)dt;
   pl.P = nranks;
+  pl.o = o;
   pl.a = base_args(sym_base, rank_stride, out, epoch);
   pl.a.n = (int64_t)count;
   pl.a.al4 = (in_bytes % 4 == 0) ? 1u : 0u;
@@ -614,16 +759,27 @@ int ll_allreduce_algo(void *sym_base, size_t rank_stride, void *out, size_t coun
   return launch(pl, stream);
 }
 
-int ll_auto_algo(size_t count, ll_dtype dt, int nranks, ll_algo *algo) {
+int ll_allreduce_algo(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt, ll_op op,
+                      int nranks, uint32_t epoch, void *stream, ll_algo algo) {
+  return ll_allreduce_ex(sym_base, rank_stride, out, count, dt, op, nranks, epoch, stream, algo, nullptr);
+}
+
+int ll_auto_algo(size_t count, ll_dtype dt, int nranks, size_t rank_stride, const ll_options *opt, ll_algo *algo) {
   if (algo == nullptr || nranks < 2 || nranks > LL_MAX_RANKS) return LL_ERR_INVALID;
   if ((int)dt != LL_F32 && (int)dt != LL_BF16) return LL_ERR_UNSUPPORTED;
-  *algo = auto_algo((uint64_t)count * esize_of(dt), nranks, g_auto_sentinel.load() != 0);
+  CallOpts o;
+  const int st = resolve_opts(opt, &o);
+  if (st != LL_OK) return st;
+  const unsigned fmt = rank_stride == 0 ? L::kFmtAll : L::formats_of(rank_stride);
+  const ll_algo a = auto_choice((uint64_t)count * esize_of(dt), nranks, auto_formats(fmt, o));
+  if (a == LL_ALGO_AUTO) return LL_ERR_SCRATCH;
+  *algo = a;
   return LL_OK;
 }
 
 int ll_allreduce(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt, ll_op op, int nranks,
                  uint32_t epoch, void *stream) {
-  return ll_allreduce_algo(sym_base, rank_stride, out, count, dt, op, nranks, epoch, stream, LL_ALGO_AUTO);
+  return ll_allreduce_ex(sym_base, rank_stride, out, count, dt, op, nranks, epoch, stream, LL_ALGO_AUTO, nullptr);
 }
 
 // ---------------------------------------------------------------- bounded scratch
@@ -708,8 +864,12 @@ int ll_iteration_span(size_t count, size_t iter_count, uint32_t it, int nranks, 
 // refused and AUTO picks among the flagged ones.
 static int buffered_call(const void *in, void *out, size_t count, ll_dtype dt, ll_op op, int nranks,
                          void *scratch_base, size_t scratch_stride, int layout_P, bool flags_only, uint32_t epoch,
-                         void *stream, ll_algo algo, uint32_t *epochs_used) {
+                         void *stream, ll_algo algo, const ll_options *opt, uint32_t *epochs_used) {
   if (epochs_used != nullptr) *epochs_used = 0;
+  CallOpts o;
+  const int so = resolve_opts(opt, &o);
+  if (so != LL_OK) return so;
+  if (flags_only) o.flags &= ~(uint32_t)LL_OPT_AUTO_SENTINEL;
   if (in == nullptr || out == nullptr || scratch_base == nullptr) return LL_ERR_INVALID;
   if (((uintptr_t)in % 16) != 0 || ((uintptr_t)out % 16) != 0) return LL_ERR_INVALID;
   if (((uintptr_t)scratch_base % LL_ALIGN) != 0) return LL_ERR_INVALID;
@@ -744,7 +904,8 @@ static int buffered_call(const void *in, void *out, size_t count, ll_dtype dt, l
     // only, and the two-shot wave kernels take their place (measured on the
     // paper's scratch study shape, 32 MiB at 8 ranks in 256 KiB .. 32 MiB
     // iterations)
-    algo = auto_algo(iter_count * es, nranks, !flags_only && g_auto_sentinel.load() != 0);
+    // (every scratch region holds all three formats)
+    algo = auto_choice(iter_count * es, nranks, auto_formats(L::kFmt8 | L::kFmtLine | L::kFmtSent, o));
     if (iters > 1 && algo == LL_ALGO_ONESHOT_WAVES) algo = LL_ALGO_TWOSHOT_WAVES;
     if (iters > 1 && algo == LL_ALGO_ONESHOT_SENTINEL_WAVES) algo = LL_ALGO_TWOSHOT_SENTINEL_WAVES;
     if (iters > 1 && algo == LL_ALGO_ONESHOT_LINE_WAVES) algo = LL_ALGO_TWOSHOT_LINE_WAVES;
@@ -755,6 +916,7 @@ static int buffered_call(const void *in, void *out, size_t count, ll_dtype dt, l
   Plan pl;
   pl.dt = (int)dt;
   pl.P = nranks;
+  pl.o = o;
   pl.a = base_args(scratch_base, scratch_stride, out, epoch);
   pl.a.in = (const char *)in;
   pl.a.in_stride = in_bytes;
@@ -775,13 +937,13 @@ static int buffered_call(const void *in, void *out, size_t count, ll_dtype dt, l
 
 int ll_allreduce_buffered(const void *in, void *out, size_t count, ll_dtype dt, ll_op op, int nranks,
                           void *scratch_base, size_t scratch_stride, uint32_t epoch, void *stream, ll_algo algo,
-                          uint32_t *epochs_used) {
+                          const ll_options *opt, uint32_t *epochs_used) {
   if (nranks < 2 || nranks > LL_MAX_RANKS) {
     if (epochs_used != nullptr) *epochs_used = 0;
     return LL_ERR_INVALID;
   }
   return buffered_call(in, out, count, dt, op, nranks, scratch_base, scratch_stride, nranks, false, epoch, stream,
-                       algo, epochs_used);
+                       algo, opt, epochs_used);
 }
 
 // ---------------------------------------------------------------- no allocation
@@ -868,16 +1030,19 @@ int ll_allreduce_static(const void *in, void *out, size_t count, ll_dtype dt, ll
   st = static_scratch_of(iters, stream, &base, &epoch);
   if (st != LL_OK) return st;
   return buffered_call(in, out, count, dt, op, nranks, base, kStaticStride, LL_MAX_RANKS, true, epoch, stream, algo,
-                       epochs_used);
+                       nullptr, epochs_used);
 }
 
-int ll_reduce_scatter_proto(void *sym_base, size_t rank_stride, void *out, size_t recvcount, ll_dtype dt,
-                            ll_op op, int nranks, uint32_t epoch, void *stream, ll_proto proto) {
+int ll_reduce_scatter_ex(void *sym_base, size_t rank_stride, void *out, size_t recvcount, ll_dtype dt, ll_op op,
+                         int nranks, uint32_t epoch, void *stream, ll_proto proto, const ll_options *opt) {
   int st = check_common(sym_base, rank_stride, out, nranks, epoch);
   if (st != LL_OK) return st;
   st = check_dtype_op((int)dt, (int)op);
   if (st != LL_OK) return st;
   if ((int)proto < LL_PROTO_AUTO || (int)proto > LL_PROTO_SENTINEL) return LL_ERR_INVALID;
+  CallOpts o;
+  st = resolve_opts(opt, &o);
+  if (st != LL_OK) return st;
   const int es = esize_of(dt);
   if (recvcount > L::kMaxInputBytes) return LL_ERR_UNSUPPORTED;
   const uint64_t chunk_bytes = (uint64_t)recvcount * es;
@@ -886,12 +1051,17 @@ int ll_reduce_scatter_proto(void *sym_base, size_t rank_stride, void *out, size_
   Region rg;
   st = region_of(rank_stride, nranks, in_bytes, &rg);
   if (st != LL_OK) return st;
+  if (proto == LL_PROTO_AUTO) {
+    proto = proto_choice(auto_proto(in_bytes, nranks, o.sentinel_ok()), auto_formats(rg.fmt, o));
+    if (proto == LL_PROTO_AUTO) return LL_ERR_SCRATCH;
+  }
+  if ((rg.fmt & proto_fmt(proto)) == 0) return LL_ERR_SCRATCH;
   if (recvcount == 0) return LL_OK;
-  if (proto == LL_PROTO_AUTO) proto = auto_proto(in_bytes, nranks, g_auto_sentinel.load() != 0);
   Plan pl;
-  pl.kind = use_wave_kernel(proto, in_bytes, nranks, false) ? K_RS_WAVES : K_RS;
+  pl.kind = use_wave_kernel(proto, in_bytes, nranks, false, o) ? K_RS_WAVES : K_RS;
   pl.dt = (int)dt;
   pl.P = nranks;
+  pl.o = o;
   pl.proto = proto == LL_PROTO_LINE128 ? PR_LINE : (proto == LL_PROTO_SENTINEL ? PR_SENT : PR_LL);
   pl.a = base_args(sym_base, rank_stride, out, epoch);
   pl.a.n = (int64_t)recvcount;
@@ -904,17 +1074,20 @@ int ll_reduce_scatter_proto(void *sym_base, size_t rank_stride, void *out, size_
 
 int ll_reduce_scatter(void *sym_base, size_t rank_stride, void *out, size_t recvcount, ll_dtype dt, ll_op op,
                       int nranks, uint32_t epoch, void *stream) {
-  return ll_reduce_scatter_proto(sym_base, rank_stride, out, recvcount, dt, op, nranks, epoch, stream,
-                                 LL_PROTO_AUTO);
+  return ll_reduce_scatter_ex(sym_base, rank_stride, out, recvcount, dt, op, nranks, epoch, stream, LL_PROTO_AUTO,
+                              nullptr);
 }
 
-int ll_allgather_proto(void *sym_base, size_t rank_stride, void *out, size_t sendcount, ll_dtype dt, int nranks,
-                       uint32_t epoch, void *stream, ll_proto proto) {
+int ll_allgather_ex(void *sym_base, size_t rank_stride, void *out, size_t sendcount, ll_dtype dt, int nranks,
+                    uint32_t epoch, void *stream, ll_proto proto, const ll_options *opt) {
   int st = check_common(sym_base, rank_stride, out, nranks, epoch);
   if (st != LL_OK) return st;
   st = check_dtype_op((int)dt, LL_SUM);
   if (st != LL_OK) return st;
   if ((int)proto < LL_PROTO_AUTO || (int)proto > LL_PROTO_SENTINEL) return LL_ERR_INVALID;
+  CallOpts o;
+  st = resolve_opts(opt, &o);
+  if (st != LL_OK) return st;
   const int es = esize_of(dt);
   if (sendcount > L::kMaxInputBytes) return LL_ERR_UNSUPPORTED;
   const uint64_t in_bytes = (uint64_t)sendcount * es;
@@ -922,12 +1095,17 @@ int ll_allgather_proto(void *sym_base, size_t rank_stride, void *out, size_t sen
   Region rg;
   st = region_of(rank_stride, nranks, in_bytes, &rg);
   if (st != LL_OK) return st;
+  if (proto == LL_PROTO_AUTO) {
+    proto = proto_choice(auto_proto(in_bytes * nranks, nranks, o.sentinel_ok()), auto_formats(rg.fmt, o));
+    if (proto == LL_PROTO_AUTO) return LL_ERR_SCRATCH;
+  }
+  if ((rg.fmt & proto_fmt(proto)) == 0) return LL_ERR_SCRATCH;
   if (sendcount == 0) return LL_OK;
-  if (proto == LL_PROTO_AUTO) proto = auto_proto(in_bytes * nranks, nranks, g_auto_sentinel.load() != 0);
   Plan pl;
-  pl.kind = use_wave_kernel(proto, in_bytes * nranks, nranks, true) ? K_AG_WAVES : K_AG;
+  pl.kind = use_wave_kernel(proto, in_bytes * nranks, nranks, true, o) ? K_AG_WAVES : K_AG;
   pl.dt = (int)dt;
   pl.P = nranks;
+  pl.o = o;
   pl.proto = proto == LL_PROTO_LINE128 ? PR_LINE : (proto == LL_PROTO_SENTINEL ? PR_SENT : PR_LL);
   pl.a = base_args(sym_base, rank_stride, out, epoch);
   pl.a.n = (int64_t)sendcount;
@@ -940,16 +1118,19 @@ int ll_allgather_proto(void *sym_base, size_t rank_stride, void *out, size_t sen
 
 int ll_allgather(void *sym_base, size_t rank_stride, void *out, size_t sendcount, ll_dtype dt, int nranks,
                  uint32_t epoch, void *stream) {
-  return ll_allgather_proto(sym_base, rank_stride, out, sendcount, dt, nranks, epoch, stream, LL_PROTO_AUTO);
+  return ll_allgather_ex(sym_base, rank_stride, out, sendcount, dt, nranks, epoch, stream, LL_PROTO_AUTO, nullptr);
 }
 
 // Broadcast / Reduce: one exchange in the one-shot slots of the chosen format.
 static int rooted_call(Kind kind, void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt, int root,
-                       int nranks, uint32_t epoch, void *stream, ll_proto proto) {
+                       int nranks, uint32_t epoch, void *stream, ll_proto proto, const ll_options *opt) {
   int st = check_common(sym_base, rank_stride, out, nranks, epoch);
   if (st != LL_OK) return st;
   if (root < 0 || root >= nranks) return LL_ERR_INVALID;
   if ((int)proto < LL_PROTO_AUTO || (int)proto > LL_PROTO_SENTINEL) return LL_ERR_INVALID;
+  CallOpts o;
+  st = resolve_opts(opt, &o);
+  if (st != LL_OK) return st;
   const int es = esize_of(dt);
   if (count > L::kMaxInputBytes) return LL_ERR_UNSUPPORTED;
   const uint64_t in_bytes = (uint64_t)count * es;
@@ -958,12 +1139,17 @@ static int rooted_call(Kind kind, void *sym_base, size_t rank_stride, void *out,
   Region rg;
   st = region_of(rank_stride, nranks, in_bytes, &rg);
   if (st != LL_OK) return st;
+  if (proto == LL_PROTO_AUTO) {
+    proto = proto_choice(auto_proto_rooted(in_bytes, o.sentinel_ok()), auto_formats(rg.fmt, o));
+    if (proto == LL_PROTO_AUTO) return LL_ERR_SCRATCH;
+  }
+  if ((rg.fmt & proto_fmt(proto)) == 0) return LL_ERR_SCRATCH;
   if (count == 0) return LL_OK;
-  if (proto == LL_PROTO_AUTO) proto = auto_proto_rooted(in_bytes, g_auto_sentinel.load() != 0);
   Plan pl;
   pl.kind = kind;
   pl.dt = (int)dt;
   pl.P = nranks;
+  pl.o = o;
   pl.proto = proto == LL_PROTO_LINE128 ? PR_LINE : (proto == LL_PROTO_SENTINEL ? PR_SENT : PR_LL);
   pl.a = base_args(sym_base, rank_stride, out, epoch);
   pl.a.n = (int64_t)count;
@@ -976,17 +1162,17 @@ static int rooted_call(Kind kind, void *sym_base, size_t rank_stride, void *out,
 }
 
 int ll_broadcast(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt, int root, int nranks,
-                 uint32_t epoch, void *stream, ll_proto proto) {
+                 uint32_t epoch, void *stream, ll_proto proto, const ll_options *opt) {
   const int st = check_dtype_op((int)dt, LL_SUM);
   if (st != LL_OK) return st;
-  return rooted_call(K_BCAST, sym_base, rank_stride, out, count, dt, root, nranks, epoch, stream, proto);
+  return rooted_call(K_BCAST, sym_base, rank_stride, out, count, dt, root, nranks, epoch, stream, proto, opt);
 }
 
 int ll_reduce(void *sym_base, size_t rank_stride, void *out, size_t count, ll_dtype dt, ll_op op, int root,
-              int nranks, uint32_t epoch, void *stream, ll_proto proto) {
+              int nranks, uint32_t epoch, void *stream, ll_proto proto, const ll_options *opt) {
   const int st = check_dtype_op((int)dt, (int)op);
   if (st != LL_OK) return st;
-  return rooted_call(K_REDUCE, sym_base, rank_stride, out, count, dt, root, nranks, epoch, stream, proto);
+  return rooted_call(K_REDUCE, sym_base, rank_stride, out, count, dt, root, nranks, epoch, stream, proto, opt);
 }
 
 int ll_check(void *stream) {
@@ -1045,7 +1231,8 @@ const char *ll_strerror(int status) {
     case LL_ERR_UNSUPPORTED:
       return "unsupported data type, operation or size";
     case LL_ERR_SCRATCH:
-      return "input larger than the region's input capacity (rank_stride too small)";
+      return "the region cannot serve this call: input larger than its input capacity, or no area for the "
+             "call's packet format (rank_stride too small, or sized for another algorithm)";
     case LL_ERR_HIP:
       snprintf(t_msg, sizeof t_msg, "HIP runtime error: %s", hipGetErrorString((hipError_t)t_last_hip));
       return t_msg;
@@ -1054,73 +1241,6 @@ const char *ll_strerror(int status) {
     default:
       return "unknown status";
   }
-}
-
-int ll_set_launch(int workgroups_per_rank, int threads) {
-  if (workgroups_per_rank < 0 || workgroups_per_rank > 4096) return LL_ERR_INVALID;
-  if (threads != 0 && (threads < 64 || threads > 1024 || threads % 64 != 0)) return LL_ERR_INVALID;
-  g_wg_per_rank.store(workgroups_per_rank);
-  g_threads.store(threads);
-  return LL_OK;
-}
-
-int ll_set_poll_pacing(int first_wait, int poll_gap) {
-  if (first_wait < 0 || first_wait > 1000 || poll_gap < 0 || poll_gap > 1000) return LL_ERR_INVALID;
-  g_first_wait.store(first_wait);
-  g_poll_gap.store(poll_gap);
-  return LL_OK;
-}
-
-int ll_set_pipeline_lag(int lag) {
-  if (lag < 0 || lag > 64) return LL_ERR_INVALID;
-  g_lag.store(lag);
-  return LL_OK;
-}
-
-int ll_set_wave_kernels(int mode) {
-  if (mode < 0 || mode > 2) return LL_ERR_INVALID;
-  g_wave_kernels.store(mode);
-  return LL_OK;
-}
-
-int ll_set_auto_sentinel(int allow) {
-  if (allow != 0 && allow != 1) return LL_ERR_INVALID;
-  g_auto_sentinel.store(allow);
-  return LL_OK;
-}
-
-int ll_set_wave_units(int units_per_lane) {
-  if (units_per_lane != 0 && units_per_lane != 1 && units_per_lane != 2 && units_per_lane != 4) return LL_ERR_INVALID;
-  g_wave_units.store(units_per_lane);
-  return LL_OK;
-}
-
-int ll_set_poll_timeout(uint64_t ticks) {
-  if (ticks == 0) return LL_ERR_INVALID;
-  g_timeout.store(ticks);
-  return LL_OK;
-}
-
-int ll_debug_mute_rank(int rank) {
-  if (rank < -1 || rank >= LL_MAX_RANKS) return LL_ERR_INVALID;
-  g_mute.store(rank);
-  return LL_OK;
-}
-
-int ll_debug_stamp_next(uint64_t *stamps) {
-  g_stamps.store(stamps);
-  return LL_OK;
-}
-
-int ll_debug_phase_next(uint64_t *phases) {
-  g_phases.store(phases);
-  return LL_OK;
-}
-
-int ll_last_grid(int *grid, int *threads) {
-  if (grid) *grid = g_last_grid.load();
-  if (threads) *threads = g_last_threads.load();
-  return LL_OK;
 }
 
 // ------------------------------------------------------------------ probes
@@ -1184,82 +1304,99 @@ int ll_probe_spin(uint64_t ticks, void *stream) {
   return hip_status();
 }
 
-int ll_bench_allreduce(void *sym_base, size_t rank_stride, void *out, size_t count, int dt, int nranks,
-                       uint32_t first_epoch, int calls, int algo, uint64_t *stamps, int stamp_stride,
-                       void *stream) {
+// Per-call options of a benchmark loop: a copy of `opt` (NULL = defaults)
+// whose tuning points at the stamps of call i.
+struct BenchOpts {
+  ll_options o;
+  ll_tuning t;
+  uint64_t *stamps;
+  int stride;
+  BenchOpts(const ll_options *opt, uint64_t *st, int sd) : stamps(st), stride(sd) {
+    ll_options_init(&o);
+    ll_tuning_init(&t);
+    if (opt != nullptr) {
+      o = *opt;
+      if (opt->tuning != nullptr) t = *opt->tuning;
+    }
+    o.tuning = &t;
+  }
+  const ll_options *at(int i) {
+    t.stamps = stamps ? stamps + (size_t)i * (size_t)stride : nullptr;
+    return &o;
+  }
+};
+
+static int bench_args(uint32_t first_epoch, int calls, const uint64_t *stamps, int stamp_stride,
+                      const ll_options *opt) {
   if (calls < 1 || first_epoch == 0 || (uint64_t)first_epoch + (uint64_t)calls - 1 > 0xFFFFFFFFull)
     return LL_ERR_INVALID;
   if (stamps != nullptr && stamp_stride < 1) return LL_ERR_INVALID;
+  if (opt != nullptr && (opt->size != sizeof(ll_options) ||
+                         (opt->tuning != nullptr && opt->tuning->size != sizeof(ll_tuning))))
+    return LL_ERR_INVALID;
+  return LL_OK;
+}
+
+int ll_bench_allreduce(void *sym_base, size_t rank_stride, void *out, size_t count, int dt, int nranks,
+                       uint32_t first_epoch, int calls, int algo, const ll_options *opt, uint64_t *stamps,
+                       int stamp_stride, void *stream) {
+  int st = bench_args(first_epoch, calls, stamps, stamp_stride, opt);
+  if (st != LL_OK) return st;
+  BenchOpts bo(opt, stamps, stamp_stride);
   for (int i = 0; i < calls; ++i) {
     if (fills_output((ll_algo)algo)) {  // its precondition, timed with it
-      const int sf = ll_fill_sentinel(out, count, (ll_dtype)dt, nranks, stream);
-      if (sf != LL_OK) return sf;
+      st = ll_fill_sentinel(out, count, (ll_dtype)dt, nranks, stream);
+      if (st != LL_OK) return st;
     }
-    if (stamps != nullptr) g_stamps.store(stamps + (size_t)i * (size_t)stamp_stride);
-    const int st = ll_allreduce_algo(sym_base, rank_stride, out, count, (ll_dtype)dt, LL_SUM, nranks,
-                                     first_epoch + (uint32_t)i, stream, (ll_algo)algo);
-    if (st != LL_OK) {
-      g_stamps.store(nullptr);
-      return st;
-    }
+    st = ll_allreduce_ex(sym_base, rank_stride, out, count, (ll_dtype)dt, LL_SUM, nranks, first_epoch + (uint32_t)i,
+                         stream, (ll_algo)algo, bo.at(i));
+    if (st != LL_OK) return st;
   }
   return LL_OK;
 }
 
 int ll_bench_rooted(int kind, void *sym_base, size_t rank_stride, void *out, size_t count, int dt, int root,
-                    int nranks, uint32_t first_epoch, int calls, int proto, uint64_t *stamps, int stamp_stride,
-                    void *stream) {
+                    int nranks, uint32_t first_epoch, int calls, int proto, const ll_options *opt,
+                    uint64_t *stamps, int stamp_stride, void *stream) {
   if (kind != 0 && kind != 1) return LL_ERR_INVALID;
-  if (calls < 1 || first_epoch == 0 || (uint64_t)first_epoch + (uint64_t)calls - 1 > 0xFFFFFFFFull)
-    return LL_ERR_INVALID;
-  if (stamps != nullptr && stamp_stride < 1) return LL_ERR_INVALID;
+  int st = bench_args(first_epoch, calls, stamps, stamp_stride, opt);
+  if (st != LL_OK) return st;
+  BenchOpts bo(opt, stamps, stamp_stride);
   for (int i = 0; i < calls; ++i) {
-    if (stamps != nullptr) g_stamps.store(stamps + (size_t)i * (size_t)stamp_stride);
     const uint32_t e = first_epoch + (uint32_t)i;
-    const int st = kind == 0 ? ll_broadcast(sym_base, rank_stride, out, count, (ll_dtype)dt, root, nranks, e, stream,
-                                            (ll_proto)proto)
-                             : ll_reduce(sym_base, rank_stride, out, count, (ll_dtype)dt, LL_SUM, root, nranks, e,
-                                         stream, (ll_proto)proto);
-    if (st != LL_OK) {
-      g_stamps.store(nullptr);
-      return st;
-    }
+    st = kind == 0 ? ll_broadcast(sym_base, rank_stride, out, count, (ll_dtype)dt, root, nranks, e, stream,
+                                  (ll_proto)proto, bo.at(i))
+                   : ll_reduce(sym_base, rank_stride, out, count, (ll_dtype)dt, LL_SUM, root, nranks, e, stream,
+                               (ll_proto)proto, bo.at(i));
+    if (st != LL_OK) return st;
   }
   return LL_OK;
 }
 
 int ll_bench_reduce_scatter(void *sym_base, size_t rank_stride, void *out, size_t recvcount, int dt, int nranks,
-                            uint32_t first_epoch, int calls, int proto, uint64_t *stamps, int stamp_stride,
-                            void *stream) {
-  if (calls < 1 || first_epoch == 0 || (uint64_t)first_epoch + (uint64_t)calls - 1 > 0xFFFFFFFFull)
-    return LL_ERR_INVALID;
-  if (stamps != nullptr && stamp_stride < 1) return LL_ERR_INVALID;
+                            uint32_t first_epoch, int calls, int proto, const ll_options *opt, uint64_t *stamps,
+                            int stamp_stride, void *stream) {
+  int st = bench_args(first_epoch, calls, stamps, stamp_stride, opt);
+  if (st != LL_OK) return st;
+  BenchOpts bo(opt, stamps, stamp_stride);
   for (int i = 0; i < calls; ++i) {
-    if (stamps != nullptr) g_stamps.store(stamps + (size_t)i * (size_t)stamp_stride);
-    const int st = ll_reduce_scatter_proto(sym_base, rank_stride, out, recvcount, (ll_dtype)dt, LL_SUM, nranks,
-                                           first_epoch + (uint32_t)i, stream, (ll_proto)proto);
-    if (st != LL_OK) {
-      g_stamps.store(nullptr);
-      return st;
-    }
+    st = ll_reduce_scatter_ex(sym_base, rank_stride, out, recvcount, (ll_dtype)dt, LL_SUM, nranks,
+                              first_epoch + (uint32_t)i, stream, (ll_proto)proto, bo.at(i));
+    if (st != LL_OK) return st;
   }
   return LL_OK;
 }
 
 int ll_bench_allgather(void *sym_base, size_t rank_stride, void *out, size_t sendcount, int dt, int nranks,
-                       uint32_t first_epoch, int calls, int proto, uint64_t *stamps, int stamp_stride,
-                       void *stream) {
-  if (calls < 1 || first_epoch == 0 || (uint64_t)first_epoch + (uint64_t)calls - 1 > 0xFFFFFFFFull)
-    return LL_ERR_INVALID;
-  if (stamps != nullptr && stamp_stride < 1) return LL_ERR_INVALID;
+                       uint32_t first_epoch, int calls, int proto, const ll_options *opt, uint64_t *stamps,
+                       int stamp_stride, void *stream) {
+  int st = bench_args(first_epoch, calls, stamps, stamp_stride, opt);
+  if (st != LL_OK) return st;
+  BenchOpts bo(opt, stamps, stamp_stride);
   for (int i = 0; i < calls; ++i) {
-    if (stamps != nullptr) g_stamps.store(stamps + (size_t)i * (size_t)stamp_stride);
-    const int st = ll_allgather_proto(sym_base, rank_stride, out, sendcount, (ll_dtype)dt, nranks,
-                                      first_epoch + (uint32_t)i, stream, (ll_proto)proto);
-    if (st != LL_OK) {
-      g_stamps.store(nullptr);
-      return st;
-    }
+    st = ll_allgather_ex(sym_base, rank_stride, out, sendcount, (ll_dtype)dt, nranks, first_epoch + (uint32_t)i,
+                         stream, (ll_proto)proto, bo.at(i));
+    if (st != LL_OK) return st;
   }
   return LL_OK;
 }
@@ -1293,7 +1430,8 @@ int ll_bench_empty(int grid, int threads, int calls, uint64_t *stamps, int stamp
 }
 
 int ll_bench_exchange(void *sym_base, size_t rank_stride, void *out, size_t count, int dt, int nranks,
-                      uint32_t first_epoch, int calls, uint64_t *stamps, int stamp_stride, void *stream) {
+                      uint32_t first_epoch, int calls, uint64_t *stamps, int stamp_stride, int *grid_out,
+                      void *stream) {
   int st = check_common(sym_base, rank_stride, out, nranks, first_epoch);
   if (st != LL_OK) return st;
   st = check_dtype_op(dt, LL_SUM);
@@ -1305,6 +1443,7 @@ int ll_bench_exchange(void *sym_base, size_t rank_stride, void *out, size_t coun
   Region rg;
   st = region_of(rank_stride, nranks, bytes, &rg);
   if (st != LL_OK) return st;
+  if ((rg.fmt & L::kFmt8) == 0) return LL_ERR_SCRATCH;
   static kernel_fn const fns[LL_MAX_RANKS + 1] = {nullptr,
                                                   nullptr,
                                                   k_probe_exchange<2>,
@@ -1329,7 +1468,7 @@ int ll_bench_exchange(void *sym_base, size_t rank_stride, void *out, size_t coun
   a.area = rg.area_of(PR_LL);
   a.slot = slot_bytes(PR_LL, bytes);
   a.units = (int64_t)units;
-  a.timeout = g_timeout.load();
+  a.timeout = kDefaultTimeout;
   a.grid = (uint32_t)grid;
   a.block = (uint32_t)threads;
   st = status_of(stream, &a.status);
@@ -1339,8 +1478,7 @@ int ll_bench_exchange(void *sym_base, size_t rank_stride, void *out, size_t coun
     a.stamps = stamps ? stamps + (size_t)i * (size_t)stamp_stride : nullptr;
     hipLaunchKernelGGL(fn, dim3(grid), dim3(threads), 0, (hipStream_t)stream, a);
   }
-  g_last_grid.store(grid);
-  g_last_threads.store(threads);
+  if (grid_out != nullptr) *grid_out = grid;
   return hip_status();
 }
 

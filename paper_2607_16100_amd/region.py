@@ -31,17 +31,21 @@ class SymRegion:
     """P slices of ``rank_stride`` bytes in one allocation, plus ``out``.
 
     ``max_count`` elements of ``dtype`` ("f32" / "bf16") is the largest
-    per-rank input the region must hold; ``out_elems`` sizes the output
-    buffer (defaults to what an AllGather of max_count needs).
+    per-rank input the region must hold; ``sized_for`` names the algorithm
+    the region is sized for ("auto": every algorithm and packet format);
+    ``out_elems`` sizes the output buffer (defaults to what an AllGather of
+    max_count needs).  ``opt`` (an llcoll.Options or None) is passed to every
+    call that takes options unless the call names its own.
     """
 
     def __init__(self, nranks: int, max_count: int, dtype: str, device="cuda:0", out_elems: int | None = None,
-                 rank_stride: int | None = None):
+                 rank_stride: int | None = None, sized_for: str = "auto", opt=None):
         self.nranks = nranks
         self.dtype = dtype
         self.dt = ll.DTYPES[dtype]
         self.esize = 4 if dtype == "f32" else 2
-        st, need = ll.ll_slice_bytes(max_count, self.dt, nranks)
+        self.opt = opt
+        st, need = ll.ll_slice_bytes(max_count, self.dt, nranks, ll.ALGOS[sized_for])
         ll.check(st, "ll_slice_bytes")
         self.rank_stride = rank_stride if rank_stride is not None else need
         self.device = torch.device(device)
@@ -106,21 +110,26 @@ class SymRegion:
         return self.out[:nbytes].cpu().numpy().view(np_dtype).copy()
 
     # -- collectives (one launch each, on the given stream)
-    def broadcast(self, count: int, root: int, proto: str = "auto", stream=None, epoch: int | None = None) -> int:
+    def _opt(self, opt):
+        return self.opt if opt is None else opt
+
+    def broadcast(self, count: int, root: int, proto: str = "auto", stream=None, epoch: int | None = None,
+                  opt=None) -> int:
         e = self.next_epoch() if epoch is None else epoch
         return ll.ll_broadcast(self.base, self.rank_stride, self.out_ptr, count, self.dt, root, self.nranks, e,
-                               self.stream_handle(stream), ll.PROTOS[proto])
+                               self.stream_handle(stream), ll.PROTOS[proto], self._opt(opt))
 
-    def reduce(self, count: int, root: int, proto: str = "auto", stream=None, epoch: int | None = None) -> int:
+    def reduce(self, count: int, root: int, proto: str = "auto", stream=None, epoch: int | None = None,
+               opt=None) -> int:
         e = self.next_epoch() if epoch is None else epoch
         return ll.ll_reduce(self.base, self.rank_stride, self.out_ptr, count, self.dt, ll.LL_SUM, root, self.nranks,
-                            e, self.stream_handle(stream), ll.PROTOS[proto])
+                            e, self.stream_handle(stream), ll.PROTOS[proto], self._opt(opt))
 
     def fill_out_sentinel(self, count: int, stream=None) -> int:
         """Fill the P outputs of `count` elements with the sentinel."""
         return ll.ll_fill_sentinel(self.out_ptr, count, self.dt, self.nranks, self.stream_handle(stream))
 
-    def allreduce(self, count: int, algo: str = "auto", stream=None, epoch: int | None = None) -> int:
+    def allreduce(self, count: int, algo: str = "auto", stream=None, epoch: int | None = None, opt=None) -> int:
         """One AllReduce.  For "twoshot_sentinel_out" and "twoshot_atomic" the
         outputs are first refilled with the sentinel (their precondition), on
         the same stream."""
@@ -129,18 +138,20 @@ class SymRegion:
             st = self.fill_out_sentinel(count, stream)
             if st != ll.LL_OK:
                 return st
-        return ll.ll_allreduce_algo(self.base, self.rank_stride, self.out_ptr, count, self.dt, ll.LL_SUM,
-                                    self.nranks, e, self.stream_handle(stream), ll.ALGOS[algo])
+        return ll.ll_allreduce_ex(self.base, self.rank_stride, self.out_ptr, count, self.dt, ll.LL_SUM,
+                                  self.nranks, e, self.stream_handle(stream), ll.ALGOS[algo], self._opt(opt))
 
-    def reduce_scatter(self, recvcount: int, proto: str = "auto", stream=None, epoch: int | None = None) -> int:
+    def reduce_scatter(self, recvcount: int, proto: str = "auto", stream=None, epoch: int | None = None,
+                       opt=None) -> int:
         e = self.next_epoch() if epoch is None else epoch
-        return ll.ll_reduce_scatter_proto(self.base, self.rank_stride, self.out_ptr, recvcount, self.dt, ll.LL_SUM,
-                                          self.nranks, e, self.stream_handle(stream), ll.PROTOS[proto])
+        return ll.ll_reduce_scatter_ex(self.base, self.rank_stride, self.out_ptr, recvcount, self.dt, ll.LL_SUM,
+                                       self.nranks, e, self.stream_handle(stream), ll.PROTOS[proto], self._opt(opt))
 
-    def allgather(self, sendcount: int, proto: str = "auto", stream=None, epoch: int | None = None) -> int:
+    def allgather(self, sendcount: int, proto: str = "auto", stream=None, epoch: int | None = None,
+                  opt=None) -> int:
         e = self.next_epoch() if epoch is None else epoch
-        return ll.ll_allgather_proto(self.base, self.rank_stride, self.out_ptr, sendcount, self.dt, self.nranks, e,
-                                     self.stream_handle(stream), ll.PROTOS[proto])
+        return ll.ll_allgather_ex(self.base, self.rank_stride, self.out_ptr, sendcount, self.dt, self.nranks, e,
+                                  self.stream_handle(stream), ll.PROTOS[proto], self._opt(opt))
 
 
 class ScratchRegion:
@@ -150,8 +161,9 @@ class ScratchRegion:
     elements.  ``in_place=True`` makes the output the input buffer."""
 
     def __init__(self, nranks: int, max_count: int, dtype: str, iter_bytes: int, device="cuda:0",
-                 in_place: bool = False):
+                 in_place: bool = False, opt=None):
         self.nranks = nranks
+        self.opt = opt
         self.dtype = dtype
         self.dt = ll.DTYPES[dtype]
         self.esize = 4 if dtype == "f32" else 2
@@ -187,7 +199,7 @@ class ScratchRegion:
         nbytes = nelems_total * np.dtype(np_dtype).itemsize
         return self.out[:nbytes].cpu().numpy().view(np_dtype).copy()
 
-    def allreduce(self, count: int, algo: str = "auto", stream=None) -> int:
+    def allreduce(self, count: int, algo: str = "auto", stream=None, opt=None) -> int:
         """One call; advances the epoch by the iterations it used.  For
         "twoshot_sentinel_out" the outputs are refilled with the sentinel first."""
         s = SymRegion.stream_handle(stream)
@@ -197,7 +209,7 @@ class ScratchRegion:
                 return st
         st, used = ll.ll_allreduce_buffered(self.inp.data_ptr(), self.out.data_ptr(), count, self.dt, ll.LL_SUM,
                                             self.nranks, self.scratch.data_ptr(), self.scratch_stride,
-                                            self.epoch + 1, s, ll.ALGOS[algo])
+                                            self.epoch + 1, s, ll.ALGOS[algo], self.opt if opt is None else opt)
         if st == ll.LL_OK:
             self.epoch += used
         self.last_iters = used

@@ -86,8 +86,8 @@ def test_scratch_error_when_input_exceeds_capacity():
 
 def test_rs_ag_argument_checks():
     stride = stride_for(8 * 64, BF16, 8)
-    rs = ll.ll_reduce_scatter_proto
-    ag = ll.ll_allgather_proto
+    rs = ll.ll_reduce_scatter_ex
+    ag = ll.ll_allgather_ex
     assert rs(GOOD_BASE, stride, GOOD_OUT, 64, BF16, ll.LL_SUM, 8, 0, 0, 0) == ll.LL_ERR_INVALID
     assert rs(GOOD_BASE, stride, GOOD_OUT, 64, BF16, 3, 8, 1, 0, 0) == ll.LL_ERR_UNSUPPORTED
     assert rs(GOOD_BASE, stride, GOOD_OUT, 64, BF16, ll.LL_SUM, 8, 1, 0, 5) == ll.LL_ERR_INVALID
@@ -104,11 +104,6 @@ def test_fill_sentinel_and_auto_sentinel_argument_checks():
     assert ll.ll_fill_sentinel(GOOD_OUT, 16, F32, 9, 0) == ll.LL_ERR_INVALID
     assert ll.ll_fill_sentinel(GOOD_OUT, 16, 4, 4, 0) == ll.LL_ERR_UNSUPPORTED
     assert ll.ll_fill_sentinel(GOOD_OUT, 0, BF16, 4, 0) == ll.LL_OK
-    assert ll.ll_set_wave_kernels(3) == ll.LL_ERR_INVALID
-    assert ll.ll_set_wave_kernels(0) == ll.LL_OK
-    assert ll.ll_set_auto_sentinel(2) == ll.LL_ERR_INVALID
-    assert ll.ll_set_auto_sentinel(1) == ll.LL_OK
-    assert ll.ll_set_auto_sentinel(0) == ll.LL_OK
 
 
 @pytest.mark.parametrize("p", [2, 4, 8])
@@ -131,7 +126,7 @@ def test_buffered_argument_checks():
     IN, OUT = GOOD_BASE, GOOD_OUT
 
     def b(inp=IN, out=OUT, count=4096, dt=F32, op=0, p=4, base=scr, s=stride, epoch=1, algo=0):
-        return ll.ll_allreduce_buffered(inp, out, count, dt, op, p, base, s, epoch, 0, algo)
+        return ll.ll_allreduce_buffered(inp, out, count, dt, op, p, base, s, epoch, 0, algo, None)
 
     assert b(inp=0)[0] == ll.LL_ERR_INVALID
     assert b(out=OUT + 8)[0] == ll.LL_ERR_INVALID
@@ -181,7 +176,7 @@ def test_slice_bytes_gives_enough_capacity(dt, es, p):
     prev = 0
     for count in [1, 2, 3, 7, 64, 1000, 4096, 8192, 7168 * 16, 1 << 20, (64 << 20) // es]:
         st, stride = ll.ll_slice_bytes(count, dt, p)
-        assert st == ll.LL_OK and stride % 256 == 0
+        assert st == ll.LL_OK and stride % 4096 == 0  # every format: no format bits
         assert stride >= prev  # monotone in the input size
         prev = stride
         st, cap = ll.ll_input_capacity(stride, p)
@@ -203,7 +198,7 @@ def test_slice_bytes_argument_checks():
 @pytest.mark.parametrize("p", [2, 5, 8])
 def test_slice_layout_areas_are_ordered_and_fit(p):
     for count in [1, 1000, 7168, 1 << 20]:
-        stride = ll.ll_slice_bytes(count, F32, p)[1] + 512
+        stride = ll.ll_slice_bytes(count, F32, p)[1] + 4096
         st, offs = ll.ll_slice_layout(stride, p)
         assert st == ll.LL_OK
         assert offs[0] == 0 and offs[1] == ll.ll_input_capacity(stride, p)[1]
@@ -223,21 +218,58 @@ def test_capacity_is_a_function_of_stride_and_ranks_only():
     for p in (2, 8):
         s = ll.ll_slice_bytes(5000, F32, p)[1]
         assert ll.ll_input_capacity(s, p) == ll.ll_input_capacity(s, p)
-        assert ll.ll_input_capacity(s + 256, p)[1] >= ll.ll_input_capacity(s, p)[1]
+        assert ll.ll_input_capacity(s + 4096, p)[1] >= ll.ll_input_capacity(s, p)[1]
 
 
-def test_setters():
-    assert ll.ll_set_launch(0, 0) == ll.LL_OK
-    assert ll.ll_set_launch(1, 100) == ll.LL_ERR_INVALID
-    assert ll.ll_set_launch(-1, 64) == ll.LL_ERR_INVALID
-    assert ll.ll_set_poll_timeout(0) == ll.LL_ERR_INVALID
-    assert ll.ll_set_poll_timeout(200_000_000) == ll.LL_OK
-    assert ll.ll_debug_mute_rank(9) == ll.LL_ERR_INVALID
-    assert ll.ll_debug_mute_rank(-1) == ll.LL_OK
-    assert ll.ll_set_pipeline_lag(-1) == ll.LL_ERR_INVALID
-    assert ll.ll_set_pipeline_lag(65) == ll.LL_ERR_INVALID
-    assert ll.ll_set_pipeline_lag(0) == ll.LL_OK
-    assert ll.ll_set_pipeline_lag(1) == ll.LL_OK
+def test_options_are_checked_before_any_hip_call():
+    stride = stride_for(1024, F32, 4)
+
+    def call(opt):
+        return ll.ll_allreduce_ex(GOOD_BASE, stride, GOOD_OUT, 1024, F32, ll.LL_SUM, 4, 1, 0, ll.LL_ALGO_ONESHOT, opt)
+
+    bad = ll.Options()
+    bad.o.size = 8  # not sizeof(ll_options)
+    assert call(bad) == ll.LL_ERR_INVALID
+    assert call(ll.Options(flags=0x80)) == ll.LL_ERR_INVALID  # unknown flag
+    for field, value in [("workgroups_per_rank", -1), ("workgroups_per_rank", 5000), ("threads", 100),
+                         ("threads", 2048), ("wave_units", 3), ("wave_kernels", 3), ("pipeline_lag", -2),
+                         ("pipeline_lag", 65), ("first_wait", 1001), ("poll_gap", -1), ("mute_rank", 8),
+                         ("mute_rank", -2)]:
+        assert call(ll.Options(**{field: value})) == ll.LL_ERR_INVALID, (field, value)
+    t = ll.Options(mute_rank=1)
+    t.t.size = 4
+    assert call(t) == ll.LL_ERR_INVALID
+    # the same checks in the other entry points that take options
+    assert ll.ll_reduce_scatter_ex(GOOD_BASE, stride, GOOD_OUT, 256, F32, ll.LL_SUM, 4, 1, 0, 0, bad) == \
+        ll.LL_ERR_INVALID
+    assert ll.ll_allgather_ex(GOOD_BASE, stride, GOOD_OUT, 256, F32, 4, 1, 0, 0, bad) == ll.LL_ERR_INVALID
+    assert ll.ll_broadcast(GOOD_BASE, stride, GOOD_OUT, 256, F32, 0, 4, 1, 0, 0, bad) == ll.LL_ERR_INVALID
+    assert ll.ll_auto_algo(1024, F32, 4, 0, bad)[0] == ll.LL_ERR_INVALID
+    # well-formed options with nothing to do: no launch, success
+    assert ll.ll_allreduce_ex(GOOD_BASE, stride, GOOD_OUT, 0, F32, ll.LL_SUM, 4, 1, 0, 0,
+                              ll.Options(flags=ll.LL_OPT_NO_LINES, mute_rank=2, threads=128)) == ll.LL_OK
+
+
+def test_no_setting_outlives_a_call():
+    """The product header declares no function that changes what later calls
+    do (the tuning and test hooks are per-call options in lltune.h), and a
+    call's options do not change the choices of calls made without them."""
+    text = open(os.path.join(ROOT, "include", "llcoll.h")).read()
+    assert "ll_set_" not in text and "ll_debug_" not in text
+    lib = ll.library()
+    for name in ("ll_set_launch", "ll_set_auto_sentinel", "ll_set_poll_timeout", "ll_debug_mute_rank",
+                 "ll_debug_stamp_next", "ll_last_grid"):
+        assert not hasattr(lib, name), name
+    A = ll.ALGOS
+    defaults = [ll.ll_auto_algo(n, BF16, p) for p in (2, 4, 8) for n in (4096, 8192, 1 << 19, 1 << 24)]
+    stride = stride_for(1 << 19, BF16, 8)
+    for opt in (ll.Options(flags=ll.LL_OPT_AUTO_SENTINEL), ll.Options(flags=ll.LL_OPT_NO_LINES),
+                ll.Options(flags=3, poll_timeout=5, mute_rank=3, threads=64, workgroups_per_rank=2, wave_units=4,
+                           wave_kernels=1, pipeline_lag=0)):
+        ll.ll_auto_algo(8192, BF16, 8, 0, opt)
+        ll.ll_allreduce_ex(GOOD_BASE, stride, GOOD_OUT, 0, BF16, ll.LL_SUM, 8, 1, 0, 0, opt)  # count 0: no launch
+    assert [ll.ll_auto_algo(n, BF16, p) for p in (2, 4, 8) for n in (4096, 8192, 1 << 19, 1 << 24)] == defaults
+    assert ll.ll_auto_algo(8192, BF16, 8) == (ll.LL_OK, A["oneshot_line_waves"])
 
 
 def test_strerror_covers_every_code():
@@ -283,30 +315,26 @@ def test_auto_algo_choices():
     messages grow."""
     A = ll.ALGOS
     f32, bf16 = ll.LL_F32, ll.LL_BF16
-    assert ll.ll_set_auto_sentinel(0) == ll.LL_OK
     assert ll.ll_auto_algo(4096, bf16, 8) == (ll.LL_OK, A["oneshot_waves"])            # 8 KiB
     assert ll.ll_auto_algo(8192, bf16, 8) == (ll.LL_OK, A["oneshot_line_waves"])       # C2, 16 KiB
     assert ll.ll_auto_algo(64 * 8192, bf16, 8) == (ll.LL_OK, A["twoshot_line_waves"])  # C3, 1 MiB
     assert ll.ll_auto_algo(16 << 20, f32, 8) == (ll.LL_OK, A["twoshot_line"])          # C4, 64 MiB
     assert ll.ll_auto_algo(1024, f32, 4) == (ll.LL_OK, A["oneshot_waves"])             # C1
-    assert ll.ll_set_auto_sentinel(1) == ll.LL_OK
-    try:
-        assert ll.ll_auto_algo(8192, bf16, 8) == (ll.LL_OK, A["oneshot_sentinel_waves"])
-        assert ll.ll_auto_algo(64 * 8192, bf16, 8) == (ll.LL_OK, A["twoshot_sentinel_waves"])
-        assert ll.ll_auto_algo(16 << 20, f32, 8) == (ll.LL_OK, A["twoshot_line"])
-    finally:
-        assert ll.ll_set_auto_sentinel(0) == ll.LL_OK
+    sent = ll.Options(flags=ll.LL_OPT_AUTO_SENTINEL)
+    assert ll.ll_auto_algo(8192, bf16, 8, 0, sent) == (ll.LL_OK, A["oneshot_sentinel_waves"])
+    assert ll.ll_auto_algo(64 * 8192, bf16, 8, 0, sent) == (ll.LL_OK, A["twoshot_sentinel_waves"])
+    assert ll.ll_auto_algo(16 << 20, f32, 8, 0, sent) == (ll.LL_OK, A["twoshot_line"])
     assert ll.ll_auto_algo(1, f32, 1)[0] == ll.LL_ERR_INVALID
     assert ll.ll_auto_algo(1, f32, 9)[0] == ll.LL_ERR_INVALID
     assert ll.ll_auto_algo(1, 7, 8)[0] == ll.LL_ERR_UNSUPPORTED
     names = {v: k for k, v in A.items()}
     for sentinel in (0, 1):
-        assert ll.ll_set_auto_sentinel(sentinel) == ll.LL_OK
+        opt = ll.Options(flags=ll.LL_OPT_AUTO_SENTINEL if sentinel else 0)
         for p in range(2, 9):
             for dt, es in ((f32, 4), (bf16, 2)):
                 seen_twoshot = False
                 for k in range(0, 29):
-                    st, algo = ll.ll_auto_algo((1 << k) // es or 1, dt, p)
+                    st, algo = ll.ll_auto_algo((1 << k) // es or 1, dt, p, 0, opt)
                     assert st == ll.LL_OK
                     name = names[algo]
                     assert name not in ("auto", "twoshot_sentinel_out", "twoshot_atomic")
@@ -316,7 +344,75 @@ def test_auto_algo_choices():
                         seen_twoshot = True
                     else:
                         assert not seen_twoshot, f"P={p} {2**k} bytes: one-shot after two-shot"
-    assert ll.ll_set_auto_sentinel(0) == ll.LL_OK
+
+
+def test_one_algorithm_regions():
+    """ll_slice_bytes with a named algorithm sizes a region for that
+    algorithm's packet format only: a stride with that format's bit, several
+    times smaller than an every-format region at large sizes; calls in other
+    formats are refused before any HIP call, and AUTO chooses inside the
+    region's format."""
+    A = ll.ALGOS
+    fmt_of = {"oneshot": 1, "twoshot": 1, "oneshot_waves": 1, "twoshot_waves": 1, "twoshot_line": 2,
+              "oneshot_line": 2, "oneshot_line_waves": 2, "twoshot_line_waves": 2, "oneshot_sentinel": 4,
+              "twoshot_sentinel": 4, "twoshot_sentinel_out": 4, "twoshot_sentinel_waves": 4,
+              "oneshot_sentinel_waves": 4, "twoshot_atomic": 8}
+    for p in (2, 5, 8):
+        for count, dt, es in ((8192, BF16, 2), (1 << 24, F32, 4), (1000, F32, 4)):
+            full = ll.ll_slice_bytes(count, dt, p)[1]
+            for name, f in fmt_of.items():
+                st, stride = ll.ll_slice_bytes(count, dt, p, A[name])
+                assert st == ll.LL_OK
+                assert (stride // 256) % 16 == f, name          # the format bits
+                assert ll.ll_input_capacity(stride, p)[1] >= count * es
+                assert stride < full
+                if count == 1 << 24 and p == 8:
+                    # 8-byte packets need 15x the input, lines and sentinel units
+                    # 8.5x and 8x, the atomic accumulators ~1.3x; all formats 29.5x
+                    assert stride * (1.9 if f == 1 else 3.3) < full, name
+                st, offs = ll.ll_slice_layout(stride, p)
+                sizes = [offs[i + 1] - offs[i] for i in (1, 2, 3, 4)]  # 8-byte, line, atomic, sentinel areas
+                present = [bool(f & 1), bool(f & 2), bool(f & 8), bool(f & 4)]
+                assert [sz > 0 for sz in sizes] == present, name
+                # a call in the region's format passes the checks (count 0: no launch); others are refused
+                for other, g in fmt_of.items():
+                    want = ll.LL_OK if g == f else ll.LL_ERR_SCRATCH
+                    if other in ("twoshot_sentinel_out", "twoshot_atomic"):
+                        continue  # their extra preconditions are tested elsewhere
+                    got = ll.ll_allreduce_algo(GOOD_BASE, stride, GOOD_OUT, count, dt, ll.LL_SUM, p, 1, 0, A[other]) \
+                        if g != f else ll.ll_allreduce_algo(GOOD_BASE, stride, GOOD_OUT, 0, dt, ll.LL_SUM, p, 1, 0,
+                                                            A[other])
+                    assert got == want, (name, other)
+                if f in (1, 2):
+                    st, auto = ll.ll_auto_algo(count, dt, p, stride)
+                    assert st == ll.LL_OK and fmt_of[[k for k, v in A.items() if v == auto][0]] == f
+    # proto-named calls follow the same rule
+    stride = ll.ll_slice_bytes(7168, BF16, 8, A["twoshot_line"])[1]
+    assert ll.ll_reduce_scatter_ex(GOOD_BASE, stride, GOOD_OUT, 896, BF16, ll.LL_SUM, 8, 1, 0,
+                                   ll.LL_PROTO_PACKET8) == ll.LL_ERR_SCRATCH
+    assert ll.ll_allgather_ex(GOOD_BASE, stride, GOOD_OUT, 896, BF16, 8, 1, 0, ll.LL_PROTO_SENTINEL) == \
+        ll.LL_ERR_SCRATCH
+    assert ll.ll_broadcast(GOOD_BASE, stride, GOOD_OUT, 7168, BF16, 0, 8, 1, 0, ll.LL_PROTO_PACKET8) == \
+        ll.LL_ERR_SCRATCH
+    assert ll.ll_slice_bytes(10, F32, 4, 15)[0] == ll.LL_ERR_INVALID
+
+
+def test_no_lines_option_keeps_auto_off_line_packets():
+    """LL_OPT_NO_LINES: at every size and rank count AUTO takes the
+    8-byte-packet algorithm of the shape it would otherwise run with lines."""
+    A = ll.ALGOS
+    names = {v: k for k, v in A.items()}
+    opt = ll.Options(flags=ll.LL_OPT_NO_LINES)
+    for p in range(2, 9):
+        for k in range(0, 29):
+            n = (1 << k) // 4 or 1
+            _, plain = ll.ll_auto_algo(n, ll.LL_F32, p)
+            st, safe = ll.ll_auto_algo(n, ll.LL_F32, p, 0, opt)
+            assert st == ll.LL_OK and "line" not in names[safe]
+            assert names[safe] == names[plain].replace("_line", ""), (p, 1 << k, names[plain], names[safe])
+    # a lines-only region has nothing AUTO may use with the option
+    stride = ll.ll_slice_bytes(4096, ll.LL_F32, 8, A["twoshot_line"])[1]
+    assert ll.ll_auto_algo(4096, ll.LL_F32, 8, stride, opt)[0] == ll.LL_ERR_SCRATCH
 
 
 @pytest.mark.parametrize("p", [2, 3, 5, 6, 7, 8])

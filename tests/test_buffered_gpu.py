@@ -50,21 +50,15 @@ def assert_bits_equal(got, want, what):
                              f"got {int(got[r, i]):#x} want {int(want[r, i]):#x}")
 
 
-@pytest.fixture(autouse=True)
-def _reset_settings():
-    ll.ll_set_launch(0, 0)
-    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
-    ll.ll_debug_mute_rank(-1)
-    yield
-    ll.ll_set_launch(0, 0)
-    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
-    ll.ll_debug_mute_rank(-1)
+def opts(**kw):
+    kw.setdefault("poll_timeout", TEST_TIMEOUT_TICKS)
+    return ll.Options(**kw)
 
 
-def run(reg, x, algo):
+def run(reg, x, algo, opt=None):
     p, n = x.shape
     reg.write_inputs(x)
-    check_ok(reg.allreduce(n, algo), f"buffered {algo} P={p} n={n}")
+    check_ok(reg.allreduce(n, algo, opt=opt), f"buffered {algo} P={p} n={n}")
     return reg.read_out(p * n, x.dtype).reshape(p, n)
 
 
@@ -157,9 +151,9 @@ def test_many_iterations_small_grids(algo):
     x = wl.normal(p, n, "f32", seed=77)
     want = oracle.allreduce(x)
     for wg, threads in [(1, 64), (2, 256), (0, 0)]:
-        ll.ll_set_launch(wg, threads)
         say(f"64 iterations {algo} wg={wg} t={threads}")
-        assert_bits_equal(run(reg, x, algo), want, f"{algo} wg={wg} t={threads}")
+        assert_bits_equal(run(reg, x, algo, opts(workgroups_per_rank=wg, threads=threads)), want,
+                          f"{algo} wg={wg} t={threads}")
         assert reg.last_iters == 64
 
 
@@ -173,7 +167,7 @@ def test_epochs_advance_by_iterations():
     # a call that would run past epoch 0xFFFFFFFF is refused before launching
     st, _ = ll.ll_allreduce_buffered(reg.inp.data_ptr(), reg.out.data_ptr(), n, ll.LL_F32, ll.LL_SUM, p,
                                      reg.scratch.data_ptr(), reg.scratch_stride, 0xFFFFFFFF, stream(),
-                                     ll.LL_ALGO_TWOSHOT)
+                                     ll.LL_ALGO_TWOSHOT, None)
     assert st == ll.LL_ERR_INVALID
 
 
@@ -199,11 +193,7 @@ def test_missing_peer_times_out_and_scratch_init_recovers(algo):
     reg.init()
     x = wl.uniform(p, n, "f32", seed=2)
     reg.write_inputs(x)
-    ll.ll_set_poll_timeout(200_000)
-    ll.ll_debug_mute_rank(6)
-    assert reg.allreduce(n, algo) == ll.LL_OK
+    assert reg.allreduce(n, algo, opt=opts(poll_timeout=200_000, mute_rank=6)) == ll.LL_OK
     assert ll.ll_check(stream()) == ll.LL_ERR_TIMEOUT
-    ll.ll_debug_mute_rank(-1)
-    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
     reg.init()
     assert_bits_equal(run(reg, x, algo), oracle.allreduce(x), f"{algo} after timeout")

@@ -122,15 +122,6 @@ def check_ok(st, what, s=None):
     assert st2 == ll.LL_OK, f"{what}: ll_check says {ll.ll_strerror(st2)}"
 
 
-@pytest.fixture(autouse=True)
-def _reset_settings():
-    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
-    ll.ll_debug_mute_rank(-1)
-    yield
-    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
-    ll.ll_debug_mute_rank(-1)
-
-
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("p", [3, 6, 7, 8])
 def test_edge_values_every_allreduce_algorithm(dtype, p):
@@ -208,8 +199,10 @@ def test_exchange_probe_moves_the_inputs(p, n):
     reg.write_inputs(x)
     s = reg.stream_handle()
     say(f"exchange probe P={p} n={n}")
-    st = ll.ll_bench_exchange(reg.base, reg.rank_stride, reg.out_ptr, n, ll.LL_BF16, p, reg.epoch + 1, 20, 0, 0, s)
+    st, grid = ll.ll_bench_exchange(reg.base, reg.rank_stride, reg.out_ptr, n, ll.LL_BF16, p, reg.epoch + 1, 20, 0,
+                                    0, s)
     assert st == ll.LL_OK, ll.ll_strerror(st)
+    assert grid == p * -(-n * 2 // 512)  # one tile of 64 8-byte units per workgroup
     reg.epoch += 20
     assert ll.ll_check(s) == ll.LL_OK
     got = reg.read_out(p * n, np.uint16).reshape(p, n)
@@ -236,12 +229,9 @@ def test_timeouts_are_reported_on_their_own_stream_only():
             reg.write_inputs(x)
     torch.cuda.synchronize()
     for order in ("b_first", "a_first"):
-        ll.ll_set_poll_timeout(200_000)  # 2 ms
-        ll.ll_debug_mute_rank(5)
         say(f"muted call on stream A ({order})")
-        assert ra.allreduce(n, "oneshot_waves", stream=sa) == ll.LL_OK
-        ll.ll_debug_mute_rank(-1)
-        ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
+        muted = ll.Options(poll_timeout=200_000, mute_rank=5)  # 2 ms waits
+        assert ra.allreduce(n, "oneshot_waves", stream=sa, opt=muted) == ll.LL_OK
         assert rb.allreduce(n, "oneshot_waves", stream=sb) == ll.LL_OK
         if order == "b_first":
             assert ll.ll_check(sb.cuda_stream) == ll.LL_OK

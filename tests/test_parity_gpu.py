@@ -47,10 +47,10 @@ def check_ok(st, what):
     assert st2 == ll.LL_OK, f"{what}: ll_check says {ll.ll_strerror(st2)}"
 
 
-def run_allreduce(reg: SymRegion, x: np.ndarray, algo: str) -> np.ndarray:
+def run_allreduce(reg: SymRegion, x: np.ndarray, algo: str, opt=None) -> np.ndarray:
     p, n = x.shape
     reg.write_inputs(x)
-    check_ok(reg.allreduce(n, algo), f"allreduce {algo} P={p} n={n}")
+    check_ok(reg.allreduce(n, algo, opt=opt), f"allreduce {algo} P={p} n={n}")
     return reg.read_out(p * n, x.dtype).reshape(p, n)
 
 
@@ -65,18 +65,13 @@ def assert_bits_equal(got, want, what):
 TEST_TIMEOUT_TICKS = 20_000_000  # 200 ms per flag wait: thousands of times a correct call's duration
 
 
-@pytest.fixture(autouse=True)
-def _reset_settings():
-    ll.ll_set_wave_units(0)
-    ll.ll_set_wave_kernels(0)
-    ll.ll_set_launch(0, 0)
-    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
-    ll.ll_debug_mute_rank(-1)
-    yield
-    ll.ll_set_wave_kernels(0)
-    ll.ll_set_launch(0, 0)
-    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
-    ll.ll_debug_mute_rank(-1)
+def opts(**kw):
+    """Per-call options: the tests' short wait bound plus any tuning fields."""
+    kw.setdefault("poll_timeout", TEST_TIMEOUT_TICKS)
+    return ll.Options(**kw)
+
+
+MUTED_TIMEOUT_TICKS = 200_000  # 2 ms: waits for a muted rank expire quickly
 
 
 # ------------------------------------------------------------ configuration C1
@@ -171,16 +166,18 @@ def test_benchmark_launch_loop_is_exact(algo):
     s = reg.stream_handle()
     code = ll.ALGOS[algo]
     say(f"bench loop {algo}: 1990 calls")
+    shape = ll.Options(report=True)
     st = ll.ll_bench_allreduce(reg.base, reg.rank_stride, reg.out_ptr, n, ll.LL_BF16, p, reg.epoch + 1, 1990, code,
-                               0, 0, s)
+                               shape, 0, 0, s)
     assert st == ll.LL_OK, ll.ll_strerror(st)
     reg.epoch += 1990
     assert ll.ll_check(s) == ll.LL_OK
-    grid, _ = ll.ll_last_grid()
+    grid = shape.grid
+    assert grid > 0
     stamps = torch.zeros(10 * 2 * grid, dtype=torch.int64, device="cuda")
     say(f"bench loop {algo}: 10 stamped calls, grid {grid}")
     st = ll.ll_bench_allreduce(reg.base, reg.rank_stride, reg.out_ptr, n, ll.LL_BF16, p, reg.epoch + 1, 10, code,
-                               stamps.data_ptr(), 2 * grid, s)
+                               None, stamps.data_ptr(), 2 * grid, s)
     assert st == ll.LL_OK, ll.ll_strerror(st)
     reg.epoch += 10
     assert ll.ll_check(s) == ll.LL_OK
@@ -203,7 +200,7 @@ def test_benchmark_rs_ag_loops_are_exact(proto):
     reg.write_inputs(x)
     say(f"bench RS loop {proto}")
     st = ll.ll_bench_reduce_scatter(reg.base, reg.rank_stride, reg.out_ptr, m, ll.LL_BF16, p, reg.epoch + 1, 500,
-                                    ll.PROTOS[proto], 0, 0, s)
+                                    ll.PROTOS[proto], None, 0, 0, s)
     assert st == ll.LL_OK, ll.ll_strerror(st)
     reg.epoch += 500
     assert ll.ll_check(s) == ll.LL_OK
@@ -212,7 +209,7 @@ def test_benchmark_rs_ag_loops_are_exact(proto):
     reg.write_inputs(rs)
     say(f"bench AG loop {proto}")
     st = ll.ll_bench_allgather(reg.base, reg.rank_stride, reg.out_ptr, m, ll.LL_BF16, p, reg.epoch + 1, 500,
-                               ll.PROTOS[proto], 0, 0, s)
+                               ll.PROTOS[proto], None, 0, 0, s)
     assert st == ll.LL_OK, ll.ll_strerror(st)
     reg.epoch += 500
     assert ll.ll_check(s) == ll.LL_OK
@@ -338,7 +335,7 @@ def test_c5_reduce_scatter_and_allgather(p, b, kind):
     reg = SymRegion(p, total, "bf16", out_elems=p * total)
     reg.init()
     for proto, wk in [(pr, w) for pr in PROTOS for w in (1, 2)] + [("auto", 0)]:
-        ll.ll_set_wave_kernels(wk)
+        reg.opt = opts(wave_kernels=wk)
         say(f"C5 RS {kind} P={p} b={b} {proto} kernels={wk}")
         reg.write_inputs(x)
         check_ok(reg.reduce_scatter(m, proto), "reduce_scatter")
@@ -350,7 +347,6 @@ def test_c5_reduce_scatter_and_allgather(p, b, kind):
         got_ag = reg.read_out(p * p * m, np.uint16).reshape(p, p * m)
         assert_bits_equal(got_ag, oracle.allgather(got_rs), f"AG {proto} kernels={wk}")
         assert_bits_equal(got_ag, oracle.allreduce(x), f"AG(RS) == AR {proto} kernels={wk}")
-    ll.ll_set_wave_kernels(0)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -363,19 +359,16 @@ def test_rs_ag_ragged(dtype, proto, p, m):
     x = wl.uniform(p, p * m, dtype, seed=7)
     reg = SymRegion(p, p * m, dtype, out_elems=p * p * m)
     reg.init()
-    try:
-        for wk in (1, 2):
-            ll.ll_set_wave_kernels(wk)
-            reg.write_inputs(x)
-            check_ok(reg.reduce_scatter(m, proto), "rs")
-            rs = reg.read_out(p * m, NP[dtype]).reshape(p, m)
-            assert_bits_equal(rs, oracle.reduce_scatter(x), f"RS ragged {proto} kernels={wk}")
-            reg.write_inputs(x[:, :m].copy())
-            check_ok(reg.allgather(m, proto), "ag")
-            ag = reg.read_out(p * p * m, NP[dtype]).reshape(p, p * m)
-            assert_bits_equal(ag, oracle.allgather(x[:, :m].copy()), f"AG ragged {proto} kernels={wk}")
-    finally:
-        ll.ll_set_wave_kernels(0)
+    for wk in (1, 2):
+        reg.opt = opts(wave_kernels=wk)
+        reg.write_inputs(x)
+        check_ok(reg.reduce_scatter(m, proto), "rs")
+        rs = reg.read_out(p * m, NP[dtype]).reshape(p, m)
+        assert_bits_equal(rs, oracle.reduce_scatter(x), f"RS ragged {proto} kernels={wk}")
+        reg.write_inputs(x[:, :m].copy())
+        check_ok(reg.allgather(m, proto), "ag")
+        ag = reg.read_out(p * p * m, NP[dtype]).reshape(p, p * m)
+        assert_bits_equal(ag, oracle.allgather(x[:, :m].copy()), f"AG ragged {proto} kernels={wk}")
 
 
 # ------------------------------------------------------------ invariants
@@ -387,15 +380,15 @@ def test_result_independent_of_launch_shape(algo):
     reg = SymRegion(p, n, "bf16")
     reg.init()
     for wg, threads in [(1, 64), (1, 1024), (3, 256), (16, 128), (0, 0)]:
-        ll.ll_set_launch(wg, threads)
         if algo == "twoshot_sentinel":  # the direct-output variant shares the launch shapes
             say(f"launch twoshot_sentinel_out wg={wg} threads={threads}")
-            assert_bits_equal(run_allreduce(reg, x, "twoshot_sentinel_out"), want, f"direct wg={wg} t={threads}")
+            assert_bits_equal(run_allreduce(reg, x, "twoshot_sentinel_out",
+                                            opts(workgroups_per_rank=wg, threads=threads)),
+                              want, f"direct wg={wg} t={threads}")
         for units in ([1, 2, 4, 0] if algo.endswith("_waves") else [0]):
-            ll.ll_set_wave_units(units)
             say(f"launch {algo} wg={wg} threads={threads} units={units}")
-            assert_bits_equal(run_allreduce(reg, x, algo), want, f"{algo} wg={wg} t={threads} u={units}")
-    ll.ll_set_wave_units(0)
+            o = opts(workgroups_per_rank=wg, threads=threads, wave_units=units)
+            assert_bits_equal(run_allreduce(reg, x, algo, o), want, f"{algo} wg={wg} t={threads} u={units}")
 
 
 WAVE_ALGOS = ["oneshot_waves", "oneshot_sentinel_waves", "oneshot_line_waves", "twoshot_waves",
@@ -415,11 +408,7 @@ def test_workgroups_past_the_last_tile(algo, n):
     reg.init()
     guard = np.uint8(0xA5)
     reg.out.fill_(int(guard))
-    ll.ll_set_launch(16, 0)
-    try:
-        got = run_allreduce(reg, x, algo)
-    finally:
-        ll.ll_set_launch(0, 0)
+    got = run_allreduce(reg, x, algo, opts(workgroups_per_rank=16))
     assert_bits_equal(got, oracle.allreduce(x), f"{algo} n={n} W=16")
     tail = reg.out[p * n * 2:].cpu().numpy()
     assert (tail == guard).all(), f"{algo}: {int((tail != guard).sum())} bytes written past the output"
@@ -433,22 +422,17 @@ def test_rs_ag_workgroups_past_the_last_tile(proto):
     reg = SymRegion(p, p * m, "bf16", out_elems=p * p * m + 4096)
     reg.init()
     guard = np.uint8(0x5A)
-    ll.ll_set_wave_kernels(2)
-    ll.ll_set_launch(16, 0)
-    try:
-        reg.out.fill_(int(guard))
-        reg.write_inputs(x)
-        check_ok(reg.reduce_scatter(m, proto), "rs")
-        rs = reg.read_out(p * m, np.uint16).reshape(p, m)
-        assert (reg.out[p * m * 2:].cpu().numpy() == guard).all(), "RS wrote past its output"
-        reg.out.fill_(int(guard))
-        reg.write_inputs(rs)
-        check_ok(reg.allgather(m, proto), "ag")
-        ag = reg.read_out(p * p * m, np.uint16).reshape(p, p * m)
-        assert (reg.out[p * p * m * 2:].cpu().numpy() == guard).all(), "AG wrote past its output"
-    finally:
-        ll.ll_set_launch(0, 0)
-        ll.ll_set_wave_kernels(0)
+    reg.opt = opts(wave_kernels=2, workgroups_per_rank=16)
+    reg.out.fill_(int(guard))
+    reg.write_inputs(x)
+    check_ok(reg.reduce_scatter(m, proto), "rs")
+    rs = reg.read_out(p * m, np.uint16).reshape(p, m)
+    assert (reg.out[p * m * 2:].cpu().numpy() == guard).all(), "RS wrote past its output"
+    reg.out.fill_(int(guard))
+    reg.write_inputs(rs)
+    check_ok(reg.allgather(m, proto), "ag")
+    ag = reg.read_out(p * p * m, np.uint16).reshape(p, p * m)
+    assert (reg.out[p * p * m * 2:].cpu().numpy() == guard).all(), "AG wrote past its output"
     assert_bits_equal(rs, oracle.reduce_scatter(x), f"RS {proto} W=16")
     assert_bits_equal(ag, oracle.allgather(rs), f"AG {proto} W=16")
 
@@ -462,26 +446,21 @@ def test_result_independent_of_pipeline_lag(lag):
     want = oracle.allreduce(x)
     reg = SymRegion(p, n, "bf16", out_elems=p * n)
     reg.init()
-    ll.ll_set_pipeline_lag(lag)
-    try:
-        for wg, threads in [(1, 64), (4, 256), (0, 0)]:
-            ll.ll_set_launch(wg, threads)
-            for algo in ("twoshot", "twoshot_line", "twoshot_sentinel", "twoshot_sentinel_out"):
-                say(f"lag={lag} {algo} wg={wg} t={threads}")
-                assert_bits_equal(run_allreduce(reg, x, algo), want, f"{algo} lag={lag} wg={wg}")
-            m = n // p
-            for proto in PROTOS:
-                reg.write_inputs(x)
-                check_ok(reg.reduce_scatter(m, proto), "rs")
-                rs = reg.read_out(p * m, np.uint16).reshape(p, m)
-                assert_bits_equal(rs, oracle.reduce_scatter(x), f"RS {proto} lag={lag}")
-                reg.write_inputs(rs)
-                check_ok(reg.allgather(m, proto), "ag")
-                ag = reg.read_out(p * p * m, np.uint16).reshape(p, p * m)
-                assert_bits_equal(ag, oracle.allgather(rs), f"AG {proto} lag={lag}")
-    finally:
-        ll.ll_set_pipeline_lag(1)
-        ll.ll_set_launch(0, 0)
+    for wg, threads in [(1, 64), (4, 256), (0, 0)]:
+        reg.opt = opts(pipeline_lag=lag, workgroups_per_rank=wg, threads=threads)
+        for algo in ("twoshot", "twoshot_line", "twoshot_sentinel", "twoshot_sentinel_out"):
+            say(f"lag={lag} {algo} wg={wg} t={threads}")
+            assert_bits_equal(run_allreduce(reg, x, algo), want, f"{algo} lag={lag} wg={wg}")
+        m = n // p
+        for proto in PROTOS:
+            reg.write_inputs(x)
+            check_ok(reg.reduce_scatter(m, proto), "rs")
+            rs = reg.read_out(p * m, np.uint16).reshape(p, m)
+            assert_bits_equal(rs, oracle.reduce_scatter(x), f"RS {proto} lag={lag}")
+            reg.write_inputs(rs)
+            check_ok(reg.allgather(m, proto), "ag")
+            ag = reg.read_out(p * p * m, np.uint16).reshape(p, p * m)
+            assert_bits_equal(ag, oracle.allgather(rs), f"AG {proto} lag={lag}")
 
 
 def test_large_epochs_and_reinit():
@@ -526,9 +505,7 @@ def test_missing_peer_times_out_and_is_reported(algo):
     reg = SymRegion(p, n, "f32")
     reg.init()
     reg.write_inputs(x)
-    ll.ll_set_poll_timeout(200_000)  # 2 ms
-    ll.ll_debug_mute_rank(3)
-    st = reg.allreduce(n, algo)
+    st = reg.allreduce(n, algo, opt=opts(poll_timeout=MUTED_TIMEOUT_TICKS, mute_rank=3))
     assert st == ll.LL_OK
     assert ll.ll_check(stream()) == ll.LL_ERR_TIMEOUT
     rank, missing, epoch = ll.ll_last_timeout()
@@ -536,8 +513,6 @@ def test_missing_peer_times_out_and_is_reported(algo):
     if algo.startswith("oneshot"):
         # only rank 3's packets are missing; the first rank to give up names it
         assert rank != 3 and missing == (1 << 3)
-    ll.ll_debug_mute_rank(-1)
-    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
     reg.init()
     check_ok(reg.allreduce(n, algo), "after timeout")
     assert_bits_equal(reg.read_out(p * n, np.uint32).reshape(p, n), oracle.allreduce(x), "after timeout")
@@ -605,15 +580,13 @@ def test_data_equal_to_sentinel_times_out_and_reinit_recovers(algo, dtype):
     reg = SymRegion(p, n, dtype)
     reg.init()
     reg.write_inputs(bad)
-    ll.ll_set_poll_timeout(200_000)  # 2 ms
     say(f"sentinel-valued data {algo} {dtype}")
-    assert reg.allreduce(n, algo) == ll.LL_OK
+    assert reg.allreduce(n, algo, opt=opts(poll_timeout=MUTED_TIMEOUT_TICKS)) == ll.LL_OK
     assert ll.ll_check(stream()) == ll.LL_ERR_TIMEOUT
     rank, missing, _ = ll.ll_last_timeout()
     assert missing != 0
     if algo == "oneshot_sentinel":
         assert rank != 2 and missing == (1 << 2)
-    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
     # the flagged one-shot handles the same words (NaN propagates through the sum)
     reg.init()
     check_ok(reg.allreduce(n, "oneshot"), "flagged on sentinel-valued data")
@@ -688,12 +661,8 @@ def test_direct_output_missing_peer_times_out():
     reg = SymRegion(p, n, "f32")
     reg.init()
     reg.write_inputs(x)
-    ll.ll_set_poll_timeout(200_000)
-    ll.ll_debug_mute_rank(5)
-    assert reg.allreduce(n, "twoshot_sentinel_out") == ll.LL_OK
+    assert reg.allreduce(n, "twoshot_sentinel_out", opt=opts(poll_timeout=MUTED_TIMEOUT_TICKS, mute_rank=5)) == ll.LL_OK
     assert ll.ll_check(stream()) == ll.LL_ERR_TIMEOUT
-    ll.ll_debug_mute_rank(-1)
-    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
     reg.init()
     check_ok(reg.allreduce(n, "twoshot_sentinel_out"), "after timeout")
     assert_bits_equal(reg.read_out(p * n, np.uint32).reshape(p, n), oracle.allreduce(x), "after timeout")
@@ -702,23 +671,19 @@ def test_direct_output_missing_peer_times_out():
 @pytest.mark.parametrize("p", [2, 4, 6, 7, 8])
 def test_auto_with_sentinel_allowed(p):
     """With sentinel mode allowed, AUTO gives the same bits at every size."""
-    ll.ll_set_auto_sentinel(1)
-    try:
-        for n in [7, 4096, 20_000, 300_000, 3_000_001]:
-            x = wl.normal(p, n, "bf16", seed=n)
-            reg = SymRegion(p, n, "bf16")
-            reg.init()
-            say(f"auto+sentinel P={p} n={n}")
-            assert_bits_equal(run_allreduce(reg, x, "auto"), oracle.allreduce(x), f"auto+sentinel P={p} n={n}")
-            m = n // p
-            if m:
-                reg.write_inputs(x)
-                check_ok(reg.reduce_scatter(m, "auto"), "rs auto")
-                rs = reg.read_out(p * m, np.uint16).reshape(p, m)
-                assert_bits_equal(rs, oracle.reduce_scatter(x[:, :p * m].copy()), f"RS auto+sentinel P={p} m={m}")
-            del reg
-    finally:
-        ll.ll_set_auto_sentinel(0)
+    for n in [7, 4096, 20_000, 300_000, 3_000_001]:
+        x = wl.normal(p, n, "bf16", seed=n)
+        reg = SymRegion(p, n, "bf16", opt=opts(flags=ll.LL_OPT_AUTO_SENTINEL))
+        reg.init()
+        say(f"auto+sentinel P={p} n={n}")
+        assert_bits_equal(run_allreduce(reg, x, "auto"), oracle.allreduce(x), f"auto+sentinel P={p} n={n}")
+        m = n // p
+        if m:
+            reg.write_inputs(x)
+            check_ok(reg.reduce_scatter(m, "auto"), "rs auto")
+            rs = reg.read_out(p * m, np.uint16).reshape(p, m)
+            assert_bits_equal(rs, oracle.reduce_scatter(x[:, :p * m].copy()), f"RS auto+sentinel P={p} m={m}")
+        del reg
 
 
 # ------------------------------------------------ atomic-accumulation two-shot
@@ -757,10 +722,10 @@ def test_atomic_twoshot_launch_shapes():
     reg = SymRegion(p, n, "f32")
     reg.init()
     for wg, threads in [(1, 64), (3, 256), (16, 128), (0, 0)]:
-        ll.ll_set_launch(wg, threads)
         say(f"atomic launch wg={wg} threads={threads}")
-        assert_within_summation_bound(run_allreduce(reg, x, "twoshot_atomic"), x, "f32", f"atomic wg={wg}")
-    ll.ll_set_launch(0, 0)
+        assert_within_summation_bound(run_allreduce(reg, x, "twoshot_atomic", opts(workgroups_per_rank=wg,
+                                                                                   threads=threads)),
+                                      x, "f32", f"atomic wg={wg}")
 
 
 def test_atomic_twoshot_missing_peer_times_out():
@@ -769,12 +734,8 @@ def test_atomic_twoshot_missing_peer_times_out():
     reg = SymRegion(p, n, "f32")
     reg.init()
     reg.write_inputs(x)
-    ll.ll_set_poll_timeout(200_000)
-    ll.ll_debug_mute_rank(2)
-    assert reg.allreduce(n, "twoshot_atomic") == ll.LL_OK
+    assert reg.allreduce(n, "twoshot_atomic", opt=opts(poll_timeout=MUTED_TIMEOUT_TICKS, mute_rank=2)) == ll.LL_OK
     assert ll.ll_check(stream()) == ll.LL_ERR_TIMEOUT
-    ll.ll_debug_mute_rank(-1)
-    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
     reg.init()
     assert_within_summation_bound(run_allreduce(reg, x, "twoshot_atomic"), x, "f32", "after timeout")
 
@@ -821,15 +782,12 @@ def test_rooted_missing_rank_times_out(kind):
     reg = SymRegion(p, n, "f32")
     reg.init()
     reg.write_inputs(x)
-    ll.ll_set_poll_timeout(200_000)
-    ll.ll_debug_mute_rank(2 if kind == "broadcast" else 6)  # the root, or a contributor
-    st = reg.broadcast(n, 2, "packet8") if kind == "broadcast" else reg.reduce(n, 2, "packet8")
+    mute = opts(poll_timeout=MUTED_TIMEOUT_TICKS, mute_rank=2 if kind == "broadcast" else 6)  # root, or contributor
+    st = reg.broadcast(n, 2, "packet8", opt=mute) if kind == "broadcast" else reg.reduce(n, 2, "packet8", opt=mute)
     assert st == ll.LL_OK
     assert ll.ll_check(stream()) == ll.LL_ERR_TIMEOUT
     rank, missing, _ = ll.ll_last_timeout()
     assert missing == (1 << (2 if kind == "broadcast" else 6))
-    ll.ll_debug_mute_rank(-1)
-    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
     reg.init()
     check_ok(reg.reduce(n, 2, "packet8"), "after timeout")
     assert_bits_equal(reg.read_out(n, np.uint32).reshape(1, n), oracle.reduce(x, 2).reshape(1, n), "after timeout")
@@ -843,11 +801,9 @@ def test_rs_ag_wave_kernels_launch_shapes_and_timeouts(proto):
     x = wl.normal(p, p * m, "bf16", seed=17)
     reg = SymRegion(p, p * m, "bf16", out_elems=p * p * m)
     reg.init()
-    ll.ll_set_wave_kernels(2)
     for wg in (1, 3, 0):
         for units in (1, 2, 4, 0):
-            ll.ll_set_launch(wg, 0)
-            ll.ll_set_wave_units(units)
+            reg.opt = opts(wave_kernels=2, workgroups_per_rank=wg, wave_units=units)
             say(f"RS/AG waves {proto} wg={wg} units={units}")
             reg.write_inputs(x)
             check_ok(reg.reduce_scatter(m, proto), "rs")
@@ -857,17 +813,13 @@ def test_rs_ag_wave_kernels_launch_shapes_and_timeouts(proto):
             check_ok(reg.allgather(m, proto), "ag")
             assert_bits_equal(reg.read_out(p * p * m, np.uint16).reshape(p, p * m), oracle.allgather(rs),
                               f"AG waves wg={wg} u={units}")
-    ll.ll_set_launch(0, 0)
-    ll.ll_set_wave_units(0)
-    ll.ll_set_poll_timeout(200_000)
-    ll.ll_debug_mute_rank(4)
+    reg.opt = opts(wave_kernels=2, poll_timeout=MUTED_TIMEOUT_TICKS, mute_rank=4)
     reg.write_inputs(x)
     assert reg.reduce_scatter(m, proto) == ll.LL_OK
     assert ll.ll_check(stream()) == ll.LL_ERR_TIMEOUT
     assert reg.allgather(m, proto) == ll.LL_OK
     assert ll.ll_check(stream()) == ll.LL_ERR_TIMEOUT
-    ll.ll_debug_mute_rank(-1)
-    ll.ll_set_poll_timeout(TEST_TIMEOUT_TICKS)
+    reg.opt = opts(wave_kernels=2)
     reg.init()
     reg.write_inputs(x)
     check_ok(reg.reduce_scatter(m, proto), "rs after timeout")
