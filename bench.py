@@ -49,7 +49,7 @@ def kernel_source_hash() -> str:
     """Hash of the device code (kernels, primitives, slot layout)."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2607_16100_amd", "csrc")
-    for name in ("ll_device.hpp", "ll_kernels.hpp", "ll_layout.hpp"):
+    for name in ("ll_device.hpp", "ll_kernels.hpp", "ll_layout.hpp", "ll_iter.hpp"):
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(name.encode())
             h.update(f.read())

@@ -826,3 +826,33 @@ def test_rs_ag_wave_kernels_launch_shapes_and_timeouts(proto):
     assert_bits_equal(reg.read_out(p * m, np.uint16).reshape(p, m), oracle.reduce_scatter(x), "RS after timeout")
     if proto == "sentinel":
         assert (reg.read_area(4) == SENT).all()
+
+
+# ------------------------------------------------ fallback off line packets
+@pytest.mark.parametrize("p,n,dtype,sized_for", [(8, 8192, "bf16", "auto"), (8, 64 * 8192, "bf16", "auto"),
+                                                 (4, 7168 * 16, "bf16", "auto"),
+                                                 (8, 16 << 20, "f32", "twoshot")])
+def test_no_lines_fallback_parity(p, n, dtype, sized_for):
+    """LL_OPT_NO_LINES at the sizes where AUTO otherwise runs 128-byte lines
+    (the 16 KiB line one-shot, the 1 MiB line two-shot with one wave per
+    peer, the 64 MiB line two-shot): AUTO takes the 8-byte-packet algorithm
+    of the same shape, whose correctness rests on the 8-byte atomicity the
+    memory model guarantees, and the result is the oracle's, bit for bit.  The
+    64 MiB case runs on a region sized for 8-byte packets only."""
+    es = 4 if dtype == "f32" else 2
+    st, plain = ll.ll_auto_algo(n, ll.DTYPES[dtype], p)
+    assert st == ll.LL_OK and "line" in [k for k, v in ll.ALGOS.items() if v == plain][0]
+    opt = opts(flags=ll.LL_OPT_NO_LINES)
+    reg = SymRegion(p, n, dtype, sized_for=sized_for, out_elems=p * n, opt=opt)
+    st, chosen = ll.ll_auto_algo(n, ll.DTYPES[dtype], p, reg.rank_stride, opt)
+    name = [k for k, v in ll.ALGOS.items() if v == chosen][0]
+    assert st == ll.LL_OK and "line" not in name and "sentinel" not in name
+    reg.init()
+    x = wl.uniform(p, n, dtype, seed=21) if dtype == "f32" else wl.normal(p, n, dtype, seed=21)
+    for k in range(2):
+        say(f"no-lines fallback P={p} n={n} {dtype} ({name}) call {k}")
+        assert_bits_equal(run_allreduce(reg, x, "auto"), oracle.allreduce(x), f"no lines P={p} n={n} call {k}")
+    if sized_for != "auto":
+        assert reg.allreduce(n, "twoshot_line") == ll.LL_ERR_SCRATCH  # the region holds no line area
+    del reg
+    torch.cuda.empty_cache()
