@@ -284,6 +284,10 @@ __device__ __forceinline__ void store_words_rs(rsrc_t rs, uint32_t w0, u32x4 v) 
   }
 }
 
+// A word index whose byte offset lies past every buffer resource: a load
+// from it returns zeros without touching memory.
+constexpr uint32_t kNoWord = 0x3FFFFFFCu;
+
 // ---------------------------------------------------------------------------
 // Packet formats.  A unit is what one group of lanes moves with one 16-byte
 // packet store each; `sub` is the lane's position in its group.  Each format
@@ -304,6 +308,11 @@ struct ProtoLL {
   __device__ static __forceinline__ void store(char *base, int64_t u, int /*sub*/, int64_t nelem, bool al4, u32x4 w) {
     store_words<DT>(base, 2 * u, 2, nelem, al4, w);
   }
+  // The first payload word of unit u that the lane loads (kNoWord: none),
+  // and the step after the load (none here); see ProtoLine.
+  __device__ static __forceinline__ uint32_t first_word(uint32_t u, int /*sub*/) { return 2 * u; }
+  __device__ static __forceinline__ u32x4 finish_load(u32x4 v, int /*sub*/) { return v; }
+  __device__ static __forceinline__ u32x4 start_store(u32x4 w, int /*sub*/) { return w; }
   __device__ static __forceinline__ u32x4 pack(u32x4 w, uint32_t epoch, int /*sub*/) {
     u32x4 p = {w.x, epoch, w.y, epoch};
     return p;
@@ -370,6 +379,11 @@ struct ProtoLine {
   __device__ static __forceinline__ u32x4 load(const char *base, int64_t u, int sub, int64_t nelem, bool al4) {
     return finish_load(load_raw<DT, NT>(base, u, sub, nelem, al4), sub);
   }
+  // The first of the 4 payload words of unit u that a data lane loads; the
+  // extra lanes load none.
+  __device__ static __forceinline__ uint32_t first_word(uint32_t u, int sub) {
+    return sub < 60 ? 240 * u + 4 * (uint32_t)sub : kNoWord;
+  }
   // Payload word `wd` (0..239) of a unit: the lane and word slot that carry
   // it in packet order.
   __device__ static __forceinline__ void slot_of_word(int wd, int *lane, int *slot) {
@@ -382,24 +396,27 @@ struct ProtoLine {
       *slot = wd & 3;
     }
   }
-  // Called with the whole wave active; w is in packet order.
-  template <int DT>
-  __device__ static __forceinline__ void store(char *base, int64_t u, int sub, int64_t nelem, bool al4, u32x4 w) {
-    const int64_t w0 = 240 * u;
-    // the flag lane of quad j takes its last word back from extra lane 60 + j/4
+  // A data lane's 4 payload words in stream order, from w in packet order:
+  // the flag lane of quad j takes its last word back from extra lane
+  // 60 + j/4.  Called with the whole wave active.
+  __device__ static __forceinline__ u32x4 start_store(u32x4 w, int sub) {
     const int j = (sub >> 2) & 15;
     const int src = 60 + (j >> 2);
     const uint32_t c0 = from_lane(src, w.x);
     const uint32_t c1 = from_lane(src, w.y);
     const uint32_t c2 = from_lane(src, w.z);
     const uint32_t c3 = from_lane(src, w.w);
-    if (sub < 60) {
-      if ((sub & 3) == 3) {
-        const int c = j & 3;
-        w.w = c == 0 ? c0 : (c == 1 ? c1 : (c == 2 ? c2 : c3));
-      }
-      store_words<DT>(base, w0 + 4 * sub, 4, nelem, al4, w);
+    if ((sub & 3) == 3) {
+      const int c = j & 3;
+      w.w = c == 0 ? c0 : (c == 1 ? c1 : (c == 2 ? c2 : c3));
     }
+    return w;
+  }
+  // Called with the whole wave active; w is in packet order.
+  template <int DT>
+  __device__ static __forceinline__ void store(char *base, int64_t u, int sub, int64_t nelem, bool al4, u32x4 w) {
+    w = start_store(w, sub);
+    if (sub < 60) store_words<DT>(base, 240 * u + 4 * sub, 4, nelem, al4, w);
   }
   __device__ static __forceinline__ u32x4 pack(u32x4 w, uint32_t epoch, int sub) {
     if ((sub & 3) == 3) w.w = epoch;
@@ -440,6 +457,9 @@ struct ProtoSent {
   __device__ static __forceinline__ void store(char *base, int64_t u, int /*sub*/, int64_t nelem, bool al4, u32x4 w) {
     store_words<DT>(base, 4 * u, 4, nelem, al4, w);
   }
+  __device__ static __forceinline__ uint32_t first_word(uint32_t u, int /*sub*/) { return 4 * u; }
+  __device__ static __forceinline__ u32x4 finish_load(u32x4 v, int /*sub*/) { return v; }
+  __device__ static __forceinline__ u32x4 start_store(u32x4 w, int /*sub*/) { return w; }
   __device__ static __forceinline__ u32x4 pack(u32x4 w, uint32_t /*epoch*/, int /*sub*/) { return w; }
   __device__ static __forceinline__ bool ready(u32x4 p, uint32_t /*epoch*/) {
     return p.x != kSentinel && p.y != kSentinel && p.z != kSentinel && p.w != kSentinel;

@@ -875,10 +875,12 @@ __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(LLCOLL_TWO
 // same offset in every chunk (lane l owns units l, l+64, ... of the tile).
 // ReduceScatter: wave q != r sends the tile of chunk q to its owner q (one
 // store per unit) and polls the tile of chunk r that peer q sent to this
-// rank; wave r loads its own chunk r.  Each wave stages its values, widened
-// to binary32, in LDS row q.  After a workgroup barrier every wave forms the
-// ordered sum of the rows for its lanes' units (all waves compute the same
-// sums) and rounds once.  AllGather: wave q != r sends the reduced tile (for
+// rank; wave r loads its own chunk r.  Each wave stages the raw payload
+// words in LDS row q.  After a workgroup barrier the workgroup's threads
+// share the ordered sum: each reduces some payload words of the tile over the
+// P rows, widened to binary32 in ascending rank order, rounds once and
+// writes the result to a reduced row; after a second barrier every wave reads
+// its lanes' reduced words.  AllGather: wave q != r sends the reduced tile (for
 // Mode 2: the own input) to peer q and polls the tile of chunk q that peer q
 // sends back, and stores it; wave r stores the own chunk.  As in the one-shot
 // wave kernel, a wave's polls never wait for more than its own U stores.
@@ -895,10 +897,12 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
   constexpr int K = Elem<DT>::kPerWord;
   using WU = WaveUnits<Pr, U>;
   constexpr int WPU = Pr::kMaxWords;  // payload words per lane and unit slot
-  constexpr int EPU = WPU * K;        // elements per lane and unit slot
   constexpr bool kRS = Mode != 2, kAG = Mode != 1;
   constexpr uint32_t kNowhere = 0xFFFFFFF0u;  // past every slot: the buffer resource discards the store
-  __shared__ float stage[kRS ? P : 1][64 * U * EPU];
+  // ReduceScatter staging: the raw payload words of each rank's tile (row q:
+  // rank q's values, in lane order), and the reduced tile.
+  __shared__ u32x4 stage[kRS ? P : 1][64 * U];
+  __shared__ u32x4 red[kRS ? 64 * U : 1];
   const uint32_t r = blockIdx.x % P;
   const uint32_t w = blockIdx.x / P;
   const uint32_t q = (uint32_t)uniform_u32(threadIdx.x >> 6);  // this wave's peer (q == r: the own values)
@@ -952,11 +956,31 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
   // The host launches no more workgroups per rank than there are tiles; a
   // workgroup past the last tile (a forced launch shape) loads and stores
   // nothing, since every access is guarded by the unit count.
+  // With 4-byte aligned inputs the loads go through a buffer resource that
+  // covers the chunk: no branch separates them, so the U loads of a lane are
+  // all in flight before the first result is used (line units move their
+  // displaced words only then).
   auto load_units = [&](const char *src, int64_t len, uint32_t tile, u32x4 *v) {
+    if (in_al4) {
+      const rsrc_t rs = make_rsrc(src, ((uint32_t)len * (uint32_t)E + 3u) & ~3u);
+      uint32_t w0[U];
 #pragma unroll
-    for (int k = 0; k < U; ++k) {
-      const uint32_t u = (uint32_t)WU::unit(tile, k, lane);
-      v[k] = u < units ? Pr::template load<DT>(src, u, sub, len, in_al4) : u32x4{0u, 0u, 0u, 0u};
+      for (int k = 0; k < U; ++k) {
+        const uint32_t u = (uint32_t)WU::unit(tile, k, lane);
+        w0[k] = u < units ? Pr::first_word(u, sub) : kNoWord;
+        v[k] = load_words_rs<WPU>(rs, w0[k]);
+      }
+#pragma unroll
+      for (int k = 0; k < U; ++k) {
+        if (ResetsSlots<Pr>::value) v[k] = clear_tail<DT, WPU>(v[k], w0[k], (uint32_t)len);
+        v[k] = Pr::finish_load(v[k], sub);
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < U; ++k) {
+        const uint32_t u = (uint32_t)WU::unit(tile, k, lane);
+        v[k] = u < units ? Pr::template load<DT>(src, u, sub, len, in_al4) : u32x4{0u, 0u, 0u, 0u};
+      }
     }
   };
   u32x4 first[U];
@@ -979,19 +1003,29 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
     if (Mode == 1) return out_rank;
     return out_rank + out_off + (uint64_t)c * C * E;
   };
+  // Store U units (packet order) of a result stream of len elements.  With a
+  // 4-byte aligned output and whole words the stores go through a buffer
+  // resource that covers the stream (no branch, the range check drops what
+  // lies past the end); otherwise element-wise at the edges.
+  auto store_out = [&](char *dst, int64_t len, uint32_t tile, const u32x4 *v) {
+    const uint32_t nb = (uint32_t)len * (uint32_t)E;
+    if (al4 && (nb & 3u) == 0) {
+      const rsrc_t rs = make_rsrc(dst, nb);
+#pragma unroll
+      for (int k = 0; k < U; ++k) {
+        const uint32_t u = (uint32_t)WU::unit(tile, k, lane);
+        const u32x4 w = Pr::start_store(v[k], sub);
+        store_words_rs<WPU>(rs, u < units ? Pr::first_word(u, sub) : kNoWord, w);
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < U; ++k) Pr::template store<DT>(dst, WU::unit(tile, k, lane), sub, len, al4, v[k]);
+    }
+  };
 
   auto stage_row = [&](const u32x4 *v) {
 #pragma unroll
-    for (int k = 0; k < U; ++k) {
-      const uint32_t wv[4] = {v[k].x, v[k].y, v[k].z, v[k].w};
-#pragma unroll
-      for (int j = 0; j < WPU; ++j) {
-        float f[K];
-        Elem<DT>::widen(wv[j], f);
-#pragma unroll
-        for (int e = 0; e < K; ++e) stage[kRS ? q : 0][(k * 64 + lane) * EPU + j * K + e] = f[e];
-      }
-    }
+    for (int k = 0; k < U; ++k) stage[kRS ? q : 0][k * 64 + lane] = v[k];
   };
 
   // Poll U units of slot `src` (this rank's slice) from peer q; sentinel
@@ -1007,6 +1041,7 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
       pend |= ((uint32_t)WU::unit(tile, k, lane) < units ? 1u : 0u) << k;
     }
     const uint32_t want = pend;
+    idle64(a.first_wait);
     uint32_t spins = 0;
     while (true) {
       compiler_fence();
@@ -1025,6 +1060,7 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
         if (pend != 0) budget.report((int)r, 1u << q, epoch);
         break;
       }
+      idle64(a.poll_gap);
     }
     if (ResetsSlots<Pr>::value) {
       const u32x4 sent = {ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel};
@@ -1036,6 +1072,16 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
 
   const uint32_t iters = Mode == 0 ? a.iters : 1u;
   const uint32_t W = a.grid / P;
+  bool pre_sent = true;  // the first tile's first step went out above
+// Diagnostics (-DLLCOLL_WAVE_PHASES=1): for lane 0 of each wave and the first
+// tile, the times its ReduceScatter packets went out (k = 0), its peer's
+// ReduceScatter packets were seen (1), it left the barrier (2) and its peer's
+// AllGather packets were seen (3).
+#define LL_TW_PHASE(k, expr)                                                          \
+  do {                                                                                \
+    if (LLCOLL_WAVE_PHASES && a.phases != nullptr && lane == 0 && tile == w && it == 0) \
+      a.phases[4 * (blockIdx.x * P + q) + (k)] = (expr);                              \
+  } while (0)
   for (uint32_t it = 0; it < iters; ++it) {
     if (Mode == 0 && it > 0) {
       const IterSpan sp = iter_span(a.n, a.iter_n, it, P, E);
@@ -1050,11 +1096,15 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
     }
     const uint32_t tiles = (uint32_t)((units + WU::kPerTile - 1) / WU::kPerTile);
     for (uint32_t tile = w; tile < tiles; tile += W) {
-      const bool sent_already = it == 0 && tile == w;  // the first step of the first tile went out above
+      const bool sent_already = pre_sent;  // this tile's first step went out earlier
+      pre_sent = false;
       u32x4 res[U];
       if constexpr (kRS) {
         // ---- ReduceScatter of this tile: wave q sends chunk q's tile to
-        // peer q (above, for the first tile), then polls what peer q sent
+        // peer q (earlier, for the first tile and for one sent ahead), then
+        // sends the workgroup's next tile of the iteration ahead, so that its
+        // packets travel while this tile is reduced and gathered, and polls
+        // what peer q sent for this tile
         u32x4 mine[U];
         if (sent_already) {
 #pragma unroll
@@ -1063,32 +1113,47 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
           load_units(in_chunk(q), chunk_len(q), tile, mine);
           store_units(slot_out + area, tile, mine);
         }
+        if (tile + W < tiles) {
+          load_units(in_chunk(q), chunk_len(q), tile + W, first);
+          store_units(slot_out + area, tile + W, first);
+          pre_sent = true;
+        }
+        LL_TW_PHASE(0, now_ticks() + (mine[0].x & 0u));
         if (q == r) {
           stage_row(mine);
         } else {
           u32x4 v[U];
           poll_peer(slot_in + area, tile, v);
+          LL_TW_PHASE(1, now_ticks() + (v[0].x & 0u));
           stage_row(v);
         }
         lds_barrier();
-        // ---- the ordered sum of the tile (every wave computes the same values)
-#pragma unroll
-        for (int k = 0; k < U; ++k) {
-          uint32_t o[4] = {0u, 0u, 0u, 0u};
-#pragma unroll
-          for (int j = 0; j < WPU; ++j) {
+        LL_TW_PHASE(2, now_ticks());
+        // ---- the ordered sum of the tile, split over the workgroup: thread
+        // t reduces payload words t, t + 64 P, ... of the tile over the P
+        // rows in ascending rank order, in binary32, and rounds once; then
+        // every wave takes the reduced words of its lanes
+        {
+          constexpr int kWords = 64 * U * WPU;
+          const uint32_t *const rows = reinterpret_cast<const uint32_t *>(&stage[0][0]);
+          uint32_t *const red_w = reinterpret_cast<uint32_t *>(&red[0]);
+          for (int i = (int)threadIdx.x; i < kWords; i += 64 * P) {
+            const int at = (i / WPU) * 4 + i % WPU;  // word j of a lane's unit slot sits at 4 * slot + j
             float acc[K];
-#pragma unroll
-            for (int e = 0; e < K; ++e) acc[e] = stage[0][(k * 64 + lane) * EPU + j * K + e];
+            Elem<DT>::widen(rows[at], acc);
 #pragma unroll
             for (int p = 1; p < P; ++p) {
+              float f[K];
+              Elem<DT>::widen(rows[p * 64 * U * 4 + at], f);
 #pragma unroll
-              for (int e = 0; e < K; ++e) acc[e] = acc[e] + stage[p][(k * 64 + lane) * EPU + j * K + e];
+              for (int e = 0; e < K; ++e) acc[e] = acc[e] + f[e];
             }
-            o[j] = Elem<DT>::narrow(acc);
+            red_w[at] = Elem<DT>::narrow(acc);
           }
-          res[k] = u32x4{o[0], o[1], o[2], o[3]};
         }
+        lds_barrier();
+#pragma unroll
+        for (int k = 0; k < U; ++k) res[k] = red[k * 64 + lane];
       } else {
         if (sent_already) {
 #pragma unroll
@@ -1103,22 +1168,15 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
       if constexpr (kAG) {
         if (!(Mode == 2 && sent_already)) store_units(slot_out + area + ag_off, tile, res);
         if (q == r) {
-#pragma unroll
-          for (int k = 0; k < U; ++k)
-            Pr::template store<DT>(out_chunk(r), WU::unit(tile, k, lane), sub, chunk_len(r), al4, res[k]);
+          store_out(out_chunk(r), chunk_len(r), tile, res);
         } else {
           u32x4 v[U];
           poll_peer(slot_in + area + ag_off, tile, v);
-#pragma unroll
-          for (int k = 0; k < U; ++k)
-            Pr::template store<DT>(out_chunk(q), WU::unit(tile, k, lane), sub, chunk_len(q), al4, v[k]);
+          LL_TW_PHASE(3, now_ticks() + (v[0].x & 0u));
+          store_out(out_chunk(q), chunk_len(q), tile, v);
         }
       } else {
-        if (q == r) {
-#pragma unroll
-          for (int k = 0; k < U; ++k)
-            Pr::template store<DT>(out_chunk(r), WU::unit(tile, k, lane), sub, chunk_len(r), al4, res[k]);
-        }
+        if (q == r) store_out(out_chunk(r), chunk_len(r), tile, res);
       }
       if constexpr (kRS) lds_barrier();  // the next tile overwrites the staging rows
     }
@@ -1126,6 +1184,7 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
   }
   stamp_end(a, t_start);
 }
+#undef LL_TW_PHASE
 
 // ---------------------------------------------------------------------------
 // Two-shot AllReduce with atomic accumulation: the gfx950 analogue of the
