@@ -305,8 +305,20 @@ def bench_rooted(torch, ll, steps):
     return out
 
 
-def bench_c3(torch, ll, steps):
-    """1 MiB per rank (batch 64 x hidden 8192 bf16, 8 ranks): two-shot against one-shot."""
+def bound_us(floor_p50_us, p, n, esize):
+    """Lower bound of one AllReduce call: the latency floor plus the time the
+    bytes no algorithm can avoid -- every rank reads its input and writes its
+    output once -- take at the HBM peak."""
+    if not floor_p50_us:
+        return None
+    return floor_p50_us + 2 * p * n * esize / (PEAK_HBM_GBS * 1e3)
+
+
+def bench_c3(torch, ll, steps, floor_p50_us=None):
+    """1 MiB per rank (batch 64 x hidden 8192 bf16, 8 ranks): two-shot against
+    one-shot, each with its fraction of the floor + bytes/peak bound; then AUTO
+    (flag formats only, and with the sentinel allowed) over 128 KiB .. 8 MiB
+    per rank (batch 8 .. 512)."""
     from paper_2607_16100_amd import workloads as wl
     from paper_2607_16100_amd.region import SymRegion
 
@@ -315,11 +327,35 @@ def bench_c3(torch, ll, steps):
     reg.init()
     reg.write_inputs(wl.normal(p, n, "bf16", sigma=0.5, seed=0))
     out = {}
-    for algo in ("twoshot", "twoshot_line", "twoshot_waves", "twoshot_sentinel", "twoshot_sentinel_waves",
-                 "twoshot_sentinel_out", "twoshot_atomic", "oneshot", "oneshot_line", "oneshot_sentinel", "auto"):
+    for algo in ("twoshot", "twoshot_line", "twoshot_waves", "twoshot_line_waves", "twoshot_sentinel",
+                 "twoshot_sentinel_waves", "twoshot_sentinel_out", "twoshot_atomic", "oneshot", "oneshot_line",
+                 "oneshot_sentinel", "auto"):
         out[algo] = paced_collective(torch, ll, reg, "ar", n, ll.ALGOS[algo], steps, 20)
     out["auto_sentinel_allowed"] = paced_collective(torch, ll, reg, "ar", n, ll.ALGOS["auto"], steps, 20,
                                                     flags=ll.LL_OPT_AUTO_SENTINEL)
+    b = bound_us(floor_p50_us, p, n, 2)
+    for r in out.values():
+        r["bound_us"] = round(b, 3) if b else None
+        r["frac_of_bound"] = round(b / r["p50_us"], 4) if b else None
+    del reg
+    sizes = {}
+    for batch in (8, 16, 32, 64, 128, 256, 512):
+        m = batch * 8192
+        reg = SymRegion(p, m, "bf16")
+        reg.init()
+        reg.write_inputs(wl.normal(p, m, "bf16", sigma=0.5, seed=batch))
+        st = steps if batch <= 64 else max(200, steps // 4)
+        row = {"bytes_per_rank": m * 2}
+        bb = bound_us(floor_p50_us, p, m, 2)
+        row["bound_us"] = round(bb, 3) if bb else None
+        for key, flags in (("auto", 0), ("auto_sentinel_allowed", ll.LL_OPT_AUTO_SENTINEL)):
+            r = paced_collective(torch, ll, reg, "ar", m, ll.ALGOS["auto"], st, 20, flags=flags)
+            row[key] = {"p50_us": r["p50_us"], "p99_us": r["p99_us"],
+                        "frac_of_bound": round(bb / r["p50_us"], 4) if bb else None}
+        sizes[f"{m * 2 >> 10}KiB"] = row
+        log(json.dumps({f"{m * 2 >> 10}KiB": row}))
+        del reg
+    out["auto_by_size"] = sizes
     return out
 
 
@@ -409,9 +445,11 @@ def bench_sweep(torch, ll, path, floor_p50_us=None):
                     continue
                 r = paced_collective(torch, ll, reg, "ar", n, ll.ALGOS[algo], steps, min(20, steps))
                 gbps = (bytemodel.allreduce_bytes(algo, p, n, 4) / r["p50_us"] / 1e3) if algo != "auto" else None
+                b = bound_us(floor_p50_us, p, n, 4)
                 r.update({"elements": n, "bytes_per_rank": n * 4, "algo": algo, "algorithmic_gbps_p50": gbps,
                           "hbm_frac_p50": gbps / PEAK_HBM_GBS if gbps else None,
-                          "ratio_to_floor": r["p50_us"] / floor_p50_us if floor_p50_us else None})
+                          "ratio_to_floor": r["p50_us"] / floor_p50_us if floor_p50_us else None,
+                          "bound_us": b, "frac_of_bound": b / r["p50_us"] if b else None})
                 f.write(json.dumps(r) + "\n")
                 f.flush()
                 log(f"sweep n={n} {algo} p50={r['p50_us']:.2f}")
@@ -681,7 +719,7 @@ def main():
         log(json.dumps(result["copy"]))
     if want("c3"):
         log("C3: 1 MiB bf16, two-shot vs one-shot")
-        result["c3"] = bench_c3(torch, ll, min(args.steps, 2000))
+        result["c3"] = bench_c3(torch, ll, min(args.steps, 2000), result.get("floor", {}).get("floor", {}).get("p50_us"))
         log(json.dumps(result["c3"]))
     if want("c5"):
         log("C5: reduce-scatter / all-gather")
@@ -705,6 +743,7 @@ def main():
 
     h = result.get("headline", {})
     fl = result.get("floor", {}).get("floor", {})
+    c3 = result.get("c3")
     bw = result.get("bw", {}).get("twoshot_line")
     khash = kernel_source_hash()
     roofline = None
@@ -764,6 +803,8 @@ def main():
         "floor_p50_us": round(fl["p50_us"], 3) if fl else None,
         "ratio_to_floor": round(h["p50_us"] / fl["p50_us"], 3) if (h and fl) else None,
         "hbm_gbps_64MB": round(bw["gbps"], 1) if bw else None,
+        "c3_1MiB": ({k: {"p50_us": round(c3[k]["p50_us"], 3), "frac_of_bound": c3[k]["frac_of_bound"]}
+                     for k in ("auto", "auto_sentinel_allowed")} | {"bound_us": c3["auto"]["bound_us"]}) if c3 else None,
         "roofline": roofline,
         "cpu_baseline": result.get("cpu"),
         "detail": result,

@@ -415,45 +415,62 @@ KArgs base_args(void *sym_base, size_t rank_stride, void *out, uint32_t epoch) {
 }
 
 // Size thresholds measured on MI355X (p50 of back-to-back calls of every
-// algorithm at 1 KiB .. 8 MiB per rank, P = 2, 4, 8, bfloat16; binary32
+// algorithm at 2 KiB .. 16 MiB per rank, P = 2 .. 8, bfloat16; binary32
 // crosses over at the same byte sizes); M = input bytes per rank.  Flags only
 // unless the caller allows sentinel mode, which wins from the smallest sizes
-// up to a few MiB, as the paper observes for larger messages and rank counts.
+// up to 1-8 MiB (by rank count), as the paper observes for larger messages
+// and rank counts.
 ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
   const uint64_t KiB = 1024, MiB = 1024 * 1024;
-  if (P <= 2) {
-    if (sentinel_ok) {
-      if (in_bytes <= 1 * MiB) return LL_ALGO_ONESHOT_SENTINEL_WAVES;
-      if (in_bytes <= 2 * MiB) return LL_ALGO_ONESHOT_SENTINEL;
-      if (in_bytes <= 16 * MiB) return LL_ALGO_TWOSHOT_SENTINEL_WAVES;
-      return LL_ALGO_TWOSHOT_LINE;
+  // the line two-shot with one wave per peer, up to 16 MiB (8 MiB at 6-7
+  // ranks); the one-lane line two-shot above
+  const uint64_t line_waves_max = (P == 6 || P == 7 ? 8 : 16) * MiB;
+  auto large = [&]() { return in_bytes <= line_waves_max ? LL_ALGO_TWOSHOT_LINE_WAVES : LL_ALGO_TWOSHOT_LINE; };
+  if (sentinel_ok) {
+    uint64_t one_max, two_max;  // one-shot, then two-shot, sentinel units with one wave per peer
+    if (P <= 3) {
+      one_max = 1 * MiB;
+      two_max = (P == 2 ? 8 : 4) * MiB;
+    } else if (P <= 5) {
+      one_max = 256 * KiB;
+      two_max = 2 * MiB;
+    } else if (P <= 7) {
+      one_max = 128 * KiB;
+      two_max = (P == 6 ? 2 : 1) * MiB;
+    } else {
+      one_max = 64 * KiB;
+      two_max = 1 * MiB;
     }
-    if (in_bytes <= 256 * KiB) return LL_ALGO_ONESHOT_WAVES;
+    if (in_bytes <= one_max) return LL_ALGO_ONESHOT_SENTINEL_WAVES;
+    if (P == 2 && in_bytes <= 2 * MiB) return LL_ALGO_ONESHOT_SENTINEL;
+    if (in_bytes <= two_max) return LL_ALGO_TWOSHOT_SENTINEL_WAVES;
+    return large();
+  }
+  if (P == 2) {
+    if (in_bytes <= 512 * KiB) return LL_ALGO_ONESHOT_WAVES;
     if (in_bytes <= 1 * MiB) return LL_ALGO_ONESHOT_LINE_WAVES;
     if (in_bytes <= 2 * MiB) return LL_ALGO_ONESHOT_LINE;
-    if (in_bytes <= 8 * MiB) return LL_ALGO_TWOSHOT_LINE_WAVES;
-    return LL_ALGO_TWOSHOT_LINE;
-  }
-  // the line two-shot with one wave per peer serves up to 8 MiB at 3-4 ranks
-  const uint64_t line_waves_max = (P <= 4 ? 8 : 4) * MiB;
-  if (sentinel_ok) {
-    if (in_bytes <= (P <= 4 ? 256 : 64) * KiB) return LL_ALGO_ONESHOT_SENTINEL_WAVES;
-    if (in_bytes <= 2 * MiB) return LL_ALGO_TWOSHOT_SENTINEL_WAVES;
-    if (in_bytes <= line_waves_max) return LL_ALGO_TWOSHOT_LINE_WAVES;
-    return LL_ALGO_TWOSHOT_LINE;
+    return large();
   }
   // the line one-shot sums a word per thread from 4 ranks up (64*P threads
-  // for 240 words), which makes it the faster one-shot from 16 KiB
-  if (P <= 4) {
-    if (in_bytes <= (P == 4 ? 64 : 128) * KiB) return LL_ALGO_ONESHOT_WAVES;
-    if (in_bytes <= 256 * KiB) return P == 4 ? LL_ALGO_ONESHOT_LINE_WAVES : LL_ALGO_TWOSHOT_WAVES;
+  // for 240 words), which makes it the faster one-shot from 16-128 KiB
+  uint64_t one8_max, line_max;  // one-shot 8-byte packets, then lines, one wave per peer
+  if (P == 3) {
+    one8_max = 128 * KiB;
+    line_max = 512 * KiB;
+  } else if (P == 4) {
+    one8_max = 64 * KiB;
+    line_max = 256 * KiB;
+  } else if (P <= 6) {
+    one8_max = 16 * KiB;
+    line_max = 128 * KiB;
   } else {
-    if (in_bytes <= 8 * KiB) return LL_ALGO_ONESHOT_WAVES;
-    if (in_bytes <= 32 * KiB) return LL_ALGO_ONESHOT_LINE_WAVES;
-    if (in_bytes <= 128 * KiB) return LL_ALGO_TWOSHOT_WAVES;
+    one8_max = 8 * KiB;
+    line_max = 64 * KiB;
   }
-  if (in_bytes <= line_waves_max) return LL_ALGO_TWOSHOT_LINE_WAVES;
-  return LL_ALGO_TWOSHOT_LINE;
+  if (in_bytes <= one8_max) return LL_ALGO_ONESHOT_WAVES;
+  if (in_bytes <= line_max) return LL_ALGO_ONESHOT_LINE_WAVES;
+  return large();
 }
 
 // ReduceScatter / AllGather, by the bytes of data per rank (input for

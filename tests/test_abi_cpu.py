@@ -324,6 +324,16 @@ def test_auto_algo_choices():
     assert ll.ll_auto_algo(8192, bf16, 8, 0, sent) == (ll.LL_OK, A["oneshot_sentinel_waves"])
     assert ll.ll_auto_algo(64 * 8192, bf16, 8, 0, sent) == (ll.LL_OK, A["twoshot_sentinel_waves"])
     assert ll.ll_auto_algo(16 << 20, f32, 8, 0, sent) == (ll.LL_OK, A["twoshot_line"])
+    # measured crossovers away from the configurations' sizes
+    assert ll.ll_auto_algo(4 << 20, bf16, 8) == (ll.LL_OK, A["twoshot_line_waves"])           # 8 MiB
+    assert ll.ll_auto_algo(4 * 8192, bf16, 8) == (ll.LL_OK, A["oneshot_line_waves"])         # 64 KiB
+    assert ll.ll_auto_algo(64 * 8192, bf16, 8) == (ll.LL_OK, A["twoshot_line_waves"])        # 1 MiB
+    assert ll.ll_auto_algo(1 << 20, bf16, 8, 0, sent) == (ll.LL_OK, A["twoshot_line_waves"])  # 2 MiB
+    assert ll.ll_auto_algo(1 << 17, bf16, 3) == (ll.LL_OK, A["oneshot_line_waves"])          # 256 KiB
+    assert ll.ll_auto_algo(4 << 20, bf16, 6) == (ll.LL_OK, A["twoshot_line_waves"])          # 8 MiB
+    assert ll.ll_auto_algo(8 << 20, bf16, 6) == (ll.LL_OK, A["twoshot_line"])                # 16 MiB
+    assert ll.ll_auto_algo(8 << 20, bf16, 8) == (ll.LL_OK, A["twoshot_line_waves"])          # 16 MiB
+    assert ll.ll_auto_algo(1 << 19, bf16, 2, 0, sent) == (ll.LL_OK, A["oneshot_sentinel_waves"])
     assert ll.ll_auto_algo(1, f32, 1)[0] == ll.LL_ERR_INVALID
     assert ll.ll_auto_algo(1, f32, 9)[0] == ll.LL_ERR_INVALID
     assert ll.ll_auto_algo(1, 7, 8)[0] == ll.LL_ERR_UNSUPPORTED

@@ -50,6 +50,7 @@ ORACLES = [("c", oracle.allreduce), ("numpy", npref.allreduce), ("c_reduce", _re
 
 
 # ---------------------------------------------------------------- wrong oracles
+@np.errstate(over="ignore")  # the overflow pins feed these on purpose
 def wrong_descending(x):
     acc = npref.widen(x[-1]).copy()
     for q in range(x.shape[0] - 2, -1, -1):
@@ -57,6 +58,7 @@ def wrong_descending(x):
     return npref.narrow(acc, x.dtype)
 
 
+@np.errstate(over="ignore")  # the overflow pins feed these on purpose
 def wrong_pairwise(x):
     vals = [npref.widen(x[q]).copy() for q in range(x.shape[0])]
     while len(vals) > 1:
@@ -67,6 +69,7 @@ def wrong_pairwise(x):
     return npref.narrow(vals[0], x.dtype)
 
 
+@np.errstate(over="ignore")  # the overflow pins feed these on purpose
 def wrong_own_first(x, r):
     acc = npref.widen(x[r]).copy()
     for q in range(x.shape[0]):
@@ -75,6 +78,7 @@ def wrong_own_first(x, r):
     return npref.narrow(acc, x.dtype)
 
 
+@np.errstate(over="ignore")  # the overflow pins feed these on purpose
 def wrong_zero_start(x):
     acc = np.zeros(x.shape[1], np.float32)
     for q in range(x.shape[0]):
@@ -82,6 +86,7 @@ def wrong_zero_start(x):
     return npref.narrow(acc, x.dtype)
 
 
+@np.errstate(over="ignore")  # the overflow pins feed these on purpose
 def wrong_bf16_per_step(x):
     acc = npref.widen(x[0]).copy()
     for q in range(1, x.shape[0]):
