@@ -44,13 +44,17 @@ struct ll_tuning {
   uint64_t *stamps;         /* device memory or NULL: each workgroup b writes its
                                start and end time (100 MHz ticks) to stamps[b]
                                and stamps[grid + b] */
-  uint64_t *phases;         /* device memory or NULL: phase times of the one-shot
-                               wave kernels, in a library built with
+  uint64_t *phases;         /* device memory or NULL: phase times of the wave
+                               kernels, in a library built with
                                -DLLCOLL_WAVE_PHASES=1 (4*grid*nranks words: for
-                               lane 0 of wave w of workgroup b, [4(b*nranks+w)]
-                               = packet store issued, [+1] = peer's packets all
-                               seen, [+2] = past the workgroup barrier);
-                               ignored otherwise */
+                               lane 0 of wave w of workgroup b, at
+                               [4(b*nranks+w)]: one-shot: packet store issued,
+                               [+1] peer's packets all seen, [+2] past the
+                               workgroup barrier; two-shot AllReduce, the
+                               workgroup's first tile: ReduceScatter packets
+                               issued, [+1] peer's ReduceScatter packets seen,
+                               [+2] past the barrier, [+3] peer's AllGather
+                               packets seen); ignored otherwise */
   int *grid_out;            /* host memory or NULL: receives the launch's total
                                workgroups */
   int *threads_out;         /* host memory or NULL: receives its threads per

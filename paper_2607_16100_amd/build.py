@@ -11,7 +11,7 @@ each to an object of its own, in parallel, then linked into one shared
 library.  Extra preprocessor definitions (diagnostic builds) can be passed
 with ``extra_defines``; such a build goes to ``out`` instead of the default
 library path.  ``build_phases`` (``--phases``) builds the diagnostic variant
-with the one-shot wave kernels' phase stamps compiled in,
+with the wave kernels' phase stamps compiled in,
 ``libllcoll_phases.so``, which ``timeline.py`` loads.
 """
 from __future__ import annotations

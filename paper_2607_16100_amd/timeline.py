@@ -1,19 +1,23 @@
-"""Phase timeline of the one-shot AllReduce with one wave per peer.
+"""Phase timeline of the one-shot and two-shot AllReduce with one wave per peer.
 
-Run with the diagnostic build of the library, whose one-shot wave kernels
-record phase times (``python -m paper_2607_16100_amd.build --phases``):
+Run with the diagnostic build of the library, whose wave kernels record phase
+times (``python -m paper_2607_16100_amd.build --phases``):
 
     LLCOLL_LIBRARY=paper_2607_16100_amd/libllcoll_phases.so \\
-        python -m paper_2607_16100_amd.timeline [--calls 300] [--json out.jsonl]
+        python -m paper_2607_16100_amd.timeline [--twoshot] [--calls 300] [--json out.jsonl]
 
-For each case (8 ranks, bfloat16, 128 bytes and 16 KiB per rank, every packet
-format), `calls` back-to-back calls are queued behind a spin kernel and each
-records, from the 100 MHz constant clock, every workgroup's start and end and,
-for lane 0 of every wave, three phase times: its packet store issued, its
-peer's packets all seen, and past the workgroup barrier.  The table gives
-microseconds from the call's first workgroup start, as the median over calls
-of the median over waves (max over the grid in brackets), plus the median
-call-to-call interval.  The stamps themselves add about 0.1 us.
+For each case, `calls` back-to-back calls are queued behind a spin kernel and
+each records, from the 100 MHz constant clock, every workgroup's start and end
+and, for lane 0 of every wave, its phase times.  One-shot (8 ranks, bfloat16,
+128 bytes and 16 KiB per rank, every packet format): its packet store issued,
+its peer's packets all seen, past the workgroup barrier.  Two-shot
+(``--twoshot``: 8 ranks, bfloat16, 1 MiB per rank, every packet format; the
+first tile of each workgroup): its ReduceScatter packets issued, its peer's
+ReduceScatter packets seen, past the barrier, its peer's AllGather packets
+seen.  The table gives microseconds from the call's first workgroup start, as
+the median over calls of the median over waves (max over the grid in
+brackets), plus the median call-to-call interval.  The stamps themselves add
+about 0.1 us.
 """
 from __future__ import annotations
 
@@ -30,9 +34,10 @@ if ROOT not in sys.path:
 
 TICK_US = 0.01
 PHASES = ("store issued", "peer's packets seen", "past the barrier")
+PHASES_TWOSHOT = ("RS packets issued", "peer's RS packets seen", "past the barrier", "peer's AG packets seen")
 
 
-def run_case(p: int, n: int, dtype: str, algo: str, calls: int):
+def run_case(p: int, n: int, dtype: str, algo: str, calls: int, phases=PHASES):
     import torch
 
     from paper_2607_16100_amd import llcoll as ll
@@ -70,7 +75,7 @@ def run_case(p: int, n: int, dtype: str, algo: str, calls: int):
     row = {"ranks": p, "bytes_per_rank": n * (2 if dtype == "bf16" else 4), "dtype": dtype, "algo": algo,
            "grid": grid, "threads": threads, "interval_p50_us": round(float(np.median(np.diff(ends))) * TICK_US, 3),
            "span_p50_us": round(float(np.median(ends - t0)) * TICK_US, 3), "workgroup_start": med_max(rel(st[:, :grid]))}
-    for k, name in enumerate(PHASES):
+    for k, name in enumerate(phases):
         a = ph[:, :, k]
         ok = a[0] != 0
         if ok.any():
@@ -83,22 +88,28 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--calls", type=int, default=300)
     ap.add_argument("--json", default="")
+    ap.add_argument("--twoshot", action="store_true")
     args = ap.parse_args()
     import torch
 
     torch.cuda.set_device(0)
     rows = []
-    for n in (64, 8192):
-        for algo in ("oneshot_waves", "oneshot_line_waves", "oneshot_sentinel_waves"):
-            rows.append(run_case(8, n, "bf16", algo, args.calls))
-            print(json.dumps(rows[-1]), file=sys.stderr, flush=True)
+    if args.twoshot:
+        phases = PHASES_TWOSHOT
+        cases = [(64 * 8192, a) for a in ("twoshot_line_waves", "twoshot_sentinel_waves", "twoshot_waves")]
+    else:
+        phases = PHASES
+        cases = [(n, a) for n in (64, 8192) for a in ("oneshot_waves", "oneshot_line_waves", "oneshot_sentinel_waves")]
+    for n, algo in cases:
+        rows.append(run_case(8, n, "bf16", algo, args.calls, phases))
+        print(json.dumps(rows[-1]), file=sys.stderr, flush=True)
     if args.json:
         with open(args.json, "w") as f:
             for r in rows:
                 f.write(json.dumps(r) + "\n")
-    keys = ["workgroup_start", *PHASES, "workgroup_end"]
+    keys = ["workgroup_start", *phases, "workgroup_end"]
     print("| phase (us from the first workgroup start) | " +
-          " | ".join(f"{r['algo'].replace('oneshot_', '')} {r['bytes_per_rank']} B" for r in rows) + " |")
+          " | ".join(f"{r['algo']} {r['bytes_per_rank']} B" for r in rows) + " |")
     print("|---|" + "---:|" * len(rows))
     print("| workgroups | " + " | ".join(str(r["grid"]) for r in rows) + " |")
     for k in keys:
