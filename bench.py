@@ -645,11 +645,18 @@ def bench_cpu_all_cores(seconds: float):
                       "of repeated calls split into one contiguous column block per core"}
 
 
+# The 64 MiB leg's kernel: what AUTO runs for 64 MiB of binary32 per rank at 8
+# ranks (the line two-shot with one wave per peer, four units per lane).
+BW_ALGO = "twoshot_line_waves"
+BW_KERNEL = "k_twoshot_waves<ProtoLine, f32, 8, 4> (64 MiB per rank, 8 ranks)"
+BW_COUNTERS = "twoshot_line_waves_f32_64MiB_p8_counters.txt"
+
+
 def traffic_from_profiles(kernel_hash: str, grid_threads: int):
     """HBM bytes per launch from the committed counter summary (rocprofv3
     FETCH_SIZE and WRITE_SIZE, scaled by what they read for a 1 GiB copy), if
     it was taken from the current device code with the same launch grid."""
-    path = os.path.join(ROOT, "profiles", "twoshot_line_f32_64MiB_p8_counters.txt")
+    path = os.path.join(ROOT, "profiles", BW_COUNTERS)
     if not os.path.exists(path):
         return None
     try:
@@ -708,7 +715,8 @@ def main():
         log(json.dumps(result["sol"]))
     if want("bw"):
         log("bandwidth at 64 MiB per rank")
-        result["bw"] = bench_bandwidth(torch, ll, 16 << 20, ["twoshot_line", "twoshot", "twoshot_sentinel",
+        result["bw"] = bench_bandwidth(torch, ll, 16 << 20, ["twoshot_line_waves", "twoshot_line", "twoshot",
+                                                                "twoshot_sentinel", "twoshot_sentinel_waves",
                                                                 "twoshot_sentinel_out", "twoshot_atomic",
                                                                 "oneshot_line", "oneshot", "oneshot_sentinel"],
                                        iters=args.bw_iters)
@@ -744,14 +752,14 @@ def main():
     h = result.get("headline", {})
     fl = result.get("floor", {}).get("floor", {})
     c3 = result.get("c3")
-    bw = result.get("bw", {}).get("twoshot_line")
+    bw = result.get("bw", {}).get(BW_ALGO)
     khash = kernel_source_hash()
     roofline = None
     if bw:
         roofline = {"bound": "hbm", "achieved": round(bw["gbps"], 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                     "frac": round(bw["gbps"] / PEAK_HBM_GBS, 4),
                     "traffic": traffic_from_profiles(khash, bw["grid"] * bw["threads"]),
-                    "kernel": "k_twoshot<ProtoLine, f32, 8> (64 MiB per rank)",
+                    "kernel": BW_KERNEL,
                     "kernel_us": round(bw["kernel_us"], 2), "algorithmic_bytes": bw["algorithmic_bytes"]}
         if roofline["traffic"]:
             # the counters' bytes (FETCH_SIZE + WRITE_SIZE, calibrated) over the same kernel time

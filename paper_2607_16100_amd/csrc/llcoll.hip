@@ -253,11 +253,13 @@ struct Plan {
 };
 
 // Units per lane (U) of the wave-per-peer kernels, measured at 16 KiB ..
-// 4 MiB per rank and 2, 4 and 8 ranks.  One unit per lane, except in the
+// 64 MiB per rank and 2 .. 8 ranks.  One unit per lane, except in the
 // two-shot AllReduce once its tiles would need a second round of
 // workgroups, which costs a whole extra exchange:
 //  - lines (a line unit is a whole wave): two units per lane once the P
-//    tiles of a step hold more than 1536 line units;
+//    tiles of a step hold more than 1536 line units, four once they hold
+//    more than 8192 (from about 8 MiB per rank, where the kernel is bound by
+//    bandwidth and fewer, longer waves move the bytes faster);
 //  - 8-byte packets and sentinel units: two once a chunk has more tiles of
 //    64 units than resident workgroups per rank.
 // Elsewhere two units per lane are never more than about 3 % faster and up
@@ -268,7 +270,7 @@ int wave_units_log2(const Plan &pl, int wpr) {
   if (forced == 2) return 1;
   if (forced == 4) return 2;
   if (pl.kind != K_TWOSHOT_WAVES) return 0;
-  if (pl.proto == PR_LINE) return pl.units * pl.P <= 1536 ? 0 : 1;
+  if (pl.proto == PR_LINE) return pl.units * pl.P <= 1536 ? 0 : (pl.units * pl.P <= 8192 ? 1 : 2);
   int cap = 0;
   if (resident_grid(table().twaves[0][0][wpr][pl.dt][pl.P], 64 * pl.P, &cap) != LL_OK) return 1;
   return (pl.units + 63) / 64 <= cap / pl.P ? 0 : 1;
@@ -422,9 +424,10 @@ KArgs base_args(void *sym_base, size_t rank_stride, void *out, uint32_t epoch) {
 // and rank counts.
 ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
   const uint64_t KiB = 1024, MiB = 1024 * 1024;
-  // the line two-shot with one wave per peer, up to 16 MiB (8 MiB at 6-7
-  // ranks); the one-lane line two-shot above
-  const uint64_t line_waves_max = (P == 6 || P == 7 ? 8 : 16) * MiB;
+  // the line two-shot with one wave per peer at every size up to the
+  // maximum, except above 8 MiB at 6 ranks and 16 MiB at 5, where the
+  // one-lane line two-shot is faster (measured at 8-64 MiB, binary32)
+  const uint64_t line_waves_max = P == 6 ? 8 * MiB : (P == 5 ? 16 * MiB : L::kMaxInputBytes);
   auto large = [&]() { return in_bytes <= line_waves_max ? LL_ALGO_TWOSHOT_LINE_WAVES : LL_ALGO_TWOSHOT_LINE; };
   if (sentinel_ok) {
     uint64_t one_max, two_max;  // one-shot, then two-shot, sentinel units with one wave per peer

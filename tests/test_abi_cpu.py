@@ -318,12 +318,15 @@ def test_auto_algo_choices():
     assert ll.ll_auto_algo(4096, bf16, 8) == (ll.LL_OK, A["oneshot_waves"])            # 8 KiB
     assert ll.ll_auto_algo(8192, bf16, 8) == (ll.LL_OK, A["oneshot_line_waves"])       # C2, 16 KiB
     assert ll.ll_auto_algo(64 * 8192, bf16, 8) == (ll.LL_OK, A["twoshot_line_waves"])  # C3, 1 MiB
-    assert ll.ll_auto_algo(16 << 20, f32, 8) == (ll.LL_OK, A["twoshot_line"])          # C4, 64 MiB
+    assert ll.ll_auto_algo(16 << 20, f32, 8) == (ll.LL_OK, A["twoshot_line_waves"])    # C4, 64 MiB
     assert ll.ll_auto_algo(1024, f32, 4) == (ll.LL_OK, A["oneshot_waves"])             # C1
     sent = ll.Options(flags=ll.LL_OPT_AUTO_SENTINEL)
     assert ll.ll_auto_algo(8192, bf16, 8, 0, sent) == (ll.LL_OK, A["oneshot_sentinel_waves"])
     assert ll.ll_auto_algo(64 * 8192, bf16, 8, 0, sent) == (ll.LL_OK, A["twoshot_sentinel_waves"])
-    assert ll.ll_auto_algo(16 << 20, f32, 8, 0, sent) == (ll.LL_OK, A["twoshot_line"])
+    assert ll.ll_auto_algo(16 << 20, f32, 8, 0, sent) == (ll.LL_OK, A["twoshot_line_waves"])
+    assert ll.ll_auto_algo(16 << 20, f32, 6) == (ll.LL_OK, A["twoshot_line"])          # 64 MiB, 6 ranks
+    assert ll.ll_auto_algo(4 << 20, f32, 5) == (ll.LL_OK, A["twoshot_line_waves"])     # 16 MiB, 5 ranks
+    assert ll.ll_auto_algo(8 << 20, f32, 5) == (ll.LL_OK, A["twoshot_line"])           # 32 MiB, 5 ranks
     # measured crossovers away from the configurations' sizes
     assert ll.ll_auto_algo(4 << 20, bf16, 8) == (ll.LL_OK, A["twoshot_line_waves"])           # 8 MiB
     assert ll.ll_auto_algo(4 * 8192, bf16, 8) == (ll.LL_OK, A["oneshot_line_waves"])         # 64 KiB
@@ -333,6 +336,7 @@ def test_auto_algo_choices():
     assert ll.ll_auto_algo(4 << 20, bf16, 6) == (ll.LL_OK, A["twoshot_line_waves"])          # 8 MiB
     assert ll.ll_auto_algo(8 << 20, bf16, 6) == (ll.LL_OK, A["twoshot_line"])                # 16 MiB
     assert ll.ll_auto_algo(8 << 20, bf16, 8) == (ll.LL_OK, A["twoshot_line_waves"])          # 16 MiB
+    assert ll.ll_auto_algo(64 << 20, bf16, 7) == (ll.LL_OK, A["twoshot_line_waves"])         # 128 MiB
     assert ll.ll_auto_algo(1 << 19, bf16, 2, 0, sent) == (ll.LL_OK, A["oneshot_sentinel_waves"])
     assert ll.ll_auto_algo(1, f32, 1)[0] == ll.LL_ERR_INVALID
     assert ll.ll_auto_algo(1, f32, 9)[0] == ll.LL_ERR_INVALID
