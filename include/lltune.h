@@ -41,6 +41,10 @@ struct ll_tuning {
   int poll_gap;             /* idle time between polls, same units */
   int mute_rank;            /* test hook: this rank publishes nothing, so its
                                peers' waits expire; -1 = off */
+  int clear_slots;          /* whether the reader of a flagged packet slot
+                               stores zeros back into it: 0 = by kernel and
+                               size (the default), 1 = always (wave-per-peer
+                               kernels), 2 = never */
   uint64_t *stamps;         /* device memory or NULL: each workgroup b writes its
                                start and end time (100 MHz ticks) to stamps[b]
                                and stamps[grid + b] */

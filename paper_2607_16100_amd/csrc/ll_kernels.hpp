@@ -41,6 +41,7 @@ struct KArgs {
   uint16_t poll_gap;    // idle time between polls, in units of 64 shader cycles
   uint32_t lag;         // two-shot pipeline distance between publish, reduce and gather (>= 0)
   uint32_t in_al4;      // every rank's input starts 4-byte aligned
+  uint32_t clear;       // flagged formats: the reader stores zeros back into every slot it has read
   const char *in;       // rank r's input at in + r * in_stride
   uint64_t in_stride;
   // Multi-iteration calls (bounded scratch, Sec. IV "Bidirectional
@@ -87,6 +88,7 @@ __device__ __forceinline__ KArgs pin_args(const KArgs &k) {
   a.poll_gap = (uint16_t)in_sgpr((uint32_t)k.poll_gap);
   a.lag = in_sgpr(k.lag);
   a.in_al4 = in_sgpr(k.in_al4);
+  a.clear = in_sgpr(k.clear);
   a.in = in_sgpr(k.in);
   a.in_stride = in_sgpr(k.in_stride);
   a.iter_n = in_sgpr(k.iter_n);
@@ -490,11 +492,11 @@ __global__ __launch_bounds__(512) void k_oneshot_waves(KArgs ka) {
       }
       idle64(a.poll_gap);
     }
-    if (ResetsSlots<Pr>::value) {
-      const u32x4 sent = {ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel};
+    if (ResetsSlots<Pr>::value || a.clear != 0) {
+      const uint32_t fill = ResetsSlots<Pr>::value ? ProtoSent::kSentinel : 0u;
 #pragma unroll
       for (int k = 0; k < U; ++k) {
-        if (want & (1u << k)) st_pkt(rs, WU::off(WU::unit(tile, k, lane), lane), sent);
+        if (want & (1u << k)) st_pkt(rs, WU::off(WU::unit(tile, k, lane), lane), u32x4{fill, fill, fill, fill});
       }
     }
   };
@@ -649,6 +651,8 @@ __global__ __launch_bounds__(512) void k_oneshot_tile(KArgs ka) {
     if (ResetsSlots<Pr>::value) {
       const u32x4 sent = {ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel};
       if (u < (uint32_t)a.units) st_pkt(rs, u * 16, sent);
+    } else if (a.clear != 0) {
+      if (u < (uint32_t)a.units) st_pkt(rs, u * 16, u32x4{0u, 0u, 0u, 0u});
     }
   }
   LL_WAVE_PHASE(1, now_ticks() + (v.x & 0u));
@@ -1062,11 +1066,11 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
       }
       idle64(a.poll_gap);
     }
-    if (ResetsSlots<Pr>::value) {
-      const u32x4 sent = {ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel};
+    if (ResetsSlots<Pr>::value || a.clear != 0) {
+      const uint32_t fill = ResetsSlots<Pr>::value ? ProtoSent::kSentinel : 0u;
 #pragma unroll
       for (int k = 0; k < U; ++k)
-        if (want & (1u << k)) st_pkt(rs, WU::off(WU::unit(tile, k, lane), lane), sent);
+        if (want & (1u << k)) st_pkt(rs, WU::off(WU::unit(tile, k, lane), lane), u32x4{fill, fill, fill, fill});
     }
   };
 
@@ -1180,7 +1184,9 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
       }
       if constexpr (kRS) lds_barrier();  // the next tile overwrites the staging rows
     }
-    if (ResetsSlots<Pr>::value && it + 1 < iters) wait_vm_all();
+    // slot resets are stores: acknowledged before the next iteration's packets
+    // go out, so that none can land after a peer's refill of its sub-buffer
+    if ((ResetsSlots<Pr>::value || a.clear != 0) && it + 1 < iters) wait_vm_all();
   }
   stamp_end(a, t_start);
 }

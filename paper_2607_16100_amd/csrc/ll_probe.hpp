@@ -293,9 +293,10 @@ __global__ __launch_bounds__(1024) void k_probe_stream(const u32x4 *src, u32x4 *
 // q of the workgroup loads the tile's input (each lane 8 bytes), stores it as
 // one 16-byte packet store per lane into slot (q <- r) of peer q, polls the
 // same units of slot (r <- q) in its own slice until both flags of every lane
-// equal the epoch (a wave vote ends the loop), and stores the 8 payload bytes
-// it received to the rank's output tile.  The own-rank wave stores its own
-// input there without an exchange.  No LDS, no barrier, no sum: every wave of
+// equal the epoch (a wave vote ends the loop), clears the slot it read when
+// the call asks for it (as the one-shot collective does at every size), and
+// stores the 8 payload bytes it received to the rank's output tile.  The
+// own-rank wave stores its own input there without an exchange.  No LDS, no barrier, no sum: every wave of
 // a workgroup writes the same output tile, so each output element ends up as
 // one rank's input element (which one is unspecified).  The same instruction
 // order as the collective: input load first, then the packet store with no
@@ -337,6 +338,7 @@ __global__ __launch_bounds__(512) void k_probe_exchange(KArgs ka) {
         break;
       }
     }
+    if (a.clear != 0 && u < units) st_pkt(rs, u * 16, u32x4{0u, 0u, 0u, 0u});
   }
   const rsrc_t out_rs = make_rsrc(a.out + (uint64_t)r * in_bytes, in_bytes);
   __builtin_amdgcn_raw_buffer_store_b64(v, out_rs, (int)(u * 8), 0, kNT);

@@ -43,6 +43,7 @@ struct CallOpts {
   uint32_t flags = 0;
   uint64_t timeout = kDefaultTimeout;
   int wg_per_rank = 0, threads = 0, wave_units = 0, wave_kernels = 0, lag = 1, first_wait = 0, poll_gap = 0;
+  int clear_slots = 0;  // 0 = by kernel and size, 1 = always, 2 = never
   int mute = -1;
   uint64_t *stamps = nullptr, *phases = nullptr;
   int *grid_out = nullptr, *threads_out = nullptr;
@@ -69,6 +70,7 @@ int resolve_opts(const ll_options *o, CallOpts *c) {
   if (t->pipeline_lag < -1 || t->pipeline_lag > 64) return LL_ERR_INVALID;
   if (t->first_wait < 0 || t->first_wait > 1000 || t->poll_gap < 0 || t->poll_gap > 1000) return LL_ERR_INVALID;
   if (t->mute_rank < -1 || t->mute_rank >= LL_MAX_RANKS) return LL_ERR_INVALID;
+  if (t->clear_slots < 0 || t->clear_slots > 2) return LL_ERR_INVALID;
   c->wg_per_rank = t->workgroups_per_rank;
   c->threads = t->threads;
   c->wave_units = t->wave_units;
@@ -77,6 +79,7 @@ int resolve_opts(const ll_options *o, CallOpts *c) {
   c->first_wait = t->first_wait;
   c->poll_gap = t->poll_gap;
   c->mute = t->mute_rank;
+  c->clear_slots = t->clear_slots;
   c->stamps = t->stamps;
   c->phases = t->phases;
   c->grid_out = t->grid_out;
@@ -276,6 +279,36 @@ int wave_units_log2(const Plan &pl, int wpr) {
   return (pl.units + 63) / 64 <= cap / pl.P ? 0 : 1;
 }
 
+// Whether the reader of a flagged packet slot stores zeros back into it
+// after reading it (KArgs::clear; sentinel slots are always reset).  A zero
+// flag is never accepted, so the protocol is unchanged; what changes is
+// timing.  Measured on MI355X, a slot that its reader has written back takes
+// the next call's packets sooner: 0.26-0.34 us off the 16 KiB one-shot at 8
+// ranks, 0.5-0.9 us off the 512 KiB-1 MiB line two-shot; but the stores cost
+// bandwidth once a call is bound by it (the 8 MiB line two-shot at 8 ranks
+// went from 59 to 70 us).  The crossover lies where the packet bytes of a
+// call pass about 16 MiB, counted as (data per rank and iteration, the
+// larger of input and output) x (P - 1) x (exchanges: 2 for the two-shot
+// AllReduce, 1 for a stand-alone ReduceScatter or AllGather): measured at
+// 2, 4 and 8 ranks for the AllReduce (1 / 2 / 8 MiB) and at 4 and 8 ranks
+// for RS / AG (C5 shapes up to b = 512).  So: on for the one-shot wave
+// kernels, and for the two-shot and stand-alone RS / AG wave kernels below
+// that crossover.  The one-lane kernels never clear.
+constexpr uint64_t kClearMaxBytes = 16ull << 20;
+
+uint32_t clear_slots(const Plan &pl) {
+  const bool waves = pl.kind == K_ONESHOT_WAVES || pl.kind == K_TWOSHOT_WAVES || pl.kind == K_RS_WAVES ||
+                     pl.kind == K_AG_WAVES;
+  if (!waves || pl.proto == PR_SENT || pl.o.clear_slots == 2) return 0;
+  if (pl.o.clear_slots == 1 || pl.kind == K_ONESHOT_WAVES) return 1;
+  const uint64_t es = pl.dt == LL_BF16 ? 2 : 4;
+  const uint64_t n = (uint64_t)(pl.a.iters > 1 ? pl.a.iter_n : pl.a.n);
+  // AllReduce: n elements in and out; ReduceScatter: P*n in; AllGather: P*n out
+  const uint64_t bytes = (pl.kind == K_TWOSHOT_WAVES ? 1 : (uint64_t)pl.P) * n * es;
+  const uint64_t exchanges = pl.kind == K_TWOSHOT_WAVES ? 2 : 1;
+  return bytes * (uint64_t)(pl.P - 1) * exchanges <= kClearMaxBytes ? 1u : 0u;
+}
+
 int launch_kernel(kernel_fn fn, const Plan &pl, int W, int threads, void *stream);
 
 int launch(const Plan &pl, void *stream) {
@@ -350,6 +383,7 @@ int launch_kernel(kernel_fn fn, const Plan &pl, int W, int threads, void *stream
   a.first_wait = (uint16_t)pl.o.first_wait;
   a.poll_gap = (uint16_t)pl.o.poll_gap;
   a.lag = (uint32_t)pl.o.lag;
+  a.clear = clear_slots(pl);
   a.grid = (uint32_t)grid;
   a.block = (uint32_t)threads;
   a.units = pl.units;
@@ -1491,6 +1525,7 @@ int ll_bench_exchange(void *sym_base, size_t rank_stride, void *out, size_t coun
   a.timeout = kDefaultTimeout;
   a.grid = (uint32_t)grid;
   a.block = (uint32_t)threads;
+  a.clear = 1;  // as the one-shot wave kernels
   st = status_of(stream, &a.status);
   if (st != LL_OK) return st;
   for (int i = 0; i < calls; ++i) {

@@ -58,7 +58,8 @@ class LLTuning(ctypes.Structure):
     """struct ll_tuning (include/lltune.h)."""
     _fields_ = [("size", _u32), ("workgroups_per_rank", _i), ("threads", _i), ("wave_units", _i),
                 ("wave_kernels", _i), ("pipeline_lag", _i), ("first_wait", _i), ("poll_gap", _i),
-                ("mute_rank", _i), ("stamps", _vp), ("phases", _vp), ("grid_out", _vp), ("threads_out", _vp)]
+                ("mute_rank", _i), ("clear_slots", _i), ("stamps", _vp), ("phases", _vp), ("grid_out", _vp),
+                ("threads_out", _vp)]
 
 
 class LLOptions(ctypes.Structure):
@@ -151,7 +152,7 @@ def library():
 
 
 _TUNING_FIELDS = ("workgroups_per_rank", "threads", "wave_units", "wave_kernels", "pipeline_lag", "first_wait",
-                  "poll_gap", "mute_rank", "stamps", "phases")
+                  "poll_gap", "mute_rank", "clear_slots", "stamps", "phases")
 
 
 class Options:

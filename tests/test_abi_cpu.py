@@ -234,7 +234,7 @@ def test_options_are_checked_before_any_hip_call():
     for field, value in [("workgroups_per_rank", -1), ("workgroups_per_rank", 5000), ("threads", 100),
                          ("threads", 2048), ("wave_units", 3), ("wave_kernels", 3), ("pipeline_lag", -2),
                          ("pipeline_lag", 65), ("first_wait", 1001), ("poll_gap", -1), ("mute_rank", 8),
-                         ("mute_rank", -2)]:
+                         ("mute_rank", -2), ("clear_slots", -1), ("clear_slots", 3)]:
         assert call(ll.Options(**{field: value})) == ll.LL_ERR_INVALID, (field, value)
     t = ll.Options(mute_rank=1)
     t.t.size = 4
@@ -265,7 +265,7 @@ def test_no_setting_outlives_a_call():
     stride = stride_for(1 << 19, BF16, 8)
     for opt in (ll.Options(flags=ll.LL_OPT_AUTO_SENTINEL), ll.Options(flags=ll.LL_OPT_NO_LINES),
                 ll.Options(flags=3, poll_timeout=5, mute_rank=3, threads=64, workgroups_per_rank=2, wave_units=4,
-                           wave_kernels=1, pipeline_lag=0)):
+                           wave_kernels=1, pipeline_lag=0, clear_slots=2)):
         ll.ll_auto_algo(8192, BF16, 8, 0, opt)
         ll.ll_allreduce_ex(GOOD_BASE, stride, GOOD_OUT, 0, BF16, ll.LL_SUM, 8, 1, 0, 0, opt)  # count 0: no launch
     assert [ll.ll_auto_algo(n, BF16, p) for p in (2, 4, 8) for n in (4096, 8192, 1 << 19, 1 << 24)] == defaults
