@@ -459,11 +459,14 @@ KArgs base_args(void *sym_base, size_t rank_stride, void *out, uint32_t epoch) {
 ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
   const uint64_t KiB = 1024, MiB = 1024 * 1024;
   // the line two-shot with one wave per peer at every size up to the
-  // maximum, except above 8 MiB at 6 ranks and 16 MiB at 5, where the
-  // one-lane line two-shot is faster (measured at 8-64 MiB, binary32)
-  const uint64_t line_waves_max = P == 6 ? 8 * MiB : (P == 5 ? 16 * MiB : L::kMaxInputBytes);
+  // maximum, except above 16 MiB at 5-6 ranks, where the one-lane line
+  // two-shot is faster (measured at 8-64 MiB, binary32)
+  const uint64_t line_waves_max = (P == 5 || P == 6) ? 16 * MiB : L::kMaxInputBytes;
   auto large = [&]() { return in_bytes <= line_waves_max ? LL_ALGO_TWOSHOT_LINE_WAVES : LL_ALGO_TWOSHOT_LINE; };
-  if (sentinel_ok) {
+  // With sentinel mode allowed, messages of at most 8 KiB at 3 or more ranks
+  // still take the 8-byte one-shot (whose slots are cleared after reading),
+  // which is as fast or faster there: flags win for the smallest messages.
+  if (sentinel_ok && (P == 2 || in_bytes > 8 * KiB)) {
     uint64_t one_max, two_max;  // one-shot, then two-shot, sentinel units with one wave per peer
     if (P <= 3) {
       one_max = 1 * MiB;
@@ -494,16 +497,13 @@ ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
   uint64_t one8_max, line_max;  // one-shot 8-byte packets, then lines, one wave per peer
   if (P == 3) {
     one8_max = 128 * KiB;
-    line_max = 512 * KiB;
+    line_max = 1 * MiB;
   } else if (P == 4) {
     one8_max = 64 * KiB;
     line_max = 256 * KiB;
-  } else if (P <= 6) {
-    one8_max = 16 * KiB;
-    line_max = 128 * KiB;
   } else {
-    one8_max = 8 * KiB;
-    line_max = 64 * KiB;
+    one8_max = 16 * KiB;
+    line_max = P == 8 ? 64 * KiB : 128 * KiB;
   }
   if (in_bytes <= one8_max) return LL_ALGO_ONESHOT_WAVES;
   if (in_bytes <= line_max) return LL_ALGO_ONESHOT_LINE_WAVES;

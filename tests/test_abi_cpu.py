@@ -269,7 +269,7 @@ def test_no_setting_outlives_a_call():
         ll.ll_auto_algo(8192, BF16, 8, 0, opt)
         ll.ll_allreduce_ex(GOOD_BASE, stride, GOOD_OUT, 0, BF16, ll.LL_SUM, 8, 1, 0, 0, opt)  # count 0: no launch
     assert [ll.ll_auto_algo(n, BF16, p) for p in (2, 4, 8) for n in (4096, 8192, 1 << 19, 1 << 24)] == defaults
-    assert ll.ll_auto_algo(8192, BF16, 8) == (ll.LL_OK, A["oneshot_line_waves"])
+    assert ll.ll_auto_algo(8192, BF16, 8) == (ll.LL_OK, A["oneshot_waves"])
 
 
 def test_strerror_covers_every_code():
@@ -316,7 +316,7 @@ def test_auto_algo_choices():
     A = ll.ALGOS
     f32, bf16 = ll.LL_F32, ll.LL_BF16
     assert ll.ll_auto_algo(4096, bf16, 8) == (ll.LL_OK, A["oneshot_waves"])            # 8 KiB
-    assert ll.ll_auto_algo(8192, bf16, 8) == (ll.LL_OK, A["oneshot_line_waves"])       # C2, 16 KiB
+    assert ll.ll_auto_algo(8192, bf16, 8) == (ll.LL_OK, A["oneshot_waves"])            # C2, 16 KiB
     assert ll.ll_auto_algo(64 * 8192, bf16, 8) == (ll.LL_OK, A["twoshot_line_waves"])  # C3, 1 MiB
     assert ll.ll_auto_algo(16 << 20, f32, 8) == (ll.LL_OK, A["twoshot_line_waves"])    # C4, 64 MiB
     assert ll.ll_auto_algo(1024, f32, 4) == (ll.LL_OK, A["oneshot_waves"])             # C1
@@ -325,6 +325,8 @@ def test_auto_algo_choices():
     assert ll.ll_auto_algo(64 * 8192, bf16, 8, 0, sent) == (ll.LL_OK, A["twoshot_sentinel_waves"])
     assert ll.ll_auto_algo(16 << 20, f32, 8, 0, sent) == (ll.LL_OK, A["twoshot_line_waves"])
     assert ll.ll_auto_algo(16 << 20, f32, 6) == (ll.LL_OK, A["twoshot_line"])          # 64 MiB, 6 ranks
+    assert ll.ll_auto_algo(2048, bf16, 8, 0, sent) == (ll.LL_OK, A["oneshot_waves"])     # 4 KiB: flags win
+    assert ll.ll_auto_algo(2048, bf16, 2, 0, sent) == (ll.LL_OK, A["oneshot_sentinel_waves"])
     assert ll.ll_auto_algo(4 << 20, f32, 5) == (ll.LL_OK, A["twoshot_line_waves"])     # 16 MiB, 5 ranks
     assert ll.ll_auto_algo(8 << 20, f32, 5) == (ll.LL_OK, A["twoshot_line"])           # 32 MiB, 5 ranks
     # measured crossovers away from the configurations' sizes
@@ -334,7 +336,8 @@ def test_auto_algo_choices():
     assert ll.ll_auto_algo(1 << 20, bf16, 8, 0, sent) == (ll.LL_OK, A["twoshot_line_waves"])  # 2 MiB
     assert ll.ll_auto_algo(1 << 17, bf16, 3) == (ll.LL_OK, A["oneshot_line_waves"])          # 256 KiB
     assert ll.ll_auto_algo(4 << 20, bf16, 6) == (ll.LL_OK, A["twoshot_line_waves"])          # 8 MiB
-    assert ll.ll_auto_algo(8 << 20, bf16, 6) == (ll.LL_OK, A["twoshot_line"])                # 16 MiB
+    assert ll.ll_auto_algo(8 << 20, bf16, 6) == (ll.LL_OK, A["twoshot_line_waves"])          # 16 MiB
+    assert ll.ll_auto_algo(16 << 20, bf16, 6) == (ll.LL_OK, A["twoshot_line"])               # 32 MiB
     assert ll.ll_auto_algo(8 << 20, bf16, 8) == (ll.LL_OK, A["twoshot_line_waves"])          # 16 MiB
     assert ll.ll_auto_algo(64 << 20, bf16, 7) == (ll.LL_OK, A["twoshot_line_waves"])         # 128 MiB
     assert ll.ll_auto_algo(1 << 19, bf16, 2, 0, sent) == (ll.LL_OK, A["oneshot_sentinel_waves"])
