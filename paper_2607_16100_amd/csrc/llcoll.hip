@@ -291,9 +291,12 @@ int wave_units_log2(const Plan &pl, int wpr) {
 // larger of input and output) x (P - 1) x (exchanges: 2 for the two-shot
 // AllReduce, 1 for a stand-alone ReduceScatter or AllGather): measured at
 // 2, 4 and 8 ranks for the AllReduce (1 / 2 / 8 MiB) and at 4 and 8 ranks
-// for RS / AG (C5 shapes up to b = 512).  So: on for the one-shot wave
-// kernels, and for the two-shot and stand-alone RS / AG wave kernels below
-// that crossover.  The one-lane kernels never clear.
+// for RS / AG (C5 shapes up to b = 512).  A call of several iterations
+// must also wait at every iteration boundary for its clearing stores to be
+// acknowledged, which costs more than clearing saves (32 MiB in 1 MiB
+// iterations at 8 ranks: 339 -> 433 us).  So: on for the one-shot wave
+// kernels, and for single-iteration two-shot and stand-alone RS / AG wave
+// calls below that crossover.  The one-lane kernels never clear.
 constexpr uint64_t kClearMaxBytes = 16ull << 20;
 
 uint32_t clear_slots(const Plan &pl) {
@@ -301,6 +304,7 @@ uint32_t clear_slots(const Plan &pl) {
                      pl.kind == K_AG_WAVES;
   if (!waves || pl.proto == PR_SENT || pl.o.clear_slots == 2) return 0;
   if (pl.o.clear_slots == 1 || pl.kind == K_ONESHOT_WAVES) return 1;
+  if (pl.a.iters > 1) return 0;
   const uint64_t es = pl.dt == LL_BF16 ? 2 : 4;
   const uint64_t n = (uint64_t)(pl.a.iters > 1 ? pl.a.iter_n : pl.a.n);
   // AllReduce: n elements in and out; ReduceScatter: P*n in; AllGather: P*n out

@@ -829,13 +829,14 @@ def test_rs_ag_wave_kernels_launch_shapes_and_timeouts(proto):
 
 
 # ------------------------------------------------ fallback off line packets
-@pytest.mark.parametrize("p,n,dtype,sized_for", [(8, 8192, "bf16", "auto"), (8, 64 * 8192, "bf16", "auto"),
+@pytest.mark.parametrize("p,n,dtype,sized_for", [(8, 4 * 8192, "bf16", "auto"), (8, 64 * 8192, "bf16", "auto"),
                                                  (4, 7168 * 16, "bf16", "auto"),
                                                  (8, 16 << 20, "f32", "twoshot")])
 def test_no_lines_fallback_parity(p, n, dtype, sized_for):
     """LL_OPT_NO_LINES at the sizes where AUTO otherwise runs 128-byte lines
-    (the 16 KiB line one-shot, the 1 MiB line two-shot with one wave per
-    peer, the 64 MiB line two-shot): AUTO takes the 8-byte-packet algorithm
+    (the 64 KiB line one-shot at 8 ranks, the 224 KiB line one-shot at 4,
+    the 1 MiB line two-shot with one wave per peer, the 64 MiB line
+    two-shot): AUTO takes the 8-byte-packet algorithm
     of the same shape, whose correctness rests on the 8-byte atomicity the
     memory model guarantees, and the result is the oracle's, bit for bit.  The
     64 MiB case runs on a region sized for 8-byte packets only."""
