@@ -274,13 +274,18 @@ __device__ __forceinline__ u32x4 clear_tail(u32x4 v, uint32_t w0, uint32_t nelem
 }
 
 // The matching store of NW words at word w0, for a stream whose byte length
-// is a multiple of 4 (so that no word is partly past the end); streaming hint.
-template <int NW>
+// is a multiple of 4 (so that no word is partly past the end); with the
+// streaming hint unless NT is false.  Tiny outputs of several ranks share
+// cache lines (the P outputs lie back to back), and there streaming stores
+// from several XCDs into one line cost up to 0.8 us a call (8 bytes per rank
+// at 8 ranks); plain stores do not.
+template <int NW, bool NT = true>
 __device__ __forceinline__ void store_words_rs(rsrc_t rs, uint32_t w0, u32x4 v) {
+  constexpr int kPolicy = NT ? kNT : 0;
   if constexpr (NW == 2) {
-    __builtin_amdgcn_raw_buffer_store_b64(u32x2{v.x, v.y}, rs, (int)(w0 * 4), 0, kNT);
+    __builtin_amdgcn_raw_buffer_store_b64(u32x2{v.x, v.y}, rs, (int)(w0 * 4), 0, kPolicy);
   } else {
-    __builtin_amdgcn_raw_buffer_store_b128(v, rs, (int)(w0 * 4), 0, kNT);
+    __builtin_amdgcn_raw_buffer_store_b128(v, rs, (int)(w0 * 4), 0, kPolicy);
   }
 }
 

@@ -682,8 +682,9 @@ __global__ __launch_bounds__(512) void k_oneshot_tile(KArgs ka) {
       }
       o[j] = Elem<DT>::narrow(acc);
     }
-    // al4: nb is a whole number of words, so no stored word is partly past the end
-    store_words_rs<NW>(make_rsrc(a.out + (uint64_t)r * nb, nb), u * NW, u32x4{o[0], o[1], o[2], o[3]});
+    // al4: nb is a whole number of words, so no stored word is partly past the end;
+    // plain stores (the outputs of tiny calls share cache lines across ranks)
+    store_words_rs<NW, false>(make_rsrc(a.out + (uint64_t)r * nb, nb), u * NW, u32x4{o[0], o[1], o[2], o[3]});
   }
   stamp_end(a, t_start);
 }
