@@ -26,6 +26,7 @@ from __future__ import annotations
 
 import argparse
 import hashlib
+import re
 import json
 import os
 import sys
@@ -45,14 +46,23 @@ def log(msg: str) -> None:
     print(msg, file=sys.stderr, flush=True)
 
 
+def _code_only(text: str) -> str:
+    """C++ source without its comments and blank lines (string literals in
+    these headers hold no comment markers)."""
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    return "\n".join(line.rstrip() for line in text.splitlines() if line.strip())
+
+
 def kernel_source_hash() -> str:
-    """Hash of the device code (kernels, primitives, slot layout)."""
+    """Hash of the device code (kernels, primitives, slot layout), comments
+    left out: a counter summary stays valid across comment edits."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2607_16100_amd", "csrc")
     for name in ("ll_device.hpp", "ll_kernels.hpp", "ll_layout.hpp", "ll_iter.hpp"):
-        with open(os.path.join(csrc, name), "rb") as f:
+        with open(os.path.join(csrc, name), encoding="utf-8") as f:
             h.update(name.encode())
-            h.update(f.read())
+            h.update(_code_only(f.read()).encode())
     return h.hexdigest()[:16]
 
 

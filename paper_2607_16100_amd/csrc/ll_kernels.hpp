@@ -888,7 +888,10 @@ __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(LLCOLL_TWO
 // its lanes' reduced words.  AllGather: wave q != r sends the reduced tile (for
 // Mode 2: the own input) to peer q and polls the tile of chunk q that peer q
 // sends back, and stores it; wave r stores the own chunk.  As in the one-shot
-// wave kernel, a wave's polls never wait for more than its own U stores.
+// wave kernel, a wave's polls wait for no stores but its own: those of this
+// tile and, when the workgroup has another tile in the iteration, that
+// tile's ReduceScatter packets, which go out ahead.  Readers clear the slots
+// they have read when the call asks for it (KArgs::clear).
 //
 // Chunks: Mode 0 cuts the n-element input into chunks of a.chunk elements
 // (the last ones may be short); Mode 1 takes P chunks of a.n elements;
@@ -1034,7 +1037,8 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
   };
 
   // Poll U units of slot `src` (this rank's slice) from peer q; sentinel
-  // units are given back to the sentinel once read.  The loop runs while any
+  // units are given back to the sentinel once read, flagged units set to zero
+  // when the call clears slots.  The loop runs while any
   // lane of the wave still waits (a wave vote ends it) and re-loads every
   // unit each round.
   auto poll_peer = [&](char *src, uint32_t tile, u32x4 *v) {
