@@ -1049,7 +1049,6 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
       v[k] = u32x4{0u, 0u, 0u, 0u};
       pend |= ((uint32_t)WU::unit(tile, k, lane) < units ? 1u : 0u) << k;
     }
-    const uint32_t want = pend;
     idle64(a.first_wait);
     uint32_t spins = 0;
     while (true) {
@@ -1074,8 +1073,10 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
     if (ResetsSlots<Pr>::value || a.clear != 0) {
       const uint32_t fill = ResetsSlots<Pr>::value ? ProtoSent::kSentinel : 0u;
 #pragma unroll
-      for (int k = 0; k < U; ++k)
-        if (want & (1u << k)) st_pkt(rs, WU::off(WU::unit(tile, k, lane), lane), u32x4{fill, fill, fill, fill});
+      for (int k = 0; k < U; ++k) {
+        const uint32_t u = (uint32_t)WU::unit(tile, k, lane);
+        if (u < units) st_pkt(rs, WU::off(u, lane), u32x4{fill, fill, fill, fill});
+      }
     }
   };
 
@@ -1176,14 +1177,18 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
       // own-rank wave stores the rank's own result
       if constexpr (kAG) {
         if (!(Mode == 2 && sent_already)) store_units(slot_out + area + ag_off, tile, res);
+        // one output store site for both kinds of wave (chunk q; q == r:
+        // the own result): the kernel is shorter, and measured faster at
+        // every size, than with an inlined store_out in each branch
+        u32x4 v[U];
         if (q == r) {
-          store_out(out_chunk(r), chunk_len(r), tile, res);
+#pragma unroll
+          for (int k = 0; k < U; ++k) v[k] = res[k];
         } else {
-          u32x4 v[U];
           poll_peer(slot_in + area + ag_off, tile, v);
           LL_TW_PHASE(3, now_ticks() + (v[0].x & 0u));
-          store_out(out_chunk(q), chunk_len(q), tile, v);
         }
+        store_out(out_chunk(q), chunk_len(q), tile, v);
       } else {
         if (q == r) store_out(out_chunk(r), chunk_len(r), tile, res);
       }
