@@ -83,6 +83,14 @@ void fill(Table *t) {
   t->tile[0][1][P] = k_oneshot_tile<ProtoLL, 1, P>;
   t->tile[1][0][P] = k_oneshot_tile<ProtoSent, 0, P>;
   t->tile[1][1][P] = k_oneshot_tile<ProtoSent, 1, P>;
+  t->tile[2][0][P] = k_oneshot_line_tile<0, P>;
+  t->tile[2][1][P] = k_oneshot_line_tile<1, P>;
+  t->ttile[0][0][P] = k_twoshot_tile<ProtoLL, 0, P>;
+  t->ttile[0][1][P] = k_twoshot_tile<ProtoLL, 1, P>;
+  t->ttile[1][0][P] = k_twoshot_tile<ProtoSent, 0, P>;
+  t->ttile[1][1][P] = k_twoshot_tile<ProtoSent, 1, P>;
+  t->ttile[2][0][P] = k_twoshot_tile<ProtoLine, 0, P>;
+  t->ttile[2][1][P] = k_twoshot_tile<ProtoLine, 1, P>;
   fill_twaves<0, P>(t);
   fill_twaves<1, P>(t);
   fill_twaves<2, P>(t);

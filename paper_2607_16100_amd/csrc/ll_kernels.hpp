@@ -688,6 +688,128 @@ __global__ __launch_bounds__(512) void k_oneshot_tile(KArgs ka) {
   }
   stamp_end(a, t_start);
 }
+
+// One-shot AllReduce with 128-byte line packets, one wave per peer and one
+// line unit per workgroup, every stream 4-byte aligned: the straight-line
+// counterpart of k_oneshot_waves<ProtoLine, DT, P, 1> for calls whose units
+// are all resident at once, with no multi-tile loop and no element-wise
+// fallback for unaligned streams (as for k_oneshot_tile, the instructions a
+// call runs are paid for in latency).
+//
+// Workgroup (r, w) serves rank r and line unit w (payload words 240w ..
+// 240w + 239 of every input).  Wave q loads the unit (the data lanes 4
+// words each, the extra lanes the displaced words after the load), stores it
+// as one unit of line packets to slot (q <- r) of peer q (the own-rank wave
+// and a muted rank at an offset the resource discards), polls slot (r <- q)
+// until both flags of every 128-byte line carry the epoch, and stages the
+// payload in packet order, widened to binary32, in LDS row q.  After one
+// barrier the ordered sum over the P rows is formed and rounded once: from 4
+// ranks up, thread t < 240 takes payload word t from the lane and slot that
+// carry it and stores it (4 bytes); with fewer threads than words the
+// own-rank wave sums its lanes' words, moves the displaced words back (each
+// flag lane takes its last word from an extra lane) and stores 16 bytes per
+// data lane.
+template <int DT, int P>
+__global__ __launch_bounds__(512) void k_oneshot_line_tile(KArgs ka) {
+  const KArgs a = pin_args(ka);
+  const uint64_t t_start = stamp_start(a);
+  constexpr int E = Elem<DT>::kBytes;
+  constexpr int K = Elem<DT>::kPerWord;
+  constexpr int EPL = 4 * K;  // elements per lane
+  __shared__ float stage[P][64 * EPL];
+  const uint32_t r = blockIdx.x % P;
+  const uint32_t w = blockIdx.x / P;
+  const uint32_t q = (uint32_t)uniform_u32(threadIdx.x >> 6);
+  const int lane = (int)(threadIdx.x & 63);
+  const uint32_t nb = (uint32_t)(a.n * E);  // input bytes per rank (< 256 MiB)
+  const uint32_t w0 = ProtoLine::first_word(w, lane);
+  const rsrc_t in_rs = make_rsrc(a.in + (uint64_t)r * a.in_stride, nb);
+  u32x4 x = load_words_rs<4>(in_rs, w0);
+  constexpr uint32_t kNowhere = 0xFFFFFFF0u;
+  const uint32_t slot = (uint32_t)a.slot;
+  const uint32_t off = w * 1024u + (uint32_t)lane * 16u;
+  const bool publish = q != r && w < (uint32_t)a.units && (int)r != a.mute;
+  const rsrc_t rd = make_rsrc(a.sym + a.area + (uint64_t)q * a.stride + (r - (r > q ? 1u : 0u)) * slot, slot);
+  x = ProtoLine::finish_load(x, lane);
+  st_pkt(rd, publish ? off : kNowhere, ProtoLine::pack(x, a.epoch, lane));
+  const int wv = (int)q;  // diagnostics, as in k_oneshot_waves
+  const uint32_t tile = w;
+  LL_WAVE_PHASE(0, now_ticks() + (x.x & 0u));
+  WaitBudget budget(a.timeout, a.status);
+  u32x4 v = x;
+  if (q != r) {
+    const rsrc_t rs = make_rsrc(a.sym + a.area + (uint64_t)r * a.stride + (q - (q > r ? 1u : 0u)) * slot, slot);
+    bool pend = w < (uint32_t)a.units;
+    uint32_t spins = 0;
+    while (true) {
+      compiler_fence();
+      const u32x4 pk = ld_pkt(rs, off);
+      // every lane of the wave runs the readiness check: it reads its quad's
+      // flag lane
+      const bool ready = ProtoLine::ready(pk, a.epoch);
+      if (pend && ready) {
+        v = ProtoLine::unpack(pk, lane);
+        pend = false;
+      }
+      if (__builtin_amdgcn_ballot_w64(pend) == 0) break;
+      if ((++spins & 15) == 0 && budget.expired()) {
+        if (pend) budget.report((int)r, 1u << q, a.epoch);
+        break;
+      }
+    }
+    if (a.clear != 0 && w < (uint32_t)a.units) st_pkt(rs, off, u32x4{0u, 0u, 0u, 0u});
+  }
+  LL_WAVE_PHASE(1, now_ticks() + (v.x & 0u));
+  {
+    const uint32_t vw[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float f[K];
+      Elem<DT>::widen(vw[j], f);
+#pragma unroll
+      for (int e = 0; e < K; ++e) stage[q][lane * EPL + j * K + e] = f[e];
+    }
+  }
+  lds_barrier();
+  LL_WAVE_PHASE(2, now_ticks());
+  if constexpr (64 * P >= 240) {
+    const int t = (int)threadIdx.x;
+    if (t < 240) {
+      int sl, sj;
+      ProtoLine::slot_of_word(t, &sl, &sj);
+      const int at = sl * EPL + sj * K;
+      float acc[K];
+#pragma unroll
+      for (int e = 0; e < K; ++e) acc[e] = stage[0][at + e];
+#pragma unroll
+      for (int p = 1; p < P; ++p) {
+#pragma unroll
+        for (int e = 0; e < K; ++e) acc[e] = acc[e] + stage[p][at + e];
+      }
+      // plain stores, as in k_oneshot_tile; a word past the end is discarded
+      __builtin_amdgcn_raw_buffer_store_b32(Elem<DT>::narrow(acc), make_rsrc(a.out + (uint64_t)r * nb, nb),
+                                            (int)((240u * w + (uint32_t)t) * 4u), 0, 0);
+    }
+  } else if (q == r) {
+    uint32_t o[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float acc[K];
+#pragma unroll
+      for (int e = 0; e < K; ++e) acc[e] = stage[0][lane * EPL + j * K + e];
+#pragma unroll
+      for (int p = 1; p < P; ++p) {
+#pragma unroll
+        for (int e = 0; e < K; ++e) acc[e] = acc[e] + stage[p][lane * EPL + j * K + e];
+      }
+      o[j] = Elem<DT>::narrow(acc);
+    }
+    // plain stores, as in k_oneshot_tile; the extra lanes store nothing
+    const u32x4 ow = ProtoLine::start_store(u32x4{o[0], o[1], o[2], o[3]}, lane);
+    store_words_rs<4, false>(make_rsrc(a.out + (uint64_t)r * nb, nb), w0, ow);
+  }
+  stamp_end(a, t_start);
+}
 #undef LL_WAVE_PHASE
 
 // ---------------------------------------------------------------------------
@@ -1201,6 +1323,143 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
   stamp_end(a, t_start);
 }
 #undef LL_TW_PHASE
+
+// Two-shot AllReduce, one wave per peer, one tile per workgroup, one unit per
+// lane (a line unit, or 64 one-lane units), one iteration, every stream
+// 4-byte aligned: the straight-line counterpart of k_twoshot_waves<Pr, DT,
+// P, 1, 0> for calls whose tiles are all resident at once.  It carries no
+// tile loop, no tile sent ahead, no iteration and no element-wise fallback
+// for unaligned streams, which shortens what every workgroup runs (the
+// instructions of a latency-bound call are paid for in its latency, see
+// k_oneshot_tile).
+//
+// Workgroup (r, w) serves rank r and tile w of every chunk.  ReduceScatter:
+// wave q loads tile w of chunk q of rank r's input and sends it to peer q
+// (the own-rank wave keeps its own chunk's tile); every other wave polls
+// what peer q sent for chunk r, and each stages its row in LDS.  After a
+// barrier the workgroup forms the ordered sum word by word (binary32 in
+// ascending rank order, one rounding) into a reduced row.  AllGather: wave q
+// sends the reduced tile to peer q and polls the tile of chunk q that peer q
+// sends back; every wave stores its chunk's tile of the output.
+template <class Pr, int DT, int P>
+__global__ __launch_bounds__(512) void k_twoshot_tile(KArgs ka) {
+  const KArgs a = pin_args(ka);
+  const uint64_t t_start = stamp_start(a);
+  constexpr int E = Elem<DT>::kBytes;
+  constexpr int K = Elem<DT>::kPerWord;
+  using WU = WaveUnits<Pr, 1>;
+  constexpr int WPU = Pr::kMaxWords;          // payload words per lane
+  constexpr uint32_t kNowhere = 0xFFFFFFF0u;  // past every slot: the buffer resource discards the access
+  __shared__ u32x4 stage[P][64];
+  __shared__ u32x4 red[64];
+  const uint32_t r = blockIdx.x % P;
+  const uint32_t w = blockIdx.x / P;
+  const uint32_t q = (uint32_t)uniform_u32(threadIdx.x >> 6);  // this wave's peer (q == r: the own values)
+  const int lane = (int)(threadIdx.x & 63);
+  const int sub = WU::sub(lane);
+  const uint32_t u = (uint32_t)WU::unit(w, 0, lane);
+  const bool have = u < (uint32_t)a.units;
+  // chunks of C elements (a multiple of 16 bytes), the last ones short or
+  // empty; every chunk's byte length is a multiple of 4
+  const uint32_t C = (uint32_t)a.chunk;
+  const uint32_t n = (uint32_t)a.n;
+  auto chunk_bytes = [&](uint32_t c) -> uint32_t {
+    const uint32_t c0 = c * C;
+    return c0 >= n ? 0u : ((n - c0 < C ? n - c0 : C) * (uint32_t)E);
+  };
+  const uint32_t fw = have ? Pr::first_word(u, sub) : kNoWord;
+  u32x4 x = load_words_rs<WPU>(make_rsrc(a.in + (uint64_t)r * a.in_stride + (uint64_t)q * C * E, chunk_bytes(q)), fw);
+  const uint32_t slot = (uint32_t)a.slot;
+  const uint32_t off = have ? WU::off(u, lane) : kNowhere;
+  const bool publish = (int)r != a.mute && q != r;
+  // slot (q <- r) in peer q's slice and slot (r <- q) in this rank's slice;
+  // the AllGather slots follow the P - 1 ReduceScatter slots
+  char *const slot_out = a.sym + a.area + (uint64_t)q * a.stride + (r - (r > q ? 1u : 0u)) * slot;
+  char *const slot_in = a.sym + a.area + (uint64_t)r * a.stride + (q - (q > r ? 1u : 0u)) * slot;
+  const uint64_t ag_off = (uint64_t)(P - 1) * slot;
+  x = Pr::finish_load(x, sub);
+  st_pkt(make_rsrc(slot_out, slot), publish ? off : kNowhere, Pr::pack(x, a.epoch, sub));
+#define LL_TT_PHASE(k, expr)                                            \
+  do {                                                                  \
+    if (LLCOLL_WAVE_PHASES && a.phases != nullptr && lane == 0)         \
+      a.phases[4 * (blockIdx.x * P + q) + (k)] = (expr);                \
+  } while (0)
+  LL_TT_PHASE(0, now_ticks() + (x.x & 0u));
+  WaitBudget budget(a.timeout, a.status);
+  // Poll the unit from peer q in `src` (this rank's slice), then give the
+  // slot back to the sentinel (sentinel units) or to zero (flagged units,
+  // when the call clears slots).  Every lane runs the readiness check (a
+  // line's flag sits in the last lane of each quad).
+  auto poll = [&](char *src) -> u32x4 {
+    const rsrc_t rs = make_rsrc(src, slot);
+    u32x4 v = {0u, 0u, 0u, 0u};
+    bool pend = have;
+    idle64(a.first_wait);
+    uint32_t spins = 0;
+    while (true) {
+      compiler_fence();
+      const u32x4 pk = ld_pkt(rs, off);
+      const bool ok = Pr::ready(pk, a.epoch);
+      if (pend && ok) {
+        v = Pr::unpack(pk, sub);
+        pend = false;
+      }
+      if (__builtin_amdgcn_ballot_w64(pend) == 0) break;
+      if ((++spins & 15) == 0 && budget.expired()) {
+        if (pend) budget.report((int)r, 1u << q, a.epoch);
+        break;
+      }
+      idle64(a.poll_gap);
+    }
+    if (ResetsSlots<Pr>::value || a.clear != 0) {
+      const uint32_t fill = ResetsSlots<Pr>::value ? ProtoSent::kSentinel : 0u;
+      st_pkt(rs, off, u32x4{fill, fill, fill, fill});
+    }
+    return v;
+  };
+  {
+    u32x4 v = x;
+    if (q != r) {
+      v = poll(slot_in);
+      LL_TT_PHASE(1, now_ticks() + (v.x & 0u));
+    }
+    stage[q][lane] = v;
+  }
+  lds_barrier();
+  LL_TT_PHASE(2, now_ticks());
+  // thread t reduces payload words t, t + 64 P, ... of the tile over the P
+  // rows (word j of a lane sits at 4 * lane + j)
+  {
+    const uint32_t *const rows = reinterpret_cast<const uint32_t *>(&stage[0][0]);
+    uint32_t *const red_w = reinterpret_cast<uint32_t *>(&red[0]);
+    for (int i = (int)threadIdx.x; i < 64 * WPU; i += 64 * P) {
+      const int at = (i / WPU) * 4 + i % WPU;
+      float acc[K];
+      Elem<DT>::widen(rows[at], acc);
+#pragma unroll
+      for (int p = 1; p < P; ++p) {
+        float f[K];
+        Elem<DT>::widen(rows[p * 64 * 4 + at], f);
+#pragma unroll
+        for (int e = 0; e < K; ++e) acc[e] = acc[e] + f[e];
+      }
+      red_w[at] = Elem<DT>::narrow(acc);
+    }
+  }
+  lds_barrier();
+  const u32x4 res = red[lane];
+  st_pkt(make_rsrc(slot_out + ag_off, slot), publish ? off : kNowhere, Pr::pack(res, a.epoch, sub));
+  u32x4 o = res;
+  if (q != r) {
+    o = poll(slot_in + ag_off);
+    LL_TT_PHASE(3, now_ticks() + (o.x & 0u));
+  }
+  // the tile of chunk q of rank r's output
+  const uint32_t ob = chunk_bytes(q);
+  store_words_rs<WPU>(make_rsrc(a.out + ((uint64_t)r * n + (uint64_t)q * C) * E, ob), fw, Pr::start_store(o, sub));
+#undef LL_TT_PHASE
+  stamp_end(a, t_start);
+}
 
 // ---------------------------------------------------------------------------
 // Two-shot AllReduce with atomic accumulation: the gfx950 analogue of the

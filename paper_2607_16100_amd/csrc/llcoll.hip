@@ -267,12 +267,54 @@ struct Plan {
 //    64 units than resident workgroups per rank.
 // Elsewhere two units per lane are never more than about 3 % faster and up
 // to 25 % slower.
+// Launch shape of the two-shot AllReduce with one wave per peer, measured on
+// MI355X (bfloat16, P = 2, 4, 6, 8, 128 KiB - 8 MiB per rank, p50 of
+// back-to-back calls).  A workgroup has P waves, so a grid of G workgroups
+// puts G P / CUs waves on a CU, of the 32 a CU holds.
+//  1. The one-tile kernel (k_twoshot_tile: one unit per lane, one tile per
+//     workgroup) is the fastest while its waves per CU stay at most 24 for
+//     lines, 20 for sentinel units and 16 for 8-byte packets (and it needs
+//     one iteration, 4-byte aligned streams, no forced launch shape, and
+//     every tile resident at once).
+//  2. Where the one-tile kernel could run but has too many waves, two units
+//     per lane, in one round of at most 16 waves per CU (two workgroups of 8
+//     waves), beats one unit per lane in more waves.
+//  3. Otherwise the size rules of wave_units_log2.
+// Against the best of the three shapes at every size measured, the rule
+// loses at most 0.44 us (lines at 4 ranks and 1.5 MiB).
+bool twoshot_tile_eligible(const Plan &pl) {
+  return pl.kind == K_TWOSHOT_WAVES && !pl.o.forced_shape() && pl.o.wave_units <= 1 && pl.a.al4 != 0 &&
+         (pl.a.in == nullptr || pl.a.in_al4 != 0) && pl.a.iters <= 1;
+}
+
+bool twoshot_tile_ok(const Plan &pl, int wpr, kernel_fn *tf, int64_t *tiles) {
+  if (!twoshot_tile_eligible(pl)) return false;
+  kernel_fn f = table().ttile[wpr][pl.dt][pl.P];
+  int cap = 0;
+  DevInfo d;
+  if (f == nullptr || resident_grid(f, 64 * pl.P, &cap) != LL_OK || device_info(&d) != LL_OK) return false;
+  const int64_t t = pl.proto == PR_LINE ? pl.units : (pl.units + 63) / 64;
+  const int64_t max_waves_per_cu = pl.proto == PR_LINE ? 24 : (pl.proto == PR_SENT ? 20 : 16);
+  if (t > cap / pl.P || t * pl.P * pl.P > max_waves_per_cu * d.cus) return false;
+  *tf = f;
+  *tiles = t;
+  return true;
+}
+
 int wave_units_log2(const Plan &pl, int wpr) {
   const int forced = pl.o.wave_units;
   if (forced == 1) return 0;
   if (forced == 2) return 1;
   if (forced == 4) return 2;
   if (pl.kind != K_TWOSHOT_WAVES) return 0;
+  kernel_fn tf = nullptr;
+  int64_t tiles = 0;
+  if (twoshot_tile_ok(pl, wpr, &tf, &tiles)) return 0;
+  if (twoshot_tile_eligible(pl)) {
+    DevInfo d;
+    const int64_t blocks = pl.proto == PR_LINE ? pl.units : (pl.units + 63) / 64;
+    if (device_info(&d) == LL_OK && (blocks + 1) / 2 * pl.P * pl.P <= 16 * (int64_t)d.cus) return 1;
+  }
   if (pl.proto == PR_LINE) return pl.units * pl.P <= 1536 ? 0 : (pl.units * pl.P <= 8192 ? 1 : 2);
   int cap = 0;
   if (resident_grid(table().twaves[0][0][wpr][pl.dt][pl.P], 64 * pl.P, &cap) != LL_OK) return 1;
@@ -330,17 +372,24 @@ int launch(const Plan &pl, void *stream) {
     fn = table().k[pl.proto][pl.dt][pl.P][pl.kind];
   }
   if (fn == nullptr) return LL_ERR_UNSUPPORTED;
-  // The latency-bound one-shot: one tile of 64 one-lane units per workgroup,
-  // every stream 4-byte aligned, all tiles resident at once, no forced
-  // launch shape -> the straight-line one-tile kernel.
-  if (pl.kind == K_ONESHOT_WAVES && wlog == 0 && pl.proto != PR_LINE && !pl.o.forced_shape() && pl.a.al4 != 0 &&
+  // The latency-bound one-shot: one tile per workgroup (64 one-lane units,
+  // or one line unit), every stream 4-byte aligned, all tiles resident at
+  // once, no forced launch shape -> the straight-line one-tile kernels.
+  if (pl.kind == K_ONESHOT_WAVES && wlog == 0 && !pl.o.forced_shape() && pl.a.al4 != 0 &&
       (pl.a.in == nullptr || pl.a.in_al4 != 0) && pl.a.iters <= 1) {
-    kernel_fn tf = table().tile[pl.proto == PR_SENT ? 1 : 0][pl.dt][pl.P];
+    kernel_fn tf = table().tile[pl.proto == PR_SENT ? 1 : (pl.proto == PR_LINE ? 2 : 0)][pl.dt][pl.P];
     int cap = 0;
     const int rc = resident_grid(tf, 64 * pl.P, &cap);
     if (rc != LL_OK) return rc;
-    const int64_t tiles = (pl.units + 63) / 64;
+    const int64_t tiles = pl.proto == PR_LINE ? pl.units : (pl.units + 63) / 64;
     if (tf != nullptr && tiles <= cap / pl.P) return launch_kernel(tf, pl, (int)tiles, 64 * pl.P, stream);
+  }
+  // The same for the two-shot AllReduce with one unit per lane and one
+  // iteration: the straight-line two-shot kernel.
+  if (wlog == 0) {
+    kernel_fn tf = nullptr;
+    int64_t tiles = 0;
+    if (twoshot_tile_ok(pl, wpr, &tf, &tiles)) return launch_kernel(tf, pl, (int)tiles, 64 * pl.P, stream);
   }
   int threads = pl.o.threads;
   if (threads == 0) threads = 256;
@@ -473,13 +522,13 @@ ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
   if (sentinel_ok && (P == 2 || in_bytes > 8 * KiB)) {
     uint64_t one_max, two_max;  // one-shot, then two-shot, sentinel units with one wave per peer
     if (P <= 3) {
-      one_max = 1 * MiB;
+      one_max = (P == 2 ? 1024 : 512) * KiB;
       two_max = (P == 2 ? 8 : 4) * MiB;
     } else if (P <= 5) {
-      one_max = 256 * KiB;
+      one_max = (P == 4 ? 256 : 128) * KiB;
       two_max = 2 * MiB;
     } else if (P <= 7) {
-      one_max = 128 * KiB;
+      one_max = (P == 6 ? 128 : 64) * KiB;
       two_max = (P == 6 ? 2 : 1) * MiB;
     } else {
       one_max = 64 * KiB;
@@ -492,22 +541,22 @@ ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
   }
   if (P == 2) {
     if (in_bytes <= 512 * KiB) return LL_ALGO_ONESHOT_WAVES;
-    if (in_bytes <= 1 * MiB) return LL_ALGO_ONESHOT_LINE_WAVES;
-    if (in_bytes <= 2 * MiB) return LL_ALGO_ONESHOT_LINE;
+    if (in_bytes <= 2 * MiB) return LL_ALGO_ONESHOT_LINE_WAVES;
     return large();
   }
-  // the line one-shot sums a word per thread from 4 ranks up (64*P threads
-  // for 240 words), which makes it the faster one-shot from 16-128 KiB
-  uint64_t one8_max, line_max;  // one-shot 8-byte packets, then lines, one wave per peer
+  // one-shot with 8-byte packets, then with lines, then the line two-shot
+  // (whose one-tile kernel takes the two-shot below the one-shot from
+  // 32-512 KiB, by rank count)
+  uint64_t one8_max, line_max;
   if (P == 3) {
-    one8_max = 128 * KiB;
-    line_max = 1 * MiB;
-  } else if (P == 4) {
     one8_max = 64 * KiB;
-    line_max = 256 * KiB;
+    line_max = 512 * KiB;
+  } else if (P == 4) {
+    one8_max = 32 * KiB;
+    line_max = 128 * KiB;
   } else {
     one8_max = 16 * KiB;
-    line_max = P == 8 ? 64 * KiB : 128 * KiB;
+    line_max = P == 8 ? 32 * KiB : (P == 5 ? 128 * KiB : 64 * KiB);
   }
   if (in_bytes <= one8_max) return LL_ALGO_ONESHOT_WAVES;
   if (in_bytes <= line_max) return LL_ALGO_ONESHOT_LINE_WAVES;

@@ -331,7 +331,12 @@ def test_auto_algo_choices():
     assert ll.ll_auto_algo(8 << 20, f32, 5) == (ll.LL_OK, A["twoshot_line"])           # 32 MiB, 5 ranks
     # measured crossovers away from the configurations' sizes
     assert ll.ll_auto_algo(4 << 20, bf16, 8) == (ll.LL_OK, A["twoshot_line_waves"])           # 8 MiB
-    assert ll.ll_auto_algo(4 * 8192, bf16, 8) == (ll.LL_OK, A["oneshot_line_waves"])         # 64 KiB
+    assert ll.ll_auto_algo(2 * 8192, bf16, 8) == (ll.LL_OK, A["oneshot_line_waves"])         # 32 KiB
+    assert ll.ll_auto_algo(4 * 8192, bf16, 8) == (ll.LL_OK, A["twoshot_line_waves"])         # 64 KiB
+    assert ll.ll_auto_algo(1 << 19, bf16, 2) == (ll.LL_OK, A["oneshot_line_waves"])          # 1 MiB, 2 ranks
+    assert ll.ll_auto_algo(1 << 20, bf16, 2) == (ll.LL_OK, A["oneshot_line_waves"])          # 2 MiB, 2 ranks
+    assert ll.ll_auto_algo(1 << 19, bf16, 3) == (ll.LL_OK, A["twoshot_line_waves"])          # 1 MiB, 3 ranks
+    assert ll.ll_auto_algo(1 << 16, bf16, 7, 0, sent) == (ll.LL_OK, A["twoshot_sentinel_waves"])  # 128 KiB
     assert ll.ll_auto_algo(64 * 8192, bf16, 8) == (ll.LL_OK, A["twoshot_line_waves"])        # 1 MiB
     assert ll.ll_auto_algo(1 << 20, bf16, 8, 0, sent) == (ll.LL_OK, A["twoshot_line_waves"])  # 2 MiB
     assert ll.ll_auto_algo(1 << 17, bf16, 3) == (ll.LL_OK, A["oneshot_line_waves"])          # 256 KiB

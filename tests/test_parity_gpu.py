@@ -105,6 +105,38 @@ def test_allreduce_all_algorithms_ragged(dtype, p):
             assert_bits_equal(run_allreduce(reg, x, algo), want, f"{algo} P={p} {dtype} n={n}")
 
 
+# Element counts around the unit boundaries of the one-tile kernels: a line
+# unit carries 240 words (480 bfloat16 or 240 binary32 elements), a tile of
+# one-lane units 1 KiB of payload (512 or 256 elements); 61440 bfloat16 are
+# 128 line units, the most a launch of 4 workgroups per CU keeps resident at
+# 8 ranks (one more unit takes the multi-tile kernel).
+TILE_N = {"bf16": [2, 478, 480, 482, 958, 960, 1024, 480 * 37 + 2, 61440, 61442],
+          "f32": [1, 239, 240, 241, 256, 257, 240 * 50 + 3, 30720, 30721]}
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("p", [2, 3, 5, 8])
+def test_one_tile_kernels_at_unit_boundaries(dtype, p):
+    """The one-tile kernels, one-shot and two-shot (8-byte packets, sentinel
+    units, lines; the host takes them for 4-byte aligned streams whose tiles
+    are all resident) at counts on both sides of a unit and of the resident
+    limit, with slot clearing forced on and off, two calls per case.  The
+    two-shot splits the counts into P chunks, so its tiles meet ragged chunk
+    ends and, for the smallest counts, empty chunks."""
+    sizes = TILE_N[dtype]
+    reg = SymRegion(p, max(sizes), dtype)
+    reg.init()
+    for n in sizes:
+        for algo in ("oneshot_waves", "oneshot_sentinel_waves", "oneshot_line_waves", "twoshot_waves",
+                     "twoshot_sentinel_waves", "twoshot_line_waves"):
+            for clear in (1, 2):
+                for call in range(2):
+                    x = wl.normal(p, n, dtype, seed=31 * n + call)
+                    say(f"one-tile {algo} P={p} {dtype} n={n} clear={clear} call {call}")
+                    got = run_allreduce(reg, x, algo, opt=opts(clear_slots=clear))
+                    assert_bits_equal(got, oracle.allreduce(x), f"{algo} P={p} {dtype} n={n} clear={clear}")
+
+
 @pytest.mark.parametrize("algo", AR_ALGOS)
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_allreduce_special_values(algo, dtype):
