@@ -53,6 +53,21 @@ void fill_twaves(Table *t) {
   t->twaves[M][2][2][1][P] = k_twoshot_waves<ProtoLine, 1, P, 4, M>;
 }
 
+// One unit per lane for every packet format; two for lines only (with
+// 8-byte packets and sentinel units the multi-tile kernel at two units per
+// lane measured as fast or faster).
+template <int P>
+void fill_ttile(Table *t) {
+  t->ttile[0][0][0][P] = k_twoshot_tile<ProtoLL, 0, P, 1>;
+  t->ttile[0][0][1][P] = k_twoshot_tile<ProtoLL, 1, P, 1>;
+  t->ttile[0][1][0][P] = k_twoshot_tile<ProtoSent, 0, P, 1>;
+  t->ttile[0][1][1][P] = k_twoshot_tile<ProtoSent, 1, P, 1>;
+  t->ttile[0][2][0][P] = k_twoshot_tile<ProtoLine, 0, P, 1>;
+  t->ttile[0][2][1][P] = k_twoshot_tile<ProtoLine, 1, P, 1>;
+  t->ttile[1][2][0][P] = k_twoshot_tile<ProtoLine, 0, P, 2>;
+  t->ttile[1][2][1][P] = k_twoshot_tile<ProtoLine, 1, P, 2>;
+}
+
 template <int P>
 void fill(Table *t) {
   fill_row<ProtoLL, 0, P>(t->k[PR_LL][0][P]);
@@ -85,12 +100,7 @@ void fill(Table *t) {
   t->tile[1][1][P] = k_oneshot_tile<ProtoSent, 1, P>;
   t->tile[2][0][P] = k_oneshot_line_tile<0, P>;
   t->tile[2][1][P] = k_oneshot_line_tile<1, P>;
-  t->ttile[0][0][P] = k_twoshot_tile<ProtoLL, 0, P>;
-  t->ttile[0][1][P] = k_twoshot_tile<ProtoLL, 1, P>;
-  t->ttile[1][0][P] = k_twoshot_tile<ProtoSent, 0, P>;
-  t->ttile[1][1][P] = k_twoshot_tile<ProtoSent, 1, P>;
-  t->ttile[2][0][P] = k_twoshot_tile<ProtoLine, 0, P>;
-  t->ttile[2][1][P] = k_twoshot_tile<ProtoLine, 1, P>;
+  fill_ttile<P>(t);
   fill_twaves<0, P>(t);
   fill_twaves<1, P>(t);
   fill_twaves<2, P>(t);

@@ -1324,13 +1324,13 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
 }
 #undef LL_TW_PHASE
 
-// Two-shot AllReduce, one wave per peer, one tile per workgroup, one unit per
-// lane (a line unit, or 64 one-lane units), one iteration, every stream
-// 4-byte aligned: the straight-line counterpart of k_twoshot_waves<Pr, DT,
-// P, 1, 0> for calls whose tiles are all resident at once.  It carries no
-// tile loop, no tile sent ahead, no iteration and no element-wise fallback
-// for unaligned streams, which shortens what every workgroup runs (the
-// instructions of a latency-bound call are paid for in its latency, see
+// Two-shot AllReduce, one wave per peer, one tile of U units per lane per
+// workgroup (U line units, or 64 U one-lane units), one iteration, every
+// stream 4-byte aligned: the straight-line counterpart of k_twoshot_waves<Pr,
+// DT, P, U, 0> for calls whose tiles are all resident at once.  It carries
+// no tile loop, no tile sent ahead, no iteration and no element-wise
+// fallback for unaligned streams, which shortens what every workgroup runs
+// (the instructions of a latency-bound call are paid for in its latency, see
 // k_oneshot_tile).
 //
 // Workgroup (r, w) serves rank r and tile w of every chunk.  ReduceScatter:
@@ -1341,24 +1341,22 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
 // ascending rank order, one rounding) into a reduced row.  AllGather: wave q
 // sends the reduced tile to peer q and polls the tile of chunk q that peer q
 // sends back; every wave stores its chunk's tile of the output.
-template <class Pr, int DT, int P>
+template <class Pr, int DT, int P, int U>
 __global__ __launch_bounds__(512) void k_twoshot_tile(KArgs ka) {
   const KArgs a = pin_args(ka);
   const uint64_t t_start = stamp_start(a);
   constexpr int E = Elem<DT>::kBytes;
   constexpr int K = Elem<DT>::kPerWord;
-  using WU = WaveUnits<Pr, 1>;
-  constexpr int WPU = Pr::kMaxWords;          // payload words per lane
+  using WU = WaveUnits<Pr, U>;
+  constexpr int WPU = Pr::kMaxWords;          // payload words per lane and unit slot
   constexpr uint32_t kNowhere = 0xFFFFFFF0u;  // past every slot: the buffer resource discards the access
-  __shared__ u32x4 stage[P][64];
-  __shared__ u32x4 red[64];
+  __shared__ u32x4 stage[P][64 * U];
+  __shared__ u32x4 red[64 * U];
   const uint32_t r = blockIdx.x % P;
   const uint32_t w = blockIdx.x / P;
   const uint32_t q = (uint32_t)uniform_u32(threadIdx.x >> 6);  // this wave's peer (q == r: the own values)
   const int lane = (int)(threadIdx.x & 63);
   const int sub = WU::sub(lane);
-  const uint32_t u = (uint32_t)WU::unit(w, 0, lane);
-  const bool have = u < (uint32_t)a.units;
   // chunks of C elements (a multiple of 16 bytes), the last ones short or
   // empty; every chunk's byte length is a multiple of 4
   const uint32_t C = (uint32_t)a.chunk;
@@ -1367,79 +1365,111 @@ __global__ __launch_bounds__(512) void k_twoshot_tile(KArgs ka) {
     const uint32_t c0 = c * C;
     return c0 >= n ? 0u : ((n - c0 < C ? n - c0 : C) * (uint32_t)E);
   };
-  const uint32_t fw = have ? Pr::first_word(u, sub) : kNoWord;
-  u32x4 x = load_words_rs<WPU>(make_rsrc(a.in + (uint64_t)r * a.in_stride + (uint64_t)q * C * E, chunk_bytes(q)), fw);
+  // the lane's unit slots: first payload word and packet offset (past the
+  // end for a unit beyond the chunk)
+  uint32_t fw[U], off[U];
+  uint32_t have = 0;
+#pragma unroll
+  for (int k = 0; k < U; ++k) {
+    const uint32_t u = (uint32_t)WU::unit(w, k, lane);
+    const bool h = u < (uint32_t)a.units;
+    have |= (h ? 1u : 0u) << k;
+    fw[k] = h ? Pr::first_word(u, sub) : kNoWord;
+    off[k] = h ? WU::off(u, lane) : kNowhere;
+  }
+  u32x4 x[U];
+  {
+    const rsrc_t in_rs = make_rsrc(a.in + (uint64_t)r * a.in_stride + (uint64_t)q * C * E, chunk_bytes(q));
+#pragma unroll
+    for (int k = 0; k < U; ++k) x[k] = load_words_rs<WPU>(in_rs, fw[k]);
+  }
   const uint32_t slot = (uint32_t)a.slot;
-  const uint32_t off = have ? WU::off(u, lane) : kNowhere;
   const bool publish = (int)r != a.mute && q != r;
   // slot (q <- r) in peer q's slice and slot (r <- q) in this rank's slice;
   // the AllGather slots follow the P - 1 ReduceScatter slots
   char *const slot_out = a.sym + a.area + (uint64_t)q * a.stride + (r - (r > q ? 1u : 0u)) * slot;
   char *const slot_in = a.sym + a.area + (uint64_t)r * a.stride + (q - (q > r ? 1u : 0u)) * slot;
   const uint64_t ag_off = (uint64_t)(P - 1) * slot;
-  x = Pr::finish_load(x, sub);
-  st_pkt(make_rsrc(slot_out, slot), publish ? off : kNowhere, Pr::pack(x, a.epoch, sub));
+  {
+    const rsrc_t rd = make_rsrc(slot_out, slot);
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      x[k] = Pr::finish_load(x[k], sub);
+      st_pkt(rd, publish ? off[k] : kNowhere, Pr::pack(x[k], a.epoch, sub));
+    }
+  }
 #define LL_TT_PHASE(k, expr)                                            \
   do {                                                                  \
     if (LLCOLL_WAVE_PHASES && a.phases != nullptr && lane == 0)         \
       a.phases[4 * (blockIdx.x * P + q) + (k)] = (expr);                \
   } while (0)
-  LL_TT_PHASE(0, now_ticks() + (x.x & 0u));
+  LL_TT_PHASE(0, now_ticks() + (x[0].x & 0u));
   WaitBudget budget(a.timeout, a.status);
-  // Poll the unit from peer q in `src` (this rank's slice), then give the
-  // slot back to the sentinel (sentinel units) or to zero (flagged units,
+  // Poll the U units from peer q in `src` (this rank's slice), then give the
+  // slots back to the sentinel (sentinel units) or to zero (flagged units,
   // when the call clears slots).  Every lane runs the readiness check (a
   // line's flag sits in the last lane of each quad).
-  auto poll = [&](char *src) -> u32x4 {
+  auto poll = [&](char *src, u32x4 *v) {
     const rsrc_t rs = make_rsrc(src, slot);
-    u32x4 v = {0u, 0u, 0u, 0u};
-    bool pend = have;
+    uint32_t pend = have;
+#pragma unroll
+    for (int k = 0; k < U; ++k) v[k] = u32x4{0u, 0u, 0u, 0u};
     idle64(a.first_wait);
     uint32_t spins = 0;
     while (true) {
       compiler_fence();
-      const u32x4 pk = ld_pkt(rs, off);
-      const bool ok = Pr::ready(pk, a.epoch);
-      if (pend && ok) {
-        v = Pr::unpack(pk, sub);
-        pend = false;
+      u32x4 pk[U];
+#pragma unroll
+      for (int k = 0; k < U; ++k) pk[k] = ld_pkt(rs, off[k]);
+#pragma unroll
+      for (int k = 0; k < U; ++k) {
+        const bool ok = Pr::ready(pk[k], a.epoch);
+        if ((pend & (1u << k)) && ok) {
+          v[k] = Pr::unpack(pk[k], sub);
+          pend &= ~(1u << k);
+        }
       }
-      if (__builtin_amdgcn_ballot_w64(pend) == 0) break;
+      if (__builtin_amdgcn_ballot_w64(pend != 0) == 0) break;
       if ((++spins & 15) == 0 && budget.expired()) {
-        if (pend) budget.report((int)r, 1u << q, a.epoch);
+        if (pend != 0) budget.report((int)r, 1u << q, a.epoch);
         break;
       }
       idle64(a.poll_gap);
     }
     if (ResetsSlots<Pr>::value || a.clear != 0) {
       const uint32_t fill = ResetsSlots<Pr>::value ? ProtoSent::kSentinel : 0u;
-      st_pkt(rs, off, u32x4{fill, fill, fill, fill});
+#pragma unroll
+      for (int k = 0; k < U; ++k) st_pkt(rs, off[k], u32x4{fill, fill, fill, fill});
     }
-    return v;
   };
   {
-    u32x4 v = x;
+    u32x4 v[U];
     if (q != r) {
-      v = poll(slot_in);
-      LL_TT_PHASE(1, now_ticks() + (v.x & 0u));
+      poll(slot_in, v);
+      LL_TT_PHASE(1, now_ticks() + (v[0].x & 0u));
+    } else {
+#pragma unroll
+      for (int k = 0; k < U; ++k) v[k] = x[k];
     }
-    stage[q][lane] = v;
+#pragma unroll
+    for (int k = 0; k < U; ++k) stage[q][k * 64 + lane] = v[k];
   }
   lds_barrier();
   LL_TT_PHASE(2, now_ticks());
   // thread t reduces payload words t, t + 64 P, ... of the tile over the P
-  // rows (word j of a lane sits at 4 * lane + j)
+  // rows (word j of unit slot s sits at 4 * s + j)
   {
+    constexpr int kWords = 64 * U * WPU;
     const uint32_t *const rows = reinterpret_cast<const uint32_t *>(&stage[0][0]);
     uint32_t *const red_w = reinterpret_cast<uint32_t *>(&red[0]);
-    for (int i = (int)threadIdx.x; i < 64 * WPU; i += 64 * P) {
+    for (int i = (int)threadIdx.x; i < kWords; i += 64 * P) {
       const int at = (i / WPU) * 4 + i % WPU;
       float acc[K];
       Elem<DT>::widen(rows[at], acc);
 #pragma unroll
       for (int p = 1; p < P; ++p) {
         float f[K];
-        Elem<DT>::widen(rows[p * 64 * 4 + at], f);
+        Elem<DT>::widen(rows[p * 64 * U * 4 + at], f);
 #pragma unroll
         for (int e = 0; e < K; ++e) acc[e] = acc[e] + f[e];
       }
@@ -1447,16 +1477,26 @@ __global__ __launch_bounds__(512) void k_twoshot_tile(KArgs ka) {
     }
   }
   lds_barrier();
-  const u32x4 res = red[lane];
-  st_pkt(make_rsrc(slot_out + ag_off, slot), publish ? off : kNowhere, Pr::pack(res, a.epoch, sub));
-  u32x4 o = res;
+  u32x4 res[U];
+#pragma unroll
+  for (int k = 0; k < U; ++k) res[k] = red[k * 64 + lane];
+  {
+    const rsrc_t rd = make_rsrc(slot_out + ag_off, slot);
+#pragma unroll
+    for (int k = 0; k < U; ++k) st_pkt(rd, publish ? off[k] : kNowhere, Pr::pack(res[k], a.epoch, sub));
+  }
+  u32x4 o[U];
   if (q != r) {
-    o = poll(slot_in + ag_off);
-    LL_TT_PHASE(3, now_ticks() + (o.x & 0u));
+    poll(slot_in + ag_off, o);
+    LL_TT_PHASE(3, now_ticks() + (o[0].x & 0u));
+  } else {
+#pragma unroll
+    for (int k = 0; k < U; ++k) o[k] = res[k];
   }
   // the tile of chunk q of rank r's output
-  const uint32_t ob = chunk_bytes(q);
-  store_words_rs<WPU>(make_rsrc(a.out + ((uint64_t)r * n + (uint64_t)q * C) * E, ob), fw, Pr::start_store(o, sub));
+  const rsrc_t out_rs = make_rsrc(a.out + ((uint64_t)r * n + (uint64_t)q * C) * E, chunk_bytes(q));
+#pragma unroll
+  for (int k = 0; k < U; ++k) store_words_rs<WPU>(out_rs, fw[k], Pr::start_store(o[k], sub));
 #undef LL_TT_PHASE
   stamp_end(a, t_start);
 }

@@ -280,22 +280,36 @@ struct Plan {
 //     per lane, in one round of at most 16 waves per CU (two workgroups of 8
 //     waves), beats one unit per lane in more waves.
 //  3. Otherwise the size rules of wave_units_log2.
-// Against the best of the three shapes at every size measured, the rule
-// loses at most 0.44 us (lines at 4 ranks and 1.5 MiB).
+// Whenever two units per lane result, lines take the one-tile kernel with
+// two units per lane if its tiles are all resident (8 ranks, 1.5 MiB:
+// 15.19 -> 14.48 us; 4 ranks, 3 MiB: 15.34 -> 13.04 us; 2 ranks, 4 MiB: 8.28
+// -> 7.54 us); 8-byte packets and sentinel units keep the multi-tile kernel,
+// which was as fast or faster for them at 4-8 ranks.  Against the best
+// shape measured (one and two units per lane, one-tile and multi-tile
+// kernels) the rule loses at most 0.3 us at 4-8 ranks; at 2 ranks and
+// 4-8 MiB, where two units per lane in one tile would have been faster for
+// 8-byte packets and sentinel units too, up to 0.8 us.
 bool twoshot_tile_eligible(const Plan &pl) {
-  return pl.kind == K_TWOSHOT_WAVES && !pl.o.forced_shape() && pl.o.wave_units <= 1 && pl.a.al4 != 0 &&
+  return pl.kind == K_TWOSHOT_WAVES && !pl.o.forced_shape() && pl.o.wave_units <= 2 && pl.a.al4 != 0 &&
          (pl.a.in == nullptr || pl.a.in_al4 != 0) && pl.a.iters <= 1;
 }
 
-bool twoshot_tile_ok(const Plan &pl, int wpr, kernel_fn *tf, int64_t *tiles) {
-  if (!twoshot_tile_eligible(pl)) return false;
-  kernel_fn f = table().ttile[wpr][pl.dt][pl.P];
+// The one-tile kernel with 2^lu units per lane, if it can run this call:
+// every tile resident, and (unless the units per lane are forced) within the
+// waves-per-CU limit of rule 1 for one unit per lane.
+bool twoshot_tile_ok(const Plan &pl, int wpr, int lu, kernel_fn *tf, int64_t *tiles) {
+  if (!twoshot_tile_eligible(pl) || lu > 1) return false;
+  kernel_fn f = table().ttile[lu][wpr][pl.dt][pl.P];
   int cap = 0;
   DevInfo d;
   if (f == nullptr || resident_grid(f, 64 * pl.P, &cap) != LL_OK || device_info(&d) != LL_OK) return false;
-  const int64_t t = pl.proto == PR_LINE ? pl.units : (pl.units + 63) / 64;
-  const int64_t max_waves_per_cu = pl.proto == PR_LINE ? 24 : (pl.proto == PR_SENT ? 20 : 16);
-  if (t > cap / pl.P || t * pl.P * pl.P > max_waves_per_cu * d.cus) return false;
+  const int64_t blocks = pl.proto == PR_LINE ? pl.units : (pl.units + 63) / 64;
+  const int64_t t = (blocks + (1 << lu) - 1) >> lu;
+  if (t > cap / pl.P) return false;
+  if (pl.o.wave_units == 0 && lu == 0) {
+    const int64_t max_waves_per_cu = pl.proto == PR_LINE ? 24 : (pl.proto == PR_SENT ? 20 : 16);
+    if (t * pl.P * pl.P > max_waves_per_cu * d.cus) return false;
+  }
   *tf = f;
   *tiles = t;
   return true;
@@ -309,13 +323,13 @@ int wave_units_log2(const Plan &pl, int wpr) {
   if (pl.kind != K_TWOSHOT_WAVES) return 0;
   kernel_fn tf = nullptr;
   int64_t tiles = 0;
-  if (twoshot_tile_ok(pl, wpr, &tf, &tiles)) return 0;
+  if (twoshot_tile_ok(pl, wpr, 0, &tf, &tiles)) return 0;
   if (twoshot_tile_eligible(pl)) {
     DevInfo d;
     const int64_t blocks = pl.proto == PR_LINE ? pl.units : (pl.units + 63) / 64;
     if (device_info(&d) == LL_OK && (blocks + 1) / 2 * pl.P * pl.P <= 16 * (int64_t)d.cus) return 1;
   }
-  if (pl.proto == PR_LINE) return pl.units * pl.P <= 1536 ? 0 : (pl.units * pl.P <= 8192 ? 1 : 2);
+  if (pl.proto == PR_LINE) return pl.units * pl.P <= 1200 ? 0 : (pl.units * pl.P <= 8192 ? 1 : 2);
   int cap = 0;
   if (resident_grid(table().twaves[0][0][wpr][pl.dt][pl.P], 64 * pl.P, &cap) != LL_OK) return 1;
   return (pl.units + 63) / 64 <= cap / pl.P ? 0 : 1;
@@ -384,12 +398,12 @@ int launch(const Plan &pl, void *stream) {
     const int64_t tiles = pl.proto == PR_LINE ? pl.units : (pl.units + 63) / 64;
     if (tf != nullptr && tiles <= cap / pl.P) return launch_kernel(tf, pl, (int)tiles, 64 * pl.P, stream);
   }
-  // The same for the two-shot AllReduce with one unit per lane and one
-  // iteration: the straight-line two-shot kernel.
-  if (wlog == 0) {
+  // The same for the two-shot AllReduce with one or two units per lane and
+  // one iteration: the straight-line two-shot kernel.
+  if (pl.kind == K_TWOSHOT_WAVES) {
     kernel_fn tf = nullptr;
     int64_t tiles = 0;
-    if (twoshot_tile_ok(pl, wpr, &tf, &tiles)) return launch_kernel(tf, pl, (int)tiles, 64 * pl.P, stream);
+    if (twoshot_tile_ok(pl, wpr, wlog, &tf, &tiles)) return launch_kernel(tf, pl, (int)tiles, 64 * pl.P, stream);
   }
   int threads = pl.o.threads;
   if (threads == 0) threads = 256;
