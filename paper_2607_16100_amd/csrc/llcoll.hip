@@ -255,18 +255,6 @@ struct Plan {
   CallOpts o;     // the call's options
 };
 
-// Units per lane (U) of the wave-per-peer kernels, measured at 16 KiB ..
-// 64 MiB per rank and 2 .. 8 ranks.  One unit per lane, except in the
-// two-shot AllReduce once its tiles would need a second round of
-// workgroups, which costs a whole extra exchange:
-//  - lines (a line unit is a whole wave): two units per lane once the P
-//    tiles of a step hold more than 1536 line units, four once they hold
-//    more than 8192 (from about 8 MiB per rank, where the kernel is bound by
-//    bandwidth and fewer, longer waves move the bytes faster);
-//  - 8-byte packets and sentinel units: two once a chunk has more tiles of
-//    64 units than resident workgroups per rank.
-// Elsewhere two units per lane are never more than about 3 % faster and up
-// to 25 % slower.
 // Launch shape of the two-shot AllReduce with one wave per peer, measured on
 // MI355X (bfloat16, P = 2, 4, 6, 8, 128 KiB - 8 MiB per rank, p50 of
 // back-to-back calls).  A workgroup has P waves, so a grid of G workgroups
@@ -315,6 +303,19 @@ bool twoshot_tile_ok(const Plan &pl, int wpr, int lu, kernel_fn *tf, int64_t *ti
   return true;
 }
 
+// Units per lane (U) of the wave-per-peer kernels, measured at 16 KiB ..
+// 64 MiB per rank and 2 .. 8 ranks.  The two-shot AllReduce takes rules 1
+// and 2 above first.  Otherwise one unit per lane, except in the two-shot
+// AllReduce once its tiles would need a second round of workgroups, which
+// costs a whole extra exchange:
+//  - lines (a line unit is a whole wave): two units per lane once the P
+//    tiles of a step hold more than 1200 line units, four once they hold
+//    more than 8192 (from about 8 MiB per rank, where the kernel is bound by
+//    bandwidth and fewer, longer waves move the bytes faster);
+//  - 8-byte packets and sentinel units: two once a chunk has more tiles of
+//    64 units than resident workgroups per rank.
+// Elsewhere two units per lane are never more than about 3 % faster and up
+// to 25 % slower.
 int wave_units_log2(const Plan &pl, int wpr) {
   const int forced = pl.o.wave_units;
   if (forced == 1) return 0;
