@@ -111,6 +111,25 @@ def test_in_place(algo):
         assert_bits_equal(run(reg, x, algo), oracle.allreduce(x), f"in place {algo} call {k}")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("p", [3, 5, 8])
+def test_in_place_one_iteration(dtype, p):
+    """in == out with the whole message in one iteration, where the one-tile
+    kernels run: each wave reads a tile of its chunk's input and later
+    writes the same tile of the output.  Two calls per algorithm, ragged
+    chunk ends."""
+    n = 30_001 if dtype == "f32" else 30_002
+    reg = ScratchRegion(p, n, dtype, iter_bytes=1 << 20, in_place=True)
+    reg.init()
+    for algo in ("twoshot_waves", "twoshot_sentinel_waves", "twoshot_line_waves", "oneshot_waves",
+                 "oneshot_sentinel_waves", "oneshot_line_waves", "auto"):
+        for k in range(2):
+            x = wl.normal(p, n, dtype, seed=70 + k + p)
+            say(f"in place, one iteration: {algo} P={p} {dtype} call {k}")
+            assert_bits_equal(run(reg, x, algo), oracle.allreduce(x), f"in place one iteration {algo} P={p}")
+            assert reg.last_iters == 1
+
+
 IN_PLACE_ALGOS = ["auto", "twoshot", "twoshot_line", "twoshot_sentinel", "twoshot_waves", "twoshot_sentinel_waves",
                   "twoshot_line_waves", "oneshot", "oneshot_line"]
 
