@@ -537,7 +537,7 @@ ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
   if (sentinel_ok && (P == 2 || in_bytes > 8 * KiB)) {
     uint64_t one_max, two_max;  // one-shot, then two-shot, sentinel units with one wave per peer
     if (P <= 3) {
-      one_max = (P == 2 ? 1024 : 512) * KiB;
+      one_max = (P == 2 ? 2048 : 512) * KiB;
       two_max = (P == 2 ? 8 : 4) * MiB;
     } else if (P <= 5) {
       one_max = (P == 4 ? 256 : 128) * KiB;
@@ -550,7 +550,9 @@ ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
       two_max = 1 * MiB;
     }
     if (in_bytes <= one_max) return LL_ALGO_ONESHOT_SENTINEL_WAVES;
-    if (P == 2 && in_bytes <= 2 * MiB) return LL_ALGO_ONESHOT_SENTINEL;
+    // at 2 ranks the line two-shot beats the sentinel two-shot from 2 to
+    // 4 MiB (3 MiB: 6.41 against 7.25 us), the sentinel two-shot it above
+    if (P == 2 && in_bytes <= 4 * MiB) return large();
     if (in_bytes <= two_max) return LL_ALGO_TWOSHOT_SENTINEL_WAVES;
     return large();
   }

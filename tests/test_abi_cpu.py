@@ -346,6 +346,9 @@ def test_auto_algo_choices():
     assert ll.ll_auto_algo(8 << 20, bf16, 8) == (ll.LL_OK, A["twoshot_line_waves"])          # 16 MiB
     assert ll.ll_auto_algo(64 << 20, bf16, 7) == (ll.LL_OK, A["twoshot_line_waves"])         # 128 MiB
     assert ll.ll_auto_algo(1 << 19, bf16, 2, 0, sent) == (ll.LL_OK, A["oneshot_sentinel_waves"])
+    assert ll.ll_auto_algo(1 << 20, bf16, 2, 0, sent) == (ll.LL_OK, A["oneshot_sentinel_waves"])  # 2 MiB
+    assert ll.ll_auto_algo(3 << 19, bf16, 2, 0, sent) == (ll.LL_OK, A["twoshot_line_waves"])      # 3 MiB
+    assert ll.ll_auto_algo(4 << 20, bf16, 2, 0, sent) == (ll.LL_OK, A["twoshot_sentinel_waves"])  # 8 MiB
     assert ll.ll_auto_algo(1, f32, 1)[0] == ll.LL_ERR_INVALID
     assert ll.ll_auto_algo(1, f32, 9)[0] == ll.LL_ERR_INVALID
     assert ll.ll_auto_algo(1, 7, 8)[0] == ll.LL_ERR_UNSUPPORTED
