@@ -321,6 +321,26 @@ int wave_units_log2(const Plan &pl, int wpr) {
   if (forced == 1) return 0;
   if (forced == 2) return 1;
   if (forced == 4) return 2;
+  if (pl.kind == K_RS_WAVES || pl.kind == K_AG_WAVES) {
+    // stand-alone ReduceScatter / AllGather (measured at 4 and 8 ranks, C5
+    // shapes, b = 1 .. 256): one unit per lane below 256 KiB of data per
+    // rank; above, ReduceScatter two (8 ranks, lines, b = 64: 6.67 -> 5.55
+    // us; b = 256: 17.51 -> 15.6 us), except at 2-4 ranks from 2 MiB, where
+    // one stays faster (4 ranks, b = 256: 7.85 against 8.70 us); AllGather
+    // four from 512 KiB if its workgroups then hold at most 16 waves per CU
+    // (8 ranks, b = 128: 11.41 -> 10.09 us; 4 ranks, b = 256: 9.85 -> 9.28
+    // us), otherwise two (8 ranks, b = 256: 23.3 us in the one-lane kernel,
+    // 17.9 us).
+    const uint64_t data = (uint64_t)pl.a.n * (pl.dt == LL_BF16 ? 2u : 4u) * (uint64_t)pl.P;
+    const uint64_t KiB = 1024;
+    if (data < 256 * KiB) return 0;
+    if (pl.kind == K_RS_WAVES) return pl.P <= 4 && data >= 2048 * KiB ? 0 : 1;
+    DevInfo d;
+    const int64_t blocks = pl.proto == PR_LINE ? pl.units : (pl.units + 63) / 64;
+    if (data >= 512 * KiB && device_info(&d) == LL_OK && (blocks + 3) / 4 * pl.P * pl.P <= 16 * (int64_t)d.cus)
+      return 2;
+    return 1;
+  }
   if (pl.kind != K_TWOSHOT_WAVES) return 0;
   kernel_fn tf = nullptr;
   int64_t tiles = 0;
@@ -582,13 +602,15 @@ ll_algo auto_algo(uint64_t in_bytes, int P, bool sentinel_ok) {
 
 // ReduceScatter / AllGather, by the bytes of data per rank (input for
 // ReduceScatter, output for AllGather), measured the same way at 4 KiB ..
-// 8 MiB at 4 and 8 ranks: 8-byte packets up to 128 KiB (256 KiB at 2-4
-// ranks), lines above; with sentinel mode allowed, sentinel units up to 2 MiB
-// (4 MiB at 2-4 ranks).
-ll_proto auto_proto(uint64_t bytes, int P, bool sentinel_ok) {
+// 8 MiB at 4 and 8 ranks: ReduceScatter with 8-byte packets up to 128 KiB
+// and lines above (4 ranks, b = 16, 224 KiB: 3.20 us with 8-byte packets,
+// 3.08 us with lines); AllGather with lines at every size (8 ranks, b = 1,
+// 14 KiB: 3.28 us with 8-byte packets, 3.08 us with lines); with sentinel
+// mode allowed, sentinel units up to 2 MiB (4 MiB at 2-4 ranks).
+ll_proto auto_proto(uint64_t bytes, int P, bool sentinel_ok, bool allgather) {
   const uint64_t KiB = 1024, MiB = 1024 * 1024;
   if (sentinel_ok) return bytes <= (P >= 5 ? 2 : 4) * MiB ? LL_PROTO_SENTINEL : LL_PROTO_LINE128;
-  return bytes <= (P >= 5 ? 128 : 256) * KiB ? LL_PROTO_PACKET8 : LL_PROTO_LINE128;
+  return !allgather && bytes <= 128 * KiB ? LL_PROTO_PACKET8 : LL_PROTO_LINE128;
 }
 
 // Broadcast / Reduce: 8-byte packets up to 64 KiB per rank, lines above, or
@@ -601,14 +623,16 @@ ll_proto auto_proto_rooted(uint64_t bytes, bool sentinel_ok) {
 // Stand-alone ReduceScatter / AllGather: the wave-per-peer kernels serve
 // each format up to the size where the one-lane-per-unit kernels catch up
 // (measured at 4 and 8 ranks): 8-byte packets and sentinel units up to
-// 2 MiB of data per rank; lines up to 8 MiB at 2-4 ranks, and at 5-8 ranks
-// up to 4 MiB (ReduceScatter) or 2 MiB (AllGather).  ll_tuning.wave_kernels
-// forces either family.
+// 2 MiB of data per rank; lines up to 8 MiB at 2-4 ranks and 4 MiB at 5-8
+// ranks (8 ranks, b = 256, 3.5 MiB: AllGather 23.3 us with one lane per
+// unit, 17.9 us with one wave per peer at two units per lane).
+// ll_tuning.wave_kernels forces either family.
 bool use_wave_kernel(ll_proto proto, uint64_t bytes, int P, bool allgather, const CallOpts &o) {
+  (void)allgather;
   const int m = o.wave_kernels;
   if (m != 0) return m == 2;
   const uint64_t MiB = 1024 * 1024;
-  if (proto == LL_PROTO_LINE128) return bytes <= (P >= 5 ? (allgather ? 2 : 4) : 8) * MiB;
+  if (proto == LL_PROTO_LINE128) return bytes <= (P >= 5 ? 4 : 8) * MiB;
   return bytes <= 2 * MiB;
 }
 
@@ -1176,7 +1200,7 @@ int ll_reduce_scatter_ex(void *sym_base, size_t rank_stride, void *out, size_t r
   st = region_of(rank_stride, nranks, in_bytes, &rg);
   if (st != LL_OK) return st;
   if (proto == LL_PROTO_AUTO) {
-    proto = proto_choice(auto_proto(in_bytes, nranks, o.sentinel_ok()), auto_formats(rg.fmt, o));
+    proto = proto_choice(auto_proto(in_bytes, nranks, o.sentinel_ok(), false), auto_formats(rg.fmt, o));
     if (proto == LL_PROTO_AUTO) return LL_ERR_SCRATCH;
   }
   if ((rg.fmt & proto_fmt(proto)) == 0) return LL_ERR_SCRATCH;
@@ -1220,7 +1244,7 @@ int ll_allgather_ex(void *sym_base, size_t rank_stride, void *out, size_t sendco
   st = region_of(rank_stride, nranks, in_bytes, &rg);
   if (st != LL_OK) return st;
   if (proto == LL_PROTO_AUTO) {
-    proto = proto_choice(auto_proto(in_bytes * nranks, nranks, o.sentinel_ok()), auto_formats(rg.fmt, o));
+    proto = proto_choice(auto_proto(in_bytes * nranks, nranks, o.sentinel_ok(), true), auto_formats(rg.fmt, o));
     if (proto == LL_PROTO_AUTO) return LL_ERR_SCRATCH;
   }
   if ((rg.fmt & proto_fmt(proto)) == 0) return LL_ERR_SCRATCH;
