@@ -69,6 +69,18 @@ void fill_ttile(Table *t) {
 }
 
 template <int P>
+void fill_rtile(Table *t) {
+  t->rtile[0][0][0][P] = k_rooted_tile<ProtoLL, 0, P, 0>;
+  t->rtile[0][0][1][P] = k_rooted_tile<ProtoLL, 1, P, 0>;
+  t->rtile[0][1][0][P] = k_rooted_tile<ProtoLL, 0, P, 1>;
+  t->rtile[0][1][1][P] = k_rooted_tile<ProtoLL, 1, P, 1>;
+  t->rtile[1][0][0][P] = k_rooted_tile<ProtoSent, 0, P, 0>;
+  t->rtile[1][0][1][P] = k_rooted_tile<ProtoSent, 1, P, 0>;
+  t->rtile[1][1][0][P] = k_rooted_tile<ProtoSent, 0, P, 1>;
+  t->rtile[1][1][1][P] = k_rooted_tile<ProtoSent, 1, P, 1>;
+}
+
+template <int P>
 void fill(Table *t) {
   fill_row<ProtoLL, 0, P>(t->k[PR_LL][0][P]);
   fill_row<ProtoLL, 1, P>(t->k[PR_LL][1][P]);
@@ -101,6 +113,7 @@ void fill(Table *t) {
   t->tile[2][0][P] = k_oneshot_line_tile<0, P>;
   t->tile[2][1][P] = k_oneshot_line_tile<1, P>;
   fill_ttile<P>(t);
+  fill_rtile<P>(t);
   fill_twaves<0, P>(t);
   fill_twaves<1, P>(t);
   fill_twaves<2, P>(t);

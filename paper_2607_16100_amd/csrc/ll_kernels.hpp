@@ -1741,6 +1741,133 @@ __global__ __launch_bounds__(1024) void k_reduce(KArgs ka) {
   stamp_end(a, t_start);
 }
 
+// Broadcast and Reduce with one wave per peer and one tile of 64 one-lane
+// units per workgroup (8-byte packets or sentinel units), every stream 4-byte
+// aligned, all tiles resident at once: the straight-line counterparts of
+// k_broadcast and k_reduce, in the form of k_oneshot_tile.  Lane l of
+// workgroup (r, w) owns unit u = 64 w + l.
+//   Broadcast (Kind 0): on the root, wave q loads the unit of the root's
+//     input and stores it as a packet to slot (q <- root) of peer q (the
+//     root's own wave stores it to the root's output instead); on any other
+//     rank, wave 0 polls slot (r <- root) and stores the payload to the
+//     rank's output, and the other waves have nothing to do.
+//   Reduce (Kind 1): on every other rank, wave 0 loads the unit and stores
+//     it to slot (root <- r) of the root; on the root, wave q polls slot
+//     (root <- q) (its own wave loads its input), stages the values widened
+//     to binary32 in LDS row q, and after one barrier wave 0 sums the P rows
+//     in ascending rank order, rounds once and stores the root's output.
+// Readers clear (flagged) or reset (sentinel) the slots they have read.
+template <class Pr, int DT, int P, int Kind>
+__global__ __launch_bounds__(512) void k_rooted_tile(KArgs ka) {
+  static_assert(Pr::kLanes == 1, "one-lane packet formats only");
+  const KArgs a = pin_args(ka);
+  const uint64_t t_start = stamp_start(a);
+  constexpr int E = Elem<DT>::kBytes;
+  constexpr int K = Elem<DT>::kPerWord;
+  constexpr int NW = Pr::kMaxWords;  // payload words per lane
+  constexpr int EPL = NW * K;        // elements per lane
+  constexpr uint32_t kNowhere = 0xFFFFFFF0u;
+  __shared__ float stage[Kind == 1 ? P : 1][Kind == 1 ? 64 * EPL : 1];
+  const uint32_t r = blockIdx.x % P;
+  const uint32_t w = blockIdx.x / P;
+  const uint32_t q = (uint32_t)uniform_u32(threadIdx.x >> 6);
+  const uint32_t lane = threadIdx.x & 63;
+  const uint32_t u = w * 64 + lane;
+  const uint32_t root = (uint32_t)a.root;
+  const uint32_t nb = (uint32_t)(a.n * E);  // bytes per rank (< 256 MiB)
+  const uint32_t slot = (uint32_t)a.slot;
+  const bool have = u < (uint32_t)a.units;
+  const uint32_t off = have ? u * 16 : kNowhere;
+  const bool publish = (int)r != a.mute;
+  // Poll the unit in slot `src` of this rank's slice, then clear or reset it.
+  auto poll = [&](char *src) -> u32x4 {
+    const rsrc_t rs = make_rsrc(src, slot);
+    WaitBudget budget(a.timeout, a.status);
+    u32x4 v = {0u, 0u, 0u, 0u};
+    bool pend = have;
+    uint32_t spins = 0;
+    while (true) {
+      compiler_fence();
+      const u32x4 pk = ld_pkt(rs, off);
+      if (pend && Pr::ready(pk, a.epoch)) {
+        v = Pr::unpack(pk, 0);
+        pend = false;
+      }
+      if (__builtin_amdgcn_ballot_w64(pend) == 0) break;
+      if ((++spins & 15) == 0 && budget.expired()) {
+        if (pend) budget.report((int)r, 1u << (Kind == 0 ? root : q), a.epoch);
+        break;
+      }
+    }
+    if (ResetsSlots<Pr>::value) {
+      st_pkt(rs, off, u32x4{ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel, ProtoSent::kSentinel});
+    } else if (a.clear != 0) {
+      st_pkt(rs, off, u32x4{0u, 0u, 0u, 0u});
+    }
+    return v;
+  };
+  auto load_own = [&]() -> u32x4 {
+    u32x4 x = load_words_rs<NW>(make_rsrc(a.in + (uint64_t)r * a.in_stride, (nb + 3u) & ~3u), u * NW);
+    if (ResetsSlots<Pr>::value) x = clear_tail<DT, NW>(x, u * NW, (uint32_t)a.n);
+    return x;
+  };
+  if constexpr (Kind == 0) {
+    if (r == root) {
+      const u32x4 x = load_own();
+      if (q != r) {
+        char *const dst = a.sym + a.area + (uint64_t)q * a.stride + (uint64_t)slot_of((int)r, (int)q) * slot;
+        st_pkt(make_rsrc(dst, slot), publish ? off : kNowhere, Pr::pack(x, a.epoch, 0));
+      } else {
+        store_words_rs<NW, false>(make_rsrc(a.out + (uint64_t)r * nb, nb), u * NW, x);
+      }
+    } else if (q == 0) {
+      const u32x4 v = poll(a.sym + a.area + (uint64_t)r * a.stride + (uint64_t)slot_of((int)root, (int)r) * slot);
+      store_words_rs<NW, false>(make_rsrc(a.out + (uint64_t)r * nb, nb), u * NW, v);
+    }
+  } else {
+    if (r != root) {
+      if (q == 0) {
+        const u32x4 x = load_own();
+        char *const dst = a.sym + a.area + (uint64_t)root * a.stride + (uint64_t)slot_of((int)r, (int)root) * slot;
+        st_pkt(make_rsrc(dst, slot), publish ? off : kNowhere, Pr::pack(x, a.epoch, 0));
+      }
+    } else {
+      u32x4 v;
+      if (q == r) {
+        v = load_own();
+      } else {
+        v = poll(a.sym + a.area + (uint64_t)r * a.stride + (uint64_t)slot_of((int)q, (int)r) * slot);
+      }
+      const uint32_t vw[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int j = 0; j < NW; ++j) {
+        float f[K];
+        Elem<DT>::widen(vw[j], f);
+#pragma unroll
+        for (int e = 0; e < K; ++e) stage[q][lane * EPL + j * K + e] = f[e];
+      }
+      lds_barrier();
+      if (q == 0) {
+        uint32_t o[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int j = 0; j < NW; ++j) {
+          float acc[K];
+#pragma unroll
+          for (int e = 0; e < K; ++e) acc[e] = stage[0][lane * EPL + j * K + e];
+#pragma unroll
+          for (int p = 1; p < P; ++p) {
+#pragma unroll
+            for (int e = 0; e < K; ++e) acc[e] = acc[e] + stage[p][lane * EPL + j * K + e];
+          }
+          o[j] = Elem<DT>::narrow(acc);
+        }
+        store_words_rs<NW, false>(make_rsrc(a.out, nb), u * NW, u32x4{o[0], o[1], o[2], o[3]});
+      }
+    }
+  }
+  stamp_end(a, t_start);
+}
+
 // ---------------------------------------------------------------------------
 // Stand-alone ReduceScatter: rank r's input is P chunks of m = a.n elements;
 // chunk c goes to slot (c <- r); rank r reduces chunk r.  The same two steps

@@ -253,6 +253,7 @@ struct Plan {
   KArgs a;
   int64_t units;  // packet units per stream
   CallOpts o;     // the call's options
+  bool rooted_tile = false;  // Broadcast / Reduce on the one-tile kernel
 };
 
 // Launch shape of the two-shot AllReduce with one wave per peer, measured on
@@ -378,9 +379,9 @@ constexpr uint64_t kClearMaxBytes = 16ull << 20;
 
 uint32_t clear_slots(const Plan &pl) {
   const bool waves = pl.kind == K_ONESHOT_WAVES || pl.kind == K_TWOSHOT_WAVES || pl.kind == K_RS_WAVES ||
-                     pl.kind == K_AG_WAVES;
+                     pl.kind == K_AG_WAVES || pl.rooted_tile;
   if (!waves || pl.proto == PR_SENT || pl.o.clear_slots == 2) return 0;
-  if (pl.o.clear_slots == 1 || pl.kind == K_ONESHOT_WAVES) return 1;
+  if (pl.o.clear_slots == 1 || pl.kind == K_ONESHOT_WAVES || pl.rooted_tile) return 1;
   if (pl.a.iters > 1) return 0;
   const uint64_t es = pl.dt == LL_BF16 ? 2 : 4;
   const uint64_t n = (uint64_t)(pl.a.iters > 1 ? pl.a.iter_n : pl.a.n);
@@ -418,6 +419,21 @@ int launch(const Plan &pl, void *stream) {
     if (rc != LL_OK) return rc;
     const int64_t tiles = pl.proto == PR_LINE ? pl.units : (pl.units + 63) / 64;
     if (tf != nullptr && tiles <= cap / pl.P) return launch_kernel(tf, pl, (int)tiles, 64 * pl.P, stream);
+  }
+  // Broadcast / Reduce with a one-lane format under the same conditions:
+  // the straight-line rooted kernel (one tile of 64 units per workgroup).
+  if ((pl.kind == K_BCAST || pl.kind == K_REDUCE) && pl.proto != PR_LINE && !pl.o.forced_shape() &&
+      pl.a.al4 != 0 && (pl.a.in == nullptr || pl.a.in_al4 != 0)) {
+    kernel_fn tf = table().rtile[pl.proto == PR_SENT ? 1 : 0][pl.kind == K_BCAST ? 0 : 1][pl.dt][pl.P];
+    int cap = 0;
+    const int rc = resident_grid(tf, 64 * pl.P, &cap);
+    if (rc != LL_OK) return rc;
+    const int64_t tiles = (pl.units + 63) / 64;
+    if (tf != nullptr && tiles <= cap / pl.P) {
+      Plan tp = pl;
+      tp.rooted_tile = true;
+      return launch_kernel(tf, tp, (int)tiles, 64 * pl.P, stream);
+    }
   }
   // The same for the two-shot AllReduce with one or two units per lane and
   // one iteration: the straight-line two-shot kernel.
