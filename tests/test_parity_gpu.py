@@ -807,6 +807,30 @@ def test_broadcast_reduce_compose_to_allreduce():
     assert_bits_equal(reg.read_out(p * n, np.uint16).reshape(p, n), oracle.allreduce(x), "reduce+broadcast")
 
 
+@pytest.mark.parametrize("p", [2, 5, 8])
+def test_rooted_auto_with_sentinel_allowed(p):
+    """Broadcast and Reduce under AUTO with sentinel units allowed (the
+    one-tile sentinel kernel up to 64 KiB, lines above), every root, two
+    calls per size; the sentinel slots are back to the sentinel afterwards."""
+    sizes = [1000, 8192, 32768, 100_000]
+    reg = SymRegion(p, max(sizes), "bf16")
+    reg.init()
+    sent = opts(flags=ll.LL_OPT_AUTO_SENTINEL)
+    for n in sizes:
+        for root in range(p):
+            for call in range(2):
+                x = wl.normal(p, n, "bf16", seed=n + 10 * root + call)
+                reg.write_inputs(x)
+                say(f"rooted auto+sentinel P={p} n={n} root={root} call {call}")
+                check_ok(reg.broadcast(n, root, "auto", opt=sent), "broadcast")
+                assert_bits_equal(reg.read_out(p * n, np.uint16).reshape(p, n), oracle.broadcast(x, root),
+                                  f"broadcast P={p} n={n} root={root}")
+                check_ok(reg.reduce(n, root, "auto", opt=sent), "reduce")
+                assert_bits_equal(reg.read_out(n, np.uint16).reshape(1, n), oracle.reduce(x, root).reshape(1, n),
+                                  f"reduce P={p} n={n} root={root}")
+    assert (reg.read_area(4) == SENT).all()
+
+
 @pytest.mark.parametrize("kind", ["broadcast", "reduce"])
 def test_rooted_missing_rank_times_out(kind):
     p, n = 8, 4096
