@@ -53,19 +53,26 @@ void fill_twaves(Table *t) {
   t->twaves[M][2][2][1][P] = k_twoshot_waves<ProtoLine, 1, P, 4, M>;
 }
 
-// One unit per lane for every packet format; two for lines only (with
-// 8-byte packets and sentinel units the multi-tile kernel at two units per
-// lane measured as fast or faster).
+// One unit per lane for every packet format and mode; two for the AllReduce
+// with lines only (with 8-byte packets and sentinel units the multi-tile
+// kernel at two units per lane measured as fast or faster).
+template <int M, int P>
+void fill_ttile_u1(Table *t) {
+  t->ttile[M][0][0][0][P] = k_twoshot_tile<ProtoLL, 0, P, 1, M>;
+  t->ttile[M][0][0][1][P] = k_twoshot_tile<ProtoLL, 1, P, 1, M>;
+  t->ttile[M][0][1][0][P] = k_twoshot_tile<ProtoSent, 0, P, 1, M>;
+  t->ttile[M][0][1][1][P] = k_twoshot_tile<ProtoSent, 1, P, 1, M>;
+  t->ttile[M][0][2][0][P] = k_twoshot_tile<ProtoLine, 0, P, 1, M>;
+  t->ttile[M][0][2][1][P] = k_twoshot_tile<ProtoLine, 1, P, 1, M>;
+}
+
 template <int P>
 void fill_ttile(Table *t) {
-  t->ttile[0][0][0][P] = k_twoshot_tile<ProtoLL, 0, P, 1>;
-  t->ttile[0][0][1][P] = k_twoshot_tile<ProtoLL, 1, P, 1>;
-  t->ttile[0][1][0][P] = k_twoshot_tile<ProtoSent, 0, P, 1>;
-  t->ttile[0][1][1][P] = k_twoshot_tile<ProtoSent, 1, P, 1>;
-  t->ttile[0][2][0][P] = k_twoshot_tile<ProtoLine, 0, P, 1>;
-  t->ttile[0][2][1][P] = k_twoshot_tile<ProtoLine, 1, P, 1>;
-  t->ttile[1][2][0][P] = k_twoshot_tile<ProtoLine, 0, P, 2>;
-  t->ttile[1][2][1][P] = k_twoshot_tile<ProtoLine, 1, P, 2>;
+  fill_ttile_u1<0, P>(t);
+  fill_ttile_u1<1, P>(t);
+  fill_ttile_u1<2, P>(t);
+  t->ttile[0][1][2][0][P] = k_twoshot_tile<ProtoLine, 0, P, 2, 0>;
+  t->ttile[0][1][2][1][P] = k_twoshot_tile<ProtoLine, 1, P, 2, 0>;
 }
 
 template <int P>

@@ -1324,10 +1324,11 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
 }
 #undef LL_TW_PHASE
 
-// Two-shot AllReduce, one wave per peer, one tile of U units per lane per
+// Two-shot AllReduce (Mode 0), stand-alone ReduceScatter (Mode 1) or
+// AllGather (Mode 2), one wave per peer, one tile of U units per lane per
 // workgroup (U line units, or 64 U one-lane units), one iteration, every
 // stream 4-byte aligned: the straight-line counterpart of k_twoshot_waves<Pr,
-// DT, P, U, 0> for calls whose tiles are all resident at once.  It carries
+// DT, P, U, Mode> for calls whose tiles are all resident at once.  It carries
 // no tile loop, no tile sent ahead, no iteration and no element-wise
 // fallback for unaligned streams, which shortens what every workgroup runs
 // (the instructions of a latency-bound call are paid for in its latency, see
@@ -1338,10 +1339,12 @@ __global__ __launch_bounds__(512) void k_twoshot_waves(KArgs ka) {
 // (the own-rank wave keeps its own chunk's tile); every other wave polls
 // what peer q sent for chunk r, and each stages its row in LDS.  After a
 // barrier the workgroup forms the ordered sum word by word (binary32 in
-// ascending rank order, one rounding) into a reduced row.  AllGather: wave q
-// sends the reduced tile to peer q and polls the tile of chunk q that peer q
-// sends back; every wave stores its chunk's tile of the output.
-template <class Pr, int DT, int P, int U>
+// ascending rank order, one rounding) into a reduced row (Mode 1: the own
+// wave stores it).  AllGather: wave q sends the reduced tile (Mode 2: the
+// tile of the rank's input) to peer q and polls the tile of chunk q that
+// peer q sends back; every wave stores its chunk's (block's) tile of the
+// output.
+template <class Pr, int DT, int P, int U, int Mode = 0>
 __global__ __launch_bounds__(512) void k_twoshot_tile(KArgs ka) {
   const KArgs a = pin_args(ka);
   const uint64_t t_start = stamp_start(a);
@@ -1350,18 +1353,21 @@ __global__ __launch_bounds__(512) void k_twoshot_tile(KArgs ka) {
   using WU = WaveUnits<Pr, U>;
   constexpr int WPU = Pr::kMaxWords;          // payload words per lane and unit slot
   constexpr uint32_t kNowhere = 0xFFFFFFF0u;  // past every slot: the buffer resource discards the access
-  __shared__ u32x4 stage[P][64 * U];
-  __shared__ u32x4 red[64 * U];
+  constexpr bool kRS = Mode != 2, kAG = Mode != 1;
+  __shared__ u32x4 stage[kRS ? P : 1][kRS ? 64 * U : 1];
+  __shared__ u32x4 red[kRS ? 64 * U : 1];
   const uint32_t r = blockIdx.x % P;
   const uint32_t w = blockIdx.x / P;
   const uint32_t q = (uint32_t)uniform_u32(threadIdx.x >> 6);  // this wave's peer (q == r: the own values)
   const int lane = (int)(threadIdx.x & 63);
   const int sub = WU::sub(lane);
-  // chunks of C elements (a multiple of 16 bytes), the last ones short or
-  // empty; every chunk's byte length is a multiple of 4
-  const uint32_t C = (uint32_t)a.chunk;
+  // Mode 0: chunks of C elements (a multiple of 16 bytes), the last ones
+  // short or empty; Mode 1: P chunks of n elements; Mode 2: one input of n
+  // elements.  Every chunk's byte length is a multiple of 4.
   const uint32_t n = (uint32_t)a.n;
+  const uint32_t C = Mode == 0 ? (uint32_t)a.chunk : n;
   auto chunk_bytes = [&](uint32_t c) -> uint32_t {
+    if (Mode != 0) return n * (uint32_t)E;
     const uint32_t c0 = c * C;
     return c0 >= n ? 0u : ((n - c0 < C ? n - c0 : C) * (uint32_t)E);
   };
@@ -1379,17 +1385,20 @@ __global__ __launch_bounds__(512) void k_twoshot_tile(KArgs ka) {
   }
   u32x4 x[U];
   {
-    const rsrc_t in_rs = make_rsrc(a.in + (uint64_t)r * a.in_stride + (uint64_t)q * C * E, chunk_bytes(q));
+    const rsrc_t in_rs =
+        make_rsrc(a.in + (uint64_t)r * a.in_stride + (Mode == 2 ? 0 : (uint64_t)q * C * E), chunk_bytes(q));
 #pragma unroll
     for (int k = 0; k < U; ++k) x[k] = load_words_rs<WPU>(in_rs, fw[k]);
   }
   const uint32_t slot = (uint32_t)a.slot;
   const bool publish = (int)r != a.mute && q != r;
   // slot (q <- r) in peer q's slice and slot (r <- q) in this rank's slice;
-  // the AllGather slots follow the P - 1 ReduceScatter slots
+  // the AllGather slots follow the P - 1 ReduceScatter slots (Mode 2 has
+  // AllGather slots only).  The first store is the ReduceScatter (Mode 2:
+  // the AllGather) of the tile.
   char *const slot_out = a.sym + a.area + (uint64_t)q * a.stride + (r - (r > q ? 1u : 0u)) * slot;
   char *const slot_in = a.sym + a.area + (uint64_t)r * a.stride + (q - (q > r ? 1u : 0u)) * slot;
-  const uint64_t ag_off = (uint64_t)(P - 1) * slot;
+  const uint64_t ag_off = Mode == 2 ? 0 : (uint64_t)(P - 1) * slot;
   {
     const rsrc_t rd = make_rsrc(slot_out, slot);
 #pragma unroll
@@ -1442,23 +1451,24 @@ __global__ __launch_bounds__(512) void k_twoshot_tile(KArgs ka) {
       for (int k = 0; k < U; ++k) st_pkt(rs, off[k], u32x4{fill, fill, fill, fill});
     }
   };
-  {
-    u32x4 v[U];
-    if (q != r) {
-      poll(slot_in, v);
-      LL_TT_PHASE(1, now_ticks() + (v[0].x & 0u));
-    } else {
+  u32x4 res[U];
+  if constexpr (kRS) {
+    {
+      u32x4 v[U];
+      if (q != r) {
+        poll(slot_in, v);
+        LL_TT_PHASE(1, now_ticks() + (v[0].x & 0u));
+      } else {
 #pragma unroll
-      for (int k = 0; k < U; ++k) v[k] = x[k];
+        for (int k = 0; k < U; ++k) v[k] = x[k];
+      }
+#pragma unroll
+      for (int k = 0; k < U; ++k) stage[q][k * 64 + lane] = v[k];
     }
-#pragma unroll
-    for (int k = 0; k < U; ++k) stage[q][k * 64 + lane] = v[k];
-  }
-  lds_barrier();
-  LL_TT_PHASE(2, now_ticks());
-  // thread t reduces payload words t, t + 64 P, ... of the tile over the P
-  // rows (word j of unit slot s sits at 4 * s + j)
-  {
+    lds_barrier();
+    LL_TT_PHASE(2, now_ticks());
+    // thread t reduces payload words t, t + 64 P, ... of the tile over the
+    // P rows (word j of unit slot s sits at 4 * s + j)
     constexpr int kWords = 64 * U * WPU;
     const uint32_t *const rows = reinterpret_cast<const uint32_t *>(&stage[0][0]);
     uint32_t *const red_w = reinterpret_cast<uint32_t *>(&red[0]);
@@ -1475,28 +1485,41 @@ __global__ __launch_bounds__(512) void k_twoshot_tile(KArgs ka) {
       }
       red_w[at] = Elem<DT>::narrow(acc);
     }
-  }
-  lds_barrier();
-  u32x4 res[U];
+    lds_barrier();
 #pragma unroll
-  for (int k = 0; k < U; ++k) res[k] = red[k * 64 + lane];
-  {
-    const rsrc_t rd = make_rsrc(slot_out + ag_off, slot);
-#pragma unroll
-    for (int k = 0; k < U; ++k) st_pkt(rd, publish ? off[k] : kNowhere, Pr::pack(res[k], a.epoch, sub));
-  }
-  u32x4 o[U];
-  if (q != r) {
-    poll(slot_in + ag_off, o);
-    LL_TT_PHASE(3, now_ticks() + (o[0].x & 0u));
+    for (int k = 0; k < U; ++k) res[k] = red[k * 64 + lane];
   } else {
 #pragma unroll
-    for (int k = 0; k < U; ++k) o[k] = res[k];
+    for (int k = 0; k < U; ++k) res[k] = x[k];
   }
-  // the tile of chunk q of rank r's output
-  const rsrc_t out_rs = make_rsrc(a.out + ((uint64_t)r * n + (uint64_t)q * C) * E, chunk_bytes(q));
+  if constexpr (kAG) {
+    if constexpr (Mode == 0) {
+      const rsrc_t rd = make_rsrc(slot_out + ag_off, slot);
 #pragma unroll
-  for (int k = 0; k < U; ++k) store_words_rs<WPU>(out_rs, fw[k], Pr::start_store(o[k], sub));
+      for (int k = 0; k < U; ++k) st_pkt(rd, publish ? off[k] : kNowhere, Pr::pack(res[k], a.epoch, sub));
+    }
+    u32x4 o[U];
+    if (q != r) {
+      poll(slot_in + ag_off, o);
+      LL_TT_PHASE(3, now_ticks() + (o[0].x & 0u));
+    } else {
+#pragma unroll
+      for (int k = 0; k < U; ++k) o[k] = res[k];
+    }
+    // Mode 0: the tile of chunk q of rank r's output; Mode 2: the tile of
+    // block q of rank r's P blocks
+    const uint64_t o0 = Mode == 0 ? (uint64_t)r * n + (uint64_t)q * C : ((uint64_t)r * P + q) * n;
+    const rsrc_t out_rs = make_rsrc(a.out + o0 * E, chunk_bytes(q));
+#pragma unroll
+    for (int k = 0; k < U; ++k) store_words_rs<WPU>(out_rs, fw[k], Pr::start_store(o[k], sub));
+  } else {
+    // Mode 1: the own chunk's tile of rank r's output
+    if (q == r) {
+      const rsrc_t out_rs = make_rsrc(a.out + (uint64_t)r * n * E, n * (uint32_t)E);
+#pragma unroll
+      for (int k = 0; k < U; ++k) store_words_rs<WPU>(out_rs, fw[k], Pr::start_store(res[k], sub));
+    }
+  }
 #undef LL_TT_PHASE
   stamp_end(a, t_start);
 }

@@ -39,8 +39,9 @@ struct Table {
   kernel_fn twaves[3][3][3][2][kMaxRanks + 1];
   // one-shot, one tile per workgroup: [8-byte packets, sentinel, lines][dtype][P]
   kernel_fn tile[3][2][kMaxRanks + 1];
-  // two-shot AllReduce, one tile per workgroup: [log2 U][8-byte packets, sentinel, lines][dtype][P]
-  kernel_fn ttile[2][3][2][kMaxRanks + 1];
+  // two-shot, one tile per workgroup: [AllReduce, ReduceScatter, AllGather][log2 U][8-byte packets, sentinel,
+  // lines][dtype][P]
+  kernel_fn ttile[3][2][3][2][kMaxRanks + 1];
   // Broadcast / Reduce, one tile per workgroup: [8-byte packets, sentinel][Broadcast, Reduce][dtype][P]
   kernel_fn rtile[2][2][2][kMaxRanks + 1];
 };

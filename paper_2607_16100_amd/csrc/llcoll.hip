@@ -279,7 +279,8 @@ struct Plan {
 // 4-8 MiB, where two units per lane in one tile would have been faster for
 // 8-byte packets and sentinel units too, up to 0.8 us.
 bool twoshot_tile_eligible(const Plan &pl) {
-  return pl.kind == K_TWOSHOT_WAVES && !pl.o.forced_shape() && pl.o.wave_units <= 2 && pl.a.al4 != 0 &&
+  const bool two = pl.kind == K_TWOSHOT_WAVES || pl.kind == K_RS_WAVES || pl.kind == K_AG_WAVES;
+  return two && !pl.o.forced_shape() && pl.o.wave_units <= 2 && pl.a.al4 != 0 &&
          (pl.a.in == nullptr || pl.a.in_al4 != 0) && pl.a.iters <= 1;
 }
 
@@ -288,7 +289,8 @@ bool twoshot_tile_eligible(const Plan &pl) {
 // waves-per-CU limit of rule 1 for one unit per lane.
 bool twoshot_tile_ok(const Plan &pl, int wpr, int lu, kernel_fn *tf, int64_t *tiles) {
   if (!twoshot_tile_eligible(pl) || lu > 1) return false;
-  kernel_fn f = table().ttile[lu][wpr][pl.dt][pl.P];
+  const int mode = pl.kind == K_TWOSHOT_WAVES ? 0 : (pl.kind == K_RS_WAVES ? 1 : 2);
+  kernel_fn f = table().ttile[mode][lu][wpr][pl.dt][pl.P];
   int cap = 0;
   DevInfo d;
   if (f == nullptr || resident_grid(f, 64 * pl.P, &cap) != LL_OK || device_info(&d) != LL_OK) return false;
@@ -435,9 +437,10 @@ int launch(const Plan &pl, void *stream) {
       return launch_kernel(tf, tp, (int)tiles, 64 * pl.P, stream);
     }
   }
-  // The same for the two-shot AllReduce with one or two units per lane and
-  // one iteration: the straight-line two-shot kernel.
-  if (pl.kind == K_TWOSHOT_WAVES) {
+  // The same for the two-shot AllReduce and the stand-alone ReduceScatter /
+  // AllGather with one unit per lane (the AllReduce with lines also two)
+  // and one iteration: the straight-line two-shot kernel.
+  if (two_waves) {
     kernel_fn tf = nullptr;
     int64_t tiles = 0;
     if (twoshot_tile_ok(pl, wpr, wlog, &tf, &tiles)) return launch_kernel(tf, pl, (int)tiles, 64 * pl.P, stream);
