@@ -150,3 +150,54 @@ def test_random_calls_match_the_oracle():
             run_case(reg, rng, *c)
         del reg
         torch.cuda.empty_cache()
+
+
+BUF_ALGOS = ["auto", "oneshot", "oneshot_line", "oneshot_sentinel", "twoshot", "twoshot_line", "twoshot_sentinel",
+             "twoshot_sentinel_out", "twoshot_waves", "twoshot_sentinel_waves", "twoshot_line_waves"]
+
+
+def test_random_bounded_scratch_calls_match_the_oracle():
+    """The bounded-scratch AllReduce (ll_allreduce_buffered) over 40 random
+    regions (rank count, element type, iteration size, in place or not), five
+    random calls each: one to several iterations with ragged last ones, every
+    algorithm and random per-call options."""
+    from paper_2607_16100_amd.region import ScratchRegion
+
+    rng = np.random.default_rng(7_2026)
+    for g in range(40):
+        p = int(rng.integers(2, 9))
+        dtype = str(rng.choice(["f32", "bf16"]))
+        es = 4 if dtype == "f32" else 2
+        iter_bytes = int(rng.choice([4096, 16384, 65536, 262144]))
+        in_place = bool(rng.random() < 0.4)
+        max_count = 6 * iter_bytes // es
+        reg = ScratchRegion(p, max_count, dtype, iter_bytes=iter_bytes, in_place=in_place)
+        reg.init()
+        d = reg.iter_bytes // es
+        for c in range(5):
+            n = log_uniform(rng, 1, min(max_count, 5 * d + d // 2))
+            algo = str(rng.choice(BUF_ALGOS))
+            if algo == "twoshot_sentinel_out":
+                if in_place:  # its output is filled with the sentinel before the call
+                    algo = "twoshot_sentinel"
+                else:
+                    k = 16 // es
+                    n = min(max_count, (n + k - 1) // k * k)
+            x = wl.normal(p, n, dtype, sigma=float(rng.choice([0.01, 1.0, 300.0])), seed=50_000 + 10 * g + c)
+            want = oracle.allreduce(x)
+            reg.write_inputs(x)
+            opt = random_options(rng, "allreduce", algo)
+            what = f"group {g} call {c}: buffered {algo} P={p} {dtype} n={n} iteration {reg.iter_bytes} B in_place={in_place}"
+            say(what)
+            st = reg.allreduce(n, algo, opt=opt)
+            assert st == ll.LL_OK, f"{what}: {ll.ll_strerror(st)}"
+            st2 = ll.ll_check(torch.cuda.current_stream().cuda_stream)
+            assert st2 == ll.LL_OK, f"{what}: ll_check says {ll.ll_strerror(st2)}"
+            got = reg.read_out(p * n, NP[dtype]).reshape(p, n)
+            if not np.array_equal(got, want):
+                bad = np.argwhere(got != want)
+                r, j = bad[0]
+                raise AssertionError(f"{what}: {len(bad)} elements differ; first at row {r} index {j}: "
+                                     f"got {int(got[r, j]):#x} want {int(want[r, j]):#x}")
+        del reg
+        torch.cuda.empty_cache()
