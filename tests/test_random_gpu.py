@@ -175,7 +175,10 @@ def test_random_bounded_scratch_calls_match_the_oracle():
         reg.init()
         d = reg.iter_bytes // es
         for c in range(5):
-            n = log_uniform(rng, 1, min(max_count, 5 * d + d // 2))
+            if rng.random() < 0.4:
+                n = log_uniform(rng, 1, d)
+            else:  # one to five iterations, the last one ragged
+                n = min(max_count, int(d * rng.uniform(1.0, 5.9)))
             algo = str(rng.choice(BUF_ALGOS))
             if algo == "twoshot_sentinel_out":
                 if in_place:  # its output is filled with the sentinel before the call
