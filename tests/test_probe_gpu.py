@@ -34,11 +34,15 @@ def test_workgroups_are_dealt_round_robin_over_xcds():
     assert np.array_equal(x, (np.arange(grid) + x[0]) % 8)
 
 
+@pytest.mark.parametrize("size", ["short", "long"])
 @pytest.mark.parametrize("layout,name", [(0, "8-byte packets"), (1, "128-byte lines, flag per 64-byte half")])
-def test_no_torn_packets_across_xcds(layout, name):
+def test_no_torn_packets_across_xcds(layout, name, size):
     """Writers on one XCD rewrite packets while readers on another XCD read
-    them: every unit whose flag is set must carry that round's payload."""
-    grid, lines, iters, reads = 16, 256, 3000, 3000
+    them: every unit whose flag is set must carry that round's payload.  The
+    long run (256 writer and 256 reader workgroups, writers rewriting their
+    lines a million times while the readers read 50,000 times) takes about
+    1.2 s per layout."""
+    grid, lines, iters, reads = (16, 256, 3000, 3000) if size == "short" else (512, 256, 1_000_000, 50_000)
     buf = torch.zeros(grid // 2 * lines * 32, dtype=torch.int32, device="cuda")
     counts = torch.zeros(4, dtype=torch.int64, device="cuda")
     st = ll.ll_probe_litmus(buf.data_ptr(), buf.numel() * 4, grid, lines, iters, reads, layout,
@@ -46,8 +50,8 @@ def test_no_torn_packets_across_xcds(layout, name):
     assert st == ll.LL_OK
     torch.cuda.synchronize()
     seen, torn, split16, splitline = counts.cpu().numpy().tolist()
-    print(f"litmus {name}: seen={seen} torn={torn} split16={split16} splitline={splitline}", flush=True)
-    assert seen > 100_000
+    print(f"litmus {name} ({size}): seen={seen} torn={torn} split16={split16} splitline={splitline}", flush=True)
+    assert seen > (100_000 if size == "short" else 1_000_000_000)
     assert torn == 0
 
 
