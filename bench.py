@@ -176,13 +176,66 @@ def bench_headline(torch, ll, steps, warmup):
     for name in ("auto", "oneshot_sentinel_waves", "oneshot_line_waves", "twoshot_waves"):
         r = paced_collective(torch, ll, reg, "ar", n, ll.ALGOS[name], min(steps, 5000), 100)
         variants[name] = {"p50_us": r["p50_us"], "p99_us": r["p99_us"]}
+    epochs = reg.epoch
+    graph = bench_graph_replay(torch, ll, reg, n, p, grid, threads)
     return {
         "algorithm": "oneshot_waves", "variants": variants,
         "p50_us": pct(intervals, 50), "p99_us": pct(intervals, 99), "mean_us": float(np.mean(intervals)),
         "span_p50_us": pct(spans, 50), "stamp_free_mean_us": stampfree, "python_launched_mean_us": host_mean,
-        "wall_s": wall, "grid": grid, "threads": threads, "epochs": reg.epoch,
+        "wall_s": wall, "grid": grid, "threads": threads, "epochs": epochs, "graph_replay": graph,
         "exchange_probe": bench_exchange_probe(torch, ll, reg, n, p, steps),
     }
+
+
+def bench_graph_replay(torch, ll, reg, n, p, grid, threads, calls=1000, reps=5):
+    """The headline call captured `calls` times into a HIP graph (epochs 1 ..
+    calls; a captured call keeps its epoch, so the region is reset eagerly
+    before every replay) and replayed `reps` times: mean per call from HIP
+    events around each replay, and every replay's output (the buffer zeroed
+    first) compared with the eager result.  Beside it the empty kernel with
+    the same grid, captured and replayed the same way.  Context for serving
+    loops that replay graphs; the headline stays the eager back-to-back p50."""
+    try:
+        want = reg.read_out(p * n, np.uint16)
+        side = torch.cuda.Stream()
+        with torch.cuda.stream(side):  # the capture stream's status word, before capture
+            reg.init(side)
+            ll.check(reg.allreduce(n, "oneshot_waves", epoch=1), "graph warm-up")
+        torch.cuda.synchronize()
+        ll.check(ll.ll_check(side.cuda_stream), "graph warm-up")
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            for i in range(calls):
+                ll.check(reg.allreduce(n, "oneshot_waves", epoch=1 + i), "graph capture")
+        g_empty = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g_empty, stream=side):
+            for _ in range(calls):
+                ll.check(ll.ll_probe_empty(grid, threads, 0, side.cuda_stream), "graph capture")
+        torch.cuda.synchronize()
+        per_call, empty, exact = [], [], True
+        for _ in range(reps):
+            reg.out.zero_()
+            reg.init()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            ll.check(ll.ll_check(side.cuda_stream), "graph replay")
+            per_call.append(e0.elapsed_time(e1) * 1000.0 / calls)
+            exact = exact and bool(np.array_equal(reg.read_out(p * n, np.uint16), want))
+            e0.record()
+            g_empty.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            empty.append(e0.elapsed_time(e1) * 1000.0 / calls)
+        reg.init()
+        torch.cuda.synchronize()
+        return {"calls_per_replay": calls, "replays": reps, "mean_us_per_call": float(np.median(per_call)),
+                "empty_kernel_mean_us": float(np.median(empty)), "bit_exact_every_replay": exact}
+    except Exception as e:  # context only: never lose the benchmark line over it
+        return {"error": repr(e)}
 
 
 def bench_exchange_probe(torch, ll, reg, n, p, steps):

@@ -50,6 +50,11 @@
  * the epoch like the others but do not use it.  After epoch 0xFFFFFFFF,
  * call ll_init again and restart at 1.  (The paper's buffer object keeps this
  * counter internally and advances it itself, Sec. V; here the caller owns it.)
+ * A call captured into a HIP graph keeps the epoch it was captured with, so
+ * every replay repeats it: reset the region (ll_init, or ll_scratch_init for
+ * a bounded-scratch region) on the replay stream before each replay after
+ * the first.  ll_allreduce_static takes its epochs when it is called, so a
+ * captured static call may be replayed once.
  *
  * Outputs.  `out` is a separate device buffer (it must not overlap the
  * symmetric region) holding the P per-rank outputs back to back:
