@@ -85,7 +85,6 @@ def test_replays_of_a_captured_bounded_scratch_call(algo):
     torch.cuda.synchronize()
     assert ll.ll_check(side.cuda_stream) == ll.LL_OK
     reg.init(side)
-    reg.epoch = 0
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g, stream=side):
