@@ -995,11 +995,12 @@ __global__ __launch_bounds__(1024) __attribute__((amdgpu_waves_per_eu(LLCOLL_TWO
 
 // ---------------------------------------------------------------------------
 // Two-shot AllReduce, one wave per peer, with LDS staging of the partial sums
-// (8-byte packets or sentinel units); its two halves serve as the
-// stand-alone ReduceScatter (Mode 1) and AllGather (Mode 2).
+// (8-byte packets, sentinel units or 128-byte lines); its two halves serve as
+// the stand-alone ReduceScatter (Mode 1) and AllGather (Mode 2).
 //
-// A workgroup has P waves and handles one tile of 64*U packet units at the
-// same offset in every chunk (lane l owns units l, l+64, ... of the tile).
+// A workgroup has P waves and handles one tile at the same offset in every
+// chunk: 64*U units of a one-lane format (lane l owns units l, l+64, ...) or
+// U line units (each a whole wave), as in WaveUnits.
 // ReduceScatter: wave q != r sends the tile of chunk q to its owner q (one
 // store per unit) and polls the tile of chunk r that peer q sent to this
 // rank; wave r loads its own chunk r.  Each wave stages the raw payload
